@@ -1,0 +1,400 @@
+"""Seeded synthetic subgraphs shaped like the paper's offloaded workloads.
+
+The paper evaluates fully offloaded image classifiers (ResNet-18, ResNet-50,
+MobileNetV2 among them; Table 1, Sec. 4.1) with trained weights on ImageNet.
+Neither is available here, so every workload is synthetic: random weights of
+the same architecture and random inputs of the same shape, drawn from fixed
+seeds.  This module builds, for each workload, the serialized subgraph (the
+JSON graph representation of Sec. 3.3, Option 1), the constant list handed
+over once at engine creation (Sec. 3.4, metadata module) and the inputs.
+
+It holds no operator arithmetic: it draws random numbers and folds a
+batch-norm into conv weights using layer-wide statistics predicted by a
+scalar second-moment model (see ``GraphBuilder``), not measured by running
+the network.  The same arrays feed the HIP library and the CPU checker.
+
+Seeding: tensor ``t`` of workload ``cid`` is drawn from
+``np.random.default_rng(np.random.SeedSequence([cid, t]))``; tensor 0 is the
+input, constants follow in creation order, and the batch-norm shift of the
+i-th folded conv uses tensor id 1_000_000 + i.
+"""
+
+import json
+import math
+
+import numpy as np
+
+CONFIG_IDS = {
+    "conv_f32": 0,
+    "resnet18_block": 1,
+    "resnet50_v1": 2,
+    "mobilenet_v2": 3,
+    "bert_ffn": 4,
+}
+
+_BN_EPS = 1e-5
+_BN_SHIFT_STD = 0.01
+# mean square of a 3x3 max over ReLU outputs relative to its input's: the max
+# of 9 independent standard normals has mean 1.485 and variance 0.357, so
+# E[max^2] = 2.56 s^2 against E[relu^2] = s^2 / 2
+_MAXPOOL_GAIN = 5.1
+# share of a non-negative activation's mean square that its spatial mean keeps
+_GAP_GAIN = 0.5
+_ADD_RELU_KEEP = 0.75
+
+
+class Workload:
+    """A serialized subgraph with its constants and inputs.
+
+    graph   dict in the JSON schema accepted by ``byoc_subgraph_create``
+    consts  list of float32 arrays, indexed by each constant's ``index``
+    inputs  list of float32 arrays in the order of ``graph["inputs"]``
+            (bf16-declared inputs hold values already representable in bf16)
+    macs    multiply-accumulates of the conv and dense composites
+    """
+
+    def __init__(self, graph, consts, inputs, macs, conv_macs):
+        self.graph = graph
+        self.consts = consts
+        self.inputs = inputs
+        self.macs = macs
+        self.conv_macs = conv_macs
+
+    @property
+    def json(self):
+        return json.dumps(self.graph)
+
+    @property
+    def batch(self):
+        return self.graph["inputs"][0]["shape"][0]
+
+
+def to_bf16_values(a):
+    """Round float32 values to bfloat16 (ties to even) and return float32.
+
+    Input preparation only: a bf16-declared input must already hold bf16
+    values, so the generator rounds its random draws once.
+    """
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    u = (u + 0x7FFF + lsb) >> 16
+    return (u.astype(np.uint32) << 16).view(np.float32)
+
+
+class GraphBuilder:
+    """Accumulates nodes and constants of one synthetic subgraph.
+
+    Weight scales follow a scalar second-moment model: with zero-mean random
+    weights, the mean square of a linear layer's output, averaged over output
+    channels, is fan_in * var(w) * E[x^2] in expectation over the weight draw,
+    whatever the correlations of the input; ReLU keeps half of it because the
+    weight draw makes each channel's pre-activation symmetric.  A folded
+    batch-norm uses these layer-wide statistics (mean 0, variance the
+    predicted mean square) so that every normalized conv output has a mean
+    square of about 1.
+    """
+
+    def __init__(self, name, cid, dtype="bf16"):
+        self.name = name
+        self.cid = cid
+        self.dtype = dtype
+        self.inputs = []
+        self.input_arrays = []
+        self.constants = []
+        self.const_arrays = []
+        self.nodes = []
+        self.outputs = []
+        self.shapes = {}
+        self.m2 = {}
+        self.next_tensor = 1
+        self.n_folded = 0
+        self.macs = 0
+        self.conv_macs = 0
+
+    # -- random draws ------------------------------------------------------
+    def rng(self, tensor_id):
+        return np.random.default_rng(np.random.SeedSequence([self.cid, tensor_id]))
+
+    def _const(self, name, arr, layout):
+        idx = len(self.const_arrays)
+        self.constants.append({"name": name, "index": idx, "shape": list(arr.shape),
+                               "dtype": "f32", "layout": layout})
+        self.const_arrays.append(np.ascontiguousarray(arr, dtype=np.float32))
+        return name
+
+    # -- graph construction ------------------------------------------------
+    def input(self, name, shape, dist="uniform", dtype=None, layout=None):
+        dtype = dtype or self.dtype
+        rng = self.rng(0 if not self.inputs else 100 + len(self.inputs))
+        if dist == "uniform":
+            a = rng.random(shape, dtype=np.float64).astype(np.float32)
+            m2 = 1.0 / 3.0
+        elif dist == "normal":
+            a = rng.standard_normal(shape, dtype=np.float64).astype(np.float32)
+            m2 = 1.0
+        else:
+            raise ValueError(dist)
+        if dtype == "bf16":
+            a = to_bf16_values(a)
+        if layout is None:
+            layout = "NCHW" if len(shape) == 4 else "ROWMAJOR"
+        self.inputs.append({"name": name, "shape": list(shape), "dtype": dtype, "layout": layout})
+        self.input_arrays.append(a)
+        self.shapes[name] = list(shape)
+        self.m2[name] = m2
+        return name
+
+    def _after_add_act(self, m2_stream, m2_branch, act):
+        if not act:
+            return m2_stream + m2_branch
+        # the stream is non-negative after its own ReLU and the branch is
+        # symmetric: between half and all of the branch survives the ReLU
+        return m2_stream + _ADD_RELU_KEEP * m2_branch
+
+    def conv(self, x, k, r, stride=1, pad=None, groups=1, act="relu", bias=True, residual=None,
+             bn=True, gamma=1.0, w_std=None, b_std=None, name=None):
+        """Conv composite with He-normal weights and an optional folded BN."""
+        n, c, h, w = self.shapes[x]
+        pad = (r // 2) if pad is None else pad
+        pads = [pad] * 4 if isinstance(pad, int) else list(pad)
+        strides = [stride, stride] if isinstance(stride, int) else list(stride)
+        cg = c // groups
+        fan_in = cg * r * r
+        tid = self.next_tensor
+        self.next_tensor += 2
+        std = w_std if w_std is not None else math.sqrt(2.0 / fan_in)
+        wt = self.rng(tid).normal(0.0, std, size=(k, cg, r, r))
+        m2_in = self.m2[x]
+        if bn:
+            var_pred = fan_in * std * std * m2_in
+            beta = self.rng(1_000_000 + self.n_folded).normal(0.0, _BN_SHIFT_STD, size=k)
+            self.n_folded += 1
+            wt = wt * (gamma / math.sqrt(var_pred + _BN_EPS))
+            b = beta
+            m2 = gamma * gamma + _BN_SHIFT_STD ** 2
+        else:
+            bs = b_std if b_std is not None else 0.01
+            b = self.rng(tid + 1).normal(0.0, bs, size=k)
+            m2 = fan_in * std * std * m2_in + bs * bs
+        name = name or "n%d" % len(self.nodes)
+        wname = self._const(name + ".w", wt, "OIHW")
+        ins = [x, wname]
+        comp = "conv2d"
+        if bias:
+            ins.append(self._const(name + ".b", b, "O"))
+            comp += "_bias"
+        if residual is not None:
+            ins.append(residual)
+            comp += "_add"
+            m2 = self._after_add_act(self.m2[residual], m2, act)
+        elif act:
+            m2 = 0.5 * m2
+        if act:
+            comp += "_" + act
+        p = (h + pads[0] + pads[2] - r) // strides[0] + 1
+        q = (w + pads[1] + pads[3] - r) // strides[1] + 1
+        self.nodes.append({"name": name, "composite": comp, "inputs": ins,
+                           "attrs": {"strides": strides, "padding": pads, "dilation": [1, 1],
+                                     "groups": groups},
+                           "out_dtype": self.dtype})
+        self.shapes[name] = [n, k, p, q]
+        self.m2[name] = m2
+        macs = n * k * p * q * cg * r * r
+        self.macs += macs
+        self.conv_macs += macs
+        return name
+
+    def dense(self, x, n_out, act=None, residual=None, w_std=None, b_std=0.01, name=None):
+        m, kin = self.shapes[x]
+        tid = self.next_tensor
+        self.next_tensor += 2
+        std = w_std if w_std is not None else math.sqrt(2.0 / kin)
+        wt = self.rng(tid).normal(0.0, std, size=(n_out, kin))
+        b = self.rng(tid + 1).normal(0.0, b_std, size=n_out)
+        name = name or "n%d" % len(self.nodes)
+        ins = [x, self._const(name + ".w", wt, "OI"), self._const(name + ".b", b, "O")]
+        comp = "dense_bias"
+        m2 = kin * std * std * self.m2[x] + b_std * b_std
+        if residual is not None:
+            ins.append(residual)
+            comp += "_add"
+            m2 = self._after_add_act(self.m2[residual], m2, act)
+        elif act:
+            m2 = 0.5 * m2
+        if act:
+            comp += "_" + act
+        self.nodes.append({"name": name, "composite": comp, "inputs": ins, "attrs": {},
+                           "out_dtype": self.dtype})
+        self.shapes[name] = [m, n_out]
+        self.m2[name] = m2
+        self.macs += m * n_out * kin
+        return name
+
+    def max_pool(self, x, size=3, stride=2, pad=1, name=None):
+        n, c, h, w = self.shapes[x]
+        name = name or "n%d" % len(self.nodes)
+        self.nodes.append({"name": name, "composite": "max_pool2d", "inputs": [x],
+                           "attrs": {"pool_size": [size, size], "strides": [stride, stride],
+                                     "padding": [pad] * 4},
+                           "out_dtype": self.dtype})
+        p = (h + 2 * pad - size) // stride + 1
+        q = (w + 2 * pad - size) // stride + 1
+        self.shapes[name] = [n, c, p, q]
+        self.m2[name] = _MAXPOOL_GAIN * self.m2[x]
+        return name
+
+    def global_avg_pool(self, x, name=None):
+        n, c, h, w = self.shapes[x]
+        name = name or "n%d" % len(self.nodes)
+        self.nodes.append({"name": name, "composite": "global_avg_pool2d", "inputs": [x],
+                           "attrs": {}, "out_dtype": self.dtype})
+        self.shapes[name] = [n, c]
+        self.m2[name] = _GAP_GAIN * self.m2[x]
+        return name
+
+    def add(self, a, b, act=None, name=None):
+        name = name or "n%d" % len(self.nodes)
+        comp = "add" + ("_" + act if act else "")
+        self.nodes.append({"name": name, "composite": comp, "inputs": [a, b], "attrs": {},
+                           "out_dtype": self.dtype})
+        self.shapes[name] = list(self.shapes[a])
+        self.m2[name] = self._after_add_act(self.m2[a], self.m2[b], act)
+        return name
+
+    def output(self, x, dtype=None, layout=None):
+        shape = self.shapes[x]
+        if layout is None:
+            layout = "NCHW" if len(shape) == 4 else "ROWMAJOR"
+        self.outputs.append({"name": x, "dtype": dtype or self.dtype, "layout": layout})
+
+    def finish(self, meta=None):
+        graph = {"format": "byoc-subgraph", "version": 1,
+                 "meta": dict({"workload": self.name, "seed_config_id": self.cid}, **(meta or {})),
+                 "inputs": self.inputs, "constants": self.constants, "nodes": self.nodes,
+                 "outputs": self.outputs}
+        return Workload(graph, self.const_arrays, self.input_arrays, self.macs, self.conv_macs)
+
+
+# ---------------------------------------------------------------------------
+# The five workloads
+# ---------------------------------------------------------------------------
+
+def conv_f32(n=1, c=16, hw=32, k=32):
+    """One conv2d(3x3, s1, p1)+bias+ReLU composite in fp32.
+
+    x U[0,1), W N(0, 0.1), b N(0, 0.01).
+    """
+    g = GraphBuilder("conv_f32", CONFIG_IDS["conv_f32"], dtype="f32")
+    x = g.input("x", [n, c, hw, hw], "uniform")
+    y = g.conv(x, k, 3, stride=1, pad=1, act="relu", bn=False, w_std=0.1, b_std=0.01, name="conv")
+    g.output(y)
+    return g.finish({"batch": n})
+
+
+def resnet18_block(n=1, c=64, hw=56):
+    """ResNet-18 basic block: conv3x3+bias+ReLU, conv3x3+bias, +x, ReLU (bf16)."""
+    g = GraphBuilder("resnet18_block", CONFIG_IDS["resnet18_block"])
+    x = g.input("x", [n, c, hw, hw], "uniform")
+    a = g.conv(x, c, 3, act="relu", name="conv1")
+    y = g.conv(a, c, 3, act="relu", residual=x, name="conv2")
+    g.output(y)
+    return g.finish({"batch": n})
+
+
+def _bottleneck(g, x, mid, out, stride, downsample, stride_on, prefix):
+    s1 = stride if stride_on == "1x1" else 1
+    s3 = stride if stride_on == "3x3" else 1
+    sc = x
+    if downsample:
+        sc = g.conv(x, out, 1, stride=stride, pad=0, act=None, name=prefix + ".down")
+    a = g.conv(x, mid, 1, stride=s1, pad=0, act="relu", name=prefix + ".a")
+    b = g.conv(a, mid, 3, stride=s3, pad=1, act="relu", name=prefix + ".b")
+    return g.conv(b, out, 1, stride=1, pad=0, act="relu", residual=sc, name=prefix + ".c")
+
+
+def resnet50(n=1, hw=224, variant="v1", input_dtype="bf16", num_classes=1000):
+    """ResNet-50 v1 (stride on the first 1x1 of a downsampling block) or v1b
+    (stride on the 3x3), batch-norm folded, max-pool, global average pool and
+    the 2048->1000 classifier; bf16 activations."""
+    g = GraphBuilder("resnet50_" + variant, CONFIG_IDS["resnet50_v1"])
+    x = g.input("x", [n, 3, hw, hw], "uniform", dtype=input_dtype)
+    y = g.conv(x, 64, 7, stride=2, pad=3, act="relu", name="stem")
+    y = g.max_pool(y, 3, 2, 1, name="pool")
+    stride_on = "1x1" if variant == "v1" else "3x3"
+    cin = 64
+    for si, (mid, blocks, stride) in enumerate([(64, 3, 1), (128, 4, 2), (256, 6, 2), (512, 3, 2)]):
+        out = mid * 4
+        for bi in range(blocks):
+            st = stride if bi == 0 else 1
+            y = _bottleneck(g, y, mid, out, st, bi == 0, stride_on, "s%d.b%d" % (si + 1, bi))
+        cin = out
+    y = g.global_avg_pool(y, name="gap")
+    y = g.dense(y, num_classes, name="fc")
+    g.output(y)
+    del cin
+    return g.finish({"batch": n, "variant": variant})
+
+
+_MBV2_SETTINGS = [(1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2),
+                  (6, 96, 3, 1), (6, 160, 3, 2), (6, 320, 1, 1)]
+
+
+def mobilenet_v2(n=1, hw=224, input_dtype="bf16", num_classes=1000):
+    """MobileNetV2-1.0: stem 3x3 s2 + ReLU6, 17 inverted residual blocks
+    (1x1 expand + ReLU6, depthwise 3x3 + ReLU6, 1x1 linear project, residual
+    when the shape is kept), 1x1 -> 1280 + ReLU6, GAP, 1280 -> 1000."""
+    g = GraphBuilder("mobilenet_v2", CONFIG_IDS["mobilenet_v2"])
+    x = g.input("x", [n, 3, hw, hw], "uniform", dtype=input_dtype)
+    y = g.conv(x, 32, 3, stride=2, pad=1, act="relu6", name="stem")
+    cin = 32
+    bidx = 0
+    for t, c, reps, s in _MBV2_SETTINGS:
+        for i in range(reps):
+            stride = s if i == 0 else 1
+            hidden = cin * t
+            pre = "ir%d" % bidx
+            h = y
+            if t != 1:
+                h = g.conv(h, hidden, 1, pad=0, act="relu6", name=pre + ".expand")
+            h = g.conv(h, hidden, 3, stride=stride, pad=1, groups=hidden, act="relu6",
+                       name=pre + ".dw")
+            res = y if (stride == 1 and cin == c) else None
+            y = g.conv(h, c, 1, pad=0, act=None, residual=res, name=pre + ".project")
+            cin = c
+            bidx += 1
+    y = g.conv(y, 1280, 1, pad=0, act="relu6", name="head")
+    y = g.global_avg_pool(y, name="gap")
+    y = g.dense(y, num_classes, name="fc")
+    g.output(y)
+    return g.finish({"batch": n})
+
+
+def bert_ffn(batch=8, seq=128, hidden=768, ffn=3072, layers=12):
+    """BERT-base-shaped FFN stack: x <- x + (GELU(x W1^T + b1) W2^T + b2), 12
+    layers, tokens row-major [batch*seq, hidden]; x N(0,1), W and b N(0, 0.02)."""
+    g = GraphBuilder("bert_ffn", CONFIG_IDS["bert_ffn"])
+    x = g.input("x", [batch * seq, hidden], "normal")
+    for layer in range(layers):
+        h = g.dense(x, ffn, act="gelu", w_std=0.02, b_std=0.02, name="l%d.ffn1" % layer)
+        x = g.dense(h, hidden, residual=x, w_std=0.02, b_std=0.02, name="l%d.ffn2" % layer)
+    g.output(x)
+    return g.finish({"batch": batch, "seq": seq})
+
+
+def build(name, **kw):
+    """Build a workload by name: conv_f32, resnet18_block, resnet50_v1,
+    resnet50_v1b, mobilenet_v2, bert_ffn."""
+    if name == "conv_f32":
+        return conv_f32(**kw)
+    if name == "resnet18_block":
+        return resnet18_block(**kw)
+    if name == "resnet50_v1":
+        return resnet50(variant="v1", **kw)
+    if name == "resnet50_v1b":
+        return resnet50(variant="v1b", **kw)
+    if name == "mobilenet_v2":
+        return mobilenet_v2(**kw)
+    if name == "bert_ffn":
+        return bert_ffn(**kw)
+    raise ValueError("unknown workload %r" % name)

@@ -1,0 +1,70 @@
+"""The seeded synthetic workloads: shapes, op counts, determinism, scale."""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2105_03215_amd import workloads
+
+
+def _count(wl, prefix):
+    return sum(1 for n in wl.graph["nodes"] if n["composite"].startswith(prefix))
+
+
+def test_resnet50_v1_structure_and_work():
+    wl = workloads.build("resnet50_v1", n=1)
+    convs = [n for n in wl.graph["nodes"] if n["composite"].startswith("conv2d")]
+    assert len(convs) == 53
+    assert _count(wl, "max_pool2d") == 1 and _count(wl, "global_avg_pool2d") == 1
+    assert _count(wl, "dense") == 1
+    assert sum(1 for n in convs if "_add" in n["composite"]) == 16
+    # 7.716 GFLOP per image for v1 (stride on the 1x1), 8.178 for v1b
+    assert abs(2 * wl.macs / 1e9 - 7.716) < 0.01
+    wlb = workloads.build("resnet50_v1b", n=1)
+    assert abs(2 * wlb.macs / 1e9 - 8.178) < 0.01
+    assert wl.graph["outputs"][0]["name"] == "fc"
+
+
+def test_mobilenet_v2_structure():
+    wl = workloads.build("mobilenet_v2", n=1)
+    dw = [n for n in wl.graph["nodes"] if n["composite"].startswith("conv2d") and n["attrs"]["groups"] > 1]
+    assert len(dw) == 17
+    assert _count(wl, "conv2d") - len(dw) == 35
+    assert sum(1 for n in wl.graph["nodes"] if "_add" in n["composite"]) == 10
+    assert all(n["composite"] == "conv2d_bias_relu6" for n in dw)
+
+
+def test_bert_ffn_structure():
+    wl = workloads.build("bert_ffn")
+    assert wl.graph["inputs"][0]["shape"] == [1024, 768]
+    assert _count(wl, "dense_bias_gelu") == 12 and _count(wl, "dense_bias_add") == 12
+    assert abs(2 * wl.macs / 1024 / 1e6 - 113.2) < 0.1
+
+
+def test_deterministic_and_distinct_seeds():
+    a = workloads.build("resnet18_block")
+    b = workloads.build("resnet18_block")
+    assert a.json == b.json
+    for x, y in zip(a.consts + a.inputs, b.consts + b.inputs):
+        assert np.array_equal(x, y)
+    assert not np.array_equal(a.consts[0], a.consts[2])
+
+
+def test_bf16_inputs_are_representable():
+    wl = workloads.build("resnet18_block")
+    x = wl.inputs[0]
+    assert x.dtype == np.float32
+    assert np.all((x.view(np.uint32) & 0xFFFF) == 0)
+    assert 0.0 <= x.min() and x.max() <= 1.0
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block"])
+def test_activations_stay_order_one(name):
+    wl = workloads.build(name)
+    outs, vals = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io", keep=True)
+    names = [n["name"] for n in wl.graph["nodes"]]
+    peak = max(float(np.abs(vals[n]).max()) for n in names)
+    rms_out = float(np.sqrt(np.mean(outs[0] ** 2)))
+    assert peak < 32, peak
+    assert 0.1 < rms_out < 4, rms_out
