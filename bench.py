@@ -1,0 +1,191 @@
+"""Throughput of the offloaded ResNet-50 v1 subgraph on one MI355X.
+
+One step = one run of the whole offloaded subgraph (input layout transform,
+53 conv composites, max-pool, global average pool, classifier) over a batch
+of 32 synthetic 3x224x224 images already resident in HBM.  Prints one JSON
+line with images/s, the roofline of the dominant kernel class (the bf16 MFMA
+implicit-GEMM conv/dense kernels) measured with per-launch HIP events on the
+run stream, the batch-1 figures, and the CPU oracle timed on a bounded
+sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "images/sec (bs1, bs32) ResNet-50 offloaded subgraph; conv TFLOP/s as % MFMA peak"
+PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
+PEAK_HBM_GBS = 8000.0
+
+
+def _timed_runs(sg, ins, outs, stream, steps):
+    import torch
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        start.record(stream)
+        for _ in range(steps):
+            sg.run(ins, outs, stream)
+        end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return start.elapsed_time(end) / steps, wall
+
+
+def _profile(sg, ins, outs, stream, steps):
+    """Per-launch durations (ms per run) from HIP events recorded by the
+    library on the run stream around every launch."""
+    import torch
+    sg.profile_begin(steps)
+    for _ in range(steps):
+        sg.run(ins, outs, stream)
+    ms, runs = sg.profile_end()
+    torch.cuda.synchronize()
+    return [m / max(runs, 1) for m in ms], runs
+
+
+def _roofline(launches, per_launch_ms, traffic=None):
+    conv_kinds = ("conv_mfma", "reduce")
+    conv_ms = sum(t for l, t in zip(launches, per_launch_ms) if l["kind"] in conv_kinds)
+    conv_flops = sum(l["flops"] for l in launches if l["kind"] == "conv_mfma")
+    n_conv = sum(1 for l in launches if l["kind"] == "conv_mfma")
+    achieved = conv_flops / (conv_ms * 1e-3) / 1e12 if conv_ms > 0 else 0.0
+    return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "kernel": "conv_mfma_kernel (+ splitk_reduce), %d launches per step" % n_conv,
+            "flops_per_step": conv_flops, "kernel_ms_per_step": round(conv_ms, 4)}
+
+
+def _class_summary(launches, per_launch_ms):
+    out = {}
+    for l, t in zip(launches, per_launch_ms):
+        d = out.setdefault(l["kind"], {"launches": 0, "ms": 0.0, "flops": 0, "bytes": 0})
+        d["launches"] += 1
+        d["ms"] += t
+        d["flops"] += l["flops"]
+        d["bytes"] += l["bytes"]
+    for d in out.values():
+        d["ms"] = round(d["ms"], 4)
+        d["gbs"] = round(d["bytes"] / (d["ms"] * 1e-3) / 1e9, 1) if d["ms"] > 0 else None
+        d["tflops"] = round(d["flops"] / (d["ms"] * 1e-3) / 1e12, 2) if d["ms"] > 0 else None
+    return out
+
+
+def _cpu_baseline(wl, images):
+    """The oracle (bf16io mode, float64 NumPy) on the first `images` images
+    of the workload, on this host's cores."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    graph = dict(wl.graph)
+    graph["inputs"] = [dict(d, shape=[images] + d["shape"][1:]) for d in wl.graph["inputs"]]
+    x = [np.ascontiguousarray(a[:images]) for a in wl.inputs]
+    with threadpool_limits(limits=cores):
+        t0 = time.perf_counter()
+        oracle.run_graph(graph, wl.consts, x, mode="bf16io")
+        dt = time.perf_counter() - t0
+    return {"value": round(images / dt, 4), "unit": "images/s", "cores": cores, "kind": "oracle",
+            "sample": "%d of the 32 images, one oracle call (NumPy float64, bf16io), %.1f s"
+                      % (images, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--batch", type=int, default=32)
+    ap.add_argument("--variant", default="resnet50_v1")
+    ap.add_argument("--cpu-images", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this executor has no multi-GPU path "
+              "(batch sharding across GPUs needs no collective and is not built); "
+              "use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2105_03215_amd import capi, runtime, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = workloads.build(args.variant, n=args.batch)
+    t0 = time.perf_counter()
+    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
+    create_s = time.perf_counter() - t0
+    stream = torch.cuda.Stream(device=dev)
+    ins = runtime.inputs_for(sg, wl.inputs, dev)
+    outs = runtime.outputs_for(sg, dev)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        sg.run(ins, outs, stream)
+    torch.cuda.synchronize()
+    ms, wall = _timed_runs(sg, ins, outs, stream, args.steps)
+    value = args.batch / (ms * 1e-3)
+    launches = sg.launches()
+    per_launch, runs = _profile(sg, ins, outs, stream, args.steps)
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        with open(args.traffic_json) as f:
+            tj = json.load(f)
+        if tj.get("workload") == "%s_bs%d" % (args.variant, args.batch):
+            traffic = tj.get("conv_bytes_per_step")
+    roof = _roofline(launches, per_launch, traffic)
+    roof["profiled_ms_per_step"] = round(sum(per_launch), 4)
+    stats = sg.stats()
+
+    bs1 = None
+    if not args.no_bs1 and args.batch != 1:
+        wl1 = workloads.build(args.variant, n=1)
+        sg1 = capi.Subgraph(wl1.graph, wl1.consts, device=0)
+        ins1 = runtime.inputs_for(sg1, wl1.inputs, dev)
+        outs1 = runtime.outputs_for(sg1, dev)
+        for _ in range(args.warmup):
+            sg1.run(ins1, outs1, stream)
+        ms1, _ = _timed_runs(sg1, ins1, outs1, stream, max(args.steps, 200))
+        bs1 = {"images_per_s": round(1.0 / (ms1 * 1e-3), 1), "ms_per_step": round(ms1, 4),
+               "launches": len(sg1.launches())}
+        sg1.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = _cpu_baseline(wl, args.cpu_images)
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded uniform[0,1) images, random He-init weights with folded BN)",
+        "config": {"workload": "%s_bs%d" % (args.variant, args.batch), "batch": args.batch,
+                   "input": [args.batch, 3, 224, 224], "gflop_per_image": round(2 * wl.macs / args.batch / 1e9, 3),
+                   "launches_per_step": len(launches), "parallelism": "none (1 GPU)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "bs1": bs1,
+        "kernel_classes": _class_summary(launches, per_launch),
+        "create_s": round(create_s, 3),
+        "weight_bytes": stats["weight_bytes"], "arena_bytes": stats["arena_bytes"],
+        "wall_s_timed": round(wall, 4),
+    }
+    sg.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,227 @@
+"""ctypes binding of include/byoc.h (argument marshalling only).
+
+Every computation runs in the HIP library; PyTorch supplies device memory
+and streams.  Loading fails loudly when the built library is missing.
+"""
+
+import ctypes
+import json as _json
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbyoc.so")
+
+BYOC_OK = 0
+F32, BF16 = 0, 1
+NCHW, NHWC, ROWMAJOR = 0, 1, 2
+KIND_NAMES = ["conv_mfma", "conv_f32", "depthwise", "maxpool", "avgpool", "add", "transform",
+              "reduce"]
+STATUS_NAMES = ["OK", "INVALID_ARG", "PARSE", "UNSUPPORTED", "SHAPE", "DEVICE", "OOM", "INTERNAL"]
+
+# Every entry point declared in include/byoc.h.
+EXPORTS = ["byoc_subgraph_validate", "byoc_subgraph_create", "byoc_subgraph_run",
+           "byoc_subgraph_destroy", "byoc_subgraph_num_io", "byoc_subgraph_io_desc",
+           "byoc_subgraph_stats", "byoc_subgraph_num_launches", "byoc_subgraph_launch_info",
+           "byoc_subgraph_profile_begin", "byoc_subgraph_profile_end", "byoc_last_error"]
+
+
+class ByocConst(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.POINTER(ctypes.c_int64))]
+
+
+class TensorDesc(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("layout", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("shape", ctypes.c_int64 * 8)]
+
+
+class LaunchInfo(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("node", ctypes.c_int32), ("flops", ctypes.c_int64),
+                ("bytes", ctypes.c_int64), ("name", ctypes.c_char * 64)]
+
+
+class ByocError(RuntimeError):
+    def __init__(self, status, message):
+        self.status = status
+        self.status_name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
+        super().__init__("byoc %s: %s" % (self.status_name, message))
+
+
+_lib = None
+
+
+def load_library(path=LIB_PATH):
+    """Load libbyoc.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("HIP library %s is missing: build it with "
+                           "`python -m paper_2105_03215_amd.build`" % path)
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    sig = {
+        "byoc_subgraph_validate": [ctypes.c_char_p, sz, ctypes.POINTER(ByocConst), i32],
+        "byoc_subgraph_create": [ctypes.c_char_p, sz, ctypes.POINTER(ByocConst), i32, i32,
+                                 ctypes.POINTER(P)],
+        "byoc_subgraph_run": [P, ctypes.POINTER(P), i32, ctypes.POINTER(P), i32, P],
+        "byoc_subgraph_destroy": [P],
+        "byoc_subgraph_num_io": [P, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "byoc_subgraph_io_desc": [P, i32, i32, ctypes.POINTER(TensorDesc)],
+        "byoc_subgraph_stats": [P, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)],
+        "byoc_subgraph_num_launches": [P, ctypes.POINTER(i32)],
+        "byoc_subgraph_launch_info": [P, i32, ctypes.POINTER(LaunchInfo)],
+        "byoc_subgraph_profile_begin": [P, i32],
+        "byoc_subgraph_profile_end": [P, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.byoc_last_error.argtypes = []
+    lib.byoc_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != BYOC_OK:
+        msg = load_library().byoc_last_error().decode("utf-8", "replace")
+        raise ByocError(status, msg)
+
+
+def _json_bytes(graph):
+    if isinstance(graph, (bytes, bytearray)):
+        return bytes(graph)
+    if isinstance(graph, str):
+        return graph.encode("utf-8")
+    return _json.dumps(graph).encode("utf-8")
+
+
+class _Consts:
+    """Host constant arrays marshalled into a byoc_const array (kept alive)."""
+
+    def __init__(self, consts):
+        self.arrays = []
+        self.shapes = []
+        n = len(consts)
+        self.c = (ByocConst * max(n, 1))()
+        for i, a in enumerate(consts):
+            if hasattr(a, "detach"):  # torch tensor on the host
+                import torch
+                if a.dtype == torch.bfloat16:
+                    a = a.contiguous().view(torch.int16).numpy().view(np.uint16)
+                else:
+                    a = a.detach().cpu().numpy()
+            a = np.asarray(a)
+            if a.dtype == np.uint16:
+                dt = BF16
+            else:
+                a = a.astype(np.float32, copy=False)
+                dt = F32
+            a = np.ascontiguousarray(a)
+            shape = (ctypes.c_int64 * max(a.ndim, 1))(*a.shape)
+            self.arrays.append(a)
+            self.shapes.append(shape)
+            self.c[i] = ByocConst(a.ctypes.data, dt, a.ndim, shape)
+        self.n = n
+
+
+def validate(graph, consts):
+    """Host-only check of a serialized subgraph against its constants."""
+    lib = load_library()
+    js = _json_bytes(graph)
+    cs = _Consts(consts)
+    _check(lib.byoc_subgraph_validate(js, len(js), cs.c, cs.n))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+class Subgraph:
+    """An execution engine for one serialized subgraph on one HIP device."""
+
+    def __init__(self, graph, consts, device=0):
+        self.lib = load_library()
+        js = _json_bytes(graph)
+        cs = _Consts(consts)
+        h = ctypes.c_void_p()
+        _check(self.lib.byoc_subgraph_create(js, len(js), cs.c, cs.n, int(device), ctypes.byref(h)))
+        self.handle = h
+        self.device = device
+        n_in, n_out = ctypes.c_int32(), ctypes.c_int32()
+        _check(self.lib.byoc_subgraph_num_io(h, ctypes.byref(n_in), ctypes.byref(n_out)))
+        self.n_in, self.n_out = n_in.value, n_out.value
+
+    def io_desc(self, is_output, idx):
+        d = TensorDesc()
+        _check(self.lib.byoc_subgraph_io_desc(self.handle, int(is_output), int(idx), ctypes.byref(d)))
+        return {"dtype": "bf16" if d.dtype == BF16 else "f32",
+                "layout": ["NCHW", "NHWC", "ROWMAJOR"][d.layout],
+                "shape": [d.shape[i] for i in range(d.ndim)]}
+
+    def stats(self):
+        m, w, a = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(self.lib.byoc_subgraph_stats(self.handle, ctypes.byref(m), ctypes.byref(w), ctypes.byref(a)))
+        return {"macs": m.value, "weight_bytes": w.value, "arena_bytes": a.value}
+
+    def launches(self):
+        n = ctypes.c_int32()
+        _check(self.lib.byoc_subgraph_num_launches(self.handle, ctypes.byref(n)))
+        out = []
+        for i in range(n.value):
+            li = LaunchInfo()
+            _check(self.lib.byoc_subgraph_launch_info(self.handle, i, ctypes.byref(li)))
+            out.append({"kind": KIND_NAMES[li.kind], "node": li.node, "flops": li.flops,
+                        "bytes": li.bytes, "name": li.name.decode()})
+        return out
+
+    def run(self, inputs, outputs, stream=None):
+        """Enqueue one run on `stream` (a torch.cuda.Stream, a raw hipStream_t
+        int, or None for torch's current stream)."""
+        ins = (ctypes.c_void_p * max(len(inputs), 1))(*[_ptr(t) for t in inputs])
+        outs = (ctypes.c_void_p * max(len(outputs), 1))(*[_ptr(t) for t in outputs])
+        if stream is None:
+            import torch
+            s = torch.cuda.current_stream(self.device).cuda_stream
+        elif isinstance(stream, int):
+            s = stream
+        else:
+            s = stream.cuda_stream
+        _check(self.lib.byoc_subgraph_run(self.handle, ins, len(inputs), outs, len(outputs),
+                                          ctypes.c_void_p(s)))
+
+    def profile_begin(self, max_runs):
+        _check(self.lib.byoc_subgraph_profile_begin(self.handle, int(max_runs)))
+
+    def profile_end(self):
+        n = len(self.launches())
+        ms = (ctypes.c_float * max(n, 1))()
+        runs = ctypes.c_int32()
+        _check(self.lib.byoc_subgraph_profile_end(self.handle, ms, n, ctypes.byref(runs)))
+        return [ms[i] for i in range(n)], runs.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _check(self.lib.byoc_subgraph_destroy(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

@@ -1,0 +1,302 @@
+// Implicit-GEMM convolution on CDNA4 bf16 MFMA (v_mfma_f32_16x16x32_bf16).
+//
+// The conv composite y[n,p,q,k] = act(sum_{r,s,c} x[n, p*sh-pt+r, q*sw-pl+s, c]
+// * w[k,r,s,c] + b[k] + res[n,p,q,k]) is a GEMM with M = N*P*Q output
+// pixels, N = K output channels and a reduction of length R*S*C.  With NHWC
+// activations and weights packed K-major with kk = (r*S+s)*Cp + c, a row of
+// either operand is contiguous along the reduction, so every lane moves 16
+// bytes (8 bf16) per global load and per LDS read, which is exactly one MFMA
+// operand register.  Dense layers run through the same kernel as 1x1 convs
+// on 1x1 images.
+//
+// Workgroup: 256 threads = 4 waves; tile BM pixels x BN channels; the
+// reduction advances 64 elements per LDS stage (two MFMA k-steps).  Global
+// loads for stage t+1 are issued before the MFMAs of stage t and written to
+// the other LDS buffer afterwards (one barrier per stage).  LDS rows are 128
+// bytes (8 chunks of 16 B) with the chunk index XOR-swizzled by the row so
+// that the 16 rows one MFMA operand read touches fall on distinct banks.
+//
+// The weights are the MFMA A operand and the pixels the B operand, so each
+// lane's 4 accumulators hold 4 consecutive output channels of one pixel:
+// the epilogue reads 4 biases, 4 residual values and writes 8 contiguous
+// bytes per lane, with bias, residual add, activation and bf16 rounding
+// fused.  With split-K each split writes fp32 partials and a second kernel
+// reduces them in a fixed order (bitwise reproducible) with the same
+// epilogue.
+#include "device_common.h"
+
+namespace byoc {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+constexpr int kBK = 64;          // reduction elements per stage
+constexpr int kCH = kBK / 8;     // 16-byte chunks per tile row
+constexpr int kNT = 256;         // threads per workgroup
+constexpr int kRowsPerPass = kNT / kCH;
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+template <int BM, int BN, int WM, int WN, bool ALIGNED, bool SPLIT>
+__global__ __launch_bounds__(kNT) void conv_mfma_kernel(ConvParams p) {
+  constexpr int WTM = BM / WM;
+  constexpr int WTN = BN / WN;
+  constexpr int TM = WTM / 16;
+  constexpr int TN = WTN / 16;
+  constexpr int AR = BM / kRowsPerPass;
+  constexpr int BR = BN / kRowsPerPass;
+  static_assert(WM * WN == 4, "4 waves");
+  static_assert(TM >= 1 && TN >= 1 && AR >= 1 && BR >= 1, "tile too small");
+
+  __shared__ uint4 sA[2][BM * kCH];
+  __shared__ uint4 sB[2][BN * kCH];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WN;
+  const int wn = wave % WN;
+
+  // Tile order: workgroups are dealt round-robin to the 8 XCDs; remap so
+  // that each XCD gets a contiguous run of tiles (shared activation rows
+  // stay in one L2).
+  const int ntn = (p.Kp + BN - 1) / BN;
+  int bid = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int tn = bid % ntn;
+  const int tm = bid / ntn;
+  const int m0 = tm * BM;
+  const int n0 = tn * BN;
+
+  const int nk_total = (p.Kg + kBK - 1) / kBK;
+  int kt_begin = 0, kt_end = nk_total;
+  if (SPLIT) {
+    kt_begin = blockIdx.y * p.k_tiles_per_split;
+    kt_end = min(nk_total, kt_begin + p.k_tiles_per_split);
+  }
+
+  const int cv = tid & (kCH - 1);
+  const int r0 = tid / kCH;
+  const int PQ = p.P * p.Q;
+
+  int a_base[AR], a_ih[AR], a_iw[AR];
+#pragma unroll
+  for (int i = 0; i < AR; ++i) {
+    const int m = m0 + r0 + i * kRowsPerPass;
+    if (m < p.M) {
+      const int n = m / PQ;
+      const int pq = m - n * PQ;
+      const int pp = pq / p.Q;
+      const int qq = pq - pp * p.Q;
+      a_base[i] = n * p.H * p.W * p.Cp;
+      a_ih[i] = pp * p.sh - p.pt;
+      a_iw[i] = qq * p.sw - p.pl;
+    } else {
+      a_base[i] = 0;
+      a_ih[i] = -(1 << 28);  // never inside [0, H)
+      a_iw[i] = 0;
+    }
+  }
+  const bf16_t* wrow = p.w + (size_t)(n0 + r0) * p.Kgp + cv * 8;
+
+  uint4 ra[AR], rb[BR];
+  auto load = [&](int kt) {
+    const int kk0 = kt * kBK;
+    int r, s, c;
+    bool kval = true;
+    if (ALIGNED) {
+      const int rs = kk0 / p.Cp;
+      c = kk0 - rs * p.Cp + cv * 8;
+      r = rs / p.S;
+      s = rs - r * p.S;
+    } else {
+      const int kk = kk0 + cv * 8;
+      const int rs = kk / p.Cp;
+      c = kk - rs * p.Cp;
+      r = rs / p.S;
+      s = rs - r * p.S;
+      kval = kk < p.Kg;
+    }
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+      const int ih = a_ih[i] + r;
+      const int iw = a_iw[i] + s;
+      const bool ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+      ra[i] = ok ? *(const uint4*)(p.x + a_base[i] + (ih * p.W + iw) * p.Cp + c)
+                 : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+      rb[i] = *(const uint4*)(wrow + (size_t)i * kRowsPerPass * p.Kgp + kk0);
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+      const int row = r0 + i * kRowsPerPass;
+      sA[buf][row * kCH + (cv ^ (row & 7))] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < BR; ++i) {
+      const int row = r0 + i * kRowsPerPass;
+      sB[buf][row * kCH + (cv ^ (row & 7))] = rb[i];
+    }
+  };
+
+  f32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      const int chunk = ks * 4 + (lane >> 4);
+      bf16x8 af[TN], bfr[TM];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int row = wn * WTN + i * 16 + (lane & 15);
+        af[i] = as_bf16x8(sB[buf][row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * WTM + j * 16 + (lane & 15);
+        bfr[j] = as_bf16x8(sA[buf][row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  if (kt_begin < kt_end) {
+    load(kt_begin);
+    store(0);
+    __syncthreads();
+    int buf = 0;
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
+      const bool more = kt + 1 < kt_end;
+      if (more) load(kt + 1);
+      compute(buf);
+      if (more) store(buf ^ 1);
+      __syncthreads();
+      buf ^= 1;
+    }
+  }
+
+  // Epilogue: lane holds channels k..k+3 of pixel m for each (i, j).
+#pragma unroll
+  for (int i = 0; i < TN; ++i) {
+    const int k = n0 + wn * WTN + i * 16 + 4 * (lane >> 4);
+    if (k >= p.Kp) continue;
+    if (SPLIT) {
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+        if (m >= p.M) continue;
+        float4 v = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        *(float4*)(p.partial + ((size_t)blockIdx.y * p.M + m) * p.Kp + k) = v;
+      }
+    } else {
+      const float4 bv = p.bias ? *(const float4*)(p.bias + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+        if (m >= p.M) continue;
+        float v0 = acc[i][j][0] + bv.x;
+        float v1 = acc[i][j][1] + bv.y;
+        float v2 = acc[i][j][2] + bv.z;
+        float v3 = acc[i][j][3] + bv.w;
+        if (p.res) {
+          const uint2 rr = *(const uint2*)(p.res + (size_t)m * p.ldr + k);
+          v0 += __uint_as_float(rr.x << 16);
+          v1 += __uint_as_float(rr.x & 0xFFFF0000u);
+          v2 += __uint_as_float(rr.y << 16);
+          v3 += __uint_as_float(rr.y & 0xFFFF0000u);
+        }
+        v0 = apply_act(v0, p.act);
+        v1 = apply_act(v1, p.act);
+        v2 = apply_act(v2, p.act);
+        v3 = apply_act(v3, p.act);
+        *(uint2*)(p.y + (size_t)m * p.ldy + k) = make_uint2(pack2_bf16(v0, v1), pack2_bf16(v2, v3));
+      }
+    }
+  }
+}
+
+// Split-K reduction: one thread per 4 channels of one pixel; partials summed
+// in split order, then bias, residual, activation, bf16 rounding.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
+  const int k4 = p.Kp / 4;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)p.M * k4) return;
+  const int m = (int)(idx / k4);
+  const int k = (int)(idx - (int64_t)m * k4) * 4;
+  float4 acc = *(const float4*)(p.partial + (size_t)m * p.Kp + k);
+  for (int sp = 1; sp < p.splits; ++sp) {
+    const float4 t = *(const float4*)(p.partial + ((size_t)sp * p.M + m) * p.Kp + k);
+    acc.x += t.x;
+    acc.y += t.y;
+    acc.z += t.z;
+    acc.w += t.w;
+  }
+  if (p.bias) {
+    const float4 bv = *(const float4*)(p.bias + k);
+    acc.x += bv.x;
+    acc.y += bv.y;
+    acc.z += bv.z;
+    acc.w += bv.w;
+  }
+  if (p.res) {
+    const uint2 rr = *(const uint2*)(p.res + (size_t)m * p.ldr + k);
+    acc.x += __uint_as_float(rr.x << 16);
+    acc.y += __uint_as_float(rr.x & 0xFFFF0000u);
+    acc.z += __uint_as_float(rr.y << 16);
+    acc.w += __uint_as_float(rr.y & 0xFFFF0000u);
+  }
+  *(uint2*)(p.y + (size_t)m * p.ldy + k) =
+      make_uint2(pack2_bf16(apply_act(acc.x, p.act), apply_act(acc.y, p.act)),
+                 pack2_bf16(apply_act(acc.z, p.act), apply_act(acc.w, p.act)));
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
+  const int ntm = (p.M + BM - 1) / BM;
+  const int ntn = (p.Kp + BN - 1) / BN;
+  const bool aligned = (p.Cp % kBK) == 0;
+  const bool split = p.splits > 1;
+  dim3 grid(ntm * ntn, split ? p.splits : 1);
+  if (aligned && !split) conv_mfma_kernel<BM, BN, WM, WN, true, false><<<grid, kNT, 0, s>>>(p);
+  else if (aligned) conv_mfma_kernel<BM, BN, WM, WN, true, true><<<grid, kNT, 0, s>>>(p);
+  else if (!split) conv_mfma_kernel<BM, BN, WM, WN, false, false><<<grid, kNT, 0, s>>>(p);
+  else conv_mfma_kernel<BM, BN, WM, WN, false, true><<<grid, kNT, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool conv_mfma_tile_supported(int bm, int bn) {
+  return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
+         (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+}
+
+hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s) {
+  if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2, 2>(p, s);
+  if (t.bm == 128 && t.bn == 64) return launch_tile<128, 64, 4, 1>(p, s);
+  if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 1, 4>(p, s);
+  if (t.bm == 64 && t.bn == 64) return launch_tile<64, 64, 2, 2>(p, s);
+  if (t.bm == 32 && t.bn == 64) return launch_tile<32, 64, 1, 4>(p, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.M * (p.Kp / 4);
+  splitk_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace byoc

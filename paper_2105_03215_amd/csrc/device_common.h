@@ -1,0 +1,57 @@
+// Device helpers shared by the kernel files: bf16 conversion and activations.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.h"
+
+namespace byoc {
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// Round to nearest, ties to even (the hardware v_cvt_pk_bf16_f32 rounding).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  __bf16 v = (__bf16)f;
+  return __builtin_bit_cast(bf16_t, v);
+}
+
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ float apply_act(float v, int act) {
+  switch (act) {
+    case kActRelu: return fmaxf(v, 0.0f);
+    case kActRelu6: return fminf(fmaxf(v, 0.0f), 6.0f);
+    // x * Phi(x) with Phi(x) = erfc(-x / sqrt 2) / 2: no cancellation for x << 0
+    case kActGelu: return 0.5f * v * erfcf(-v * 0.70710678118654752440f);
+    default: return v;
+  }
+}
+
+// Unpacks 8 bf16 held in a uint4 into floats.
+__device__ __forceinline__ void unpack8(const uint4& u, float* f) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+
+__device__ __forceinline__ uint4 pack8(const float* f) {
+  uint4 u;
+  u.x = pack2_bf16(f[0], f[1]);
+  u.y = pack2_bf16(f[2], f[3]);
+  u.z = pack2_bf16(f[4], f[5]);
+  u.w = pack2_bf16(f[6], f[7]);
+  return u;
+}
+
+inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+}  // namespace byoc

@@ -1,0 +1,712 @@
+// Engine creation (planning, constant packing, arena layout) and runs.
+#include "engine.h"
+
+#include <algorithm>
+#include <climits>
+#include <cstdio>
+#include <cstring>
+
+namespace byoc {
+namespace {
+
+int64_t rup(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+int64_t numel(const std::vector<int64_t>& s) {
+  int64_t n = 1;
+  for (int64_t d : s) n *= d;
+  return n;
+}
+
+#define HIP_TRY(expr, what)                                                                   \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess)                                                                     \
+      return Status::Err(e_ == hipErrorOutOfMemory ? BYOC_ERR_OOM : BYOC_ERR_DEVICE,          \
+                         std::string(what) + ": " + hipGetErrorString(e_));                   \
+  } while (0)
+
+constexpr int kRowPad = 256;  // packed weight rows are padded to this (>= any tile BN)
+constexpr int kKPad = 64;     // packed reduction length is padded to this (the stage depth)
+
+struct PackJob {
+  enum Kind { ConvW, DwW, Vec, Copy } kind;
+  int cidx = -1;       // constant index
+  int64_t dst = 0;     // byte offset in the weights region
+  int K = 0, Cg = 0, R = 0, S = 0, Cp = 0, Kgp = 0, rows = 0;
+  int n = 0, n_out = 0;
+};
+
+// Chooses the workgroup tile and split-K factor of an implicit GEMM.
+void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* kps) {
+  static const int cands[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}, {32, 64}};
+  const int nk = (int)((Kg + kKPad - 1) / kKPad);
+  int best = -1;
+  for (int i = 0; i < 5; ++i) {
+    const int bm = cands[i][0], bn = cands[i][1];
+    const int64_t tm = (M + bm - 1) / bm, tn = (Kp + bn - 1) / bn;
+    const double eff = (double)M * Kp / (double)(tm * bm * tn * bn);
+    if (tm * tn >= 240 && eff >= 0.75) {
+      best = i;
+      break;
+    }
+  }
+  if (best < 0) best = M >= 64 ? 3 : 4;
+  t->bm = cands[best][0];
+  t->bn = cands[best][1];
+  const int64_t tiles = ((M + t->bm - 1) / t->bm) * ((Kp + t->bn - 1) / t->bn);
+  *splits = 1;
+  *kps = nk;
+  if (tiles < 128 && nk >= 8) {
+    int s = (int)std::min<int64_t>(nk / 4, (256 + tiles - 1) / tiles);
+    s = std::max(1, std::min(s, 16));
+    if (s > 1) {
+      *kps = (nk + s - 1) / s;
+      *splits = (nk + *kps - 1) / *kps;
+    }
+  }
+}
+
+struct Planner {
+  Engine* e;
+  Graph& g;
+  bool bf16;
+  std::vector<Ref> loc;
+  std::vector<int> cp;  // channel stride of each value's internal form
+  std::vector<PackJob> jobs;
+  int64_t wbytes = 0;
+
+  Planner(Engine* e_, Graph& g_) : e(e_), g(g_), bf16(g_.compute == DType::BF16) {
+    loc.resize(g.values.size());
+    cp.assign(g.values.size(), 0);
+  }
+
+  int64_t internal_bytes(int v) const {
+    const auto& s = g.values[v].shape;
+    if (!bf16) return numel(s) * 4;
+    const int64_t c = rup(s[1], 8);
+    return (s.size() == 4 ? s[0] * s[2] * s[3] : s[0]) * c * 2;
+  }
+  Ref arena(int64_t bytes) {
+    ArenaBuf b;
+    b.bytes = rup(bytes, 256);
+    b.first = INT_MAX;
+    b.last = -1;
+    e->bufs.push_back(b);
+    Ref r;
+    r.kind = Ref::Arena;
+    r.idx = (int)e->bufs.size() - 1;
+    return r;
+  }
+  Ref wslot(int64_t bytes) {
+    Ref r;
+    r.kind = Ref::Weights;
+    r.off = wbytes;
+    wbytes += rup(bytes, 256);
+    return r;
+  }
+  static Ref io(Ref::Kind k, int i) {
+    Ref r;
+    r.kind = k;
+    r.idx = i;
+    return r;
+  }
+  void name(Launch& L, const char* s) { std::snprintf(L.info.name, sizeof(L.info.name), "%s", s); }
+
+  int64_t ext_bytes(int v, DType dt) const {
+    return numel(g.values[v].shape) * (dt == DType::BF16 ? 2 : 4);
+  }
+  int64_t act_bytes(int v) const { return numel(g.values[v].shape) * (bf16 ? 2 : 4); }
+
+  Status plan();
+  void plan_node(int ni);
+};
+
+Status Planner::plan() {
+  // ---- inputs: direct use or boundary transform ----------------------------
+  for (size_t i = 0; i < g.inputs.size(); ++i) {
+    const IoDesc& in = g.inputs[i];
+    const int v = in.value;
+    const auto& s = g.values[v].shape;
+    cp[v] = bf16 ? (int)rup(s[1], 8) : (int)s[1];
+    const bool direct = bf16 ? (s.size() == 2 && in.dtype == DType::BF16 && s[1] % 8 == 0)
+                             : (in.dtype == DType::F32);
+    if (direct) {
+      loc[v] = io(Ref::Input, (int)i);
+      continue;
+    }
+    loc[v] = arena(internal_bytes(v));
+    Launch L;
+    L.info.kind = BYOC_K_TRANSFORM;
+    L.info.node = -1;
+    L.x = io(Ref::Input, (int)i);
+    L.y = loc[v];
+    L.src_bf16 = in.dtype == DType::BF16;
+    L.info.bytes = ext_bytes(v, in.dtype) + act_bytes(v);
+    if (!bf16) {
+      L.op = Launch::Cast;
+      L.dst_bf16 = false;
+      L.n = numel(s);
+      name(L, "cast_in");
+    } else if (s.size() == 4) {
+      L.op = Launch::NchwToNhwc;
+      L.N = (int)s[0], L.C = (int)s[1], L.H = (int)s[2], L.W = (int)s[3], L.Cp = cp[v];
+      name(L, "nchw_to_nhwc");
+    } else {
+      L.op = Launch::RowsToPadded;
+      L.M = (int)s[0], L.K = (int)s[1], L.Kp = cp[v];
+      name(L, "rows_to_padded");
+    }
+    e->launches.push_back(L);
+  }
+  // ---- nodes ---------------------------------------------------------------
+  std::vector<bool> direct_out(g.outputs.size(), false);
+  for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
+    const Node& n = g.nodes[ni];
+    const int v = n.out;
+    const auto& s = g.values[v].shape;
+    cp[v] = bf16 ? (int)rup(s[1], 8) : (int)s[1];
+    bool placed = false;
+    for (size_t j = 0; j < g.outputs.size() && !placed; ++j) {
+      const IoDesc& o = g.outputs[j];
+      if (o.value != v || direct_out[j]) continue;
+      const bool ok = bf16 ? (s.size() == 2 && o.dtype == DType::BF16 && s[1] % 8 == 0)
+                           : (o.dtype == DType::F32);
+      if (ok) {
+        loc[v] = io(Ref::Output, (int)j);
+        direct_out[j] = true;
+        placed = true;
+      }
+    }
+    if (!placed) loc[v] = arena(internal_bytes(v));
+    plan_node((int)ni);
+  }
+  // ---- outputs not written in place: boundary transforms ---------------------
+  for (size_t j = 0; j < g.outputs.size(); ++j) {
+    if (direct_out[j]) continue;
+    const IoDesc& o = g.outputs[j];
+    const int v = o.value;
+    const auto& s = g.values[v].shape;
+    Launch L;
+    L.info.kind = BYOC_K_TRANSFORM;
+    L.info.node = -1;
+    L.x = loc[v];
+    L.y = io(Ref::Output, (int)j);
+    L.dst_bf16 = o.dtype == DType::BF16;
+    L.info.bytes = act_bytes(v) + ext_bytes(v, o.dtype);
+    const bool src_is_input = g.values[v].source == Value::Input && loc[v].kind == Ref::Input;
+    if (!bf16) {
+      L.op = Launch::Cast;
+      L.src_bf16 = src_is_input ? g.inputs[g.values[v].index].dtype == DType::BF16 : false;
+      L.n = numel(s);
+      name(L, "cast_out");
+    } else if (s.size() == 4) {
+      L.op = Launch::NhwcToNchw;
+      L.N = (int)s[0], L.C = (int)s[1], L.H = (int)s[2], L.W = (int)s[3], L.Cp = cp[v];
+      name(L, "nhwc_to_nchw");
+    } else {
+      L.op = Launch::PaddedToRows;
+      L.M = (int)s[0], L.K = (int)s[1], L.Kp = cp[v];
+      name(L, "padded_to_rows");
+    }
+    e->launches.push_back(L);
+  }
+  return Status::Ok();
+}
+
+void Planner::plan_node(int ni) {
+  const Node& n = g.nodes[ni];
+  const auto& xs = g.values[n.data].shape;
+  const auto& ys = g.values[n.out].shape;
+  Launch L;
+  L.info.node = ni;
+  L.x = loc[n.data];
+  L.y = loc[n.out];
+  L.act = (int)n.act;
+  if (n.residual >= 0) L.res = loc[n.residual];
+  const int64_t ebytes = bf16 ? 2 : 4;
+
+  if (n.op == OpKind::Conv || n.op == OpKind::Dense) {
+    const auto& ws = g.values[n.weight].shape;
+    const bool dense = n.op == OpKind::Dense;
+    const int K = (int)ws[0];
+    const int Cg = dense ? (int)ws[1] : (int)ws[1];
+    const int R = dense ? 1 : (int)ws[2];
+    const int S = dense ? 1 : (int)ws[3];
+    const int N = (int)xs[0];
+    const int C = (int)xs[1];
+    const int H = dense ? 1 : (int)xs[2];
+    const int W = dense ? 1 : (int)xs[3];
+    const int P = dense ? 1 : (int)ys[2];
+    const int Q = dense ? 1 : (int)ys[3];
+    const int wc = g.values[n.weight].index;
+    const int bc = n.bias >= 0 ? g.values[n.bias].index : -1;
+    L.info.flops = 2 * n.macs;
+    L.info.bytes = act_bytes(n.data) + numel(ws) * ebytes + (bc >= 0 ? K * 4 : 0) +
+                   act_bytes(n.out) * (n.residual >= 0 ? 2 : 1);
+    if (!bf16) {
+      L.op = Launch::ConvF32;
+      L.info.kind = BYOC_K_CONV_F32;
+      ConvF32Params& p = L.cf;
+      p.N = N, p.C = C, p.H = H, p.W = W, p.K = K, p.P = P, p.Q = Q, p.R = R, p.S = S;
+      p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1];
+      p.groups = n.groups, p.act = (int)n.act;
+      L.w = wslot(numel(ws) * 4);
+      jobs.push_back({PackJob::Copy, wc, L.w.off, 0, 0, 0, 0, 0, 0, 0, (int)numel(ws), (int)numel(ws)});
+      if (bc >= 0) {
+        L.bias = wslot(K * 4);
+        jobs.push_back({PackJob::Vec, bc, L.bias.off, 0, 0, 0, 0, 0, 0, 0, K, K});
+      }
+      name(L, n.depthwise ? "conv_f32_depthwise" : "conv_f32_direct");
+      e->launches.push_back(L);
+      return;
+    }
+    const int Cp = cp[n.data];
+    const int Kp = cp[n.out];
+    if (n.depthwise) {
+      L.op = Launch::Depthwise;
+      L.info.kind = BYOC_K_DEPTHWISE;
+      DwParams& p = L.dw;
+      p.N = N, p.H = H, p.W = W, p.Cp = Cp, p.P = P, p.Q = Q, p.R = R, p.S = S;
+      p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1], p.act = (int)n.act;
+      L.w = wslot((int64_t)R * S * Cp * 2);
+      jobs.push_back({PackJob::DwW, wc, L.w.off, K, 1, R, S, Cp, 0, 0, 0, 0});
+      L.bias = wslot(Cp * 4);
+      jobs.push_back({PackJob::Vec, bc, L.bias.off, 0, 0, 0, 0, 0, 0, 0, K, Cp});
+      name(L, "depthwise_nhwc");
+      e->launches.push_back(L);
+      return;
+    }
+    ConvParams& p = L.conv;
+    p.N = N, p.H = H, p.W = W, p.Cp = Cp, p.P = P, p.Q = Q, p.R = R, p.S = S;
+    p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1];
+    p.M = N * P * Q;
+    p.Kp = Kp;
+    p.Kg = R * S * Cp;
+    p.Kgp = (int)rup(p.Kg, kKPad);
+    p.ldy = Kp;
+    p.ldr = Kp;
+    p.act = (int)n.act;
+    const int rows = (int)rup(Kp, kRowPad);
+    L.w = wslot((int64_t)rows * p.Kgp * 2);
+    jobs.push_back({PackJob::ConvW, wc, L.w.off, K, Cg, R, S, Cp, p.Kgp, rows, 0, 0});
+    L.bias = wslot((int64_t)rows * 4);
+    jobs.push_back({PackJob::Vec, bc, L.bias.off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? K : 0, rows});
+    int splits, kps;
+    choose_conv_tile(p.M, Kp, p.Kg, &L.tile, &splits, &kps);
+    p.splits = splits;
+    p.k_tiles_per_split = kps;
+    L.op = Launch::ConvMfma;
+    L.info.kind = BYOC_K_CONV_MFMA;
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_split%d", L.tile.bm,
+                  L.tile.bn, splits);
+    if (splits > 1) {
+      L.partial = arena((int64_t)splits * p.M * Kp * 4);
+      Launch Rd = L;
+      Rd.op = Launch::SplitReduce;
+      Rd.info.kind = BYOC_K_REDUCE;
+      Rd.info.flops = 0;
+      Rd.info.bytes = 0;
+      name(Rd, "splitk_reduce");
+      L.y = Ref();
+      L.res = Ref();
+      Ref keep_bias = L.bias;
+      L.bias = Ref();
+      e->launches.push_back(L);
+      Rd.bias = keep_bias;
+      Rd.x = Ref();
+      Rd.w = Ref();
+      e->launches.push_back(Rd);
+    } else {
+      e->launches.push_back(L);
+    }
+    return;
+  }
+  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool) {
+    PoolParams& p = L.pool;
+    p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3], p.Cp = cp[n.data];
+    p.R = n.pool[0], p.S = n.pool[1], p.sh = n.stride[0], p.sw = n.stride[1];
+    p.pt = n.pad[0], p.pl = n.pad[1];
+    p.P = n.op == OpKind::MaxPool ? (int)ys[2] : 1;
+    p.Q = n.op == OpKind::MaxPool ? (int)ys[3] : 1;
+    L.info.bytes = act_bytes(n.data) + act_bytes(n.out);
+    if (n.op == OpKind::MaxPool) {
+      L.op = bf16 ? Launch::MaxPoolBf16 : Launch::MaxPoolF32;
+      L.info.kind = BYOC_K_MAXPOOL;
+      name(L, bf16 ? "maxpool_nhwc" : "maxpool_nchw_f32");
+    } else {
+      L.op = bf16 ? Launch::AvgPoolBf16 : Launch::AvgPoolF32;
+      L.info.kind = BYOC_K_AVGPOOL;
+      name(L, bf16 ? "avgpool_nhwc" : "avgpool_nchw_f32");
+    }
+    e->launches.push_back(L);
+    return;
+  }
+  // Add
+  L.op = bf16 ? Launch::AddBf16 : Launch::AddF32;
+  L.info.kind = BYOC_K_ADD;
+  L.other = loc[n.other];
+  L.n = bf16 ? internal_bytes(n.out) / 2 : numel(ys);
+  L.info.bytes = 3 * act_bytes(n.out);
+  name(L, bf16 ? "add_bf16" : "add_f32");
+  e->launches.push_back(L);
+}
+
+// First-fit offset allocator over the arena with coalescing frees.
+struct OffsetAlloc {
+  std::vector<std::pair<int64_t, int64_t>> free_;  // (offset, size), sorted by offset
+  int64_t hwm = 0;
+  int64_t alloc(int64_t size) {
+    for (size_t i = 0; i < free_.size(); ++i) {
+      if (free_[i].second >= size) {
+        int64_t off = free_[i].first;
+        free_[i].first += size;
+        free_[i].second -= size;
+        if (free_[i].second == 0) free_.erase(free_.begin() + i);
+        return off;
+      }
+    }
+    // extend: merge with a trailing free block that ends at hwm
+    if (!free_.empty() && free_.back().first + free_.back().second == hwm) {
+      int64_t off = free_.back().first;
+      hwm = off + size;
+      free_.pop_back();
+      return off;
+    }
+    int64_t off = hwm;
+    hwm += size;
+    return off;
+  }
+  void release(int64_t off, int64_t size) {
+    auto it = std::lower_bound(free_.begin(), free_.end(), std::make_pair(off, (int64_t)0));
+    it = free_.insert(it, {off, size});
+    size_t i = it - free_.begin();
+    if (i + 1 < free_.size() && free_[i].first + free_[i].second == free_[i + 1].first) {
+      free_[i].second += free_[i + 1].second;
+      free_.erase(free_.begin() + i + 1);
+    }
+    if (i > 0 && free_[i - 1].first + free_[i - 1].second == free_[i].first) {
+      free_[i - 1].second += free_[i].second;
+      free_.erase(free_.begin() + i);
+    }
+  }
+};
+
+void layout_arena(Engine* e) {
+  auto touch = [&](const Ref& r, int li) {
+    if (r.kind != Ref::Arena) return;
+    ArenaBuf& b = e->bufs[r.idx];
+    b.first = std::min(b.first, li);
+    b.last = std::max(b.last, li);
+  };
+  for (size_t i = 0; i < e->launches.size(); ++i) {
+    const Launch& L = e->launches[i];
+    for (const Ref* r : {&L.x, &L.w, &L.bias, &L.res, &L.y, &L.partial, &L.other}) touch(*r, (int)i);
+  }
+  OffsetAlloc a;
+  for (size_t i = 0; i < e->launches.size(); ++i) {
+    for (auto& b : e->bufs)
+      if (b.first == (int)i && b.off < 0) b.off = a.alloc(b.bytes);
+    for (auto& b : e->bufs)
+      if (b.last == (int)i && b.off >= 0) a.release(b.off, b.bytes);
+  }
+  for (auto& b : e->bufs)
+    if (b.off < 0) b.off = a.alloc(b.bytes);  // unused buffer: give it space anyway
+  e->arena_bytes = a.hwm;
+}
+
+struct RunCtx {
+  const Engine* e;
+  const void* const* in;
+  void* const* out;
+  hipStream_t s;
+  void* ptr(const Ref& r) const {
+    switch (r.kind) {
+      case Ref::Arena: return e->arena + e->bufs[r.idx].off;
+      case Ref::Input: return const_cast<void*>(in[r.idx]);
+      case Ref::Output: return out[r.idx];
+      case Ref::Weights: return e->weights + r.off;
+      default: return nullptr;
+    }
+  }
+};
+
+hipError_t exec(const Launch& L, const RunCtx& c) {
+  switch (L.op) {
+    case Launch::ConvMfma:
+    case Launch::SplitReduce: {
+      ConvParams p = L.conv;
+      p.x = (const bf16_t*)c.ptr(L.x);
+      p.w = (const bf16_t*)c.ptr(L.w);
+      p.bias = (const float*)c.ptr(L.bias);
+      p.res = (const bf16_t*)c.ptr(L.res);
+      p.y = (bf16_t*)c.ptr(L.y);
+      p.partial = (float*)c.ptr(L.partial);
+      return L.op == Launch::ConvMfma ? launch_conv_mfma(p, L.tile, c.s) : launch_splitk_reduce(p, c.s);
+    }
+    case Launch::ConvF32: {
+      ConvF32Params p = L.cf;
+      p.x = (const float*)c.ptr(L.x);
+      p.w = (const float*)c.ptr(L.w);
+      p.bias = (const float*)c.ptr(L.bias);
+      p.res = (const float*)c.ptr(L.res);
+      p.y = (float*)c.ptr(L.y);
+      return launch_conv_f32(p, c.s);
+    }
+    case Launch::Depthwise: {
+      DwParams p = L.dw;
+      p.x = (const bf16_t*)c.ptr(L.x);
+      p.w = (const bf16_t*)c.ptr(L.w);
+      p.bias = (const float*)c.ptr(L.bias);
+      p.res = (const bf16_t*)c.ptr(L.res);
+      p.y = (bf16_t*)c.ptr(L.y);
+      return launch_depthwise(p, c.s);
+    }
+    case Launch::MaxPoolBf16:
+    case Launch::AvgPoolBf16:
+    case Launch::MaxPoolF32:
+    case Launch::AvgPoolF32: {
+      PoolParams p = L.pool;
+      p.x = c.ptr(L.x);
+      p.y = c.ptr(L.y);
+      if (L.op == Launch::MaxPoolBf16) return launch_maxpool_nhwc_bf16(p, c.s);
+      if (L.op == Launch::AvgPoolBf16) return launch_avgpool_nhwc_bf16(p, c.s);
+      if (L.op == Launch::MaxPoolF32) return launch_maxpool_nchw_f32(p, c.s);
+      return launch_avgpool_nchw_f32(p, c.s);
+    }
+    case Launch::AddBf16:
+      return launch_add_bf16((const bf16_t*)c.ptr(L.x), (const bf16_t*)c.ptr(L.other),
+                             (bf16_t*)c.ptr(L.y), L.n, L.act, c.s);
+    case Launch::AddF32:
+      return launch_add_f32((const float*)c.ptr(L.x), (const float*)c.ptr(L.other),
+                            (float*)c.ptr(L.y), L.n, L.act, c.s);
+    case Launch::NchwToNhwc:
+      return launch_nchw_to_nhwc(c.ptr(L.x), L.src_bf16, (bf16_t*)c.ptr(L.y), L.N, L.C, L.H, L.W,
+                                 L.Cp, c.s);
+    case Launch::NhwcToNchw:
+      return launch_nhwc_to_nchw((const bf16_t*)c.ptr(L.x), c.ptr(L.y), L.dst_bf16, L.N, L.C, L.H,
+                                 L.W, L.Cp, c.s);
+    case Launch::RowsToPadded:
+      return launch_rows_to_padded(c.ptr(L.x), L.src_bf16, (bf16_t*)c.ptr(L.y), L.M, L.K, L.Kp,
+                                   c.s);
+    case Launch::PaddedToRows:
+      return launch_padded_to_rows((const bf16_t*)c.ptr(L.x), c.ptr(L.y), L.dst_bf16, L.M, L.K,
+                                   L.Kp, c.s);
+    case Launch::Cast:
+      return launch_cast(c.ptr(L.x), L.src_bf16, c.ptr(L.y), L.dst_bf16, L.n, c.s);
+  }
+  return hipErrorInvalidValue;
+}
+
+void release(Engine* e) {
+  if (!e) return;
+  for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);
+  e->events.clear();
+  if (e->arena) (void)hipFree(e->arena);
+  if (e->weights) (void)hipFree(e->weights);
+  e->arena = nullptr;
+  e->weights = nullptr;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+Status build_device_state(Engine* e, Planner& pl, const byoc_const* consts) {
+  HIP_TRY(hipSetDevice(e->device), "hipSetDevice");
+  layout_arena(e);
+  e->weight_bytes = pl.wbytes;
+  if (e->weight_bytes > 0) HIP_TRY(hipMalloc(&e->weights, e->weight_bytes), "weights hipMalloc");
+  if (e->arena_bytes > 0) HIP_TRY(hipMalloc(&e->arena, e->arena_bytes), "arena hipMalloc");
+  // Stage every constant used by a pack job, then pack on the device.
+  std::vector<int64_t> stage_off(pl.g.const_values.size(), -1);
+  int64_t stage_bytes = 0;
+  for (const PackJob& j : pl.jobs) {
+    if (j.cidx < 0 || stage_off[j.cidx] >= 0) continue;
+    const Value& v = pl.g.values[pl.g.const_values[j.cidx]];
+    stage_off[j.cidx] = stage_bytes;
+    stage_bytes += rup(numel(v.shape) * (v.dtype == DType::BF16 ? 2 : 4), 256);
+  }
+  char* stage = nullptr;
+  if (stage_bytes > 0) HIP_TRY(hipMalloc(&stage, stage_bytes), "staging hipMalloc");
+  Status st;
+  for (size_t ci = 0; ci < stage_off.size() && st.ok(); ++ci) {
+    if (stage_off[ci] < 0) continue;
+    const Value& v = pl.g.values[pl.g.const_values[ci]];
+    const int64_t bytes = numel(v.shape) * (v.dtype == DType::BF16 ? 2 : 4);
+    hipError_t err = hipMemcpy(stage + stage_off[ci], consts[ci].data, bytes, hipMemcpyHostToDevice);
+    if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("constant upload: ") + hipGetErrorString(err));
+  }
+  for (const PackJob& j : pl.jobs) {
+    if (!st.ok()) break;
+    hipError_t err = hipSuccess;
+    char* dst = e->weights + j.dst;
+    if (j.cidx < 0) {
+      err = hipMemsetAsync(dst, 0, (size_t)j.n_out * 4, nullptr);
+    } else {
+      const Value& v = pl.g.values[pl.g.const_values[j.cidx]];
+      const bool sb = v.dtype == DType::BF16;
+      const void* src = stage + stage_off[j.cidx];
+      switch (j.kind) {
+        case PackJob::ConvW:
+          err = launch_pack_conv_weights(src, sb, (bf16_t*)dst, j.K, j.Cg, j.R, j.S, j.Cp, j.Kgp,
+                                         j.rows, nullptr);
+          break;
+        case PackJob::DwW:
+          err = launch_pack_dw_weights(src, sb, (bf16_t*)dst, j.K, j.R, j.S, j.Cp, nullptr);
+          break;
+        case PackJob::Vec:
+          err = launch_pack_vector_f32(src, sb, (float*)dst, j.n, j.n_out, nullptr);
+          break;
+        case PackJob::Copy:
+          err = launch_cast(src, sb, dst, false, j.n, nullptr);
+          break;
+      }
+    }
+    if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("constant packing: ") + hipGetErrorString(err));
+  }
+  hipError_t serr = hipDeviceSynchronize();
+  if (stage) (void)hipFree(stage);
+  if (st.ok() && serr != hipSuccess)
+    st = Status::Err(BYOC_ERR_DEVICE, std::string("constant packing: ") + hipGetErrorString(serr));
+  return st;
+}
+
+}  // namespace
+
+Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int device,
+                     Engine** out) {
+  (void)n_consts;
+  *out = nullptr;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev == 0)
+    return Status::Err(BYOC_ERR_DEVICE, "no HIP device available");
+  if (device < 0 || device >= ndev)
+    return Status::Err(BYOC_ERR_INVALID_ARG, "device " + std::to_string(device) + " out of range");
+  Engine* e = new Engine();
+  e->graph = std::move(g);
+  e->device = device;
+  DeviceGuard guard(device);
+  Planner pl(e, e->graph);
+  Status st = pl.plan();
+  if (st.ok()) st = build_device_state(e, pl, consts);
+  if (!st.ok()) {
+    release(e);
+    delete e;
+    return st;
+  }
+  *out = e;
+  return Status::Ok();
+}
+
+Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
+                  int32_t n_out, hipStream_t stream) {
+  if (n_in != (int32_t)e->graph.inputs.size())
+    return Status::Err(BYOC_ERR_INVALID_ARG, "expected " + std::to_string(e->graph.inputs.size()) +
+                                                 " inputs, got " + std::to_string(n_in));
+  if (n_out != (int32_t)e->graph.outputs.size())
+    return Status::Err(BYOC_ERR_INVALID_ARG, "expected " + std::to_string(e->graph.outputs.size()) +
+                                                 " outputs, got " + std::to_string(n_out));
+  if (n_in > 0 && !inputs) return Status::Err(BYOC_ERR_INVALID_ARG, "inputs is NULL");
+  if (!outputs) return Status::Err(BYOC_ERR_INVALID_ARG, "outputs is NULL");
+  for (int i = 0; i < n_in; ++i)
+    if (!inputs[i]) return Status::Err(BYOC_ERR_INVALID_ARG, "input " + std::to_string(i) + " is NULL");
+  for (int i = 0; i < n_out; ++i)
+    if (!outputs[i]) return Status::Err(BYOC_ERR_INVALID_ARG, "output " + std::to_string(i) + " is NULL");
+  DeviceGuard guard(e->device);
+  RunCtx c{e, inputs, outputs, stream};
+  const bool prof = !e->events.empty() && e->prof_runs < e->prof_max_runs;
+  const size_t nl = e->launches.size();
+  hipEvent_t* ev = prof ? &e->events[(size_t)e->prof_runs * (nl + 1)] : nullptr;
+  if (prof) HIP_TRY(hipEventRecord(ev[0], stream), "hipEventRecord");
+  for (size_t i = 0; i < nl; ++i) {
+    hipError_t err = exec(e->launches[i], c);
+    if (err != hipSuccess)
+      return Status::Err(BYOC_ERR_DEVICE, std::string("launch ") + std::to_string(i) + " (" +
+                                              e->launches[i].info.name + "): " + hipGetErrorString(err));
+    if (prof) HIP_TRY(hipEventRecord(ev[i + 1], stream), "hipEventRecord");
+  }
+  if (prof) {
+    e->prof_runs++;
+    e->prof_last_stream = stream;
+  }
+  return Status::Ok();
+}
+
+Status engine_profile_begin(Engine* e, int max_runs) {
+  if (max_runs < 1 || max_runs > 100000)
+    return Status::Err(BYOC_ERR_INVALID_ARG, "max_runs must be in [1, 100000]");
+  DeviceGuard guard(e->device);
+  for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);
+  e->events.clear();
+  const size_t n = (size_t)max_runs * (e->launches.size() + 1);
+  e->events.resize(n);
+  for (size_t i = 0; i < n; ++i) {
+    hipError_t err = hipEventCreate(&e->events[i]);
+    if (err != hipSuccess) {
+      e->events.resize(i);
+      for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);
+      e->events.clear();
+      return Status::Err(BYOC_ERR_DEVICE, std::string("hipEventCreate: ") + hipGetErrorString(err));
+    }
+  }
+  e->prof_max_runs = max_runs;
+  e->prof_runs = 0;
+  return Status::Ok();
+}
+
+Status engine_profile_end(Engine* e, float* ms, int n, int* runs) {
+  const size_t nl = e->launches.size();
+  if (e->events.empty()) return Status::Err(BYOC_ERR_INVALID_ARG, "profiling was not begun");
+  if (ms && n < (int)nl)
+    return Status::Err(BYOC_ERR_INVALID_ARG, "ms holds " + std::to_string(n) + " entries, need " +
+                                                 std::to_string(nl));
+  DeviceGuard guard(e->device);
+  Status st;
+  if (ms)
+    for (size_t i = 0; i < nl; ++i) ms[i] = 0.f;
+  if (e->prof_runs > 0) {
+    hipEvent_t* last = &e->events[(size_t)(e->prof_runs - 1) * (nl + 1)];
+    hipError_t err = hipEventSynchronize(last[nl]);
+    if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("hipEventSynchronize: ") + hipGetErrorString(err));
+    for (int r = 0; r < e->prof_runs && st.ok() && ms; ++r) {
+      hipEvent_t* ev = &e->events[(size_t)r * (nl + 1)];
+      for (size_t i = 0; i < nl; ++i) {
+        float t = 0.f;
+        err = hipEventElapsedTime(&t, ev[i], ev[i + 1]);
+        if (err != hipSuccess) {
+          st = Status::Err(BYOC_ERR_DEVICE, std::string("hipEventElapsedTime: ") + hipGetErrorString(err));
+          break;
+        }
+        ms[i] += t;
+      }
+    }
+  }
+  if (runs) *runs = e->prof_runs;
+  for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);
+  e->events.clear();
+  e->prof_runs = 0;
+  e->prof_max_runs = 0;
+  return st;
+}
+
+Status engine_destroy(Engine* e) {
+  if (!e) return Status::Ok();
+  Status st;
+  {
+    DeviceGuard guard(e->device);
+    hipError_t err = hipDeviceSynchronize();
+    if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("destroy: ") + hipGetErrorString(err));
+    release(e);
+  }
+  delete e;
+  return st;
+}
+
+}  // namespace byoc

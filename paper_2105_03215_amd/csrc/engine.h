@@ -1,0 +1,73 @@
+// Execution engine of one offloaded subgraph: the plan (launch sequence,
+// arena layout, packed constants) built once at creation and replayed by
+// every run (Sec. 3.4: the accelerator engine is initialised once, cached,
+// and each invocation reads inputs, executes and writes outputs).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <string>
+#include <vector>
+
+#include "graph.h"
+#include "kernels.h"
+
+namespace byoc {
+
+// Where a tensor lives during a run.
+struct Ref {
+  enum Kind : uint8_t { None, Arena, Input, Output, Weights } kind = None;
+  int idx = -1;       // arena buffer id, input or output number
+  int64_t off = 0;    // byte offset (weights region)
+};
+
+struct Launch {
+  enum Op {
+    ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
+    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast
+  } op;
+  byoc_launch_info info{};
+  Ref x, w, bias, res, y, partial, other;
+  ConvParams conv{};
+  ConvTile tile{};
+  ConvF32Params cf{};
+  DwParams dw{};
+  PoolParams pool{};
+  int64_t n = 0;
+  int act = 0;
+  bool src_bf16 = false, dst_bf16 = false;
+  int N = 0, C = 0, H = 0, W = 0, Cp = 0, M = 0, K = 0, Kp = 0;
+};
+
+struct ArenaBuf {
+  int64_t bytes = 0;
+  int first = 0, last = 0;  // launch indices of definition and last use
+  int64_t off = -1;
+};
+
+struct Engine {
+  Graph graph;
+  int device = 0;
+  std::vector<Launch> launches;
+  std::vector<ArenaBuf> bufs;
+  char* arena = nullptr;
+  int64_t arena_bytes = 0;
+  char* weights = nullptr;
+  int64_t weight_bytes = 0;
+  // profiling
+  std::vector<hipEvent_t> events;
+  int prof_max_runs = 0;
+  int prof_runs = 0;
+  hipStream_t prof_last_stream = nullptr;
+};
+
+// Builds the plan and device state.  On failure releases everything.
+Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int device,
+                     Engine** out);
+Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
+                  int32_t n_out, hipStream_t stream);
+Status engine_destroy(Engine* e);
+Status engine_profile_begin(Engine* e, int max_runs);
+Status engine_profile_end(Engine* e, float* ms, int n, int* runs);
+
+}  // namespace byoc

@@ -1,0 +1,113 @@
+// Device kernels of the subgraph executor and their host-side launchers.
+// Every launcher enqueues on the given stream and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace byoc {
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
+enum ActCode { kActNone = 0, kActRelu = 1, kActRelu6 = 2, kActGelu = 3 };
+
+// Implicit-GEMM convolution (and dense, as a 1x1 conv on 1x1 images) on
+// bf16 MFMA.  Activations NHWC with Cp channels (multiple of 8); weights
+// packed [rows >= Kp][Kgp] with the reduction index kk = (r*S + s)*Cp + c.
+struct ConvParams {
+  const bf16_t* x;
+  const bf16_t* w;
+  const float* bias;  // [>= Kp] (zero-padded) or nullptr
+  const bf16_t* res;  // [M][ldr] or nullptr
+  bf16_t* y;          // [M][ldy]
+  float* partial;     // split-K: [splits][M][Kp] fp32 partial sums, else nullptr
+  int N, H, W, Cp;
+  int P, Q, R, S;
+  int sh, sw, pt, pl;
+  int M;    // N*P*Q output pixels
+  int Kp;   // output channels written (multiple of 8)
+  int Kg;   // R*S*Cp reduction length
+  int Kgp;  // packed weight row stride (multiple of 64)
+  int ldy, ldr;
+  int act;
+  int splits;   // split-K factor (1 = none)
+  int k_tiles_per_split;
+};
+
+struct ConvTile {
+  int bm, bn;  // pixels x channels per workgroup
+};
+
+// Tile configurations with a compiled kernel.
+bool conv_mfma_tile_supported(int bm, int bn);
+hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
+// Sums split-K partials in a fixed order and applies bias, residual, act.
+hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s);
+
+// fp32 direct convolution over NCHW with generic groups (1 or depthwise);
+// dense is the 1x1 case on [M, K, 1, 1].
+struct ConvF32Params {
+  const float* x;
+  const float* w;  // OIHW [K][C/groups][R][S]
+  const float* bias;
+  const float* res;  // NCHW like y, or nullptr
+  float* y;
+  int N, C, H, W, K, P, Q, R, S, sh, sw, pt, pl, groups, act;
+};
+hipError_t launch_conv_f32(const ConvF32Params& p, hipStream_t s);
+
+// Depthwise conv NHWC bf16: weights packed [R*S][Cp] bf16, bias fp32 [Cp].
+struct DwParams {
+  const bf16_t* x;
+  const bf16_t* w;
+  const float* bias;
+  const bf16_t* res;
+  bf16_t* y;
+  int N, H, W, Cp, P, Q, R, S, sh, sw, pt, pl, act;
+};
+hipError_t launch_depthwise(const DwParams& p, hipStream_t s);
+
+struct PoolParams {
+  const void* x;
+  void* y;
+  int N, C, H, W, Cp, P, Q, R, S, sh, sw, pt, pl;
+};
+hipError_t launch_maxpool_nhwc_bf16(const PoolParams& p, hipStream_t s);
+hipError_t launch_avgpool_nhwc_bf16(const PoolParams& p, hipStream_t s);  // y [N][Cp]
+hipError_t launch_maxpool_nchw_f32(const PoolParams& p, hipStream_t s);
+hipError_t launch_avgpool_nchw_f32(const PoolParams& p, hipStream_t s);   // y [N][C]
+
+// y = act(a + b) over n elements (n multiple of 8 for bf16).
+hipError_t launch_add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* y, int64_t n, int act,
+                           hipStream_t s);
+hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, int act,
+                          hipStream_t s);
+
+// Boundary transforms.  src_bf16 / dst_bf16 select the external dtype.
+hipError_t launch_nchw_to_nhwc(const void* x, bool src_bf16, bf16_t* y, int N, int C, int H,
+                               int W, int Cp, hipStream_t s);
+hipError_t launch_nhwc_to_nchw(const bf16_t* x, void* y, bool dst_bf16, int N, int C, int H,
+                               int W, int Cp, hipStream_t s);
+// Row-major [M, K] <-> [M, Kp] bf16 with cast.
+hipError_t launch_rows_to_padded(const void* x, bool src_bf16, bf16_t* y, int M, int K, int Kp,
+                                 hipStream_t s);
+hipError_t launch_padded_to_rows(const bf16_t* x, void* y, bool dst_bf16, int M, int K, int Kp,
+                                 hipStream_t s);
+// Elementwise dtype change (fp32 graphs): f32 <-> bf16, or a plain copy.
+hipError_t launch_cast(const void* x, bool src_bf16, void* y, bool dst_bf16, int64_t n,
+                       hipStream_t s);
+
+// Constant packing at engine creation.
+// Conv / dense weights OIHW (f32 or bf16 source) -> [rows][Kgp] bf16 with
+// kk = (r*S + s)*Cp + c; zero outside the source.
+hipError_t launch_pack_conv_weights(const void* src, bool src_bf16, bf16_t* dst, int K, int Cg,
+                                    int R, int S, int Cp, int Kgp, int rows, hipStream_t s);
+// Depthwise weights [C][1][R][S] -> [R*S][Cp] bf16.
+hipError_t launch_pack_dw_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R,
+                                  int S, int Cp, hipStream_t s);
+// Vector [K] (f32 or bf16) -> fp32 [n_out], zero-padded.
+hipError_t launch_pack_vector_f32(const void* src, bool src_bf16, float* dst, int K, int n_out,
+                                  hipStream_t s);
+
+}  // namespace byoc

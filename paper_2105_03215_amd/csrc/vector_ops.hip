@@ -1,0 +1,432 @@
+// Bandwidth-bound kernels: depthwise conv, pooling, elementwise add, the
+// boundary layout/dtype transforms and the constant packers.  No MFMA: each
+// lane moves 16-byte vectors (8 bf16 channels of one NHWC pixel) and
+// consecutive lanes take consecutive channel groups of a pixel, so a wave
+// reads and writes contiguous runs of memory.
+#include "device_common.h"
+
+namespace byoc {
+namespace {
+
+constexpr int kThreads = 256;
+
+inline unsigned grid_for(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
+
+// ---------------------------------------------------------------------------
+// Depthwise conv, NHWC bf16, one thread per (pixel, 8-channel group).
+__global__ __launch_bounds__(kThreads) void depthwise_kernel(DwParams p) {
+  const int G = p.Cp / 8;
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t total = (int64_t)p.N * p.P * p.Q * G;
+  if (idx >= total) return;
+  const int g = (int)(idx % G);
+  int64_t t = idx / G;
+  const int q = (int)(t % p.Q);
+  t /= p.Q;
+  const int pp = (int)(t % p.P);
+  const int n = (int)(t / p.P);
+  float acc[8];
+  const float4 b0 = *(const float4*)(p.bias + g * 8);
+  const float4 b1 = *(const float4*)(p.bias + g * 8 + 4);
+  acc[0] = b0.x; acc[1] = b0.y; acc[2] = b0.z; acc[3] = b0.w;
+  acc[4] = b1.x; acc[5] = b1.y; acc[6] = b1.z; acc[7] = b1.w;
+  const int ih0 = pp * p.sh - p.pt;
+  const int iw0 = q * p.sw - p.pl;
+  const bf16_t* xn = p.x + (size_t)n * p.H * p.W * p.Cp + g * 8;
+  for (int r = 0; r < p.R; ++r) {
+    const int ih = ih0 + r;
+    if ((unsigned)ih >= (unsigned)p.H) continue;
+    for (int s = 0; s < p.S; ++s) {
+      const int iw = iw0 + s;
+      if ((unsigned)iw >= (unsigned)p.W) continue;
+      float xv[8], wv[8];
+      unpack8(*(const uint4*)(xn + ((size_t)ih * p.W + iw) * p.Cp), xv);
+      unpack8(*(const uint4*)(p.w + (size_t)(r * p.S + s) * p.Cp + g * 8), wv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] = fmaf(xv[i], wv[i], acc[i]);
+    }
+  }
+  const size_t o = (((size_t)n * p.P + pp) * p.Q + q) * p.Cp + g * 8;
+  if (p.res) {
+    float rv[8];
+    unpack8(*(const uint4*)(p.res + o), rv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] += rv[i];
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = apply_act(acc[i], p.act);
+  *(uint4*)(p.y + o) = pack8(acc);
+}
+
+// Max pool NHWC bf16; the max of bf16 values is exact, no rounding.
+__global__ __launch_bounds__(kThreads) void maxpool_nhwc_kernel(PoolParams p) {
+  const int G = p.Cp / 8;
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t total = (int64_t)p.N * p.P * p.Q * G;
+  if (idx >= total) return;
+  const int g = (int)(idx % G);
+  int64_t t = idx / G;
+  const int q = (int)(t % p.Q);
+  t /= p.Q;
+  const int pp = (int)(t % p.P);
+  const int n = (int)(t / p.P);
+  const bf16_t* x = (const bf16_t*)p.x + (size_t)n * p.H * p.W * p.Cp + g * 8;
+  float m[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m[i] = -INFINITY;
+  const int ih0 = pp * p.sh - p.pt;
+  const int iw0 = q * p.sw - p.pl;
+  for (int r = 0; r < p.R; ++r) {
+    const int ih = ih0 + r;
+    if ((unsigned)ih >= (unsigned)p.H) continue;
+    for (int s = 0; s < p.S; ++s) {
+      const int iw = iw0 + s;
+      if ((unsigned)iw >= (unsigned)p.W) continue;
+      float v[8];
+      unpack8(*(const uint4*)(x + ((size_t)ih * p.W + iw) * p.Cp), v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) m[i] = fmaxf(m[i], v[i]);
+    }
+  }
+  *(uint4*)((bf16_t*)p.y + (((size_t)n * p.P + pp) * p.Q + q) * p.Cp + g * 8) = pack8(m);
+}
+
+// Global average pool NHWC bf16 -> [N][Cp] bf16; fp32 sum in pixel order.
+__global__ __launch_bounds__(kThreads) void avgpool_nhwc_kernel(PoolParams p) {
+  const int G = p.Cp / 8;
+  const int idx = blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= p.N * G) return;
+  const int g = idx % G;
+  const int n = idx / G;
+  const bf16_t* x = (const bf16_t*)p.x + (size_t)n * p.H * p.W * p.Cp + g * 8;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const int HW = p.H * p.W;
+  for (int i = 0; i < HW; ++i) {
+    float v[8];
+    unpack8(*(const uint4*)(x + (size_t)i * p.Cp), v);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] += v[c];
+  }
+  const float inv = 1.0f / (float)HW;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] *= inv;
+  *(uint4*)((bf16_t*)p.y + (size_t)n * p.Cp + g * 8) = pack8(acc);
+}
+
+// fp32 NCHW pools, one thread per output.
+__global__ __launch_bounds__(kThreads) void maxpool_nchw_f32_kernel(PoolParams p) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t total = (int64_t)p.N * p.C * p.P * p.Q;
+  if (idx >= total) return;
+  const int q = (int)(idx % p.Q);
+  int64_t t = idx / p.Q;
+  const int pp = (int)(t % p.P);
+  t /= p.P;
+  const float* x = (const float*)p.x + (size_t)t * p.H * p.W;
+  float m = -INFINITY;
+  for (int r = 0; r < p.R; ++r) {
+    const int ih = pp * p.sh - p.pt + r;
+    if ((unsigned)ih >= (unsigned)p.H) continue;
+    for (int s = 0; s < p.S; ++s) {
+      const int iw = q * p.sw - p.pl + s;
+      if ((unsigned)iw >= (unsigned)p.W) continue;
+      m = fmaxf(m, x[ih * p.W + iw]);
+    }
+  }
+  ((float*)p.y)[idx] = m;
+}
+
+__global__ __launch_bounds__(kThreads) void avgpool_nchw_f32_kernel(PoolParams p) {
+  const int idx = blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= p.N * p.C) return;
+  const float* x = (const float*)p.x + (size_t)idx * p.H * p.W;
+  float acc = 0.f;
+  for (int i = 0; i < p.H * p.W; ++i) acc += x[i];
+  ((float*)p.y)[idx] = acc / (float)(p.H * p.W);
+}
+
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void add_bf16_kernel(const bf16_t* a, const bf16_t* b,
+                                                            bf16_t* y, int64_t n8, int act) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n8) return;
+  float va[8], vb[8];
+  unpack8(((const uint4*)a)[i], va);
+  unpack8(((const uint4*)b)[i], vb);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) va[c] = apply_act(va[c] + vb[c], act);
+  ((uint4*)y)[i] = pack8(va);
+}
+
+__global__ __launch_bounds__(kThreads) void add_f32_kernel(const float* a, const float* b,
+                                                           float* y, int64_t n, int act) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  y[i] = apply_act(a[i] + b[i], act);
+}
+
+// ---------------------------------------------------------------------------
+// NCHW (f32 or bf16) -> NHWC bf16 with Cp >= C channels (pad zero).  Thread
+// per (n, channel group, h, w) with w fastest: reads are contiguous along w
+// for each channel; each thread writes one 16-byte vector.
+template <typename SrcT>
+__global__ __launch_bounds__(kThreads) void nchw_to_nhwc_kernel(const SrcT* x, bf16_t* y, int N,
+                                                                int C, int H, int W, int Cp) {
+  const int G = Cp / 8;
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t HW = (int64_t)H * W;
+  if (idx >= (int64_t)N * G * HW) return;
+  const int64_t hw = idx % HW;
+  const int64_t t = idx / HW;
+  const int g = (int)(t % G);
+  const int n = (int)(t / G);
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = g * 8 + i;
+    float f = 0.f;
+    if (c < C) {
+      const SrcT e = x[((size_t)n * C + c) * HW + hw];
+      if constexpr (sizeof(SrcT) == 2) f = bf16_to_f32(e);
+      else f = e;
+    }
+    v[i] = f;
+  }
+  *(uint4*)(y + ((size_t)n * HW + hw) * Cp + g * 8) = pack8(v);
+}
+
+template <typename DstT>
+__global__ __launch_bounds__(kThreads) void nhwc_to_nchw_kernel(const bf16_t* x, DstT* y, int N,
+                                                                int C, int H, int W, int Cp) {
+  const int G = Cp / 8;
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t HW = (int64_t)H * W;
+  if (idx >= (int64_t)N * G * HW) return;
+  const int64_t hw = idx % HW;
+  const int64_t t = idx / HW;
+  const int g = (int)(t % G);
+  const int n = (int)(t / G);
+  const uint4 u = *(const uint4*)(x + ((size_t)n * HW + hw) * Cp + g * 8);
+  const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = g * 8 + i;
+    if (c >= C) break;
+    const bf16_t h = (bf16_t)((i & 1) ? (w4[i >> 1] >> 16) : (w4[i >> 1] & 0xFFFF));
+    if constexpr (sizeof(DstT) == 2) y[((size_t)n * C + c) * HW + hw] = h;
+    else y[((size_t)n * C + c) * HW + hw] = bf16_to_f32(h);
+  }
+}
+
+template <typename SrcT>
+__global__ __launch_bounds__(kThreads) void rows_to_padded_kernel(const SrcT* x, bf16_t* y, int M,
+                                                                  int K, int Kp) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)M * Kp) return;
+  const int k = (int)(idx % Kp);
+  const int64_t m = idx / Kp;
+  bf16_t o = 0;
+  if (k < K) {
+    const SrcT e = x[m * K + k];
+    if constexpr (sizeof(SrcT) == 2) o = e;
+    else o = f32_to_bf16(e);
+  }
+  y[idx] = o;
+}
+
+template <typename DstT>
+__global__ __launch_bounds__(kThreads) void padded_to_rows_kernel(const bf16_t* x, DstT* y, int M,
+                                                                  int K, int Kp) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)M * K) return;
+  const int k = (int)(idx % K);
+  const int64_t m = idx / K;
+  const bf16_t h = x[m * Kp + k];
+  if constexpr (sizeof(DstT) == 2) y[idx] = h;
+  else y[idx] = bf16_to_f32(h);
+}
+
+template <typename SrcT, typename DstT>
+__global__ __launch_bounds__(kThreads) void cast_kernel(const SrcT* x, DstT* y, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  float f;
+  if constexpr (sizeof(SrcT) == 2) f = bf16_to_f32(x[i]);
+  else f = x[i];
+  if constexpr (sizeof(DstT) == 2) y[i] = f32_to_bf16(f);
+  else y[i] = f;
+}
+
+// ---------------------------------------------------------------------------
+// Constant packers (engine creation only).
+template <typename SrcT>
+__device__ __forceinline__ float load_f(const SrcT* p, size_t i) {
+  if constexpr (sizeof(SrcT) == 2) return bf16_to_f32(p[i]);
+  else return p[i];
+}
+
+template <typename SrcT>
+__global__ __launch_bounds__(kThreads) void pack_conv_weights_kernel(const SrcT* src, bf16_t* dst,
+                                                                     int K, int Cg, int R, int S,
+                                                                     int Cp, int Kgp, int rows) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)rows * Kgp) return;
+  const int kk = (int)(idx % Kgp);
+  const int k = (int)(idx / Kgp);
+  const int rs = kk / Cp;
+  const int c = kk - rs * Cp;
+  bf16_t o = 0;
+  if (k < K && rs < R * S && c < Cg) {
+    const int r = rs / S;
+    const int s = rs - r * S;
+    o = f32_to_bf16(load_f(src, (((size_t)k * Cg + c) * R + r) * S + s));
+  }
+  dst[idx] = o;
+}
+
+template <typename SrcT>
+__global__ __launch_bounds__(kThreads) void pack_dw_weights_kernel(const SrcT* src, bf16_t* dst,
+                                                                   int C, int R, int S, int Cp) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)R * S * Cp) return;
+  const int c = (int)(idx % Cp);
+  const int rs = (int)(idx / Cp);
+  dst[idx] = c < C ? f32_to_bf16(load_f(src, (size_t)c * R * S + rs)) : (bf16_t)0;
+}
+
+template <typename SrcT>
+__global__ __launch_bounds__(kThreads) void pack_vector_kernel(const SrcT* src, float* dst, int K,
+                                                               int n_out) {
+  const int i = blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n_out) return;
+  dst[i] = i < K ? load_f(src, i) : 0.f;
+}
+
+}  // namespace
+
+hipError_t launch_depthwise(const DwParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.N * p.P * p.Q * (p.Cp / 8);
+  depthwise_kernel<<<grid_for(n), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.N * p.P * p.Q * (p.Cp / 8);
+  maxpool_nhwc_kernel<<<grid_for(n), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
+  avgpool_nhwc_kernel<<<grid_for((int64_t)p.N * (p.Cp / 8)), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_nchw_f32(const PoolParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.N * p.C * p.P * p.Q;
+  maxpool_nchw_f32_kernel<<<grid_for(n), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool_nchw_f32(const PoolParams& p, hipStream_t s) {
+  avgpool_nchw_f32_kernel<<<grid_for((int64_t)p.N * p.C), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* y, int64_t n, int act,
+                           hipStream_t s) {
+  add_bf16_kernel<<<grid_for(n / 8), kThreads, 0, s>>>(a, b, y, n / 8, act);
+  return hipGetLastError();
+}
+
+hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, int act,
+                          hipStream_t s) {
+  add_f32_kernel<<<grid_for(n), kThreads, 0, s>>>(a, b, y, n, act);
+  return hipGetLastError();
+}
+
+hipError_t launch_nchw_to_nhwc(const void* x, bool src_bf16, bf16_t* y, int N, int C, int H,
+                               int W, int Cp, hipStream_t s) {
+  const int64_t n = (int64_t)N * (Cp / 8) * H * W;
+  if (src_bf16)
+    nchw_to_nhwc_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)x, y, N, C, H, W, Cp);
+  else
+    nchw_to_nhwc_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)x, y, N, C, H, W, Cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_nhwc_to_nchw(const bf16_t* x, void* y, bool dst_bf16, int N, int C, int H,
+                               int W, int Cp, hipStream_t s) {
+  const int64_t n = (int64_t)N * (Cp / 8) * H * W;
+  if (dst_bf16)
+    nhwc_to_nchw_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>(x, (bf16_t*)y, N, C, H, W, Cp);
+  else
+    nhwc_to_nchw_kernel<float><<<grid_for(n), kThreads, 0, s>>>(x, (float*)y, N, C, H, W, Cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_to_padded(const void* x, bool src_bf16, bf16_t* y, int M, int K, int Kp,
+                                 hipStream_t s) {
+  const int64_t n = (int64_t)M * Kp;
+  if (src_bf16)
+    rows_to_padded_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)x, y, M, K, Kp);
+  else
+    rows_to_padded_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)x, y, M, K, Kp);
+  return hipGetLastError();
+}
+
+hipError_t launch_padded_to_rows(const bf16_t* x, void* y, bool dst_bf16, int M, int K, int Kp,
+                                 hipStream_t s) {
+  const int64_t n = (int64_t)M * K;
+  if (dst_bf16)
+    padded_to_rows_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>(x, (bf16_t*)y, M, K, Kp);
+  else
+    padded_to_rows_kernel<float><<<grid_for(n), kThreads, 0, s>>>(x, (float*)y, M, K, Kp);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast(const void* x, bool src_bf16, void* y, bool dst_bf16, int64_t n,
+                       hipStream_t s) {
+  const unsigned g = grid_for(n);
+  if (src_bf16 && dst_bf16)
+    cast_kernel<bf16_t, bf16_t><<<g, kThreads, 0, s>>>((const bf16_t*)x, (bf16_t*)y, n);
+  else if (src_bf16)
+    cast_kernel<bf16_t, float><<<g, kThreads, 0, s>>>((const bf16_t*)x, (float*)y, n);
+  else if (dst_bf16)
+    cast_kernel<float, bf16_t><<<g, kThreads, 0, s>>>((const float*)x, (bf16_t*)y, n);
+  else
+    cast_kernel<float, float><<<g, kThreads, 0, s>>>((const float*)x, (float*)y, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_conv_weights(const void* src, bool src_bf16, bf16_t* dst, int K, int Cg,
+                                    int R, int S, int Cp, int Kgp, int rows, hipStream_t s) {
+  const int64_t n = (int64_t)rows * Kgp;
+  if (src_bf16)
+    pack_conv_weights_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)src, dst, K, Cg,
+                                                                      R, S, Cp, Kgp, rows);
+  else
+    pack_conv_weights_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)src, dst, K, Cg,
+                                                                     R, S, Cp, Kgp, rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_dw_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R,
+                                  int S, int Cp, hipStream_t s) {
+  const int64_t n = (int64_t)R * S * Cp;
+  if (src_bf16)
+    pack_dw_weights_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)src, dst, C, R, S, Cp);
+  else
+    pack_dw_weights_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)src, dst, C, R, S, Cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_vector_f32(const void* src, bool src_bf16, float* dst, int K, int n_out,
+                                  hipStream_t s) {
+  if (src_bf16)
+    pack_vector_kernel<bf16_t><<<grid_for(n_out), kThreads, 0, s>>>((const bf16_t*)src, dst, K, n_out);
+  else
+    pack_vector_kernel<float><<<grid_for(n_out), kThreads, 0, s>>>((const float*)src, dst, K, n_out);
+  return hipGetLastError();
+}
+
+}  // namespace byoc

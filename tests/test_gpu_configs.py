@@ -1,0 +1,169 @@
+"""End-to-end parity of the five workloads on the GPU against the oracle.
+
+Small workloads are compared on every output element; the batched ones at
+their full size in the benchmark's launch configuration, on images (or
+token rows) that the oracle recomputes one by one - every image of a CNN
+batch and every token row of the FFN stack is independent of the others.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2105_03215_amd import workloads
+from parity_util import (BF16_TOL, F32_TOL, announce, rel_err, term_scale_node,
+                         within_one_ulp)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _gpu(wl):
+    from paper_2105_03215_amd import capi, runtime
+    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
+    try:
+        return runtime.run_once(sg, wl.inputs, DEV)
+    finally:
+        sg.close()
+
+
+def _sample_inputs(wl, rows):
+    return [np.ascontiguousarray(a[rows]) for a in wl.inputs]
+
+
+def _sample_graph(wl, n):
+    g = dict(wl.graph)
+    g["inputs"] = [dict(d, shape=[n] + d["shape"][1:]) for d in wl.graph["inputs"]]
+    return g
+
+
+def test_conv_f32_config():
+    announce("conv_f32 config")
+    wl = workloads.conv_f32()
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="exact")[0]
+    assert rel_err(g, o) <= F32_TOL
+
+
+def test_resnet18_block():
+    announce("resnet18_block 1x64x56x56")
+    wl = workloads.resnet18_block()
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    assert g.shape == (1, 64, 56, 56)
+    assert rel_err(g, o) <= BF16_TOL
+
+
+def test_resnet18_block_teacher_forced():
+    """Every composite recomputed by the oracle from the GPU's own inputs."""
+    announce("resnet18_block teacher forced")
+    wl = workloads.resnet18_block()
+    graph = dict(wl.graph)
+    graph["outputs"] = [{"name": n["name"], "dtype": "bf16", "layout": "NCHW"} for n in graph["nodes"]]
+    wl2 = workloads.Workload(graph, wl.consts, wl.inputs, wl.macs, wl.conv_macs)
+    gpu = _gpu(wl2)
+    vals = {"x": oracle.bf16.round_bf16(wl.inputs[0])}
+    for c in graph["constants"]:
+        vals[c["name"]] = wl.consts[c["index"]]
+    for node, g in zip(graph["nodes"], gpu):
+        args = [vals[r] for r in node["inputs"]]
+        ref = oracle.run_node(node, args)
+        assert within_one_ulp(g, ref, term_scale_node(node, args)).all(), node["name"]
+        vals[node["name"]] = g
+
+
+@pytest.mark.parametrize("variant", ["resnet50_v1", "resnet50_v1b"])
+def test_resnet50_bs1(variant):
+    announce(variant + " bs1")
+    wl = workloads.build(variant, n=1)
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    assert g.shape == (1, 1000)
+    err = rel_err(g, o)
+    print("%s bs1 err %.3e" % (variant, err))
+    assert err <= BF16_TOL
+
+
+def test_resnet50_bs32_sampled():
+    announce("resnet50_v1 bs32 sampled images 0 and 31")
+    wl = workloads.build("resnet50_v1", n=32)
+    g = _gpu(wl)[0]
+    rows = [0, 31]
+    o = oracle.run_graph(_sample_graph(wl, 2), wl.consts, _sample_inputs(wl, rows), mode="bf16io")[0]
+    err = rel_err(g[rows], o)
+    print("resnet50 bs32 err %.3e" % err)
+    assert err <= BF16_TOL
+    assert np.all(np.isfinite(g))
+
+
+def test_resnet50_f32_input_boundary():
+    announce("resnet50_v1 bs2 f32 input (boundary cast)")
+    wl = workloads.resnet50(n=2, input_dtype="f32")
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    assert rel_err(g, o) <= BF16_TOL
+
+
+def test_mobilenet_v2_bs1():
+    announce("mobilenet_v2 bs1")
+    wl = workloads.build("mobilenet_v2", n=1)
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    err = rel_err(g, o)
+    print("mobilenet_v2 bs1 err %.3e" % err)
+    assert err <= BF16_TOL
+
+
+def test_mobilenet_v2_bs16_sampled():
+    announce("mobilenet_v2 bs16 sampled images 0 and 15")
+    wl = workloads.build("mobilenet_v2", n=16)
+    g = _gpu(wl)[0]
+    rows = [0, 15]
+    o = oracle.run_graph(_sample_graph(wl, 2), wl.consts, _sample_inputs(wl, rows), mode="bf16io")[0]
+    err = rel_err(g[rows], o)
+    print("mobilenet_v2 bs16 err %.3e" % err)
+    assert err <= BF16_TOL
+
+
+def test_bert_ffn_layers_teacher_forced():
+    """All 24 dense composites at full size (1024 tokens), each recomputed by
+    the oracle on 64 sampled token rows from the GPU's own layer input."""
+    announce("bert_ffn teacher forced, 24 composites")
+    wl = workloads.build("bert_ffn")
+    graph = dict(wl.graph)
+    graph["outputs"] = [{"name": n["name"], "dtype": "bf16"} for n in graph["nodes"]]
+    wl2 = workloads.Workload(graph, wl.consts, wl.inputs, wl.macs, wl.conv_macs)
+    gpu = _gpu(wl2)
+    rows = np.random.default_rng(0).choice(1024, 64, replace=False)
+    vals = {"x": wl.inputs[0][rows]}
+    consts = {c["name"]: wl.consts[c["index"]] for c in graph["constants"]}
+    worst = 0.0
+    for node, g in zip(graph["nodes"], gpu):
+        args = [vals[r] if r in vals else consts[r] for r in node["inputs"]]
+        ref = oracle.run_node(node, args)
+        assert within_one_ulp(g[rows], ref, term_scale_node(node, args)).all(), node["name"]
+        worst = max(worst, rel_err(g[rows], ref))
+        vals[node["name"]] = g[rows]
+    print("bert per-layer worst err %.3e" % worst)
+    assert worst <= BF16_TOL
+
+
+def test_bert_ffn_end_to_end_sampled():
+    """Full stack on 64 sampled rows.  Twelve residual layers of bf16 storage
+    let any two correct implementations drift apart by more than one
+    rounding; the bound is twice the oracle's own bf16io-vs-exact spread on
+    the same rows (the drift of a correct implementation), and never below
+    the 1e-2 of the comparison."""
+    announce("bert_ffn end to end sampled rows")
+    wl = workloads.build("bert_ffn")
+    g = _gpu(wl)[0]
+    rows = np.random.default_rng(1).choice(1024, 64, replace=False)
+    graph = dict(wl.graph)
+    graph["inputs"] = [dict(graph["inputs"][0], shape=[64, 768])]
+    io = oracle.run_graph(graph, wl.consts, [wl.inputs[0][rows]], mode="bf16io")[0]
+    ex = oracle.run_graph(graph, wl.consts, [wl.inputs[0][rows]], mode="exact")[0]
+    spread = rel_err(io, ex)
+    err = rel_err(g[rows], io)
+    print("bert e2e err %.3e, oracle bf16io-vs-exact spread %.3e" % (err, spread))
+    assert err <= max(BF16_TOL, 2 * spread)
