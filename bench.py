@@ -112,6 +112,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    ap.add_argument("--dump-launches", default=None,
+                    help="write a per-launch table (time, flops, bytes, roofline) to this JSON file")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this executor has no multi-GPU path "
@@ -148,6 +150,14 @@ def main():
             traffic = tj.get("conv_bytes_per_step")
     roof = _roofline(launches, per_launch, traffic)
     roof["profiled_ms_per_step"] = round(sum(per_launch), 4)
+    if args.dump_launches:
+        table = []
+        for l, t in zip(launches, per_launch):
+            floor_ms = max(l["flops"] / (PEAK_BF16_TFLOPS * 1e12), l["bytes"] / (PEAK_HBM_GBS * 1e9)) * 1e3
+            table.append(dict(l, ms=round(t, 5), roofline_ms=round(floor_ms, 5),
+                              frac=round(floor_ms / t, 4) if t > 0 else None))
+        with open(args.dump_launches, "w") as f:
+            json.dump(table, f, indent=1)
     stats = sg.stats()
 
     bs1 = None

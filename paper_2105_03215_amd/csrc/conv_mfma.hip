@@ -11,8 +11,8 @@
 //
 // Workgroup: 256 threads = 4 waves; tile BM pixels x BN channels; the
 // reduction advances 64 elements per LDS stage (two MFMA k-steps).  Global
-// loads for stage t+1 are issued before the MFMAs of stage t and written to
-// the other LDS buffer afterwards (one barrier per stage).  LDS rows are 128
+// loads run two stages ahead through two register sets; LDS is double
+// buffered with one barrier per stage.  LDS rows are 128
 // bytes (8 chunks of 16 B) with the chunk index XOR-swizzled by the row so
 // that the 16 rows one MFMA operand read touches fall on distinct banks.
 //
@@ -38,25 +38,124 @@ constexpr int kRowsPerPass = kNT / kCH;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
+// Per-thread state of one workgroup's main loop.  The two prefetch register
+// sets are members indexed by a template parameter so that they stay in
+// VGPRs (never addressable memory).
+template <int BM, int BN, int WM, int WN, bool ALIGNED>
+struct ConvTileLoop {
+  static constexpr int WTM = BM / WM;
+  static constexpr int WTN = BN / WN;
+  static constexpr int TM = WTM / 16;
+  static constexpr int TN = WTN / 16;
+  static constexpr int AR = BM / kRowsPerPass;
+  static constexpr int BR = BN / kRowsPerPass;
+
+  uint4 ra[2][AR];
+  uint4 rb[2][BR];
+  f32x4 acc[TN][TM];
+  int a_base[AR], a_ih[AR], a_iw[AR];
+  const bf16_t* wrow;
+  // reduction position of this thread's next load: tap (r, s), channel c,
+  // flattened index kk (non-aligned path) and packed-weight column
+  int r, s, c, kk, wcol;
+  int cv, r0, lane, wm, wn;
+
+  __device__ __forceinline__ void advance(const ConvParams& p) {
+    wcol += kBK;
+    if (ALIGNED) {
+      c += kBK;
+      if (c >= p.Cp) {
+        c -= p.Cp;
+        if (++s == p.S) {
+          s = 0;
+          ++r;
+        }
+      }
+    } else {
+      kk += kBK;
+      c += kBK;
+      while (c >= p.Cp) {
+        c -= p.Cp;
+        if (++s == p.S) {
+          s = 0;
+          ++r;
+        }
+      }
+    }
+  }
+
+  template <int SET>
+  __device__ __forceinline__ void load(const ConvParams& p) {
+    const bool kval = ALIGNED || kk < p.Kg;
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+      const int ih = a_ih[i] + r;
+      const int iw = a_iw[i] + s;
+      const bool ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+      ra[SET][i] = ok ? *(const uint4*)(p.x + a_base[i] + (ih * p.W + iw) * p.Cp + c)
+                      : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+      rb[SET][i] = *(const uint4*)(wrow + (size_t)i * kRowsPerPass * p.Kgp + wcol);
+    advance(p);
+  }
+
+  template <int SET>
+  __device__ __forceinline__ void store(uint4* sA, uint4* sB) {
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+      const int row = r0 + i * kRowsPerPass;
+      sA[row * kCH + (cv ^ (row & 7))] = ra[SET][i];
+    }
+#pragma unroll
+    for (int i = 0; i < BR; ++i) {
+      const int row = r0 + i * kRowsPerPass;
+      sB[row * kCH + (cv ^ (row & 7))] = rb[SET][i];
+    }
+  }
+
+  __device__ __forceinline__ void compute(const uint4* sA, const uint4* sB) {
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      const int chunk = ks * 4 + (lane >> 4);
+      bf16x8 af[TN], bfr[TM];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int row = wn * WTN + i * 16 + (lane & 15);
+        af[i] = as_bf16x8(sB[row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * WTM + j * 16 + (lane & 15);
+        bfr[j] = as_bf16x8(sA[row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  }
+};
+
 template <int BM, int BN, int WM, int WN, bool ALIGNED, bool SPLIT>
-__global__ __launch_bounds__(kNT) void conv_mfma_kernel(ConvParams p) {
-  constexpr int WTM = BM / WM;
-  constexpr int WTN = BN / WN;
-  constexpr int TM = WTM / 16;
-  constexpr int TN = WTN / 16;
-  constexpr int AR = BM / kRowsPerPass;
-  constexpr int BR = BN / kRowsPerPass;
+__global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
+  using L = ConvTileLoop<BM, BN, WM, WN, ALIGNED>;
   static_assert(WM * WN == 4, "4 waves");
-  static_assert(TM >= 1 && TN >= 1 && AR >= 1 && BR >= 1, "tile too small");
+  static_assert(L::TM >= 1 && L::TN >= 1 && L::AR >= 1 && L::BR >= 1, "tile too small");
+  constexpr int WTM = L::WTM, WTN = L::WTN, TM = L::TM, TN = L::TN, AR = L::AR;
 
   __shared__ uint4 sA[2][BM * kCH];
   __shared__ uint4 sB[2][BN * kCH];
 
+  L st;
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
+  st.lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave / WN;
-  const int wn = wave % WN;
+  st.wm = wave / WN;
+  st.wn = wave % WN;
+  const int lane = st.lane, wm = st.wm, wn = st.wn;
 
   // Tile order: workgroups are dealt round-robin to the 8 XCDs; remap so
   // that each XCD gets a contiguous run of tiles (shared activation rows
@@ -77,114 +176,62 @@ __global__ __launch_bounds__(kNT) void conv_mfma_kernel(ConvParams p) {
     kt_end = min(nk_total, kt_begin + p.k_tiles_per_split);
   }
 
-  const int cv = tid & (kCH - 1);
-  const int r0 = tid / kCH;
+  st.cv = tid & (kCH - 1);
+  st.r0 = tid / kCH;
   const int PQ = p.P * p.Q;
-
-  int a_base[AR], a_ih[AR], a_iw[AR];
 #pragma unroll
   for (int i = 0; i < AR; ++i) {
-    const int m = m0 + r0 + i * kRowsPerPass;
+    const int m = m0 + st.r0 + i * kRowsPerPass;
     if (m < p.M) {
       const int n = m / PQ;
       const int pq = m - n * PQ;
       const int pp = pq / p.Q;
       const int qq = pq - pp * p.Q;
-      a_base[i] = n * p.H * p.W * p.Cp;
-      a_ih[i] = pp * p.sh - p.pt;
-      a_iw[i] = qq * p.sw - p.pl;
+      st.a_base[i] = n * p.H * p.W * p.Cp;
+      st.a_ih[i] = pp * p.sh - p.pt;
+      st.a_iw[i] = qq * p.sw - p.pl;
     } else {
-      a_base[i] = 0;
-      a_ih[i] = -(1 << 28);  // never inside [0, H)
-      a_iw[i] = 0;
+      st.a_base[i] = 0;
+      st.a_ih[i] = -(1 << 28);  // never inside [0, H)
+      st.a_iw[i] = 0;
     }
   }
-  const bf16_t* wrow = p.w + (size_t)(n0 + r0) * p.Kgp + cv * 8;
-
-  uint4 ra[AR], rb[BR];
-  auto load = [&](int kt) {
-    const int kk0 = kt * kBK;
-    int r, s, c;
-    bool kval = true;
-    if (ALIGNED) {
-      const int rs = kk0 / p.Cp;
-      c = kk0 - rs * p.Cp + cv * 8;
-      r = rs / p.S;
-      s = rs - r * p.S;
-    } else {
-      const int kk = kk0 + cv * 8;
-      const int rs = kk / p.Cp;
-      c = kk - rs * p.Cp;
-      r = rs / p.S;
-      s = rs - r * p.S;
-      kval = kk < p.Kg;
-    }
-#pragma unroll
-    for (int i = 0; i < AR; ++i) {
-      const int ih = a_ih[i] + r;
-      const int iw = a_iw[i] + s;
-      const bool ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
-      ra[i] = ok ? *(const uint4*)(p.x + a_base[i] + (ih * p.W + iw) * p.Cp + c)
-                 : make_uint4(0u, 0u, 0u, 0u);
-    }
-#pragma unroll
-    for (int i = 0; i < BR; ++i)
-      rb[i] = *(const uint4*)(wrow + (size_t)i * kRowsPerPass * p.Kgp + kk0);
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < AR; ++i) {
-      const int row = r0 + i * kRowsPerPass;
-      sA[buf][row * kCH + (cv ^ (row & 7))] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BR; ++i) {
-      const int row = r0 + i * kRowsPerPass;
-      sB[buf][row * kCH + (cv ^ (row & 7))] = rb[i];
-    }
-  };
-
-  f32x4 acc[TN][TM];
+  st.wrow = p.w + (size_t)(n0 + st.r0) * p.Kgp + st.cv * 8;
+  // starting reduction position of this thread's vector
+  {
+    const int kk0 = kt_begin * kBK + (ALIGNED ? 0 : st.cv * 8);
+    const int rs = kk0 / p.Cp;
+    st.c = kk0 - rs * p.Cp + (ALIGNED ? st.cv * 8 : 0);
+    st.r = rs / p.S;
+    st.s = rs - st.r * p.S;
+    st.kk = kk0;
+    st.wcol = kt_begin * kBK;
+  }
 #pragma unroll
   for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TM; ++j) st.acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](int buf) {
-#pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      const int chunk = ks * 4 + (lane >> 4);
-      bf16x8 af[TN], bfr[TM];
-#pragma unroll
-      for (int i = 0; i < TN; ++i) {
-        const int row = wn * WTN + i * 16 + (lane & 15);
-        af[i] = as_bf16x8(sB[buf][row * kCH + (chunk ^ (row & 7))]);
-      }
-#pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        const int row = wm * WTM + j * 16 + (lane & 15);
-        bfr[j] = as_bf16x8(sA[buf][row * kCH + (chunk ^ (row & 7))]);
-      }
-#pragma unroll
-      for (int i = 0; i < TN; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-  };
-
-  if (kt_begin < kt_end) {
-    load(kt_begin);
-    store(0);
+  // Two register sets: the loads of tile t+2 are issued before the MFMAs
+  // of tile t and written to LDS after those of tile t+1.
+  const int nkt = kt_end - kt_begin;
+  if (nkt > 0) {
+    st.template load<0>(p);
+    if (nkt > 1) st.template load<1>(p);
+    st.template store<0>(sA[0], sB[0]);
     __syncthreads();
-    int buf = 0;
-    for (int kt = kt_begin; kt < kt_end; ++kt) {
-      const bool more = kt + 1 < kt_end;
-      if (more) load(kt + 1);
-      compute(buf);
-      if (more) store(buf ^ 1);
+    for (int t = 0; t < nkt; t += 2) {
+      // LDS 0 holds tile t, register set 1 holds tile t+1
+      if (t + 2 < nkt) st.template load<0>(p);
+      st.compute(sA[0], sB[0]);
+      if (t + 1 < nkt) st.template store<1>(sA[1], sB[1]);
       __syncthreads();
-      buf ^= 1;
+      if (t + 1 >= nkt) break;
+      // LDS 1 holds tile t+1, register set 0 holds tile t+2
+      if (t + 3 < nkt) st.template load<1>(p);
+      st.compute(sA[1], sB[1]);
+      if (t + 2 < nkt) st.template store<0>(sA[0], sB[0]);
+      __syncthreads();
     }
   }
 
@@ -198,8 +245,8 @@ __global__ __launch_bounds__(kNT) void conv_mfma_kernel(ConvParams p) {
       for (int j = 0; j < TM; ++j) {
         const int m = m0 + wm * WTM + j * 16 + (lane & 15);
         if (m >= p.M) continue;
-        float4 v = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-        *(float4*)(p.partial + ((size_t)blockIdx.y * p.M + m) * p.Kp + k) = v;
+        const f32x4 a = st.acc[i][j];
+        *(float4*)(p.partial + ((size_t)blockIdx.y * p.M + m) * p.Kp + k) = make_float4(a[0], a[1], a[2], a[3]);
       }
     } else {
       const float4 bv = p.bias ? *(const float4*)(p.bias + k) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -207,10 +254,11 @@ __global__ __launch_bounds__(kNT) void conv_mfma_kernel(ConvParams p) {
       for (int j = 0; j < TM; ++j) {
         const int m = m0 + wm * WTM + j * 16 + (lane & 15);
         if (m >= p.M) continue;
-        float v0 = acc[i][j][0] + bv.x;
-        float v1 = acc[i][j][1] + bv.y;
-        float v2 = acc[i][j][2] + bv.z;
-        float v3 = acc[i][j][3] + bv.w;
+        const f32x4 a = st.acc[i][j];
+        float v0 = a[0] + bv.x;
+        float v1 = a[1] + bv.y;
+        float v2 = a[2] + bv.z;
+        float v3 = a[3] + bv.w;
         if (p.res) {
           const uint2 rr = *(const uint2*)(p.res + (size_t)m * p.ldr + k);
           v0 += __uint_as_float(rr.x << 16);

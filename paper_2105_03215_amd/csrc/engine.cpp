@@ -35,32 +35,38 @@ struct PackJob {
   int n = 0, n_out = 0;
 };
 
-// Chooses the workgroup tile and split-K factor of an implicit GEMM.
+// Chooses the workgroup tile and split-K factor of an implicit GEMM.  The
+// kernel is latency bound per stage, so the model favours the largest tile
+// that still yields about two workgroups per CU, splitting the reduction
+// (deterministically, reduced by a second kernel) when the output has too
+// few tiles and the reduction is long enough to share.
 void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* kps) {
-  static const int cands[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}, {32, 64}};
+  struct Cand { int bm, bn, occ; double t_stage; };
+  static const Cand cands[] = {
+      {128, 128, 2, 1.00}, {128, 64, 3, 0.80}, {64, 128, 3, 0.80}, {64, 64, 5, 0.62}, {32, 64, 6, 0.55}};
   const int nk = (int)((Kg + kKPad - 1) / kKPad);
-  int best = -1;
-  for (int i = 0; i < 5; ++i) {
-    const int bm = cands[i][0], bn = cands[i][1];
-    const int64_t tm = (M + bm - 1) / bm, tn = (Kp + bn - 1) / bn;
-    const double eff = (double)M * Kp / (double)(tm * bm * tn * bn);
-    if (tm * tn >= 240 && eff >= 0.75) {
-      best = i;
-      break;
-    }
-  }
-  if (best < 0) best = M >= 64 ? 3 : 4;
-  t->bm = cands[best][0];
-  t->bn = cands[best][1];
-  const int64_t tiles = ((M + t->bm - 1) / t->bm) * ((Kp + t->bn - 1) / t->bn);
-  *splits = 1;
-  *kps = nk;
-  if (tiles < 128 && nk >= 8) {
-    int s = (int)std::min<int64_t>(nk / 4, (256 + tiles - 1) / tiles);
-    s = std::max(1, std::min(s, 16));
-    if (s > 1) {
-      *kps = (nk + s - 1) / s;
-      *splits = (nk + *kps - 1) / *kps;
+  const int kCUs = 256;
+  double best = 1e30;
+  for (const Cand& c : cands) {
+    const int64_t tiles = ((M + c.bm - 1) / c.bm) * ((Kp + c.bn - 1) / c.bn);
+    for (int s = 1; s <= 16; s *= 2) {
+      if (s > 1 && (nk / s < 4)) break;
+      const int k_per = (nk + s - 1) / s;
+      const int sp = (nk + k_per - 1) / k_per;
+      const int64_t blocks = tiles * sp;
+      const int64_t slots = (int64_t)c.occ * kCUs;
+      const double rounds = (double)((blocks + slots - 1) / slots);
+      // a round of `occ` co-resident workgroups takes about one stage time per k-tile
+      double est = rounds * k_per * c.t_stage;
+      // split-K moves fp32 partials: write + read, relative to stage time units
+      if (sp > 1) est += (double)sp * M * Kp * 8.0 / 4.0e12 / 0.8e-6;
+      if (est < best * 0.98) {
+        best = est;
+        t->bm = c.bm;
+        t->bn = c.bn;
+        *splits = sp;
+        *kps = k_per;
+      }
     }
   }
 }
