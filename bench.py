@@ -81,6 +81,28 @@ def _class_summary(launches, per_launch_ms):
     return out
 
 
+def _conv_kernel_digest():
+    """Digest of the conv kernel source: stored traffic counts apply only to
+    the kernel they were measured on."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2105_03215_amd", "csrc", "conv_mfma.hip")
+    with open(src, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _copy_calibration(mib):
+    """A plain device-to-device copy of known size (for scaling the HBM
+    byte counters): three copies of `mib` MiB."""
+    import torch
+    n = mib * 2 ** 20 // 4
+    a = torch.empty(n, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+
+
 def _cpu_baseline(wl, images):
     """The oracle (bf16io mode, float64 NumPy) on the first `images` images
     of the workload, on this host's cores."""
@@ -108,10 +130,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=32)
     ap.add_argument("--variant", default="resnet50_v1")
-    ap.add_argument("--cpu-images", type=int, default=4)
+    ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a device copy of MIB MiB three times (counter calibration)")
     ap.add_argument("--dump-launches", default=None,
                     help="write a per-launch table (time, flops, bytes, roofline) to this JSON file")
     args = ap.parse_args()
@@ -124,6 +148,11 @@ def main():
     import torch
 
     from paper_2105_03215_amd import capi, runtime, workloads
+
+    if args.copy_calibration:
+        _copy_calibration(args.copy_calibration)
+        print(json.dumps({"copy_calibration_mib": args.copy_calibration, "copies": 3}))
+        return
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -146,7 +175,8 @@ def main():
     if os.path.exists(args.traffic_json):
         with open(args.traffic_json) as f:
             tj = json.load(f)
-        if tj.get("workload") == "%s_bs%d" % (args.variant, args.batch):
+        if (tj.get("workload") == "%s_bs%d" % (args.variant, args.batch)
+                and tj.get("conv_kernel_digest") == _conv_kernel_digest()):
             traffic = tj.get("conv_bytes_per_step")
     roof = _roofline(launches, per_launch, traffic)
     roof["profiled_ms_per_step"] = round(sum(per_launch), 4)

@@ -35,6 +35,8 @@ constexpr int kBK = 64;          // reduction elements per stage
 constexpr int kCH = kBK / 8;     // 16-byte chunks per tile row
 constexpr int kNT = 256;         // threads per workgroup
 constexpr int kRowsPerPass = kNT / kCH;
+// Buffer resource word 3 for raw (untyped, stride 0) buffer access on gfx9.
+constexpr int kBufferFlags = 0x00020000;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
@@ -53,19 +55,25 @@ struct ConvTileLoop {
   uint4 ra[2][AR];
   uint4 rb[2][BR];
   f32x4 acc[TN][TM];
-  int a_base[AR], a_ih[AR], a_iw[AR];
-  const bf16_t* wrow;
-  // reduction position of this thread's next load: tap (r, s), channel c,
-  // flattened index kk (non-aligned path) and packed-weight column
+  // Activation rows.  Aligned path: pix = element offset of the row's
+  // window origin plus this thread's 8 channels, tapmask bit r*S+s set when
+  // that tap lies inside the image.  Non-aligned path: the window origin.
+  int pix[AR], a_ih[AR], a_iw[AR];
+  uint32_t tapmask[AR];
+  __amdgpu_buffer_rsrc_t xr, wr;
+  uint32_t wvoff[BR];  // byte offset of this thread's weight rows and chunk
+  // reduction position of the next load: tap (r, s), channel c, flattened
+  // index kk (non-aligned path) and packed-weight column
   int r, s, c, kk, wcol;
   int cv, r0, lane, wm, wn;
 
   __device__ __forceinline__ void advance(const ConvParams& p) {
     wcol += kBK;
     if (ALIGNED) {
+      // c is the wave-uniform channel base of the stage (Cp % 64 == 0)
       c += kBK;
-      if (c >= p.Cp) {
-        c -= p.Cp;
+      if (c == p.Cp) {
+        c = 0;
         if (++s == p.S) {
           s = 0;
           ++r;
@@ -84,21 +92,39 @@ struct ConvTileLoop {
     }
   }
 
+  // Raw buffer loads: an out-of-range offset returns zeros, which supplies
+  // the conv padding and the ragged pixel/reduction tails without branches.
+  // The position advances before every load but the first; a load asked
+  // for past the last stage (more == false) re-reads the last stage, whose
+  // data is then never used.
   template <int SET>
-  __device__ __forceinline__ void load(const ConvParams& p) {
-    const bool kval = ALIGNED || kk < p.Kg;
+  __device__ __forceinline__ void load(const ConvParams& p, bool first, bool more) {
+    if (!first && more) advance(p);
+    if (ALIGNED) {
+      const int tap = (r * p.W + s) * p.Cp + c;
+      const int bit = r * p.S + s;
 #pragma unroll
-    for (int i = 0; i < AR; ++i) {
-      const int ih = a_ih[i] + r;
-      const int iw = a_iw[i] + s;
-      const bool ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
-      ra[SET][i] = ok ? *(const uint4*)(p.x + a_base[i] + (ih * p.W + iw) * p.Cp + c)
-                      : make_uint4(0u, 0u, 0u, 0u);
+      for (int i = 0; i < AR; ++i) {
+        const bool ok = (tapmask[i] >> bit) & 1u;
+        const uint32_t off = ok ? (uint32_t)(pix[i] + tap) * 2u : 0x80000000u;
+        ra[SET][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+      }
+    } else {
+      const bool kval = kk < p.Kg;
+      const int tap = (r * p.W + s) * p.Cp + c;
+#pragma unroll
+      for (int i = 0; i < AR; ++i) {
+        const int ih = a_ih[i] + r;
+        const int iw = a_iw[i] + s;
+        const bool ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+        const uint32_t off = ok ? (uint32_t)(pix[i] + tap) * 2u : 0x80000000u;
+        ra[SET][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+      }
     }
+    const uint32_t wc = (uint32_t)wcol * 2u;
 #pragma unroll
     for (int i = 0; i < BR; ++i)
-      rb[SET][i] = *(const uint4*)(wrow + (size_t)i * kRowsPerPass * p.Kgp + wcol);
-    advance(p);
+      rb[SET][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, wvoff[i] + wc, 0, 0));
   }
 
   template <int SET>
@@ -182,26 +208,39 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
 #pragma unroll
   for (int i = 0; i < AR; ++i) {
     const int m = m0 + st.r0 + i * kRowsPerPass;
+    int ih0 = -(1 << 28), iw0 = 0, n = 0;  // rows past M: never inside the image
     if (m < p.M) {
-      const int n = m / PQ;
+      n = m / PQ;
       const int pq = m - n * PQ;
       const int pp = pq / p.Q;
       const int qq = pq - pp * p.Q;
-      st.a_base[i] = n * p.H * p.W * p.Cp;
-      st.a_ih[i] = pp * p.sh - p.pt;
-      st.a_iw[i] = qq * p.sw - p.pl;
-    } else {
-      st.a_base[i] = 0;
-      st.a_ih[i] = -(1 << 28);  // never inside [0, H)
-      st.a_iw[i] = 0;
+      ih0 = pp * p.sh - p.pt;
+      iw0 = qq * p.sw - p.pl;
+    }
+    st.a_ih[i] = ih0;
+    st.a_iw[i] = iw0;
+    st.pix[i] = m < p.M ? ((n * p.H + ih0) * p.W + iw0) * p.Cp : 0;
+    if (ALIGNED) {
+      st.pix[i] += st.cv * 8;
+      uint32_t mask = 0;
+      for (int r = 0; r < p.R; ++r)
+        for (int s = 0; s < p.S; ++s)
+          if ((unsigned)(ih0 + r) < (unsigned)p.H && (unsigned)(iw0 + s) < (unsigned)p.W)
+            mask |= 1u << (r * p.S + s);
+      st.tapmask[i] = mask;
     }
   }
-  st.wrow = p.w + (size_t)(n0 + st.r0) * p.Kgp + st.cv * 8;
-  // starting reduction position of this thread's vector
+  st.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p.x), (short)0, p.x_bytes, kBufferFlags);
+  st.wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p.w), (short)0, p.w_bytes, kBufferFlags);
+#pragma unroll
+  for (int i = 0; i < L::BR; ++i)
+    st.wvoff[i] = (uint32_t)(((n0 + st.r0 + i * kRowsPerPass) * p.Kgp + st.cv * 8) * 2);
+  // starting reduction position (aligned: wave-uniform stage origin; the
+  // thread's 8 channels are added at use)
   {
     const int kk0 = kt_begin * kBK + (ALIGNED ? 0 : st.cv * 8);
     const int rs = kk0 / p.Cp;
-    st.c = kk0 - rs * p.Cp + (ALIGNED ? st.cv * 8 : 0);
+    st.c = kk0 - rs * p.Cp;
     st.r = rs / p.S;
     st.s = rs - st.r * p.S;
     st.kk = kk0;
@@ -216,21 +255,21 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   // of tile t and written to LDS after those of tile t+1.
   const int nkt = kt_end - kt_begin;
   if (nkt > 0) {
-    st.template load<0>(p);
-    if (nkt > 1) st.template load<1>(p);
+    st.template load<0>(p, true, true);
+    st.template load<1>(p, false, nkt > 1);
     st.template store<0>(sA[0], sB[0]);
     __syncthreads();
     for (int t = 0; t < nkt; t += 2) {
       // LDS 0 holds tile t, register set 1 holds tile t+1
-      if (t + 2 < nkt) st.template load<0>(p);
+      st.template load<0>(p, false, t + 2 < nkt);
       st.compute(sA[0], sB[0]);
-      if (t + 1 < nkt) st.template store<1>(sA[1], sB[1]);
+      st.template store<1>(sA[1], sB[1]);
       __syncthreads();
-      if (t + 1 >= nkt) break;
-      // LDS 1 holds tile t+1, register set 0 holds tile t+2
-      if (t + 3 < nkt) st.template load<1>(p);
-      st.compute(sA[1], sB[1]);
-      if (t + 2 < nkt) st.template store<0>(sA[0], sB[0]);
+      // LDS 1 holds tile t+1 (a repeat of the last tile past the end),
+      // register set 0 holds tile t+2
+      st.template load<1>(p, false, t + 3 < nkt);
+      if (t + 1 < nkt) st.compute(sA[1], sB[1]);
+      st.template store<0>(sA[0], sB[0]);
       __syncthreads();
     }
   }
@@ -315,7 +354,7 @@ template <int BM, int BN, int WM, int WN>
 hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
   const int ntm = (p.M + BM - 1) / BM;
   const int ntn = (p.Kp + BN - 1) / BN;
-  const bool aligned = (p.Cp % kBK) == 0;
+  const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
   const bool split = p.splits > 1;
   dim3 grid(ntm * ntn, split ? p.splits : 1);
   if (aligned && !split) conv_mfma_kernel<BM, BN, WM, WN, true, false><<<grid, kNT, 0, s>>>(p);

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 
 namespace byoc {
@@ -71,6 +72,25 @@ void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* 
   }
 }
 
+// Tuning override (environment, read at engine creation):
+// BYOC_CONV_TILE=<bm>x<bn> forces a compiled tile, BYOC_CONV_SPLIT=<n> a
+// split-K factor, for every conv/dense composite of the engine.
+void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
+  if (const char* e = std::getenv("BYOC_CONV_TILE")) {
+    int bm = 0, bn = 0;
+    if (std::sscanf(e, "%dx%d", &bm, &bn) == 2 && conv_mfma_tile_supported(bm, bn)) {
+      t->bm = bm;
+      t->bn = bn;
+    }
+  }
+  if (const char* e = std::getenv("BYOC_CONV_SPLIT")) {
+    const int nk = (Kg + kKPad - 1) / kKPad;
+    const int sp = std::max(1, std::min(std::atoi(e), nk));
+    *kps = (nk + sp - 1) / sp;
+    *splits = (nk + *kps - 1) / *kps;
+  }
+}
+
 struct Planner {
   Engine* e;
   Graph& g;
@@ -79,6 +99,7 @@ struct Planner {
   std::vector<int> cp;  // channel stride of each value's internal form
   std::vector<PackJob> jobs;
   int64_t wbytes = 0;
+  Status err;
 
   Planner(Engine* e_, Graph& g_) : e(e_), g(g_), bf16(g_.compute == DType::BF16) {
     loc.resize(g.values.size());
@@ -184,6 +205,7 @@ Status Planner::plan() {
     }
     if (!placed) loc[v] = arena(internal_bytes(v));
     plan_node((int)ni);
+    if (!err.ok()) return err;
   }
   // ---- outputs not written in place: boundary transforms ---------------------
   for (size_t j = 0; j < g.outputs.size(); ++j) {
@@ -292,12 +314,21 @@ void Planner::plan_node(int ni) {
     p.ldr = Kp;
     p.act = (int)n.act;
     const int rows = (int)rup(Kp, kRowPad);
+    const int64_t xb = (int64_t)N * H * W * Cp * 2, wb = (int64_t)rows * p.Kgp * 2;
+    if (xb >= (int64_t(1) << 31) || wb >= (int64_t(1) << 31)) {
+      err = Status::Err(BYOC_ERR_UNSUPPORTED, "node " + std::to_string(ni) + " (" + n.composite +
+                                                  "): input or packed weights of 2 GiB or more");
+      return;
+    }
+    p.x_bytes = (int)xb;
+    p.w_bytes = (int)wb;
     L.w = wslot((int64_t)rows * p.Kgp * 2);
     jobs.push_back({PackJob::ConvW, wc, L.w.off, K, Cg, R, S, Cp, p.Kgp, rows, 0, 0});
     L.bias = wslot((int64_t)rows * 4);
     jobs.push_back({PackJob::Vec, bc, L.bias.off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? K : 0, rows});
     int splits, kps;
     choose_conv_tile(p.M, Kp, p.Kg, &L.tile, &splits, &kps);
+    apply_tile_override(p.Kg, &L.tile, &splits, &kps);
     p.splits = splits;
     p.k_tiles_per_split = kps;
     L.op = Launch::ConvMfma;

@@ -33,6 +33,8 @@ struct ConvParams {
   int act;
   int splits;   // split-K factor (1 = none)
   int k_tiles_per_split;
+  int x_bytes;  // extent of x and w in bytes (buffer-load range; < 2^31)
+  int w_bytes;
 };
 
 struct ConvTile {
