@@ -23,6 +23,8 @@
 // fused.  With split-K each split writes fp32 partials and a second kernel
 // reduces them in a fixed order (bitwise reproducible) with the same
 // epilogue.
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace byoc {
@@ -30,6 +32,7 @@ namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
 
 constexpr int kBK = 64;          // reduction elements per stage
 constexpr int kCH = kBK / 8;     // 16-byte chunks per tile row
@@ -43,18 +46,19 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast
 // Per-thread state of one workgroup's main loop.  The two prefetch register
 // sets are members indexed by a template parameter so that they stay in
 // VGPRs (never addressable memory).
-template <int BM, int BN, int WM, int WN, bool ALIGNED>
+template <int BM, int BN, int WM, int WN, int MF, bool ALIGNED>
 struct ConvTileLoop {
   static constexpr int WTM = BM / WM;
   static constexpr int WTN = BN / WN;
-  static constexpr int TM = WTM / 16;
-  static constexpr int TN = WTN / 16;
+  static constexpr int TM = WTM / MF;  // MFMA tiles per wave along pixels
+  static constexpr int TN = WTN / MF;  // and along channels
   static constexpr int AR = BM / kRowsPerPass;
   static constexpr int BR = BN / kRowsPerPass;
 
+  using Acc = typename std::conditional<MF == 32, f32x16, f32x4>::type;
   uint4 ra[2][AR];
   uint4 rb[2][BR];
-  f32x4 acc[TN][TM];
+  Acc acc[TN][TM];
   // Activation rows.  Aligned path: pix = element offset of the row's
   // window origin plus this thread's 8 channels, tapmask bit r*S+s set when
   // that tap lies inside the image.  Non-aligned path: the window origin.
@@ -141,39 +145,60 @@ struct ConvTileLoop {
     }
   }
 
+  // One LDS stage (64 reduction elements): 2 k-steps of the 16x16x32 MFMA
+  // or 4 of the 32x32x16 one.  Lane l reads 16 bytes (8 consecutive
+  // reduction elements) of row l % MF at chunk (k-step, l / MF).
   __device__ __forceinline__ void compute(const uint4* sA, const uint4* sB) {
+    constexpr int KS = MF == 32 ? 16 : 32;
+    constexpr int GROUPS = 64 / MF;  // lane groups sharing a row
 #pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      const int chunk = ks * 4 + (lane >> 4);
+    for (int ks = 0; ks < kBK / KS; ++ks) {
+      const int chunk = ks * (KS / 8) + (lane / MF);
       bf16x8 af[TN], bfr[TM];
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
-        const int row = wn * WTN + i * 16 + (lane & 15);
+        const int row = wn * WTN + i * MF + (lane % MF);
         af[i] = as_bf16x8(sB[row * kCH + (chunk ^ (row & 7))]);
       }
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
-        const int row = wm * WTM + j * 16 + (lane & 15);
+        const int row = wm * WTM + j * MF + (lane % MF);
         bfr[j] = as_bf16x8(sA[row * kCH + (chunk ^ (row & 7))]);
       }
+      (void)GROUPS;
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TM; ++j) {
+          if constexpr (MF == 32)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
     }
+  }
+
+  // Channel (row of the MFMA output) held by accumulator element e of this
+  // lane, relative to the MFMA tile: 16x16 -> 4 (lane/16) + e; 32x32 ->
+  // 8 (e/4) + 4 (lane/32) + e%4.  The pixel (column) is lane % MF.
+  __device__ __forceinline__ int acc_row(int e) const {
+    if (MF == 32) return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+    return 4 * (lane >> 4) + e;
   }
 };
 
-template <int BM, int BN, int WM, int WN, bool ALIGNED, bool SPLIT>
+template <int BM, int BN, int WM, int WN, int MF, bool ALIGNED, bool SPLIT>
 __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
-  using L = ConvTileLoop<BM, BN, WM, WN, ALIGNED>;
+  using L = ConvTileLoop<BM, BN, WM, WN, MF, ALIGNED>;
   static_assert(WM * WN == 4, "4 waves");
   static_assert(L::TM >= 1 && L::TN >= 1 && L::AR >= 1 && L::BR >= 1, "tile too small");
   constexpr int WTM = L::WTM, WTN = L::WTN, TM = L::TM, TN = L::TN, AR = L::AR;
 
-  __shared__ uint4 sA[2][BM * kCH];
-  __shared__ uint4 sB[2][BN * kCH];
+  // Main-loop operand tiles (double buffered); the epilogue reuses the same
+  // memory as an fp32 staging tile.
+  __shared__ uint4 smem[2 * (BM + BN) * kCH];
+  uint4 (*sA)[BM * kCH] = reinterpret_cast<uint4 (*)[BM * kCH]>(smem);
+  uint4 (*sB)[BN * kCH] = reinterpret_cast<uint4 (*)[BN * kCH]>(smem + 2 * BM * kCH);
 
   L st;
   const int tid = threadIdx.x;
@@ -249,10 +274,42 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
 #pragma unroll
   for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j) st.acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TM; ++j) st.acc[i][j] = typename L::Acc{};
 
   // Two register sets: the loads of tile t+2 are issued before the MFMAs
   // of tile t and written to LDS after those of tile t+1.
+  // Epilogue operands (bias and residual of the 8 channels this thread will
+  // finish for each of its pixels) are fetched before the main loop, so their
+  // latency overlaps the reduction instead of following it.
+  constexpr int kEC = 64;              // channels per epilogue pass
+  constexpr int NPASS = BN / kEC;
+  constexpr int EPV = BM * (kEC / 8) / kNT;  // pixels per thread per pass
+  static_assert(EPV >= 1, "epilogue vectors");
+  const int ec8 = (tid % (kEC / 8)) * 8;
+  uint4 resv[NPASS][EPV];
+  float4 biasv[NPASS][2];
+  if (!SPLIT) {
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16_t*>(p.res), (short)0, p.res ? p.res_bytes : 0, kBufferFlags);
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int k = n0 + pass * kEC + ec8;
+      if (p.bias) {
+        biasv[pass][0] = *(const float4*)(p.bias + k);
+        biasv[pass][1] = *(const float4*)(p.bias + k + 4);
+      } else {
+        biasv[pass][0] = biasv[pass][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) {
+        const int m = m0 + (tid + q * kNT) / (kEC / 8);
+        const uint32_t off = (m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) * 2u : 0x80000000u;
+        resv[pass][q] = p.res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0))
+                              : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+  }
+
   const int nkt = kt_end - kt_begin;
   if (nkt > 0) {
     st.template load<0>(p, true, true);
@@ -274,43 +331,68 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
     }
   }
 
-  // Epilogue: lane holds channels k..k+3 of pixel m for each (i, j).
+  constexpr int NE = MF == 32 ? 16 : 4;  // accumulator elements per lane per tile
+  if (SPLIT) {
+    // fp32 partials of this split: each group of 4 accumulator elements is
+    // 4 consecutive channels of one pixel
 #pragma unroll
-  for (int i = 0; i < TN; ++i) {
-    const int k = n0 + wn * WTN + i * 16 + 4 * (lane >> 4);
-    if (k >= p.Kp) continue;
-    if (SPLIT) {
-#pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        const int m = m0 + wm * WTM + j * 16 + (lane & 15);
-        if (m >= p.M) continue;
-        const f32x4 a = st.acc[i][j];
-        *(float4*)(p.partial + ((size_t)blockIdx.y * p.M + m) * p.Kp + k) = make_float4(a[0], a[1], a[2], a[3]);
-      }
-    } else {
-      const float4 bv = p.bias ? *(const float4*)(p.bias + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < TN; ++i)
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
-        const int m = m0 + wm * WTM + j * 16 + (lane & 15);
-        if (m >= p.M) continue;
-        const f32x4 a = st.acc[i][j];
-        float v0 = a[0] + bv.x;
-        float v1 = a[1] + bv.y;
-        float v2 = a[2] + bv.z;
-        float v3 = a[3] + bv.w;
-        if (p.res) {
-          const uint2 rr = *(const uint2*)(p.res + (size_t)m * p.ldr + k);
-          v0 += __uint_as_float(rr.x << 16);
-          v1 += __uint_as_float(rr.x & 0xFFFF0000u);
-          v2 += __uint_as_float(rr.y << 16);
-          v3 += __uint_as_float(rr.y & 0xFFFF0000u);
+        const int m = m0 + wm * WTM + j * MF + (lane % MF);
+#pragma unroll
+        for (int e = 0; e < NE; e += 4) {
+          const int k = n0 + wn * WTN + i * MF + st.acc_row(e);
+          if (m >= p.M || k >= p.Kp) continue;
+          *(float4*)(p.partial + ((size_t)blockIdx.y * p.M + m) * p.Kp + k) =
+              make_float4(st.acc[i][j][e], st.acc[i][j][e + 1], st.acc[i][j][e + 2], st.acc[i][j][e + 3]);
         }
-        v0 = apply_act(v0, p.act);
-        v1 = apply_act(v1, p.act);
-        v2 = apply_act(v2, p.act);
-        v3 = apply_act(v3, p.act);
-        *(uint2*)(p.y + (size_t)m * p.ldy + k) = make_uint2(pack2_bf16(v0, v1), pack2_bf16(v2, v3));
       }
+    return;
+  }
+
+  // Epilogue through LDS, 64 channels per pass: the waves park their fp32
+  // accumulators in a [BM][64 + 4] tile, then every thread takes 8
+  // consecutive channels of one pixel, adds bias and residual, applies the
+  // activation, rounds to bf16 and writes 16 bytes; 8 neighbouring lanes
+  // cover one pixel's 128-byte run, so stores and residual loads are whole
+  // cache lines.
+  constexpr int kLd = kEC + 4;  // padded row (floats): 16 rows hit distinct banks
+  static_assert(BN % kEC == 0 && BM * kLd * 4 <= (int)sizeof(smem), "staging tile");
+  float* stage = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int pass = 0; pass < NPASS; ++pass) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int px = wm * WTM + j * MF + (lane % MF);
+#pragma unroll
+        for (int e = 0; e < NE; e += 4) {
+          const int ch = wn * WTN + i * MF + st.acc_row(e) - pass * kEC;
+          if (ch < 0 || ch >= kEC) continue;
+          *(float4*)(stage + px * kLd + ch) =
+              make_float4(st.acc[i][j][e], st.acc[i][j][e + 1], st.acc[i][j][e + 2], st.acc[i][j][e + 3]);
+        }
+      }
+    __syncthreads();
+    const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+    for (int q = 0; q < EPV; ++q) {
+      const int px = (tid + q * kNT) / (kEC / 8);
+      const int m = m0 + px;
+      if (m >= p.M || k >= p.Kp) continue;
+      float f[8], r[8];
+      const float4 lo = *(const float4*)(stage + px * kLd + ec8);
+      const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
+      const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
+      unpack8(resv[pass][q], r);
+      f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
+      f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = apply_act(f[e] + r[e], p.act);
+      *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
     }
   }
 }
@@ -350,33 +432,45 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
                  pack2_bf16(apply_act(acc.z, p.act), apply_act(acc.w, p.act)));
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int MF>
 hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
   const int ntm = (p.M + BM - 1) / BM;
   const int ntn = (p.Kp + BN - 1) / BN;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
   const bool split = p.splits > 1;
   dim3 grid(ntm * ntn, split ? p.splits : 1);
-  if (aligned && !split) conv_mfma_kernel<BM, BN, WM, WN, true, false><<<grid, kNT, 0, s>>>(p);
-  else if (aligned) conv_mfma_kernel<BM, BN, WM, WN, true, true><<<grid, kNT, 0, s>>>(p);
-  else if (!split) conv_mfma_kernel<BM, BN, WM, WN, false, false><<<grid, kNT, 0, s>>>(p);
-  else conv_mfma_kernel<BM, BN, WM, WN, false, true><<<grid, kNT, 0, s>>>(p);
+  if (aligned && !split) conv_mfma_kernel<BM, BN, WM, WN, MF, true, false><<<grid, kNT, 0, s>>>(p);
+  else if (aligned) conv_mfma_kernel<BM, BN, WM, WN, MF, true, true><<<grid, kNT, 0, s>>>(p);
+  else if (!split) conv_mfma_kernel<BM, BN, WM, WN, MF, false, false><<<grid, kNT, 0, s>>>(p);
+  else conv_mfma_kernel<BM, BN, WM, WN, MF, false, true><<<grid, kNT, 0, s>>>(p);
   return hipGetLastError();
 }
 
 }  // namespace
 
-bool conv_mfma_tile_supported(int bm, int bn) {
-  return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
-         (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+bool conv_mfma_tile_supported(int bm, int bn, int mf) {
+  if (mf == 16)
+    return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
+           (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+  if (mf == 32)
+    return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
+           (bm == 64 && bn == 64);
+  return false;
 }
 
 hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s) {
-  if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2, 2>(p, s);
-  if (t.bm == 128 && t.bn == 64) return launch_tile<128, 64, 4, 1>(p, s);
-  if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 1, 4>(p, s);
-  if (t.bm == 64 && t.bn == 64) return launch_tile<64, 64, 2, 2>(p, s);
-  if (t.bm == 32 && t.bn == 64) return launch_tile<32, 64, 1, 4>(p, s);
+  if (t.mf == 32) {
+    if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2, 2, 32>(p, s);
+    if (t.bm == 128 && t.bn == 64) return launch_tile<128, 64, 2, 2, 32>(p, s);
+    if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 2, 2, 32>(p, s);
+    if (t.bm == 64 && t.bn == 64) return launch_tile<64, 64, 2, 2, 32>(p, s);
+    return hipErrorInvalidValue;
+  }
+  if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2, 2, 16>(p, s);
+  if (t.bm == 128 && t.bn == 64) return launch_tile<128, 64, 4, 1, 16>(p, s);
+  if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 1, 4, 16>(p, s);
+  if (t.bm == 64 && t.bn == 64) return launch_tile<64, 64, 2, 2, 16>(p, s);
+  if (t.bm == 32 && t.bn == 64) return launch_tile<32, 64, 1, 4, 16>(p, s);
   return hipErrorInvalidValue;
 }
 

@@ -42,45 +42,38 @@ struct PackJob {
 // (deterministically, reduced by a second kernel) when the output has too
 // few tiles and the reduction is long enough to share.
 void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* kps) {
-  struct Cand { int bm, bn, occ; double t_stage; };
-  static const Cand cands[] = {
-      {128, 128, 2, 1.00}, {128, 64, 3, 0.80}, {64, 128, 3, 0.80}, {64, 64, 5, 0.62}, {32, 64, 6, 0.55}};
+  // Measured on MI355X over the ResNet-50 layers: 64x64 tiles (16x16x32
+  // MFMA) win at every batch-32 shape - larger tiles leave fewer workgroups
+  // per CU to overlap each one's load/compute/epilogue phases - and split-K
+  // only pays when the output has very few tiles.
+  t->bm = M >= 48 ? 64 : 32;
+  t->bn = 64;
+  t->mf = 16;
   const int nk = (int)((Kg + kKPad - 1) / kKPad);
-  const int kCUs = 256;
-  double best = 1e30;
-  for (const Cand& c : cands) {
-    const int64_t tiles = ((M + c.bm - 1) / c.bm) * ((Kp + c.bn - 1) / c.bn);
-    for (int s = 1; s <= 16; s *= 2) {
-      if (s > 1 && (nk / s < 4)) break;
-      const int k_per = (nk + s - 1) / s;
-      const int sp = (nk + k_per - 1) / k_per;
-      const int64_t blocks = tiles * sp;
-      const int64_t slots = (int64_t)c.occ * kCUs;
-      const double rounds = (double)((blocks + slots - 1) / slots);
-      // a round of `occ` co-resident workgroups takes about one stage time per k-tile
-      double est = rounds * k_per * c.t_stage;
-      // split-K moves fp32 partials: write + read, relative to stage time units
-      if (sp > 1) est += (double)sp * M * Kp * 8.0 / 4.0e12 / 0.8e-6;
-      if (est < best * 0.98) {
-        best = est;
-        t->bm = c.bm;
-        t->bn = c.bn;
-        *splits = sp;
-        *kps = k_per;
-      }
+  const int64_t tiles = ((M + t->bm - 1) / t->bm) * ((Kp + t->bn - 1) / t->bn);
+  *splits = 1;
+  *kps = nk;
+  if (tiles < 64 && nk >= 8) {
+    int s = (int)std::min<int64_t>(nk / 4, (128 + tiles - 1) / tiles);
+    s = std::max(1, std::min(s, 16));
+    if (s > 1) {
+      *kps = (nk + s - 1) / s;
+      *splits = (nk + *kps - 1) / *kps;
     }
   }
 }
 
 // Tuning override (environment, read at engine creation):
-// BYOC_CONV_TILE=<bm>x<bn> forces a compiled tile, BYOC_CONV_SPLIT=<n> a
+// BYOC_CONV_TILE=<bm>x<bn>[x<mfma 16|32>] forces a compiled tile, BYOC_CONV_SPLIT=<n> a
 // split-K factor, for every conv/dense composite of the engine.
 void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
   if (const char* e = std::getenv("BYOC_CONV_TILE")) {
-    int bm = 0, bn = 0;
-    if (std::sscanf(e, "%dx%d", &bm, &bn) == 2 && conv_mfma_tile_supported(bm, bn)) {
+    int bm = 0, bn = 0, mf = 16;
+    const int got = std::sscanf(e, "%dx%dx%d", &bm, &bn, &mf);
+    if (got >= 2 && conv_mfma_tile_supported(bm, bn, mf)) {
       t->bm = bm;
       t->bn = bn;
+      t->mf = mf;
     }
   }
   if (const char* e = std::getenv("BYOC_CONV_SPLIT")) {
@@ -320,8 +313,15 @@ void Planner::plan_node(int ni) {
                                                   "): input or packed weights of 2 GiB or more");
       return;
     }
+    const int64_t rb = (int64_t)p.M * Kp * 2;
+    if (rb >= (int64_t(1) << 31)) {
+      err = Status::Err(BYOC_ERR_UNSUPPORTED, "node " + std::to_string(ni) + " (" + n.composite +
+                                                  "): output of 2 GiB or more");
+      return;
+    }
     p.x_bytes = (int)xb;
     p.w_bytes = (int)wb;
+    p.res_bytes = (int)rb;
     L.w = wslot((int64_t)rows * p.Kgp * 2);
     jobs.push_back({PackJob::ConvW, wc, L.w.off, K, Cg, R, S, Cp, p.Kgp, rows, 0, 0});
     L.bias = wslot((int64_t)rows * 4);
@@ -333,8 +333,8 @@ void Planner::plan_node(int ni) {
     p.k_tiles_per_split = kps;
     L.op = Launch::ConvMfma;
     L.info.kind = BYOC_K_CONV_MFMA;
-    std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_split%d", L.tile.bm,
-                  L.tile.bn, splits);
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_mf%d_split%d", L.tile.bm,
+                  L.tile.bn, L.tile.mf, splits);
     if (splits > 1) {
       L.partial = arena((int64_t)splits * p.M * Kp * 4);
       Launch Rd = L;

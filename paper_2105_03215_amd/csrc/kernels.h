@@ -33,16 +33,18 @@ struct ConvParams {
   int act;
   int splits;   // split-K factor (1 = none)
   int k_tiles_per_split;
-  int x_bytes;  // extent of x and w in bytes (buffer-load range; < 2^31)
+  int x_bytes;  // extent of x, w and res in bytes (buffer-load range; < 2^31)
   int w_bytes;
+  int res_bytes;
 };
 
 struct ConvTile {
-  int bm, bn;  // pixels x channels per workgroup
+  int bm, bn;   // pixels x channels per workgroup
+  int mf = 16;  // MFMA shape: 16 (16x16x32) or 32 (32x32x16)
 };
 
 // Tile configurations with a compiled kernel.
-bool conv_mfma_tile_supported(int bm, int bn);
+bool conv_mfma_tile_supported(int bm, int bn, int mf);
 hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
 // Sums split-K partials in a fixed order and applies bias, residual, act.
 hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s);

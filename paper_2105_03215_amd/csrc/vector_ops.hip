@@ -91,26 +91,41 @@ __global__ __launch_bounds__(kThreads) void maxpool_nhwc_kernel(PoolParams p) {
   *(uint4*)((bf16_t*)p.y + (((size_t)n * p.P + pp) * p.Q + q) * p.Cp + g * 8) = pack8(m);
 }
 
-// Global average pool NHWC bf16 -> [N][Cp] bf16; fp32 sum in pixel order.
+// Global average pool NHWC bf16 -> [N][Cp] bf16.  Workgroup = one image x
+// 8 channel groups (64 channels); 32 lanes per group stride over the pixels,
+// then one lane per group sums the 32 partials in lane order (fixed order,
+// run-to-run identical) and divides by H*W.
 __global__ __launch_bounds__(kThreads) void avgpool_nhwc_kernel(PoolParams p) {
+  __shared__ float part[32][8][8];
   const int G = p.Cp / 8;
-  const int idx = blockIdx.x * kThreads + threadIdx.x;
-  if (idx >= p.N * G) return;
-  const int g = idx % G;
-  const int n = idx / G;
-  const bf16_t* x = (const bf16_t*)p.x + (size_t)n * p.H * p.W * p.Cp + g * 8;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const int n = blockIdx.x;
+  const int gl = threadIdx.x % 8;
+  const int pl = threadIdx.x / 8;
+  const int g = blockIdx.y * 8 + gl;
   const int HW = p.H * p.W;
-  for (int i = 0; i < HW; ++i) {
-    float v[8];
-    unpack8(*(const uint4*)(x + (size_t)i * p.Cp), v);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (g < G) {
+    const bf16_t* x = (const bf16_t*)p.x + (size_t)n * HW * p.Cp + g * 8;
+    for (int i = pl; i < HW; i += 32) {
+      float v[8];
+      unpack8(*(const uint4*)(x + (size_t)i * p.Cp), v);
 #pragma unroll
-    for (int c = 0; c < 8; ++c) acc[c] += v[c];
+      for (int c = 0; c < 8; ++c) acc[c] += v[c];
+    }
   }
-  const float inv = 1.0f / (float)HW;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) acc[c] *= inv;
-  *(uint4*)((bf16_t*)p.y + (size_t)n * p.Cp + g * 8) = pack8(acc);
+  for (int c = 0; c < 8; ++c) part[pl][gl][c] = acc[c];
+  __syncthreads();
+  if (pl == 0 && g < G) {
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int l = 0; l < 32; ++l)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) s[c] += part[l][gl][c];
+    const float inv = 1.0f / (float)HW;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) s[c] *= inv;
+    *(uint4*)((bf16_t*)p.y + (size_t)n * p.Cp + g * 8) = pack8(s);
+  }
 }
 
 // fp32 NCHW pools, one thread per output.
@@ -317,7 +332,7 @@ hipError_t launch_maxpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
 }
 
 hipError_t launch_avgpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
-  avgpool_nhwc_kernel<<<grid_for((int64_t)p.N * (p.Cp / 8)), kThreads, 0, s>>>(p);
+  avgpool_nhwc_kernel<<<dim3(p.N, (p.Cp / 8 + 7) / 8), kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
