@@ -133,6 +133,8 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="headline value from direct launches instead of HIP-graph replay")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device copy of MIB MiB three times (counter calibration)")
@@ -167,7 +169,17 @@ def main():
     for _ in range(args.warmup):
         sg.run(ins, outs, stream)
     torch.cuda.synchronize()
-    ms, wall = _timed_runs(sg, ins, outs, stream, args.steps)
+    ms_eager, wall_eager = _timed_runs(sg, ins, outs, stream, args.steps)
+    sg.set_options(graph_replay=True)
+    for _ in range(args.warmup):
+        sg.run(ins, outs, stream)
+    torch.cuda.synchronize()
+    ms_graph, wall_graph = _timed_runs(sg, ins, outs, stream, args.steps)
+    sg.set_options(graph_replay=False)
+    if args.eager:
+        ms, wall, mode = ms_eager, wall_eager, "direct launches"
+    else:
+        ms, wall, mode = ms_graph, wall_graph, "HIP graph replay"
     value = args.batch / (ms * 1e-3)
     launches = sg.launches()
     per_launch, runs = _profile(sg, ins, outs, stream, args.steps)
@@ -198,8 +210,14 @@ def main():
         outs1 = runtime.outputs_for(sg1, dev)
         for _ in range(args.warmup):
             sg1.run(ins1, outs1, stream)
-        ms1, _ = _timed_runs(sg1, ins1, outs1, stream, max(args.steps, 200))
+        ms1e, _ = _timed_runs(sg1, ins1, outs1, stream, max(args.steps, 200))
+        sg1.set_options(graph_replay=True)
+        for _ in range(args.warmup):
+            sg1.run(ins1, outs1, stream)
+        ms1g, _ = _timed_runs(sg1, ins1, outs1, stream, max(args.steps, 200))
+        ms1 = ms1e if args.eager else ms1g
         bs1 = {"images_per_s": round(1.0 / (ms1 * 1e-3), 1), "ms_per_step": round(ms1, 4),
+               "launch_mode": mode, "eager_images_per_s": round(1.0 / (ms1e * 1e-3), 1),
                "launches": len(sg1.launches())}
         sg1.close()
 
@@ -214,7 +232,10 @@ def main():
         "data": "synthetic (seeded uniform[0,1) images, random He-init weights with folded BN)",
         "config": {"workload": "%s_bs%d" % (args.variant, args.batch), "batch": args.batch,
                    "input": [args.batch, 3, 224, 224], "gflop_per_image": round(2 * wl.macs / args.batch / 1e9, 3),
-                   "launches_per_step": len(launches), "parallelism": "none (1 GPU)"},
+                   "launches_per_step": len(launches), "parallelism": "none (1 GPU)",
+                   "launch_mode": mode},
+        "eager_images_per_s": round(args.batch / (ms_eager * 1e-3), 1),
+        "graph_images_per_s": round(args.batch / (ms_graph * 1e-3), 1),
         "roofline": roof,
         "cpu_baseline": cpu,
         "bs1": bs1,

@@ -181,6 +181,20 @@ byoc_status byoc_subgraph_launch_info(const byoc_subgraph* g, int32_t i, byoc_la
 byoc_status byoc_subgraph_profile_begin(byoc_subgraph* g, int32_t max_runs);
 byoc_status byoc_subgraph_profile_end(byoc_subgraph* g, float* ms, int32_t n, int32_t* runs);
 
+/* Engine options (bit flags) for byoc_subgraph_set_options. */
+enum { BYOC_OPT_GRAPH_REPLAY = 1 };
+
+/* Set engine options (default 0).  BYOC_OPT_GRAPH_REPLAY: run() records its
+ * launch sequence as a HIP graph the first time it sees a (stream, inputs,
+ * outputs) combination and afterwards replays that graph - one graph launch
+ * instead of one launch per kernel - while the combination repeats; a new
+ * combination is recorded again.  Recording and instantiating allocate host
+ * and device memory on those runs, so an allocation-free run() needs the
+ * option off.  Runs on the NULL stream, runs while profiling and runs on a
+ * stream that is already being captured by the caller use direct launches.
+ * Unknown flag bits are rejected with BYOC_ERR_INVALID_ARG. */
+byoc_status byoc_subgraph_set_options(byoc_subgraph* g, int32_t flags);
+
 /* Thread-local text of the last error ("" if none). */
 const char* byoc_last_error(void);
 

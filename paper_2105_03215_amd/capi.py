@@ -24,7 +24,9 @@ STATUS_NAMES = ["OK", "INVALID_ARG", "PARSE", "UNSUPPORTED", "SHAPE", "DEVICE", 
 EXPORTS = ["byoc_subgraph_validate", "byoc_subgraph_create", "byoc_subgraph_run",
            "byoc_subgraph_destroy", "byoc_subgraph_num_io", "byoc_subgraph_io_desc",
            "byoc_subgraph_stats", "byoc_subgraph_num_launches", "byoc_subgraph_launch_info",
-           "byoc_subgraph_profile_begin", "byoc_subgraph_profile_end", "byoc_last_error"]
+           "byoc_subgraph_profile_begin", "byoc_subgraph_profile_end",
+           "byoc_subgraph_set_options", "byoc_last_error"]
+OPT_GRAPH_REPLAY = 1
 
 
 class ByocConst(ctypes.Structure):
@@ -75,6 +77,7 @@ def load_library(path=LIB_PATH):
         "byoc_subgraph_num_launches": [P, ctypes.POINTER(i32)],
         "byoc_subgraph_launch_info": [P, i32, ctypes.POINTER(LaunchInfo)],
         "byoc_subgraph_profile_begin": [P, i32],
+        "byoc_subgraph_set_options": [P, i32],
         "byoc_subgraph_profile_end": [P, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)],
     }
     for name, args in sig.items():
@@ -198,6 +201,10 @@ class Subgraph:
             s = stream.cuda_stream
         _check(self.lib.byoc_subgraph_run(self.handle, ins, len(inputs), outs, len(outputs),
                                           ctypes.c_void_p(s)))
+
+    def set_options(self, graph_replay=False):
+        """Enable or disable HIP-graph replay of the launch sequence."""
+        _check(self.lib.byoc_subgraph_set_options(self.handle, OPT_GRAPH_REPLAY if graph_replay else 0))
 
     def profile_begin(self, max_runs):
         _check(self.lib.byoc_subgraph_profile_begin(self.handle, int(max_runs)))

@@ -128,6 +128,13 @@ byoc_status byoc_subgraph_launch_info(const byoc_subgraph* g, int32_t i, byoc_la
   return BYOC_OK;
 }
 
+byoc_status byoc_subgraph_set_options(byoc_subgraph* g, int32_t flags) {
+  g_last_error.clear();
+  if (!g || !g->engine) return fail(BYOC_ERR_INVALID_ARG, "subgraph handle is NULL");
+  byoc::Status st = byoc::engine_set_options(g->engine, flags);
+  return st.ok() ? BYOC_OK : fail(st);
+}
+
 byoc_status byoc_subgraph_profile_begin(byoc_subgraph* g, int32_t max_runs) {
   g_last_error.clear();
   if (!g || !g->engine) return fail(BYOC_ERR_INVALID_ARG, "subgraph handle is NULL");

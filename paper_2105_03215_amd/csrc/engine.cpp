@@ -535,6 +535,8 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
 
 void release(Engine* e) {
   if (!e) return;
+  if (e->gexec) (void)hipGraphExecDestroy(e->gexec);
+  e->gexec = nullptr;
   for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);
   e->events.clear();
   if (e->arena) (void)hipFree(e->arena);
@@ -642,6 +644,67 @@ Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int 
   return Status::Ok();
 }
 
+namespace {
+
+void drop_graph(Engine* e) {
+  if (e->gexec) (void)hipGraphExecDestroy(e->gexec);
+  e->gexec = nullptr;
+  e->g_in.clear();
+  e->g_out.clear();
+  e->g_stream = nullptr;
+}
+
+// Replays the recorded graph when stream and I/O pointers match the
+// recording, otherwise records the launch sequence anew.
+Status run_graph(Engine* e, const RunCtx& c, int32_t n_in, int32_t n_out) {
+  const bool same = e->gexec && e->g_stream == c.s &&
+                    std::equal(e->g_in.begin(), e->g_in.end(), c.in) &&
+                    std::equal(e->g_out.begin(), e->g_out.end(), c.out) &&
+                    (int32_t)e->g_in.size() == n_in && (int32_t)e->g_out.size() == n_out;
+  if (!same) {
+    drop_graph(e);
+    HIP_TRY(hipStreamBeginCapture(c.s, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+    hipError_t lerr = hipSuccess;
+    size_t bad = 0;
+    for (size_t i = 0; i < e->launches.size() && lerr == hipSuccess; ++i) {
+      lerr = exec(e->launches[i], c);
+      bad = i;
+    }
+    hipGraph_t graph = nullptr;
+    hipError_t cerr = hipStreamEndCapture(c.s, &graph);
+    if (lerr != hipSuccess || cerr != hipSuccess) {
+      if (graph) (void)hipGraphDestroy(graph);
+      if (lerr != hipSuccess)
+        return Status::Err(BYOC_ERR_DEVICE, std::string("launch ") + std::to_string(bad) + " (" +
+                                                e->launches[bad].info.name + ") during graph capture: " +
+                                                hipGetErrorString(lerr));
+      return Status::Err(BYOC_ERR_DEVICE, std::string("hipStreamEndCapture: ") + hipGetErrorString(cerr));
+    }
+    hipError_t ierr = hipGraphInstantiate(&e->gexec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ierr != hipSuccess) {
+      e->gexec = nullptr;
+      return Status::Err(BYOC_ERR_DEVICE, std::string("hipGraphInstantiate: ") + hipGetErrorString(ierr));
+    }
+    e->g_stream = c.s;
+    e->g_in.assign(c.in, c.in + n_in);
+    e->g_out.assign(c.out, c.out + n_out);
+  }
+  HIP_TRY(hipGraphLaunch(e->gexec, c.s), "hipGraphLaunch");
+  return Status::Ok();
+}
+
+}  // namespace
+
+Status engine_set_options(Engine* e, int flags) {
+  if (flags & ~BYOC_OPT_GRAPH_REPLAY)
+    return Status::Err(BYOC_ERR_INVALID_ARG, "unknown option bits " + std::to_string(flags));
+  DeviceGuard guard(e->device);
+  if (!(flags & BYOC_OPT_GRAPH_REPLAY)) drop_graph(e);
+  e->options = flags;
+  return Status::Ok();
+}
+
 Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
                   int32_t n_out, hipStream_t stream) {
   if (n_in != (int32_t)e->graph.inputs.size())
@@ -659,6 +722,11 @@ Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* cons
   DeviceGuard guard(e->device);
   RunCtx c{e, inputs, outputs, stream};
   const bool prof = !e->events.empty() && e->prof_runs < e->prof_max_runs;
+  if ((e->options & BYOC_OPT_GRAPH_REPLAY) && !prof && stream != nullptr) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+    if (cs == hipStreamCaptureStatusNone) return run_graph(e, c, n_in, n_out);
+  }
   const size_t nl = e->launches.size();
   hipEvent_t* ev = prof ? &e->events[(size_t)e->prof_runs * (nl + 1)] : nullptr;
   if (prof) HIP_TRY(hipEventRecord(ev[0], stream), "hipEventRecord");

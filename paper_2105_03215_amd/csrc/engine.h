@@ -54,6 +54,12 @@ struct Engine {
   int64_t arena_bytes = 0;
   char* weights = nullptr;
   int64_t weight_bytes = 0;
+  // graph replay (BYOC_OPT_GRAPH_REPLAY)
+  int options = 0;
+  hipGraphExec_t gexec = nullptr;
+  hipStream_t g_stream = nullptr;
+  std::vector<const void*> g_in;
+  std::vector<void*> g_out;
   // profiling
   std::vector<hipEvent_t> events;
   int prof_max_runs = 0;
@@ -67,6 +73,7 @@ Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int 
 Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
                   int32_t n_out, hipStream_t stream);
 Status engine_destroy(Engine* e);
+Status engine_set_options(Engine* e, int flags);
 Status engine_profile_begin(Engine* e, int max_runs);
 Status engine_profile_end(Engine* e, float* ms, int n, int* runs);
 

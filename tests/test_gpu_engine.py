@@ -150,3 +150,42 @@ def test_run_argument_errors():
         assert lib.byoc_subgraph_run(None, None, 0, None, 0, None) == 1
     finally:
         sg.close()
+
+
+def test_graph_replay_matches_eager():
+    """HIP-graph replay: every replay, with eager torch work and host
+    synchronisations between replays, equals the direct-launch result bit for
+    bit; new output pointers are recorded anew; the null stream falls back to
+    direct launches."""
+    announce("graph replay")
+    wl = workloads.resnet18_block(n=2, c=64, hw=28)
+    sg = capi.Subgraph(wl.graph, wl.consts)
+    s = torch.cuda.Stream(device=DEV)
+    try:
+        ins = runtime.inputs_for(sg, wl.inputs, DEV)
+        ref = runtime.outputs_for(sg, DEV)
+        sg.run(ins, ref, s)
+        s.synchronize()
+        sg.set_options(graph_replay=True)
+        outs = runtime.outputs_for(sg, DEV)
+        for rep in range(4):
+            outs[0].fill_(-1.0)
+            torch.cuda.synchronize()
+            sg.run(ins, outs, s)
+            s.synchronize()
+            assert torch.equal(outs[0].view(torch.int16), ref[0].view(torch.int16)), rep
+        other = runtime.outputs_for(sg, DEV)
+        sg.run(ins, other, s)
+        sg.run(ins, outs, s)
+        s.synchronize()
+        assert torch.equal(other[0].view(torch.int16), ref[0].view(torch.int16))
+        assert torch.equal(outs[0].view(torch.int16), ref[0].view(torch.int16))
+        null_out = runtime.outputs_for(sg, DEV)
+        sg.run(ins, null_out, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(null_out[0].view(torch.int16), ref[0].view(torch.int16))
+        with pytest.raises(capi.ByocError):
+            capi._check(sg.lib.byoc_subgraph_set_options(sg.handle, 6))
+        sg.set_options(graph_replay=False)
+    finally:
+        sg.close()
