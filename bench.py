@@ -82,12 +82,10 @@ def _class_summary(launches, per_launch_ms):
 
 
 def _conv_kernel_digest():
-    """Digest of the conv kernel source: stored traffic counts apply only to
-    the kernel they were measured on."""
-    import hashlib
-    src = os.path.join(ROOT, "paper_2105_03215_amd", "csrc", "conv_mfma.hip")
-    with open(src, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Digest of the conv kernel sources and their planner: stored traffic
+    counts apply only to the kernels they were measured on."""
+    from paper_2105_03215_amd import profiling
+    return profiling.conv_kernel_digest()
 
 
 def _copy_calibration(mib):
@@ -133,6 +131,8 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--no-autotune", action="store_true",
+                    help="keep the built-in conv kernel choice (no on-device tuning at setup)")
     ap.add_argument("--eager", action="store_true",
                     help="headline value from direct launches instead of HIP-graph replay")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
@@ -166,6 +166,11 @@ def main():
     ins = runtime.inputs_for(sg, wl.inputs, dev)
     outs = runtime.outputs_for(sg, dev)
     torch.cuda.synchronize()
+    tune_s = None
+    if not args.no_autotune:
+        t0 = time.perf_counter()
+        sg.set_options(autotune=True)
+        tune_s = time.perf_counter() - t0
     for _ in range(args.warmup):
         sg.run(ins, outs, stream)
     torch.cuda.synchronize()
@@ -206,6 +211,8 @@ def main():
     if not args.no_bs1 and args.batch != 1:
         wl1 = workloads.build(args.variant, n=1)
         sg1 = capi.Subgraph(wl1.graph, wl1.consts, device=0)
+        if not args.no_autotune:
+            sg1.set_options(autotune=True)
         ins1 = runtime.inputs_for(sg1, wl1.inputs, dev)
         outs1 = runtime.outputs_for(sg1, dev)
         for _ in range(args.warmup):
@@ -241,6 +248,7 @@ def main():
         "bs1": bs1,
         "kernel_classes": _class_summary(launches, per_launch),
         "create_s": round(create_s, 3),
+        "autotune_s": None if tune_s is None else round(tune_s, 3),
         "weight_bytes": stats["weight_bytes"], "arena_bytes": stats["arena_bytes"],
         "wall_s_timed": round(wall, 4),
     }

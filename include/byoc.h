@@ -182,7 +182,7 @@ byoc_status byoc_subgraph_profile_begin(byoc_subgraph* g, int32_t max_runs);
 byoc_status byoc_subgraph_profile_end(byoc_subgraph* g, float* ms, int32_t n, int32_t* runs);
 
 /* Engine options (bit flags) for byoc_subgraph_set_options. */
-enum { BYOC_OPT_GRAPH_REPLAY = 1 };
+enum { BYOC_OPT_GRAPH_REPLAY = 1, BYOC_OPT_AUTOTUNE = 2 };
 
 /* Set engine options (default 0).  BYOC_OPT_GRAPH_REPLAY: run() records its
  * launch sequence as a HIP graph the first time it sees a (stream, inputs,
@@ -192,7 +192,14 @@ enum { BYOC_OPT_GRAPH_REPLAY = 1 };
  * and device memory on those runs, so an allocation-free run() needs the
  * option off.  Runs on the NULL stream, runs while profiling and runs on a
  * stream that is already being captured by the caller use direct launches.
- * Unknown flag bits are rejected with BYOC_ERR_INVALID_ARG. */
+ * BYOC_OPT_AUTOTUNE: when the bit is turned on, this call times on the
+ * device (synchronously, on a stream of its own, with scratch input and
+ * output buffers it allocates and frees) every kernel variant the engine
+ * has for each convolution / dense composite whose results are bit-for-bit
+ * those of the built-in choice (same tile reduction order, no split-K
+ * change) and keeps the fastest; turning it off restores the built-in
+ * choice.  The computed values never change, only the speed.  Unknown flag
+ * bits are rejected with BYOC_ERR_INVALID_ARG. */
 byoc_status byoc_subgraph_set_options(byoc_subgraph* g, int32_t flags);
 
 /* Thread-local text of the last error ("" if none). */

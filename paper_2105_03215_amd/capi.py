@@ -27,6 +27,7 @@ EXPORTS = ["byoc_subgraph_validate", "byoc_subgraph_create", "byoc_subgraph_run"
            "byoc_subgraph_profile_begin", "byoc_subgraph_profile_end",
            "byoc_subgraph_set_options", "byoc_last_error"]
 OPT_GRAPH_REPLAY = 1
+OPT_AUTOTUNE = 2
 
 
 class ByocConst(ctypes.Structure):
@@ -160,6 +161,7 @@ class Subgraph:
         _check(self.lib.byoc_subgraph_create(js, len(js), cs.c, cs.n, int(device), ctypes.byref(h)))
         self.handle = h
         self.device = device
+        self._options = 0
         n_in, n_out = ctypes.c_int32(), ctypes.c_int32()
         _check(self.lib.byoc_subgraph_num_io(h, ctypes.byref(n_in), ctypes.byref(n_out)))
         self.n_in, self.n_out = n_in.value, n_out.value
@@ -202,9 +204,20 @@ class Subgraph:
         _check(self.lib.byoc_subgraph_run(self.handle, ins, len(inputs), outs, len(outputs),
                                           ctypes.c_void_p(s)))
 
-    def set_options(self, graph_replay=False):
-        """Enable or disable HIP-graph replay of the launch sequence."""
-        _check(self.lib.byoc_subgraph_set_options(self.handle, OPT_GRAPH_REPLAY if graph_replay else 0))
+    def set_options(self, graph_replay=None, autotune=None):
+        """Turn engine options on or off; None keeps an option as it is.
+
+        graph_replay: HIP-graph replay of the launch sequence.
+        autotune: time the result-identical kernel variants of every conv /
+        dense composite on the device now and keep the fastest (off restores
+        the built-in choice)."""
+        flags = self._options
+        if graph_replay is not None:
+            flags = (flags | OPT_GRAPH_REPLAY) if graph_replay else (flags & ~OPT_GRAPH_REPLAY)
+        if autotune is not None:
+            flags = (flags | OPT_AUTOTUNE) if autotune else (flags & ~OPT_AUTOTUNE)
+        _check(self.lib.byoc_subgraph_set_options(self.handle, flags))
+        self._options = flags
 
     def profile_begin(self, max_runs):
         _check(self.lib.byoc_subgraph_profile_begin(self.handle, int(max_runs)))

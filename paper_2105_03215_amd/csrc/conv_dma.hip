@@ -1,0 +1,474 @@
+// Implicit-GEMM convolution on CDNA4 bf16 MFMA with a direct HBM->LDS
+// pipeline (buffer_load_dwordx4 ... lds).
+//
+// The conv composite y[n,p,q,k] = act(sum_{r,s,c} x[n, p*sh-pt+r, q*sw-pl+s, c]
+// * w[k,r,s,c] + b[k] + res[n,p,q,k]) is a GEMM with M = N*P*Q output
+// pixels, N = K output channels and a reduction of length R*S*C.  With NHWC
+// activations and weights packed K-major with kk = (r*S+s)*Cp + c, a row of
+// either operand is contiguous along the reduction: every lane moves 16 bytes
+// (8 bf16, one MFMA operand register) per load.  Dense layers run through the
+// same kernel as 1x1 convs on 1x1 images.
+//
+// Workgroup: 256 threads = 4 waves, tile BM pixels x BN channels, 64
+// reduction elements per stage.  The operand tiles of NS stages live in NS
+// LDS buffers; the loads of stage t+NS-1 are issued (straight into LDS, no
+// registers) before the MFMAs of stage t, so NS-1 stages of loads are in
+// flight while the matrix cores work.  Each buffer is its own __shared__
+// array: the compiler then knows which pending LDS fills a read depends on
+// and waits only for those; the wait before the one barrier per stage is
+// explicit.  An out-of-range buffer offset fills zeros, which supplies the
+// conv padding and the ragged pixel/reduction tails without branches.
+//
+// LDS rows are 128 bytes (8 chunks of 16 B).  A load instruction fills 8
+// consecutive rows (lane l -> row l/8, slot l%8), so the swizzle that keeps
+// MFMA operand reads conflict-free (logical chunk ch of row rw at slot
+// ch ^ (rw & 7)) is applied on the fetch side: lane l fetches logical chunk
+// (l%8) ^ (l/8).
+//
+// The weights are the MFMA A operand and the pixels the B operand, so each
+// lane's 4 accumulators hold 4 consecutive output channels of one pixel.  The
+// epilogue stages fp32 results through LDS in 32-channel passes so that each
+// thread finishes 8 consecutive channels of one pixel (bias, residual,
+// activation, bf16 rounding fused) with one 16-byte store.  With split-K each
+// split writes fp32 partials and a second kernel reduces them in a fixed
+// order.
+#include <type_traits>
+
+#include "device_common.h"
+
+namespace byoc {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+
+constexpr int kBK = 64;                 // reduction elements per stage
+constexpr int kCH = kBK / 8;            // 16-byte chunks per tile row
+constexpr int kNT = 256;                // threads per workgroup
+constexpr int kRowsPerPass = kNT / kCH;  // rows one load instruction of every wave covers
+constexpr int kBufferFlags = 0x00020000;  // raw (untyped) buffer access, gfx9 word 3
+constexpr uint32_t kOOB = 0x80000000u;    // offset past any buffer: reads zeros
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+// Raw buffer resource (base, stride 0, num_records = bytes): offsets at or
+// past `bytes` read zeros.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int bytes) {
+  const uint64_t a = (uint64_t)base;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32) & 0xFFFF);
+  r[2] = __builtin_amdgcn_readfirstlane(bytes);
+  r[3] = kBufferFlags;
+  return r;
+}
+
+// 16 bytes per lane from a buffer straight into LDS: lane l writes bytes
+// [16 l, 16 l + 16) after the wave-uniform LDS address.  Written as inline
+// assembly so that the compiler neither tracks these fills (the kernel
+// waits for them itself, per stage, before its barrier) nor inserts
+// conservative waits for them in front of unrelated LDS reads.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_fill16(i32x4 rsrc, uint32_t lds_addr, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+
+template <int BM, int BN, int WM, int WN, int NS, bool ALIGNED, bool SPLIT>
+__global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
+  static_assert(WM * WN == 4, "4 waves");
+  static_assert(NS >= 2 && NS <= 4, "stages");
+  constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
+  constexpr int TM = WTM / 16, TN = WTN / 16;  // 16x16 MFMA tiles per wave
+  constexpr int AR = BM / kRowsPerPass, BR = BN / kRowsPerPass;
+  static_assert(TM >= 1 && TN >= 1 && AR >= 1 && BR >= 1, "tile too small");
+  constexpr int LPS = AR + BR;  // load instructions per thread per stage
+  constexpr int STAGE = (BM + BN) * kCH;  // uint4 per stage buffer
+
+  __shared__ uint4 lds0[STAGE];
+  __shared__ uint4 lds1[STAGE];
+  __shared__ uint4 lds2[NS > 2 ? STAGE : 1];
+  __shared__ uint4 lds3[NS > 3 ? STAGE : 1];
+  auto buf = [&](auto tag) -> uint4* {
+    constexpr int S = decltype(tag)::value;
+    if constexpr (S == 0) return lds0;
+    else if constexpr (S == 1) return lds1;
+    else if constexpr (S == 2) return lds2;
+    else return lds3;
+  };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int r0 = tid / kCH;                       // first row this thread fills
+  const int cv = (lane & 7) ^ ((lane >> 3) & 7);  // logical chunk it fetches
+
+  // Tile placement: the hardware deals workgroups round-robin to the 8
+  // XCDs (block b runs on XCD b % 8).  With xcd_py > 0 every XCD owns one
+  // block of a (8 / xcd_py) x xcd_py partition of the tile grid and walks it
+  // channel tile fastest; the grid is padded to 8 equal shares and surplus
+  // workgroups exit at once.  Otherwise each XCD gets a contiguous run of
+  // the row-major tile order.
+  const int ntn = (p.Kp + BN - 1) / BN;
+  const int ntm = (p.M + BM - 1) / BM;
+  int tm, tn;
+  if (p.xcd_py > 0) {
+    const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+    const int py = p.xcd_py, px = 8 / py;
+    const int gx = x / py, gy = x - (x / py) * py;
+    const int m_lo = gx * ntm / px, m_hi = (gx + 1) * ntm / px;
+    const int n_lo = gy * ntn / py, n_hi = (gy + 1) * ntn / py;
+    const int nh = n_hi - n_lo;
+    if (nh <= 0 || j >= (m_hi - m_lo) * nh) return;
+    tm = m_lo + j / nh;
+    tn = n_lo + j % nh;
+  } else {
+    int bid = blockIdx.x;
+    const int nb = gridDim.x;
+    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+    tn = bid % ntn;
+    tm = bid / ntn;
+  }
+  const int m0 = tm * BM;
+  const int n0 = tn * BN;
+
+  const int nk_total = (p.Kg + kBK - 1) / kBK;
+  int kt_begin = 0, kt_end = nk_total;
+  if (SPLIT) {
+    kt_begin = blockIdx.y * p.k_tiles_per_split;
+    kt_end = min(nk_total, kt_begin + p.k_tiles_per_split);
+  }
+
+  // Activation rows of this thread.  Aligned path (Cp % 64 == 0, a stage is
+  // 64 channels of one tap): pix = element offset of the row's window origin
+  // plus this thread's chunk, tapmask bit r*S+s set when that tap lies inside
+  // the image.  Non-aligned path: the window origin.
+  int pix[AR], a_ih[AR], a_iw[AR];
+  uint32_t tapmask[AR];
+  const int PQ = p.P * p.Q;
+#pragma unroll
+  for (int i = 0; i < AR; ++i) {
+    const int m = m0 + r0 + i * kRowsPerPass;
+    int ih0 = -(1 << 28), iw0 = 0, n = 0;  // rows past M: never inside the image
+    if (m < p.M) {
+      n = m / PQ;
+      const int pq = m - n * PQ;
+      const int pp = pq / p.Q;
+      const int qq = pq - pp * p.Q;
+      ih0 = pp * p.sh - p.pt;
+      iw0 = qq * p.sw - p.pl;
+    }
+    a_ih[i] = ih0;
+    a_iw[i] = iw0;
+    pix[i] = m < p.M ? ((n * p.H + ih0) * p.W + iw0) * p.Cp : 0;
+    if (ALIGNED) {
+      pix[i] += cv * 8;
+      uint32_t mask = 0;
+      for (int r = 0; r < p.R; ++r)
+        for (int s = 0; s < p.S; ++s)
+          if ((unsigned)(ih0 + r) < (unsigned)p.H && (unsigned)(iw0 + s) < (unsigned)p.W)
+            mask |= 1u << (r * p.S + s);
+      tapmask[i] = mask;
+    }
+  }
+  const i32x4 xr = buffer_rsrc(p.x, p.x_bytes);
+  const i32x4 wr = buffer_rsrc(p.w, p.w_bytes);
+  uint32_t wvoff[BR];  // byte offset of this thread's weight rows and chunk
+#pragma unroll
+  for (int i = 0; i < BR; ++i) wvoff[i] = (uint32_t)(((n0 + r0 + i * kRowsPerPass) * p.Kgp + cv * 8) * 2);
+
+  // Reduction position of the next stage to load: tap (r, s), channel c,
+  // flattened index kk (non-aligned path: this thread's own chunk) and the
+  // packed-weight column.
+  int r, s, c, kk, wcol;
+  {
+    const int kk0 = kt_begin * kBK + (ALIGNED ? 0 : cv * 8);
+    const int rs = kk0 / p.Cp;
+    c = kk0 - rs * p.Cp;
+    r = rs / p.S;
+    s = rs - r * p.S;
+    kk = kk0;
+    wcol = kt_begin * kBK;
+  }
+
+  // Issues the loads of the next stage into buffer SET and advances the
+  // position.  Every step issues the same number of loads, also past the end
+  // of this split's reduction (those read zeros from an out-of-range offset
+  // and are never computed), which keeps the count of loads in flight fixed.
+  int kleft = kt_end - kt_begin;
+  auto issue = [&](auto set_tag) {
+    uint4* dst = buf(set_tag);
+    const bool live = kleft-- > 0;
+    const int tap = (r * p.W + s) * p.Cp + c;
+    const int bit = (r * p.S + s) & 31;
+    const bool kval = live && (ALIGNED || kk < p.Kg);
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+      bool ok;
+      if (ALIGNED) {
+        ok = live && ((tapmask[i] >> bit) & 1u);
+      } else {
+        const int ih = a_ih[i] + r;
+        const int iw = a_iw[i] + s;
+        ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+      }
+      const uint32_t off = ok ? (uint32_t)(pix[i] + tap) * 2u : kOOB;
+      lds_fill16(xr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (i * kRowsPerPass + wave * 8) * kCH)), off);
+    }
+    const uint32_t wc = (uint32_t)wcol * 2u;
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+      lds_fill16(wr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (BM + i * kRowsPerPass + wave * 8) * kCH)),
+                 live ? wvoff[i] + wc : kOOB);
+    wcol += kBK;
+    c += kBK;
+    if (ALIGNED) {
+      if (c == p.Cp) {
+        c = 0;
+        if (++s == p.S) {
+          s = 0;
+          ++r;
+        }
+      }
+    } else {
+      kk += kBK;
+      while (c >= p.Cp) {
+        c -= p.Cp;
+        if (++s == p.S) {
+          s = 0;
+          ++r;
+        }
+      }
+    }
+  };
+
+  f32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // One stage from LDS: 2 k-steps of the 16x16x32 MFMA.  Lane l reads 16
+  // bytes (8 consecutive reduction elements) of row l % 16 at chunk
+  // (k-step, l / 16).
+  auto compute = [&](auto set_tag) {
+    const uint4* sA = buf(set_tag);
+    const uint4* sB = sA + BM * kCH;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      const int chunk = ks * 4 + (lane >> 4);
+      bf16x8 af[TN], bfr[TM];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int row = wn * WTN + i * 16 + (lane & 15);
+        af[i] = as_bf16x8(sB[row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * WTM + j * 16 + (lane & 15);
+        bfr[j] = as_bf16x8(sA[row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  // Epilogue operands (bias and residual of the 8 channels this thread
+  // finishes per pass) are fetched before the main loop so that their
+  // latency overlaps the reduction.
+  constexpr int kEC = 32;  // channels per epilogue pass
+  constexpr int NPASS = BN / kEC;
+  constexpr int TPP = kEC / 8;  // threads per pixel
+  constexpr int EPV = (BM * TPP + kNT - 1) / kNT;  // pixels per thread per pass
+  const int ec8 = (tid % TPP) * 8;
+  uint4 resv[SPLIT ? 1 : NPASS][EPV];
+  float4 biasv[SPLIT ? 1 : NPASS][2];
+  if (!SPLIT) {
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16_t*>(p.res), (short)0, p.res ? p.res_bytes : 0, kBufferFlags);
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int k = n0 + pass * kEC + ec8;
+      if (p.bias) {
+        biasv[pass][0] = *(const float4*)(p.bias + k);
+        biasv[pass][1] = *(const float4*)(p.bias + k + 4);
+      } else {
+        biasv[pass][0] = biasv[pass][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) {
+        const int px = (tid + q * kNT) / TPP;
+        const int m = m0 + px;
+        const uint32_t off =
+            (px < BM && m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) * 2u : kOOB;
+        resv[pass][q] = p.res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0))
+                              : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+  }
+
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  const int nkt = kt_end - kt_begin;
+
+  // Stage t lives in buffer t % NS.  Before computing it: wait for this
+  // thread's fills of stage t (the NS-2 younger stages may stay in flight)
+  // and for its own LDS reads, then barrier so every wave's fills are
+  // visible and every wave is done with stage t-1, whose buffer the fills
+  // of stage t+NS-1 then reuse.
+  auto step = [&](auto cur, auto nxt) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 2) * LPS) : "memory");
+    issue(nxt);
+    compute(cur);
+  };
+
+  issue(S0{});
+  if constexpr (NS > 2) issue(S1{});
+  if constexpr (NS > 3) issue(S2{});
+  // full groups of NS stages (stage t in buffer t % NS), then the tail
+  int t = 0;
+  for (; t + NS <= nkt; t += NS) {
+    if constexpr (NS == 2) {
+      step(S0{}, S1{});
+      step(S1{}, S0{});
+    } else if constexpr (NS == 3) {
+      step(S0{}, S2{});
+      step(S1{}, S0{});
+      step(S2{}, S1{});
+    } else {
+      step(S0{}, S3{});
+      step(S1{}, S0{});
+      step(S2{}, S1{});
+      step(S3{}, S2{});
+    }
+  }
+  const int rem = nkt - t;
+  if (rem > 0) {
+    if constexpr (NS == 2) step(S0{}, S1{});
+    else if constexpr (NS == 3) step(S0{}, S2{});
+    else step(S0{}, S3{});
+  }
+  if constexpr (NS > 2) {
+    if (rem > 1) step(S1{}, S0{});
+  }
+  if constexpr (NS > 3) {
+    if (rem > 2) step(S2{}, S1{});
+  }
+  // all fills (including the zero fills past the end) landed, all waves
+  // done reading the operand buffers
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  if (SPLIT) {
+    // fp32 partials of this split: accumulator elements are 4 consecutive
+    // channels (4 (lane/16) + e) of pixel lane % 16
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+        const int k = n0 + wn * WTN + i * 16 + 4 * (lane >> 4);
+        if (m >= p.M || k >= p.Kp) continue;
+        const f32x4 a = acc[i][j];
+        *(float4*)(p.partial + ((size_t)blockIdx.y * p.M + m) * p.Kp + k) = make_float4(a[0], a[1], a[2], a[3]);
+      }
+    return;
+  }
+
+  // Epilogue through LDS (buffer 0 as a [BM][kEC + 4] fp32 tile; the pad
+  // puts the 16 pixels of one accumulator write on distinct banks).
+  constexpr int kLd = kEC + 4;
+  static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
+  float* stage = reinterpret_cast<float*>(lds0);
+#pragma unroll
+  for (int pass = 0; pass < NPASS; ++pass) {
+    if (pass > 0) __syncthreads();
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int ch = wn * WTN + i * 16 + 4 * (lane >> 4) - pass * kEC;
+      if (ch < 0 || ch >= kEC) continue;
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int px = wm * WTM + j * 16 + (lane & 15);
+        const f32x4 a = acc[i][j];
+        *(float4*)(stage + px * kLd + ch) = make_float4(a[0], a[1], a[2], a[3]);
+      }
+    }
+    __syncthreads();
+    const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+    for (int q = 0; q < EPV; ++q) {
+      const int px = (tid + q * kNT) / TPP;
+      const int m = m0 + px;
+      if (px >= BM || m >= p.M || k >= p.Kp) continue;
+      float f[8], rv[8];
+      const float4 lo = *(const float4*)(stage + px * kLd + ec8);
+      const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
+      const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
+      unpack8(resv[pass][q], rv);
+      f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
+      f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = apply_act(f[e] + rv[e], p.act);
+      *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int NS>
+hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
+  const int ntm = (p.M + BM - 1) / BM;
+  const int ntn = (p.Kp + BN - 1) / BN;
+  const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
+  const bool split = p.splits > 1;
+  int blocks = ntm * ntn;
+  if (p.xcd_py > 0) {
+    const int py = p.xcd_py, px = 8 / py;
+    blocks = 8 * ((ntm + px - 1) / px) * ((ntn + py - 1) / py);
+  }
+  dim3 grid(blocks, split ? p.splits : 1);
+  if (aligned && !split) conv_dma_kernel<BM, BN, WM, WN, NS, true, false><<<grid, kNT, 0, s>>>(p);
+  else if (aligned) conv_dma_kernel<BM, BN, WM, WN, NS, true, true><<<grid, kNT, 0, s>>>(p);
+  else if (!split) conv_dma_kernel<BM, BN, WM, WN, NS, false, false><<<grid, kNT, 0, s>>>(p);
+  else conv_dma_kernel<BM, BN, WM, WN, NS, false, true><<<grid, kNT, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
+  if (ns == 2) return launch_tile<BM, BN, WM, WN, 2>(p, s);
+  if (ns == 3) return launch_tile<BM, BN, WM, WN, 3>(p, s);
+  if (ns == 4) return launch_tile<BM, BN, WM, WN, 4>(p, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool conv_dma_tile_supported(int bm, int bn, int stages) {
+  if (stages < 2 || stages > 4) return false;
+  return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
+         (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+}
+
+hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, hipStream_t s) {
+  if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2>(p, stages, s);
+  if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2>(p, stages, s);
+  if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 2>(p, stages, s);
+  if (bm == 64 && bn == 64) return launch_stages<64, 64, 2, 2>(p, stages, s);
+  if (bm == 32 && bn == 64) return launch_stages<32, 64, 1, 4>(p, stages, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace byoc

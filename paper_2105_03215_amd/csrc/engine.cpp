@@ -64,16 +64,29 @@ void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* 
 }
 
 // Tuning override (environment, read at engine creation):
-// BYOC_CONV_TILE=<bm>x<bn>[x<mfma 16|32>] forces a compiled tile, BYOC_CONV_SPLIT=<n> a
+// BYOC_CONV_TILE=<bm>x<bn>[x<mfma 16|32>] (register-staged) or d<bm>x<bn>s<stages>
+// (HBM->LDS pipeline) forces a compiled tile, BYOC_CONV_SPLIT=<n> a
 // split-K factor, for every conv/dense composite of the engine.
 void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
   if (const char* e = std::getenv("BYOC_CONV_TILE")) {
     int bm = 0, bn = 0, mf = 16;
-    const int got = std::sscanf(e, "%dx%dx%d", &bm, &bn, &mf);
-    if (got >= 2 && conv_mfma_tile_supported(bm, bn, mf)) {
-      t->bm = bm;
-      t->bn = bn;
-      t->mf = mf;
+    int ns = 0;
+    if (e[0] == 'd') {
+      // d<bm>x<bn>s<stages>: direct HBM->LDS pipeline
+      if (std::sscanf(e + 1, "%dx%ds%d", &bm, &bn, &ns) == 3 && conv_dma_tile_supported(bm, bn, ns)) {
+        t->bm = bm;
+        t->bn = bn;
+        t->mf = 16;
+        t->stages = ns;
+      }
+    } else {
+      const int got = std::sscanf(e, "%dx%dx%d", &bm, &bn, &mf);
+      if (got >= 2 && conv_mfma_tile_supported(bm, bn, mf)) {
+        t->bm = bm;
+        t->bn = bn;
+        t->mf = mf;
+        t->stages = 0;
+      }
     }
   }
   if (const char* e = std::getenv("BYOC_CONV_SPLIT")) {
@@ -82,6 +95,40 @@ void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
     *kps = (nk + sp - 1) / sp;
     *splits = (nk + *kps - 1) / *kps;
   }
+}
+
+// XCD placement of conv_dma tiles: the (8 / py) x py split of the tile grid
+// that minimises one XCD's working set (its share of the input activations
+// plus its share of the packed weights), so that each XCD's L2 serves the
+// re-reads of its tiles.  BYOC_CONV_XCD=<py> (0 = linear order) overrides.
+int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
+  if (const char* e = std::getenv("BYOC_CONV_XCD")) {
+    const int v = std::atoi(e);
+    if (v == 0 || v == 1 || v == 2 || v == 4 || v == 8) return v;
+  }
+  const int64_t ntm = (p.M + t.bm - 1) / t.bm, ntn = (p.Kp + t.bn - 1) / t.bn;
+  const double a = (double)p.x_bytes, w = (double)p.Kp * p.Kg * 2.0;
+  int best = 0;
+  double best_ws = 0;
+  for (int py : {1, 2, 4, 8}) {
+    const int px = 8 / py;
+    if (py > ntn || px > ntm) continue;
+    const double ws = a / px + w / py;
+    if (best == 0 || ws < best_ws) {
+      best = py;
+      best_ws = ws;
+    }
+  }
+  return best;
+}
+
+void name_conv(Launch& L) {
+  if (L.tile.stages > 0)
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_dma_%dx%d_s%d_split%d", L.tile.bm, L.tile.bn,
+                  L.tile.stages, L.conv.splits);
+  else
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_mf%d_split%d", L.tile.bm, L.tile.bn,
+                  L.tile.mf, L.conv.splits);
 }
 
 struct Planner {
@@ -331,10 +378,11 @@ void Planner::plan_node(int ni) {
     apply_tile_override(p.Kg, &L.tile, &splits, &kps);
     p.splits = splits;
     p.k_tiles_per_split = kps;
+    p.xcd_py = L.tile.stages > 0 ? choose_xcd_split(p, L.tile) : 0;
+    L.tile_default = L.tile;
     L.op = Launch::ConvMfma;
     L.info.kind = BYOC_K_CONV_MFMA;
-    std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_mf%d_split%d", L.tile.bm,
-                  L.tile.bn, L.tile.mf, splits);
+    name_conv(L);
     if (splits > 1) {
       L.partial = arena((int64_t)splits * p.M * Kp * 4);
       Launch Rd = L;
@@ -477,7 +525,9 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.res = (const bf16_t*)c.ptr(L.res);
       p.y = (bf16_t*)c.ptr(L.y);
       p.partial = (float*)c.ptr(L.partial);
-      return L.op == Launch::ConvMfma ? launch_conv_mfma(p, L.tile, c.s) : launch_splitk_reduce(p, c.s);
+      if (L.op == Launch::SplitReduce) return launch_splitk_reduce(p, c.s);
+      return L.tile.stages > 0 ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, c.s)
+                               : launch_conv_mfma(p, L.tile, c.s);
     }
     case Launch::ConvF32: {
       ConvF32Params p = L.cf;
@@ -696,11 +746,129 @@ Status run_graph(Engine* e, const RunCtx& c, int32_t n_in, int32_t n_out) {
 
 }  // namespace
 
+namespace {
+
+// Result-identical kernel variants of one conv launch: every variant keeps
+// the 16x16x32 MFMA and the reduction order of the built-in choice, so only
+// the speed differs.  Split-K launches keep their plan.
+std::vector<ConvTile> conv_candidates(const Launch& L) {
+  std::vector<ConvTile> c;
+  c.push_back(L.tile_default);
+  if (L.conv.splits > 1 || L.tile_default.mf != 16) return c;
+  const ConvParams& p = L.conv;
+  const int bms[] = {32, 64, 128}, bns[] = {64, 128};
+  for (int bm : bms)
+    for (int bn : bns) {
+      if (bm == 32 && bn == 128) continue;
+      if (bm == 32 && p.M >= 48) continue;
+      if (bm == 128 && p.M < 4096) continue;
+      if (bn == 128 && p.Kp < 128) continue;
+      for (int ns = 2; ns <= 4; ++ns) {
+        if (!conv_dma_tile_supported(bm, bn, ns)) continue;
+        if ((bm + bn) * 128 * ns > 131072) continue;
+        ConvTile t;
+        t.bm = bm;
+        t.bn = bn;
+        t.mf = 16;
+        t.stages = ns;
+        c.push_back(t);
+      }
+    }
+  return c;
+}
+
+void apply_tile(Launch& L, const ConvTile& t) {
+  L.tile = t;
+  L.conv.xcd_py = t.stages > 0 ? choose_xcd_split(L.conv, t) : 0;
+  name_conv(L);
+}
+
+struct DevBuf {
+  void* p = nullptr;
+  ~DevBuf() {
+    if (p) (void)hipFree(p);
+  }
+};
+
+Status autotune(Engine* e) {
+  const Graph& g = e->graph;
+  std::vector<DevBuf> ins(g.inputs.size()), outs(g.outputs.size());
+  std::vector<const void*> in_ptr(g.inputs.size());
+  std::vector<void*> out_ptr(g.outputs.size());
+  for (size_t i = 0; i < g.inputs.size(); ++i) {
+    const IoDesc& io = g.inputs[i];
+    const int64_t bytes = numel(g.values[io.value].shape) * (io.dtype == DType::BF16 ? 2 : 4);
+    HIP_TRY(hipMalloc(&ins[i].p, (size_t)std::max<int64_t>(bytes, 16)), "autotune hipMalloc");
+    HIP_TRY(hipMemset(ins[i].p, 0, (size_t)std::max<int64_t>(bytes, 16)), "autotune hipMemset");
+    in_ptr[i] = ins[i].p;
+  }
+  for (size_t i = 0; i < g.outputs.size(); ++i) {
+    const IoDesc& io = g.outputs[i];
+    const int64_t bytes = numel(g.values[io.value].shape) * (io.dtype == DType::BF16 ? 2 : 4);
+    HIP_TRY(hipMalloc(&outs[i].p, (size_t)std::max<int64_t>(bytes, 16)), "autotune hipMalloc");
+    out_ptr[i] = outs[i].p;
+  }
+  hipStream_t s = nullptr;
+  HIP_TRY(hipStreamCreate(&s), "autotune hipStreamCreate");
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  hipError_t err = hipEventCreate(&ev0);
+  if (err == hipSuccess) err = hipEventCreate(&ev1);
+  RunCtx c{e, in_ptr.data(), out_ptr.data(), s};
+  // the arena holds whatever the last run left: the timing does not depend on values
+  for (size_t i = 0; i < e->launches.size() && err == hipSuccess; ++i) {
+    Launch& L = e->launches[i];
+    if (L.op != Launch::ConvMfma) continue;
+    const std::vector<ConvTile> cand = conv_candidates(L);
+    if (cand.size() < 2) continue;
+    float best_ms = 0;
+    ConvTile best = L.tile_default;
+    for (size_t k = 0; k < cand.size() && err == hipSuccess; ++k) {
+      Launch T = L;
+      apply_tile(T, cand[k]);
+      for (int w = 0; w < 2 && err == hipSuccess; ++w) err = exec(T, c);
+      if (err == hipSuccess) err = hipEventRecord(ev0, s);
+      constexpr int kReps = 5;
+      for (int r = 0; r < kReps && err == hipSuccess; ++r) err = exec(T, c);
+      if (err == hipSuccess) err = hipEventRecord(ev1, s);
+      if (err == hipSuccess) err = hipEventSynchronize(ev1);
+      float ms = 0;
+      if (err == hipSuccess) err = hipEventElapsedTime(&ms, ev0, ev1);
+      if (err == hipSuccess && (k == 0 || ms < best_ms)) {
+        best_ms = ms;
+        best = cand[k];
+      }
+    }
+    if (err == hipSuccess) apply_tile(L, best);
+  }
+  hipError_t serr = hipStreamSynchronize(s);
+  if (ev0) (void)hipEventDestroy(ev0);
+  if (ev1) (void)hipEventDestroy(ev1);
+  (void)hipStreamDestroy(s);
+  if (err == hipSuccess) err = serr;
+  if (err != hipSuccess) {
+    for (Launch& L : e->launches)
+      if (L.op == Launch::ConvMfma) apply_tile(L, L.tile_default);
+    return Status::Err(BYOC_ERR_DEVICE, std::string("autotune: ") + hipGetErrorString(err));
+  }
+  return Status::Ok();
+}
+
+}  // namespace
+
 Status engine_set_options(Engine* e, int flags) {
-  if (flags & ~BYOC_OPT_GRAPH_REPLAY)
+  if (flags & ~(BYOC_OPT_GRAPH_REPLAY | BYOC_OPT_AUTOTUNE))
     return Status::Err(BYOC_ERR_INVALID_ARG, "unknown option bits " + std::to_string(flags));
   DeviceGuard guard(e->device);
-  if (!(flags & BYOC_OPT_GRAPH_REPLAY)) drop_graph(e);
+  const bool tune_on = (flags & BYOC_OPT_AUTOTUNE) && !(e->options & BYOC_OPT_AUTOTUNE);
+  const bool tune_off = !(flags & BYOC_OPT_AUTOTUNE) && (e->options & BYOC_OPT_AUTOTUNE);
+  if (!(flags & BYOC_OPT_GRAPH_REPLAY) || tune_on || tune_off) drop_graph(e);
+  if (tune_on) {
+    Status st = autotune(e);
+    if (!st.ok()) return st;
+  }
+  if (tune_off)
+    for (Launch& L : e->launches)
+      if (L.op == Launch::ConvMfma) apply_tile(L, L.tile_default);
   e->options = flags;
   return Status::Ok();
 }

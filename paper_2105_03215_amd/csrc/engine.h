@@ -30,6 +30,7 @@ struct Launch {
   Ref x, w, bias, res, y, partial, other;
   ConvParams conv{};
   ConvTile tile{};
+  ConvTile tile_default{};  // built-in choice (autotune may replace `tile`)
   ConvF32Params cf{};
   DwParams dw{};
   PoolParams pool{};

@@ -36,16 +36,24 @@ struct ConvParams {
   int x_bytes;  // extent of x, w and res in bytes (buffer-load range; < 2^31)
   int w_bytes;
   int res_bytes;
+  // conv_dma tile placement: > 0 splits the tile grid into (8 / xcd_py) x
+  // xcd_py blocks along (pixels, channels), one per XCD, so that an XCD's L2
+  // holds only its share of both operands; 0 deals tiles out linearly.
+  int xcd_py;
 };
 
 struct ConvTile {
-  int bm, bn;   // pixels x channels per workgroup
-  int mf = 16;  // MFMA shape: 16 (16x16x32) or 32 (32x32x16)
+  int bm, bn;       // pixels x channels per workgroup
+  int mf = 16;      // MFMA shape: 16 (16x16x32) or 32 (32x32x16)
+  int stages = 0;   // > 0: HBM->LDS pipeline of that many stages (conv_dma)
 };
 
 // Tile configurations with a compiled kernel.
 bool conv_mfma_tile_supported(int bm, int bn, int mf);
 hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
+// Direct HBM->LDS pipelined variant (16x16x32 MFMA only).
+bool conv_dma_tile_supported(int bm, int bn, int stages);
+hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, hipStream_t s);
 // Sums split-K partials in a fixed order and applies bias, residual, act.
 hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s);
 

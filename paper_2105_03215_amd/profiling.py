@@ -24,7 +24,7 @@ import os
 import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-CONV_KERNELS = ("conv_mfma_kernel", "splitk_reduce_kernel")
+CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "splitk_reduce_kernel")
 RUN_MARKER = "nchw_to_nhwc_kernel"  # one dispatch per run of the CNN subgraphs
 
 
@@ -64,9 +64,12 @@ def _copy_kib(path, counter):
 
 
 def conv_kernel_digest():
-    src = os.path.join(ROOT, "paper_2105_03215_amd", "csrc", "conv_mfma.hip")
-    with open(src, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Digest of the conv kernel sources and of the planner that picks them."""
+    h = hashlib.sha256()
+    for name in ("conv_mfma.hip", "conv_dma.hip", "engine.cpp"):
+        with open(os.path.join(ROOT, "paper_2105_03215_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic(fetch, write, copy_fetch, copy_write, copy_mib, workload, out):

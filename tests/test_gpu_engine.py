@@ -192,3 +192,38 @@ def test_graph_replay_matches_eager():
         sg.set_options(graph_replay=False)
     finally:
         sg.close()
+
+
+@pytest.mark.parametrize("name", ["resnet18_block", "resnet50_bs2", "bert_ffn"])
+def test_autotune_keeps_results_bitwise(name):
+    """Autotune swaps conv kernel variants only among result-identical ones:
+    outputs stay bit-for-bit those of the built-in choice, also under graph
+    replay, and turning it off restores the built-in launch plan."""
+    announce("autotune " + name)
+    if name == "resnet18_block":
+        wl = workloads.resnet18_block(n=2, c=64, hw=28)
+    elif name == "resnet50_bs2":
+        wl = workloads.build("resnet50_v1", n=2)
+    else:
+        wl = workloads.bert_ffn(batch=1, seq=40, layers=1)
+    sg = capi.Subgraph(wl.graph, wl.consts)
+    s = torch.cuda.Stream(device=DEV)
+    try:
+        ins = runtime.inputs_for(sg, wl.inputs, DEV)
+        ref = runtime.outputs_for(sg, DEV)
+        sg.run(ins, ref, s)
+        s.synchronize()
+        names0 = [l["name"] for l in sg.launches()]
+        sg.set_options(autotune=True)
+        for replay in (False, True):
+            sg.set_options(graph_replay=replay)
+            out = runtime.outputs_for(sg, DEV)
+            sg.run(ins, out, s)
+            sg.run(ins, out, s)
+            s.synchronize()
+            for a, b in zip(ref, out):
+                assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (name, replay)
+        sg.set_options(graph_replay=False, autotune=False)
+        assert [l["name"] for l in sg.launches()] == names0
+    finally:
+        sg.close()
