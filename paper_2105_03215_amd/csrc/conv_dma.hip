@@ -104,6 +104,7 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
     else return lds3;
   };
 
+  materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -121,21 +122,22 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
   const int ntm = (p.M + BM - 1) / BM;
   int tm, tn;
   if (p.xcd_py > 0) {
+    // XCD x = (gx, gy) owns m tiles [gx*mh, gx*mh + mh) and n tiles
+    // [gy*nh, gy*nh + nh) of the grid (clipped at its edge); mg_tile divides by nh
     const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
-    const int py = p.xcd_py, px = 8 / py;
-    const int gx = x / py, gy = x - (x / py) * py;
-    const int m_lo = gx * ntm / px, m_hi = (gx + 1) * ntm / px;
-    const int n_lo = gy * ntn / py, n_hi = (gy + 1) * ntn / py;
-    const int nh = n_hi - n_lo;
-    if (nh <= 0 || j >= (m_hi - m_lo) * nh) return;
-    tm = m_lo + j / nh;
-    tn = n_lo + j % nh;
+    const int lpy = 31 - __builtin_clz(p.xcd_py);  // xcd_py is 1, 2, 4 or 8
+    const int mh = (ntm + (8 >> lpy) - 1) >> (3 - lpy), nh = (ntn + p.xcd_py - 1) >> lpy;
+    const int gx = x >> lpy, gy = x & (p.xcd_py - 1);
+    const int jm = mdiv(j, p.mg_tile);
+    tm = gx * mh + jm;
+    tn = gy * nh + (j - jm * nh);
+    if (jm >= mh || tm >= ntm || tn >= ntn) return;
   } else {
     int bid = blockIdx.x;
-    const int nb = gridDim.x;
+    const int nb = ntm * ntn;  // the launch grid (no kernel-argument fetch)
     if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-    tn = bid % ntn;
-    tm = bid / ntn;
+    tm = mdiv(bid, p.mg_tile);
+    tn = bid - tm * ntn;
   }
   const int m0 = tm * BM;
   const int n0 = tn * BN;
@@ -159,9 +161,9 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
     const int m = m0 + r0 + i * kRowsPerPass;
     int ih0 = -(1 << 28), iw0 = 0, n = 0;  // rows past M: never inside the image
     if (m < p.M) {
-      n = m / PQ;
+      n = mdiv(m, p.mg_pq);
       const int pq = m - n * PQ;
-      const int pp = pq / p.Q;
+      const int pp = mdiv(pq, p.mg_q);
       const int qq = pq - pp * p.Q;
       ih0 = pp * p.sh - p.pt;
       iw0 = qq * p.sw - p.pl;
@@ -191,9 +193,9 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
   int r, s, c, kk, wcol;
   {
     const int kk0 = kt_begin * kBK + (ALIGNED ? 0 : cv * 8);
-    const int rs = kk0 / p.Cp;
+    const int rs = mdiv(kk0, p.mg_cp);
     c = kk0 - rs * p.Cp;
-    r = rs / p.S;
+    r = mdiv(rs, p.mg_s);
     s = rs - r * p.S;
     kk = kk0;
     wcol = kt_begin * kBK;
@@ -394,7 +396,7 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
   float* stage = reinterpret_cast<float*>(lds0);
 #pragma unroll
   for (int pass = 0; pass < NPASS; ++pass) {
-    if (pass > 0) __syncthreads();
+    if (pass > 0) lds_barrier();
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
       const int ch = wn * WTN + i * 16 + 4 * (lane >> 4) - pass * kEC;
@@ -406,7 +408,7 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
         *(float4*)(stage + px * kLd + ch) = make_float4(a[0], a[1], a[2], a[3]);
       }
     }
-    __syncthreads();
+    lds_barrier();
     const int k = n0 + pass * kEC + ec8;
 #pragma unroll
     for (int q = 0; q < EPV; ++q) {
@@ -428,7 +430,8 @@ __global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
 }
 
 template <int BM, int BN, int WM, int WN, int NS>
-hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
+hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
+  ConvParams p = p_in;
   const int ntm = (p.M + BM - 1) / BM;
   const int ntn = (p.Kp + BN - 1) / BN;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
@@ -436,7 +439,11 @@ hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
   int blocks = ntm * ntn;
   if (p.xcd_py > 0) {
     const int py = p.xcd_py, px = 8 / py;
-    blocks = 8 * ((ntm + px - 1) / px) * ((ntn + py - 1) / py);
+    const int mh = (ntm + px - 1) / px, nh = (ntn + py - 1) / py;
+    blocks = 8 * mh * nh;
+    p.mg_tile = magic40(nh);
+  } else {
+    p.mg_tile = magic40(ntn);
   }
   dim3 grid(blocks, split ? p.splits : 1);
   if (aligned && !split) conv_dma_kernel<BM, BN, WM, WN, NS, true, false><<<grid, kNT, 0, s>>>(p);

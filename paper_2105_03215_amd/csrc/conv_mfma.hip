@@ -200,6 +200,7 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   uint4 (*sA)[BM * kCH] = reinterpret_cast<uint4 (*)[BM * kCH]>(smem);
   uint4 (*sB)[BN * kCH] = reinterpret_cast<uint4 (*)[BN * kCH]>(smem + 2 * BM * kCH);
 
+  materialize_args(p);
   L st;
   const int tid = threadIdx.x;
   st.lane = tid & 63;
@@ -213,10 +214,10 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   // stay in one L2).
   const int ntn = (p.Kp + BN - 1) / BN;
   int bid = blockIdx.x;
-  const int nb = gridDim.x;
+  const int nb = ((p.M + BM - 1) / BM) * ntn;  // the launch grid (no kernel-argument fetch)
   if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-  const int tn = bid % ntn;
-  const int tm = bid / ntn;
+  const int tm = mdiv(bid, p.mg_tile);
+  const int tn = bid - tm * ntn;
   const int m0 = tm * BM;
   const int n0 = tn * BN;
 
@@ -235,9 +236,9 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
     const int m = m0 + st.r0 + i * kRowsPerPass;
     int ih0 = -(1 << 28), iw0 = 0, n = 0;  // rows past M: never inside the image
     if (m < p.M) {
-      n = m / PQ;
+      n = mdiv(m, p.mg_pq);
       const int pq = m - n * PQ;
-      const int pp = pq / p.Q;
+      const int pp = mdiv(pq, p.mg_q);
       const int qq = pq - pp * p.Q;
       ih0 = pp * p.sh - p.pt;
       iw0 = qq * p.sw - p.pl;
@@ -264,9 +265,9 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   // thread's 8 channels are added at use)
   {
     const int kk0 = kt_begin * kBK + (ALIGNED ? 0 : st.cv * 8);
-    const int rs = kk0 / p.Cp;
+    const int rs = mdiv(kk0, p.mg_cp);
     st.c = kk0 - rs * p.Cp;
-    st.r = rs / p.S;
+    st.r = mdiv(rs, p.mg_s);
     st.s = rs - st.r * p.S;
     st.kk = kk0;
     st.wcol = kt_begin * kBK;
@@ -362,7 +363,7 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   float* stage = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int pass = 0; pass < NPASS; ++pass) {
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -376,7 +377,7 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
               make_float4(st.acc[i][j][e], st.acc[i][j][e + 1], st.acc[i][j][e + 2], st.acc[i][j][e + 3]);
         }
       }
-    __syncthreads();
+    lds_barrier();
     const int k = n0 + pass * kEC + ec8;
 #pragma unroll
     for (int q = 0; q < EPV; ++q) {
@@ -401,10 +402,10 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
 // in split order, then bias, residual, activation, bf16 rounding.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
   const int k4 = p.Kp / 4;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)p.M * k4) return;
-  const int m = (int)(idx / k4);
-  const int k = (int)(idx - (int64_t)m * k4) * 4;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;  // < M * Kp / 4 < 2^29
+  if (idx >= p.M * k4) return;
+  const int m = mdiv(idx, p.mg_tile);  // mg_tile divides by Kp / 4 here
+  const int k = (idx - m * k4) * 4;
   float4 acc = *(const float4*)(p.partial + (size_t)m * p.Kp + k);
   for (int sp = 1; sp < p.splits; ++sp) {
     const float4 t = *(const float4*)(p.partial + ((size_t)sp * p.M + m) * p.Kp + k);
@@ -433,11 +434,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
 }
 
 template <int BM, int BN, int WM, int WN, int MF>
-hipError_t launch_tile(const ConvParams& p, hipStream_t s) {
+hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
+  ConvParams p = p_in;
   const int ntm = (p.M + BM - 1) / BM;
   const int ntn = (p.Kp + BN - 1) / BN;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
   const bool split = p.splits > 1;
+  p.mg_tile = magic40(ntn);
   dim3 grid(ntm * ntn, split ? p.splits : 1);
   if (aligned && !split) conv_mfma_kernel<BM, BN, WM, WN, MF, true, false><<<grid, kNT, 0, s>>>(p);
   else if (aligned) conv_mfma_kernel<BM, BN, WM, WN, MF, true, true><<<grid, kNT, 0, s>>>(p);
@@ -474,7 +477,9 @@ hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s) {
+hipError_t launch_splitk_reduce(const ConvParams& p_in, hipStream_t s) {
+  ConvParams p = p_in;
+  p.mg_tile = magic40(p.Kp / 4);
   const int64_t n = (int64_t)p.M * (p.Kp / 4);
   splitk_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p);
   return hipGetLastError();

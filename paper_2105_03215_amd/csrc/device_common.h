@@ -52,6 +52,28 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
   return u;
 }
 
+// Pulls every field of the conv parameters into scalar registers at once.
+// Left alone, the compiler fetches kernel arguments lazily where they are
+// first used, which costs several dependent memory round trips spread over
+// the prologue of every workgroup.
+__device__ __forceinline__ void materialize_args(const ConvParams& p) {
+  asm volatile("" ::"s"(p.x), "s"(p.w), "s"(p.bias), "s"(p.res), "s"(p.y), "s"(p.partial));
+  asm volatile("" ::"s"(p.N), "s"(p.H), "s"(p.W), "s"(p.Cp), "s"(p.P), "s"(p.Q), "s"(p.R), "s"(p.S),
+               "s"(p.sh), "s"(p.sw), "s"(p.pt), "s"(p.pl));
+  asm volatile("" ::"s"(p.M), "s"(p.Kp), "s"(p.Kg), "s"(p.Kgp), "s"(p.ldy), "s"(p.ldr), "s"(p.act),
+               "s"(p.splits), "s"(p.k_tiles_per_split), "s"(p.x_bytes), "s"(p.w_bytes), "s"(p.res_bytes),
+               "s"(p.xcd_py));
+  asm volatile("" ::"s"(p.mg_pq), "s"(p.mg_q), "s"(p.mg_cp), "s"(p.mg_s), "s"(p.mg_tile));
+}
+
+// floor(n / d) for 0 <= n with n * d < 2^40, given mg = ceil(2^40 / d).
+__device__ __forceinline__ int mdiv(int n, uint64_t mg) { return (int)(((uint64_t)(uint32_t)n * mg) >> 40); }
+
+// Workgroup barrier that orders LDS accesses only: each wave waits for its
+// own LDS operations, not for its outstanding global stores (the release
+// fence of __syncthreads() would wait for those to be acknowledged).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 }  // namespace byoc

@@ -369,6 +369,17 @@ void Planner::plan_node(int ni) {
     p.x_bytes = (int)xb;
     p.w_bytes = (int)wb;
     p.res_bytes = (int)rb;
+    // index math divides by P*Q, Q, Cp and S with 40-bit reciprocals (exact
+    // while dividend * divisor < 2^40)
+    if ((int64_t)p.M * P * Q >= (int64_t(1) << 40) || (int64_t)p.Kg * Cp >= (int64_t(1) << 40)) {
+      err = Status::Err(BYOC_ERR_UNSUPPORTED, "node " + std::to_string(ni) + " (" + n.composite +
+                                                  "): too many output pixels for the index arithmetic");
+      return;
+    }
+    p.mg_pq = magic40(P * Q);
+    p.mg_q = magic40(Q);
+    p.mg_cp = magic40(Cp);
+    p.mg_s = magic40(S);
     L.w = wslot((int64_t)rows * p.Kgp * 2);
     jobs.push_back({PackJob::ConvW, wc, L.w.off, K, Cg, R, S, Cp, p.Kgp, rows, 0, 0});
     L.bias = wslot((int64_t)rows * 4);

@@ -40,7 +40,15 @@ struct ConvParams {
   // xcd_py blocks along (pixels, channels), one per XCD, so that an XCD's L2
   // holds only its share of both operands; 0 deals tiles out linearly.
   int xcd_py;
+  // Exact division by the runtime divisors of the index math, as
+  // floor(n / d) = (n * mg) >> 40 with mg = ceil(2^40 / d), valid while
+  // n * d < 2^40 (checked when the launch is planned).  Set by the kernel
+  // launchers (the tile divisor depends on the tile shape).
+  uint64_t mg_pq, mg_q, mg_cp, mg_s;
+  uint64_t mg_tile;  // divisor: channel tiles per row of the tile grid (or per XCD block)
 };
+
+inline uint64_t magic40(int d) { return ((uint64_t(1) << 40) + (uint64_t)d - 1) / (uint64_t)d; }
 
 struct ConvTile {
   int bm, bn;       // pixels x channels per workgroup
