@@ -45,8 +45,6 @@ typedef __attribute__((ext_vector_type(4))) int i32x4;
 
 constexpr int kBK = 64;                 // reduction elements per stage
 constexpr int kCH = kBK / 8;            // 16-byte chunks per tile row
-constexpr int kNT = 256;                // threads per workgroup
-constexpr int kRowsPerPass = kNT / kCH;  // rows one load instruction of every wave covers
 constexpr int kBufferFlags = 0x00020000;  // raw (untyped) buffer access, gfx9 word 3
 constexpr uint32_t kOOB = 0x80000000u;    // offset past any buffer: reads zeros
 
@@ -82,8 +80,10 @@ __device__ __forceinline__ void lds_fill16(i32x4 rsrc, uint32_t lds_addr, uint32
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
 template <int BM, int BN, int WM, int WN, int NS, bool ALIGNED, bool SPLIT>
-__global__ __launch_bounds__(kNT) void conv_dma_kernel(ConvParams p) {
-  static_assert(WM * WN == 4, "4 waves");
+__global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
+  static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves");
+  constexpr int kNT = 64 * WM * WN;          // threads per workgroup
+  constexpr int kRowsPerPass = kNT / kCH;    // rows one load instruction of every wave covers
   static_assert(NS >= 2 && NS <= 4, "stages");
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;  // 16x16 MFMA tiles per wave
@@ -446,6 +446,7 @@ hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
     p.mg_tile = magic40(ntn);
   }
   dim3 grid(blocks, split ? p.splits : 1);
+  constexpr int kNT = 64 * WM * WN;
   if (aligned && !split) conv_dma_kernel<BM, BN, WM, WN, NS, true, false><<<grid, kNT, 0, s>>>(p);
   else if (aligned) conv_dma_kernel<BM, BN, WM, WN, NS, true, true><<<grid, kNT, 0, s>>>(p);
   else if (!split) conv_dma_kernel<BM, BN, WM, WN, NS, false, false><<<grid, kNT, 0, s>>>(p);
@@ -455,21 +456,35 @@ hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
 
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
+  constexpr int kStage = (BM + BN) * 128;  // bytes of one ring buffer
   if (ns == 2) return launch_tile<BM, BN, WM, WN, 2>(p, s);
-  if (ns == 3) return launch_tile<BM, BN, WM, WN, 3>(p, s);
-  if (ns == 4) return launch_tile<BM, BN, WM, WN, 4>(p, s);
+  if constexpr (3 * kStage <= 160 * 1024 - 32)
+    if (ns == 3) return launch_tile<BM, BN, WM, WN, 3>(p, s);
+  if constexpr (4 * kStage <= 160 * 1024 - 32)
+    if (ns == 4) return launch_tile<BM, BN, WM, WN, 4>(p, s);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-bool conv_dma_tile_supported(int bm, int bn, int stages) {
+bool conv_dma_tile_supported(int bm, int bn, int stages, int threads) {
   if (stages < 2 || stages > 4) return false;
-  return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
-         (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+  if ((bm + bn) * 128 * stages > 160 * 1024 - 32) return false;  // LDS of the stage ring
+  if (threads == 256)
+    return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
+           (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+  if (threads == 512) return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128);
+  return false;
 }
 
-hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, hipStream_t s) {
+hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s) {
+  if (!conv_dma_tile_supported(bm, bn, stages, threads)) return hipErrorInvalidValue;
+  if (threads == 512) {
+    if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 4>(p, stages, s);
+    if (bm == 128 && bn == 64) return launch_stages<128, 64, 4, 2>(p, stages, s);
+    if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 4>(p, stages, s);
+    return hipErrorInvalidValue;
+  }
   if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2>(p, stages, s);
   if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2>(p, stages, s);
   if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 2>(p, stages, s);

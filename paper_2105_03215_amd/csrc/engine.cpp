@@ -72,12 +72,14 @@ void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
     int bm = 0, bn = 0, mf = 16;
     int ns = 0;
     if (e[0] == 'd') {
-      // d<bm>x<bn>s<stages>: direct HBM->LDS pipeline
-      if (std::sscanf(e + 1, "%dx%ds%d", &bm, &bn, &ns) == 3 && conv_dma_tile_supported(bm, bn, ns)) {
+      // d<bm>x<bn>s<stages>[t<threads>]: direct HBM->LDS pipeline
+      int nt = 256;
+      if (std::sscanf(e + 1, "%dx%ds%dt%d", &bm, &bn, &ns, &nt) >= 3 && conv_dma_tile_supported(bm, bn, ns, nt)) {
         t->bm = bm;
         t->bn = bn;
         t->mf = 16;
         t->stages = ns;
+        t->threads = nt;
       }
     } else {
       const int got = std::sscanf(e, "%dx%dx%d", &bm, &bn, &mf);
@@ -124,8 +126,8 @@ int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
 
 void name_conv(Launch& L) {
   if (L.tile.stages > 0)
-    std::snprintf(L.info.name, sizeof(L.info.name), "conv_dma_%dx%d_s%d_split%d", L.tile.bm, L.tile.bn,
-                  L.tile.stages, L.conv.splits);
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_dma_%dx%d_s%d_w%d_split%d", L.tile.bm, L.tile.bn,
+                  L.tile.stages, L.tile.threads / 64, L.conv.splits);
   else
     std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_mf%d_split%d", L.tile.bm, L.tile.bn,
                   L.tile.mf, L.conv.splits);
@@ -537,7 +539,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.y = (bf16_t*)c.ptr(L.y);
       p.partial = (float*)c.ptr(L.partial);
       if (L.op == Launch::SplitReduce) return launch_splitk_reduce(p, c.s);
-      return L.tile.stages > 0 ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, c.s)
+      return L.tile.stages > 0 ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, c.s)
                                : launch_conv_mfma(p, L.tile, c.s);
     }
     case Launch::ConvF32: {
@@ -768,23 +770,23 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
   if (L.conv.splits > 1 || L.tile_default.mf != 16) return c;
   const ConvParams& p = L.conv;
   const int bms[] = {32, 64, 128}, bns[] = {64, 128};
-  for (int bm : bms)
-    for (int bn : bns) {
-      if (bm == 32 && bn == 128) continue;
-      if (bm == 32 && p.M >= 48) continue;
-      if (bm == 128 && p.M < 4096) continue;
-      if (bn == 128 && p.Kp < 128) continue;
-      for (int ns = 2; ns <= 4; ++ns) {
-        if (!conv_dma_tile_supported(bm, bn, ns)) continue;
-        if ((bm + bn) * 128 * ns > 131072) continue;
-        ConvTile t;
-        t.bm = bm;
-        t.bn = bn;
-        t.mf = 16;
-        t.stages = ns;
-        c.push_back(t);
+  for (int nt : {256, 512})
+    for (int bm : bms)
+      for (int bn : bns) {
+        if (bm == 32 && p.M >= 48) continue;
+        if (bm == 128 && p.M < 4096) continue;
+        if (bn == 128 && p.Kp < 128) continue;
+        for (int ns = 2; ns <= 4; ++ns) {
+          if (!conv_dma_tile_supported(bm, bn, ns, nt)) continue;
+          ConvTile t;
+          t.bm = bm;
+          t.bn = bn;
+          t.mf = 16;
+          t.stages = ns;
+          t.threads = nt;
+          c.push_back(t);
+        }
       }
-    }
   return c;
 }
 
@@ -821,39 +823,53 @@ Status autotune(Engine* e) {
   }
   hipStream_t s = nullptr;
   HIP_TRY(hipStreamCreate(&s), "autotune hipStreamCreate");
-  hipEvent_t ev0 = nullptr, ev1 = nullptr;
-  hipError_t err = hipEventCreate(&ev0);
-  if (err == hipSuccess) err = hipEventCreate(&ev1);
+  const size_t nl = e->launches.size();
+  std::vector<hipEvent_t> ev(nl + 1, nullptr);
+  hipError_t err = hipSuccess;
+  for (size_t i = 0; i <= nl && err == hipSuccess; ++i) err = hipEventCreate(&ev[i]);
   RunCtx c{e, in_ptr.data(), out_ptr.data(), s};
-  // the arena holds whatever the last run left: the timing does not depend on values
-  for (size_t i = 0; i < e->launches.size() && err == hipSuccess; ++i) {
-    Launch& L = e->launches[i];
-    if (L.op != Launch::ConvMfma) continue;
-    const std::vector<ConvTile> cand = conv_candidates(L);
-    if (cand.size() < 2) continue;
-    float best_ms = 0;
-    ConvTile best = L.tile_default;
-    for (size_t k = 0; k < cand.size() && err == hipSuccess; ++k) {
-      Launch T = L;
-      apply_tile(T, cand[k]);
-      for (int w = 0; w < 2 && err == hipSuccess; ++w) err = exec(T, c);
-      if (err == hipSuccess) err = hipEventRecord(ev0, s);
-      constexpr int kReps = 5;
-      for (int r = 0; r < kReps && err == hipSuccess; ++r) err = exec(T, c);
-      if (err == hipSuccess) err = hipEventRecord(ev1, s);
-      if (err == hipSuccess) err = hipEventSynchronize(ev1);
-      float ms = 0;
-      if (err == hipSuccess) err = hipEventElapsedTime(&ms, ev0, ev1);
-      if (err == hipSuccess && (k == 0 || ms < best_ms)) {
-        best_ms = ms;
-        best = cand[k];
+  // Candidate k of every conv launch is timed inside full runs of the whole
+  // launch sequence (each launch between its real neighbours, so with the
+  // cache state the run leaves it), best of kReps runs; round k uses each
+  // launch's k-th candidate (its built-in choice when it has fewer).
+  std::vector<std::vector<ConvTile>> cand(nl);
+  size_t rounds = 1;
+  for (size_t i = 0; i < nl; ++i)
+    if (e->launches[i].op == Launch::ConvMfma) {
+      cand[i] = conv_candidates(e->launches[i]);
+      rounds = std::max(rounds, cand[i].size());
+    }
+  std::vector<float> best_ms(nl, 0.f);
+  std::vector<size_t> best_k(nl, 0);
+  constexpr int kReps = 3;
+  for (size_t k = 0; k < rounds && err == hipSuccess; ++k) {
+    for (size_t i = 0; i < nl; ++i)
+      if (!cand[i].empty()) apply_tile(e->launches[i], cand[i][k < cand[i].size() ? k : 0]);
+    std::vector<float> round_ms(nl, 0.f);
+    for (int rep = -1; rep < kReps && err == hipSuccess; ++rep) {  // rep -1: warm-up run
+      err = hipEventRecord(ev[0], s);
+      for (size_t i = 0; i < nl && err == hipSuccess; ++i) {
+        err = exec(e->launches[i], c);
+        if (err == hipSuccess) err = hipEventRecord(ev[i + 1], s);
+      }
+      if (err == hipSuccess) err = hipEventSynchronize(ev[nl]);
+      for (size_t i = 0; i < nl && err == hipSuccess && rep >= 0; ++i) {
+        float ms = 0.f;
+        err = hipEventElapsedTime(&ms, ev[i], ev[i + 1]);
+        if (rep == 0 || ms < round_ms[i]) round_ms[i] = ms;
       }
     }
-    if (err == hipSuccess) apply_tile(L, best);
+    for (size_t i = 0; i < nl && err == hipSuccess; ++i)
+      if (k < cand[i].size() && (k == 0 || round_ms[i] < best_ms[i])) {
+        best_ms[i] = round_ms[i];
+        best_k[i] = k;
+      }
   }
+  for (size_t i = 0; i < nl; ++i)
+    if (!cand[i].empty()) apply_tile(e->launches[i], err == hipSuccess ? cand[i][best_k[i]] : e->launches[i].tile_default);
+  for (hipEvent_t x : ev)
+    if (x) (void)hipEventDestroy(x);
   hipError_t serr = hipStreamSynchronize(s);
-  if (ev0) (void)hipEventDestroy(ev0);
-  if (ev1) (void)hipEventDestroy(ev1);
   (void)hipStreamDestroy(s);
   if (err == hipSuccess) err = serr;
   if (err != hipSuccess) {

@@ -54,14 +54,15 @@ struct ConvTile {
   int bm, bn;       // pixels x channels per workgroup
   int mf = 16;      // MFMA shape: 16 (16x16x32) or 32 (32x32x16)
   int stages = 0;   // > 0: HBM->LDS pipeline of that many stages (conv_dma)
+  int threads = 256;  // conv_dma workgroup size: 256 (4 waves) or 512 (8 waves)
 };
 
 // Tile configurations with a compiled kernel.
 bool conv_mfma_tile_supported(int bm, int bn, int mf);
 hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
 // Direct HBM->LDS pipelined variant (16x16x32 MFMA only).
-bool conv_dma_tile_supported(int bm, int bn, int stages);
-hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, hipStream_t s);
+bool conv_dma_tile_supported(int bm, int bn, int stages, int threads);
+hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s);
 // Sums split-K partials in a fixed order and applies bias, residual, act.
 hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s);
 
