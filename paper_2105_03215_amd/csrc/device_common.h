@@ -23,14 +23,16 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+// x * Phi(x) with Phi(x) = erfc(-x / sqrt 2) / 2: no cancellation for x << 0.
+// Kept out of line: inlined at every epilogue site its expansion would make
+// the kernels several times larger than the instruction cache.
+__device__ __attribute__((noinline)) float gelu(float v) { return 0.5f * v * erfcf(-v * 0.70710678118654752440f); }
+
+// none / ReLU / ReLU6 as one branch-free clamp; GELU through the call above.
 __device__ __forceinline__ float apply_act(float v, int act) {
-  switch (act) {
-    case kActRelu: return fmaxf(v, 0.0f);
-    case kActRelu6: return fminf(fmaxf(v, 0.0f), 6.0f);
-    // x * Phi(x) with Phi(x) = erfc(-x / sqrt 2) / 2: no cancellation for x << 0
-    case kActGelu: return 0.5f * v * erfcf(-v * 0.70710678118654752440f);
-    default: return v;
-  }
+  if (act == kActGelu) return gelu(v);
+  const float c = fminf(fmaxf(v, 0.0f), act == kActRelu6 ? 6.0f : INFINITY);
+  return act == kActNone ? v : c;
 }
 
 // Unpacks 8 bf16 held in a uint4 into floats.

@@ -29,7 +29,7 @@ constexpr int kRowPad = 256;  // packed weight rows are padded to this (>= any t
 constexpr int kKPad = 64;     // packed reduction length is padded to this (the stage depth)
 
 struct PackJob {
-  enum Kind { ConvW, DwW, Vec, Copy } kind;
+  enum Kind { ConvW, DwW, Vec, Copy, StemW } kind;
   int cidx = -1;       // constant index
   int64_t dst = 0;     // byte offset in the weights region
   int K = 0, Cg = 0, R = 0, S = 0, Cp = 0, Kgp = 0, rows = 0;
@@ -142,6 +142,8 @@ struct Planner {
   std::vector<PackJob> jobs;
   int64_t wbytes = 0;
   Status err;
+  // fused stems: conv node -> its max-pool node, max-pool node -> conv node
+  std::vector<int> stem_pool, stem_conv;
 
   Planner(Engine* e_, Graph& g_) : e(e_), g(g_), bf16(g_.compute == DType::BF16) {
     loc.resize(g.values.size());
@@ -187,15 +189,103 @@ struct Planner {
 
   Status plan();
   void plan_node(int ni);
+  void find_stems();
+  void plan_stem(int conv_ni, int pool_ni);
 };
 
+// A graph input in NCHW with at most 4 channels feeding only a conv whose
+// output feeds only a max pool is planned as one fused stem kernel: the
+// input is read in place (no layout transform) and the full-resolution conv
+// output never exists.
+void Planner::find_stems() {
+  stem_pool.assign(g.nodes.size(), -1);
+  stem_conv.assign(g.nodes.size(), -1);
+  if (!bf16) return;
+  auto uses = [&](int v, int* user) {
+    int count = 0;
+    for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
+      const Node& n = g.nodes[ni];
+      for (int u : {n.data, n.weight, n.bias, n.residual, n.other})
+        if (u == v) {
+          ++count;
+          *user = (int)ni;
+        }
+    }
+    for (const IoDesc& o : g.outputs)
+      if (o.value == v) count += 2;
+    return count;
+  };
+  for (const IoDesc& in : g.inputs) {
+    const auto& xs = g.values[in.value].shape;
+    if (xs.size() != 4 || in.layout != BYOC_NCHW) continue;
+    int ci = -1, pi = -1;
+    if (uses(in.value, &ci) != 1) continue;
+    const Node& c = g.nodes[ci];
+    if (c.op != OpKind::Conv || c.data != in.value || c.depthwise || c.groups != 1 || c.residual >= 0) continue;
+    if (uses(c.out, &pi) != 1) continue;
+    const Node& pn = g.nodes[pi];
+    if (pn.op != OpKind::MaxPool || pn.data != c.out) continue;
+    const auto& ws = g.values[c.weight].shape;
+    if (!stem_supported((int)xs[1], (int)ws[0], (int)ws[2], (int)ws[3], c.stride[0], c.stride[1], pn.pool[0],
+                        pn.pool[1], pn.stride[0], pn.stride[1]))
+      continue;
+    stem_pool[ci] = pi;
+    stem_conv[pi] = ci;
+  }
+}
+
+void Planner::plan_stem(int ci, int pi) {
+  const Node& c = g.nodes[ci];
+  const Node& pn = g.nodes[pi];
+  const auto& xs = g.values[c.data].shape;
+  const auto& cs = g.values[c.out].shape;
+  const auto& ps = g.values[pn.out].shape;
+  const auto& ws = g.values[c.weight].shape;
+  const int in_idx = g.values[c.data].index;
+  Launch L;
+  L.op = Launch::StemConvPool;
+  L.info.kind = BYOC_K_CONV_MFMA;
+  L.info.node = ci;
+  L.x = loc[c.data];
+  L.y = loc[pn.out];
+  StemParams& p = L.stem;
+  p.x_bf16 = g.inputs[in_idx].dtype == DType::BF16;
+  p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3];
+  p.R = (int)ws[2], p.S = (int)ws[3], p.sh = c.stride[0], p.sw = c.stride[1], p.pt = c.pad[0], p.pl = c.pad[1];
+  p.P = (int)cs[2], p.Q = (int)cs[3];
+  p.kph = pn.pool[0], p.kpw = pn.pool[1], p.sph = pn.stride[0], p.spw = pn.stride[1];
+  p.ppt = pn.pad[0], p.ppl = pn.pad[1];
+  p.PO = (int)ps[2], p.QO = (int)ps[3];
+  p.act = (int)c.act;
+  p.wld = stem_weight_ld(p.R);
+  const int wc = g.values[c.weight].index;
+  const int bc = c.bias >= 0 ? g.values[c.bias].index : -1;
+  L.w = wslot((int64_t)64 * p.wld * 2);
+  PackJob j{PackJob::StemW, wc, L.w.off, 64, p.C, p.R, p.S, 0, 0, 0, p.wld, 0};
+  jobs.push_back(j);
+  L.bias = wslot(64 * 4);
+  jobs.push_back({PackJob::Vec, bc, L.bias.off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? 64 : 0, 64});
+  L.info.flops = 2 * c.macs;
+  L.info.bytes = ext_bytes(c.data, g.inputs[in_idx].dtype) + numel(ws) * 2 + 64 * 4 + act_bytes(pn.out);
+  name(L, "stem_conv_maxpool");
+  e->launches.push_back(L);
+}
+
 Status Planner::plan() {
+  find_stems();
   // ---- inputs: direct use or boundary transform ----------------------------
   for (size_t i = 0; i < g.inputs.size(); ++i) {
     const IoDesc& in = g.inputs[i];
     const int v = in.value;
     const auto& s = g.values[v].shape;
     cp[v] = bf16 ? (int)rup(s[1], 8) : (int)s[1];
+    bool fused_stem = false;
+    for (size_t ni = 0; ni < g.nodes.size(); ++ni)
+      if (stem_pool[ni] >= 0 && g.nodes[ni].data == v) fused_stem = true;
+    if (fused_stem) {  // read in place by the fused stem kernel
+      loc[v] = io(Ref::Input, (int)i);
+      continue;
+    }
     const bool direct = bf16 ? (s.size() == 2 && in.dtype == DType::BF16 && s[1] % 8 == 0)
                              : (in.dtype == DType::F32);
     if (direct) {
@@ -245,8 +335,15 @@ Status Planner::plan() {
         placed = true;
       }
     }
+    if (stem_pool[ni] >= 0) {  // conv of a fused stem: its output is never stored
+      loc[v] = Ref();
+      continue;
+    }
     if (!placed) loc[v] = arena(internal_bytes(v));
-    plan_node((int)ni);
+    if (stem_conv[ni] >= 0)
+      plan_stem(stem_conv[ni], (int)ni);
+    else
+      plan_node((int)ni);
     if (!err.ok()) return err;
   }
   // ---- outputs not written in place: boundary transforms ---------------------
@@ -592,6 +689,14 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
                                    L.Kp, c.s);
     case Launch::Cast:
       return launch_cast(c.ptr(L.x), L.src_bf16, c.ptr(L.y), L.dst_bf16, L.n, c.s);
+    case Launch::StemConvPool: {
+      StemParams p = L.stem;
+      p.x = c.ptr(L.x);
+      p.w = (const bf16_t*)c.ptr(L.w);
+      p.bias = (const float*)c.ptr(L.bias);
+      p.y = (bf16_t*)c.ptr(L.y);
+      return launch_stem_conv_maxpool(p, c.s);
+    }
   }
   return hipErrorInvalidValue;
 }
@@ -668,6 +773,9 @@ Status build_device_state(Engine* e, Planner& pl, const byoc_const* consts) {
           break;
         case PackJob::Copy:
           err = launch_cast(src, sb, dst, false, j.n, nullptr);
+          break;
+        case PackJob::StemW:
+          err = launch_pack_stem_weights(src, sb, (bf16_t*)dst, j.Cg, j.R, j.S, j.n, nullptr);
           break;
       }
     }

@@ -24,7 +24,7 @@ struct Ref {
 struct Launch {
   enum Op {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
-    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast
+    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;
@@ -34,6 +34,7 @@ struct Launch {
   ConvF32Params cf{};
   DwParams dw{};
   PoolParams pool{};
+  StemParams stem{};
   int64_t n = 0;
   int act = 0;
   bool src_bf16 = false, dst_bf16 = false;

@@ -63,6 +63,27 @@ hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
 // Direct HBM->LDS pipelined variant (16x16x32 MFMA only).
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads);
 hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s);
+// Fused stem: conv (C <= 4 NCHW input channels, 64 output channels) + bias
+// + activation followed by max pooling; output NHWC bf16 with 64 channels.
+struct StemParams {
+  const void* x;  // graph input [N][C][H][W], bf16 or f32
+  int x_bf16;
+  const bf16_t* w;  // packed [64][wld], column r*32 + s*4 + c
+  int wld;
+  const float* bias;  // [64] or nullptr
+  bf16_t* y;          // [N][PO][QO][64]
+  int N, C, H, W;
+  int R, S, sh, sw, pt, pl;      // conv
+  int P, Q;                      // conv output size
+  int kph, kpw, sph, spw, ppt, ppl;  // pool window, stride, padding
+  int PO, QO;                    // pool output size
+  int act;
+};
+bool stem_supported(int C, int K, int R, int S, int sh, int sw, int kph, int kpw, int sph, int spw);
+int stem_weight_ld(int R);
+hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s);
+hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R, int S, int wld,
+                                    hipStream_t s);
 // Sums split-K partials in a fixed order and applies bias, residual, act.
 hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s);
 

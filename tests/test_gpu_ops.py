@@ -187,3 +187,28 @@ def test_f32_other_ops():
     g.output(d)
     g.output(s)
     _check_f32(g.finish(), "fp32 dw/maxpool/add/gap/dense")
+
+
+STEM_CASES = [
+    # name, (n, c, h, w), r, stride, pad, act, (pool size, stride, pad), input dtype
+    ("resnet_stem_ragged", (2, 3, 45, 45), 7, 2, 3, "relu", (3, 2, 1), "bf16"),
+    ("stem_f32_c1", (1, 1, 32, 30), 7, 2, 3, "relu", (3, 2, 1), "f32"),
+    ("stem_3x3_s1_pool2", (2, 4, 20, 21), 3, 1, 1, None, (2, 2, 0), "bf16"),
+    ("stem_5x5_s2_pool3_s1", (1, 3, 24, 24), 5, 2, 2, "relu6", (3, 1, 1), "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", STEM_CASES, ids=[c[0] for c in STEM_CASES])
+def test_fused_stem_conv_maxpool(case):
+    """A few-channel NCHW input feeding conv -> max pool runs as one fused
+    kernel (no layout transform, no full-resolution conv output) and matches
+    the unfused oracle chain."""
+    name, shape, r, stride, pad, act, (ps, pst, ppad), dt = case
+    g = GraphBuilder("stem_" + name, 1600 + STEM_CASES.index(case))
+    x = g.input("x", list(shape), "uniform", dtype=dt)
+    y = g.conv(x, 64, r, stride=stride, pad=pad, act=act, name="conv")
+    p = g.max_pool(y, ps, pst, ppad, name="pool")
+    g.output(p)
+    launches = _check_bf16(g.finish(), "stem " + name)
+    names = [l["name"] for l in launches]
+    assert names[0] == "stem_conv_maxpool" and "nchw_to_nhwc" not in names, names
