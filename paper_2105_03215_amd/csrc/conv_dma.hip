@@ -394,39 +394,47 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
   float* stage = reinterpret_cast<float*>(lds0);
+  const ActClamp ac = act_clamp_of(p.act);
+  auto epilogue = [&](auto gelu_tag) {
+    constexpr bool G = decltype(gelu_tag)::value;
 #pragma unroll
-  for (int pass = 0; pass < NPASS; ++pass) {
-    if (pass > 0) lds_barrier();
+    for (int pass = 0; pass < NPASS; ++pass) {
+      if (pass > 0) lds_barrier();
 #pragma unroll
-    for (int i = 0; i < TN; ++i) {
-      const int ch = wn * WTN + i * 16 + 4 * (lane >> 4) - pass * kEC;
-      if (ch < 0 || ch >= kEC) continue;
+      for (int i = 0; i < TN; ++i) {
+        const int ch = wn * WTN + i * 16 + 4 * (lane >> 4) - pass * kEC;
+        if (ch < 0 || ch >= kEC) continue;
 #pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        const int px = wm * WTM + j * 16 + (lane & 15);
-        const f32x4 a = acc[i][j];
-        *(float4*)(stage + px * kLd + ch) = make_float4(a[0], a[1], a[2], a[3]);
+        for (int j = 0; j < TM; ++j) {
+          const int px = wm * WTM + j * 16 + (lane & 15);
+          const f32x4 a = acc[i][j];
+          *(float4*)(stage + px * kLd + ch) = make_float4(a[0], a[1], a[2], a[3]);
+        }
+      }
+      lds_barrier();
+      const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) {
+        const int px = (tid + q * kNT) / TPP;
+        const int m = m0 + px;
+        if (px >= BM || m >= p.M || k >= p.Kp) continue;
+        float f[8], rv[8];
+        const float4 lo = *(const float4*)(stage + px * kLd + ec8);
+        const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
+        const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
+        unpack8(resv[pass][q], rv);
+        f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
+        f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = act_apply<G>(f[e] + rv[e], ac);
+        *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
       }
     }
-    lds_barrier();
-    const int k = n0 + pass * kEC + ec8;
-#pragma unroll
-    for (int q = 0; q < EPV; ++q) {
-      const int px = (tid + q * kNT) / TPP;
-      const int m = m0 + px;
-      if (px >= BM || m >= p.M || k >= p.Kp) continue;
-      float f[8], rv[8];
-      const float4 lo = *(const float4*)(stage + px * kLd + ec8);
-      const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
-      const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
-      unpack8(resv[pass][q], rv);
-      f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
-      f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = apply_act(f[e] + rv[e], p.act);
-      *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
-    }
-  }
+  };
+  if (p.act == kActGelu)
+    epilogue(std::true_type{});
+  else
+    epilogue(std::false_type{});
 }
 
 template <int BM, int BN, int WM, int WN, int NS>

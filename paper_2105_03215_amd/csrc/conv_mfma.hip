@@ -361,41 +361,49 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   constexpr int kLd = kEC + 4;  // padded row (floats): 16 rows hit distinct banks
   static_assert(BN % kEC == 0 && BM * kLd * 4 <= (int)sizeof(smem), "staging tile");
   float* stage = reinterpret_cast<float*>(smem);
+  const ActClamp ac = act_clamp_of(p.act);
+  auto epilogue = [&](auto gelu_tag) {
+    constexpr bool G = decltype(gelu_tag)::value;
 #pragma unroll
-  for (int pass = 0; pass < NPASS; ++pass) {
-    lds_barrier();
+    for (int pass = 0; pass < NPASS; ++pass) {
+      lds_barrier();
 #pragma unroll
-    for (int i = 0; i < TN; ++i)
+      for (int i = 0; i < TN; ++i)
 #pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        const int px = wm * WTM + j * MF + (lane % MF);
+        for (int j = 0; j < TM; ++j) {
+          const int px = wm * WTM + j * MF + (lane % MF);
 #pragma unroll
-        for (int e = 0; e < NE; e += 4) {
-          const int ch = wn * WTN + i * MF + st.acc_row(e) - pass * kEC;
-          if (ch < 0 || ch >= kEC) continue;
-          *(float4*)(stage + px * kLd + ch) =
-              make_float4(st.acc[i][j][e], st.acc[i][j][e + 1], st.acc[i][j][e + 2], st.acc[i][j][e + 3]);
+          for (int e = 0; e < NE; e += 4) {
+            const int ch = wn * WTN + i * MF + st.acc_row(e) - pass * kEC;
+            if (ch < 0 || ch >= kEC) continue;
+            *(float4*)(stage + px * kLd + ch) =
+                make_float4(st.acc[i][j][e], st.acc[i][j][e + 1], st.acc[i][j][e + 2], st.acc[i][j][e + 3]);
+          }
         }
+      lds_barrier();
+      const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) {
+        const int px = (tid + q * kNT) / (kEC / 8);
+        const int m = m0 + px;
+        if (m >= p.M || k >= p.Kp) continue;
+        float f[8], r[8];
+        const float4 lo = *(const float4*)(stage + px * kLd + ec8);
+        const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
+        const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
+        unpack8(resv[pass][q], r);
+        f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
+        f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = act_apply<G>(f[e] + r[e], ac);
+        *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
       }
-    lds_barrier();
-    const int k = n0 + pass * kEC + ec8;
-#pragma unroll
-    for (int q = 0; q < EPV; ++q) {
-      const int px = (tid + q * kNT) / (kEC / 8);
-      const int m = m0 + px;
-      if (m >= p.M || k >= p.Kp) continue;
-      float f[8], r[8];
-      const float4 lo = *(const float4*)(stage + px * kLd + ec8);
-      const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
-      const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
-      unpack8(resv[pass][q], r);
-      f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
-      f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = apply_act(f[e] + r[e], p.act);
-      *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
     }
-  }
+  };
+  if (p.act == kActGelu)
+    epilogue(std::true_type{});
+  else
+    epilogue(std::false_type{});
 }
 
 // Split-K reduction: one thread per 4 channels of one pixel; partials summed

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -28,11 +29,28 @@ __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
 // the kernels several times larger than the instruction cache.
 __device__ __attribute__((noinline)) float gelu(float v) { return 0.5f * v * erfcf(-v * 0.70710678118654752440f); }
 
-// none / ReLU / ReLU6 as one branch-free clamp; GELU through the call above.
+// Epilogue activation.  Kernels pick the GELU or the clamp instantiation
+// once (the choice is uniform), so the per-element code has no branch:
+// none / ReLU / ReLU6 are one median-of-three clamp to [0, hi] (or the
+// value itself for none), GELU the out-of-line call above.
+struct ActClamp {
+  float hi;   // 6 for ReLU6, +inf otherwise
+  bool none;  // no activation
+};
+__device__ __forceinline__ ActClamp act_clamp_of(int act) {
+  return ActClamp{act == kActRelu6 ? 6.0f : INFINITY, act == kActNone};
+}
+template <bool GELU>
+__device__ __forceinline__ float act_apply(float v, ActClamp a) {
+  if constexpr (GELU) {
+    return gelu(v);
+  } else {
+    const float c = __builtin_amdgcn_fmed3f(v, 0.0f, a.hi);
+    return a.none ? v : c;
+  }
+}
 __device__ __forceinline__ float apply_act(float v, int act) {
-  if (act == kActGelu) return gelu(v);
-  const float c = fminf(fmaxf(v, 0.0f), act == kActRelu6 ? 6.0f : INFINITY);
-  return act == kActNone ? v : c;
+  return act == kActGelu ? gelu(v) : act_apply<false>(v, act_clamp_of(act));
 }
 
 // Unpacks 8 bf16 held in a uint4 into floats.

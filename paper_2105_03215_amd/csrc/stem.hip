@@ -144,8 +144,7 @@ __global__ __launch_bounds__(kThreads) void stem_conv_maxpool_kernel(StemParams 
     for (int j = 0; j < 4; ++j)
       a[j] = as_bf16x8(*reinterpret_cast<const uint4*>(wl + (j * 16 + (lane & 15)) * p.wld + r * 32 + g * 8));
 #pragma unroll
-    for (int i = 0; i < kFragsPerWave; ++i) {
-      if (wave + 4 * i >= kFrags) break;
+    for (int i = 0; i < kFragsPerWave; ++i) {  // a wave's surplus tile computes discarded values
       const uint2 t0 = patch[pbase[i] + r * kPatch];
       const uint2 t1 = patch[pbase[i] + r * kPatch + 1];
       const bf16x8 b = as_bf16x8(make_uint4(t0.x, t0.y, t1.x, t1.y));
@@ -156,26 +155,34 @@ __global__ __launch_bounds__(kThreads) void stem_conv_maxpool_kernel(StemParams 
   __syncthreads();  // patch and weights are dead: the conv tile overlays them
 
   // 3. bias, activation, bf16; conv outputs outside the image -> -inf
+  const ActClamp ac = act_clamp_of(p.act);
+  auto epilogue = [&](auto gelu_tag) {
+    constexpr bool G = decltype(gelu_tag)::value;
 #pragma unroll
-  for (int i = 0; i < kFragsPerWave; ++i) {
-    if (wave + 4 * i >= kFrags) break;
-    const int m = (wave + 4 * i) * 16 + (lane & 15);
-    if (m >= npix) continue;
-    const int lr = m / CC, lc = m - (m / CC) * CC;
-    const bool inside = (unsigned)(cr0 + lr) < (unsigned)p.P && (unsigned)(cc0 + lc) < (unsigned)p.Q;
+    for (int i = 0; i < kFragsPerWave; ++i) {
+      if (wave + 4 * i >= kFrags) break;
+      const int m = (wave + 4 * i) * 16 + (lane & 15);
+      if (m >= npix) continue;
+      const int lr = m / CC, lc = m - (m / CC) * CC;
+      const bool inside = (unsigned)(cr0 + lr) < (unsigned)p.P && (unsigned)(cc0 + lc) < (unsigned)p.Q;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint2 o;
-      if (inside) {
-        const f32x4 v = acc[i][j];
-        o = make_uint2(pack2_bf16(apply_act(v[0] + bv[j].x, p.act), apply_act(v[1] + bv[j].y, p.act)),
-                       pack2_bf16(apply_act(v[2] + bv[j].z, p.act), apply_act(v[3] + bv[j].w, p.act)));
-      } else {
-        o = make_uint2(0xFF80FF80u, 0xFF80FF80u);  // bf16 -inf
+      for (int j = 0; j < 4; ++j) {
+        uint2 o;
+        if (inside) {
+          const f32x4 v = acc[i][j];
+          o = make_uint2(pack2_bf16(act_apply<G>(v[0] + bv[j].x, ac), act_apply<G>(v[1] + bv[j].y, ac)),
+                         pack2_bf16(act_apply<G>(v[2] + bv[j].z, ac), act_apply<G>(v[3] + bv[j].w, ac)));
+        } else {
+          o = make_uint2(0xFF80FF80u, 0xFF80FF80u);  // bf16 -inf
+        }
+        *reinterpret_cast<uint2*>(tile + m * kTileLd + j * 16 + 4 * g) = o;
       }
-      *reinterpret_cast<uint2*>(tile + m * kTileLd + j * 16 + 4 * g) = o;
     }
-  }
+  };
+  if (p.act == kActGelu)
+    epilogue(std::true_type{});
+  else
+    epilogue(std::false_type{});
   __syncthreads();
 
   // 4. pooling: 64 pooled pixels x 8 channel groups, two per thread
@@ -187,11 +194,20 @@ __global__ __launch_bounds__(kThreads) void stem_conv_maxpool_kernel(StemParams 
     float mx[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) mx[e] = -INFINITY;
-    for (int dr = 0; dr < p.kph; ++dr)
-      for (int dc = 0; dc < p.kpw; ++dc) {
-        const int m = (pi * p.sph + dr) * CC + pj * p.spw + dc;
+    uint4 win[3][3];  // all window reads issued before the first max
+#pragma unroll
+    for (int dr = 0; dr < 3; ++dr)
+#pragma unroll
+      for (int dc = 0; dc < 3; ++dc) {
+        const int m = (pi * p.sph + (dr < p.kph ? dr : 0)) * CC + pj * p.spw + (dc < p.kpw ? dc : 0);
+        win[dr][dc] = *reinterpret_cast<const uint4*>(tile + m * kTileLd + c8);
+      }
+#pragma unroll
+    for (int dr = 0; dr < 3; ++dr)
+#pragma unroll
+      for (int dc = 0; dc < 3; ++dc) {
         float v[8];
-        unpack8(*reinterpret_cast<const uint4*>(tile + m * kTileLd + c8), v);
+        unpack8(win[dr][dc], v);  // taps past the window repeat its first one: no effect on the max
 #pragma unroll
         for (int e = 0; e < 8; ++e) mx[e] = fmaxf(mx[e], v[e]);
       }
