@@ -934,7 +934,8 @@ Status autotune(Engine* e) {
   const size_t nl = e->launches.size();
   std::vector<hipEvent_t> ev(nl + 1, nullptr);
   hipError_t err = hipSuccess;
-  for (size_t i = 0; i <= nl && err == hipSuccess; ++i) err = hipEventCreate(&ev[i]);
+  // no system-scope fence per event: timing only, the stream orders the work
+  for (size_t i = 0; i <= nl && err == hipSuccess; ++i) err = hipEventCreateWithFlags(&ev[i], hipEventDisableSystemFence);
   RunCtx c{e, in_ptr.data(), out_ptr.data(), s};
   // Candidate k of every conv launch is timed inside full runs of the whole
   // launch sequence (each launch between its real neighbours, so with the
@@ -1056,7 +1057,7 @@ Status engine_profile_begin(Engine* e, int max_runs) {
   const size_t n = (size_t)max_runs * (e->launches.size() + 1);
   e->events.resize(n);
   for (size_t i = 0; i < n; ++i) {
-    hipError_t err = hipEventCreate(&e->events[i]);
+    hipError_t err = hipEventCreateWithFlags(&e->events[i], hipEventDisableSystemFence);
     if (err != hipSuccess) {
       e->events.resize(i);
       for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);

@@ -1,19 +1,25 @@
 """Summaries of rocprofv3 output for the committed profiles.
 
-stats    kernel-trace statistics (``--kernel-trace --stats --output-format
-         csv``) -> a short text table headed by the command that made it.
-traffic  HBM bytes of the conv kernels per step from two counter runs
+stats    kernel trace (``--kernel-trace --stats --output-format csv``, the
+         per-dispatch ``*_kernel_trace.csv``) -> a short text table headed by
+         the command that made it: per kernel, calls and time per run over the
+         last N runs of the subgraph (the runs after the engine's autotune),
+         and the per-run time of the conv/dense MFMA kernel class.
+traffic  HBM bytes of the conv kernels per run from two counter runs
          (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``, KiB per dispatch),
          each scaled by what the same counter reads for a plain device copy of
          known size (``bench.py --copy-calibration MIB`` under the same
-         counter) -> JSON read by bench.py.
+         counter), over the last N runs -> JSON read by bench.py.
+
+A run of the ResNet subgraph starts with its fused stem kernel, the marker
+used to split the dispatch stream into runs.
 
 Usage:
-  python -m paper_2105_03215_amd.profiling stats --csv X_kernel_stats.csv \
-      --cmd "<command>" --out profiles/NAME.txt
+  python -m paper_2105_03215_amd.profiling stats --trace X_kernel_trace.csv \
+      --cmd "<command>" --last-runs 60 --flops-per-run F --out profiles/NAME.txt
   python -m paper_2105_03215_amd.profiling traffic --fetch F.csv --write W.csv \
-      --copy-fetch CF.csv --copy-write CW.csv --copy-mib 512 --workload resnet50_v1_bs32 \
-      --out profiles/traffic.json
+      --copy-fetch CF.csv --copy-write CW.csv --copy-mib 512 --last-runs 2 \
+      --workload resnet50_v1_bs32 --out profiles/traffic.json
 """
 
 import argparse
@@ -24,23 +30,49 @@ import os
 import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "splitk_reduce_kernel")
-RUN_MARKER = "nchw_to_nhwc_kernel"  # one dispatch per run of the CNN subgraphs
+CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "stem_conv_maxpool_kernel", "splitk_reduce_kernel")
+RUN_MARKER = "stem_conv_maxpool_kernel"  # one dispatch per run of the ResNet subgraphs
 
 
 def _short(name):
     return name.replace("byoc::(anonymous namespace)::", "").replace("void ", "")
 
 
-def stats(csv_path, cmd, out, top=25):
-    rows = list(csv.DictReader(open(csv_path)))
-    total = sum(float(r["TotalDurationNs"]) for r in rows)
-    lines = ["# rocprofv3 kernel statistics", "# command: " + cmd,
-             "# %-70s %6s %12s %10s %6s" % ("kernel", "calls", "total_us", "avg_us", "pct")]
-    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"]))[:top]:
-        lines.append("  %-70s %6s %12.1f %10.2f %6.2f" % (
-            _short(r["Name"])[:70], r["Calls"], float(r["TotalDurationNs"]) / 1e3,
-            float(r["AverageNs"]) / 1e3, 100.0 * float(r["TotalDurationNs"]) / total))
+def _is_conv(name):
+    return any(k in name for k in CONV_KERNELS)
+
+
+def _last_runs(rows, name_key, last_runs, marker=RUN_MARKER):
+    """The rows from the start of the last `last_runs` runs on."""
+    starts = [i for i, r in enumerate(rows) if marker in r[name_key]]
+    if len(starts) < last_runs:
+        raise RuntimeError("only %d runs (marker %s) in the trace" % (len(starts), marker))
+    return rows[starts[-last_runs]:], last_runs
+
+
+def stats(trace_path, cmd, out, last_runs, flops_per_run=0.0, top=25):
+    rows = sorted(csv.DictReader(open(trace_path)), key=lambda r: int(r["Start_Timestamp"]))
+    rows, runs = _last_runs(rows, "Kernel_Name", last_runs)
+    per = {}
+    for r in rows:
+        d = per.setdefault(r["Kernel_Name"], [0, 0])
+        d[0] += 1
+        d[1] += int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    total = sum(v[1] for v in per.values())
+    conv_ns = sum(v[1] for k, v in per.items() if _is_conv(k))
+    conv_calls = sum(v[0] for k, v in per.items() if _is_conv(k))
+    lines = ["# rocprofv3 kernel statistics (last %d runs of the subgraph, after autotune)" % runs,
+             "# command: " + cmd,
+             "# %-70s %9s %10s %12s %6s" % ("kernel", "calls/run", "avg_us", "us/run", "pct")]
+    for k, (calls, ns) in sorted(per.items(), key=lambda kv: -kv[1][1])[:top]:
+        lines.append("  %-70s %9.2f %10.2f %12.2f %6.2f" % (
+            _short(k)[:70], calls / runs, ns / calls / 1e3, ns / runs / 1e3, 100.0 * ns / total))
+    lines.append("# all kernels: %.1f us per run" % (total / runs / 1e3))
+    lines.append("# conv/dense MFMA class (%s): %.1f launches, %.1f us per run, avg %.2f us per launch" % (
+        ", ".join(CONV_KERNELS), conv_calls / runs, conv_ns / runs / 1e3, conv_ns / max(conv_calls, 1) / 1e3))
+    if flops_per_run:
+        lines.append("# conv/dense class: %.1f GFLOP per run -> %.1f TFLOP/s of pure kernel time" % (
+            flops_per_run / 1e9, flops_per_run / (conv_ns / runs * 1e-9) / 1e12))
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     return out
@@ -51,12 +83,12 @@ def _counter(path, counter):
     for r in csv.DictReader(open(path)):
         if r["Counter_Name"] != counter:
             continue
-        per[int(r["Dispatch_Id"])] = (r["Kernel_Name"], float(r["Counter_Value"]))
+        per[int(r["Dispatch_Id"])] = {"name": r["Kernel_Name"], "value": float(r["Counter_Value"])}
     return [per[k] for k in sorted(per)]
 
 
 def _copy_kib(path, counter):
-    vals = [v for n, v in _counter(path, counter) if "copyBuffer" in n or "copy" in n.lower()]
+    vals = [d["value"] for d in _counter(path, counter) if "copy" in d["name"].lower()]
     if not vals:
         raise RuntimeError("no copy kernel in %s" % path)
     big = max(vals)
@@ -66,23 +98,22 @@ def _copy_kib(path, counter):
 def conv_kernel_digest():
     """Digest of the conv kernel sources and of the planner that picks them."""
     h = hashlib.sha256()
-    for name in ("conv_mfma.hip", "conv_dma.hip", "engine.cpp"):
+    for name in ("conv_mfma.hip", "conv_dma.hip", "stem.hip", "engine.cpp"):
         with open(os.path.join(ROOT, "paper_2105_03215_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic(fetch, write, copy_fetch, copy_write, copy_mib, workload, out):
+def traffic(fetch, write, copy_fetch, copy_write, copy_mib, workload, out, last_runs):
     copy_bytes = copy_mib * 2 ** 20
     f_scale = copy_bytes / (_copy_kib(copy_fetch, "FETCH_SIZE") * 1024.0)
     w_scale = copy_bytes / (_copy_kib(copy_write, "WRITE_SIZE") * 1024.0)
     res = {}
     for name, path, counter, scale in (("fetch", fetch, "FETCH_SIZE", f_scale),
                                        ("write", write, "WRITE_SIZE", w_scale)):
-        disp = _counter(path, counter)
-        runs = sum(1 for n, _ in disp if RUN_MARKER in n)
-        conv = sum(v for n, v in disp if any(k in n for k in CONV_KERNELS))
-        res[name] = conv * 1024.0 * scale / max(runs, 1)
+        disp, runs = _last_runs(_counter(path, counter), "name", last_runs)
+        conv = sum(d["value"] for d in disp if _is_conv(d["name"]))
+        res[name] = conv * 1024.0 * scale / runs
         res[name + "_runs"] = runs
     doc = {"workload": workload, "conv_kernel_digest": conv_kernel_digest(),
            "conv_bytes_per_step": round(res["fetch"] + res["write"]),
@@ -100,19 +131,22 @@ def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd_name", required=True)
     a = sub.add_parser("stats")
-    a.add_argument("--csv", required=True)
+    a.add_argument("--trace", required=True)
     a.add_argument("--cmd", required=True)
     a.add_argument("--out", required=True)
+    a.add_argument("--last-runs", type=int, required=True)
+    a.add_argument("--flops-per-run", type=float, default=0.0)
     b = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy-fetch", "copy-write", "workload", "out"):
         b.add_argument("--" + k, required=True)
     b.add_argument("--copy-mib", type=int, required=True)
+    b.add_argument("--last-runs", type=int, required=True)
     args = ap.parse_args()
     if args.cmd_name == "stats":
-        print(stats(args.csv, args.cmd, args.out))
+        print(stats(args.trace, args.cmd, args.out, args.last_runs, args.flops_per_run))
     else:
         print(json.dumps(traffic(args.fetch, args.write, args.copy_fetch, args.copy_write,
-                                 args.copy_mib, args.workload, args.out)))
+                                 args.copy_mib, args.workload, args.out, args.last_runs)))
 
 
 if __name__ == "__main__":
