@@ -79,10 +79,12 @@ __device__ __forceinline__ void lds_fill16(i32x4 rsrc, uint32_t lds_addr, uint32
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
-template <int BM, int BN, int WM, int WN, int NS, bool ALIGNED, bool SPLIT>
-__global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
-  static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves");
-  constexpr int kNT = 64 * WM * WN;          // threads per workgroup
+template <int BM, int BN, int WM, int WN, int KG, int NS, bool ALIGNED, bool SPLIT>
+__global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams p) {
+  static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves per reduction group");
+  static_assert(KG == 1 || (KG == 2 && !SPLIT), "reduction groups");
+  constexpr int kNT = 64 * WM * WN;          // threads of one reduction group
+  constexpr int kNTall = kNT * KG;           // threads per workgroup
   constexpr int kRowsPerPass = kNT / kCH;    // rows one load instruction of every wave covers
   static_assert(NS >= 2 && NS <= 4, "stages");
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
@@ -92,24 +94,24 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
   constexpr int LPS = AR + BR;  // load instructions per thread per stage
   constexpr int STAGE = (BM + BN) * kCH;  // uint4 per stage buffer
 
-  __shared__ uint4 lds0[STAGE];
-  __shared__ uint4 lds1[STAGE];
-  __shared__ uint4 lds2[NS > 2 ? STAGE : 1];
-  __shared__ uint4 lds3[NS > 3 ? STAGE : 1];
-  auto buf = [&](auto tag) -> uint4* {
-    constexpr int S = decltype(tag)::value;
-    if constexpr (S == 0) return lds0;
-    else if constexpr (S == 1) return lds1;
-    else if constexpr (S == 2) return lds2;
-    else return lds3;
-  };
-
+  // KG reduction groups of WM x WN waves each run their own ring of NS
+  // stage buffers over every KG-th stage of the reduction (group g: stages
+  // g, g + KG, ...), which multiplies the loads in flight and the MFMA issue
+  // of a workgroup; the groups' sums are added in group order at the end.
+  __shared__ uint4 ring[KG * NS * STAGE];
   materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = __builtin_amdgcn_readfirstlane(tid / kNT);        // reduction group
+  const int tg = tid - kg * kNT;                                      // thread within the group
+  const int wave = __builtin_amdgcn_readfirstlane((tid >> 6) % (WM * WN));  // wave within the group
+  uint4* const gring = ring + kg * NS * STAGE;
+  auto buf = [&](auto tag) -> uint4* {
+    constexpr int S = decltype(tag)::value;
+    return gring + S * STAGE;
+  };
   const int wm = wave / WN, wn = wave % WN;
-  const int r0 = tid / kCH;                       // first row this thread fills
+  const int r0 = tg / kCH;                        // first row this thread fills
   const int cv = (lane & 7) ^ ((lane >> 3) & 7);  // logical chunk it fetches
 
   // Tile placement: the hardware deals workgroups round-robin to the 8
@@ -192,20 +194,20 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
   // packed-weight column.
   int r, s, c, kk, wcol;
   {
-    const int kk0 = kt_begin * kBK + (ALIGNED ? 0 : cv * 8);
+    const int kk0 = (kt_begin + kg) * kBK + (ALIGNED ? 0 : cv * 8);
     const int rs = mdiv(kk0, p.mg_cp);
     c = kk0 - rs * p.Cp;
     r = mdiv(rs, p.mg_s);
     s = rs - r * p.S;
     kk = kk0;
-    wcol = kt_begin * kBK;
+    wcol = (kt_begin + kg) * kBK;
   }
 
   // Issues the loads of the next stage into buffer SET and advances the
   // position.  Every step issues the same number of loads, also past the end
   // of this split's reduction (those read zeros from an out-of-range offset
   // and are never computed), which keeps the count of loads in flight fixed.
-  int kleft = kt_end - kt_begin;
+  int kleft = (kt_end - kt_begin - kg + KG - 1) / KG;  // stages of this group
   auto issue = [&](auto set_tag) {
     uint4* dst = buf(set_tag);
     const bool live = kleft-- > 0;
@@ -230,23 +232,26 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
     for (int i = 0; i < BR; ++i)
       lds_fill16(wr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (BM + i * kRowsPerPass + wave * 8) * kCH)),
                  live ? wvoff[i] + wc : kOOB);
-    wcol += kBK;
-    c += kBK;
-    if (ALIGNED) {
-      if (c == p.Cp) {
-        c = 0;
-        if (++s == p.S) {
-          s = 0;
-          ++r;
+#pragma unroll
+    for (int a = 0; a < KG; ++a) {  // to this group's next stage
+      wcol += kBK;
+      c += kBK;
+      if (ALIGNED) {
+        if (c == p.Cp) {
+          c = 0;
+          if (++s == p.S) {
+            s = 0;
+            ++r;
+          }
         }
-      }
-    } else {
-      kk += kBK;
-      while (c >= p.Cp) {
-        c -= p.Cp;
-        if (++s == p.S) {
-          s = 0;
-          ++r;
+      } else {
+        kk += kBK;
+        while (c >= p.Cp) {
+          c -= p.Cp;
+          if (++s == p.S) {
+            s = 0;
+            ++r;
+          }
         }
       }
     }
@@ -292,7 +297,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
   constexpr int kEC = 32;  // channels per epilogue pass
   constexpr int NPASS = BN / kEC;
   constexpr int TPP = kEC / 8;  // threads per pixel
-  constexpr int EPV = (BM * TPP + kNT - 1) / kNT;  // pixels per thread per pass
+  constexpr int EPV = (BM * TPP + kNTall - 1) / kNTall;  // pixels per thread per pass
   const int ec8 = (tid % TPP) * 8;
   uint4 resv[SPLIT ? 1 : NPASS][EPV];
   float4 biasv[SPLIT ? 1 : NPASS][2];
@@ -310,7 +315,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
       }
 #pragma unroll
       for (int q = 0; q < EPV; ++q) {
-        const int px = (tid + q * kNT) / TPP;
+        const int px = (tid + q * kNTall) / TPP;
         const int m = m0 + px;
         const uint32_t off =
             (px < BM && m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) * 2u : kOOB;
@@ -324,7 +329,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
   using S1 = std::integral_constant<int, 1>;
   using S2 = std::integral_constant<int, 2>;
   using S3 = std::integral_constant<int, 3>;
-  const int nkt = kt_end - kt_begin;
+  const int nkt = (kt_end - kt_begin + KG - 1) / KG;  // steps (stages per group, rounded up)
 
   // Stage t lives in buffer t % NS.  Before computing it: wait for this
   // thread's fills of stage t (the NS-2 younger stages may stay in flight)
@@ -389,11 +394,14 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
     return;
   }
 
-  // Epilogue through LDS (buffer 0 as a [BM][kEC + 4] fp32 tile; the pad
-  // puts the 16 pixels of one accumulator write on distinct banks).
+  // Epilogue through LDS: each group parks its fp32 sums of a 32-channel
+  // slice in a [BM][kEC + 4] tile in its ring (the pad puts the 16 pixels of
+  // one accumulator write on distinct banks); every thread then takes 8
+  // consecutive channels of one pixel, adds the groups' sums in group order,
+  // bias and residual, applies the activation and stores 16 bytes.
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
-  float* stage = reinterpret_cast<float*>(lds0);
+  float* stage = reinterpret_cast<float*>(gring);
   const ActClamp ac = act_clamp_of(p.act);
   auto epilogue = [&](auto gelu_tag) {
     constexpr bool G = decltype(gelu_tag)::value;
@@ -415,12 +423,20 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
       const int k = n0 + pass * kEC + ec8;
 #pragma unroll
       for (int q = 0; q < EPV; ++q) {
-        const int px = (tid + q * kNT) / TPP;
+        const int px = (tid + q * kNTall) / TPP;
         const int m = m0 + px;
         if (px >= BM || m >= p.M || k >= p.Kp) continue;
+        const float* st0 = reinterpret_cast<const float*>(ring) + px * kLd + ec8;
+        float4 lo = *(const float4*)st0;
+        float4 hi = *(const float4*)(st0 + 4);
+#pragma unroll
+        for (int g = 1; g < KG; ++g) {
+          const float* stg = reinterpret_cast<const float*>(ring + g * NS * STAGE) + px * kLd + ec8;
+          const float4 l2 = *(const float4*)stg, h2 = *(const float4*)(stg + 4);
+          lo.x += l2.x; lo.y += l2.y; lo.z += l2.z; lo.w += l2.w;
+          hi.x += h2.x; hi.y += h2.y; hi.z += h2.z; hi.w += h2.w;
+        }
         float f[8], rv[8];
-        const float4 lo = *(const float4*)(stage + px * kLd + ec8);
-        const float4 hi = *(const float4*)(stage + px * kLd + ec8 + 4);
         const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
         unpack8(resv[pass][q], rv);
         f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
@@ -437,13 +453,14 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_dma_kernel(ConvParams p) {
     epilogue(std::false_type{});
 }
 
-template <int BM, int BN, int WM, int WN, int NS>
+template <int BM, int BN, int WM, int WN, int KG, int NS>
 hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
   ConvParams p = p_in;
   const int ntm = (p.M + BM - 1) / BM;
   const int ntn = (p.Kp + BN - 1) / BN;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
   const bool split = p.splits > 1;
+  if (KG > 1 && split) return hipErrorInvalidValue;
   int blocks = ntm * ntn;
   if (p.xcd_py > 0) {
     const int py = p.xcd_py, px = 8 / py;
@@ -454,50 +471,67 @@ hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
     p.mg_tile = magic40(ntn);
   }
   dim3 grid(blocks, split ? p.splits : 1);
-  constexpr int kNT = 64 * WM * WN;
-  if (aligned && !split) conv_dma_kernel<BM, BN, WM, WN, NS, true, false><<<grid, kNT, 0, s>>>(p);
-  else if (aligned) conv_dma_kernel<BM, BN, WM, WN, NS, true, true><<<grid, kNT, 0, s>>>(p);
-  else if (!split) conv_dma_kernel<BM, BN, WM, WN, NS, false, false><<<grid, kNT, 0, s>>>(p);
-  else conv_dma_kernel<BM, BN, WM, WN, NS, false, true><<<grid, kNT, 0, s>>>(p);
+  constexpr int kThreads = 64 * WM * WN * KG;
+  if constexpr (KG == 1) {
+    if (aligned && !split) conv_dma_kernel<BM, BN, WM, WN, 1, NS, true, false><<<grid, kThreads, 0, s>>>(p);
+    else if (aligned) conv_dma_kernel<BM, BN, WM, WN, 1, NS, true, true><<<grid, kThreads, 0, s>>>(p);
+    else if (!split) conv_dma_kernel<BM, BN, WM, WN, 1, NS, false, false><<<grid, kThreads, 0, s>>>(p);
+    else conv_dma_kernel<BM, BN, WM, WN, 1, NS, false, true><<<grid, kThreads, 0, s>>>(p);
+  } else {
+    if (aligned) conv_dma_kernel<BM, BN, WM, WN, KG, NS, true, false><<<grid, kThreads, 0, s>>>(p);
+    else conv_dma_kernel<BM, BN, WM, WN, KG, NS, false, false><<<grid, kThreads, 0, s>>>(p);
+  }
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int KG>
 hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
-  constexpr int kStage = (BM + BN) * 128;  // bytes of one ring buffer
-  if (ns == 2) return launch_tile<BM, BN, WM, WN, 2>(p, s);
-  if constexpr (3 * kStage <= 160 * 1024 - 32)
-    if (ns == 3) return launch_tile<BM, BN, WM, WN, 3>(p, s);
-  if constexpr (4 * kStage <= 160 * 1024 - 32)
-    if (ns == 4) return launch_tile<BM, BN, WM, WN, 4>(p, s);
+  constexpr int kStage = (BM + BN) * 128 * KG;  // bytes of one ring slot, all groups
+  if (ns == 2) return launch_tile<BM, BN, WM, WN, KG, 2>(p, s);
+  if constexpr (3 * kStage <= 160 * 1024)
+    if (ns == 3) return launch_tile<BM, BN, WM, WN, KG, 3>(p, s);
+  if constexpr (4 * kStage <= 160 * 1024)
+    if (ns == 4) return launch_tile<BM, BN, WM, WN, KG, 4>(p, s);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-bool conv_dma_tile_supported(int bm, int bn, int stages, int threads) {
-  if (stages < 2 || stages > 4) return false;
-  if ((bm + bn) * 128 * stages > 160 * 1024 - 32) return false;  // LDS of the stage ring
-  if (threads == 256)
+bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
+  if (stages < 2 || stages > 4 || (kgroups != 1 && kgroups != 2)) return false;
+  if ((bm + bn) * 128 * stages * kgroups > 160 * 1024) return false;  // LDS of the stage rings
+  const int waves = threads / (64 * kgroups);  // per reduction group
+  if (threads != 64 * waves * kgroups) return false;
+  if (waves == 4)
     return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
            (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
-  if (threads == 512) return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128);
+  if (waves == 8 && kgroups == 1)
+    return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128);
   return false;
 }
 
-hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s) {
-  if (!conv_dma_tile_supported(bm, bn, stages, threads)) return hipErrorInvalidValue;
-  if (threads == 512) {
-    if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 4>(p, stages, s);
-    if (bm == 128 && bn == 64) return launch_stages<128, 64, 4, 2>(p, stages, s);
-    if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 4>(p, stages, s);
+hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, int kgroups,
+                           hipStream_t s) {
+  if (!conv_dma_tile_supported(bm, bn, stages, threads, kgroups)) return hipErrorInvalidValue;
+  if (kgroups == 2) {
+    if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2, 2>(p, stages, s);
+    if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2, 2>(p, stages, s);
+    if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 2, 2>(p, stages, s);
+    if (bm == 64 && bn == 64) return launch_stages<64, 64, 2, 2, 2>(p, stages, s);
+    if (bm == 32 && bn == 64) return launch_stages<32, 64, 1, 4, 2>(p, stages, s);
     return hipErrorInvalidValue;
   }
-  if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2>(p, stages, s);
-  if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2>(p, stages, s);
-  if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 2>(p, stages, s);
-  if (bm == 64 && bn == 64) return launch_stages<64, 64, 2, 2>(p, stages, s);
-  if (bm == 32 && bn == 64) return launch_stages<32, 64, 1, 4>(p, stages, s);
+  if (threads == 512) {
+    if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 4, 1>(p, stages, s);
+    if (bm == 128 && bn == 64) return launch_stages<128, 64, 4, 2, 1>(p, stages, s);
+    if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 4, 1>(p, stages, s);
+    return hipErrorInvalidValue;
+  }
+  if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2, 1>(p, stages, s);
+  if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2, 1>(p, stages, s);
+  if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 2, 1>(p, stages, s);
+  if (bm == 64 && bn == 64) return launch_stages<64, 64, 2, 2, 1>(p, stages, s);
+  if (bm == 32 && bn == 64) return launch_stages<32, 64, 1, 4, 1>(p, stages, s);
   return hipErrorInvalidValue;
 }
 

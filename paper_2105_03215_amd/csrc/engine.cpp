@@ -43,12 +43,17 @@ struct PackJob {
 // few tiles and the reduction is long enough to share.
 void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* kps) {
   // Measured on MI355X over the ResNet-50 layers: 64x64 tiles (16x16x32
-  // MFMA) win at every batch-32 shape - larger tiles leave fewer workgroups
+  // MFMA) win at most batch-32 shapes - larger tiles leave fewer workgroups
   // per CU to overlap each one's load/compute/epilogue phases - and split-K
-  // only pays when the output has very few tiles.
+  // only pays when the output has very few tiles.  Layers with few tiles and
+  // a long reduction are latency bound: there two reduction groups per
+  // workgroup (HBM->LDS pipeline) double the loads in flight.
   t->bm = M >= 48 ? 64 : 32;
   t->bn = 64;
   t->mf = 16;
+  t->stages = 0;
+  t->threads = 256;
+  t->kgroups = 1;
   const int nk = (int)((Kg + kKPad - 1) / kKPad);
   const int64_t tiles = ((M + t->bm - 1) / t->bm) * ((Kp + t->bn - 1) / t->bn);
   *splits = 1;
@@ -61,6 +66,11 @@ void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* 
       *splits = (nk + *kps - 1) / *kps;
     }
   }
+  if (*splits == 1 && tiles <= 256 && nk >= 8) {
+    t->stages = 3;
+    t->threads = 512;
+    t->kgroups = 2;
+  }
 }
 
 // Tuning override (environment, read at engine creation):
@@ -72,14 +82,16 @@ void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
     int bm = 0, bn = 0, mf = 16;
     int ns = 0;
     if (e[0] == 'd') {
-      // d<bm>x<bn>s<stages>[t<threads>]: direct HBM->LDS pipeline
-      int nt = 256;
-      if (std::sscanf(e + 1, "%dx%ds%dt%d", &bm, &bn, &ns, &nt) >= 3 && conv_dma_tile_supported(bm, bn, ns, nt)) {
+      // d<bm>x<bn>s<stages>[t<threads>[k<groups>]]: direct HBM->LDS pipeline
+      int nt = 256, kgr = 1;
+      if (std::sscanf(e + 1, "%dx%ds%dt%dk%d", &bm, &bn, &ns, &nt, &kgr) >= 3 &&
+          conv_dma_tile_supported(bm, bn, ns, nt, kgr)) {
         t->bm = bm;
         t->bn = bn;
         t->mf = 16;
         t->stages = ns;
         t->threads = nt;
+        t->kgroups = kgr;
       }
     } else {
       const int got = std::sscanf(e, "%dx%dx%d", &bm, &bn, &mf);
@@ -90,6 +102,11 @@ void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
         t->stages = 0;
       }
     }
+  }
+  if (t->kgroups > 1) {  // reduction groups replace split-K
+    *splits = 1;
+    *kps = (Kg + kKPad - 1) / kKPad;
+    return;
   }
   if (const char* e = std::getenv("BYOC_CONV_SPLIT")) {
     const int nk = (Kg + kKPad - 1) / kKPad;
@@ -126,8 +143,8 @@ int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
 
 void name_conv(Launch& L) {
   if (L.tile.stages > 0)
-    std::snprintf(L.info.name, sizeof(L.info.name), "conv_dma_%dx%d_s%d_w%d_split%d", L.tile.bm, L.tile.bn,
-                  L.tile.stages, L.tile.threads / 64, L.conv.splits);
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_dma_%dx%d_s%d_w%d_k%d_split%d", L.tile.bm, L.tile.bn,
+                  L.tile.stages, L.tile.threads / 64, L.tile.kgroups, L.conv.splits);
   else
     std::snprintf(L.info.name, sizeof(L.info.name), "conv_mfma_%dx%d_mf%d_split%d", L.tile.bm, L.tile.bn,
                   L.tile.mf, L.conv.splits);
@@ -636,7 +653,8 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.y = (bf16_t*)c.ptr(L.y);
       p.partial = (float*)c.ptr(L.partial);
       if (L.op == Launch::SplitReduce) return launch_splitk_reduce(p, c.s);
-      return L.tile.stages > 0 ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, c.s)
+      return L.tile.stages > 0
+                 ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, L.tile.kgroups, c.s)
                                : launch_conv_mfma(p, L.tile, c.s);
     }
     case Launch::ConvF32: {
@@ -877,6 +895,7 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
   c.push_back(L.tile_default);
   if (L.conv.splits > 1 || L.tile_default.mf != 16) return c;
   const ConvParams& p = L.conv;
+  const int kgr = L.tile_default.kgroups;  // the reduction order class of the built-in choice
   const int bms[] = {32, 64, 128}, bns[] = {64, 128};
   for (int nt : {256, 512})
     for (int bm : bms)
@@ -885,16 +904,28 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
         if (bm == 128 && p.M < 4096) continue;
         if (bn == 128 && p.Kp < 128) continue;
         for (int ns = 2; ns <= 4; ++ns) {
-          if (!conv_dma_tile_supported(bm, bn, ns, nt)) continue;
+          const int threads = nt * kgr;
+          if (kgr > 1 && nt != 256) continue;
+          if (!conv_dma_tile_supported(bm, bn, ns, threads, kgr)) continue;
           ConvTile t;
           t.bm = bm;
           t.bn = bn;
           t.mf = 16;
           t.stages = ns;
-          t.threads = nt;
+          t.threads = threads;
+          t.kgroups = kgr;
+          if (t.bm == L.tile_default.bm && t.bn == L.tile_default.bn && t.stages == L.tile_default.stages &&
+              t.threads == L.tile_default.threads)
+            continue;  // the built-in choice is candidate 0 already
           c.push_back(t);
         }
       }
+  if (kgr == 1 && L.tile_default.stages > 0) {  // the register-staged kernel as well
+    ConvTile t;
+    t.bm = L.conv.M >= 48 ? 64 : 32;
+    t.bn = 64;
+    c.push_back(t);
+  }
   return c;
 }
 

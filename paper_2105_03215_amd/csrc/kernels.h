@@ -55,14 +55,16 @@ struct ConvTile {
   int mf = 16;      // MFMA shape: 16 (16x16x32) or 32 (32x32x16)
   int stages = 0;   // > 0: HBM->LDS pipeline of that many stages (conv_dma)
   int threads = 256;  // conv_dma workgroup size: 256 (4 waves) or 512 (8 waves)
+  int kgroups = 1;    // conv_dma reduction groups (2: two 4-wave groups split the reduction stages)
 };
 
 // Tile configurations with a compiled kernel.
 bool conv_mfma_tile_supported(int bm, int bn, int mf);
 hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
 // Direct HBM->LDS pipelined variant (16x16x32 MFMA only).
-bool conv_dma_tile_supported(int bm, int bn, int stages, int threads);
-hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s);
+bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups);
+hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, int kgroups,
+                           hipStream_t s);
 // Fused stem: conv (C <= 4 NCHW input channels, 64 output channels) + bias
 // + activation followed by max pooling; output NHWC bf16 with 64 channels.
 struct StemParams {
