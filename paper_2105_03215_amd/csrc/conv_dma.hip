@@ -47,6 +47,7 @@ constexpr int kBK = 64;                 // reduction elements per stage
 constexpr int kCH = kBK / 8;            // 16-byte chunks per tile row
 constexpr int kBufferFlags = 0x00020000;  // raw (untyped) buffer access, gfx9 word 3
 constexpr uint32_t kOOB = 0x80000000u;    // offset past any buffer: reads zeros
+constexpr int kLdsLimit = 160 * 1024;     // LDS bytes per workgroup on gfx950
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
@@ -99,6 +100,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   // g, g + KG, ...), which multiplies the loads in flight and the MFMA issue
   // of a workgroup; the groups' sums are added in group order at the end.
   __shared__ uint4 ring[KG * NS * STAGE];
+  __shared__ float4 sbias[BN / 4];  // bias of the tile's channels
   materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -300,19 +302,12 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   constexpr int EPV = (BM * TPP + kNTall - 1) / kNTall;  // pixels per thread per pass
   const int ec8 = (tid % TPP) * 8;
   uint4 resv[SPLIT ? 1 : NPASS][EPV];
-  float4 biasv[SPLIT ? 1 : NPASS][2];
   if (!SPLIT) {
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<bf16_t*>(p.res), (short)0, p.res ? p.res_bytes : 0, kBufferFlags);
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       const int k = n0 + pass * kEC + ec8;
-      if (p.bias) {
-        biasv[pass][0] = *(const float4*)(p.bias + k);
-        biasv[pass][1] = *(const float4*)(p.bias + k + 4);
-      } else {
-        biasv[pass][0] = biasv[pass][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-      }
 #pragma unroll
       for (int q = 0; q < EPV; ++q) {
         const int px = (tid + q * kNTall) / TPP;
@@ -342,6 +337,13 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
     compute(cur);
   };
 
+  // the tile's bias, straight into LDS (zeros without a bias); issued first,
+  // so every later wait of this wave covers it
+  if (!SPLIT && tid < 64) {
+    const i32x4 br = buffer_rsrc(p.bias, p.bias ? ((p.Kp + 255) / 256) * 256 * 4 : 0);
+    const uint32_t off = lane < BN / 4 ? (uint32_t)(n0 + 4 * lane) * 4u : kOOB;
+    lds_fill16(br, __builtin_amdgcn_readfirstlane(lds_addr(sbias)), off);
+  }
   issue(S0{});
   if constexpr (NS > 2) issue(S1{});
   if constexpr (NS > 3) issue(S2{});
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
           hi.x += h2.x; hi.y += h2.y; hi.z += h2.z; hi.w += h2.w;
         }
         float f[8], rv[8];
-        const float4 b0 = biasv[pass][0], b1 = biasv[pass][1];
+        const float4 b0 = sbias[(pass * kEC + ec8) / 4], b1 = sbias[(pass * kEC + ec8) / 4 + 1];
         unpack8(resv[pass][q], rv);
         f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
         f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
@@ -487,10 +489,12 @@ hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
 template <int BM, int BN, int WM, int WN, int KG>
 hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
   constexpr int kStage = (BM + BN) * 128 * KG;  // bytes of one ring slot, all groups
-  if (ns == 2) return launch_tile<BM, BN, WM, WN, KG, 2>(p, s);
-  if constexpr (3 * kStage <= 160 * 1024)
+  constexpr int kFixed = BN * 4;                 // the bias tile
+  if constexpr (2 * kStage + kFixed <= kLdsLimit)
+    if (ns == 2) return launch_tile<BM, BN, WM, WN, KG, 2>(p, s);
+  if constexpr (3 * kStage + kFixed <= kLdsLimit)
     if (ns == 3) return launch_tile<BM, BN, WM, WN, KG, 3>(p, s);
-  if constexpr (4 * kStage <= 160 * 1024)
+  if constexpr (4 * kStage + kFixed <= kLdsLimit)
     if (ns == 4) return launch_tile<BM, BN, WM, WN, KG, 4>(p, s);
   return hipErrorInvalidValue;
 }
@@ -499,14 +503,16 @@ hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
 
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
   if (stages < 2 || stages > 4 || (kgroups != 1 && kgroups != 2)) return false;
-  if ((bm + bn) * 128 * stages * kgroups > 160 * 1024) return false;  // LDS of the stage rings
+  if ((bm + bn) * 128 * stages * kgroups + bn * 4 > kLdsLimit) return false;  // LDS: stage rings + bias
   const int waves = threads / (64 * kgroups);  // per reduction group
   if (threads != 64 * waves * kgroups) return false;
   if (waves == 4)
     return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
-           (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+           (bm == 64 && bn == 64) || (bm == 32 && bn == 64) ||
+           (kgroups == 1 && ((bm == 64 && bn == 256) || (bm == 256 && bn == 64)));
   if (waves == 8 && kgroups == 1)
-    return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128);
+    return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
+           (bm == 128 && bn == 256) || (bm == 256 && bn == 128);
   return false;
 }
 
@@ -522,11 +528,15 @@ hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int 
     return hipErrorInvalidValue;
   }
   if (threads == 512) {
+    if (bm == 128 && bn == 256) return launch_stages<128, 256, 2, 4, 1>(p, stages, s);
+    if (bm == 256 && bn == 128) return launch_stages<256, 128, 4, 2, 1>(p, stages, s);
     if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 4, 1>(p, stages, s);
     if (bm == 128 && bn == 64) return launch_stages<128, 64, 4, 2, 1>(p, stages, s);
     if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 4, 1>(p, stages, s);
     return hipErrorInvalidValue;
   }
+  if (bm == 64 && bn == 256) return launch_stages<64, 256, 1, 4, 1>(p, stages, s);
+  if (bm == 256 && bn == 64) return launch_stages<256, 64, 4, 1, 1>(p, stages, s);
   if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2, 1>(p, stages, s);
   if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2, 1>(p, stages, s);
   if (bm == 64 && bn == 128) return launch_stages<64, 128, 2, 2, 1>(p, stages, s);

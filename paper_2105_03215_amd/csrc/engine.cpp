@@ -896,13 +896,13 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
   if (L.conv.splits > 1 || L.tile_default.mf != 16) return c;
   const ConvParams& p = L.conv;
   const int kgr = L.tile_default.kgroups;  // the reduction order class of the built-in choice
-  const int bms[] = {32, 64, 128}, bns[] = {64, 128};
+  const int bms[] = {32, 64, 128, 256}, bns[] = {64, 128, 256};
   for (int nt : {256, 512})
     for (int bm : bms)
       for (int bn : bns) {
         if (bm == 32 && p.M >= 48) continue;
-        if (bm == 128 && p.M < 4096) continue;
-        if (bn == 128 && p.Kp < 128) continue;
+        if (bm >= 128 && p.M < 32 * bm) continue;
+        if (bn >= 128 && p.Kp < bn) continue;
         for (int ns = 2; ns <= 4; ++ns) {
           const int threads = nt * kgr;
           if (kgr > 1 && nt != 256) continue;
