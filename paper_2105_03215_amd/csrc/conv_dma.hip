@@ -87,7 +87,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   constexpr int kNT = 64 * WM * WN;          // threads of one reduction group
   constexpr int kNTall = kNT * KG;           // threads per workgroup
   constexpr int kRowsPerPass = kNT / kCH;    // rows one load instruction of every wave covers
-  static_assert(NS >= 2 && NS <= 4, "stages");
+  static_assert(NS >= 1 && NS <= 4, "stages");
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;  // 16x16 MFMA tiles per wave
   constexpr int AR = BM / kRowsPerPass, BR = BN / kRowsPerPass;
@@ -332,9 +332,16 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   // visible and every wave is done with stage t-1, whose buffer the fills
   // of stage t+NS-1 then reuse.
   auto step = [&](auto cur, auto nxt) {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 2) * LPS) : "memory");
-    issue(nxt);
-    compute(cur);
+    if constexpr (NS == 1) {  // single buffer: load, compute, then refill it
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      compute(cur);
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      issue(nxt);
+    } else {
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 2) * LPS) : "memory");
+      issue(nxt);
+      compute(cur);
+    }
   };
 
   // the tile's bias, straight into LDS (zeros without a bias); issued first,
@@ -350,7 +357,9 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   // full groups of NS stages (stage t in buffer t % NS), then the tail
   int t = 0;
   for (; t + NS <= nkt; t += NS) {
-    if constexpr (NS == 2) {
+    if constexpr (NS == 1) {
+      step(S0{}, S0{});
+    } else if constexpr (NS == 2) {
       step(S0{}, S1{});
       step(S1{}, S0{});
     } else if constexpr (NS == 3) {
@@ -365,8 +374,9 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
     }
   }
   const int rem = nkt - t;
-  if (rem > 0) {
-    if constexpr (NS == 2) step(S0{}, S1{});
+  if (NS > 1 && rem > 0) {
+    if constexpr (NS == 1) step(S0{}, S0{});
+    else if constexpr (NS == 2) step(S0{}, S1{});
     else if constexpr (NS == 3) step(S0{}, S2{});
     else step(S0{}, S3{});
   }
@@ -490,6 +500,7 @@ template <int BM, int BN, int WM, int WN, int KG>
 hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
   constexpr int kStage = (BM + BN) * 128 * KG;  // bytes of one ring slot, all groups
   constexpr int kFixed = BN * 4;                 // the bias tile
+  if (ns == 1) return launch_tile<BM, BN, WM, WN, KG, 1>(p, s);
   if constexpr (2 * kStage + kFixed <= kLdsLimit)
     if (ns == 2) return launch_tile<BM, BN, WM, WN, KG, 2>(p, s);
   if constexpr (3 * kStage + kFixed <= kLdsLimit)
@@ -502,7 +513,7 @@ hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
 }  // namespace
 
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
-  if (stages < 2 || stages > 4 || (kgroups != 1 && kgroups != 2)) return false;
+  if (stages < 1 || stages > 4 || (kgroups != 1 && kgroups != 2)) return false;
   if ((bm + bn) * 128 * stages * kgroups + bn * 4 > kLdsLimit) return false;  // LDS: stage rings + bias
   const int waves = threads / (64 * kgroups);  // per reduction group
   if (threads != 64 * waves * kgroups) return false;

@@ -275,6 +275,9 @@ void Planner::plan_stem(int ci, int pi) {
   p.PO = (int)ps[2], p.QO = (int)ps[3];
   p.act = (int)c.act;
   p.wld = stem_weight_ld(p.R);
+  // BYOC_STEM_GRID=<n>: at most n persistent workgroups (tests drive several
+  // tiles through one workgroup on small inputs with it)
+  if (const char* ev = std::getenv("BYOC_STEM_GRID")) p.grid_cap = std::max(0, std::atoi(ev));
   const int wc = g.values[c.weight].index;
   const int bc = c.bias >= 0 ? g.values[c.bias].index : -1;
   L.w = wslot((int64_t)64 * p.wld * 2);
@@ -903,7 +906,7 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
         if (bm == 32 && p.M >= 48) continue;
         if (bm >= 128 && p.M < 32 * bm) continue;
         if (bn >= 128 && p.Kp < bn) continue;
-        for (int ns = 2; ns <= 4; ++ns) {
+        for (int ns = 1; ns <= 4; ++ns) {
           const int threads = nt * kgr;
           if (kgr > 1 && nt != 256) continue;
           if (!conv_dma_tile_supported(bm, bn, ns, threads, kgr)) continue;

@@ -80,6 +80,7 @@ struct StemParams {
   int kph, kpw, sph, spw, ppt, ppl;  // pool window, stride, padding
   int PO, QO;                    // pool output size
   int act;
+  int grid_cap;                  // > 0: at most this many workgroups
 };
 bool stem_supported(int C, int K, int R, int S, int sh, int sw, int kph, int kpw, int sph, int spw);
 int stem_weight_ld(int R);

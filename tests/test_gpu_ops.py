@@ -195,6 +195,7 @@ STEM_CASES = [
     ("stem_f32_c1", (1, 1, 32, 30), 7, 2, 3, "relu", (3, 2, 1), "f32"),
     ("stem_3x3_s1_pool2", (2, 4, 20, 21), 3, 1, 1, None, (2, 2, 0), "bf16"),
     ("stem_5x5_s2_pool3_s1", (1, 3, 24, 24), 5, 2, 2, "relu6", (3, 1, 1), "bf16"),
+    ("resnet_stem_f32_aligned", (2, 3, 48, 48), 7, 2, 3, "relu", (3, 2, 1), "f32"),
 ]
 
 
@@ -212,3 +213,27 @@ def test_fused_stem_conv_maxpool(case):
     launches = _check_bf16(g.finish(), "stem " + name)
     names = [l["name"] for l in launches]
     assert names[0] == "stem_conv_maxpool" and "nchw_to_nhwc" not in names, names
+
+
+# (case, workgroups): each workgroup walks several tiles, so the patch
+# prefetch of the next tile and the tile loop's LDS reuse are exercised
+STEM_LOOP_CASES = [
+    (("resnet_stem_12_tiles", (3, 3, 64, 64), 7, 2, 3, "relu", (3, 2, 1), "bf16"), 3),
+    (("resnet_stem_ragged_8_tiles", (2, 3, 45, 45), 7, 2, 3, "relu", (3, 2, 1), "bf16"), 3),
+    (("stem_f32_8_tiles", (2, 3, 48, 48), 7, 2, 3, "gelu", (3, 2, 1), "f32"), 2),
+]
+
+
+@pytest.mark.parametrize("case,grid", STEM_LOOP_CASES, ids=[c[0][0] for c in STEM_LOOP_CASES])
+def test_fused_stem_tile_loop(case, grid, monkeypatch):
+    """Fewer persistent workgroups than tiles: results match the oracle
+    for every tile a workgroup computes after its first."""
+    monkeypatch.setenv("BYOC_STEM_GRID", str(grid))
+    name, shape, r, stride, pad, act, (ps, pst, ppad), dt = case
+    g = GraphBuilder("stem_loop_" + name, 1700 + [c[0] for c in STEM_LOOP_CASES].index(case))
+    x = g.input("x", list(shape), "uniform", dtype=dt)
+    y = g.conv(x, 64, r, stride=stride, pad=pad, act=act, name="conv")
+    p = g.max_pool(y, ps, pst, ppad, name="pool")
+    g.output(p)
+    launches = _check_bf16(g.finish(), "stem loop %s grid %d" % (name, grid))
+    assert launches[0]["name"] == "stem_conv_maxpool", launches[0]
