@@ -45,8 +45,6 @@ typedef __attribute__((ext_vector_type(4))) int i32x4;
 
 constexpr int kBK = 64;                 // reduction elements per stage
 constexpr int kCH = kBK / 8;            // 16-byte chunks per tile row
-constexpr int kBufferFlags = 0x00020000;  // raw (untyped) buffer access, gfx9 word 3
-constexpr uint32_t kOOB = 0x80000000u;    // offset past any buffer: reads zeros
 constexpr int kLdsLimit = 160 * 1024;     // LDS bytes per workgroup on gfx950
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }

@@ -10,6 +10,11 @@
 
 namespace byoc {
 
+// Raw buffer accesses: descriptor word 3 for untyped access on gfx9, and an
+// offset past any buffer (reads return zeros, nothing is fetched).
+constexpr int kBufferFlags = 0x00020000;
+constexpr uint32_t kOOB = 0x80000000u;
+
 __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
   return __uint_as_float(((uint32_t)h) << 16);
 }
@@ -20,8 +25,11 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return __builtin_bit_cast(bf16_t, v);
 }
 
+// Two values in one v_cvt_pk_bf16_f32 (same rounding as f32_to_bf16).
 __device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
-  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
 // x * Phi(x) with Phi(x) = erfc(-x / sqrt 2) / 2: no cancellation for x << 0.
@@ -31,23 +39,21 @@ __device__ __attribute__((noinline)) float gelu(float v) { return 0.5f * v * erf
 
 // Epilogue activation.  Kernels pick the GELU or the clamp instantiation
 // once (the choice is uniform), so the per-element code has no branch:
-// none / ReLU / ReLU6 are one median-of-three clamp to [0, hi] (or the
-// value itself for none), GELU the out-of-line call above.
+// none / ReLU / ReLU6 are one median-of-three clamp to [lo, hi] (none:
+// [-inf, +inf], the value itself), GELU the out-of-line call above.
 struct ActClamp {
-  float hi;   // 6 for ReLU6, +inf otherwise
-  bool none;  // no activation
+  float lo;  // 0, or -inf for no activation
+  float hi;  // 6 for ReLU6, +inf otherwise
 };
 __device__ __forceinline__ ActClamp act_clamp_of(int act) {
-  return ActClamp{act == kActRelu6 ? 6.0f : INFINITY, act == kActNone};
+  return ActClamp{act == kActNone ? -INFINITY : 0.0f, act == kActRelu6 ? 6.0f : INFINITY};
 }
 template <bool GELU>
 __device__ __forceinline__ float act_apply(float v, ActClamp a) {
-  if constexpr (GELU) {
+  if constexpr (GELU)
     return gelu(v);
-  } else {
-    const float c = __builtin_amdgcn_fmed3f(v, 0.0f, a.hi);
-    return a.none ? v : c;
-  }
+  else
+    return __builtin_amdgcn_fmed3f(v, a.lo, a.hi);
 }
 __device__ __forceinline__ float apply_act(float v, int act) {
   return act == kActGelu ? gelu(v) : act_apply<false>(v, act_clamp_of(act));

@@ -8,25 +8,28 @@
 // (Sec. 3.2) that the input would otherwise need.  Values are those of the
 // unfused chain: each conv output is rounded to bf16 before the pooling max.
 //
-// Work unit ("tile"): one 8x8 block of pooled outputs x 64 channels of one
-// image.  It needs the (7*sp + kp)^2 conv outputs its windows cover (at most
-// 17x17 for a 3x3 / stride-2 pool), so neighbouring tiles recompute a border
-// of one conv row and column.  Workgroups are persistent (two per CU, 256
-// threads each) and stride over the tiles:
-//  - the packed weights [64][R*32 + 8] are staged in LDS once;
+// Work unit ("tile"): TH = 8 rows x TW columns of pooled outputs x 64
+// channels of one image, TW = (16 - pool width) / pool stride + 1 (7 for a
+// 3x3 / stride-2 pool).  Each of the 4 waves computes two pooled rows: the
+// conv rows their windows cover (sph + kph <= 5 rows, a row shared with the
+// next wave is recomputed), each row a 16-pixel MFMA tile whose lane l holds
+// conv column l.  So the pooling never leaves registers: the window's rows
+// are accumulators of the same lane, its columns neighbouring lanes (DPP
+// row shifts).  Workgroups are persistent (256 threads) and stride over
+// the tiles:
+//  - the packed weights [64][R*32 + 8] and the bias are staged in LDS once;
 //  - the input patch of a tile is staged in LDS as [row][col][4 channels]
 //    bf16 cells (zero outside the image); the global loads of the next
-//    tile's patch are issued at the end of a tile and land in registers
-//    while the current tile computes;
+//    tile's patch are issued one tile ahead and land in registers while
+//    the current tile computes;
 //  - implicit GEMM on v_mfma_f32_16x16x32_bf16: one 32-element reduction
 //    step per kernel row r, ordered (tap s < 8, channel c < 4); a lane's 8
 //    reduction elements are taps 2g and 2g+1 of its conv pixel, i.e. two
-//    adjacent patch cells.  Weights are the A operand, pixels B;
-//  - bias, activation and bf16 rounding; the conv tile goes to LDS over the
-//    dead patch (conv outputs outside the image as -inf, which never win
-//    the max);
-//  - each thread pools 8 channels of two pooled pixels; the 16-byte NHWC
-//    stores go out after the next patch is in LDS.
+//    adjacent patch cells.  Weights are the A operand, pixels B, and the
+//    accumulators start at the bias;
+//  - activation, -inf for conv outputs outside the image (they never win
+//    the max), max over the window, bf16 rounding (monotone, so rounding
+//    after the max equals the max of rounded values), 8-byte NHWC stores.
 // Barriers inside the tile loop wait on LDS only, so the patch loads in
 // flight cross them.
 #include "device_common.h"
@@ -40,24 +43,33 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int kThreads = 256;
-constexpr int kPI = 8, kPJ = 8;  // pooled outputs per tile
-constexpr int kCMax = 17;        // conv rows / cols per tile (7 * 2 + 3)
-constexpr int kPR = 40;          // patch rows: (kCMax - 1) * 2 + 8
-constexpr int kPC = 48;          // patch cols: (kCMax - 1) * 2 + 8 + 3 (alignment offset), in 4-cell segments
+constexpr int kTH = 8;        // pooled rows per tile (2 per wave)
+constexpr int kRowsWave = 5;  // conv rows (MFMA tiles) per wave: sph + kph <= 5
+constexpr int kPR = 40;       // patch rows: (3 * 2 * 2 + 4) * 2 + 8
+constexpr int kPC = 48;       // patch cols: 15 * 2 + 8 + 3 (alignment offset), in 4-cell segments
 constexpr int kSegs = kPC / 4;
 constexpr int kUnits = (kPR * kSegs + kThreads - 1) / kThreads;  // (row, segment) units per thread
-constexpr int kK = 64;           // output channels
-constexpr int kTileLd = kK + 8;  // conv tile row (bf16): 144 bytes, 16 rows on distinct banks
-constexpr int kFrags = (kCMax * kCMax + 15) / 16;  // 16-pixel MFMA tiles (19)
-constexpr int kFragsPerWave = (kFrags + 3) / 4;    // 5
+constexpr int kK = 64;                                           // output channels
 constexpr int kWeightLdMax = 8 * 32 + 8;
-constexpr int kWeightBytes = kK * kWeightLdMax * 2;
-constexpr int kPatchBytes = kPR * kPC * 8;
-constexpr int kTileBytes = kCMax * kCMax * kTileLd * 2;
-constexpr int kLdsBytes = kWeightBytes + (kPatchBytes > kTileBytes ? kPatchBytes : kTileBytes);
-static_assert(2 * kLdsBytes <= 160 * 1024, "two workgroups per CU");
+constexpr int kWChunks = (kK * kWeightLdMax / 8 + kThreads - 1) / kThreads;  // 16-byte weight chunks per thread
+constexpr int kWeightBytes = kWChunks * kThreads * 16;  // >= 64 rows of kWeightLdMax; every thread fills its chunks
+constexpr int kBiasBytes = kK * 4;
+constexpr int kPatchBytes = kUnits * kThreads * 32;  // every thread writes its units, the last ones past the patch
+constexpr int kLdsBytes = kWeightBytes + kBiasBytes + kPatchBytes;
+static_assert(kPatchBytes >= kPR * kPC * 8, "patch");
+static_assert(3 * kLdsBytes <= 160 * 1024, "three workgroups per CU");
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+// max(a, b) in one instruction (median of a, b and +inf); no NaN handling
+__device__ __forceinline__ float max2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, INFINITY); }
+
+// Lane l + k of the same 16-lane row (k = 1, 2); lanes past the row's end
+// read their own value (they are never kept).
+template <int K>
+__device__ __forceinline__ float row_next(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x100 + K, 0xF, 0xF, false));
+}
 
 // Input values of one (patch row, 4-column segment) unit, per channel:
 // 4 bf16 (XBF) or 4 f32.
@@ -67,61 +79,66 @@ struct PatchRegs {
   T v[kUnits][4];
 };
 
-// Issues the loads of a tile's patch (rows ir0.., columns ic0.. of image n).
+// Issues the loads of a tile's patch (rows ir0.., columns ic0.. of image n)
+// through a buffer descriptor over the image: positions outside the image
+// take an out-of-range offset and read zeros, so every load is issued
+// unconditionally and back to back, and no select follows it.
 // VEC: a segment is one vector load (W % 4 == 0 and ic0 % 4 == 0, so a
 // segment is wholly inside or outside the image); else per-element loads.
-// Every load is unconditional (out-of-image lanes read element 0 and are
-// zeroed), so they all issue back to back.
 template <bool VEC, bool XBF>
 __device__ __forceinline__ void load_patch(PatchRegs<XBF>& r, const StemParams& p, int n, int ir0, int ic0,
                                            int tid) {
-  using E = std::conditional_t<XBF, uint16_t, float>;
-  const E* x = static_cast<const E*>(p.x);
+  constexpr int kE = XBF ? 2 : 4;       // element bytes
+  const int img = p.C * p.H * p.W * kE;  // image bytes (< 2^31, checked by the launcher)
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(static_cast<const char*>(p.x)) + (size_t)n * img, (short)0, img, kBufferFlags);
 #pragma unroll
   for (int u = 0; u < kUnits; ++u) {
     const int unit = tid + u * kThreads;
     const int row = unit / kSegs, seg = unit - (unit / kSegs) * kSegs;
     const int ih = ir0 + row, iw0 = ic0 + 4 * seg;
-    const bool rok = unit < kPR * kSegs && (unsigned)ih < (unsigned)p.H;
+    // non-short-circuit tests: the offsets are selects, not branches
+    const bool rok = (unit < kPR * kSegs) & ((unsigned)ih < (unsigned)p.H);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const bool cok = rok && c < p.C;
-      const size_t rbase = (((size_t)n * p.C + c) * p.H + ih) * p.W;
+      const bool cok = rok & (c < p.C);
+      const int rbase = (c * p.H + ih) * p.W;  // element offset of the row (used only when in range)
       if constexpr (VEC) {
-        const bool ok = cok && iw0 >= 0 && iw0 < p.W;
-        const size_t o = ok ? rbase + iw0 : 0;
-        if constexpr (XBF) {
-          const uint2 v = *reinterpret_cast<const uint2*>(x + o);
-          r.v[u][c] = ok ? v : make_uint2(0u, 0u);
-        } else {
-          const float4 v = *reinterpret_cast<const float4*>(x + o);
-          r.v[u][c] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        const uint32_t off = (cok & (iw0 >= 0) & (iw0 < p.W)) ? (uint32_t)(rbase + iw0) * kE : kOOB;
+        if constexpr (XBF)
+          r.v[u][c] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+        else
+          r.v[u][c] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
       } else {
-        E e4[4];
+        uint32_t e4[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool ok = cok && (unsigned)(iw0 + e) < (unsigned)p.W;
-          const E v = x[ok ? rbase + iw0 + e : 0];
-          e4[e] = ok ? v : (E)0;
+          const uint32_t off = (cok & ((unsigned)(iw0 + e) < (unsigned)p.W)) ? (uint32_t)(rbase + iw0 + e) * kE : kOOB;
+          if constexpr (XBF)
+            e4[e] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
+          else
+            e4[e] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
         }
         if constexpr (XBF)
-          r.v[u][c] = make_uint2((uint32_t)e4[0] | ((uint32_t)e4[1] << 16), (uint32_t)e4[2] | ((uint32_t)e4[3] << 16));
+          r.v[u][c] = make_uint2(e4[0] | (e4[1] << 16), e4[2] | (e4[3] << 16));
         else
-          r.v[u][c] = make_float4(e4[0], e4[1], e4[2], e4[3]);
+          r.v[u][c] = make_float4(__uint_as_float(e4[0]), __uint_as_float(e4[1]), __uint_as_float(e4[2]),
+                                  __uint_as_float(e4[3]));
       }
     }
   }
 }
 
 // Writes the loaded units as 4-channel cells: unit (row, seg) is cells
-// [row][4 seg .. 4 seg + 3], 32 contiguous bytes.
+// [row][4 seg .. 4 seg + 3], 32 contiguous bytes.  Units past the patch
+// (zeros) land in the padding after it; the writes are unconditional so
+// that every load is waited for on every path (a skipped wait would make
+// the compiler wait again inside the tile loop).
 template <bool XBF>
 __device__ __forceinline__ void store_patch(const PatchRegs<XBF>& r, uint2* patch, int tid) {
 #pragma unroll
   for (int u = 0; u < kUnits; ++u) {
     const int unit = tid + u * kThreads;
-    if (unit >= kPR * kSegs) break;
     uint32_t h[4][4];  // [channel][pixel] bf16 bits
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -148,185 +165,174 @@ __device__ __forceinline__ void store_patch(const PatchRegs<XBF>& r, uint2* patc
 template <bool VEC, bool XBF>
 __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemParams p) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
-  bf16_t* wl = reinterpret_cast<bf16_t*>(lds);                    // [64][wld]
-  uint2* patch = reinterpret_cast<uint2*>(lds + kWeightBytes);    // [kPR][kPC] cells
-  bf16_t* tile = reinterpret_cast<bf16_t*>(lds + kWeightBytes);   // [CR*CC][kTileLd], over the patch
+  bf16_t* wl = reinterpret_cast<bf16_t*>(lds);                               // [64][wld]
+  float* sbias = reinterpret_cast<float*>(lds + kWeightBytes);               // [64]
+  uint2* patch = reinterpret_cast<uint2*>(lds + kWeightBytes + kBiasBytes);  // [kPR][kPC] cells
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane >> 4;
-  const int TJ = (p.QO + kPJ - 1) / kPJ, TI = (p.PO + kPI - 1) / kPI;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int TW = (16 - p.kpw) / p.spw + 1;  // pooled columns per tile
+  const int TJ = (p.QO + TW - 1) / TW, TI = (p.PO + kTH - 1) / kTH;
   const int ntiles = p.N * TI * TJ;
   const int G = gridDim.x;
   int t = blockIdx.x;
   if (t >= ntiles) return;
 
-  const int CR = (kPI - 1) * p.sph + p.kph;  // conv rows / cols of a tile
-  const int CC = (kPJ - 1) * p.spw + p.kpw;
-  const int npix = CR * CC;
-  // patch column 0 sits `off` columns left of the tile's first input column,
-  // so that it is 4-aligned in the image (the same for every tile: tile
-  // origins step by multiples of 4 input columns)
-  const int off = VEC ? (-(p.ppl * p.sw + p.pl)) & 3 : 0;
-  // tile tt: image n, tile row / col ti, tj, global conv row / col of its local (0, 0)
+  // tile tt: image n, tile row / col ti, tj, global conv row / col of the
+  // tile's first conv row / column (lane 0 of wave 0's first MFMA tile)
   auto origin = [&](int tt, int& n, int& ti, int& tj, int& cr0, int& cc0) {
     tj = tt % TJ;
     const int rest = tt / TJ;
     ti = rest % TI;
     n = rest / TI;
-    cr0 = ti * kPI * p.sph - p.ppt;
-    cc0 = tj * kPJ * p.spw - p.ppl;
+    cr0 = ti * kTH * p.sph - p.ppt;
+    cc0 = tj * TW * p.spw - p.ppl;
   };
+  // patch column 0 is the tile's first input column rounded down to a
+  // multiple of 4 (vector loads); `off` is the difference
+  auto col_off = [&](int cc0) { return VEC ? (cc0 * p.sw - p.pl) & 3 : 0; };
   auto issue_patch = [&](PatchRegs<XBF>& r, int tt) {
     int n, ti, tj, cr0, cc0;
     origin(tt, n, ti, tj, cr0, cc0);
-    load_patch<VEC, XBF>(r, p, n, cr0 * p.sh - p.pt, cc0 * p.sw - p.pl - off, tid);
+    load_patch<VEC, XBF>(r, p, n, cr0 * p.sh - p.pt, cc0 * p.sw - p.pl - col_off(cc0), tid);
   };
 
-  // per-lane GEMM addressing, the same for every tile: patch cell of this
-  // lane's pixel at tap (0, 0), and its (row, col) in the conv tile
-  int pbase[kFragsPerWave], lrc[kFragsPerWave];
+  // this wave's conv rows: local rows wave * 2 * sph + f, f < kRowsWave;
+  // patch cell of lane (row f, column l16) at tap (0, 0), before `off`
+  const int lrow0 = wave * 2 * p.sph;
+  int pbase[kRowsWave];
 #pragma unroll
-  for (int i = 0; i < kFragsPerWave; ++i) {
-    const int m0 = (wave + 4 * i) * 16 + (lane & 15);
-    const int m = m0 < npix ? m0 : 0;  // padding rows of the last tile: any valid address
-    const int lr = m / CC, lc = m - (m / CC) * CC;
-    pbase[i] = lr * p.sh * kPC + lc * p.sw + off + 2 * g;
-    lrc[i] = m0 < npix ? (lr << 16) | lc : -1;
-  }
-  // bias of the 16 channels this lane finishes
-  float4 bv[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    bv[j] = p.bias ? *reinterpret_cast<const float4*>(p.bias + j * 16 + 4 * g) : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int f = 0; f < kRowsWave; ++f) pbase[f] = (lrow0 + f) * p.sh * kPC + l16 * p.sw + 2 * g;
 
-  // weights into LDS, once (16-byte chunks, all loads issued before the writes)
+  // weights, bias and the first patch: every load is issued before the
+  // first LDS write, and all are unconditional (buffer loads past the end
+  // read zeros), so their latencies overlap.  Values the tile loop uses
+  // never come straight from a global load: the compiler's wait tracking
+  // would then stall the loop on the patch loads in flight.
   {
-    constexpr int kWChunks = (kK * kWeightLdMax / 8 + kThreads - 1) / kThreads;
-    const uint4* src = reinterpret_cast<const uint4*>(p.w);
-    uint4* dst = reinterpret_cast<uint4*>(wl);
-    const int chunks = kK * p.wld / 8;
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p.w), (short)0,
+                                                                         kK * p.wld * 2, kBufferFlags);
     uint4 wv[kWChunks];
 #pragma unroll
-    for (int i = 0; i < kWChunks; ++i) {
-      const int idx = tid + i * kThreads;
-      wv[i] = src[idx < chunks ? idx : 0];
-    }
+    for (int i = 0; i < kWChunks; ++i)
+      wv[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, (uint32_t)(tid + i * kThreads) * 16u, 0, 0));
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.bias), (short)0,
+                                                                         p.bias ? kBiasBytes : 0, kBufferFlags);
+    float4 b = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(br, tid < kK / 4 ? tid * 16u : kOOB, 0, 0));
+    PatchRegs<XBF> first;
+    issue_patch(first, t);
+    asm volatile("" : "+v"(b.x), "+v"(b.y), "+v"(b.z), "+v"(b.w));  // keeps the bias load ahead of the writes
+    uint4* dst = reinterpret_cast<uint4*>(wl);
 #pragma unroll
-    for (int i = 0; i < kWChunks; ++i) {
-      const int idx = tid + i * kThreads;
-      if (idx < chunks) dst[idx] = wv[i];
-    }
+    for (int i = 0; i < kWChunks; ++i) dst[tid + i * kThreads] = wv[i];
+    if (tid < kK / 4) reinterpret_cast<float4*>(sbias)[tid] = b;
+    store_patch<XBF>(first, patch, tid);
   }
   PatchRegs<XBF> pr;
-  issue_patch(pr, t);
-  store_patch<XBF>(pr, patch, tid);
   if (t + G < ntiles) issue_patch(pr, t + G);
   lds_barrier();
 
-  const ActClamp ac = act_clamp_of(p.act);
   for (;;) {
     int n, ti, tj, cr0, cc0;
     origin(t, n, ti, tj, cr0, cc0);
+    const int off = col_off(cc0);
 
-    // implicit GEMM: this wave owns pixel tiles wave, wave + 4, ...
-    f32x4 acc[kFragsPerWave][4];
+    // implicit GEMM.  Accumulators start at the bias of their channels, or
+    // at -inf for conv positions outside the image (then they stay -inf:
+    // the products added are finite), which excludes those positions from
+    // the pooling max.
+    const bool colok = (unsigned)(cc0 + l16) < (unsigned)p.Q;
+    f32x4 acc[kRowsWave][4];
 #pragma unroll
-    for (int i = 0; i < kFragsPerWave; ++i)
+    for (int j = 0; j < 4; ++j) {
+      const float4 b = reinterpret_cast<const float4*>(sbias)[j * 4 + g];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int f = 0; f < kRowsWave; ++f) {
+        const bool ok = colok & ((unsigned)(cr0 + lrow0 + f) < (unsigned)p.P);
+        acc[f][j] = ok ? f32x4{b.x, b.y, b.z, b.w} : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      }
+    }
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
       if (r >= p.R) break;
       bf16x8 a[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        a[j] = as_bf16x8(*reinterpret_cast<const uint4*>(wl + (j * 16 + (lane & 15)) * p.wld + r * 32 + g * 8));
+        a[j] = as_bf16x8(*reinterpret_cast<const uint4*>(wl + (j * 16 + l16) * p.wld + r * 32 + g * 8));
 #pragma unroll
-      for (int i = 0; i < kFragsPerWave; ++i) {  // a wave's surplus tile computes discarded values
-        const uint2 t0 = patch[pbase[i] + r * kPC];
-        const uint2 t1 = patch[pbase[i] + r * kPC + 1];
+      for (int f = 0; f < kRowsWave; ++f) {
+        const uint2 t0 = patch[pbase[f] + off + r * kPC];
+        const uint2 t1 = patch[pbase[f] + off + r * kPC + 1];
         const bf16x8 b = as_bf16x8(make_uint4(t0.x, t0.y, t1.x, t1.y));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], b, acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) acc[f][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], b, acc[f][j], 0, 0, 0);
       }
     }
-    lds_barrier();  // the patch is dead: the conv tile overlays it
+    lds_barrier();  // every wave is done with the patch
 
-    // bias, activation, bf16; conv outputs outside the image -> -inf
-    auto epilogue = [&](auto gelu_tag) {
-      constexpr bool GE = decltype(gelu_tag)::value;
+    // the next tile's patch (its loads were issued a tile ago), then the
+    // loads of the one after
+    const int tn = t + G;
+    if (tn < ntiles) store_patch<XBF>(pr, patch, tid);
+    if (tn + G < ntiles) issue_patch(pr, tn + G);
+
+    // GELU is not monotone: it goes before the max (outside positions stay
+    // -inf).  The clamps (none, ReLU, ReLU6) are, as is bf16 rounding: they
+    // go after it, once per pooled value.
+    if (p.act == kActGelu) {
 #pragma unroll
-      for (int i = 0; i < kFragsPerWave; ++i) {
-        if (lrc[i] < 0) continue;
-        const int lr = lrc[i] >> 16, lc = lrc[i] & 0xFFFF;
-        const int m = lr * CC + lc;
-        const bool inside = (unsigned)(cr0 + lr) < (unsigned)p.P && (unsigned)(cc0 + lc) < (unsigned)p.Q;
+      for (int f = 0; f < kRowsWave; ++f)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float x = acc[f][j][e];
+            acc[f][j][e] = x == -INFINITY ? x : gelu(x);
+          }
+    }
+    const ActClamp ac = p.act == kActGelu ? act_clamp_of(kActNone) : act_clamp_of(p.act);
+
+    // pooled rows 2 wave + q (q < 2): window rows SPH * q + dr of this
+    // wave's conv rows, window columns lanes spw * c + dc.  FULL: a 3x3
+    // window; else rows / columns past the window are masked to -inf.
+    const bool lane_out = (l16 % p.spw == 0) & (l16 / p.spw < TW);
+    const int qo = tj * TW + l16 / p.spw;
+    auto pool = [&](auto sph_tag, auto full_tag) {
+      constexpr int SPH = decltype(sph_tag)::value;
+      constexpr bool FULL = decltype(full_tag)::value;
+      const bool r1 = FULL || p.kph > 1, r2 = FULL || p.kph > 2, c1 = FULL || p.kpw > 1, c2 = FULL || p.kpw > 2;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int po = ti * kTH + 2 * wave + q;
+        const bool st = lane_out & (po < p.PO) & (qo < p.QO);
+        bf16_t* dst = p.y + (((size_t)n * p.PO + po) * p.QO + qo) * kK + 4 * g;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          uint2 o;
-          if (inside) {
-            const f32x4 v = acc[i][j];
-            o = make_uint2(pack2_bf16(act_apply<GE>(v[0] + bv[j].x, ac), act_apply<GE>(v[1] + bv[j].y, ac)),
-                           pack2_bf16(act_apply<GE>(v[2] + bv[j].z, ac), act_apply<GE>(v[3] + bv[j].w, ac)));
-          } else {
-            o = make_uint2(0xFF80FF80u, 0xFF80FF80u);  // bf16 -inf
+          float m[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float v = acc[SPH * q][j][e];
+            v = max2(v, r1 ? acc[SPH * q + 1][j][e] : -INFINITY);
+            v = max2(v, r2 ? acc[SPH * q + 2][j][e] : -INFINITY);
+            const float h1 = row_next<1>(v), h2 = row_next<2>(v);
+            float h = max2(v, c1 ? h1 : -INFINITY);
+            h = max2(h, c2 ? h2 : -INFINITY);
+            m[e] = act_apply<false>(h, ac);
           }
-          *reinterpret_cast<uint2*>(tile + m * kTileLd + j * 16 + 4 * g) = o;
+          if (st) *reinterpret_cast<uint2*>(dst + j * 16) = make_uint2(pack2_bf16(m[0], m[1]), pack2_bf16(m[2], m[3]));
         }
       }
     };
-    if (p.act == kActGelu)
-      epilogue(std::true_type{});
-    else
-      epilogue(std::false_type{});
-    lds_barrier();
-
-    // pooling: 64 pooled pixels x 8 channel groups, two per thread
-    constexpr int kItems = kPI * kPJ * (kK / 8) / kThreads;
-    static_assert(kItems * kThreads == kPI * kPJ * (kK / 8), "pooling items");
-    uint4 outv[kItems];
-#pragma unroll
-    for (int k = 0; k < kItems; ++k) {
-      const int it = tid + k * kThreads;
-      const int c8 = (it & 7) * 8;
-      const int pi = (it >> 3) / kPJ, pj = (it >> 3) % kPJ;
-      float mx[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) mx[e] = -INFINITY;
-      uint4 win[3][3];  // all window reads issued before the first max
-#pragma unroll
-      for (int dr = 0; dr < 3; ++dr)
-#pragma unroll
-        for (int dc = 0; dc < 3; ++dc) {
-          const int m = (pi * p.sph + (dr < p.kph ? dr : 0)) * CC + pj * p.spw + (dc < p.kpw ? dc : 0);
-          win[dr][dc] = *reinterpret_cast<const uint4*>(tile + m * kTileLd + c8);
-        }
-#pragma unroll
-      for (int dr = 0; dr < 3; ++dr)
-#pragma unroll
-        for (int dc = 0; dc < 3; ++dc) {
-          float v[8];
-          unpack8(win[dr][dc], v);  // taps past the window repeat its first one: no effect on the max
-#pragma unroll
-          for (int e = 0; e < 8; ++e) mx[e] = fmaxf(mx[e], v[e]);
-        }
-      outv[k] = pack8(mx);
-    }
-    lds_barrier();  // the conv tile is dead: the next patch overlays it
-
-    const int tn = t + G;
-    if (tn < ntiles) store_patch<XBF>(pr, patch, tid);
-#pragma unroll
-    for (int k = 0; k < kItems; ++k) {
-      const int it = tid + k * kThreads;
-      const int c8 = (it & 7) * 8;
-      const int po = ti * kPI + (it >> 3) / kPJ, qo = tj * kPJ + (it >> 3) % kPJ;
-      if (po < p.PO && qo < p.QO)
-        *reinterpret_cast<uint4*>(p.y + (((size_t)n * p.PO + po) * p.QO + qo) * kK + c8) = outv[k];
+    const bool full = p.kph == 3 && p.kpw == 3;
+    if (p.sph == 2) {
+      if (full) pool(std::integral_constant<int, 2>{}, std::true_type{});
+      else pool(std::integral_constant<int, 2>{}, std::false_type{});
+    } else {
+      if (full) pool(std::integral_constant<int, 1>{}, std::true_type{});
+      else pool(std::integral_constant<int, 1>{}, std::false_type{});
     }
     if (tn >= ntiles) break;
-    if (tn + G < ntiles) issue_patch(pr, tn + G);
-    lds_barrier();
+    lds_barrier();  // the next patch is in LDS
     t = tn;
   }
 }
@@ -367,9 +373,12 @@ hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s) {
     if (e != hipSuccess) return e;
     cus.store(n > 0 ? n : 1);
   }
-  const int64_t tiles = (int64_t)p.N * ((p.PO + kPI - 1) / kPI) * ((p.QO + kPJ - 1) / kPJ);
+  const int tw = (16 - p.kpw) / p.spw + 1;
+  const int64_t tiles = (int64_t)p.N * ((p.PO + kTH - 1) / kTH) * ((p.QO + tw - 1) / tw);
   if (tiles <= 0) return hipSuccess;
-  if (tiles > (1ll << 30)) return hipErrorInvalidValue;
+  // tile indices are int; one image is addressed by 32-bit buffer offsets
+  if (tiles > (1ll << 30) || (int64_t)p.C * p.H * p.W * (p.x_bf16 ? 2 : 4) >= (1ll << 31))
+    return hipErrorInvalidValue;
   int64_t grid = std::min<int64_t>(tiles, 2 * (int64_t)cus.load());
   if (p.grid_cap > 0) grid = std::min<int64_t>(grid, p.grid_cap);
   // vector segment loads need 4-aligned rows and an aligned base
