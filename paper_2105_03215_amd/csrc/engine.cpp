@@ -503,6 +503,25 @@ void Planner::plan_node(int ni) {
     jobs.push_back({PackJob::ConvW, wc, L.w.off, K, Cg, R, S, Cp, p.Kgp, rows, 0, 0});
     L.bias = wslot((int64_t)rows * 4);
     jobs.push_back({PackJob::Vec, bc, L.bias.off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? K : 0, rows});
+    // few rows of a plain matrix product (a classifier at small batch):
+    // the dense-rows kernel, one workgroup per 16 output channels with the
+    // reduction split over its waves; BYOC_DENSE_ROWS=0 (or a forced conv
+    // tile) keeps the conv kernels
+    const bool rows_gemm = R == 1 && S == 1 && H == 1 && W == 1 && P == 1 && Q == 1;
+    const char* dr_env = std::getenv("BYOC_DENSE_ROWS");
+    if (rows_gemm && p.M <= 64 && !std::getenv("BYOC_CONV_TILE") && !(dr_env && dr_env[0] == '0')) {
+      p.splits = 1;
+      p.k_tiles_per_split = p.Kgp / kKPad;
+      if (dense_rows_supported(p)) {
+        L.op = Launch::DenseRows;
+        L.info.kind = BYOC_K_CONV_MFMA;
+        char nm[32];
+        std::snprintf(nm, sizeof(nm), "dense_rows_m%d", p.M);
+        name(L, nm);
+        e->launches.push_back(L);
+        return;
+      }
+    }
     int splits, kps;
     choose_conv_tile(p.M, Kp, p.Kg, &L.tile, &splits, &kps);
     apply_tile_override(p.Kg, &L.tile, &splits, &kps);
@@ -659,6 +678,16 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       return L.tile.stages > 0
                  ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, L.tile.kgroups, c.s)
                                : launch_conv_mfma(p, L.tile, c.s);
+    }
+    case Launch::DenseRows: {
+      ConvParams p = L.conv;
+      p.x = (const bf16_t*)c.ptr(L.x);
+      p.w = (const bf16_t*)c.ptr(L.w);
+      p.bias = (const float*)c.ptr(L.bias);
+      p.res = (const bf16_t*)c.ptr(L.res);
+      p.y = (bf16_t*)c.ptr(L.y);
+      p.partial = nullptr;
+      return launch_dense_rows(p, c.s);
     }
     case Launch::ConvF32: {
       ConvF32Params p = L.cf;

@@ -24,7 +24,7 @@ struct Ref {
 struct Launch {
   enum Op {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
-    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool
+    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;

@@ -87,6 +87,10 @@ int stem_weight_ld(int R);
 hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s);
 hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R, int S, int wld,
                                     hipStream_t s);
+// Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
+// one workgroup per 16 output channels, the reduction split over its waves.
+bool dense_rows_supported(const ConvParams& p);
+hipError_t launch_dense_rows(const ConvParams& p, hipStream_t s);
 // Sums split-K partials in a fixed order and applies bias, residual, act.
 hipError_t launch_splitk_reduce(const ConvParams& p, hipStream_t s);
 

@@ -92,39 +92,49 @@ __global__ __launch_bounds__(kThreads) void maxpool_nhwc_kernel(PoolParams p) {
 }
 
 // Global average pool NHWC bf16 -> [N][Cp] bf16.  Workgroup = one image x
-// 8 channel groups (64 channels); 32 lanes per group stride over the pixels,
-// then one lane per group sums the 32 partials in lane order (fixed order,
-// run-to-run identical) and divides by H*W.
+// 32 channel groups of 8.  The 8 lanes of a group are consecutive: lane j
+// sums pixels j, j + 8, ... in order (eight loads in flight), then the 8
+// partial sums meet in a 3-step butterfly (a fixed pairing; addition is
+// commutative, so every lane holds the same bits) and are scaled by
+// 1 / (H W).  Run-to-run identical.
 __global__ __launch_bounds__(kThreads) void avgpool_nhwc_kernel(PoolParams p) {
-  __shared__ float part[32][8][8];
   const int G = p.Cp / 8;
   const int n = blockIdx.x;
-  const int gl = threadIdx.x % 8;
-  const int pl = threadIdx.x / 8;
-  const int g = blockIdx.y * 8 + gl;
+  const int pl = threadIdx.x & 7;
+  const int g = blockIdx.y * (kThreads / 8) + (threadIdx.x >> 3);
   const int HW = p.H * p.W;
+  const bool ok = g < G;
+  const bf16_t* x = (const bf16_t*)p.x + (size_t)n * HW * p.Cp + (size_t)(ok ? g : 0) * 8;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (g < G) {
-    const bf16_t* x = (const bf16_t*)p.x + (size_t)n * HW * p.Cp + g * 8;
-    for (int i = pl; i < HW; i += 32) {
-      float v[8];
-      unpack8(*(const uint4*)(x + (size_t)i * p.Cp), v);
+  auto add = [&](const uint4& u) {
+    float v[8];
+    unpack8(u, v);
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[c] += v[c];
+    for (int c = 0; c < 8; ++c) acc[c] += v[c];
+  };
+  // chunks of 64 pixels: the thread's (up to) 8 loads of a chunk are all
+  // issued before the first add (pixels past the image read pixel 0 and
+  // are not added)
+  for (int i0 = 0; i0 < HW; i0 += 64) {
+    uint4 u[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = i0 + pl + 8 * j;
+      u[j] = *(const uint4*)(x + (size_t)(i < HW ? i : 0) * p.Cp);
     }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (i0 + pl + 8 * j < HW) add(u[j]);
   }
 #pragma unroll
-  for (int c = 0; c < 8; ++c) part[pl][gl][c] = acc[c];
-  __syncthreads();
-  if (pl == 0 && g < G) {
-    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int l = 0; l < 32; ++l)
+  for (int o = 1; o < 8; o <<= 1)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) s[c] += part[l][gl][c];
+    for (int c = 0; c < 8; ++c) acc[c] += __shfl_xor(acc[c], o);
+  if (ok && pl == 0) {
     const float inv = 1.0f / (float)HW;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) s[c] *= inv;
-    *(uint4*)((bf16_t*)p.y + (size_t)n * p.Cp + g * 8) = pack8(s);
+    for (int c = 0; c < 8; ++c) acc[c] *= inv;
+    *(uint4*)((bf16_t*)p.y + (size_t)n * p.Cp + g * 8) = pack8(acc);
   }
 }
 
@@ -332,7 +342,7 @@ hipError_t launch_maxpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
 }
 
 hipError_t launch_avgpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
-  avgpool_nhwc_kernel<<<dim3(p.N, (p.Cp / 8 + 7) / 8), kThreads, 0, s>>>(p);
+  avgpool_nhwc_kernel<<<dim3(p.N, (p.Cp / 8 + kThreads / 8 - 1) / (kThreads / 8)), kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 

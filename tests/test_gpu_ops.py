@@ -215,6 +215,30 @@ def test_fused_stem_conv_maxpool(case):
     assert names[0] == "stem_conv_maxpool" and "nchw_to_nhwc" not in names, names
 
 
+DENSE_ROWS_CASES = [
+    # name, rows, k, n, act, residual
+    ("m1_k2048_n1000", 1, 2048, 1000, None, False),
+    ("m32_k2048_n1000_relu", 32, 2048, 1000, "relu", False),
+    ("m33_k1000_n24_gelu_res", 33, 1000, 24, "gelu", True),
+    ("m64_k64_n40_relu6", 64, 64, 40, "relu6", False),
+    ("m16_k4200_n16_res", 16, 4200, 16, None, True),  # more k-steps than one pass of the waves
+]
+
+
+@pytest.mark.parametrize("case", DENSE_ROWS_CASES, ids=[c[0] for c in DENSE_ROWS_CASES])
+def test_dense_rows(case):
+    """Few-row dense composites run on the dense-rows kernel (reduction split
+    over the waves of a workgroup) and match the oracle."""
+    name, rows, k, n, act, res = case
+    g = GraphBuilder("dense_rows_" + name, 1800 + DENSE_ROWS_CASES.index(case))
+    x = g.input("x", [rows, k], "normal", dtype="bf16")
+    r = g.input("r", [rows, n], "normal", dtype="bf16") if res else None
+    y = g.dense(x, n, act=act, residual=r, name="fc")
+    g.output(y)
+    launches = _check_bf16(g.finish(), "dense rows " + name)
+    assert any(l["name"].startswith("dense_rows") for l in launches), [l["name"] for l in launches]
+
+
 # (case, workgroups): each workgroup walks several tiles, so the patch
 # prefetch of the next tile and the tile loop's LDS reuse are exercised
 STEM_LOOP_CASES = [
