@@ -34,49 +34,16 @@
 // order.
 #include <type_traits>
 
-#include "device_common.h"
+#include "lds_dma.h"
 
 namespace byoc {
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((ext_vector_type(4))) int i32x4;
+using namespace dma;
 
-constexpr int kBK = 64;                 // reduction elements per stage
-constexpr int kCH = kBK / 8;            // 16-byte chunks per tile row
-constexpr int kLdsLimit = 160 * 1024;     // LDS bytes per workgroup on gfx950
-
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
-
-// Raw buffer resource (base, stride 0, num_records = bytes): offsets at or
-// past `bytes` read zeros.
-__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int bytes) {
-  const uint64_t a = (uint64_t)base;
-  i32x4 r;
-  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-  r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32) & 0xFFFF);
-  r[2] = __builtin_amdgcn_readfirstlane(bytes);
-  r[3] = kBufferFlags;
-  return r;
-}
-
-// 16 bytes per lane from a buffer straight into LDS: lane l writes bytes
-// [16 l, 16 l + 16) after the wave-uniform LDS address.  Written as inline
-// assembly so that the compiler neither tracks these fills (the kernel
-// waits for them itself, per stage, before its barrier) nor inserts
-// conservative waits for them in front of unrelated LDS reads.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_fill16(i32x4 rsrc, uint32_t lds_addr, uint32_t voff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :
-               : "s"(lds_addr), "v"(voff), "s"(rsrc)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+constexpr int kBK = 64;        // reduction elements per stage
+constexpr int kCH = kBK / 8;   // 16-byte chunks per tile row
+constexpr int kMaxStages = 4;  // deepest operand ring (deeper rings measured no faster)
 
 template <int BM, int BN, int WM, int WN, int KG, int NS, bool ALIGNED, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams p) {
@@ -85,7 +52,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   constexpr int kNT = 64 * WM * WN;          // threads of one reduction group
   constexpr int kNTall = kNT * KG;           // threads per workgroup
   constexpr int kRowsPerPass = kNT / kCH;    // rows one load instruction of every wave covers
-  static_assert(NS >= 1 && NS <= 4, "stages");
+  static_assert(NS >= 1 && NS <= kMaxStages, "stages");
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;  // 16x16 MFMA tiles per wave
   constexpr int AR = BM / kRowsPerPass, BR = BN / kRowsPerPass;
@@ -114,33 +81,8 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   const int r0 = tg / kCH;                        // first row this thread fills
   const int cv = (lane & 7) ^ ((lane >> 3) & 7);  // logical chunk it fetches
 
-  // Tile placement: the hardware deals workgroups round-robin to the 8
-  // XCDs (block b runs on XCD b % 8).  With xcd_py > 0 every XCD owns one
-  // block of a (8 / xcd_py) x xcd_py partition of the tile grid and walks it
-  // channel tile fastest; the grid is padded to 8 equal shares and surplus
-  // workgroups exit at once.  Otherwise each XCD gets a contiguous run of
-  // the row-major tile order.
-  const int ntn = (p.Kp + BN - 1) / BN;
-  const int ntm = (p.M + BM - 1) / BM;
   int tm, tn;
-  if (p.xcd_py > 0) {
-    // XCD x = (gx, gy) owns m tiles [gx*mh, gx*mh + mh) and n tiles
-    // [gy*nh, gy*nh + nh) of the grid (clipped at its edge); mg_tile divides by nh
-    const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
-    const int lpy = 31 - __builtin_clz(p.xcd_py);  // xcd_py is 1, 2, 4 or 8
-    const int mh = (ntm + (8 >> lpy) - 1) >> (3 - lpy), nh = (ntn + p.xcd_py - 1) >> lpy;
-    const int gx = x >> lpy, gy = x & (p.xcd_py - 1);
-    const int jm = mdiv(j, p.mg_tile);
-    tm = gx * mh + jm;
-    tn = gy * nh + (j - jm * nh);
-    if (jm >= mh || tm >= ntm || tn >= ntn) return;
-  } else {
-    int bid = blockIdx.x;
-    const int nb = ntm * ntn;  // the launch grid (no kernel-argument fetch)
-    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-    tm = mdiv(bid, p.mg_tile);
-    tn = bid - tm * ntn;
-  }
+  if (!place_tile<BM, BN>(p, &tm, &tn)) return;
   const int m0 = tm * BM;
   const int n0 = tn * BN;
 
@@ -175,11 +117,14 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
     pix[i] = m < p.M ? ((n * p.H + ih0) * p.W + iw0) * p.Cp : 0;
     if (ALIGNED) {
       pix[i] += cv * 8;
+      // taps inside the image: kernel rows [r_lo, r_hi) x columns [s_lo, s_hi)
+      const int r_lo = max(0, -ih0), nr = max(0, min(p.R, p.H - ih0) - r_lo);
+      const int s_lo = max(0, -iw0), s_hi = min(p.S, p.W - iw0);
+      const uint32_t cols =
+          s_hi > s_lo ? (uint32_t)(((1ull << s_hi) - 1ull) & ~((1ull << s_lo) - 1ull)) : 0u;
       uint32_t mask = 0;
       for (int r = 0; r < p.R; ++r)
-        for (int s = 0; s < p.S; ++s)
-          if ((unsigned)(ih0 + r) < (unsigned)p.H && (unsigned)(iw0 + s) < (unsigned)p.W)
-            mask |= 1u << (r * p.S + s);
+        if ((unsigned)(r - r_lo) < (unsigned)nr) mask |= cols << (r * p.S);
       tapmask[i] = mask;
     }
   }
@@ -318,10 +263,6 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
     }
   }
 
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
-  using S2 = std::integral_constant<int, 2>;
-  using S3 = std::integral_constant<int, 3>;
   const int nkt = (kt_end - kt_begin + KG - 1) / KG;  // steps (stages per group, rounded up)
 
   // Stage t lives in buffer t % NS.  Before computing it: wait for this
@@ -329,6 +270,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   // and for its own LDS reads, then barrier so every wave's fills are
   // visible and every wave is done with stage t-1, whose buffer the fills
   // of stage t+NS-1 then reuse.
+  static_assert((NS - 2) * LPS <= 63, "vmcnt immediate");
   auto step = [&](auto cur, auto nxt) {
     if constexpr (NS == 1) {  // single buffer: load, compute, then refill it
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -341,6 +283,11 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
       compute(cur);
     }
   };
+  // step i of a round of NS computes buffer i and refills buffer (i + NS - 1) % NS
+  auto round_step = [&](auto i) {
+    constexpr int I = decltype(i)::value;
+    step(i, std::integral_constant<int, (I + NS - 1) % NS>{});
+  };
 
   // the tile's bias, straight into LDS (zeros without a bias); issued first,
   // so every later wait of this wave covers it
@@ -349,40 +296,16 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
     const uint32_t off = lane < BN / 4 ? (uint32_t)(n0 + 4 * lane) * 4u : kOOB;
     lds_fill16(br, __builtin_amdgcn_readfirstlane(lds_addr(sbias)), off);
   }
-  issue(S0{});
-  if constexpr (NS > 2) issue(S1{});
-  if constexpr (NS > 3) issue(S2{});
-  // full groups of NS stages (stage t in buffer t % NS), then the tail
+  // NS - 1 stages ahead (one with a single buffer)
+  static_for<0, (NS > 1 ? NS - 1 : 1)>([&](auto i) { issue(i); });
+  // full rounds of NS stages (stage t in buffer t % NS), then the tail
   int t = 0;
-  for (; t + NS <= nkt; t += NS) {
-    if constexpr (NS == 1) {
-      step(S0{}, S0{});
-    } else if constexpr (NS == 2) {
-      step(S0{}, S1{});
-      step(S1{}, S0{});
-    } else if constexpr (NS == 3) {
-      step(S0{}, S2{});
-      step(S1{}, S0{});
-      step(S2{}, S1{});
-    } else {
-      step(S0{}, S3{});
-      step(S1{}, S0{});
-      step(S2{}, S1{});
-      step(S3{}, S2{});
-    }
-  }
+  for (; t + NS <= nkt; t += NS) static_for<0, NS>(round_step);
   const int rem = nkt - t;
-  if (NS > 1 && rem > 0) {
-    if constexpr (NS == 1) step(S0{}, S0{});
-    else if constexpr (NS == 2) step(S0{}, S1{});
-    else if constexpr (NS == 3) step(S0{}, S2{});
-    else step(S0{}, S3{});
-  }
-  if constexpr (NS > 2) {
-    if (rem > 1) step(S1{}, S0{});
-  }
-  if constexpr (NS > 3) {
-    if (rem > 2) step(S2{}, S1{});
+  if constexpr (NS > 1) {
+    static_for<0, NS - 1>([&](auto i) {
+      if (rem > decltype(i)::value) round_step(i);
+    });
   }
   // all fills (including the zero fills past the end) landed, all waves
   // done reading the operand buffers
@@ -466,20 +389,10 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
 template <int BM, int BN, int WM, int WN, int KG, int NS>
 hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
   ConvParams p = p_in;
-  const int ntm = (p.M + BM - 1) / BM;
-  const int ntn = (p.Kp + BN - 1) / BN;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
   const bool split = p.splits > 1;
   if (KG > 1 && split) return hipErrorInvalidValue;
-  int blocks = ntm * ntn;
-  if (p.xcd_py > 0) {
-    const int py = p.xcd_py, px = 8 / py;
-    const int mh = (ntm + px - 1) / px, nh = (ntn + py - 1) / py;
-    blocks = 8 * mh * nh;
-    p.mg_tile = magic40(nh);
-  } else {
-    p.mg_tile = magic40(ntn);
-  }
+  const int blocks = placed_blocks(p, BM, BN);
   dim3 grid(blocks, split ? p.splits : 1);
   constexpr int kThreads = 64 * WM * WN * KG;
   if constexpr (KG == 1) {
@@ -498,20 +411,19 @@ template <int BM, int BN, int WM, int WN, int KG>
 hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
   constexpr int kStage = (BM + BN) * 128 * KG;  // bytes of one ring slot, all groups
   constexpr int kFixed = BN * 4;                 // the bias tile
-  if (ns == 1) return launch_tile<BM, BN, WM, WN, KG, 1>(p, s);
-  if constexpr (2 * kStage + kFixed <= kLdsLimit)
-    if (ns == 2) return launch_tile<BM, BN, WM, WN, KG, 2>(p, s);
-  if constexpr (3 * kStage + kFixed <= kLdsLimit)
-    if (ns == 3) return launch_tile<BM, BN, WM, WN, KG, 3>(p, s);
-  if constexpr (4 * kStage + kFixed <= kLdsLimit)
-    if (ns == 4) return launch_tile<BM, BN, WM, WN, KG, 4>(p, s);
-  return hipErrorInvalidValue;
+  hipError_t r = hipErrorInvalidValue;
+  static_for<1, kMaxStages + 1>([&](auto i) {
+    constexpr int NS = decltype(i)::value;
+    if constexpr (NS * kStage + kFixed <= kLdsLimit)
+      if (ns == NS) r = launch_tile<BM, BN, WM, WN, KG, NS>(p, s);
+  });
+  return r;
 }
 
 }  // namespace
 
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
-  if (stages < 1 || stages > 4 || (kgroups != 1 && kgroups != 2)) return false;
+  if (stages < 1 || stages > kMaxStages || (kgroups != 1 && kgroups != 2)) return false;
   if ((bm + bn) * 128 * stages * kgroups + bn * 4 > kLdsLimit) return false;  // LDS: stage rings + bias
   const int waves = threads / (64 * kgroups);  // per reduction group
   if (threads != 64 * waves * kgroups) return false;

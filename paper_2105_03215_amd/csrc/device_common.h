@@ -89,7 +89,8 @@ __device__ __forceinline__ void materialize_args(const ConvParams& p) {
   asm volatile("" ::"s"(p.M), "s"(p.Kp), "s"(p.Kg), "s"(p.Kgp), "s"(p.ldy), "s"(p.ldr), "s"(p.act),
                "s"(p.splits), "s"(p.k_tiles_per_split), "s"(p.x_bytes), "s"(p.w_bytes), "s"(p.res_bytes),
                "s"(p.xcd_py));
-  asm volatile("" ::"s"(p.mg_pq), "s"(p.mg_q), "s"(p.mg_cp), "s"(p.mg_s), "s"(p.mg_tile));
+  asm volatile("" ::"s"(p.mg_pq), "s"(p.mg_q), "s"(p.mg_cp), "s"(p.mg_s), "s"(p.mg_tile), "s"(p.mg_wp),
+               "s"(p.mg_hp));
 }
 
 // floor(n / d) for 0 <= n with n * d < 2^40, given mg = ceil(2^40 / d).

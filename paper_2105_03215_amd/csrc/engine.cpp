@@ -27,6 +27,7 @@ int64_t numel(const std::vector<int64_t>& s) {
 
 constexpr int kRowPad = 256;  // packed weight rows are padded to this (>= any tile BN)
 constexpr int kKPad = 64;     // packed reduction length is padded to this (the stage depth)
+constexpr int kHaloStages = 3;  // halo kernel weight ring: 3 stages of one kernel row (built-in choice)
 
 struct PackJob {
   enum Kind { ConvW, DwW, Vec, Copy, StemW } kind;
@@ -81,7 +82,18 @@ void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
   if (const char* e = std::getenv("BYOC_CONV_TILE")) {
     int bm = 0, bn = 0, mf = 16;
     int ns = 0;
-    if (e[0] == 'd') {
+    if (e[0] == 'h') {
+      // h<bm>x<bn>s<stages>: halo kernel (3x3 stride-1 convs only; others keep their tile)
+      if (std::sscanf(e + 1, "%dx%ds%d", &bm, &bn, &ns) == 3) {
+        t->bm = bm;
+        t->bn = bn;
+        t->mf = 16;
+        t->stages = ns;
+        t->threads = 512;
+        t->kgroups = 1;
+        t->halo = 2;  // requested; resolved against the shape by the planner
+      }
+    } else if (e[0] == 'd') {
       // d<bm>x<bn>s<stages>[t<threads>[k<groups>]]: direct HBM->LDS pipeline
       int nt = 256, kgr = 1;
       if (std::sscanf(e + 1, "%dx%ds%dt%dk%d", &bm, &bn, &ns, &nt, &kgr) >= 3 &&
@@ -142,7 +154,10 @@ int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
 }
 
 void name_conv(Launch& L) {
-  if (L.tile.stages > 0)
+  if (L.tile.halo)
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_halo_%dx%d_s%d_lp%d_pb%d", L.tile.bm, L.tile.bn,
+                  L.tile.stages, L.tile.lp, L.tile.npb);
+  else if (L.tile.stages > 0)
     std::snprintf(L.info.name, sizeof(L.info.name), "conv_dma_%dx%d_s%d_w%d_k%d_split%d", L.tile.bm, L.tile.bn,
                   L.tile.stages, L.tile.threads / 64, L.tile.kgroups, L.conv.splits);
   else
@@ -527,6 +542,49 @@ void Planner::plan_node(int ni) {
     apply_tile_override(p.Kg, &L.tile, &splits, &kps);
     p.splits = splits;
     p.k_tiles_per_split = kps;
+    {
+      // 3x3 stride-1 convs with at least 256 input channels and enough
+      // 128x64 tiles to fill most CUs run on the halo kernel (input window
+      // staged in LDS once per 64-channel slice).  Measured on MI355X over
+      // the ResNet-50 layers at batch 32: it wins on 256 channels at 14x14
+      // (196 tiles) and loses where the patch is large against the work
+      // (64 channels at 56x56), where the implicit-GEMM kernel's 128x128
+      // tiles win (128 channels at 28x28) and where 128x64 tiles leave most
+      // CUs idle (512 channels at 7x7, 104 tiles).  BYOC_CONV_HALO=1 takes
+      // it wherever the shape allows, =0 never; a forced tile decides alone.
+      const bool forced = L.tile.halo == 2;
+      const char* he = std::getenv("BYOC_CONV_HALO");
+      const int64_t halo_tiles = ((p.M + 127) / 128) * ((Kp + 63) / 64);
+      const bool by_rule = Cp >= 256 && halo_tiles >= 160;
+      const bool want = forced || (!std::getenv("BYOC_CONV_TILE") && (he ? he[0] == '1' : by_rule));
+      const int ns = forced ? L.tile.stages : kHaloStages;
+      int lp = 0, npb = 0;
+      if (forced) {  // a forced halo tile also forgoes split-K
+        ConvParams q = p;
+        q.splits = 1;
+        if (conv_halo_plan(q, 128, 64, ns, &lp, &npb)) {
+          splits = 1;
+          kps = (int)((p.Kg + kKPad - 1) / kKPad);
+          p.splits = splits;
+          p.k_tiles_per_split = kps;
+        }
+      }
+      if (want && splits == 1 && conv_halo_plan(p, 128, 64, ns, &lp, &npb)) {
+        L.tile = ConvTile{};
+        L.tile.bm = 128;
+        L.tile.bn = 64;
+        L.tile.stages = ns;
+        L.tile.threads = 512;
+        L.tile.halo = 1;
+        L.tile.lp = lp;
+        L.tile.npb = npb;
+      } else if (forced) {
+        L.tile = ConvTile{};
+        choose_conv_tile(p.M, Kp, p.Kg, &L.tile, &splits, &kps);
+        p.splits = splits;
+        p.k_tiles_per_split = kps;
+      }
+    }
     p.xcd_py = L.tile.stages > 0 ? choose_xcd_split(p, L.tile) : 0;
     L.tile_default = L.tile;
     L.op = Launch::ConvMfma;
@@ -675,6 +733,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.y = (bf16_t*)c.ptr(L.y);
       p.partial = (float*)c.ptr(L.partial);
       if (L.op == Launch::SplitReduce) return launch_splitk_reduce(p, c.s);
+      if (L.tile.halo) return launch_conv_halo(p, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.lp, L.tile.npb, c.s);
       return L.tile.stages > 0
                  ? launch_conv_dma(p, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, L.tile.kgroups, c.s)
                                : launch_conv_mfma(p, L.tile, c.s);
@@ -925,6 +984,15 @@ namespace {
 std::vector<ConvTile> conv_candidates(const Launch& L) {
   std::vector<ConvTile> c;
   c.push_back(L.tile_default);
+  if (L.tile_default.halo) {  // the halo kernel: other weight ring depths (same reduction order)
+    for (int ns : {2, 3, 4, 6, 8}) {
+      ConvTile t = L.tile_default;
+      if (ns == t.stages || !conv_halo_plan(L.conv, t.bm, t.bn, ns, &t.lp, &t.npb)) continue;
+      t.stages = ns;
+      c.push_back(t);
+    }
+    return c;
+  }
   if (L.conv.splits > 1 || L.tile_default.mf != 16) return c;
   const ConvParams& p = L.conv;
   const int kgr = L.tile_default.kgroups;  // the reduction order class of the built-in choice

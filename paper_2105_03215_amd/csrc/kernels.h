@@ -46,6 +46,7 @@ struct ConvParams {
   // launchers (the tile divisor depends on the tile shape).
   uint64_t mg_pq, mg_q, mg_cp, mg_s;
   uint64_t mg_tile;  // divisor: channel tiles per row of the tile grid (or per XCD block)
+  uint64_t mg_wp, mg_hp;  // conv_halo: divisors W + 2 and H + 2 (set by its launcher)
 };
 
 inline uint64_t magic40(int d) { return ((uint64_t(1) << 40) + (uint64_t)d - 1) / (uint64_t)d; }
@@ -56,6 +57,8 @@ struct ConvTile {
   int stages = 0;   // > 0: HBM->LDS pipeline of that many stages (conv_dma)
   int threads = 256;  // conv_dma workgroup size: 256 (4 waves) or 512 (8 waves)
   int kgroups = 1;    // conv_dma reduction groups (2: two 4-wave groups split the reduction stages)
+  int halo = 0;       // 1: conv_halo kernel (stages = weight ring depth, lp / npb as planned)
+  int lp = 0, npb = 0;
 };
 
 // Tile configurations with a compiled kernel.
@@ -65,6 +68,17 @@ hipError_t launch_conv_mfma(const ConvParams& p, ConvTile t, hipStream_t s);
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups);
 hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, int kgroups,
                            hipStream_t s);
+// 3x3 stride-1 pad-1 convolution that stages each 64-channel slice of the
+// input window of a tile (its output pixels' rows plus a one-pixel halo) in
+// LDS once and forms all nine taps from it; weights stream per tap through
+// a ring of `stages` LDS buffers.  Requires Cp % 64 == 0, P == H, Q == W.
+// The reduction runs slice by slice (tap, then channel within the slice).
+// conv_halo_plan checks the shape and picks the patch capacity (loads per
+// thread, lp) and the number of patch buffers (npb) for a tiling; the
+// launcher takes them as planned.  `stages` is the weight ring: 2 or 3
+// stages of three taps (one kernel row), or 4, 6 or 8 stages of one tap.
+bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb);
+hipError_t launch_conv_halo(const ConvParams& p, int bm, int bn, int stages, int lp, int npb, hipStream_t s);
 // Fused stem: conv (C <= 4 NCHW input channels, 64 output channels) + bias
 // + activation followed by max pooling; output NHWC bf16 with 64 channels.
 struct StemParams {

@@ -78,6 +78,45 @@ def test_conv_composite(case):
     _check_bf16(g.finish(), "conv " + name)
 
 
+HALO_CASES = [
+    # name, (n, c, h, w), k, act, residual, forced weight-ring depth (None:
+    # the built-in ring; small outputs would otherwise go to split-K)
+    ("c128_7x7_multi_image_ragged_k", (6, 128, 7, 7), 136, "relu", False, 8),
+    ("c256_14x14_res", (2, 256, 14, 14), 64, "relu", True, 8),
+    ("c64_30x30_one_slice", (1, 64, 30, 30), 64, None, False, 6),
+    ("c192_9x5_three_slices", (3, 192, 9, 5), 72, "relu6", False, 4),
+    ("c64_56x56_wide_patch", (2, 64, 56, 56), 64, "relu", False, None),
+    ("c128_28x28_ring2", (2, 128, 28, 28), 128, "relu", True, 2),
+    ("c128_28x28_ring4", (2, 128, 28, 28), 128, "relu", True, 4),
+    ("c128_28x28_ring6", (2, 128, 28, 28), 128, "relu", True, 6),
+    ("c128_28x28_builtin", (4, 128, 28, 28), 128, "relu", True, None),
+    ("c512_7x7_gelu", (3, 512, 7, 7), 128, "gelu", False, 8),
+]
+
+
+@pytest.mark.parametrize("case", HALO_CASES, ids=[c[0] for c in HALO_CASES])
+def test_conv_halo_composite(case, monkeypatch):
+    """3x3 stride-1 convs on the kernel that stages the input window in LDS:
+    tiles spanning several images, ragged pixel and channel tails, one to
+    eight 64-channel slices, non-square images, every weight-ring depth."""
+    name, shape, k, act, res, ring = case
+    if ring is not None:
+        monkeypatch.setenv("BYOC_CONV_TILE", "h128x64s%d" % ring)
+    else:  # the halo kernel wherever the shape allows, built-in ring
+        monkeypatch.setenv("BYOC_CONV_HALO", "1")
+    g = GraphBuilder("op_halo_" + name, 1300 + HALO_CASES.index(case))
+    x = g.input("x", list(shape), "uniform")
+    n, c, h, w = shape
+    rname = g.input("res", [n, k, h, w], "normal") if res else None
+    y = g.conv(x, k, 3, stride=1, pad=1, act=act, residual=rname, name="y")
+    g.output(y)
+    launches = _check_bf16(g.finish(), "conv halo " + name)
+    names = [l["name"] for l in launches]
+    assert any(nm.startswith("conv_halo_128x64") for nm in names), names
+    if ring is not None:
+        assert any(nm.startswith("conv_halo_128x64_s%d_" % ring) for nm in names), names
+
+
 DW_CASES = [
     ("dw_s1_c96", (2, 96, 14, 14), 1, False),
     ("dw_s2_c144", (1, 144, 28, 28), 2, False),
