@@ -30,8 +30,8 @@ import os
 import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "stem_conv_maxpool_kernel", "splitk_reduce_kernel",
-                "dense_rows_kernel")
+CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "conv_halo_kernel", "stem_conv_maxpool_kernel",
+                "splitk_reduce_kernel", "dense_rows_kernel")
 RUN_MARKER = "stem_conv_maxpool_kernel"  # one dispatch per run of the ResNet subgraphs
 
 
@@ -99,7 +99,8 @@ def _copy_kib(path, counter):
 def conv_kernel_digest():
     """Digest of the conv kernel sources and of the planner that picks them."""
     h = hashlib.sha256()
-    for name in ("conv_mfma.hip", "conv_dma.hip", "stem.hip", "dense_rows.hip", "engine.cpp"):
+    for name in ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "lds_dma.h", "stem.hip", "dense_rows.hip",
+                 "engine.cpp"):
         with open(os.path.join(ROOT, "paper_2105_03215_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
