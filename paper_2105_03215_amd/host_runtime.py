@@ -1,0 +1,132 @@
+"""Runtime of a partitioned model (Sec. 3.4, Fig. 6).
+
+A ``Partitioned`` program (see ``partition.py``) is a list of steps: host
+operators and external calls of offloaded functions.  ``Module`` runs it:
+
+* metadata module - on creation it loads every constant the host operators
+  use into data entries on the device, and builds the execution engine of
+  each offloaded function once (``byoc_subgraph_create`` with the function's
+  JSON and constants; the engine packs its own copy), cached for every later
+  inference;
+* data entries - one device tensor per graph input, constant and step
+  result, addressed by the operator-graph id assigned at partitioning;
+  intermediates inside an offloaded function are the engine's own and never
+  appear here;
+* execution - the steps in order: a host operator reads its input entries,
+  computes on the device with PyTorch and writes its entry; an external call
+  hands its input entries and freshly allocated output entries to the
+  engine's run on the module's stream.
+
+Host operators compute in float32 and store in the node's dtype.  The
+offloaded functions run only through the HIP library: there is no other
+path for them.
+"""
+
+import math
+
+import torch
+import torch.nn.functional as F
+
+from . import capi
+
+
+def _tdt(dtype):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def _pads(p):
+    return [int(v) for v in p] if len(p) == 4 else [int(p[0]), int(p[1])] * 2
+
+
+def _host_op(node, args):
+    """One host operator on float32 device tensors."""
+    op, a = node.op, node.attrs
+    x = args[0]
+    if op == "nn.conv2d":
+        pt, pl, pb, pr = _pads(a.get("padding", [0, 0, 0, 0]))
+        x = F.pad(x, (pl, pr, pt, pb))
+        return F.conv2d(x, args[1], stride=tuple(a.get("strides", [1, 1])), groups=a.get("groups", 1))
+    if op == "nn.dense":
+        return x @ args[1].t().contiguous()
+    if op == "nn.bias_add":
+        return x + args[1].view([1, -1] + [1] * (x.dim() - 2))
+    if op == "add":
+        return x + args[1]
+    if op == "multiply":
+        return x * args[1]
+    if op == "nn.relu":
+        return torch.relu(x)
+    if op == "clip":
+        return torch.clamp(x, a["a_min"], a["a_max"])
+    if op == "nn.gelu":
+        return 0.5 * x * (1.0 + torch.erf(x / math.sqrt(2.0)))
+    if op == "sigmoid":
+        return torch.sigmoid(x)
+    if op == "nn.softmax":
+        return torch.softmax(x, dim=a.get("axis", -1))
+    if op == "nn.max_pool2d":
+        pt, pl, pb, pr = _pads(a.get("padding", [0, 0, 0, 0]))
+        x = F.pad(x, (pl, pr, pt, pb), value=-math.inf)
+        return F.max_pool2d(x, tuple(a["pool_size"]), stride=tuple(a["strides"]))
+    if op == "nn.global_avg_pool2d":
+        return x.mean(dim=(2, 3), keepdim=True)
+    if op == "nn.batch_flatten":
+        return x.reshape(x.shape[0], -1)
+    if op == "reshape":
+        return x.reshape(tuple(a["newshape"]))
+    if op == "transpose":
+        return x.permute(*a["axes"]).contiguous()
+    raise ValueError("no host implementation of %s" % op)
+
+
+class Module:
+    """Executable form of a partitioned model on one device."""
+
+    def __init__(self, part, device="cuda:0"):
+        self.part = part
+        self.device = torch.device(device)
+        self.dev_index = self.device.index or 0
+        g = part.graph
+        # metadata module: constants used by host operators, as data entries
+        used_by_host = set()
+        for kind, ref in part.steps:
+            if kind == "host":
+                used_by_host.update(g.nodes[ref].inputs)
+        self.const_entries = {}
+        for n in g.nodes:
+            if n.op == "const" and n.id in used_by_host:
+                self.const_entries[n.id] = torch.from_numpy(n.value).to(self.device, torch.float32)
+        # one cached execution engine per offloaded function
+        self.engines = [capi.Subgraph(f.graph, f.consts, device=self.dev_index) for f in part.functions]
+
+    def close(self):
+        for e in self.engines:
+            e.close()
+        self.engines = []
+
+    def run(self, inputs, stream=None):
+        """Run one inference; ``inputs`` are device tensors in the order of
+        the graph's inputs.  Returns the graph's outputs (device tensors)."""
+        g = self.part.graph
+        stream = stream or torch.cuda.current_stream(self.device)
+        entries = dict(self.const_entries)
+        for nid, t in zip(g.inputs, inputs):
+            entries[nid] = t.to(self.device, _tdt(g.nodes[nid].dtype)).contiguous()
+        with torch.cuda.stream(stream):
+            for kind, ref in self.part.steps:
+                if kind == "host":
+                    node = g.nodes[ref]
+                    args = [entries[i].float() for i in node.inputs]
+                    entries[ref] = _host_op(node, args).to(_tdt(node.dtype)).contiguous()
+                else:
+                    fn = self.part.functions[ref]
+                    eng = self.engines[ref]
+                    ins = [entries[i] for i in fn.inputs]
+                    outs = []
+                    for j, oid in enumerate(fn.outputs):
+                        d = eng.io_desc(1, j)
+                        outs.append(torch.empty(d["shape"], dtype=_tdt(d["dtype"]), device=self.device))
+                    eng.run(ins, outs, stream)
+                    for oid, t in zip(fn.outputs, outs):
+                        entries[oid] = t
+        return [entries[o] for o in g.outputs]
