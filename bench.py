@@ -5,8 +5,10 @@ One step = one run of the whole offloaded subgraph (input layout transform,
 of 32 synthetic 3x224x224 images already resident in HBM.  Prints one JSON
 line with images/s, the roofline of the dominant kernel class (the bf16 MFMA
 implicit-GEMM conv/dense kernels) measured with per-launch HIP events on the
-run stream, the batch-1 figures, and the CPU oracle timed on a bounded
-sample of the same workload.
+run stream, the batch-1 figures, the same network as an operator-level
+model partitioned for the executor and run by the partitioned-model runtime
+with a host softmax head, and the CPU oracle timed on a bounded sample of the
+same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -130,6 +132,47 @@ def _cpu_baseline(wl, images):
                       % (images, dt)}
 
 
+def _partitioned(args, wl, dev, stream):
+    """The same network as an operator-level model with a softmax head on the
+    host: partitioned (Sec. 3.1), then run by the partitioned-model runtime
+    (Sec. 3.4) - the head on the host, the offloaded function through its
+    cached engine."""
+    import torch
+
+    from paper_2105_03215_amd import host_runtime, partition
+
+    g = partition.lower_subgraph(wl.graph, wl.consts)
+    g.outputs = [g.call("nn.softmax", [g.outputs[0]], axis=-1)]
+    t0 = time.perf_counter()
+    part = partition.partition(g)
+    part_ms = (time.perf_counter() - t0) * 1e3
+    mod = host_runtime.Module(part, "cuda:0")
+    try:
+        if not args.no_autotune:
+            for e in mod.engines:
+                e.set_options(autotune=True)
+        xs = [torch.from_numpy(x).to(dev) for x in wl.inputs]
+        for _ in range(args.warmup):
+            mod.run(xs, stream)
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            start.record(stream)
+            for _ in range(args.steps):
+                mod.run(xs, stream)
+            end.record(stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / args.steps
+    finally:
+        mod.close()
+    st = part.stats()
+    return {"images_per_s": round(args.batch / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
+            "launch_mode": "direct launches", "partition_ms": round(part_ms, 2),
+            "functions": st["functions"], "host_steps": sum(1 for k, _ in part.steps if k == "host"),
+            "node_offload": round(st["node_offload"], 4), "mac_offload": round(st["mac_offload"], 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +183,8 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--no-partitioned", action="store_true",
+                    help="skip the operator-level model run through the partitioner and its runtime")
     ap.add_argument("--no-autotune", action="store_true",
                     help="keep the built-in conv kernel choice (no on-device tuning at setup)")
     ap.add_argument("--eager", action="store_true",
@@ -237,6 +282,10 @@ def main():
                "launches": len(sg1.launches())}
         sg1.close()
 
+    parted = None
+    if not args.no_partitioned:
+        parted = _partitioned(args, wl, dev, stream)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _cpu_baseline(wl, args.cpu_images)
@@ -255,6 +304,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "bs1": bs1,
+        "partitioned": parted,
         "kernel_classes": _class_summary(launches, per_launch),
         "create_s": round(create_s, 3),
         "autotune_s": None if tune_s is None else round(tune_s, 3),
