@@ -173,6 +173,37 @@ def _partitioned(args, wl, dev, stream):
             "node_offload": round(st["node_offload"], 4), "mac_offload": round(st["mac_offload"], 4)}
 
 
+def _other_workload(args, name, batch, dev, stream):
+    """Throughput and conv-class roofline of another fully offloaded network
+    (same measurement as the headline: graph replay, autotune, inputs in
+    HBM)."""
+    import torch
+
+    from paper_2105_03215_amd import capi, runtime, workloads
+
+    wl = workloads.build(name, n=batch)
+    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
+    try:
+        ins = runtime.inputs_for(sg, wl.inputs, dev)
+        outs = runtime.outputs_for(sg, dev)
+        if not args.no_autotune:
+            sg.set_options(autotune=True)
+        sg.set_options(graph_replay=not args.eager)
+        for _ in range(args.warmup):
+            sg.run(ins, outs, stream)
+        torch.cuda.synchronize()
+        ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
+        sg.set_options(graph_replay=False)
+        launches = sg.launches()
+        per_launch, _ = _profile(sg, ins, outs, stream, args.steps)
+    finally:
+        sg.close()
+    roof = _roofline(launches, per_launch, ms)
+    return {"workload": "%s_bs%d" % (name, batch), "images_per_s": round(batch / (ms * 1e-3), 1),
+            "ms_per_step": round(ms, 4), "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
+            "conv_tflops": roof["achieved"], "conv_frac": roof["frac"], "launches": len(launches)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -183,6 +214,7 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--no-other", action="store_true", help="skip the VGG19 bs32 line")
     ap.add_argument("--no-partitioned", action="store_true",
                     help="skip the operator-level model run through the partitioner and its runtime")
     ap.add_argument("--no-autotune", action="store_true",
@@ -285,6 +317,9 @@ def main():
     parted = None
     if not args.no_partitioned:
         parted = _partitioned(args, wl, dev, stream)
+    other = None
+    if not args.no_other:
+        other = [_other_workload(args, "vgg19", 32, dev, stream)]
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -305,6 +340,7 @@ def main():
         "cpu_baseline": cpu,
         "bs1": bs1,
         "partitioned": parted,
+        "other_workloads": other,
         "kernel_classes": _class_summary(launches, per_launch),
         "create_s": round(create_s, 3),
         "autotune_s": None if tune_s is None else round(tune_s, 3),

@@ -30,6 +30,7 @@ CONFIG_IDS = {
     "resnet50_v1": 2,
     "mobilenet_v2": 3,
     "bert_ffn": 4,
+    "vgg19": 5,
 }
 
 _BN_EPS = 1e-5
@@ -38,6 +39,10 @@ _BN_SHIFT_STD = 0.01
 # of 9 independent standard normals has mean 1.485 and variance 0.357, so
 # E[max^2] = 2.56 s^2 against E[relu^2] = s^2 / 2
 _MAXPOOL_GAIN = 5.1
+# 2x2 windows of neighbouring conv outputs are far from independent: the
+# mean-square gain of a 2x2 max over them is taken as 2 (the independent
+# bound would be 3.1)
+_MAXPOOL_GAIN_2X2 = 2.0
 # share of a non-negative activation's mean square that its spatial mean keeps
 _GAP_GAIN = 0.5
 _ADD_RELU_KEEP = 0.75
@@ -241,7 +246,7 @@ class GraphBuilder:
         p = (h + 2 * pad - size) // stride + 1
         q = (w + 2 * pad - size) // stride + 1
         self.shapes[name] = [n, c, p, q]
-        self.m2[name] = _MAXPOOL_GAIN * self.m2[x]
+        self.m2[name] = (_MAXPOOL_GAIN_2X2 if size == 2 else _MAXPOOL_GAIN) * self.m2[x]
         return name
 
     def global_avg_pool(self, x, name=None):
@@ -382,9 +387,40 @@ def bert_ffn(batch=8, seq=128, hidden=768, ffn=3072, layers=12):
     return g.finish({"batch": batch, "seq": seq})
 
 
+_VGG19 = [64, 64, "M", 128, 128, "M", 256, 256, 256, 256, "M", 512, 512, 512, 512, "M",
+          512, 512, 512, 512, "M"]
+
+
+def vgg19(n=1, hw=224, input_dtype="bf16", num_classes=1000, fc=4096):
+    """VGG19-shaped network (one of the fully offloaded rows of the paper's
+    Table 1): 16 conv3x3 + ReLU layers in five stages separated by 2x2
+    stride-2 max pools, then the classifier.  The first classifier layer
+    reads the flattened NCHW feature map, which is exactly a convolution
+    whose kernel covers the whole map (no padding) - written that way, its
+    [N, 4096, 1, 1] output is flattened by a global average pool over the
+    1x1 map; then 4096 -> 4096 + ReLU and 4096 -> classes.  Weights are
+    He-normal with the same layer-wide folded normalization as the other
+    networks (reading: keeps every activation O(1) with random weights)."""
+    g = GraphBuilder("vgg19", CONFIG_IDS["vgg19"])
+    x = g.input("x", [n, 3, hw, hw], "uniform", dtype=input_dtype)
+    y = x
+    for i, v in enumerate(_VGG19):
+        if v == "M":
+            y = g.max_pool(y, 2, 2, 0, name="pool%d" % i)
+        else:
+            y = g.conv(y, v, 3, act="relu", name="conv%d" % i)
+    s = g.shapes[y][2]
+    y = g.conv(y, fc, s, pad=0, act="relu", name="fc6")
+    y = g.global_avg_pool(y, name="flatten")
+    y = g.dense(y, fc, act="relu", name="fc7")
+    y = g.dense(y, num_classes, name="fc8")
+    g.output(y)
+    return g.finish({"batch": n})
+
+
 def build(name, **kw):
     """Build a workload by name: conv_f32, resnet18_block, resnet50_v1,
-    resnet50_v1b, mobilenet_v2, bert_ffn."""
+    resnet50_v1b, mobilenet_v2, bert_ffn, vgg19."""
     if name == "conv_f32":
         return conv_f32(**kw)
     if name == "resnet18_block":
@@ -397,4 +433,6 @@ def build(name, **kw):
         return mobilenet_v2(**kw)
     if name == "bert_ffn":
         return bert_ffn(**kw)
+    if name == "vgg19":
+        return vgg19(**kw)
     raise ValueError("unknown workload %r" % name)

@@ -1,4 +1,4 @@
-"""End-to-end parity of the five workloads on the GPU against the oracle.
+"""End-to-end parity of the workloads on the GPU against the oracle.
 
 Small workloads are compared on every output element; the batched ones at
 their full size in the benchmark's launch configuration, on images (or
@@ -124,6 +124,29 @@ def test_mobilenet_v2_bs16_sampled():
     err = rel_err(g[rows], o)
     print("mobilenet_v2 bs16 err %.3e" % err)
     assert err <= BF16_TOL
+
+
+def test_vgg19_bs1_112():
+    announce("vgg19 bs1 112x112")
+    wl = workloads.build("vgg19", n=1, hw=112)
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    assert g.shape == (1, 1000)
+    err = rel_err(g, o)
+    print("vgg19 bs1 112 err %.3e" % err)
+    assert err <= BF16_TOL
+
+
+def test_vgg19_bs8_sampled():
+    announce("vgg19 bs8 224x224 sampled image 7")
+    wl = workloads.build("vgg19", n=8)
+    g = _gpu(wl)[0]
+    rows = [7]
+    o = oracle.run_graph(_sample_graph(wl, 1), wl.consts, _sample_inputs(wl, rows), mode="bf16io")[0]
+    err = rel_err(g[rows], o)
+    print("vgg19 bs8 err %.3e" % err)
+    assert err <= BF16_TOL
+    assert np.all(np.isfinite(g))
 
 
 def test_bert_ffn_layers_teacher_forced():

@@ -41,6 +41,28 @@ def test_bert_ffn_structure():
     assert abs(2 * wl.macs / 1024 / 1e6 - 113.2) < 0.1
 
 
+def test_vgg19_structure_and_work():
+    wl = workloads.vgg19(n=1)
+    comps = [n["composite"] for n in wl.graph["nodes"]]
+    assert comps.count("conv2d_bias_relu") == 17  # 16 conv3x3 + the full-map fc6
+    assert comps.count("max_pool2d") == 5
+    assert comps[-3:] == ["global_avg_pool2d", "dense_bias_relu", "dense_bias"]
+    # 19.63 G multiply-adds per 224x224 image (the usual VGG19 count)
+    assert abs(wl.macs / 1e9 - 19.63) < 0.01
+
+
+def test_full_map_conv_is_flatten_then_dense():
+    """The reading behind fc6: a convolution whose kernel covers the whole
+    feature map (no padding) equals a dense layer on the NCHW-flattened map."""
+    import oracle
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((3, 5, 4, 4))
+    w = rng.standard_normal((7, 5, 4, 4))
+    a = oracle.ops.conv2d(x, w)[:, :, 0, 0]
+    b = oracle.ops.dense(x.reshape(3, -1), w.reshape(7, -1))
+    assert np.max(np.abs(a - b)) < 1e-12
+
+
 def test_deterministic_and_distinct_seeds():
     a = workloads.build("resnet18_block")
     b = workloads.build("resnet18_block")
@@ -59,9 +81,9 @@ def test_bf16_inputs_are_representable():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block"])
+@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block", "vgg19"])
 def test_activations_stay_order_one(name):
-    wl = workloads.build(name)
+    wl = workloads.build(name, **({"hw": 112} if name == "vgg19" else {}))
     outs, vals = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io", keep=True)
     names = [n["name"] for n in wl.graph["nodes"]]
     peak = max(float(np.abs(vals[n]).max()) for n in names)
