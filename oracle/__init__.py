@@ -24,11 +24,13 @@ bf16   round-to-nearest-even of float64 values to bfloat16, done directly on
 ops    the operator definitions in float64.
 graph  the JSON subgraph reader and executor, modes "exact" and "bf16io".
 brute  pure-Python scalar loops of the same definitions, for tiny shapes.
+quant  the affine int8 (partial quantization) definitions and an executor
+       of int8 subgraphs.
 
 Every function is pinned by a CPU test against something other than itself
 (brute force, closed forms, library routines, invariants); see tests/.
 """
 
 from .bf16 import round_bf16, bf16_bits  # noqa: F401
-from . import ops, graph, brute  # noqa: F401
+from . import ops, graph, brute, quant  # noqa: F401
 from .graph import run_graph, run_node, load_graph  # noqa: F401

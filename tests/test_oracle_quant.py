@@ -1,0 +1,246 @@
+"""Pins of the int8 oracle (partial quantization, Sec. 3.2 / Fig. 4a).
+
+Each test checks a definition of ``oracle.quant`` against something other
+than itself: exact rational arithmetic (fractions), round trips of every
+code, brute-force integer loops on tiny shapes, and the float64 operator
+definitions in the cases where quantization is exact (dyadic scales and
+weights that are integer multiples of their scale, so every multiplier is a
+power of two and the integer path must equal the rounded float result).  A
+dropped zero point, a padding filled with the wrong code, a sign error in the
+border correction, a mis-scaled bias or residual, or a wrong rounding fails
+one of them.
+"""
+
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import brute, ops
+from oracle import quant as Q
+
+
+def _round_half_away(fr):
+    """Fraction -> nearest integer, ties away from zero."""
+    mag = abs(fr)
+    r = int(mag + Fraction(1, 2))  # floor for non-negative values
+    return -r if fr < 0 else r
+
+
+def test_mulq_matches_exact_rationals():
+    rng = np.random.default_rng(0)
+    for _ in range(3000):
+        a = int(rng.integers(-(2 ** 31) + 1, 2 ** 31))
+        m0 = int(rng.integers(2 ** 30, 2 ** 31))
+        t = int(rng.integers(1, 63))
+        want = _round_half_away(Fraction(a * m0, 2 ** t))
+        assert int(Q.mulq(a, m0, t)) == want, (a, m0, t)
+    # ties go away from zero
+    assert int(Q.mulq(3, 2 ** 30, 31)) == 2   # 1.5 -> 2
+    assert int(Q.mulq(-3, 2 ** 30, 31)) == -2  # -1.5 -> -2
+    assert int(Q.mulq(5, 2 ** 30, 32)) == 1   # 1.25 -> 1
+    assert int(Q.mulq(-7, 2 ** 30, 32)) == -2  # -1.75 -> -2
+
+
+def test_fixed_multiplier_is_the_nearest_representation():
+    rng = np.random.default_rng(1)
+    for m in np.concatenate([10.0 ** rng.uniform(-9, 9, 500), [0.5, 1.0, 2.0 ** -20, 1 - 2.0 ** -40]]):
+        m0, t = Q.fixed_multiplier(m)
+        assert 2 ** 30 <= m0 < 2 ** 31 and 1 <= t <= 62
+        err = abs(Fraction(m0, 2 ** t) - Fraction(float(m)))
+        assert err <= Fraction(1, 2 ** (t + 1)), m
+    assert Q.fixed_multiplier(2.0 ** -10) == (2 ** 30, 40)
+    assert Q.fixed_multiplier(1 - 2.0 ** -40) == (2 ** 30, 30)  # rounds up to 2^31: renormalised
+    assert Q.fixed_multiplier(0.0) == (0, 1)
+    assert Q.fixed_multiplier(2.0 ** -40) == (0, 1)  # would need T > 62
+    with pytest.raises(ValueError):
+        Q.fixed_multiplier(2.0 ** 30)
+
+
+@pytest.mark.parametrize("scale,zp", [(0.02, 0), (0.0371, -128), (1.7, 45), (2.0 ** -6, 127)])
+def test_quantize_dequantize_round_trips(scale, zp):
+    codes = np.arange(-128, 128)
+    back = Q.quantize(Q.dequantize(codes, scale, zp), scale, zp)
+    assert np.array_equal(back, codes)
+    rng = np.random.default_rng(2)
+    lo, hi = scale * (-128 - zp), scale * (127 - zp)
+    x = rng.uniform(lo, hi, 5000).astype(np.float32)
+    err = np.abs(Q.dequantize(Q.quantize(x, scale, zp), scale, zp).astype(np.float64) - x)
+    assert err.max() <= scale * (0.5 + 1e-5)
+    # saturation outside the range
+    assert Q.quantize(np.float32(hi + 10 * scale), scale, zp) == 127
+    assert Q.quantize(np.float32(lo - 10 * scale), scale, zp) == -128
+    # float32 product, ties to even: x = 2.5 S lands on code Z + 2
+    assert Q.quantize(np.float32(2.5 * 2.0 ** -6), 2.0 ** -6, 0) == 2
+
+
+def test_weights_quantize_per_channel_symmetric():
+    rng = np.random.default_rng(3)
+    j = rng.integers(-127, 128, size=(5, 3, 2, 2))
+    j[:, 0, 0, 0] = 127  # channel maximum
+    w = j * 2.0 ** -7
+    wq, s_w = Q.quantize_weights(w)
+    assert np.array_equal(wq, j) and np.all(s_w == 2.0 ** -7)
+    w2 = rng.normal(size=(4, 7))
+    wq2, s2 = Q.quantize_weights(w2)
+    assert np.all(np.abs(wq2).max(axis=1) == 127)
+    assert np.all(np.abs(wq2 * s2[:, None] - w2) <= s2[:, None] / 2 + 1e-15)
+    wq0, s0 = Q.quantize_weights(np.zeros((2, 3)))
+    assert np.all(wq0 == 0) and np.all(s0 == 1.0)
+
+
+def test_relu6_bound_in_code_space():
+    assert Q.act_bounds("relu6", 0.05, -100) == (-100, 20)
+    assert Q.act_bounds("relu", 0.05, -100) == (-100, 127)
+    assert Q.act_bounds(None, 0.05, 3) == (-128, 127)
+    with pytest.raises(ValueError):
+        Q.act_bounds("gelu", 0.1, 0)
+
+
+@pytest.mark.parametrize("shape,wshape,strides,padding", [
+    ((1, 2, 5, 4), (3, 2, 3, 3), (1, 1), (1, 1, 1, 1)),
+    ((2, 3, 6, 7), (2, 3, 3, 2), (2, 1), (2, 0, 1, 1)),
+    ((1, 1, 4, 4), (2, 1, 1, 1), (1, 1), (0, 0, 0, 0)),
+])
+def test_integer_conv_against_brute_force(shape, wshape, strides, padding):
+    rng = np.random.default_rng(4)
+    xq = rng.integers(-128, 128, size=shape)
+    wq = rng.integers(-127, 128, size=wshape)
+    zx = 37
+    got = Q.conv_accumulate(xq, zx, wq, strides, padding)
+    # taps outside the image contribute nothing: brute force over (x - Z)
+    want = np.array(brute.conv2d((xq - zx).tolist(), wq.tolist(), strides, padding))
+    assert np.array_equal(got, want.astype(np.int64))
+
+
+def _dyadic_case(seed, zx, zy, act, residual):
+    """Codes and constants for which int8 execution is exact: S_x = 2^-5,
+    S_w = 2^-7 (weights integer multiples of it, channel maximum 127),
+    S_y = 2^-3, so the accumulator multiplier is 2^-9; the bias is an
+    integer multiple of S_x S_w; a residual shares S_y (multiplier 1)."""
+    rng = np.random.default_rng(seed)
+    sx, sw, sy = 2.0 ** -5, 2.0 ** -7, 2.0 ** -3
+    xq = rng.integers(-128, 128, size=(2, 3, 6, 5))
+    j = rng.integers(-127, 128, size=(4, 3, 3, 3))
+    j[:, 0, 0, 0] = 127
+    w = j * sw
+    b = rng.integers(-3000, 3000, size=4) * (sx * sw)
+    rq = rng.integers(-128, 128, size=(2, 4, 3, 3)) if residual else None
+    return sx, sy, xq, w, b, rq
+
+
+@pytest.mark.parametrize("zx,zy,act,residual", [(0, 0, None, False), (37, -20, None, False),
+                                                 (-90, -128, "relu", True), (11, 5, "relu6", True)])
+def test_quantized_conv_equals_rounded_float_conv(zx, zy, act, residual):
+    sx, sy, xq, w, b, rq = _dyadic_case(5, zx, zy, act, residual)
+    attrs = {"strides": (2, 2), "padding": (1, 1, 1, 1)}
+    qr = (sy, 13) if residual else None
+    got = Q.qconv(xq, (sx, zx), w, b, attrs, (sy, zy), act, rq, qr)
+    # float definition on the dequantized input (zero padding = code Z_x)
+    yf = ops.bias_add(ops.conv2d(sx * (xq - zx), w, (2, 2), (1, 1, 1, 1)), b)
+    if residual:
+        yf = yf + sy * (rq - 13)
+    t = yf / sy  # exact: dyadic values far below 2^53
+    want = zy + np.sign(t) * np.floor(np.abs(t) + 0.5)
+    lo, hi = Q.act_bounds(act, sy, zy)
+    want = np.clip(np.clip(want, lo, hi), -128, 127)
+    assert np.array_equal(got, want.astype(np.int64))
+
+
+def test_quantized_dense_equals_rounded_float_dense():
+    rng = np.random.default_rng(6)
+    sx, sw, sy, zx, zy = 2.0 ** -4, 2.0 ** -7, 2.0 ** -2, -50, 9
+    xq = rng.integers(-128, 128, size=(5, 40))
+    j = rng.integers(-127, 128, size=(6, 40))
+    j[:, 0] = -127
+    b = rng.integers(-500, 500, size=6) * (sx * sw)
+    got = Q.qdense(xq, (sx, zx), j * sw, b, (sy, zy), "relu")
+    t = ops.bias_add(ops.dense(sx * (xq - zx), j * sw), b) / sy
+    want = np.clip(np.maximum(zy + np.sign(t) * np.floor(np.abs(t) + 0.5), zy), -128, 127)
+    assert np.array_equal(got, want.astype(np.int64))
+
+
+def test_max_pool_commutes_with_dequantize():
+    rng = np.random.default_rng(7)
+    xq = rng.integers(-128, 128, size=(2, 3, 7, 6))
+    attrs = {"pool_size": (3, 3), "strides": (2, 2), "padding": (1, 1, 1, 1)}
+    got = Q.qmax_pool2d(xq, attrs)
+    want = brute.max_pool2d(xq.tolist(), (3, 3), (2, 2), (1, 1, 1, 1))
+    assert np.array_equal(got, np.array(want, dtype=np.int64))
+    s, z = 0.07, -30
+    assert np.array_equal(Q.dequantize(got, s, z),
+                          ops.max_pool2d(Q.dequantize(xq, s, z), (3, 3), (2, 2), (1, 1, 1, 1)).astype(np.float32))
+
+
+def test_global_avg_pool_rounds_the_mean():
+    rng = np.random.default_rng(8)
+    xq = rng.integers(-128, 128, size=(3, 5, 4, 4))
+    s, zx, zy = 0.1, 17, -3
+    got = Q.qglobal_avg_pool2d(xq, (s, zx), (s, zy))  # multiplier 1/16: exact
+    want = [[zy + _round_half_away(Fraction(int((xq[n, c] - zx).sum()), 16)) for c in range(5)]
+            for n in range(3)]
+    assert np.array_equal(got, np.clip(np.array(want), -128, 127))
+
+
+def test_add_with_shared_scale_is_integer_sum():
+    rng = np.random.default_rng(9)
+    a = rng.integers(-128, 128, size=(2, 8))
+    b = rng.integers(-128, 128, size=(2, 8))
+    s = 0.25
+    got = Q.qadd(a, (s, 10), b, (s, -4), (s, 2), "relu")
+    want = np.clip(np.maximum((a - 10) + (b + 4) + 2, 2), -128, 127)
+    assert np.array_equal(got, want)
+
+
+def _tiny_int8_graph():
+    rng = np.random.default_rng(10)
+    w1 = rng.normal(0, 0.3, size=(8, 3, 3, 3)).astype(np.float32)
+    b1 = rng.normal(0, 0.1, size=8).astype(np.float32)
+    w2 = rng.normal(0, 0.2, size=(8, 8, 1, 1)).astype(np.float32)
+    wd = rng.normal(0, 0.2, size=(5, 8)).astype(np.float32)
+
+    def q(s, z):
+        return {"scale": s, "zero_point": z}
+
+    g = {"format": "byoc-subgraph", "version": 1,
+         "inputs": [{"name": "x", "shape": [2, 3, 9, 9], "dtype": "f32", "quant": q(1 / 255, -128)}],
+         "constants": [{"name": "w1", "index": 0, "shape": [8, 3, 3, 3], "dtype": "f32"},
+                       {"name": "b1", "index": 1, "shape": [8], "dtype": "f32"},
+                       {"name": "w2", "index": 2, "shape": [8, 8, 1, 1], "dtype": "f32"},
+                       {"name": "wd", "index": 3, "shape": [5, 8], "dtype": "f32"}],
+         "nodes": [
+             {"name": "c1", "composite": "conv2d_bias_relu", "inputs": ["x", "w1", "b1"], "out_dtype": "int8",
+              "attrs": {"strides": [1, 1], "padding": [1, 1, 1, 1]}, "quant": q(0.02, -128)},
+             {"name": "c2", "composite": "conv2d_add_relu", "inputs": ["c1", "w2", "c1"], "out_dtype": "int8",
+              "quant": q(0.03, -128)},
+             {"name": "p", "composite": "max_pool2d", "inputs": ["c2"], "out_dtype": "int8",
+              "attrs": {"pool_size": [3, 3], "strides": [2, 2], "padding": [1, 1, 1, 1]}, "quant": q(0.03, -128)},
+             {"name": "g", "composite": "global_avg_pool2d", "inputs": ["p"], "out_dtype": "int8",
+              "quant": q(0.02, -128)},
+             {"name": "d", "composite": "dense", "inputs": ["g", "wd"], "out_dtype": "int8", "quant": q(0.01, 0)}],
+         "outputs": [{"name": "d", "dtype": "f32"}]}
+    return g, [w1, b1, w2, wd]
+
+
+def test_int8_graph_tracks_the_float_graph():
+    """The int8 executor reproduces the float graph within the quantization
+    error (a sanity bound, not an exact pin), and its codes chain through
+    the per-op definitions above."""
+    from oracle.graph import run_graph
+    g, consts = _tiny_int8_graph()
+    x = np.random.default_rng(11).random((2, 3, 9, 9)).astype(np.float32)
+    got, codes = Q.run_quantized_graph(g, consts, [x], keep=True)
+    gf = {**g, "nodes": [{**n, "out_dtype": "f32"} for n in g["nodes"]]}
+    ref = run_graph(gf, consts, [x], mode="exact")[0]
+    assert np.max(np.abs(got[0] - ref)) < 0.06
+    c1 = Q.qconv(Q.quantize(x, 1 / 255, -128), (1 / 255, -128), consts[0], consts[1],
+                 {"strides": [1, 1], "padding": [1, 1, 1, 1]}, (0.02, -128), "relu")
+    assert np.array_equal(codes["c1"], c1)
+    assert np.array_equal(got[0], Q.dequantize(codes["d"], 0.01, 0))
+
+
+def test_int8_graph_rejects_pool_rescaling():
+    g, consts = _tiny_int8_graph()
+    g["nodes"][2]["quant"] = {"scale": 0.05, "zero_point": -128}
+    with pytest.raises(ValueError):
+        Q.run_quantized_graph(g, consts, [np.zeros((2, 3, 9, 9), np.float32)])
