@@ -44,7 +44,20 @@
  *           even), fp32 bias, fp32 accumulation, each node's output rounded
  *           to bf16; an "f32" input is rounded to bf16 at the boundary
  *           (the partial-quantization cast of Sec. 3.2, Fig. 4a);
- *   "f32":  fp32 throughout, true fp32 products.
+ *   "f32":  fp32 throughout, true fp32 products;
+ *   "int8": partial quantization (Sec. 3.2, Fig. 4a).  Every input and
+ *           node carries "quant": {"scale": S > 0, "zero_point": Z in
+ *           [-128, 127]} for the affine codes of its tensor, T = S (T_q - Z).
+ *           Inputs are quantized at the boundary in fp32 arithmetic,
+ *           q = clip(rint(x * fl32(1/S)) + Z); outputs are dequantized to
+ *           their declared "f32" or "bf16" dtype, S (q - Z).  Weights are
+ *           quantized per output channel, symmetric (S_w = max|W|/127);
+ *           biases become int32 in the accumulator's scale.  Conv and dense
+ *           accumulate exactly in int32 on int8 MFMA; every rescaling is a
+ *           fixed-point multiply m0 2^-t rounded once, ties away from zero;
+ *           activations clamp in code space (ReLU >= Z, ReLU6 <= Z +
+ *           rint(6/S)).  A max pool keeps its input's S and Z.  Not in int8
+ *           graphs: depthwise convs and GELU.
  * Internally activations of bf16 graphs are NHWC with channels padded to a
  * multiple of 8 (the layout-transform nodes of Sec. 3.2, Fig. 4b, sit at
  * the function boundary); callers always see the declared layouts.
@@ -110,7 +123,8 @@ typedef enum {
   BYOC_K_AVGPOOL = 4,
   BYOC_K_ADD = 5,       /* standalone elementwise add                   */
   BYOC_K_TRANSFORM = 6, /* boundary layout / dtype transform            */
-  BYOC_K_REDUCE = 7     /* split-K reduction with the fused epilogue    */
+  BYOC_K_REDUCE = 7,    /* split-K reduction with the fused epilogue    */
+  BYOC_K_CONV_I8 = 8    /* implicit-GEMM conv / dense on int8 MFMA      */
 } byoc_kernel_kind;
 
 /* One entry of the launch sequence a run enqueues. */

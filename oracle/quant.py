@@ -59,6 +59,8 @@ def _as_f32(v):
 def fixed_multiplier(m):
     """(M0, T) with m ~= M0 2^-T for a real multiplier 0 <= m < 2^30.
 
+    A multiplier that rounds up to 2^30 itself is rejected as well.
+
     m = f 2^e with f in [0.5, 1) (frexp); M0 = rint(f 2^31), T = 31 - e; a
     rounding up to 2^31 is renormalised to M0 = 2^30, T - 1.  A multiplier
     too small for T <= 62 (or zero) becomes (0, 1): the term vanishes.
@@ -74,6 +76,8 @@ def fixed_multiplier(m):
     if m0 == 2 ** 31:
         m0 = 2 ** 30
         t -= 1
+    if t < 1:
+        raise ValueError("multiplier %r rounds to 2^30" % m)
     if t > 62:
         return 0, 1
     return m0, t
@@ -232,8 +236,11 @@ def run_quantized_graph(graph, consts, inputs, keep=False):
             raise ValueError("node %s: not an int8 node" % node["name"])
         op, has_bias, has_add, act = parse_composite(node["composite"])
         attrs = node.get("attrs", {})
-        qy = _qp(node, "node " + node["name"])
         ins = node["inputs"]
+        if op == "max_pool2d" and not node.get("quant"):
+            qy = qps[ins[0]]  # a max pool keeps its input's scale and zero point
+        else:
+            qy = _qp(node, "node " + node["name"])
         if op in ("conv2d", "dense"):
             x, w = ins[0], cvals[ins[1]]
             i = 2

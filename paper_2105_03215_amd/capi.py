@@ -17,7 +17,7 @@ BYOC_OK = 0
 F32, BF16 = 0, 1
 NCHW, NHWC, ROWMAJOR = 0, 1, 2
 KIND_NAMES = ["conv_mfma", "conv_f32", "depthwise", "maxpool", "avgpool", "add", "transform",
-              "reduce"]
+              "reduce", "conv_i8"]
 STATUS_NAMES = ["OK", "INVALID_ARG", "PARSE", "UNSUPPORTED", "SHAPE", "DEVICE", "OOM", "INTERNAL"]
 
 # Every entry point declared in include/byoc.h.

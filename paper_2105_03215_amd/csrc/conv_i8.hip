@@ -1,0 +1,345 @@
+// Implicit-GEMM convolution on CDNA4 int8 MFMA (v_mfma_i32_16x16x64_i8)
+// for partially quantized subgraphs (Sec. 3.2, Fig. 4a).
+//
+// The GEMM is the one of the bf16 kernels: M = N*P*Q output pixels, N = K
+// output channels, a reduction over kk = (r*S + s)*Cp + c with NHWC int8
+// activations and K-major packed int8 weights, so a row of either operand is
+// contiguous along the reduction and every lane moves 16 bytes (16 codes,
+// one MFMA operand register quadruple) per load.  The operand tiles stream
+// from HBM straight into a ring of NS LDS buffers (buffer_load ... lds), 128
+// reduction elements per stage; a 128-byte LDS row holds one operand row of
+// a stage with the chunk swizzle ch ^ (row & 7) applied on the fetch side.
+// Accumulation is exact in int32.
+//
+// Zero points.  The MFMA sums x_q * w_q over the taps inside the image (a
+// tap outside reads zeros).  The affine input needs sum (x_q - Z_x) w_q: the
+// host folds -Z_x * (sum of all weights of channel k) into the bias, and for
+// a pixel whose window crosses the border the epilogue adds back Z_x times
+// the weight sums of its taps outside the image (wtap[k][r*S + s]).
+//
+// Epilogue: each thread finishes 8 consecutive channels of one pixel from
+// int32 sums staged in LDS: bias, border correction, fixed-point rescaling
+// (one rounding), the residual's own rescaling, the activation clamp in
+// code space and the int8 clip, one 8-byte store.
+#include "lds_dma.h"
+
+namespace byoc {
+namespace {
+
+using namespace dma;
+
+constexpr int kBK = 128;       // reduction elements (bytes) per stage
+constexpr int kCH = 8;         // 16-byte chunks per tile row
+constexpr int kCE = 16;        // reduction elements per chunk
+constexpr int kMaxStages = 4;
+
+__device__ __forceinline__ i32x4 as_i32x4(uint4 u) { return __builtin_bit_cast(i32x4, u); }
+
+template <int BM, int BN, int WM, int WN, int NS, bool ALIGNED>
+__global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
+  static_assert(WM * WN == 4, "4 waves");
+  const ConvParams& p = q.g;
+  constexpr int kNT = 256;
+  constexpr int kRowsPerPass = kNT / kCH;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 16, TN = WTN / 16;
+  constexpr int AR = BM / kRowsPerPass, BR = BN / kRowsPerPass;
+  static_assert(TM >= 1 && TN >= 1 && AR >= 1 && BR >= 1, "tile too small");
+  constexpr int LPS = AR + BR;
+  constexpr int STAGE = (BM + BN) * kCH;  // uint4 per stage buffer
+  static_assert(NS >= 2 && NS <= kMaxStages, "stages");
+
+  __shared__ uint4 ring[NS * STAGE];
+  materialize_args(p);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  auto buf = [&](auto tag) -> uint4* { return ring + decltype(tag)::value * STAGE; };
+  const int wm = wave / WN, wn = wave % WN;
+  const int r0 = tid / kCH;
+  const int cv = (lane & 7) ^ ((lane >> 3) & 7);
+
+  int tm, tn;
+  if (!place_tile<BM, BN>(p, &tm, &tn)) return;
+  const int m0 = tm * BM;
+  const int n0 = tn * BN;
+  const int nkt = (p.Kg + kBK - 1) / kBK;
+
+  // Activation rows of this thread (see the bf16 kernel): element (= byte)
+  // offset of the window origin plus this thread's chunk, and on the
+  // aligned path (a stage is 128 channels of one tap) the taps inside.
+  int pix[AR], a_ih[AR], a_iw[AR];
+  uint32_t tapmask[AR];
+  const int PQ = p.P * p.Q;
+#pragma unroll
+  for (int i = 0; i < AR; ++i) {
+    const int m = m0 + r0 + i * kRowsPerPass;
+    int ih0 = -(1 << 28), iw0 = 0, n = 0;
+    if (m < p.M) {
+      n = mdiv(m, p.mg_pq);
+      const int pq = m - n * PQ;
+      const int pp = mdiv(pq, p.mg_q);
+      const int qq = pq - pp * p.Q;
+      ih0 = pp * p.sh - p.pt;
+      iw0 = qq * p.sw - p.pl;
+    }
+    a_ih[i] = ih0;
+    a_iw[i] = iw0;
+    pix[i] = m < p.M ? ((n * p.H + ih0) * p.W + iw0) * p.Cp : 0;
+    if (ALIGNED) {
+      pix[i] += cv * kCE;
+      const int r_lo = max(0, -ih0), nr = max(0, min(p.R, p.H - ih0) - r_lo);
+      const int s_lo = max(0, -iw0), s_hi = min(p.S, p.W - iw0);
+      const uint32_t cols =
+          s_hi > s_lo ? (uint32_t)(((1ull << s_hi) - 1ull) & ~((1ull << s_lo) - 1ull)) : 0u;
+      uint32_t mask = 0;
+      for (int r = 0; r < p.R; ++r)
+        if ((unsigned)(r - r_lo) < (unsigned)nr) mask |= cols << (r * p.S);
+      tapmask[i] = mask;
+    }
+  }
+  const i32x4 xr = buffer_rsrc(p.x, p.x_bytes);
+  const i32x4 wr = buffer_rsrc(p.w, p.w_bytes);
+  uint32_t wvoff[BR];
+#pragma unroll
+  for (int i = 0; i < BR; ++i) wvoff[i] = (uint32_t)((n0 + r0 + i * kRowsPerPass) * p.Kgp + cv * kCE);
+
+  int r = 0, s = 0, c = ALIGNED ? 0 : cv * kCE, kk = ALIGNED ? 0 : cv * kCE, wcol = 0;
+  if (!ALIGNED) {
+    const int rs = mdiv(kk, p.mg_cp);
+    c = kk - rs * p.Cp;
+    r = mdiv(rs, p.mg_s);
+    s = rs - r * p.S;
+  }
+
+  // Loads of the next stage into buffer SET; past the end of the reduction
+  // the offsets are out of range (zero fills), which keeps the count of
+  // loads in flight fixed.
+  int kleft = nkt;
+  auto issue = [&](auto set_tag) {
+    uint4* dst = buf(set_tag);
+    const bool live = kleft-- > 0;
+    const int tap = (r * p.W + s) * p.Cp + c;
+    const int bit = (r * p.S + s) & 31;
+    const bool kval = live && (ALIGNED || kk < p.Kg);
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+      bool ok;
+      if (ALIGNED) {
+        ok = live && ((tapmask[i] >> bit) & 1u);
+      } else {
+        const int ih = a_ih[i] + r;
+        const int iw = a_iw[i] + s;
+        ok = kval && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+      }
+      const uint32_t off = ok ? (uint32_t)(pix[i] + tap) : kOOB;
+      lds_fill16(xr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (i * kRowsPerPass + wave * 8) * kCH)), off);
+    }
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+      lds_fill16(wr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (BM + i * kRowsPerPass + wave * 8) * kCH)),
+                 live ? wvoff[i] + (uint32_t)wcol : kOOB);
+    wcol += kBK;
+    c += kBK;
+    if (ALIGNED) {
+      if (c == p.Cp) {
+        c = 0;
+        if (++s == p.S) {
+          s = 0;
+          ++r;
+        }
+      }
+    } else {
+      kk += kBK;
+      while (c >= p.Cp) {
+        c -= p.Cp;
+        if (++s == p.S) {
+          s = 0;
+          ++r;
+        }
+      }
+    }
+  };
+
+  i32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = i32x4{0, 0, 0, 0};
+
+  // One stage: 2 k-steps of the 16x16x64 MFMA; lane l reads 16 codes of
+  // row l % 16 at chunk (k-step, l / 16) of both operands.
+  auto compute = [&](auto set_tag) {
+    const uint4* sA = buf(set_tag);
+    const uint4* sB = sA + BM * kCH;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 64; ++ks) {
+      const int chunk = ks * 4 + (lane >> 4);
+      i32x4 af[TN], bfr[TM];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int row = wn * WTN + i * 16 + (lane & 15);
+        af[i] = as_i32x4(sB[row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * WTM + j * 16 + (lane & 15);
+        bfr[j] = as_i32x4(sA[row * kCH + (chunk ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  // residual codes of the 8 channels this thread finishes per pass, fetched
+  // before the reduction so that their latency overlaps it
+  constexpr int kEC = 32;
+  constexpr int NPASS = BN / kEC;
+  constexpr int TPP = kEC / 8;
+  constexpr int EPV = (BM * TPP + kNT - 1) / kNT;
+  const int ec8 = (tid % TPP) * 8;
+  uint2 resv[NPASS][EPV];
+  {
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16_t*>(p.res), (short)0, p.res ? p.res_bytes : 0, kBufferFlags);
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        const int px = (tid + e * kNT) / TPP;
+        const int m = m0 + px;
+        const uint32_t off = (px < BM && m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) : kOOB;
+        resv[pass][e] = p.res ? __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0))
+                              : make_uint2(0u, 0u);
+      }
+    }
+  }
+
+  static_assert((NS - 2) * LPS <= 63, "vmcnt immediate");
+  auto round_step = [&](auto i) {
+    constexpr int I = decltype(i)::value;
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 2) * LPS) : "memory");
+    issue(std::integral_constant<int, (I + NS - 1) % NS>{});
+    compute(i);
+  };
+  static_for<0, NS - 1>([&](auto i) { issue(i); });
+  int t = 0;
+  for (; t + NS <= nkt; t += NS) static_for<0, NS>(round_step);
+  const int rem = nkt - t;
+  static_for<0, NS - 1>([&](auto i) {
+    if (rem > decltype(i)::value) round_step(i);
+  });
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  constexpr int kLd = kEC + 4;
+  static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
+  int* stage = reinterpret_cast<int*>(ring);
+  const int RS = p.R * p.S;
+#pragma unroll
+  for (int pass = 0; pass < NPASS; ++pass) {
+    if (pass > 0) lds_barrier();
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int ch = wn * WTN + i * 16 + 4 * (lane >> 4) - pass * kEC;
+      if (ch < 0 || ch >= kEC) continue;
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int px = wm * WTM + j * 16 + (lane & 15);
+        *(i32x4*)(stage + px * kLd + ch) = acc[i][j];
+      }
+    }
+    lds_barrier();
+    const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) {
+      const int px = (tid + e * kNT) / TPP;
+      const int m = m0 + px;
+      if (px >= BM || m >= p.M || k >= p.Kp) continue;
+      const int* st = stage + px * kLd + ec8;
+      const int4 lo4 = *(const int4*)st, hi4 = *(const int4*)(st + 4);
+      int a[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
+      const int4* qc = reinterpret_cast<const int4*>(q.qch) + k;
+#pragma unroll
+      for (int c8 = 0; c8 < 8; ++c8) a[c8] += qc[c8].x;
+      if (q.wtap) {
+        // window of this pixel: taps outside the image get Z_x * their weight sums back
+        const int n = mdiv(m, p.mg_pq);
+        const int pq = m - n * PQ;
+        const int pp = mdiv(pq, p.mg_q);
+        const int qq = pq - pp * p.Q;
+        const int ih0 = pp * p.sh - p.pt, iw0 = qq * p.sw - p.pl;
+        const bool inside = ih0 >= 0 && iw0 >= 0 && ih0 + p.R <= p.H && iw0 + p.S <= p.W;
+        if (!inside) {
+          int corr[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+          for (int rr = 0; rr < p.R; ++rr)
+            for (int ss = 0; ss < p.S; ++ss) {
+              const int ih = ih0 + rr, iw = iw0 + ss;
+              if ((unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W) continue;
+              const int* wt = q.wtap + (size_t)k * RS + rr * p.S + ss;
+#pragma unroll
+              for (int c8 = 0; c8 < 8; ++c8) corr[c8] += wt[c8 * RS];
+            }
+#pragma unroll
+          for (int c8 = 0; c8 < 8; ++c8) a[c8] += q.zx * corr[c8];
+        }
+      }
+      const uint2 rv = resv[pass][e];
+      const uint32_t rw[2] = {rv.x, rv.y};
+      uint32_t out[2] = {0u, 0u};
+#pragma unroll
+      for (int c8 = 0; c8 < 8; ++c8) {
+        const int4 qcv = qc[c8];
+        int64_t v = (int64_t)q.zy + mulq(a[c8], qcv.y, qcv.z);
+        if (p.res) {
+          const int rc = (int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3)));
+          v += mulq(rc - q.zr, q.mr, q.tr);
+        }
+        v = v < q.lo ? q.lo : v;
+        v = v > q.hi ? q.hi : v;
+        out[c8 >> 2] |= ((uint32_t)clip_i8(v) & 0xFFu) << (8 * (c8 & 3));
+      }
+      *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) = make_uint2(out[0], out[1]);
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
+  QConvParams q = q_in;
+  ConvParams& p = q.g;
+  const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
+  const int blocks = placed_blocks(p, BM, BN);
+  hipError_t r = hipErrorInvalidValue;
+  static_for<2, kMaxStages + 1>([&](auto i) {
+    constexpr int NS = decltype(i)::value;
+    if constexpr (NS * (BM + BN) * 128 <= kLdsLimit) {
+      if (ns != NS) return;
+      if (aligned) conv_i8_kernel<BM, BN, WM, WN, NS, true><<<blocks, 256, 0, s>>>(q);
+      else conv_i8_kernel<BM, BN, WM, WN, NS, false><<<blocks, 256, 0, s>>>(q);
+      r = hipGetLastError();
+    }
+  });
+  return r;
+}
+
+}  // namespace
+
+bool conv_i8_tile_supported(int bm, int bn, int stages) {
+  if (stages < 2 || stages > kMaxStages) return false;
+  return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
+}
+
+hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, hipStream_t s) {
+  if (!conv_i8_tile_supported(bm, bn, stages)) return hipErrorInvalidValue;
+  if (p.g.Cp % kCE != 0 || p.g.Kp % 8 != 0 || p.g.Kgp % kBK != 0) return hipErrorInvalidValue;
+  if (bm == 128 && bn == 128) return launch_tile<128, 128, 2, 2>(p, stages, s);
+  if (bm == 128 && bn == 64) return launch_tile<128, 64, 2, 2>(p, stages, s);
+  if (bm == 64 && bn == 64) return launch_tile<64, 64, 2, 2>(p, stages, s);
+  return launch_tile<32, 64, 1, 4>(p, stages, s);
+}
+
+}  // namespace byoc

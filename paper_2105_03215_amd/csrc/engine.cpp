@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -30,12 +31,41 @@ constexpr int kKPad = 64;     // packed reduction length is padded to this (the 
 constexpr int kHaloStages = 3;  // halo kernel weight ring: 3 stages of one kernel row (built-in choice)
 
 struct PackJob {
-  enum Kind { ConvW, DwW, Vec, Copy, StemW } kind;
+  enum Kind { ConvW, DwW, Vec, Copy, StemW, Host } kind;  // Host: copy blob n, built on the host
   int cidx = -1;       // constant index
   int64_t dst = 0;     // byte offset in the weights region
   int K = 0, Cg = 0, R = 0, S = 0, Cp = 0, Kgp = 0, rows = 0;
   int n = 0, n_out = 0;
 };
+
+// Fixed-point form m0 2^-t of a real rescaling factor 0 <= m < 2^30 of an
+// int8 graph: m = f 2^e (f in [0.5, 1)), m0 = rint(f 2^31) (ties to even),
+// t = 31 - e, a rounding up to 2^31 renormalised to (2^30, t - 1); a factor
+// that needs t > 62 (or zero) becomes (0, 1).  False when out of range.
+bool fixed_multiplier(double m, int* m0, int* t) {
+  if (!(m >= 0.0 && m < 1073741824.0)) return false;
+  if (m == 0.0) {
+    *m0 = 0;
+    *t = 1;
+    return true;
+  }
+  int e = 0;
+  const double f = std::frexp(m, &e);
+  long long mm = (long long)std::nearbyint(f * 2147483648.0);
+  int tt = 31 - e;
+  if (mm == 2147483648LL) {
+    mm = 1073741824LL;
+    tt -= 1;
+  }
+  if (tt < 1) return false;
+  if (tt > 62) {
+    mm = 0;
+    tt = 1;
+  }
+  *m0 = (int)mm;
+  *t = tt;
+  return true;
+}
 
 // Chooses the workgroup tile and split-K factor of an implicit GEMM.  The
 // kernel is latency bound per stage, so the model favours the largest tile
@@ -153,6 +183,10 @@ int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
   return best;
 }
 
+void name_conv_i8(Launch& L) {
+  std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_%dx%d_s%d", L.tile.bm, L.tile.bn, L.tile.stages);
+}
+
 void name_conv(Launch& L) {
   if (L.tile.halo)
     std::snprintf(L.info.name, sizeof(L.info.name), "conv_halo_%dx%d_s%d_lp%d_pb%d", L.tile.bm, L.tile.bn,
@@ -177,13 +211,18 @@ struct Planner {
   // fused stems: conv node -> its max-pool node, max-pool node -> conv node
   std::vector<int> stem_pool, stem_conv;
 
-  Planner(Engine* e_, Graph& g_) : e(e_), g(g_), bf16(g_.compute == DType::BF16) {
+  bool i8;                                  // partially quantized (int8) graph
+  const byoc_const* consts = nullptr;       // host constants (int8 weights are quantized on the host)
+  std::vector<std::vector<uint8_t>> blobs;  // host-built constant blocks (PackJob::Host)
+
+  Planner(Engine* e_, Graph& g_) : e(e_), g(g_), bf16(g_.compute == DType::BF16), i8(g_.compute == DType::I8) {
     loc.resize(g.values.size());
     cp.assign(g.values.size(), 0);
   }
 
   int64_t internal_bytes(int v) const {
     const auto& s = g.values[v].shape;
+    if (i8) return (s.size() == 4 ? s[0] * s[2] * s[3] : s[0]) * rup(s[1], 16);
     if (!bf16) return numel(s) * 4;
     const int64_t c = rup(s[1], 8);
     return (s.size() == 4 ? s[0] * s[2] * s[3] : s[0]) * c * 2;
@@ -217,10 +256,21 @@ struct Planner {
   int64_t ext_bytes(int v, DType dt) const {
     return numel(g.values[v].shape) * (dt == DType::BF16 ? 2 : 4);
   }
-  int64_t act_bytes(int v) const { return numel(g.values[v].shape) * (bf16 ? 2 : 4); }
+  int64_t act_bytes(int v) const { return numel(g.values[v].shape) * (i8 ? 1 : (bf16 ? 2 : 4)); }
+  Ref host_blob(std::vector<uint8_t>&& b) {
+    Ref r = wslot((int64_t)b.size());
+    PackJob j{PackJob::Host};
+    j.dst = r.off;
+    j.n = (int)blobs.size();
+    jobs.push_back(j);
+    blobs.push_back(std::move(b));
+    return r;
+  }
 
   Status plan();
+  Status plan_i8();
   void plan_node(int ni);
+  void plan_node_i8(int ni);
   void find_stems();
   void plan_stem(int conv_ni, int pool_ni);
 };
@@ -307,6 +357,7 @@ void Planner::plan_stem(int ci, int pi) {
 }
 
 Status Planner::plan() {
+  if (i8) return plan_i8();
   find_stems();
   // ---- inputs: direct use or boundary transform ----------------------------
   for (size_t i = 0; i < g.inputs.size(); ++i) {
@@ -642,6 +693,276 @@ void Planner::plan_node(int ni) {
   e->launches.push_back(L);
 }
 
+// ---- int8 graphs (partial quantization, Sec. 3.2, Fig. 4a) -----------------
+// Inputs pass through a quantize node (fp32 arithmetic, NCHW -> NHWC codes
+// with channels padded to 16), every composite runs on codes, outputs pass
+// through a dequantize node.  Weights, biases and rescaling factors are
+// quantized here on the host, in float64, and uploaded as built.
+Status Planner::plan_i8() {
+  auto dims = [&](int v, int* N, int* C, int* H, int* W) {
+    const auto& s = g.values[v].shape;
+    *N = (int)s[0];
+    *C = (int)s[1];
+    *H = s.size() == 4 ? (int)s[2] : 1;
+    *W = s.size() == 4 ? (int)s[3] : 1;
+  };
+  for (size_t i = 0; i < g.inputs.size(); ++i) {
+    const IoDesc& in = g.inputs[i];
+    const int v = in.value;
+    const Value& val = g.values[v];
+    cp[v] = (int)rup(val.shape[1], 16);
+    loc[v] = arena(internal_bytes(v));
+    Launch L;
+    L.op = Launch::QuantizeI8;
+    L.info.kind = BYOC_K_TRANSFORM;
+    L.info.node = -1;
+    L.x = io(Ref::Input, (int)i);
+    L.y = loc[v];
+    L.src_bf16 = in.dtype == DType::BF16;
+    dims(v, &L.N, &L.C, &L.H, &L.W);
+    L.Cp = cp[v];
+    L.qscale = (float)(1.0 / val.qscale);
+    L.qzero = val.qzero;
+    L.info.bytes = ext_bytes(v, in.dtype) + act_bytes(v);
+    name(L, "quantize_in");
+    e->launches.push_back(L);
+  }
+  for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
+    const int v = g.nodes[ni].out;
+    cp[v] = (int)rup(g.values[v].shape[1], 16);
+    loc[v] = arena(internal_bytes(v));
+    plan_node_i8((int)ni);
+    if (!err.ok()) return err;
+  }
+  for (size_t j = 0; j < g.outputs.size(); ++j) {
+    const IoDesc& o = g.outputs[j];
+    const int v = o.value;
+    const Value& val = g.values[v];
+    Launch L;
+    L.op = Launch::DequantizeI8;
+    L.info.kind = BYOC_K_TRANSFORM;
+    L.info.node = -1;
+    L.x = loc[v];
+    L.y = io(Ref::Output, (int)j);
+    L.dst_bf16 = o.dtype == DType::BF16;
+    dims(v, &L.N, &L.C, &L.H, &L.W);
+    L.Cp = cp[v];
+    L.qscale = (float)val.qscale;
+    L.qzero = val.qzero;
+    L.info.bytes = act_bytes(v) + ext_bytes(v, o.dtype);
+    name(L, "dequantize_out");
+    e->launches.push_back(L);
+  }
+  return Status::Ok();
+}
+
+void Planner::plan_node_i8(int ni) {
+  const Node& n = g.nodes[ni];
+  const Value& xv = g.values[n.data];
+  const Value& yv = g.values[n.out];
+  const auto& xs = xv.shape;
+  const auto& ys = yv.shape;
+  const std::string where = "node " + std::to_string(ni) + " (" + n.composite + ")";
+  auto fail = [&](const std::string& m) { err = Status::Err(BYOC_ERR_UNSUPPORTED, where + ": " + m); };
+  Launch L;
+  L.info.node = ni;
+  L.x = loc[n.data];
+  L.y = loc[n.out];
+  L.act = (int)n.act;
+  // activation clamp in output codes (ReLU: v >= Z_y; ReLU6: v <= Z_y + rint(6 / S_y))
+  int lo = -128, hi = 127;
+  if (n.act == Act::Relu || n.act == Act::Relu6) lo = yv.qzero;
+  if (n.act == Act::Relu6) {
+    const double h = yv.qzero + std::nearbyint(6.0 / yv.qscale);
+    hi = h < 127.0 ? (int)h : 127;
+  }
+
+  if (n.op == OpKind::Conv || n.op == OpKind::Dense) {
+    const bool dense = n.op == OpKind::Dense;
+    const auto& ws = g.values[n.weight].shape;
+    const int K = (int)ws[0], Cg = (int)ws[1];
+    const int R = dense ? 1 : (int)ws[2], S = dense ? 1 : (int)ws[3];
+    const int N = (int)xs[0], C = (int)xs[1];
+    const int H = dense ? 1 : (int)xs[2], W = dense ? 1 : (int)xs[3];
+    const int P = dense ? 1 : (int)ys[2], Q = dense ? 1 : (int)ys[3];
+    const int Cp = cp[n.data], Kp = cp[n.out];
+    QConvParams& q = L.qc;
+    ConvParams& p = q.g;
+    p.N = N, p.H = H, p.W = W, p.Cp = Cp, p.P = P, p.Q = Q, p.R = R, p.S = S;
+    p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1];
+    p.M = N * P * Q;
+    p.Kp = Kp;
+    p.Kg = R * S * Cp;
+    p.Kgp = (int)rup(p.Kg, 128);
+    p.ldy = Kp;
+    p.ldr = Kp;
+    p.act = (int)n.act;
+    p.splits = 1;
+    p.k_tiles_per_split = p.Kgp / 128;
+    const int rows = (int)rup(Kp, kRowPad);
+    const int64_t xb = (int64_t)N * H * W * Cp, wb = (int64_t)rows * p.Kgp, rb = (int64_t)p.M * Kp;
+    if (xb >= (int64_t(1) << 31) || wb >= (int64_t(1) << 31) || rb >= (int64_t(1) << 31))
+      return fail("an operand of 2 GiB or more");
+    if ((int64_t)p.M * P * Q >= (int64_t(1) << 40) || (int64_t)p.Kg * Cp >= (int64_t(1) << 40))
+      return fail("too many output pixels for the index arithmetic");
+    // |sum of (x - Z_x) w| <= R S C 255 127 plus the folded bias (< 2^30) stays inside int32
+    if ((int64_t)R * S * Cg * 255 * 127 >= (int64_t(1) << 30)) return fail("reduction too long for int32 accumulation");
+    p.x_bytes = (int)xb;
+    p.w_bytes = (int)wb;
+    p.res_bytes = (int)rb;
+    p.mg_pq = magic40(P * Q);
+    p.mg_q = magic40(Q);
+    p.mg_cp = magic40(Cp);
+    p.mg_s = magic40(S);
+
+    // host quantization of the weights (per output channel, symmetric),
+    // the bias and the rescaling factors
+    const byoc_const& wcst = consts[g.values[n.weight].index];
+    const bool wbf = wcst.dtype == BYOC_BF16;
+    auto wget = [&](int64_t i) -> double {
+      if (wbf) {
+        const uint32_t b = (uint32_t)((const uint16_t*)wcst.data)[i] << 16;
+        float f;
+        std::memcpy(&f, &b, 4);
+        return f;
+      }
+      return ((const float*)wcst.data)[i];
+    };
+    const byoc_const* bcst = n.bias >= 0 ? &consts[g.values[n.bias].index] : nullptr;
+    auto bget = [&](int k) -> double {
+      if (bcst->dtype == BYOC_BF16) {
+        const uint32_t b = (uint32_t)((const uint16_t*)bcst->data)[k] << 16;
+        float f;
+        std::memcpy(&f, &b, 4);
+        return f;
+      }
+      return ((const float*)bcst->data)[k];
+    };
+    const int RS = R * S;
+    const bool border = !dense && xv.qzero != 0 && (n.pad[0] | n.pad[1] | n.pad[2] | n.pad[3]) != 0;
+    std::vector<uint8_t> packed((size_t)rows * p.Kgp, 0);
+    std::vector<int32_t> qch((size_t)rows * 4, 0), wtap(border ? (size_t)rows * RS : 0, 0);
+    for (int k = K; k < rows; ++k) qch[(size_t)k * 4 + 2] = 1;
+    const double sx = xv.qscale, sy = yv.qscale;
+    for (int k = 0; k < K; ++k) {
+      const int64_t base = (int64_t)k * Cg * RS;
+      double amax = 0.0;
+      for (int64_t i = 0; i < (int64_t)Cg * RS; ++i) amax = std::max(amax, std::fabs(wget(base + i)));
+      const double sw = amax > 0.0 ? amax / 127.0 : 1.0;
+      int64_t total = 0;
+      for (int c = 0; c < Cg; ++c)
+        for (int r = 0; r < R; ++r)
+          for (int s2 = 0; s2 < S; ++s2) {
+            double qv = std::nearbyint(wget(base + ((int64_t)c * R + r) * S + s2) / sw);
+            qv = std::min(127.0, std::max(-127.0, qv));
+            const int wq = (int)qv;
+            packed[(size_t)k * p.Kgp + (size_t)(r * S + s2) * Cp + c] = (uint8_t)(int8_t)wq;
+            total += wq;
+            if (border) wtap[(size_t)k * RS + r * S + s2] += wq;
+          }
+      double bq = 0.0;
+      if (bcst) {
+        bq = std::nearbyint(bget(k) / (sx * sw));
+        bq = std::min(2147483647.0, std::max(-2147483648.0, bq));
+      }
+      const int64_t beff = (int64_t)bq - (int64_t)xv.qzero * total;
+      if (beff <= -(int64_t(1) << 30) || beff >= (int64_t(1) << 30))
+        return fail("quantized bias of channel " + std::to_string(k) + " outside +-2^30");
+      int m0 = 0, t = 1;
+      if (!fixed_multiplier((sx * sw) / sy, &m0, &t))
+        return fail("rescaling factor of channel " + std::to_string(k) + " outside [0, 2^30)");
+      qch[(size_t)k * 4 + 0] = (int32_t)beff;
+      qch[(size_t)k * 4 + 1] = m0;
+      qch[(size_t)k * 4 + 2] = t;
+    }
+    L.w = host_blob(std::move(packed));
+    std::vector<uint8_t> qb(qch.size() * 4);
+    std::memcpy(qb.data(), qch.data(), qb.size());
+    L.bias = host_blob(std::move(qb));
+    if (border) {
+      std::vector<uint8_t> tb(wtap.size() * 4);
+      std::memcpy(tb.data(), wtap.data(), tb.size());
+      L.other = host_blob(std::move(tb));
+    }
+    q.zx = xv.qzero;
+    q.zy = yv.qzero;
+    q.lo = lo;
+    q.hi = hi;
+    if (n.residual >= 0) {
+      const Value& rv = g.values[n.residual];
+      L.res = loc[n.residual];
+      q.zr = rv.qzero;
+      if (!fixed_multiplier(rv.qscale / sy, &q.mr, &q.tr)) return fail("residual rescaling factor outside [0, 2^30)");
+    }
+    // tile: the largest with at least two workgroups per CU
+    auto tiles = [&](int bm, int bn) { return ((int64_t)p.M + bm - 1) / bm * ((Kp + bn - 1) / bn); };
+    ConvTile& t = L.tile;
+    t = ConvTile{};
+    t.stages = 3;
+    if (tiles(128, 128) >= 512) t.bm = 128, t.bn = 128;
+    else if (tiles(128, 64) >= 512) t.bm = 128, t.bn = 64;
+    else if (p.M <= 32) t.bm = 32, t.bn = 64;
+    else t.bm = 64, t.bn = 64;
+    // BYOC_I8_TILE=<bm>x<bn>s<stages> forces a tile (any tile gives the same codes)
+    if (const char* te = std::getenv("BYOC_I8_TILE")) {
+      int bm = 0, bn = 0, ns = 0;
+      if (std::sscanf(te, "%dx%ds%d", &bm, &bn, &ns) == 3 && conv_i8_tile_supported(bm, bn, ns))
+        t.bm = bm, t.bn = bn, t.stages = ns;
+    }
+    p.xcd_py = choose_xcd_split(p, t);
+    L.tile_default = t;
+    L.op = Launch::ConvI8;
+    L.info.kind = BYOC_K_CONV_I8;
+    L.info.flops = 2 * n.macs;
+    L.info.bytes = numel(xs) + numel(ws) + numel(ys) * (n.residual >= 0 ? 2 : 1);
+    name_conv_i8(L);
+    e->launches.push_back(L);
+    return;
+  }
+  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool) {
+    PoolParams& p = L.pool;
+    p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3], p.Cp = cp[n.data];
+    p.R = n.pool[0], p.S = n.pool[1], p.sh = n.stride[0], p.sw = n.stride[1];
+    p.pt = n.pad[0], p.pl = n.pad[1];
+    p.P = n.op == OpKind::MaxPool ? (int)ys[2] : 1;
+    p.Q = n.op == OpKind::MaxPool ? (int)ys[3] : 1;
+    L.info.bytes = act_bytes(n.data) + act_bytes(n.out);
+    if (n.op == OpKind::MaxPool) {
+      L.op = Launch::MaxPoolI8;
+      L.info.kind = BYOC_K_MAXPOOL;
+      name(L, "maxpool_nhwc_i8");
+    } else {
+      if ((int64_t)p.H * p.W * 256 >= (int64_t(1) << 31)) return fail("image too large for the int32 pool sum");
+      L.op = Launch::AvgPoolI8;
+      L.info.kind = BYOC_K_AVGPOOL;
+      L.qzx = xv.qzero;
+      L.qzy = yv.qzero;
+      if (!fixed_multiplier(xv.qscale / (yv.qscale * p.H * p.W), &L.qm0, &L.qt))
+        return fail("rescaling factor outside [0, 2^30)");
+      name(L, "avgpool_nhwc_i8");
+    }
+    e->launches.push_back(L);
+    return;
+  }
+  // Add
+  const Value& bv = g.values[n.other];
+  QAddParams& a = L.qa;
+  a.n = internal_bytes(n.out);
+  a.za = xv.qzero;
+  a.zb = bv.qzero;
+  a.zy = yv.qzero;
+  a.lo = lo;
+  a.hi = hi;
+  if (!fixed_multiplier(xv.qscale / yv.qscale, &a.ma, &a.ta) || !fixed_multiplier(bv.qscale / yv.qscale, &a.mb, &a.tb))
+    return fail("rescaling factor outside [0, 2^30)");
+  L.op = Launch::AddI8;
+  L.info.kind = BYOC_K_ADD;
+  L.other = loc[n.other];
+  L.info.bytes = 3 * act_bytes(n.out);
+  name(L, "add_i8");
+  e->launches.push_back(L);
+}
+
 // First-fit offset allocator over the arena with coalescing frees.
 struct OffsetAlloc {
   std::vector<std::pair<int64_t, int64_t>> free_;  // (offset, size), sorted by offset
@@ -798,6 +1119,37 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
                                    L.Kp, c.s);
     case Launch::Cast:
       return launch_cast(c.ptr(L.x), L.src_bf16, c.ptr(L.y), L.dst_bf16, L.n, c.s);
+    case Launch::ConvI8: {
+      QConvParams q = L.qc;
+      q.g.x = (const bf16_t*)c.ptr(L.x);
+      q.g.w = (const bf16_t*)c.ptr(L.w);
+      q.g.res = (const bf16_t*)c.ptr(L.res);
+      q.g.y = (bf16_t*)c.ptr(L.y);
+      q.qch = (const int32_t*)c.ptr(L.bias);
+      q.wtap = (const int32_t*)c.ptr(L.other);
+      return launch_conv_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, c.s);
+    }
+    case Launch::MaxPoolI8:
+    case Launch::AvgPoolI8: {
+      PoolParams p = L.pool;
+      p.x = c.ptr(L.x);
+      p.y = c.ptr(L.y);
+      if (L.op == Launch::MaxPoolI8) return launch_maxpool_nhwc_i8(p, c.s);
+      return launch_avgpool_nhwc_i8(p, L.qzx, L.qzy, L.qm0, L.qt, c.s);
+    }
+    case Launch::AddI8: {
+      QAddParams a = L.qa;
+      a.a = (const int8_t*)c.ptr(L.x);
+      a.b = (const int8_t*)c.ptr(L.other);
+      a.y = (int8_t*)c.ptr(L.y);
+      return launch_add_i8(a, c.s);
+    }
+    case Launch::QuantizeI8:
+      return launch_quantize_i8(c.ptr(L.x), L.src_bf16, (int8_t*)c.ptr(L.y), L.N, L.C, L.H, L.W, L.Cp, L.qscale,
+                                L.qzero, c.s);
+    case Launch::DequantizeI8:
+      return launch_dequantize_i8((const int8_t*)c.ptr(L.x), c.ptr(L.y), L.dst_bf16, L.N, L.C, L.H, L.W, L.Cp,
+                                  L.qscale, L.qzero, c.s);
     case Launch::StemConvPool: {
       StemParams p = L.stem;
       p.x = c.ptr(L.x);
@@ -863,7 +1215,10 @@ Status build_device_state(Engine* e, Planner& pl, const byoc_const* consts) {
     if (!st.ok()) break;
     hipError_t err = hipSuccess;
     char* dst = e->weights + j.dst;
-    if (j.cidx < 0) {
+    if (j.kind == PackJob::Host) {
+      const auto& b = pl.blobs[j.n];
+      err = hipMemcpy(dst, b.data(), b.size(), hipMemcpyHostToDevice);
+    } else if (j.cidx < 0) {
       err = hipMemsetAsync(dst, 0, (size_t)j.n_out * 4, nullptr);
     } else {
       const Value& v = pl.g.values[pl.g.const_values[j.cidx]];
@@ -913,6 +1268,7 @@ Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int 
   e->device = device;
   DeviceGuard guard(device);
   Planner pl(e, e->graph);
+  pl.consts = consts;
   Status st = pl.plan();
   if (st.ok()) st = build_device_state(e, pl, consts);
   if (!st.ok()) {

@@ -24,7 +24,8 @@ struct Ref {
 struct Launch {
   enum Op {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
-    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows
+    AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows,
+    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;
@@ -35,6 +36,11 @@ struct Launch {
   DwParams dw{};
   PoolParams pool{};
   StemParams stem{};
+  QConvParams qc{};  // int8 conv / dense (qc.g holds the geometry; tile in `tile`)
+  QAddParams qa{};   // int8 add
+  float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
+  int qzero = 0;                 // quantize / dequantize zero point
+  int qzx = 0, qzy = 0, qm0 = 0, qt = 1;  // int8 average pool
   int64_t n = 0;
   int act = 0;
   bool src_bf16 = false, dst_bf16 = false;

@@ -2,6 +2,7 @@
 // node (or input / constant) and the field at fault.
 #include "graph.h"
 
+#include <cmath>
 #include <map>
 #include <sstream>
 
@@ -58,6 +59,23 @@ bool parse_dtype(const std::string& s, DType* d) {
     return true;
   }
   return false;
+}
+
+// Optional "quant": {"scale": S > 0, "zero_point": Z in [-128, 127]}.
+Status parse_quant(const JsonValue& d, const std::string& where, Value* v) {
+  const JsonValue* q = d.get("quant");
+  if (!q) return Status::Ok();
+  if (q->kind != JsonValue::Object) return perr(where + ": quant must be an object");
+  const JsonValue* sc = q->get("scale");
+  const JsonValue* zp = q->get("zero_point");
+  if (!sc || sc->kind != JsonValue::Number || !(sc->num > 0.0) || !std::isfinite(sc->num))
+    return perr(where + ": quant.scale must be a positive finite number");
+  if (!zp || zp->kind != JsonValue::Number || !zp->is_integer || zp->inum < -128 || zp->inum > 127)
+    return perr(where + ": quant.zero_point must be an integer in [-128, 127]");
+  v->has_q = true;
+  v->qscale = sc->num;
+  v->qzero = (int)zp->inum;
+  return Status::Ok();
 }
 
 // Optional integer-pair attribute (e.g. strides) with a default.
@@ -208,6 +226,8 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
         return uerr(where + ": layout " + lay + " not supported for rank " +
                     std::to_string(v.shape.size()));
     }
+    Status qs = parse_quant(d, where, &v);
+    if (!qs.ok()) return qs;
     v.source = Value::Input;
     v.index = (int)i;
     io.value = add_value(v);
@@ -282,12 +302,13 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
     n.act = cn.act;
     std::string odt;
     DType out_dtype;
-    if (!get_string(d, "out_dtype", &odt) || !parse_dtype(odt, &out_dtype))
-      return perr(where + ": out_dtype must be \"f32\" or \"bf16\"");
+    if (get_string(d, "out_dtype", &odt) && (odt == "int8" || odt == "i8")) out_dtype = DType::I8;
+    else if (odt.empty() || !parse_dtype(odt, &out_dtype))
+      return perr(where + ": out_dtype must be \"f32\", \"bf16\" or \"int8\"");
     if (ni == 0) g.compute = out_dtype;
     else if (out_dtype != g.compute)
       return uerr(where + ": mixed out_dtype in one graph (graph computes in " +
-                  std::string(g.compute == DType::BF16 ? "bf16" : "f32") + ")");
+                  std::string(g.compute == DType::BF16 ? "bf16" : (g.compute == DType::I8 ? "int8" : "f32")) + ")");
     const JsonValue* refs = d.get("inputs");
     if (!refs || refs->kind != JsonValue::Array) return perr(where + ": inputs must be a list");
     std::vector<int> args;
@@ -422,9 +443,38 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
     ov.dtype = out_dtype;
     ov.source = Value::Node;
     ov.index = (int)ni;
+    Status qs = parse_quant(d, where, &ov);
+    if (!qs.ok()) return qs;
+    if (out_dtype == DType::I8) {
+      // the int8 forms: every tensor quantized, no depthwise, no GELU; a max
+      // pool keeps its input's codes (and inherits them when none are given)
+      for (int a : {n.data, n.residual, n.other}) {
+        if (a < 0 || g.values[a].has_q) continue;
+        return serr(where + ": int8 operand '" + g.values[a].name + "' has no quant parameters");
+      }
+      if (n.depthwise) return uerr(where + ": depthwise conv has no int8 form");
+      if (n.act == Act::Gelu) return uerr(where + ": gelu has no int8 form");
+      if (n.op == OpKind::MaxPool) {
+        const Value& xv = g.values[n.data];
+        if (ov.has_q && (ov.qscale != xv.qscale || ov.qzero != xv.qzero))
+          return serr(where + ": an int8 max pool keeps its input's scale and zero point");
+        ov.has_q = true;
+        ov.qscale = xv.qscale;
+        ov.qzero = xv.qzero;
+      }
+      if (!ov.has_q) return perr(where + ": int8 node needs quant {scale, zero_point}");
+    } else if (ov.has_q) {
+      return uerr(where + ": quant parameters only in int8 graphs");
+    }
     n.out = add_value(ov);
     g.macs += n.macs;
     g.nodes.push_back(n);
+  }
+
+  for (const IoDesc& in : g.inputs) {
+    const Value& v = g.values[in.value];
+    if (g.compute != DType::I8 && v.has_q)
+      return uerr("input " + v.name + ": quant parameters only in int8 graphs");
   }
 
   // ---- outputs -------------------------------------------------------------
@@ -445,7 +495,7 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
     io.value = it->second;
     const auto& s = g.values[io.value].shape;
     std::string dt;
-    io.dtype = g.values[io.value].dtype;
+    io.dtype = g.values[io.value].dtype == DType::I8 ? DType::F32 : g.values[io.value].dtype;
     if (get_string(d, "dtype", &dt) && !parse_dtype(dt, &io.dtype))
       return perr(where + ": dtype must be \"f32\" or \"bf16\"");
     io.layout = s.size() == 4 ? BYOC_NCHW : BYOC_ROWMAJOR;

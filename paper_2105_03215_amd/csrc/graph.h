@@ -24,7 +24,9 @@ struct Status {
   }
 };
 
-enum class DType { F32 = BYOC_F32, BF16 = BYOC_BF16 };
+// I8: the compute type of a partially quantized graph (int8 codes with an
+// affine scale and zero point per tensor); never an external dtype.
+enum class DType { F32 = BYOC_F32, BF16 = BYOC_BF16, I8 = 2 };
 enum class Act { None = 0, Relu = 1, Relu6 = 2, Gelu = 3 };
 enum class OpKind { Conv, Dense, MaxPool, AvgPool, Add };
 
@@ -35,6 +37,10 @@ struct Value {
   DType dtype = DType::F32;
   enum Source { Input, Const, Node } source = Input;
   int index = -1;  // input number, constant index or node number
+  // int8 graphs: affine codes of this tensor, value = qscale * (code - qzero)
+  bool has_q = false;
+  double qscale = 0.0;
+  int qzero = 0;
 };
 
 struct Node {

@@ -1,0 +1,190 @@
+"""Partially quantized (int8) subgraphs on the GPU against the int8 oracle.
+
+Every int8 composite is exact integer arithmetic followed by one fixed-point
+rounding, so the executor's outputs (dequantized to float32, a one-to-one
+map of the codes) must equal the oracle's bit for bit.  Cases span aligned
+(128-channel stages) and unaligned reductions, ragged channel counts, every
+tile shape, the border correction of a nonzero input zero point under
+padding, strides, residuals, ReLU / ReLU6, pools, the standalone add and the
+boundary quantize / dequantize; the ResNet-50 case runs at batch 32 and
+224x224 (the benchmark's configuration) with the scales calibrated through
+the executor, and the oracle recomputes sampled images.
+"""
+
+import copy
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import quant as OQ
+from paper_2105_03215_amd import quantize, workloads
+from parity_util import announce
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _run(graph, consts, inputs):
+    from paper_2105_03215_amd import capi, runtime
+    sg = capi.Subgraph(graph, consts, device=0)
+    try:
+        return runtime.run_once(sg, inputs, DEV), sg.launches()
+    finally:
+        sg.close()
+
+
+def _q(s, z):
+    return {"scale": float(s), "zero_point": int(z)}
+
+
+def _conv_graph(n, c, h, w, k, r, stride, pad, zx, act, residual, bias=True, seed=0):
+    rng = np.random.default_rng(seed)
+    wt = rng.normal(0, (2.0 / (c * r * r)) ** 0.5, size=(k, c, r, r)).astype(np.float32)
+    consts = [wt]
+    cdesc = [{"name": "w", "index": 0, "shape": list(wt.shape), "dtype": "f32"}]
+    ins = ["x", "w"]
+    if bias:
+        consts.append(rng.normal(0, 0.2, size=k).astype(np.float32))
+        cdesc.append({"name": "b", "index": 1, "shape": [k], "dtype": "f32"})
+        ins.append("b")
+    p = (h + 2 * pad - r) // stride + 1
+    q = (w + 2 * pad - r) // stride + 1
+    inputs_desc = [{"name": "x", "shape": [n, c, h, w], "dtype": "f32", "quant": _q(0.011, zx)}]
+    inputs = [rng.uniform(-1.2, 1.7, size=(n, c, h, w)).astype(np.float32)]
+    if residual:
+        inputs_desc.append({"name": "r", "shape": [n, k, p, q], "dtype": "f32", "quant": _q(0.019, -7)})
+        inputs.append(rng.normal(0, 1, size=(n, k, p, q)).astype(np.float32))
+        ins.append("r")
+    comp = "conv2d" + ("_bias" if bias else "") + ("_add" if residual else "") + ("_" + act if act else "")
+    g = {"format": "byoc-subgraph", "version": 1, "inputs": inputs_desc, "constants": cdesc,
+         "nodes": [{"name": "y", "composite": comp, "inputs": ins, "out_dtype": "int8",
+                    "attrs": {"strides": [stride, stride], "padding": [pad] * 4}, "quant": _q(0.023, -11)}],
+         "outputs": [{"name": "y", "dtype": "f32"}]}
+    return g, consts, inputs
+
+
+CONV_CASES = [
+    # n, c, h, w, k, r, stride, pad, zx, act, residual
+    (2, 128, 14, 14, 128, 3, 1, 1, 0, "relu", False),      # aligned, interior + border, Z_x = 0
+    (2, 128, 14, 13, 192, 3, 1, 1, 37, "relu", True),      # aligned, border correction, residual
+    (1, 200, 9, 11, 72, 3, 2, 1, -100, None, False),       # unaligned ragged channels, stride 2
+    (3, 3, 30, 30, 64, 7, 2, 3, 5, "relu", False),         # stem-like: 3 channels, 7x7
+    (4, 256, 8, 8, 512, 1, 2, 0, 64, None, True),          # 1x1 stride 2 projection, residual
+    (1, 64, 56, 56, 256, 1, 1, 0, -128, "relu6", False),  # many pixels: 128x128 tiles
+    (2, 48, 5, 5, 40, 5, 1, 2, 90, "relu6", True),         # tiny image, every pixel on the border
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[str(i) for i in range(len(CONV_CASES))])
+def test_int8_conv_bit_exact(case):
+    n, c, h, w, k, r, stride, pad, zx, act, residual = case
+    announce("int8 conv %s" % (case,))
+    g, consts, inputs = _conv_graph(n, c, h, w, k, r, stride, pad, zx, act, residual, seed=len(str(case)))
+    got, launches = _run(g, consts, inputs)
+    assert any(l["kind"] == "conv_i8" for l in launches)
+    ref = OQ.run_quantized_graph(g, consts, inputs)
+    assert got[0].shape == ref[0].shape
+    assert np.array_equal(got[0], ref[0].astype(np.float64)), np.abs(got[0] - ref[0]).max()
+
+
+def test_int8_tiles_agree():
+    """Every tile shape and ring depth gives the same codes (integer sums)."""
+    announce("int8 conv every tile")
+    import os
+    g, consts, inputs = _conv_graph(2, 144, 12, 12, 136, 3, 1, 1, 21, "relu", True, seed=3)
+    ref = OQ.run_quantized_graph(g, consts, inputs)[0]
+    for tile in ("128x128s2", "128x64s4", "64x64s3", "32x64s2"):
+        os.environ["BYOC_I8_TILE"] = tile
+        try:
+            got, launches = _run(g, consts, inputs)
+        finally:
+            del os.environ["BYOC_I8_TILE"]
+        name = [l["name"] for l in launches if l["kind"] == "conv_i8"][0]
+        assert name == "conv_i8_" + tile.replace("s", "_s"), name
+        assert np.array_equal(got[0], ref.astype(np.float64)), tile
+
+
+def test_int8_dense_pool_add():
+    announce("int8 dense, pools, add")
+    rng = np.random.default_rng(7)
+    wd = rng.normal(0, 0.1, size=(1000, 96)).astype(np.float32)
+    bd = rng.normal(0, 0.1, size=1000).astype(np.float32)
+    g = {"format": "byoc-subgraph", "version": 1,
+         "inputs": [{"name": "x", "shape": [5, 96, 9, 7], "dtype": "bf16", "quant": _q(0.02, -3)},
+                    {"name": "z", "shape": [5, 96, 9, 7], "dtype": "f32", "quant": _q(0.03, 40)}],
+         "constants": [{"name": "wd", "index": 0, "shape": [1000, 96], "dtype": "f32"},
+                       {"name": "bd", "index": 1, "shape": [1000], "dtype": "f32"}],
+         "nodes": [
+             {"name": "a", "composite": "add_relu", "inputs": ["x", "z"], "out_dtype": "int8", "quant": _q(0.04, -128)},
+             {"name": "m", "composite": "max_pool2d", "inputs": ["a"], "out_dtype": "int8",
+              "attrs": {"pool_size": [3, 3], "strides": [2, 2], "padding": [1, 1, 1, 1]}},
+             {"name": "p", "composite": "global_avg_pool2d", "inputs": ["m"], "out_dtype": "int8",
+              "quant": _q(0.01, -120)},
+             {"name": "d", "composite": "dense_bias", "inputs": ["p", "wd", "bd"], "out_dtype": "int8",
+              "quant": _q(0.05, 2)}],
+         "outputs": [{"name": "d", "dtype": "f32"}, {"name": "m", "dtype": "f32"}, {"name": "a", "dtype": "bf16"}]}
+    x = oracle.bf16.round_bf16(rng.normal(0, 1, size=(5, 96, 9, 7))).astype(np.float32)
+    z = rng.normal(0, 1, size=(5, 96, 9, 7)).astype(np.float32)
+    got, _ = _run(g, [wd, bd], [x, z])
+    ref = OQ.run_quantized_graph(g, [wd, bd], [x, z])
+    for i in range(2):
+        assert np.array_equal(got[i], ref[i].astype(np.float64)), i
+    # a bf16 output is the float32 dequantized value rounded to bf16
+    assert np.array_equal(got[2], oracle.bf16.round_bf16(ref[2].astype(np.float64)))
+
+
+def test_int8_two_runs_and_bs1_graph():
+    """The tiny mixed graph twice on one engine: identical results."""
+    from paper_2105_03215_amd import capi, runtime
+    import test_oracle_quant as T
+    announce("int8 tiny graph twice")
+    g, consts = T._tiny_int8_graph()
+    x = np.random.default_rng(12).random((2, 3, 9, 9)).astype(np.float32)
+    sg = capi.Subgraph(g, consts, device=0)
+    try:
+        a = runtime.run_once(sg, [x], DEV)[0]
+        b = runtime.run_once(sg, [x], DEV)[0]
+    finally:
+        sg.close()
+    ref = OQ.run_quantized_graph(g, consts, [x])[0]
+    assert np.array_equal(a, ref.astype(np.float64)) and np.array_equal(a, b)
+
+
+def _calibrated_resnet50(n, hw, calib_n=2):
+    import torch
+    wl = workloads.build("resnet50_v1", n=n, hw=hw)
+    cal = copy.deepcopy(wl.graph)
+    cal["inputs"] = [dict(d, shape=[calib_n] + d["shape"][1:]) for d in cal["inputs"]]
+    from paper_2105_03215_amd import runtime
+    batch = [torch.from_numpy(np.ascontiguousarray(a[:calib_n])).to(DEV).to(
+        torch.bfloat16 if d["dtype"] == "bf16" else torch.float32) for a, d in zip(wl.inputs, cal["inputs"])]
+    ranges = quantize.calibrate(cal, wl.consts, [batch])
+    qg = quantize.quantize_graph(wl.graph, ranges)
+    for o in qg["outputs"]:
+        o["dtype"] = "f32"  # float32 dequantized values map one to one onto the codes
+    return wl, qg
+
+
+def test_int8_resnet50_small_full_compare():
+    announce("int8 resnet50 n=2 hw=64")
+    wl, qg = _calibrated_resnet50(2, 64)
+    got, launches = _run(qg, wl.consts, wl.inputs)
+    ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
+    assert np.array_equal(got[0], ref.astype(np.float64))
+    assert sum(1 for l in launches if l["kind"] == "conv_i8") == 54
+    # the int8 network tracks the bf16 one (a sanity bound on calibration)
+    fl = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    assert np.corrcoef(got[0].ravel(), fl.ravel())[0, 1] > 0.9
+
+
+def test_int8_resnet50_bs32_sampled():
+    announce("int8 resnet50 bs32 224 sampled images 0 and 31")
+    wl, qg = _calibrated_resnet50(32, 224)
+    got, _ = _run(qg, wl.consts, wl.inputs)
+    rows = [0, 31]
+    g2 = copy.deepcopy(qg)
+    g2["inputs"] = [dict(d, shape=[2] + d["shape"][1:]) for d in g2["inputs"]]
+    ref = OQ.run_quantized_graph(g2, wl.consts, [np.ascontiguousarray(a[rows]) for a in wl.inputs])[0]
+    assert np.array_equal(got[0][rows], ref.astype(np.float64))

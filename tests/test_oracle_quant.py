@@ -55,6 +55,8 @@ def test_fixed_multiplier_is_the_nearest_representation():
     assert Q.fixed_multiplier(2.0 ** -40) == (0, 1)  # would need T > 62
     with pytest.raises(ValueError):
         Q.fixed_multiplier(2.0 ** 30)
+    with pytest.raises(ValueError):
+        Q.fixed_multiplier(2.0 ** 30 - 2.0 ** -30)  # rounds to 2^30
 
 
 @pytest.mark.parametrize("scale,zp", [(0.02, 0), (0.0371, -128), (1.7, 45), (2.0 ** -6, 127)])
