@@ -24,6 +24,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "images/sec (bs1, bs32) ResNet-50 offloaded subgraph; conv TFLOP/s as % MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
+PEAK_INT8_TOPS = 5033.2  # dense int8 MFMA: 256 CU x 2.4 GHz x 8192 OP/clk
 PEAK_HBM_GBS = 8000.0
 
 
@@ -173,6 +174,63 @@ def _partitioned(args, wl, dev, stream):
             "node_offload": round(st["node_offload"], 4), "mac_offload": round(st["mac_offload"], 4)}
 
 
+def _quantized(args, wl, dev, stream, calib_images=2):
+    """The same network partially quantized (Sec. 3.2, Fig. 4a): scales and
+    zero points calibrated through the executor on a few images, int8 codes
+    inside the function, quantize / dequantize at its boundary.  Same
+    measurement as the headline; the conv class is priced against the dense
+    int8 MFMA peak."""
+    import copy
+
+    import numpy as np
+    import torch
+
+    from paper_2105_03215_amd import capi, quantize, runtime
+
+    t0 = time.perf_counter()
+    cal = copy.deepcopy(wl.graph)
+    cal["inputs"] = [dict(d, shape=[calib_images] + d["shape"][1:]) for d in cal["inputs"]]
+    batch = [runtime.to_device(np.ascontiguousarray(a[:calib_images]), d["dtype"], dev)
+             for a, d in zip(wl.inputs, cal["inputs"])]
+    ranges = quantize.calibrate(cal, wl.consts, [batch])
+    qg = quantize.quantize_graph(wl.graph, ranges)
+    calib_s = time.perf_counter() - t0
+    sg = capi.Subgraph(qg, wl.consts, device=0)
+    try:
+        ins = runtime.inputs_for(sg, wl.inputs, dev)
+        outs = runtime.outputs_for(sg, dev)
+        if not args.no_autotune:
+            sg.set_options(autotune=True)
+        sg.set_options(graph_replay=not args.eager)
+        for _ in range(args.warmup):
+            sg.run(ins, outs, stream)
+        torch.cuda.synchronize()
+        ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
+        sg.set_options(graph_replay=False)
+        launches = sg.launches()
+        per_launch, _ = _profile(sg, ins, outs, stream, args.steps)
+    finally:
+        sg.close()
+    if args.dump_launches:
+        root, ext = os.path.splitext(args.dump_launches)
+        with open(root + "_int8" + ext, "w") as f:
+            json.dump([dict(l, ms=round(t, 5)) for l, t in zip(launches, per_launch)], f, indent=1)
+    other_ms = sum(t for l, t in zip(launches, per_launch) if l["kind"] != "conv_i8")
+    conv_ms = max(ms - other_ms, 1e-9)
+    ops = sum(l["flops"] for l in launches if l["kind"] == "conv_i8")
+    tops = ops / (conv_ms * 1e-3) / 1e12
+    n = wl.inputs[0].shape[0]
+    return {"workload": "%s_bs%d_int8" % (args.variant, n), "images_per_s": round(n / (ms * 1e-3), 1),
+            "ms_per_step": round(ms, 4), "dtype": "int8 codes, int32 accumulation",
+            "calibration": "%d images through the executor, %.2f s" % (calib_images, calib_s),
+            "roofline": {"bound": "mfma", "achieved": round(tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                         "frac": round(tops / PEAK_INT8_TOPS, 4), "traffic": None,
+                         "kernel": "conv/dense int8 MFMA class (conv_i8), %d launches per step"
+                                   % sum(1 for l in launches if l["kind"] == "conv_i8"),
+                         "ops_per_step": ops, "kernel_ms_per_step": round(conv_ms, 4)},
+            "kernel_classes": _class_summary(launches, per_launch), "launches": len(launches)}
+
+
 def _other_workload(args, name, batch, dev, stream):
     """Throughput and conv-class roofline of another fully offloaded network
     (same measurement as the headline: graph replay, autotune, inputs in
@@ -215,6 +273,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
     ap.add_argument("--no-other", action="store_true", help="skip the VGG19 bs32 line")
+    ap.add_argument("--no-quantized", action="store_true",
+                    help="skip the int8 (partially quantized) run of the network")
     ap.add_argument("--no-partitioned", action="store_true",
                     help="skip the operator-level model run through the partitioner and its runtime")
     ap.add_argument("--no-autotune", action="store_true",
@@ -317,6 +377,9 @@ def main():
     parted = None
     if not args.no_partitioned:
         parted = _partitioned(args, wl, dev, stream)
+    quant = None
+    if not args.no_quantized:
+        quant = _quantized(args, wl, dev, stream)
     other = None
     if not args.no_other:
         other = [_other_workload(args, "vgg19", 32, dev, stream)]
@@ -340,6 +403,7 @@ def main():
         "cpu_baseline": cpu,
         "bs1": bs1,
         "partitioned": parted,
+        "quantized": quant,
         "other_workloads": other,
         "kernel_classes": _class_summary(launches, per_launch),
         "create_s": round(create_s, 3),

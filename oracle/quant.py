@@ -20,29 +20,26 @@ others in the design notes):
   S_w[k] = max |W[k]| / 127 in float64 (1 for an all-zero channel),
   W_q = clip(rint(W / S_w[k]), -127, 127); a bias becomes the int32
   b_q[k] = rint(b[k] / (S_x S_w[k])) (saturated);
-* a real rescaling factor m is applied in fixed point, as in the
-  integer-arithmetic-only inference of Jacob et al. (CVPR 2018): m = M0 2^-T
-  with M0 an integer in [2^30, 2^31) (see ``fixed_multiplier``), and
-  mulq(a, M0, T) is a M0 / 2^T rounded to nearest, ties away from zero,
-  computed exactly (one rounding);
+* a real rescaling factor m is applied in float32: rescale(a, m) =
+  rint(fl32(fl32(a) * fl32(m))), ties to even, saturated to +-2^20 before the
+  conversion back to an integer (one rounding of the product; the factor
+  must be finite, positive and below 2^20);
 * conv / dense: acc = sum over taps inside the image and input channels of
   (x_q - Z_x) W_q, plus b_q (exact integers; padding contributes nothing,
   which is zero padding of the float tensor), then
-  v = Z_y + mulq(acc, M(S_x S_w[k] / S_y)) [+ mulq(r_q - Z_r, M(S_r / S_y))],
+  v = Z_y + rescale(acc, S_x S_w[k] / S_y) [+ rescale(r_q - Z_r, S_r / S_y)],
   the activation as a clamp in code space (ReLU: v >= Z_y; ReLU6 also
   v <= Z_y + rint(6 / S_y)), and a final clip to [-128, 127];
 * max pooling takes the largest code of the window (monotone, so the output
   keeps the input's S and Z; padding never wins);
-* global average pooling: v = Z_y + mulq(sum_hw (x_q - Z_x), M(S_x / (S_y H W)));
-* add: v = Z_y + mulq(a_q - Z_a, M(S_a / S_y)) + mulq(b_q - Z_b, M(S_b / S_y)),
+* global average pooling: v = Z_y + rescale(sum_hw (x_q - Z_x), S_x / (S_y H W));
+* add: v = Z_y + rescale(a_q - Z_a, S_a / S_y) + rescale(b_q - Z_b, S_b / S_y),
   then the activation clamp and the clip.
 
 The conv sum runs through ``ops.conv2d`` in float64 on integer-valued
 arrays: every partial sum is an integer far below 2^53, so the result is
 the exact integer whatever the summation order.
 """
-
-import math
 
 import numpy as np
 
@@ -56,44 +53,21 @@ def _as_f32(v):
     return np.asarray(v, dtype=np.float32)
 
 
-def fixed_multiplier(m):
-    """(M0, T) with m ~= M0 2^-T for a real multiplier 0 <= m < 2^30.
-
-    A multiplier that rounds up to 2^30 itself is rejected as well.
-
-    m = f 2^e with f in [0.5, 1) (frexp); M0 = rint(f 2^31), T = 31 - e; a
-    rounding up to 2^31 is renormalised to M0 = 2^30, T - 1.  A multiplier
-    too small for T <= 62 (or zero) becomes (0, 1): the term vanishes.
-    """
-    m = float(m)
-    if not (m >= 0.0 and m < 2.0 ** 30):
-        raise ValueError("multiplier %r outside [0, 2^30)" % m)
-    if m == 0.0:
-        return 0, 1
-    f, e = math.frexp(m)
-    m0 = int(np.rint(f * 2.0 ** 31))
-    t = 31 - e
-    if m0 == 2 ** 31:
-        m0 = 2 ** 30
-        t -= 1
-    if t < 1:
-        raise ValueError("multiplier %r rounds to 2^30" % m)
-    if t > 62:
-        return 0, 1
-    return m0, t
+RESCALE_LIMIT = 2.0 ** 20
 
 
-def mulq(a, m0, t):
-    """a * m0 / 2^t rounded to nearest, ties away from zero (exact, int64).
+def multiplier(m):
+    """The float32 form of a real rescaling factor (finite, 0 < m < 2^20)."""
+    m32 = np.float32(float(m))
+    if not (np.isfinite(m32) and 0.0 < float(m32) < RESCALE_LIMIT):
+        raise ValueError("rescaling factor %r outside (0, 2^20)" % m)
+    return m32
 
-    ``a`` may be an array; |a| < 2^31, 0 <= m0 < 2^31 and 1 <= t <= 62, so
-    every intermediate fits in 64 bits.
-    """
-    a = np.asarray(a, dtype=np.int64)
-    prod = a * np.int64(m0)
-    mag = np.abs(prod)
-    r = (mag + (np.int64(1) << np.int64(t - 1))) >> np.int64(t)
-    return np.where(prod < 0, -r, r)
+
+def rescale(a, m):
+    """rint(fl32(fl32(a) * fl32(m))) as int64, saturated to +-2^20."""
+    t = np.rint(np.asarray(a, dtype=np.int64).astype(np.float32) * multiplier(m))
+    return np.clip(t, -RESCALE_LIMIT, RESCALE_LIMIT).astype(np.int64)
 
 
 def quantize(x, scale, zero_point):
@@ -175,12 +149,10 @@ def _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape):
         acc = acc + quantize_bias(b, s_x, s_w).reshape(axis_shape)
     v = np.empty_like(acc)
     for k in range(acc.shape[1]):
-        m0, t = fixed_multiplier((float(s_x) * s_w[k]) / float(s_y))
-        v[:, k] = mulq(acc[:, k], m0, t)
+        v[:, k] = rescale(acc[:, k], (float(s_x) * s_w[k]) / float(s_y))
     v = v + int(z_y)
     if res is not None:
-        m0, t = fixed_multiplier(float(qr[0]) / float(s_y))
-        v = v + mulq(np.asarray(res, dtype=np.int64) - int(qr[1]), m0, t)
+        v = v + rescale(np.asarray(res, dtype=np.int64) - int(qr[1]), float(qr[0]) / float(s_y))
     return _requant_out(v, act, s_y, z_y)
 
 
@@ -196,16 +168,13 @@ def qglobal_avg_pool2d(xq, qx, qy):
     xq = np.asarray(xq, dtype=np.int64)
     n, c, h, w = xq.shape
     tot = (xq - int(qx[1])).sum(axis=(2, 3))
-    m0, t = fixed_multiplier(float(qx[0]) / (float(qy[0]) * h * w))
-    return np.clip(int(qy[1]) + mulq(tot, m0, t), QMIN, QMAX)
+    return np.clip(int(qy[1]) + rescale(tot, float(qx[0]) / (float(qy[0]) * h * w)), QMIN, QMAX)
 
 
 def qadd(aq, qa, bq, qb, qy, act=None):
     """Quantized elementwise add with activation."""
-    ma, ta = fixed_multiplier(float(qa[0]) / float(qy[0]))
-    mb, tb = fixed_multiplier(float(qb[0]) / float(qy[0]))
-    v = (int(qy[1]) + mulq(np.asarray(aq, dtype=np.int64) - int(qa[1]), ma, ta)
-         + mulq(np.asarray(bq, dtype=np.int64) - int(qb[1]), mb, tb))
+    v = (int(qy[1]) + rescale(np.asarray(aq, dtype=np.int64) - int(qa[1]), float(qa[0]) / float(qy[0]))
+         + rescale(np.asarray(bq, dtype=np.int64) - int(qb[1]), float(qb[0]) / float(qy[0])))
     return _requant_out(v, act, qy[0], qy[1])
 
 

@@ -65,7 +65,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   // g, g + KG, ...), which multiplies the loads in flight and the MFMA issue
   // of a workgroup; the groups' sums are added in group order at the end.
   __shared__ uint4 ring[KG * NS * STAGE];
-  __shared__ float4 sbias[BN / 4];  // bias of the tile's channels
+  __shared__ float4 sbias[64];  // bias of the tile's channels (a whole wave's 16-byte fill)
   materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -410,7 +410,7 @@ hipError_t launch_tile(const ConvParams& p_in, hipStream_t s) {
 template <int BM, int BN, int WM, int WN, int KG>
 hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
   constexpr int kStage = (BM + BN) * 128 * KG;  // bytes of one ring slot, all groups
-  constexpr int kFixed = BN * 4;                 // the bias tile
+  constexpr int kFixed = 64 * 16;                // the bias table (one wave's fill)
   hipError_t r = hipErrorInvalidValue;
   static_for<1, kMaxStages + 1>([&](auto i) {
     constexpr int NS = decltype(i)::value;
@@ -424,7 +424,7 @@ hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
 
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
   if (stages < 1 || stages > kMaxStages || (kgroups != 1 && kgroups != 2)) return false;
-  if ((bm + bn) * 128 * stages * kgroups + bn * 4 > kLdsLimit) return false;  // LDS: stage rings + bias
+  if ((bm + bn) * 128 * stages * kgroups + 64 * 16 > kLdsLimit) return false;  // LDS: stage rings + bias
   const int waves = threads / (64 * kgroups);  // per reduction group
   if (threads != 64 * waves * kgroups) return false;
   if (waves == 4)

@@ -82,7 +82,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   __shared__ uint4 lds[NPB * PSTAGE + NSW * WSTAGE];
   uint4* const patch = lds;                 // NPB patch buffers
   uint4* const wring = lds + NPB * PSTAGE;  // NSW weight stages
-  __shared__ float4 sbias[BN / 4];
+  __shared__ float4 sbias[64];  // bias of the tile's channels (a whole wave's 16-byte fill)
   materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -333,7 +333,7 @@ constexpr int taps_per_stage(int stages) { return stages <= 3 ? 3 : 1; }
 
 // LDS bytes of one instantiation.
 constexpr int halo_lds(int bn, int tps, int nsw, int lp, int npb, int waves) {
-  return npb * lp * waves * 8 * 128 + nsw * tps * bn * 128 + bn * 4;
+  return npb * lp * waves * 8 * 128 + nsw * tps * bn * 128 + 64 * 16;  // + the bias table (one wave's fill)
 }
 
 // Patch pixels of the largest tile of a BM-pixel tiling.

@@ -18,9 +18,10 @@
 // the weight sums of its taps outside the image (wtap[k][r*S + s]).
 //
 // Epilogue: each thread finishes 8 consecutive channels of one pixel from
-// int32 sums staged in LDS: bias, border correction, fixed-point rescaling
-// (one rounding), the residual's own rescaling, the activation clamp in
-// code space and the int8 clip, one 8-byte store.
+// int32 sums staged in LDS: bias, border correction, float32 rescaling
+// (one rounding per term, the per-channel bias and factor read from LDS),
+// the residual's own rescaling, the activation clamp in code space (which
+// also clips to int8), one 8-byte store.
 #include "lds_dma.h"
 
 namespace byoc {
@@ -50,6 +51,7 @@ __global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
   static_assert(NS >= 2 && NS <= kMaxStages, "stages");
 
   __shared__ uint4 ring[NS * STAGE];
+  __shared__ int2 sq[128];  // the tile's {bias, factor} (one wave's 16-byte fill: 128 channels)
   materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -219,6 +221,13 @@ __global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
     }
   }
 
+  // per-channel bias and factor of the tile, straight into LDS; issued
+  // before the operand ring, so every later wait of this wave covers it
+  static_assert(BN <= 128, "channel table");
+  if (wave == 0) {
+    const i32x4 qr = buffer_rsrc(q.qch, ((p.Kp + 255) / 256) * 256 * 8);
+    lds_fill16(qr, __builtin_amdgcn_readfirstlane(lds_addr(sq)), 2 * lane < BN ? (uint32_t)(n0 + 2 * lane) * 8u : kOOB);
+  }
   static_assert((NS - 2) * LPS <= 63, "vmcnt immediate");
   auto round_step = [&](auto i) {
     constexpr int I = decltype(i)::value;
@@ -262,7 +271,7 @@ __global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
       const int* st = stage + px * kLd + ec8;
       const int4 lo4 = *(const int4*)st, hi4 = *(const int4*)(st + 4);
       int a[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
-      const int4* qc = reinterpret_cast<const int4*>(q.qch) + k;
+      const int2* qc = sq + pass * kEC + ec8;
 #pragma unroll
       for (int c8 = 0; c8 < 8; ++c8) a[c8] += qc[c8].x;
       if (q.wtap) {
@@ -292,15 +301,10 @@ __global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
       uint32_t out[2] = {0u, 0u};
 #pragma unroll
       for (int c8 = 0; c8 < 8; ++c8) {
-        const int4 qcv = qc[c8];
-        int64_t v = (int64_t)q.zy + mulq(a[c8], qcv.y, qcv.z);
-        if (p.res) {
-          const int rc = (int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3)));
-          v += mulq(rc - q.zr, q.mr, q.tr);
-        }
-        v = v < q.lo ? q.lo : v;
-        v = v > q.hi ? q.hi : v;
-        out[c8 >> 2] |= ((uint32_t)clip_i8(v) & 0xFFu) << (8 * (c8 & 3));
+        int v = q.zy + rescale(a[c8], __int_as_float(qc[c8].y));
+        if (p.res) v += rescale((int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3))) - q.zr, q.mr);
+        v = min(max(v, q.lo), q.hi);
+        out[c8 >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (c8 & 3));
       }
       *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) = make_uint2(out[0], out[1]);
     }

@@ -101,16 +101,14 @@ __device__ __forceinline__ int mdiv(int n, uint64_t mg) { return (int)(((uint64_
 // fence of __syncthreads() would wait for those to be acknowledged).
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// a * m0 / 2^t rounded to nearest, ties away from zero, exactly: |a| < 2^31,
-// 0 <= m0 < 2^31 and 1 <= t <= 62 keep every step inside 64 bits.
-__device__ __forceinline__ int64_t mulq(int a, int m0, int t) {
-  const int64_t prod = (int64_t)a * (int64_t)m0;
-  const int64_t mag = prod < 0 ? -prod : prod;
-  const int64_t r = (mag + ((int64_t)1 << (t - 1))) >> t;
-  return prod < 0 ? -r : r;
+// rint(fl32(fl32(a) * m)), ties to even, saturated to +-2^20 (the float32
+// rescaling of int8 graphs; a product followed by a rounding is never
+// contracted).
+__device__ __forceinline__ int rescale(int a, float m) {
+  return (int)__builtin_amdgcn_fmed3f(__builtin_rintf((float)a * m), -1048576.0f, 1048576.0f);
 }
 
-__device__ __forceinline__ int clip_i8(int64_t v) { return (int)(v < -128 ? -128 : (v > 127 ? 127 : v)); }
+__device__ __forceinline__ int clip_i8(int v) { return min(max(v, -128), 127); }
 
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 

@@ -38,32 +38,12 @@ struct PackJob {
   int n = 0, n_out = 0;
 };
 
-// Fixed-point form m0 2^-t of a real rescaling factor 0 <= m < 2^30 of an
-// int8 graph: m = f 2^e (f in [0.5, 1)), m0 = rint(f 2^31) (ties to even),
-// t = 31 - e, a rounding up to 2^31 renormalised to (2^30, t - 1); a factor
-// that needs t > 62 (or zero) becomes (0, 1).  False when out of range.
-bool fixed_multiplier(double m, int* m0, int* t) {
-  if (!(m >= 0.0 && m < 1073741824.0)) return false;
-  if (m == 0.0) {
-    *m0 = 0;
-    *t = 1;
-    return true;
-  }
-  int e = 0;
-  const double f = std::frexp(m, &e);
-  long long mm = (long long)std::nearbyint(f * 2147483648.0);
-  int tt = 31 - e;
-  if (mm == 2147483648LL) {
-    mm = 1073741824LL;
-    tt -= 1;
-  }
-  if (tt < 1) return false;
-  if (tt > 62) {
-    mm = 0;
-    tt = 1;
-  }
-  *m0 = (int)mm;
-  *t = tt;
+// float32 form of a real rescaling factor of an int8 graph (rounded from
+// float64); false unless finite, positive and below 2^20.
+bool rescale_factor(double m, float* out) {
+  const float f = (float)m;
+  if (!(std::isfinite(f) && f > 0.0f && f < 1048576.0f)) return false;
+  *out = f;
   return true;
 }
 
@@ -841,8 +821,7 @@ void Planner::plan_node_i8(int ni) {
     const int RS = R * S;
     const bool border = !dense && xv.qzero != 0 && (n.pad[0] | n.pad[1] | n.pad[2] | n.pad[3]) != 0;
     std::vector<uint8_t> packed((size_t)rows * p.Kgp, 0);
-    std::vector<int32_t> qch((size_t)rows * 4, 0), wtap(border ? (size_t)rows * RS : 0, 0);
-    for (int k = K; k < rows; ++k) qch[(size_t)k * 4 + 2] = 1;
+    std::vector<int32_t> qch((size_t)rows * 2, 0), wtap(border ? (size_t)rows * RS : 0, 0);
     const double sx = xv.qscale, sy = yv.qscale;
     for (int k = 0; k < K; ++k) {
       const int64_t base = (int64_t)k * Cg * RS;
@@ -868,12 +847,11 @@ void Planner::plan_node_i8(int ni) {
       const int64_t beff = (int64_t)bq - (int64_t)xv.qzero * total;
       if (beff <= -(int64_t(1) << 30) || beff >= (int64_t(1) << 30))
         return fail("quantized bias of channel " + std::to_string(k) + " outside +-2^30");
-      int m0 = 0, t = 1;
-      if (!fixed_multiplier((sx * sw) / sy, &m0, &t))
-        return fail("rescaling factor of channel " + std::to_string(k) + " outside [0, 2^30)");
-      qch[(size_t)k * 4 + 0] = (int32_t)beff;
-      qch[(size_t)k * 4 + 1] = m0;
-      qch[(size_t)k * 4 + 2] = t;
+      float mk = 0.f;
+      if (!rescale_factor((sx * sw) / sy, &mk))
+        return fail("rescaling factor of channel " + std::to_string(k) + " outside (0, 2^20)");
+      qch[(size_t)k * 2 + 0] = (int32_t)beff;
+      std::memcpy(&qch[(size_t)k * 2 + 1], &mk, 4);
     }
     L.w = host_blob(std::move(packed));
     std::vector<uint8_t> qb(qch.size() * 4);
@@ -892,7 +870,7 @@ void Planner::plan_node_i8(int ni) {
       const Value& rv = g.values[n.residual];
       L.res = loc[n.residual];
       q.zr = rv.qzero;
-      if (!fixed_multiplier(rv.qscale / sy, &q.mr, &q.tr)) return fail("residual rescaling factor outside [0, 2^30)");
+      if (!rescale_factor(rv.qscale / sy, &q.mr)) return fail("residual rescaling factor outside (0, 2^20)");
     }
     // tile: the largest with at least two workgroups per CU
     auto tiles = [&](int bm, int bn) { return ((int64_t)p.M + bm - 1) / bm * ((Kp + bn - 1) / bn); };
@@ -937,8 +915,8 @@ void Planner::plan_node_i8(int ni) {
       L.info.kind = BYOC_K_AVGPOOL;
       L.qzx = xv.qzero;
       L.qzy = yv.qzero;
-      if (!fixed_multiplier(xv.qscale / (yv.qscale * p.H * p.W), &L.qm0, &L.qt))
-        return fail("rescaling factor outside [0, 2^30)");
+      if (!rescale_factor(xv.qscale / (yv.qscale * p.H * p.W), &L.qm))
+        return fail("rescaling factor outside (0, 2^20)");
       name(L, "avgpool_nhwc_i8");
     }
     e->launches.push_back(L);
@@ -953,8 +931,8 @@ void Planner::plan_node_i8(int ni) {
   a.zy = yv.qzero;
   a.lo = lo;
   a.hi = hi;
-  if (!fixed_multiplier(xv.qscale / yv.qscale, &a.ma, &a.ta) || !fixed_multiplier(bv.qscale / yv.qscale, &a.mb, &a.tb))
-    return fail("rescaling factor outside [0, 2^30)");
+  if (!rescale_factor(xv.qscale / yv.qscale, &a.ma) || !rescale_factor(bv.qscale / yv.qscale, &a.mb))
+    return fail("rescaling factor outside (0, 2^20)");
   L.op = Launch::AddI8;
   L.info.kind = BYOC_K_ADD;
   L.other = loc[n.other];
@@ -1135,7 +1113,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.x = c.ptr(L.x);
       p.y = c.ptr(L.y);
       if (L.op == Launch::MaxPoolI8) return launch_maxpool_nhwc_i8(p, c.s);
-      return launch_avgpool_nhwc_i8(p, L.qzx, L.qzy, L.qm0, L.qt, c.s);
+      return launch_avgpool_nhwc_i8(p, L.qzx, L.qzy, L.qm, c.s);
     }
     case Launch::AddI8: {
       QAddParams a = L.qa;
@@ -1385,8 +1363,30 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
   return c;
 }
 
+// int8 convs: every tile and ring depth (the integer sums, hence the
+// codes, do not depend on the tiling)
+std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
+  std::vector<ConvTile> c{L.tile_default};
+  for (auto bmn : {std::pair<int, int>{128, 128}, {128, 64}, {64, 64}, {32, 64}})
+    for (int ns : {2, 3, 4}) {
+      ConvTile t = ConvTile{};
+      t.bm = bmn.first;
+      t.bn = bmn.second;
+      t.stages = ns;
+      if (!conv_i8_tile_supported(t.bm, t.bn, t.stages)) continue;
+      if (t.bm == L.tile_default.bm && t.bn == L.tile_default.bn && t.stages == L.tile_default.stages) continue;
+      c.push_back(t);
+    }
+  return c;
+}
+
 void apply_tile(Launch& L, const ConvTile& t) {
   L.tile = t;
+  if (L.op == Launch::ConvI8) {
+    L.qc.g.xcd_py = choose_xcd_split(L.qc.g, t);
+    name_conv_i8(L);
+    return;
+  }
   L.conv.xcd_py = t.stages > 0 ? choose_xcd_split(L.conv, t) : 0;
   name_conv(L);
 }
@@ -1431,8 +1431,9 @@ Status autotune(Engine* e) {
   std::vector<std::vector<ConvTile>> cand(nl);
   size_t rounds = 1;
   for (size_t i = 0; i < nl; ++i)
-    if (e->launches[i].op == Launch::ConvMfma) {
-      cand[i] = conv_candidates(e->launches[i]);
+    if (e->launches[i].op == Launch::ConvMfma || e->launches[i].op == Launch::ConvI8) {
+      cand[i] = e->launches[i].op == Launch::ConvI8 ? conv_i8_candidates(e->launches[i])
+                                                      : conv_candidates(e->launches[i]);
       rounds = std::max(rounds, cand[i].size());
     }
   std::vector<float> best_ms(nl, 0.f);
@@ -1470,7 +1471,7 @@ Status autotune(Engine* e) {
   if (err == hipSuccess) err = serr;
   if (err != hipSuccess) {
     for (Launch& L : e->launches)
-      if (L.op == Launch::ConvMfma) apply_tile(L, L.tile_default);
+      if (L.op == Launch::ConvMfma || L.op == Launch::ConvI8) apply_tile(L, L.tile_default);
     return Status::Err(BYOC_ERR_DEVICE, std::string("autotune: ") + hipGetErrorString(err));
   }
   return Status::Ok();
@@ -1491,7 +1492,7 @@ Status engine_set_options(Engine* e, int flags) {
   }
   if (tune_off)
     for (Launch& L : e->launches)
-      if (L.op == Launch::ConvMfma) apply_tile(L, L.tile_default);
+      if (L.op == Launch::ConvMfma || L.op == Launch::ConvI8) apply_tile(L, L.tile_default);
   e->options = flags;
   return Status::Ok();
 }

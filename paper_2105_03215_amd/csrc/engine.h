@@ -40,7 +40,8 @@ struct Launch {
   QAddParams qa{};   // int8 add
   float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
   int qzero = 0;                 // quantize / dequantize zero point
-  int qzx = 0, qzy = 0, qm0 = 0, qt = 1;  // int8 average pool
+  int qzx = 0, qzy = 0;          // int8 average pool: zero points
+  float qm = 0.f;                //   and rescaling factor
   int64_t n = 0;
   int act = 0;
   bool src_bf16 = false, dst_bf16 = false;

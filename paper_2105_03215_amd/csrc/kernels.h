@@ -164,17 +164,18 @@ hipError_t launch_cast(const void* x, bool src_bf16, void* y, bool dst_bf16, int
 // ---- int8 (partial quantization) ------------------------------------------
 // Codes are int8 with an affine (scale, zero point) per activation tensor;
 // weights are symmetric per output channel.  A real rescaling factor m is
-// applied in fixed point as round(a * m0 / 2^t), ties away from zero, with
-// m0 in [2^30, 2^31) and 1 <= t <= 62 (m0 = 0: the term vanishes).
-// Activations are NHWC with Cp a multiple of 16; conv weights packed
-// [rows >= Kp][Kgp] int8 with kk = (r*S + s)*Cp + c, Kgp a multiple of 128.
+// applied in float32: rint(fl32(fl32(a) * m)), ties to even, saturated to
+// +-2^20.  Activations are NHWC with Cp a multiple of 16; conv weights
+// packed [rows >= Kp][Kgp] int8 with kk = (r*S + s)*Cp + c, Kgp a multiple
+// of 128.
 struct QConvParams {
   ConvParams g;         // geometry and operands: x, w, res, y hold int8 data; bias, partial unused
-  const int32_t* qch;   // [>= Kp][4]: bias with the input zero point folded in, m0, t, 0
+  const int32_t* qch;   // [>= Kp][2]: bias with the input zero point folded in, float32 factor bits
   const int32_t* wtap;  // [>= Kp][R*S] weight sums per tap (border correction), or nullptr
   int zx;               // input zero point (applied at the border through wtap)
-  int zy, lo, hi;       // output zero point; activation clamp in output codes
-  int zr, mr, tr;       // residual zero point and rescaling (m0, t)
+  int zy, lo, hi;       // output zero point; activation clamp in output codes (within [-128, 127])
+  int zr;               // residual zero point
+  float mr;             // residual rescaling factor
 };
 bool conv_i8_tile_supported(int bm, int bn, int stages);
 hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, hipStream_t s);
@@ -189,15 +190,17 @@ hipError_t launch_dequantize_i8(const int8_t* x, void* y, bool dst_bf16, int N, 
                                 float scale, int zp, hipStream_t s);
 // Max pooling of codes, NHWC (padding never wins).
 hipError_t launch_maxpool_nhwc_i8(const PoolParams& p, hipStream_t s);
-// Global average pooling of codes: y[n][c] = clip(zy + mulq(sum(x - zx), m0, t)), y [N][Cp].
-hipError_t launch_avgpool_nhwc_i8(const PoolParams& p, int zx, int zy, int m0, int t, hipStream_t s);
-// y = clip(clamp(zy + mulq(a - za, ma, ta) + mulq(b - zb, mb, tb), lo, hi)) over n codes.
+// Global average pooling of codes: y[n][c] = clip(zy + rescale(sum(x - zx), m)), y [N][Cp].
+hipError_t launch_avgpool_nhwc_i8(const PoolParams& p, int zx, int zy, float m, hipStream_t s);
+// y = clamp(zy + rescale(a - za, ma) + rescale(b - zb, mb), lo, hi) over n codes
+// ([lo, hi] within [-128, 127]).
 struct QAddParams {
   const int8_t* a;
   const int8_t* b;
   int8_t* y;
   int64_t n;
-  int za, ma, ta, zb, mb, tb, zy, lo, hi;
+  int za, zb, zy, lo, hi;
+  float ma, mb;
 };
 hipError_t launch_add_i8(const QAddParams& p, hipStream_t s);
 

@@ -38,7 +38,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const void* x, int s
       if (c < C) {
         float t = rintf(load_f(x, src_bf16, ((int64_t)n * C + c) * HW + hw) * inv);
         t = fminf(fmaxf(t, -512.0f), 512.0f);
-        code = clip_i8((int64_t)t + zp);
+        code = clip_i8((int)t + zp);
       }
       w4[j >> 2] |= ((uint32_t)code & 0xFFu) << (8 * (j & 3));
     }
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(kThreads) void maxpool_i8_kernel(PoolParams p) {
 }
 
 // One thread per (n, channel): the integer sum over the image is exact.
-__global__ __launch_bounds__(kThreads) void avgpool_i8_kernel(PoolParams p, int zx, int zy, int m0, int t) {
+__global__ __launch_bounds__(kThreads) void avgpool_i8_kernel(PoolParams p, int zx, int zy, float m) {
   const int64_t total = (int64_t)p.N * p.Cp;
   const int HW = p.H * p.W;
   const int8_t* x = reinterpret_cast<const int8_t*>(p.x);
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void avgpool_i8_kernel(PoolParams p, int 
     const int8_t* src = x + (int64_t)n * HW * p.Cp + c;
     int sum = 0;
     for (int j = 0; j < HW; ++j) sum += (int)src[(int64_t)j * p.Cp] - zx;
-    y[i] = (int8_t)clip_i8((int64_t)zy + mulq(sum, m0, t));
+    y[i] = (int8_t)clip_i8(zy + rescale(sum, m));
   }
 }
 
@@ -124,10 +124,8 @@ __global__ __launch_bounds__(kThreads) void add_i8_kernel(QAddParams p) {
     for (int j = 0; j < 16; ++j) {
       const int a = (int)(int8_t)(wa[j >> 2] >> (8 * (j & 3)));
       const int b = (int)(int8_t)(wb[j >> 2] >> (8 * (j & 3)));
-      int64_t v = (int64_t)p.zy + mulq(a - p.za, p.ma, p.ta) + mulq(b - p.zb, p.mb, p.tb);
-      v = v < p.lo ? p.lo : v;
-      v = v > p.hi ? p.hi : v;
-      o[j >> 2] |= ((uint32_t)clip_i8(v) & 0xFFu) << (8 * (j & 3));
+      const int v = min(max(p.zy + rescale(a - p.za, p.ma) + rescale(b - p.zb, p.mb), p.lo), p.hi);
+      o[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
     }
     *(uint4*)(p.y + i * 16) = make_uint4(o[0], o[1], o[2], o[3]);
   }
@@ -157,8 +155,8 @@ hipError_t launch_maxpool_nhwc_i8(const PoolParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_avgpool_nhwc_i8(const PoolParams& p, int zx, int zy, int m0, int t, hipStream_t s) {
-  avgpool_i8_kernel<<<grid_for((int64_t)p.N * p.Cp), kThreads, 0, s>>>(p, zx, zy, m0, t);
+hipError_t launch_avgpool_nhwc_i8(const PoolParams& p, int zx, int zy, float m, hipStream_t s) {
+  avgpool_i8_kernel<<<grid_for((int64_t)p.N * p.Cp), kThreads, 0, s>>>(p, zx, zy, m);
   return hipGetLastError();
 }
 

@@ -1,7 +1,8 @@
 """Pins of the int8 oracle (partial quantization, Sec. 3.2 / Fig. 4a).
 
 Each test checks a definition of ``oracle.quant`` against something other
-than itself: exact rational arithmetic (fractions), round trips of every
+than itself: exact rational arithmetic (fractions) and an error bound for
+the float32 rescaling, round trips of every
 code, brute-force integer loops on tiny shapes, and the float64 operator
 definitions in the cases where quantization is exact (dyadic scales and
 weights that are integer multiples of their scale, so every multiplier is a
@@ -20,43 +21,44 @@ from oracle import brute, ops
 from oracle import quant as Q
 
 
-def _round_half_away(fr):
-    """Fraction -> nearest integer, ties away from zero."""
-    mag = abs(fr)
-    r = int(mag + Fraction(1, 2))  # floor for non-negative values
-    return -r if fr < 0 else r
+def _round_half_even(fr):
+    """Fraction -> nearest integer, ties to even."""
+    f = fr.numerator // fr.denominator  # floor
+    rem = fr - f
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and f % 2 == 1):
+        f += 1
+    return f
 
 
-def test_mulq_matches_exact_rationals():
+def test_rescale_is_exact_for_power_of_two_factors():
+    """With m = 2^-j and |a| < 2^24 the float32 product is exact, so the
+    result is a * m rounded to nearest, ties to even (exact rationals)."""
     rng = np.random.default_rng(0)
     for _ in range(3000):
-        a = int(rng.integers(-(2 ** 31) + 1, 2 ** 31))
-        m0 = int(rng.integers(2 ** 30, 2 ** 31))
-        t = int(rng.integers(1, 63))
-        want = _round_half_away(Fraction(a * m0, 2 ** t))
-        assert int(Q.mulq(a, m0, t)) == want, (a, m0, t)
-    # ties go away from zero
-    assert int(Q.mulq(3, 2 ** 30, 31)) == 2   # 1.5 -> 2
-    assert int(Q.mulq(-3, 2 ** 30, 31)) == -2  # -1.5 -> -2
-    assert int(Q.mulq(5, 2 ** 30, 32)) == 1   # 1.25 -> 1
-    assert int(Q.mulq(-7, 2 ** 30, 32)) == -2  # -1.75 -> -2
+        a = int(rng.integers(-(2 ** 24) + 1, 2 ** 24))
+        j = int(rng.integers(0, 40))
+        want = _round_half_even(Fraction(a, 2 ** j))
+        want = max(-(2 ** 20), min(2 ** 20, want))
+        assert int(Q.rescale(a, 2.0 ** -j)) == want, (a, j)
+    assert int(Q.rescale(3, 0.5)) == 2 and int(Q.rescale(5, 0.5)) == 2  # ties to even
+    assert int(Q.rescale(-3, 0.5)) == -2 and int(Q.rescale(-1, 0.5)) == 0
 
 
-def test_fixed_multiplier_is_the_nearest_representation():
+def test_rescale_error_bound():
+    """For any factor the result is within half a unit plus the float32
+    rounding of a and of the product (2^-23 relative each) of a * m."""
     rng = np.random.default_rng(1)
-    for m in np.concatenate([10.0 ** rng.uniform(-9, 9, 500), [0.5, 1.0, 2.0 ** -20, 1 - 2.0 ** -40]]):
-        m0, t = Q.fixed_multiplier(m)
-        assert 2 ** 30 <= m0 < 2 ** 31 and 1 <= t <= 62
-        err = abs(Fraction(m0, 2 ** t) - Fraction(float(m)))
-        assert err <= Fraction(1, 2 ** (t + 1)), m
-    assert Q.fixed_multiplier(2.0 ** -10) == (2 ** 30, 40)
-    assert Q.fixed_multiplier(1 - 2.0 ** -40) == (2 ** 30, 30)  # rounds up to 2^31: renormalised
-    assert Q.fixed_multiplier(0.0) == (0, 1)
-    assert Q.fixed_multiplier(2.0 ** -40) == (0, 1)  # would need T > 62
+    a = rng.integers(-(2 ** 31) + 1, 2 ** 31, size=5000)
+    m = 10.0 ** rng.uniform(-9, 0, size=5000)
+    for ai, mi in zip(a, m):
+        exact = int(ai) * float(np.float32(mi))
+        got = int(Q.rescale(int(ai), mi))
+        assert abs(got - max(-2.0 ** 20, min(2.0 ** 20, exact))) <= 0.5 + abs(exact) * 2.0 ** -22 + 1e-9
     with pytest.raises(ValueError):
-        Q.fixed_multiplier(2.0 ** 30)
+        Q.multiplier(2.0 ** 20)
     with pytest.raises(ValueError):
-        Q.fixed_multiplier(2.0 ** 30 - 2.0 ** -30)  # rounds to 2^30
+        Q.multiplier(0.0)
+    assert int(Q.rescale(2 ** 30, 0.5)) == 2 ** 20  # saturation
 
 
 @pytest.mark.parametrize("scale,zp", [(0.02, 0), (0.0371, -128), (1.7, 45), (2.0 ** -6, 127)])
@@ -142,8 +144,8 @@ def test_quantized_conv_equals_rounded_float_conv(zx, zy, act, residual):
     yf = ops.bias_add(ops.conv2d(sx * (xq - zx), w, (2, 2), (1, 1, 1, 1)), b)
     if residual:
         yf = yf + sy * (rq - 13)
-    t = yf / sy  # exact: dyadic values far below 2^53
-    want = zy + np.sign(t) * np.floor(np.abs(t) + 0.5)
+    t = yf / sy  # exact: dyadic values far below 2^24 (float32 products exact)
+    want = zy + np.rint(t)
     lo, hi = Q.act_bounds(act, sy, zy)
     want = np.clip(np.clip(want, lo, hi), -128, 127)
     assert np.array_equal(got, want.astype(np.int64))
@@ -158,7 +160,7 @@ def test_quantized_dense_equals_rounded_float_dense():
     b = rng.integers(-500, 500, size=6) * (sx * sw)
     got = Q.qdense(xq, (sx, zx), j * sw, b, (sy, zy), "relu")
     t = ops.bias_add(ops.dense(sx * (xq - zx), j * sw), b) / sy
-    want = np.clip(np.maximum(zy + np.sign(t) * np.floor(np.abs(t) + 0.5), zy), -128, 127)
+    want = np.clip(np.maximum(zy + np.rint(t), zy), -128, 127)
     assert np.array_equal(got, want.astype(np.int64))
 
 
@@ -179,7 +181,7 @@ def test_global_avg_pool_rounds_the_mean():
     xq = rng.integers(-128, 128, size=(3, 5, 4, 4))
     s, zx, zy = 0.1, 17, -3
     got = Q.qglobal_avg_pool2d(xq, (s, zx), (s, zy))  # multiplier 1/16: exact
-    want = [[zy + _round_half_away(Fraction(int((xq[n, c] - zx).sum()), 16)) for c in range(5)]
+    want = [[zy + _round_half_even(Fraction(int((xq[n, c] - zx).sum()), 16)) for c in range(5)]
             for n in range(3)]
     assert np.array_equal(got, np.clip(np.array(want), -128, 127))
 
