@@ -11,8 +11,9 @@ traffic  HBM bytes of the conv kernels per run from two counter runs
          known size (``bench.py --copy-calibration MIB`` under the same
          counter), over the last N runs -> JSON read by bench.py.
 
-A run of the ResNet subgraph starts with its fused stem kernel, the marker
-used to split the dispatch stream into runs.
+A run of the ResNet subgraph starts with its fused stem kernel (of its int8
+form: the boundary quantize kernel), the marker used to split the dispatch
+stream into runs.
 
 Usage:
   python -m paper_2105_03215_amd.profiling stats --trace X_kernel_trace.csv \
@@ -39,8 +40,8 @@ def _short(name):
     return name.replace("byoc::(anonymous namespace)::", "").replace("void ", "")
 
 
-def _is_conv(name):
-    return any(k in name for k in CONV_KERNELS)
+def _is_conv(name, kernels=CONV_KERNELS):
+    return any(k in name for k in kernels)
 
 
 def _last_runs(rows, name_key, last_runs, marker=RUN_MARKER):
@@ -51,17 +52,18 @@ def _last_runs(rows, name_key, last_runs, marker=RUN_MARKER):
     return rows[starts[-last_runs]:], last_runs
 
 
-def stats(trace_path, cmd, out, last_runs, flops_per_run=0.0, top=25):
+def stats(trace_path, cmd, out, last_runs, flops_per_run=0.0, top=25, marker=RUN_MARKER,
+          kernels=CONV_KERNELS, class_name="conv/dense MFMA class", unit="FLOP"):
     rows = sorted(csv.DictReader(open(trace_path)), key=lambda r: int(r["Start_Timestamp"]))
-    rows, runs = _last_runs(rows, "Kernel_Name", last_runs)
+    rows, runs = _last_runs(rows, "Kernel_Name", last_runs, marker)
     per = {}
     for r in rows:
         d = per.setdefault(r["Kernel_Name"], [0, 0])
         d[0] += 1
         d[1] += int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
     total = sum(v[1] for v in per.values())
-    conv_ns = sum(v[1] for k, v in per.items() if _is_conv(k))
-    conv_calls = sum(v[0] for k, v in per.items() if _is_conv(k))
+    conv_ns = sum(v[1] for k, v in per.items() if _is_conv(k, kernels))
+    conv_calls = sum(v[0] for k, v in per.items() if _is_conv(k, kernels))
     lines = ["# rocprofv3 kernel statistics (last %d runs of the subgraph, after autotune)" % runs,
              "# command: " + cmd,
              "# %-70s %9s %10s %12s %6s" % ("kernel", "calls/run", "avg_us", "us/run", "pct")]
@@ -69,11 +71,11 @@ def stats(trace_path, cmd, out, last_runs, flops_per_run=0.0, top=25):
         lines.append("  %-70s %9.2f %10.2f %12.2f %6.2f" % (
             _short(k)[:70], calls / runs, ns / calls / 1e3, ns / runs / 1e3, 100.0 * ns / total))
     lines.append("# all kernels: %.1f us per run" % (total / runs / 1e3))
-    lines.append("# conv/dense MFMA class (%s): %.1f launches, %.1f us per run, avg %.2f us per launch" % (
-        ", ".join(CONV_KERNELS), conv_calls / runs, conv_ns / runs / 1e3, conv_ns / max(conv_calls, 1) / 1e3))
+    lines.append("# %s (%s): %.1f launches, %.1f us per run, avg %.2f us per launch" % (
+        class_name, ", ".join(kernels), conv_calls / runs, conv_ns / runs / 1e3, conv_ns / max(conv_calls, 1) / 1e3))
     if flops_per_run:
-        lines.append("# conv/dense class: %.1f GFLOP per run -> %.1f TFLOP/s of pure kernel time" % (
-            flops_per_run / 1e9, flops_per_run / (conv_ns / runs * 1e-9) / 1e12))
+        lines.append("# %s: %.1f G%s per run -> %.1f T%s/s of pure kernel time" % (
+            class_name, flops_per_run / 1e9, unit, flops_per_run / (conv_ns / runs * 1e-9) / 1e12, unit))
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     return out
@@ -138,6 +140,10 @@ def main():
     a.add_argument("--out", required=True)
     a.add_argument("--last-runs", type=int, required=True)
     a.add_argument("--flops-per-run", type=float, default=0.0)
+    a.add_argument("--marker", default=RUN_MARKER, help="kernel launched once per run of the subgraph")
+    a.add_argument("--kernels", default=",".join(CONV_KERNELS), help="kernels of the summed class")
+    a.add_argument("--class-name", default="conv/dense MFMA class")
+    a.add_argument("--unit", default="FLOP", help="FLOP, or OP for integer work")
     b = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy-fetch", "copy-write", "workload", "out"):
         b.add_argument("--" + k, required=True)
@@ -145,7 +151,8 @@ def main():
     b.add_argument("--last-runs", type=int, required=True)
     args = ap.parse_args()
     if args.cmd_name == "stats":
-        print(stats(args.trace, args.cmd, args.out, args.last_runs, args.flops_per_run))
+        print(stats(args.trace, args.cmd, args.out, args.last_runs, args.flops_per_run, marker=args.marker,
+                    kernels=tuple(args.kernels.split(",")), class_name=args.class_name, unit=args.unit))
     else:
         print(json.dumps(traffic(args.fetch, args.write, args.copy_fetch, args.copy_write,
                                  args.copy_mib, args.workload, args.out, args.last_runs)))
