@@ -14,9 +14,10 @@ residual add comes before the activation, as in a ResNet block):
 
     y = op(x, w);  y = bias_add(y, b);  y = add(y, residual);  y = act(y)
 
-Pattern names: ``conv2d[_bias][_add][_relu|_relu6|_gelu]``,
-``dense[_bias][_add][_relu|_relu6|_gelu]``, ``max_pool2d``,
-``global_avg_pool2d``, ``add[_relu|_relu6]``.  Inputs of a node are listed in
+Pattern names: ``conv2d[_bias][_add][_relu|_relu6|_gelu|_leaky]``,
+``dense[_bias][_add][_relu|_relu6|_gelu|_leaky]``, ``max_pool2d``,
+``global_avg_pool2d``, ``add[_relu|_relu6|_leaky]``; a leaky ReLU takes its
+slope from ``attrs.alpha`` (default 0.1).  Inputs of a node are listed in
 the order data, weight, bias, residual.
 
 Precision semantics.  A node whose ``out_dtype`` is "bf16" belongs to a bf16
@@ -39,7 +40,7 @@ import numpy as np
 from . import ops
 from .bf16 import round_bf16
 
-_ACTS = ("relu6", "relu", "gelu")
+_ACTS = ("relu6", "relu", "gelu", "leaky")
 
 
 def load_graph(js):
@@ -124,7 +125,10 @@ def run_node(node, args, mode="bf16io"):
     else:
         y = ops.global_avg_pool2d(args[0])
     if act is not None:
-        y = ops.ACTIVATIONS[act](y)
+        if act == "leaky":
+            y = ops.leaky_relu(y, float(attrs.get("alpha", 0.1)))
+        else:
+            y = ops.ACTIVATIONS[act](y)
     return _store(y, dtype, mode)
 
 

@@ -106,7 +106,13 @@ def gelu(y):
     return y * 0.5 * (1.0 + erf(y / np.sqrt(2.0)))
 
 
-ACTIVATIONS = {"relu": relu, "relu6": relu6, "gelu": gelu}
+def leaky_relu(y, alpha=0.1):
+    """y for y >= 0, alpha * y below (0 <= alpha < 1)."""
+    y = _f64(y)
+    return np.where(y >= 0.0, y, float(alpha) * y)
+
+
+ACTIVATIONS = {"relu": relu, "relu6": relu6, "gelu": gelu, "leaky": leaky_relu}
 
 
 def max_pool2d(x, pool_size=(3, 3), strides=(2, 2), padding=(1, 1, 1, 1)):

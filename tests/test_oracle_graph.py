@@ -128,3 +128,20 @@ def test_fp32_graph_is_not_rounded():
     wl = workloads.conv_f32(n=1, c=4, hw=6, k=3)
     out = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
     assert not np.array_equal(round_bf16(out), out)
+
+
+def test_leaky_node_takes_its_slope_from_attrs():
+    """A conv2d_bias_leaky node against brute-force loops: the composite's
+    pre-activation where it is >= 0, alpha times it below, with alpha read
+    from the node's attrs (default 0.1)."""
+    rng = np.random.default_rng(21)
+    x = rng.normal(size=(1, 2, 5, 4))
+    w = rng.normal(size=(3, 2, 3, 3))
+    b = rng.normal(size=3)
+    pre = np.array(brute.conv2d(x.tolist(), w.tolist(), (1, 1), (1, 1, 1, 1))) + b.reshape(1, 3, 1, 1)
+    for attrs, a in (({"padding": [1, 1, 1, 1], "alpha": 0.3}, 0.3), ({"padding": [1, 1, 1, 1]}, 0.1)):
+        node = {"name": "y", "composite": "conv2d_bias_leaky", "inputs": ["x", "w", "b"], "attrs": attrs,
+                "out_dtype": "f32"}
+        y = graph.run_node(node, [x, w, b], mode="exact")
+        np.testing.assert_allclose(y, np.where(pre >= 0, pre, a * pre), rtol=1e-12, atol=1e-12)
+        assert (pre < 0).any()

@@ -160,6 +160,17 @@ def test_relu_family_invariants():
     assert np.array_equal(r6[inside], x[inside])
 
 
+def test_leaky_relu_piecewise_and_closed_forms():
+    x = _rand(1000) * 5
+    for a in (0.1, 0.0, 0.25):
+        y = ops.leaky_relu(x, a)
+        ref = np.array([v if v >= 0 else a * v for v in x])  # the scalar definition
+        assert np.array_equal(y, ref)
+        # relu(x) - a relu(-x) is the same function
+        np.testing.assert_allclose(y, ops.relu(x) - a * ops.relu(-x), rtol=0, atol=1e-15)
+    assert np.array_equal(ops.leaky_relu(x, 0.0), ops.relu(x))
+
+
 def test_gelu_against_math_erf_and_odd_part():
     x = np.linspace(-8, 8, 2001)
     g = ops.gelu(x)
