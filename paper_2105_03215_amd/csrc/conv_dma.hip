@@ -335,7 +335,7 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
   float* stage = reinterpret_cast<float*>(gring);
-  const ActClamp ac = act_clamp_of(p.act);
+  const ActClamp ac = act_clamp_of(p.act, p.alpha);
   auto epilogue = [&](auto gelu_tag) {
     constexpr bool G = decltype(gelu_tag)::value;
 #pragma unroll

@@ -40,7 +40,7 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(ConvF32Params p) {
   }
   if (p.bias) acc += p.bias[k];
   if (p.res) acc += p.res[idx];
-  p.y[idx] = apply_act(acc, p.act);
+  p.y[idx] = apply_act(acc, p.act, p.alpha);
 }
 
 }  // namespace

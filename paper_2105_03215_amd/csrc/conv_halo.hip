@@ -283,7 +283,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= (NPB * PSTAGE + NSW * WSTAGE) * 16, "staging tile");
   float* stage = reinterpret_cast<float*>(lds);
-  const ActClamp ac = act_clamp_of(p.act);
+  const ActClamp ac = act_clamp_of(p.act, p.alpha);
   auto epilogue = [&](auto gelu_tag) {
     constexpr bool G = decltype(gelu_tag)::value;
 #pragma unroll

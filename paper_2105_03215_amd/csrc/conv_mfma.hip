@@ -361,7 +361,7 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   constexpr int kLd = kEC + 4;  // padded row (floats): 16 rows hit distinct banks
   static_assert(BN % kEC == 0 && BM * kLd * 4 <= (int)sizeof(smem), "staging tile");
   float* stage = reinterpret_cast<float*>(smem);
-  const ActClamp ac = act_clamp_of(p.act);
+  const ActClamp ac = act_clamp_of(p.act, p.alpha);
   auto epilogue = [&](auto gelu_tag) {
     constexpr bool G = decltype(gelu_tag)::value;
 #pragma unroll
@@ -437,8 +437,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
     acc.w += __uint_as_float(rr.y & 0xFFFF0000u);
   }
   *(uint2*)(p.y + (size_t)m * p.ldy + k) =
-      make_uint2(pack2_bf16(apply_act(acc.x, p.act), apply_act(acc.y, p.act)),
-                 pack2_bf16(apply_act(acc.z, p.act), apply_act(acc.w, p.act)));
+      make_uint2(pack2_bf16(apply_act(acc.x, p.act, p.alpha), apply_act(acc.y, p.act, p.alpha)),
+                 pack2_bf16(apply_act(acc.z, p.act, p.alpha), apply_act(acc.w, p.act, p.alpha)));
 }
 
 template <int BM, int BN, int WM, int WN, int MF>

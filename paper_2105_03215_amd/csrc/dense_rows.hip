@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void dense_rows_kernel(ConvParams p) {
     v[0] += bf16_to_f32((bf16_t)(r.x & 0xFFFF)), v[1] += bf16_to_f32((bf16_t)(r.x >> 16));
     v[2] += bf16_to_f32((bf16_t)(r.y & 0xFFFF)), v[3] += bf16_to_f32((bf16_t)(r.y >> 16));
   }
-  const ActClamp ac = act_clamp_of(p.act);
+  const ActClamp ac = act_clamp_of(p.act, p.alpha);
   if (p.act == kActGelu) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = act_apply<true>(v[e], ac);

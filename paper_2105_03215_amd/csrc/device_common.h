@@ -39,24 +39,28 @@ __device__ __attribute__((noinline)) float gelu(float v) { return 0.5f * v * erf
 
 // Epilogue activation.  Kernels pick the GELU or the clamp instantiation
 // once (the choice is uniform), so the per-element code has no branch:
-// none / ReLU / ReLU6 are one median-of-three clamp to [lo, hi] (none:
-// [-inf, +inf], the value itself), GELU the out-of-line call above.
+// none / ReLU / ReLU6 / leaky ReLU are med3(max(v, slope * v), lo, hi) —
+// slope 1 makes the max the value itself, slope alpha < 1 the leaky ReLU,
+// [lo, hi] the clamps (none: [-inf, +inf]) — and GELU the out-of-line call
+// above.
 struct ActClamp {
-  float lo;  // 0, or -inf for no activation
-  float hi;  // 6 for ReLU6, +inf otherwise
+  float lo;     // 0 for ReLU / ReLU6, -inf otherwise
+  float hi;     // 6 for ReLU6, +inf otherwise
+  float slope;  // alpha for the leaky ReLU, 1 otherwise
 };
-__device__ __forceinline__ ActClamp act_clamp_of(int act) {
-  return ActClamp{act == kActNone ? -INFINITY : 0.0f, act == kActRelu6 ? 6.0f : INFINITY};
+__device__ __forceinline__ ActClamp act_clamp_of(int act, float alpha) {
+  const bool clamp0 = act == kActRelu || act == kActRelu6;
+  return ActClamp{clamp0 ? 0.0f : -INFINITY, act == kActRelu6 ? 6.0f : INFINITY, act == kActLeaky ? alpha : 1.0f};
 }
 template <bool GELU>
 __device__ __forceinline__ float act_apply(float v, ActClamp a) {
   if constexpr (GELU)
     return gelu(v);
   else
-    return __builtin_amdgcn_fmed3f(v, a.lo, a.hi);
+    return __builtin_amdgcn_fmed3f(fmaxf(v, v * a.slope), a.lo, a.hi);
 }
-__device__ __forceinline__ float apply_act(float v, int act) {
-  return act == kActGelu ? gelu(v) : act_apply<false>(v, act_clamp_of(act));
+__device__ __forceinline__ float apply_act(float v, int act, float alpha) {
+  return act == kActGelu ? gelu(v) : act_apply<false>(v, act_clamp_of(act, alpha));
 }
 
 // Unpacks 8 bf16 held in a uint4 into floats.
@@ -86,7 +90,7 @@ __device__ __forceinline__ void materialize_args(const ConvParams& p) {
   asm volatile("" ::"s"(p.x), "s"(p.w), "s"(p.bias), "s"(p.res), "s"(p.y), "s"(p.partial));
   asm volatile("" ::"s"(p.N), "s"(p.H), "s"(p.W), "s"(p.Cp), "s"(p.P), "s"(p.Q), "s"(p.R), "s"(p.S),
                "s"(p.sh), "s"(p.sw), "s"(p.pt), "s"(p.pl));
-  asm volatile("" ::"s"(p.M), "s"(p.Kp), "s"(p.Kg), "s"(p.Kgp), "s"(p.ldy), "s"(p.ldr), "s"(p.act),
+  asm volatile("" ::"s"(p.M), "s"(p.Kp), "s"(p.Kg), "s"(p.Kgp), "s"(p.ldy), "s"(p.ldr), "s"(p.act), "s"(p.alpha),
                "s"(p.splits), "s"(p.k_tiles_per_split), "s"(p.x_bytes), "s"(p.w_bytes), "s"(p.res_bytes),
                "s"(p.xcd_py));
   asm volatile("" ::"s"(p.mg_pq), "s"(p.mg_q), "s"(p.mg_cp), "s"(p.mg_s), "s"(p.mg_tile), "s"(p.mg_wp),

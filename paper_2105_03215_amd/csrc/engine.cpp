@@ -319,6 +319,7 @@ void Planner::plan_stem(int ci, int pi) {
   p.ppt = pn.pad[0], p.ppl = pn.pad[1];
   p.PO = (int)ps[2], p.QO = (int)ps[3];
   p.act = (int)c.act;
+  p.alpha = c.alpha;
   p.wld = stem_weight_ld(p.R);
   // BYOC_STEM_GRID=<n>: at most n persistent workgroups (tests drive several
   // tiles through one workgroup on small inputs with it)
@@ -454,6 +455,7 @@ void Planner::plan_node(int ni) {
   L.x = loc[n.data];
   L.y = loc[n.out];
   L.act = (int)n.act;
+  L.alpha = n.alpha;
   if (n.residual >= 0) L.res = loc[n.residual];
   const int64_t ebytes = bf16 ? 2 : 4;
 
@@ -482,6 +484,7 @@ void Planner::plan_node(int ni) {
       p.N = N, p.C = C, p.H = H, p.W = W, p.K = K, p.P = P, p.Q = Q, p.R = R, p.S = S;
       p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1];
       p.groups = n.groups, p.act = (int)n.act;
+      p.alpha = n.alpha;
       L.w = wslot(numel(ws) * 4);
       jobs.push_back({PackJob::Copy, wc, L.w.off, 0, 0, 0, 0, 0, 0, 0, (int)numel(ws), (int)numel(ws)});
       if (bc >= 0) {
@@ -500,6 +503,7 @@ void Planner::plan_node(int ni) {
       DwParams& p = L.dw;
       p.N = N, p.H = H, p.W = W, p.Cp = Cp, p.P = P, p.Q = Q, p.R = R, p.S = S;
       p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1], p.act = (int)n.act;
+      p.alpha = n.alpha;
       L.w = wslot((int64_t)R * S * Cp * 2);
       jobs.push_back({PackJob::DwW, wc, L.w.off, K, 1, R, S, Cp, 0, 0, 0, 0});
       L.bias = wslot(Cp * 4);
@@ -518,6 +522,7 @@ void Planner::plan_node(int ni) {
     p.ldy = Kp;
     p.ldr = Kp;
     p.act = (int)n.act;
+    p.alpha = n.alpha;
     const int rows = (int)rup(Kp, kRowPad);
     const int64_t xb = (int64_t)N * H * W * Cp * 2, wb = (int64_t)rows * p.Kgp * 2;
     if (xb >= (int64_t(1) << 31) || wb >= (int64_t(1) << 31)) {
@@ -1079,10 +1084,10 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
     }
     case Launch::AddBf16:
       return launch_add_bf16((const bf16_t*)c.ptr(L.x), (const bf16_t*)c.ptr(L.other),
-                             (bf16_t*)c.ptr(L.y), L.n, L.act, c.s);
+                             (bf16_t*)c.ptr(L.y), L.n, L.act, L.alpha, c.s);
     case Launch::AddF32:
       return launch_add_f32((const float*)c.ptr(L.x), (const float*)c.ptr(L.other),
-                            (float*)c.ptr(L.y), L.n, L.act, c.s);
+                            (float*)c.ptr(L.y), L.n, L.act, L.alpha, c.s);
     case Launch::NchwToNhwc:
       return launch_nchw_to_nhwc(c.ptr(L.x), L.src_bf16, (bf16_t*)c.ptr(L.y), L.N, L.C, L.H, L.W,
                                  L.Cp, c.s);

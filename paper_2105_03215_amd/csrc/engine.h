@@ -44,6 +44,7 @@ struct Launch {
   float qm = 0.f;                //   and rescaling factor
   int64_t n = 0;
   int act = 0;
+  float alpha = 0.f;  // leaky ReLU slope
   bool src_bf16 = false, dst_bf16 = false;
   int N = 0, C = 0, H = 0, W = 0, Cp = 0, M = 0, K = 0, Kp = 0;
 };

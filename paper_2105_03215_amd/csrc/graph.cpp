@@ -155,6 +155,7 @@ bool split_composite(const std::string& name, CompositeName* c) {
     if (parts[i] == "relu") c->act = Act::Relu;
     else if (parts[i] == "relu6") c->act = Act::Relu6;
     else if (parts[i] == "gelu") c->act = Act::Gelu;
+    else if (parts[i] == "leaky") c->act = Act::Leaky;
     else return false;
     ++i;
   }
@@ -168,6 +169,7 @@ const char* act_name(Act a) {
     case Act::Relu: return "relu";
     case Act::Relu6: return "relu6";
     case Act::Gelu: return "gelu";
+    case Act::Leaky: return "leaky";
     default: return "none";
   }
 }
@@ -356,6 +358,12 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
       n.other = args[1];
     }
     const auto& xs = shp(n.data);
+    if (n.act == Act::Leaky && attrs && attrs->get("alpha")) {
+      const JsonValue* av = attrs->get("alpha");
+      if (av->kind != JsonValue::Number || !(av->num >= 0.0 && av->num < 1.0))
+        return perr(where + ": attrs.alpha must be a number in [0, 1)");
+      n.alpha = (float)av->num;
+    }
 
     if (n.op == OpKind::Conv) {
       if (xs.size() != 4) return serr(where + ": data must be 4-D NCHW, got " + shape_str(xs));
@@ -453,7 +461,8 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
         return serr(where + ": int8 operand '" + g.values[a].name + "' has no quant parameters");
       }
       if (n.depthwise) return uerr(where + ": depthwise conv has no int8 form");
-      if (n.act == Act::Gelu) return uerr(where + ": gelu has no int8 form");
+      if (n.act == Act::Gelu || n.act == Act::Leaky)
+        return uerr(where + ": " + act_name(n.act) + " has no int8 form");
       if (n.op == OpKind::MaxPool) {
         const Value& xv = g.values[n.data];
         if (ov.has_q && (ov.qscale != xv.qscale || ov.qzero != xv.qzero))

@@ -27,7 +27,7 @@ struct Status {
 // I8: the compute type of a partially quantized graph (int8 codes with an
 // affine scale and zero point per tensor); never an external dtype.
 enum class DType { F32 = BYOC_F32, BF16 = BYOC_BF16, I8 = 2 };
-enum class Act { None = 0, Relu = 1, Relu6 = 2, Gelu = 3 };
+enum class Act { None = 0, Relu = 1, Relu6 = 2, Gelu = 3, Leaky = 4 };
 enum class OpKind { Conv, Dense, MaxPool, AvgPool, Add };
 
 // A named tensor of the graph: a subgraph input, a constant or a node output.
@@ -50,6 +50,7 @@ struct Node {
   bool has_bias = false;
   bool has_add = false;
   Act act = Act::None;
+  float alpha = 0.1f;  // leaky ReLU slope (attrs.alpha)
   int data = -1, weight = -1, bias = -1, residual = -1, other = -1;  // value ids
   int out = -1;                                                      // value id
   int stride[2] = {1, 1};

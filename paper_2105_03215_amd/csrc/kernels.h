@@ -10,7 +10,7 @@ namespace byoc {
 
 typedef uint16_t bf16_t;  // raw bfloat16 bits
 
-enum ActCode { kActNone = 0, kActRelu = 1, kActRelu6 = 2, kActGelu = 3 };
+enum ActCode { kActNone = 0, kActRelu = 1, kActRelu6 = 2, kActGelu = 3, kActLeaky = 4 };
 
 // Implicit-GEMM convolution (and dense, as a 1x1 conv on 1x1 images) on
 // bf16 MFMA.  Activations NHWC with Cp channels (multiple of 8); weights
@@ -31,6 +31,7 @@ struct ConvParams {
   int Kgp;  // packed weight row stride (multiple of 64)
   int ldy, ldr;
   int act;
+  float alpha;  // leaky ReLU slope (act == kActLeaky)
   int splits;   // split-K factor (1 = none)
   int k_tiles_per_split;
   int x_bytes;  // extent of x, w and res in bytes (buffer-load range; < 2^31)
@@ -94,6 +95,7 @@ struct StemParams {
   int kph, kpw, sph, spw, ppt, ppl;  // pool window, stride, padding
   int PO, QO;                    // pool output size
   int act;
+  float alpha;                   // leaky ReLU slope
   int grid_cap;                  // > 0: at most this many workgroups
 };
 bool stem_supported(int C, int K, int R, int S, int sh, int sw, int kph, int kpw, int sph, int spw);
@@ -117,6 +119,7 @@ struct ConvF32Params {
   const float* res;  // NCHW like y, or nullptr
   float* y;
   int N, C, H, W, K, P, Q, R, S, sh, sw, pt, pl, groups, act;
+  float alpha;  // leaky ReLU slope
 };
 hipError_t launch_conv_f32(const ConvF32Params& p, hipStream_t s);
 
@@ -128,6 +131,7 @@ struct DwParams {
   const bf16_t* res;
   bf16_t* y;
   int N, H, W, Cp, P, Q, R, S, sh, sw, pt, pl, act;
+  float alpha;  // leaky ReLU slope
 };
 hipError_t launch_depthwise(const DwParams& p, hipStream_t s);
 
@@ -142,9 +146,9 @@ hipError_t launch_maxpool_nchw_f32(const PoolParams& p, hipStream_t s);
 hipError_t launch_avgpool_nchw_f32(const PoolParams& p, hipStream_t s);   // y [N][C]
 
 // y = act(a + b) over n elements (n multiple of 8 for bf16).
-hipError_t launch_add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* y, int64_t n, int act,
+hipError_t launch_add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* y, int64_t n, int act, float alpha,
                            hipStream_t s);
-hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, int act,
+hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, int act, float alpha,
                           hipStream_t s);
 
 // Boundary transforms.  src_bf16 / dst_bf16 select the external dtype.

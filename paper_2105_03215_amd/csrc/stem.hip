@@ -290,7 +290,7 @@ __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemPara
             acc[f][j][e] = x == -INFINITY ? x : gelu(x);
           }
     }
-    const ActClamp ac = p.act == kActGelu ? act_clamp_of(kActNone) : act_clamp_of(p.act);
+    const ActClamp ac = p.act == kActGelu ? act_clamp_of(kActNone, 0.f) : act_clamp_of(p.act, p.alpha);
 
     // pooled rows 2 wave + q (q < 2): window rows SPH * q + dr of this
     // wave's conv rows, window columns lanes spw * c + dc.  FULL: a 3x3

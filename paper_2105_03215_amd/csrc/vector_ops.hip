@@ -54,7 +54,7 @@ __global__ __launch_bounds__(kThreads) void depthwise_kernel(DwParams p) {
     for (int i = 0; i < 8; ++i) acc[i] += rv[i];
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = apply_act(acc[i], p.act);
+  for (int i = 0; i < 8; ++i) acc[i] = apply_act(acc[i], p.act, p.alpha);
   *(uint4*)(p.y + o) = pack8(acc);
 }
 
@@ -172,22 +172,22 @@ __global__ __launch_bounds__(kThreads) void avgpool_nchw_f32_kernel(PoolParams p
 
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void add_bf16_kernel(const bf16_t* a, const bf16_t* b,
-                                                            bf16_t* y, int64_t n8, int act) {
+                                                            bf16_t* y, int64_t n8, int act, float alpha) {
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (i >= n8) return;
   float va[8], vb[8];
   unpack8(((const uint4*)a)[i], va);
   unpack8(((const uint4*)b)[i], vb);
 #pragma unroll
-  for (int c = 0; c < 8; ++c) va[c] = apply_act(va[c] + vb[c], act);
+  for (int c = 0; c < 8; ++c) va[c] = apply_act(va[c] + vb[c], act, alpha);
   ((uint4*)y)[i] = pack8(va);
 }
 
 __global__ __launch_bounds__(kThreads) void add_f32_kernel(const float* a, const float* b,
-                                                           float* y, int64_t n, int act) {
+                                                           float* y, int64_t n, int act, float alpha) {
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (i >= n) return;
-  y[i] = apply_act(a[i] + b[i], act);
+  y[i] = apply_act(a[i] + b[i], act, alpha);
 }
 
 // ---------------------------------------------------------------------------
@@ -357,15 +357,15 @@ hipError_t launch_avgpool_nchw_f32(const PoolParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* y, int64_t n, int act,
+hipError_t launch_add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* y, int64_t n, int act, float alpha,
                            hipStream_t s) {
-  add_bf16_kernel<<<grid_for(n / 8), kThreads, 0, s>>>(a, b, y, n / 8, act);
+  add_bf16_kernel<<<grid_for(n / 8), kThreads, 0, s>>>(a, b, y, n / 8, act, alpha);
   return hipGetLastError();
 }
 
-hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, int act,
+hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, int act, float alpha,
                           hipStream_t s) {
-  add_f32_kernel<<<grid_for(n), kThreads, 0, s>>>(a, b, y, n, act);
+  add_f32_kernel<<<grid_for(n), kThreads, 0, s>>>(a, b, y, n, act, alpha);
   return hipGetLastError();
 }
 

@@ -58,6 +58,8 @@ def _host_op(node, args):
         return torch.relu(x)
     if op == "clip":
         return torch.clamp(x, a["a_min"], a["a_max"])
+    if op == "nn.leaky_relu":
+        return F.leaky_relu(x, float(a.get("alpha", 0.1)))
     if op == "nn.gelu":
         return 0.5 * x * (1.0 + torch.erf(x / math.sqrt(2.0)))
     if op == "sigmoid":

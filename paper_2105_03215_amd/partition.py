@@ -69,7 +69,7 @@ def _pads(padding):
 
 def _infer(op, ins, attrs):
     """Output shape of an operator from its input shapes and attributes."""
-    if op in ("nn.relu", "clip", "nn.gelu", "sigmoid", "nn.softmax"):
+    if op in ("nn.relu", "clip", "nn.gelu", "nn.leaky_relu", "sigmoid", "nn.softmax"):
         return ins[0]
     if op in ("add", "multiply"):
         if ins[0] != ins[1]:
@@ -277,7 +277,7 @@ def _with_epilogue(core):
                             is_op("add")(wildcard("residual"), x))
     return added.optional(lambda x: is_op("nn.relu")(x) |
                           is_op("clip")(x).has_attr(a_min=0.0, a_max=6.0) |
-                          is_op("nn.gelu")(x))
+                          is_op("nn.gelu")(x) | is_op("nn.leaky_relu")(x))
 
 
 def conv2d_pattern():
@@ -298,7 +298,8 @@ def global_avg_pool_pattern():
 
 def add_pattern():
     return is_op("add")(wildcard("data"), wildcard("residual")).optional(
-        lambda x: is_op("nn.relu")(x) | is_op("clip")(x).has_attr(a_min=0.0, a_max=6.0))
+        lambda x: is_op("nn.relu")(x) | is_op("clip")(x).has_attr(a_min=0.0, a_max=6.0) |
+        is_op("nn.leaky_relu")(x))
 
 
 def _act_suffix(g, env):
@@ -309,6 +310,8 @@ def _act_suffix(g, env):
         return "_relu6"
     if "nn.gelu" in by:
         return "_gelu"
+    if "nn.leaky_relu" in by:
+        return "_leaky"
     return ""
 
 
@@ -673,6 +676,9 @@ def _serialize(g, name, us, used_outside):
             attrs = {"strides": list(conv.attrs.get("strides", [1, 1])),
                      "padding": _pads(conv.attrs.get("padding", [0, 0, 0, 0])),
                      "dilation": [1, 1], "groups": conv.attrs.get("groups", 1)}
+        if comp.name.endswith("_leaky"):
+            act = g.nodes[[m for m in comp.members if g.nodes[m].op == "nn.leaky_relu"][0]]
+            attrs["alpha"] = float(act.attrs.get("alpha", 0.1))
         elif comp.name == "max_pool2d":
             pool = g.nodes[comp.root]
             attrs = {"pool_size": list(pool.attrs["pool_size"]), "strides": list(pool.attrs["strides"]),
@@ -817,7 +823,7 @@ def lower_subgraph(graph, consts):
                 k += 1
             if "add" in parts:
                 y = g.call("add", [y, ins[k]])
-            act = parts[-1] if parts[-1] in ("relu", "relu6", "gelu") else None
+            act = parts[-1] if parts[-1] in ("relu", "relu6", "gelu", "leaky") else None
         elif comp == "max_pool2d":
             y = g.call("nn.max_pool2d", ins, pool_size=list(attrs["pool_size"]),
                        strides=list(attrs["strides"]), padding=_pads(attrs.get("padding", [0] * 4)))
@@ -836,6 +842,8 @@ def lower_subgraph(graph, consts):
             y = g.call("clip", [y], a_min=0.0, a_max=6.0)
         elif act == "gelu":
             y = g.call("nn.gelu", [y])
+        elif act == "leaky":
+            y = g.call("nn.leaky_relu", [y], alpha=float(attrs.get("alpha", 0.1)))
         names[nd["name"]] = y
     for o in graph["outputs"]:
         g.output(names[o["name"]])

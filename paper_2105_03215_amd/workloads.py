@@ -31,6 +31,7 @@ CONFIG_IDS = {
     "mobilenet_v2": 3,
     "bert_ffn": 4,
     "vgg19": 5,
+    "darknet53": 6,
 }
 
 _BN_EPS = 1e-5
@@ -112,6 +113,7 @@ class GraphBuilder:
         self.outputs = []
         self.shapes = {}
         self.m2 = {}
+        self.mu = {}  # layer-wide mean of a tensor, where it is not ~0 (activation outputs, the image)
         self.next_tensor = 1
         self.n_folded = 0
         self.macs = 0
@@ -148,6 +150,7 @@ class GraphBuilder:
         self.input_arrays.append(a)
         self.shapes[name] = list(shape)
         self.m2[name] = m2
+        self.mu[name] = 0.5 if dist == "uniform" else 0.0
         return name
 
     def _after_add_act(self, m2_stream, m2_branch, act):
@@ -158,7 +161,7 @@ class GraphBuilder:
         return m2_stream + _ADD_RELU_KEEP * m2_branch
 
     def conv(self, x, k, r, stride=1, pad=None, groups=1, act="relu", bias=True, residual=None,
-             bn=True, gamma=1.0, w_std=None, b_std=None, name=None):
+             bn=True, gamma=1.0, w_std=None, b_std=None, name=None, alpha=0.1):
         """Conv composite with He-normal weights and an optional folded BN."""
         n, c, h, w = self.shapes[x]
         pad = (r // 2) if pad is None else pad
@@ -193,15 +196,21 @@ class GraphBuilder:
             ins.append(residual)
             comp += "_add"
             m2 = self._after_add_act(self.m2[residual], m2, act)
+        elif act == "leaky":
+            # the negative half keeps alpha^2 of its share; the output's mean
+            # is (1 - alpha) sigma / sqrt(2 pi) for a symmetric pre-activation
+            self.mu[name or "n%d" % len(self.nodes)] = (1.0 - alpha) * math.sqrt(m2 / (2.0 * math.pi))
+            m2 = 0.5 * (1.0 + alpha * alpha) * m2
         elif act:
             m2 = 0.5 * m2
         if act:
             comp += "_" + act
         p = (h + pads[0] + pads[2] - r) // strides[0] + 1
         q = (w + pads[1] + pads[3] - r) // strides[1] + 1
-        self.nodes.append({"name": name, "composite": comp, "inputs": ins,
-                           "attrs": {"strides": strides, "padding": pads, "dilation": [1, 1],
-                                     "groups": groups},
+        attrs = {"strides": strides, "padding": pads, "dilation": [1, 1], "groups": groups}
+        if act == "leaky":
+            attrs["alpha"] = alpha
+        self.nodes.append({"name": name, "composite": comp, "inputs": ins, "attrs": attrs,
                            "out_dtype": self.dtype})
         self.shapes[name] = [n, k, p, q]
         self.m2[name] = m2
@@ -264,7 +273,12 @@ class GraphBuilder:
         self.nodes.append({"name": name, "composite": comp, "inputs": [a, b], "attrs": {},
                            "out_dtype": self.dtype})
         self.shapes[name] = list(self.shapes[a])
-        self.m2[name] = self._after_add_act(self.m2[a], self.m2[b], act)
+        mu_a, mu_b = self.mu.get(a, 0.0), self.mu.get(b, 0.0)
+        # E[(a + b)^2] = E[a^2] + E[b^2] + 2 E[a b]; the means of two
+        # activated tensors add coherently (zero for zero-mean operands)
+        self.m2[name] = self._after_add_act(self.m2[a], self.m2[b], act) + (0.0 if act else 2.0 * mu_a * mu_b)
+        if not act:
+            self.mu[name] = mu_a + mu_b
         return name
 
     def output(self, x, dtype=None, layout=None):
@@ -418,9 +432,43 @@ def vgg19(n=1, hw=224, input_dtype="bf16", num_classes=1000, fc=4096):
     return g.finish({"batch": n})
 
 
+# DarkNet-53 (the YOLOv3 backbone): per stage, output channels and residual blocks
+_DARKNET53 = [(64, 1), (128, 2), (256, 8), (512, 8), (1024, 4)]
+# folded-BN scale of each residual branch's last conv: the branch adds after
+# its leaky ReLU, whose output has a positive mean, so with unit scale the
+# stream's mean grows coherently over a stage's blocks (to rms ~20 after 8
+# blocks); a small branch scale, as trained residual networks have, keeps it O(1)
+_DARKNET_BRANCH_GAMMA = 0.3
+
+
+def darknet53(n=1, hw=256, input_dtype="bf16", num_classes=1000, alpha=0.1):
+    """DarkNet-53-shaped network (a fully offloaded row of the paper's
+    Table 1): a 3x3 conv with 32 channels, then five stages, each a 3x3
+    stride-2 conv doubling the channels followed by residual blocks of a 1x1
+    conv halving them and a 3x3 conv restoring them, every conv with folded
+    batch norm and leaky ReLU (slope 0.1); the shortcut adds the block input
+    to the block's activated output (a standalone add, after the activation;
+    the branch's folded batch norm is scaled by 0.3, see above).
+    Global average pool and a dense classifier; 52 convs + 1 dense.  Input
+    256x256, the resolution of the published classifier."""
+    g = GraphBuilder("darknet53", CONFIG_IDS["darknet53"])
+    x = g.input("x", [n, 3, hw, hw], "uniform", dtype=input_dtype)
+    y = g.conv(x, 32, 3, act="leaky", alpha=alpha, name="conv0")
+    for si, (c, blocks) in enumerate(_DARKNET53):
+        y = g.conv(y, c, 3, stride=2, act="leaky", alpha=alpha, name="s%d_down" % si)
+        for b in range(blocks):
+            h = g.conv(y, c // 2, 1, act="leaky", alpha=alpha, name="s%d_b%d_a" % (si, b))
+            h = g.conv(h, c, 3, act="leaky", alpha=alpha, gamma=_DARKNET_BRANCH_GAMMA, name="s%d_b%d_b" % (si, b))
+            y = g.add(y, h, name="s%d_b%d_add" % (si, b))
+    y = g.global_avg_pool(y, name="pool")
+    y = g.dense(y, num_classes, name="fc")
+    g.output(y)
+    return g.finish({"batch": n})
+
+
 def build(name, **kw):
     """Build a workload by name: conv_f32, resnet18_block, resnet50_v1,
-    resnet50_v1b, mobilenet_v2, bert_ffn, vgg19."""
+    resnet50_v1b, mobilenet_v2, bert_ffn, vgg19, darknet53."""
     if name == "conv_f32":
         return conv_f32(**kw)
     if name == "resnet18_block":
@@ -435,4 +483,6 @@ def build(name, **kw):
         return bert_ffn(**kw)
     if name == "vgg19":
         return vgg19(**kw)
+    if name == "darknet53":
+        return darknet53(**kw)
     raise ValueError("unknown workload %r" % name)

@@ -33,6 +33,8 @@ def op_ref(node, args):
         return np.clip(np.asarray(x, np.float64), a["a_min"], a["a_max"])
     if op == "nn.gelu":
         return ops.gelu(x)
+    if op == "nn.leaky_relu":
+        return ops.leaky_relu(x, float(a.get("alpha", 0.1)))
     if op == "sigmoid":
         return 1.0 / (1.0 + np.exp(-np.asarray(x, np.float64)))
     if op == "nn.softmax":

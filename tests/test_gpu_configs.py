@@ -149,6 +149,54 @@ def test_vgg19_bs8_sampled():
     assert np.all(np.isfinite(g))
 
 
+def test_darknet53_teacher_forced():
+    """All 76 composites of DarkNet-53 (bs1, 128x128), each recomputed by
+    the oracle from the GPU's own inputs, within one bf16 ulp."""
+    announce("darknet53 teacher forced, 76 composites")
+    wl = workloads.build("darknet53", n=1, hw=128)
+    graph = dict(wl.graph)
+    graph["outputs"] = [{"name": n["name"], "dtype": "bf16"} for n in graph["nodes"]]
+    gpu = _gpu(workloads.Workload(graph, wl.consts, wl.inputs, wl.macs, wl.conv_macs))
+    vals = {"x": oracle.bf16.round_bf16(wl.inputs[0])}
+    consts = {c["name"]: wl.consts[c["index"]] for c in graph["constants"]}
+    for node, g in zip(graph["nodes"], gpu):
+        args = [vals[r] if r in vals else consts[r] for r in node["inputs"]]
+        ref = oracle.run_node(node, args)
+        assert within_one_ulp(g, ref, term_scale_node(node, args)).all(), node["name"]
+        vals[node["name"]] = g
+
+
+def _drift_bound(graph, consts, inputs):
+    """max(1e-2, twice the oracle's own bf16io-vs-exact spread): 23 residual
+    adds of bf16 storage after the activation let two correct
+    implementations drift apart by more than one rounding."""
+    io = oracle.run_graph(graph, consts, inputs, mode="bf16io")[0]
+    ex = oracle.run_graph(graph, consts, inputs, mode="exact")[0]
+    return io, max(BF16_TOL, 2 * rel_err(io, ex))
+
+
+def test_darknet53_bs1_128():
+    announce("darknet53 bs1 128x128")
+    wl = workloads.build("darknet53", n=1, hw=128)
+    g = _gpu(wl)[0]
+    o, bound = _drift_bound(wl.graph, wl.consts, wl.inputs)
+    err = rel_err(g, o)
+    print("darknet53 bs1 err %.3e bound %.3e" % (err, bound))
+    assert err <= bound
+
+
+def test_darknet53_bs32_sampled():
+    announce("darknet53 bs32 256x256 sampled images 0 and 31")
+    wl = workloads.build("darknet53", n=32)
+    g = _gpu(wl)[0]
+    rows = [0, 31]
+    o, bound = _drift_bound(_sample_graph(wl, 2), wl.consts, _sample_inputs(wl, rows))
+    err = rel_err(g[rows], o)
+    print("darknet53 bs32 err %.3e bound %.3e" % (err, bound))
+    assert err <= bound
+    assert np.all(np.isfinite(g))
+
+
 def test_bert_ffn_layers_teacher_forced():
     """All 24 dense composites at full size (1024 tokens), each recomputed by
     the oracle on 64 sampled token rows from the GPU's own layer input."""

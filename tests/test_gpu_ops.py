@@ -58,6 +58,9 @@ CONV_CASES = [
     ("1x1_c16_k8", (2, 16, 10, 10), 8, 1, 1, 0, None, True),
     ("3x3_big_m", (4, 64, 56, 56), 128, 3, 2, 1, "relu", False),
     ("1x1_gelu", (1, 64, 9, 9), 72, 1, 1, 0, "gelu", False),
+    ("3x3_leaky_res", (2, 64, 14, 14), 64, 3, 1, 1, "leaky", True),
+    ("3x3_s2_leaky", (2, 128, 16, 16), 256, 3, 2, 1, "leaky", False),
+    ("1x1_splitk_leaky", (1, 1024, 7, 7), 512, 1, 1, 0, "leaky", False),
 ]
 
 
@@ -91,6 +94,7 @@ HALO_CASES = [
     ("c128_28x28_ring6", (2, 128, 28, 28), 128, "relu", True, 6),
     ("c128_28x28_builtin", (4, 128, 28, 28), 128, "relu", True, None),
     ("c512_7x7_gelu", (3, 512, 7, 7), 128, "gelu", False, 8),
+    ("c256_14x14_leaky_ring3", (2, 256, 14, 14), 128, "leaky", False, 3),
 ]
 
 
@@ -235,6 +239,7 @@ STEM_CASES = [
     ("stem_3x3_s1_pool2", (2, 4, 20, 21), 3, 1, 1, None, (2, 2, 0), "bf16"),
     ("stem_5x5_s2_pool3_s1", (1, 3, 24, 24), 5, 2, 2, "relu6", (3, 1, 1), "bf16"),
     ("resnet_stem_f32_aligned", (2, 3, 48, 48), 7, 2, 3, "relu", (3, 2, 1), "f32"),
+    ("stem_leaky", (2, 3, 40, 40), 7, 2, 3, "leaky", (3, 2, 1), "bf16"),
 ]
 
 
@@ -261,6 +266,7 @@ DENSE_ROWS_CASES = [
     ("m33_k1000_n24_gelu_res", 33, 1000, 24, "gelu", True),
     ("m64_k64_n40_relu6", 64, 64, 40, "relu6", False),
     ("m16_k4200_n16_res", 16, 4200, 16, None, True),  # more k-steps than one pass of the waves
+    ("m32_k1024_n1000_leaky", 32, 1024, 1000, "leaky", False),
 ]
 
 
@@ -300,3 +306,27 @@ def test_fused_stem_tile_loop(case, grid, monkeypatch):
     g.output(p)
     launches = _check_bf16(g.finish(), "stem loop %s grid %d" % (name, grid))
     assert launches[0]["name"] == "stem_conv_maxpool", launches[0]
+
+
+def test_leaky_slopes_depthwise_add_and_f32():
+    """The leaky ReLU's slope reaches every other kernel: a non-default slope
+    on the implicit GEMM, the depthwise conv, the standalone add, and the
+    fp32 graph's direct conv and add."""
+    g = GraphBuilder("op_leaky", 1900)
+    x = g.input("x", [2, 48, 12, 12], "normal")
+    a = g.conv(x, 48, 3, act="leaky", alpha=0.25, name="a")
+    d = g.conv(a, 48, 3, groups=48, act="leaky", alpha=0.05, name="dw")
+    s = g.add(a, d, act="leaky", name="s")
+    g.output(s)
+    g.output(a)
+    wl = g.finish()
+    for n in wl.graph["nodes"]:
+        if n["name"] == "s":
+            n["attrs"]["alpha"] = 0.3
+    _check_bf16(wl, "leaky slopes: conv, depthwise, add")
+    g = GraphBuilder("op_leaky_f32", 1901, dtype="f32")
+    x = g.input("x", [2, 8, 11, 11], "normal")
+    a = g.conv(x, 8, 3, act="leaky", alpha=0.2, bn=False, w_std=0.3, name="a")
+    s = g.add(a, x, act="leaky", name="s")
+    g.output(s)
+    _check_f32(g.finish(), "fp32 leaky conv and add")

@@ -81,9 +81,24 @@ def test_bf16_inputs_are_representable():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block", "vgg19"])
+def test_darknet53_structure_and_work():
+    wl = workloads.darknet53(n=1)
+    comps = [n["composite"] for n in wl.graph["nodes"]]
+    assert comps.count("conv2d_bias_leaky") == 52 and comps.count("add") == 23
+    assert comps[-2:] == ["global_avg_pool2d", "dense_bias"]
+    assert all(n["attrs"]["alpha"] == 0.1 for n in wl.graph["nodes"] if n["composite"].endswith("_leaky"))
+    # 18.6 GFLOP per 256x256 image (the published DarkNet-53 count is 18.7 BFLOP)
+    assert abs(2 * wl.macs / 1e9 - 18.57) < 0.01
+    # the shortcut adds the block input to the activated branch
+    adds = [n for n in wl.graph["nodes"] if n["composite"] == "add"]
+    by = {n["name"]: n for n in wl.graph["nodes"]}
+    assert all(by[a["inputs"][1]]["composite"] == "conv2d_bias_leaky" for a in adds)
+
+
+@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block", "vgg19", "darknet53"])
 def test_activations_stay_order_one(name):
-    wl = workloads.build(name, **({"hw": 112} if name == "vgg19" else {}))
+    kw = {"vgg19": {"hw": 112}, "darknet53": {"hw": 128}}.get(name, {})
+    wl = workloads.build(name, **kw)
     outs, vals = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io", keep=True)
     names = [n["name"] for n in wl.graph["nodes"]]
     peak = max(float(np.abs(vals[n]).max()) for n in names)
