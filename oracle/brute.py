@@ -88,3 +88,27 @@ def global_avg_pool2d(x):
 
 def gelu(v):
     return v * 0.5 * (1.0 + math.erf(v / math.sqrt(2.0)))
+
+
+def avg_pool2d(x, pool_size=(3, 3), strides=(1, 1), padding=(1, 1, 1, 1), count_include_pad=False):
+    n_, c_, h_, w_ = len(x), len(x[0]), len(x[0][0]), len(x[0][0][0])
+    r_, s_ = pool_size
+    sh, sw = strides
+    pt, pl, pb, pr = padding
+    p_ = (h_ + pt + pb - r_) // sh + 1
+    q_ = (w_ + pl + pr - s_) // sw + 1
+    y = [[[[0.0] * q_ for _ in range(p_)] for _ in range(c_)] for _ in range(n_)]
+    for n in range(n_):
+        for c in range(c_):
+            for p in range(p_):
+                for q in range(q_):
+                    tot, cnt = 0.0, 0
+                    for r in range(r_):
+                        hi = p * sh - pt + r
+                        for s in range(s_):
+                            wi = q * sw - pl + s
+                            if 0 <= hi < h_ and 0 <= wi < w_:
+                                tot += float(x[n][c][hi][wi])
+                                cnt += 1
+                    y[n][c][p][q] = tot / (r_ * s_ if count_include_pad else cnt)
+    return y

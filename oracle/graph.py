@@ -16,8 +16,11 @@ residual add comes before the activation, as in a ResNet block):
 
 Pattern names: ``conv2d[_bias][_add][_relu|_relu6|_gelu|_leaky]``,
 ``dense[_bias][_add][_relu|_relu6|_gelu|_leaky]``, ``max_pool2d``,
-``global_avg_pool2d``, ``add[_relu|_relu6|_leaky]``; a leaky ReLU takes its
-slope from ``attrs.alpha`` (default 0.1).  Inputs of a node are listed in
+``global_avg_pool2d``, ``avg_pool2d`` (window mean; attrs pool_size,
+strides, padding, count_include_pad, default false: the divisor counts only
+positions inside the image), ``concatenate`` (any number of inputs joined
+along the channel axis), ``add[_relu|_relu6|_leaky]``; a leaky ReLU takes
+its slope from ``attrs.alpha`` (default 0.1).  Inputs of a node are listed in
 the order data, weight, bias, residual.
 
 Precision semantics.  A node whose ``out_dtype`` is "bf16" belongs to a bf16
@@ -52,7 +55,7 @@ def load_graph(js):
 
 def parse_composite(name):
     """Split a pattern name into (op, has_bias, has_add, activation)."""
-    if name in ("max_pool2d", "global_avg_pool2d"):
+    if name in ("max_pool2d", "global_avg_pool2d", "avg_pool2d", "concatenate"):
         return name, False, False, None
     parts = name.split("_")
     op = parts[0]
@@ -122,6 +125,13 @@ def run_node(node, args, mode="bf16io"):
         y = ops.max_pool2d(args[0], tuple(attrs.get("pool_size", (3, 3))),
                            tuple(attrs.get("strides", (2, 2))),
                            tuple(attrs.get("padding", (1, 1, 1, 1))))
+    elif op == "avg_pool2d":
+        y = ops.avg_pool2d(args[0], tuple(attrs.get("pool_size", (3, 3))),
+                           tuple(attrs.get("strides", (1, 1))),
+                           tuple(attrs.get("padding", (1, 1, 1, 1))),
+                           bool(attrs.get("count_include_pad", False)))
+    elif op == "concatenate":
+        y = ops.concatenate(args, axis=1)
     else:
         y = ops.global_avg_pool2d(args[0])
     if act is not None:

@@ -133,6 +133,34 @@ def max_pool2d(x, pool_size=(3, 3), strides=(2, 2), padding=(1, 1, 1, 1)):
     return y
 
 
+def avg_pool2d(x, pool_size=(3, 3), strides=(1, 1), padding=(1, 1, 1, 1), count_include_pad=False):
+    """Mean over each window.  Without count_include_pad the divisor is the
+    number of window positions inside the image; with it, the full window."""
+    x = _f64(x)
+    n, c, h, wd = x.shape
+    r, s = pool_size
+    sh, sw = strides
+    pt, pl, pb, pr = padding
+    p = conv_output_size(h, r, sh, pt, pb)
+    q = conv_output_size(wd, s, sw, pl, pr)
+    xp = np.zeros((n, c, h + pt + pb, wd + pl + pr), dtype=np.float64)
+    xp[:, :, pt:pt + h, pl:pl + wd] = x
+    inside = np.zeros((h + pt + pb, wd + pl + pr), dtype=np.float64)
+    inside[pt:pt + h, pl:pl + wd] = 1.0
+    tot = np.zeros((n, c, p, q), dtype=np.float64)
+    cnt = np.zeros((p, q), dtype=np.float64)
+    for ri in range(r):
+        for si in range(s):
+            tot += xp[:, :, ri:ri + sh * (p - 1) + 1:sh, si:si + sw * (q - 1) + 1:sw]
+            cnt += inside[ri:ri + sh * (p - 1) + 1:sh, si:si + sw * (q - 1) + 1:sw]
+    return tot / (float(r * s) if count_include_pad else cnt)
+
+
+def concatenate(xs, axis=1):
+    """Join tensors along an axis (the channel axis of NCHW)."""
+    return np.concatenate([_f64(x) for x in xs], axis=axis)
+
+
 def global_avg_pool2d(x):
     """Mean over the spatial axes; output [N, C]."""
     x = _f64(x)

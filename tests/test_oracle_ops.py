@@ -230,3 +230,41 @@ def test_conv_output_size():
     assert ops.conv_output_size(56, 1, 2, 0, 0) == 28
     assert ops.conv_output_size(7, 3, 1, 1, 1) == 7
     assert math.floor((5 + 0 - 3) / 2) + 1 == ops.conv_output_size(5, 3, 2, 0, 0)
+
+
+@pytest.mark.parametrize("pool,strides,padding,incl", [((3, 3), (1, 1), (1, 1, 1, 1), False),
+                                                       ((3, 3), (1, 1), (1, 1, 1, 1), True),
+                                                       ((3, 2), (2, 1), (1, 0, 0, 1), False),
+                                                       ((2, 2), (2, 2), (0, 0, 0, 0), False)])
+def test_avg_pool_against_brute_force(pool, strides, padding, incl):
+    x = _rand(2 * 3 * 7 * 6).reshape(2, 3, 7, 6)
+    got = ops.avg_pool2d(x, pool, strides, padding, incl)
+    want = np.array(brute.avg_pool2d(x.tolist(), pool, strides, padding, incl))
+    np.testing.assert_allclose(got, want, rtol=1e-14, atol=1e-14)
+
+
+def test_avg_pool_closed_forms():
+    # a constant image averages to itself when padding is not counted, and
+    # to the constant times the inside fraction of the window when it is
+    x = np.full((1, 2, 5, 5), 3.0)
+    assert np.allclose(ops.avg_pool2d(x, (3, 3), (1, 1), (1, 1, 1, 1), False), 3.0)
+    y = ops.avg_pool2d(x, (3, 3), (1, 1), (1, 1, 1, 1), True)
+    assert y[0, 0, 0, 0] == 3.0 * 4 / 9 and y[0, 0, 0, 2] == 3.0 * 6 / 9 and y[0, 0, 2, 2] == 3.0
+    # without padding, a window covering the image is the global mean
+    z = _rand(2 * 3 * 4 * 4).reshape(2, 3, 4, 4)
+    np.testing.assert_allclose(ops.avg_pool2d(z, (4, 4), (1, 1), (0, 0, 0, 0))[:, :, 0, 0],
+                               ops.global_avg_pool2d(z), rtol=1e-15)
+
+
+def test_concatenate_slices_back():
+    a, b = _rand(2 * 3 * 4 * 5).reshape(2, 3, 4, 5), _rand(2 * 5 * 4 * 5).reshape(2, 5, 4, 5)
+    y = ops.concatenate([a, b])
+    assert y.shape == (2, 8, 4, 5)
+    assert np.array_equal(y[:, :3], a) and np.array_equal(y[:, 3:], b)
+
+
+@pytest.mark.parametrize("incl", [False, True])
+def test_avg_pool_against_torch(incl):
+    x = _rand(2 * 4 * 9 * 8).reshape(2, 4, 9, 8)
+    want = F.avg_pool2d(torch.from_numpy(x), 3, stride=1, padding=1, count_include_pad=incl).numpy()
+    np.testing.assert_allclose(ops.avg_pool2d(x, (3, 3), (1, 1), (1, 1, 1, 1), incl), want, rtol=1e-14, atol=1e-14)
