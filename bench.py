@@ -272,7 +272,7 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
-    ap.add_argument("--no-other", action="store_true", help="skip the VGG19 and DarkNet-53 bs32 lines")
+    ap.add_argument("--no-other", action="store_true", help="skip the VGG19, DarkNet-53 and Inception V3 bs32 lines")
     ap.add_argument("--no-quantized", action="store_true",
                     help="skip the int8 (partially quantized) run of the network")
     ap.add_argument("--no-partitioned", action="store_true",
@@ -383,7 +383,8 @@ def main():
     other = None
     if not args.no_other:
         other = [_other_workload(args, "vgg19", 32, dev, stream),
-                 _other_workload(args, "darknet53", 32, dev, stream)]
+                 _other_workload(args, "darknet53", 32, dev, stream),
+                 _other_workload(args, "inception_v3", 32, dev, stream)]
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -190,6 +190,9 @@ struct Planner {
   Status err;
   // fused stems: conv node -> its max-pool node, max-pool node -> conv node
   std::vector<int> stem_pool, stem_conv;
+  // zero-copy concatenation: value -> the concatenation it is written into
+  // (-1: none) and its first channel there
+  std::vector<int> alias_of, alias_off;
 
   bool i8;                                  // partially quantized (int8) graph
   const byoc_const* consts = nullptr;       // host constants (int8 weights are quantized on the host)
@@ -252,6 +255,12 @@ struct Planner {
   void plan_node(int ni);
   void plan_node_i8(int ni);
   void find_stems();
+  void find_concat_aliases();
+  Ref slice(int vcat, int channel) const {  // channel slice of a concatenation's buffer
+    Ref r = loc[vcat];
+    r.off += (int64_t)channel * 2;
+    return r;
+  }
   void plan_stem(int conv_ni, int pool_ni);
 };
 
@@ -337,9 +346,51 @@ void Planner::plan_stem(int ci, int pi) {
   e->launches.push_back(L);
 }
 
+// A concatenation's input produced by a conv, max pool or windowed average
+// pool that nothing else reads is written by its producer straight into its
+// channel slice of the concatenation's buffer (output pixel stride = the
+// concatenation's channels); other inputs are copied in.
+void Planner::find_concat_aliases() {
+  alias_of.assign(g.values.size(), -1);
+  alias_off.assign(g.values.size(), 0);
+  std::vector<int> uses(g.values.size(), 0);
+  for (const Node& n : g.nodes) {
+    for (int a : {n.data, n.residual, n.other})
+      if (a >= 0) ++uses[a];
+    if (n.op == OpKind::Concat)
+      for (size_t k = 1; k < n.cat.size(); ++k) ++uses[n.cat[k]];
+  }
+  for (const IoDesc& o : g.outputs) ++uses[o.value];
+  for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
+    const Node& c = g.nodes[ni];
+    if (c.op != OpKind::Concat) continue;
+    int off = 0;
+    for (int a : c.cat) {
+      const Value& v = g.values[a];
+      if (v.source == Value::Node && uses[a] == 1 && alias_of[a] < 0) {
+        const Node& p = g.nodes[v.index];
+        const bool kind = (p.op == OpKind::Conv && !p.depthwise) || p.op == OpKind::MaxPool ||
+                          p.op == OpKind::AvgPoolWin;
+        if (kind && stem_pool[v.index] < 0 && stem_conv[v.index] < 0) {
+          alias_of[a] = c.out;
+          alias_off[a] = off;
+        }
+      }
+      off += (int)v.shape[1];
+    }
+  }
+}
+
 Status Planner::plan() {
   if (i8) return plan_i8();
   find_stems();
+  find_concat_aliases();
+  // concatenation outputs are allocated first: their producers write into them
+  for (const Node& n : g.nodes)
+    if (n.op == OpKind::Concat) {
+      cp[n.out] = (int)rup(g.values[n.out].shape[1], 8);
+      loc[n.out] = arena(internal_bytes(n.out));
+    }
   // ---- inputs: direct use or boundary transform ----------------------------
   for (size_t i = 0; i < g.inputs.size(); ++i) {
     const IoDesc& in = g.inputs[i];
@@ -405,6 +456,11 @@ Status Planner::plan() {
     if (stem_pool[ni] >= 0) {  // conv of a fused stem: its output is never stored
       loc[v] = Ref();
       continue;
+    }
+    if (n.op == OpKind::Concat) placed = true;  // allocated above
+    if (!placed && alias_of[v] >= 0) {
+      loc[v] = slice(alias_of[v], alias_off[v]);
+      placed = true;
     }
     if (!placed) loc[v] = arena(internal_bytes(v));
     if (stem_conv[ni] >= 0)
@@ -519,7 +575,7 @@ void Planner::plan_node(int ni) {
     p.Kp = Kp;
     p.Kg = R * S * Cp;
     p.Kgp = (int)rup(p.Kg, kKPad);
-    p.ldy = Kp;
+    p.ldy = alias_of[n.out] >= 0 ? cp[alias_of[n.out]] : Kp;
     p.ldr = Kp;
     p.act = (int)n.act;
     p.alpha = n.alpha;
@@ -648,15 +704,45 @@ void Planner::plan_node(int ni) {
     }
     return;
   }
-  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool) {
+  if (n.op == OpKind::Concat) {  // copies of the inputs not written in place
+    const auto& cs = g.values[n.out].shape;
+    int off = 0;
+    for (int a : n.cat) {
+      const int ca = (int)g.values[a].shape[1];
+      if (alias_of[a] != n.out) {
+        Launch C;
+        C.op = Launch::CopyChannels;
+        C.info.kind = BYOC_K_ADD;
+        C.info.node = ni;
+        C.x = loc[a];
+        C.y = slice(n.out, off);
+        C.M = (int)(cs[0] * cs[2] * cs[3]);
+        C.C = ca;
+        C.Cp = cp[a];
+        C.Kp = cp[n.out];
+        C.info.bytes = 2 * act_bytes(a);
+        name(C, "concat_copy");
+        e->launches.push_back(C);
+      }
+      off += ca;
+    }
+    return;
+  }
+  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool || n.op == OpKind::AvgPoolWin) {
     PoolParams& p = L.pool;
     p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3], p.Cp = cp[n.data];
     p.R = n.pool[0], p.S = n.pool[1], p.sh = n.stride[0], p.sw = n.stride[1];
     p.pt = n.pad[0], p.pl = n.pad[1];
-    p.P = n.op == OpKind::MaxPool ? (int)ys[2] : 1;
-    p.Q = n.op == OpKind::MaxPool ? (int)ys[3] : 1;
+    p.P = n.op != OpKind::AvgPool ? (int)ys[2] : 1;
+    p.Q = n.op != OpKind::AvgPool ? (int)ys[3] : 1;
+    p.ldy = alias_of[n.out] >= 0 ? cp[alias_of[n.out]] : 0;
     L.info.bytes = act_bytes(n.data) + act_bytes(n.out);
-    if (n.op == OpKind::MaxPool) {
+    if (n.op == OpKind::AvgPoolWin) {
+      L.op = Launch::AvgPoolWinBf16;
+      L.info.kind = BYOC_K_AVGPOOL;
+      L.count_include_pad = n.count_include_pad;
+      name(L, "avgpool_win_nhwc");
+    } else if (n.op == OpKind::MaxPool) {
       L.op = bf16 ? Launch::MaxPoolBf16 : Launch::MaxPoolF32;
       L.info.kind = BYOC_K_MAXPOOL;
       name(L, bf16 ? "maxpool_nhwc" : "maxpool_nchw_f32");
@@ -902,15 +988,45 @@ void Planner::plan_node_i8(int ni) {
     e->launches.push_back(L);
     return;
   }
-  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool) {
+  if (n.op == OpKind::Concat) {  // copies of the inputs not written in place
+    const auto& cs = g.values[n.out].shape;
+    int off = 0;
+    for (int a : n.cat) {
+      const int ca = (int)g.values[a].shape[1];
+      if (alias_of[a] != n.out) {
+        Launch C;
+        C.op = Launch::CopyChannels;
+        C.info.kind = BYOC_K_ADD;
+        C.info.node = ni;
+        C.x = loc[a];
+        C.y = slice(n.out, off);
+        C.M = (int)(cs[0] * cs[2] * cs[3]);
+        C.C = ca;
+        C.Cp = cp[a];
+        C.Kp = cp[n.out];
+        C.info.bytes = 2 * act_bytes(a);
+        name(C, "concat_copy");
+        e->launches.push_back(C);
+      }
+      off += ca;
+    }
+    return;
+  }
+  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool || n.op == OpKind::AvgPoolWin) {
     PoolParams& p = L.pool;
     p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3], p.Cp = cp[n.data];
     p.R = n.pool[0], p.S = n.pool[1], p.sh = n.stride[0], p.sw = n.stride[1];
     p.pt = n.pad[0], p.pl = n.pad[1];
-    p.P = n.op == OpKind::MaxPool ? (int)ys[2] : 1;
-    p.Q = n.op == OpKind::MaxPool ? (int)ys[3] : 1;
+    p.P = n.op != OpKind::AvgPool ? (int)ys[2] : 1;
+    p.Q = n.op != OpKind::AvgPool ? (int)ys[3] : 1;
+    p.ldy = alias_of[n.out] >= 0 ? cp[alias_of[n.out]] : 0;
     L.info.bytes = act_bytes(n.data) + act_bytes(n.out);
-    if (n.op == OpKind::MaxPool) {
+    if (n.op == OpKind::AvgPoolWin) {
+      L.op = Launch::AvgPoolWinBf16;
+      L.info.kind = BYOC_K_AVGPOOL;
+      L.count_include_pad = n.count_include_pad;
+      name(L, "avgpool_win_nhwc");
+    } else if (n.op == OpKind::MaxPool) {
       L.op = Launch::MaxPoolI8;
       L.info.kind = BYOC_K_MAXPOOL;
       name(L, "maxpool_nhwc_i8");
@@ -1016,7 +1132,7 @@ struct RunCtx {
   hipStream_t s;
   void* ptr(const Ref& r) const {
     switch (r.kind) {
-      case Ref::Arena: return e->arena + e->bufs[r.idx].off;
+      case Ref::Arena: return e->arena + e->bufs[r.idx].off + r.off;
       case Ref::Input: return const_cast<void*>(in[r.idx]);
       case Ref::Output: return out[r.idx];
       case Ref::Weights: return e->weights + r.off;
@@ -1070,6 +1186,14 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.y = (bf16_t*)c.ptr(L.y);
       return launch_depthwise(p, c.s);
     }
+    case Launch::AvgPoolWinBf16: {
+      PoolParams p = L.pool;
+      p.x = c.ptr(L.x);
+      p.y = c.ptr(L.y);
+      return launch_avgpool_win_nhwc_bf16(p, L.count_include_pad, c.s);
+    }
+    case Launch::CopyChannels:
+      return launch_copy_channels_bf16((const bf16_t*)c.ptr(L.x), L.Cp, (bf16_t*)c.ptr(L.y), L.Kp, L.M, L.C, c.s);
     case Launch::MaxPoolBf16:
     case Launch::AvgPoolBf16:
     case Launch::MaxPoolF32:

@@ -18,14 +18,14 @@ namespace byoc {
 struct Ref {
   enum Kind : uint8_t { None, Arena, Input, Output, Weights } kind = None;
   int idx = -1;       // arena buffer id, input or output number
-  int64_t off = 0;    // byte offset (weights region)
+  int64_t off = 0;    // byte offset (weights region; within the buffer for an arena slice)
 };
 
 struct Launch {
   enum Op {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
     AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows,
-    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8
+    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;
@@ -46,6 +46,7 @@ struct Launch {
   int act = 0;
   float alpha = 0.f;  // leaky ReLU slope
   bool src_bf16 = false, dst_bf16 = false;
+  bool count_include_pad = false;  // windowed average pool
   int N = 0, C = 0, H = 0, W = 0, Cp = 0, M = 0, K = 0, Kp = 0;
 };
 

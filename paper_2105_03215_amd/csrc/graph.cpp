@@ -128,6 +128,14 @@ bool split_composite(const std::string& name, CompositeName* c) {
     c->op = OpKind::AvgPool;
     return true;
   }
+  if (name == "avg_pool2d") {
+    c->op = OpKind::AvgPoolWin;
+    return true;
+  }
+  if (name == "concatenate") {
+    c->op = OpKind::Concat;
+    return true;
+  }
   std::vector<std::string> parts;
   std::string cur;
   for (char ch : name) {
@@ -333,8 +341,10 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
       case OpKind::Conv:
       case OpKind::Dense: want = 2 + (n.has_bias ? 1 : 0) + (n.has_add ? 1 : 0); break;
       case OpKind::MaxPool:
-      case OpKind::AvgPool: want = 1; break;
+      case OpKind::AvgPool:
+      case OpKind::AvgPoolWin: want = 1; break;
       case OpKind::Add: want = 2; break;
+      case OpKind::Concat: want = args.empty() ? 1 : args.size(); break;  // one or more
     }
     if (args.size() != want)
       return perr(where + ": expects " + std::to_string(want) + " inputs, got " +
@@ -356,6 +366,8 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
       if (n.has_add) n.residual = args[k++];
     } else if (n.op == OpKind::Add) {
       n.other = args[1];
+    } else if (n.op == OpKind::Concat) {
+      n.cat = args;
     }
     const auto& xs = shp(n.data);
     if (n.act == Act::Leaky && attrs && attrs->get("alpha")) {
@@ -433,14 +445,57 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
     } else if (n.op == OpKind::AvgPool) {
       if (xs.size() != 4) return serr(where + ": data must be 4-D NCHW, got " + shape_str(xs));
       oshape = {xs[0], xs[1]};
+    } else if (n.op == OpKind::AvgPoolWin) {
+      if (xs.size() != 4) return serr(where + ": data must be 4-D NCHW, got " + shape_str(xs));
+      if (!attrs || !attrs->get("pool_size")) return perr(where + ": attrs.pool_size missing");
+      Status st = attr_pair(attrs, "pool_size", where, 1, 1, 1, n.pool);
+      if (!st.ok()) return st;
+      st = attr_pair(attrs, "strides", where, 1, 1, 1, n.stride);
+      if (!st.ok()) return st;
+      st = attr_padding(attrs, where, n.pad);
+      if (!st.ok()) return st;
+      if (n.pad[0] >= n.pool[0] || n.pad[2] >= n.pool[0] || n.pad[1] >= n.pool[1] || n.pad[3] >= n.pool[1])
+        return uerr(where + ": padding must be smaller than the pool window");
+      if (const JsonValue* ci = attrs->get("count_include_pad")) {
+        if (ci->kind != JsonValue::Bool) return perr(where + ": attrs.count_include_pad must be a boolean");
+        n.count_include_pad = ci->b;
+      }
+      int64_t H = xs[2], W = xs[3];
+      if (H + n.pad[0] + n.pad[2] < n.pool[0] || W + n.pad[1] + n.pad[3] < n.pool[1])
+        return serr(where + ": window larger than the padded input");
+      oshape = {xs[0], xs[1], (H + n.pad[0] + n.pad[2] - n.pool[0]) / n.stride[0] + 1,
+                (W + n.pad[1] + n.pad[3] - n.pool[1]) / n.stride[1] + 1};
+    } else if (n.op == OpKind::Concat) {
+      if (attrs && attrs->get("axis")) {
+        const JsonValue* ax = attrs->get("axis");
+        if (ax->kind != JsonValue::Number || !ax->is_integer || ax->inum != 1)
+          return uerr(where + ": concatenation along an axis other than 1 (channels)");
+      }
+      int64_t ctot = 0;
+      for (int a : n.cat) {
+        const auto& s = shp(a);
+        if (s.size() != 4 || s[0] != xs[0] || s[2] != xs[2] || s[3] != xs[3])
+          return serr(where + ": input '" + g.values[a].name + "' " + shape_str(s) +
+                      " does not match the batch and image of " + shape_str(xs));
+        ctot += s[1];
+      }
+      oshape = {xs[0], ctot, xs[2], xs[3]};
     } else {
       if (shp(n.other) != xs)
         return serr(where + ": operand shapes " + shape_str(xs) + " and " + shape_str(shp(n.other)) +
                     " differ");
       oshape = xs;
     }
-    if ((n.op == OpKind::MaxPool || n.op == OpKind::AvgPool) && n.act != Act::None)
-      return uerr(where + ": activation on a pool");
+    if ((n.op == OpKind::MaxPool || n.op == OpKind::AvgPool || n.op == OpKind::AvgPoolWin ||
+         n.op == OpKind::Concat) && n.act != Act::None)
+      return uerr(where + ": activation on a pool or a concatenation");
+    if ((n.op == OpKind::AvgPoolWin || n.op == OpKind::Concat) && out_dtype != DType::BF16)
+      return uerr(where + ": " + n.composite + " only in bf16 graphs");
+    if (n.op == OpKind::Concat)
+      for (int a : n.cat)
+        if (shp(a)[1] % 8 != 0)
+          return uerr(where + ": input '" + g.values[a].name + "' has " + std::to_string(shp(a)[1]) +
+                      " channels (concatenated inputs need a multiple of 8)");
     if (n.residual >= 0 && shp(n.residual) != oshape)
       return serr(where + ": residual shape " + shape_str(shp(n.residual)) + " != output shape " +
                   shape_str(oshape));

@@ -28,7 +28,8 @@ struct Status {
 // affine scale and zero point per tensor); never an external dtype.
 enum class DType { F32 = BYOC_F32, BF16 = BYOC_BF16, I8 = 2 };
 enum class Act { None = 0, Relu = 1, Relu6 = 2, Gelu = 3, Leaky = 4 };
-enum class OpKind { Conv, Dense, MaxPool, AvgPool, Add };
+// AvgPool: global average pool; AvgPoolWin: windowed average pool.
+enum class OpKind { Conv, Dense, MaxPool, AvgPool, Add, AvgPoolWin, Concat };
 
 // A named tensor of the graph: a subgraph input, a constant or a node output.
 struct Value {
@@ -58,6 +59,8 @@ struct Node {
   int pool[2] = {1, 1};
   int groups = 1;
   bool depthwise = false;
+  bool count_include_pad = false;  // AvgPoolWin
+  std::vector<int> cat;            // Concat: the joined values, in channel order
   int64_t macs = 0;
 };
 

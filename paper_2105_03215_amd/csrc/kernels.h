@@ -139,10 +139,19 @@ struct PoolParams {
   const void* x;
   void* y;
   int N, C, H, W, Cp, P, Q, R, S, sh, sw, pt, pl;
+  int ldy;  // NHWC bf16 kernels: output pixel stride in elements (0: Cp), e.g. a channel slice of a concatenation
 };
 hipError_t launch_maxpool_nhwc_bf16(const PoolParams& p, hipStream_t s);
 hipError_t launch_avgpool_nhwc_bf16(const PoolParams& p, hipStream_t s);  // y [N][Cp]
 hipError_t launch_maxpool_nchw_f32(const PoolParams& p, hipStream_t s);
+// Windowed average pool NHWC bf16 (fp32 sum of the window's taps inside the
+// image, divided by their count, or by R*S with count_include_pad).
+hipError_t launch_avgpool_win_nhwc_bf16(const PoolParams& p, bool count_include_pad, hipStream_t s);
+// Copies [pixels][C] bf16 (source pixel stride src_ld) into a channel slice
+// of a concatenation (destination pixel stride dst_ld); C, src_ld, dst_ld
+// multiples of 8 and 16-byte aligned bases.
+hipError_t launch_copy_channels_bf16(const bf16_t* src, int src_ld, bf16_t* dst, int dst_ld, int64_t pixels, int C,
+                                     hipStream_t s);
 hipError_t launch_avgpool_nchw_f32(const PoolParams& p, hipStream_t s);   // y [N][C]
 
 // y = act(a + b) over n elements (n multiple of 8 for bf16).

@@ -88,7 +88,56 @@ __global__ __launch_bounds__(kThreads) void maxpool_nhwc_kernel(PoolParams p) {
       for (int i = 0; i < 8; ++i) m[i] = fmaxf(m[i], v[i]);
     }
   }
-  *(uint4*)((bf16_t*)p.y + (((size_t)n * p.P + pp) * p.Q + q) * p.Cp + g * 8) = pack8(m);
+  *(uint4*)((bf16_t*)p.y + (((size_t)n * p.P + pp) * p.Q + q) * (p.ldy ? p.ldy : p.Cp) + g * 8) = pack8(m);
+}
+
+// Windowed average pool, NHWC bf16, 8 channels per thread: fp32 sum of the
+// taps inside the image, divided by their count (or by the full window).
+__global__ __launch_bounds__(kThreads) void avgpool_win_nhwc_kernel(PoolParams p, int incl) {
+  const int G = p.Cp / 8;
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t total = (int64_t)p.N * p.P * p.Q * G;
+  if (idx >= total) return;
+  const int g = (int)(idx % G);
+  int64_t t = idx / G;
+  const int q = (int)(t % p.Q);
+  t /= p.Q;
+  const int pp = (int)(t % p.P);
+  const int n = (int)(t / p.P);
+  const bf16_t* x = (const bf16_t*)p.x + (size_t)n * p.H * p.W * p.Cp + g * 8;
+  float m[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m[i] = 0.0f;
+  int cnt = 0;
+  const int ih0 = pp * p.sh - p.pt;
+  const int iw0 = q * p.sw - p.pl;
+  for (int r = 0; r < p.R; ++r) {
+    const int ih = ih0 + r;
+    if ((unsigned)ih >= (unsigned)p.H) continue;
+    for (int s = 0; s < p.S; ++s) {
+      const int iw = iw0 + s;
+      if ((unsigned)iw >= (unsigned)p.W) continue;
+      float v[8];
+      unpack8(*(const uint4*)(x + ((size_t)ih * p.W + iw) * p.Cp), v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) m[i] += v[i];
+      ++cnt;
+    }
+  }
+  const float d = (float)(incl ? p.R * p.S : cnt);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m[i] = m[i] / d;
+  *(uint4*)((bf16_t*)p.y + (((size_t)n * p.P + pp) * p.Q + q) * (p.ldy ? p.ldy : p.Cp) + g * 8) = pack8(m);
+}
+
+// 8 channels (16 bytes) per thread.
+__global__ __launch_bounds__(kThreads) void copy_channels_kernel(const bf16_t* src, int src_ld, bf16_t* dst,
+                                                                 int dst_ld, int64_t pixels, int G) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= pixels * G) return;
+  const int g = (int)(idx % G);
+  const int64_t px = idx / G;
+  *(uint4*)(dst + px * dst_ld + g * 8) = *(const uint4*)(src + px * src_ld + g * 8);
 }
 
 // Global average pool NHWC bf16 -> [N][Cp] bf16.  Workgroup = one image x
@@ -338,6 +387,21 @@ hipError_t launch_depthwise(const DwParams& p, hipStream_t s) {
 hipError_t launch_maxpool_nhwc_bf16(const PoolParams& p, hipStream_t s) {
   const int64_t n = (int64_t)p.N * p.P * p.Q * (p.Cp / 8);
   maxpool_nhwc_kernel<<<grid_for(n), kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool_win_nhwc_bf16(const PoolParams& p, bool count_include_pad, hipStream_t s) {
+  if (p.Cp % 8 != 0 || (p.ldy && p.ldy % 8 != 0)) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)p.N * p.P * p.Q * (p.Cp / 8);
+  avgpool_win_nhwc_kernel<<<grid_for(n), kThreads, 0, s>>>(p, count_include_pad ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_channels_bf16(const bf16_t* src, int src_ld, bf16_t* dst, int dst_ld, int64_t pixels, int C,
+                                     hipStream_t s) {
+  if (C % 8 != 0 || src_ld % 8 != 0 || dst_ld % 8 != 0 || C > src_ld || C > dst_ld) return hipErrorInvalidValue;
+  if (pixels * (C / 8) == 0) return hipSuccess;
+  copy_channels_kernel<<<grid_for(pixels * (C / 8)), kThreads, 0, s>>>(src, src_ld, dst, dst_ld, pixels, C / 8);
   return hipGetLastError();
 }
 

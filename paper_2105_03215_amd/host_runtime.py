@@ -70,6 +70,14 @@ def _host_op(node, args):
         pt, pl, pb, pr = _pads(a.get("padding", [0, 0, 0, 0]))
         x = F.pad(x, (pl, pr, pt, pb), value=-math.inf)
         return F.max_pool2d(x, tuple(a["pool_size"]), stride=tuple(a["strides"]))
+    if op == "nn.avg_pool2d":
+        pt, pl, pb, pr = _pads(a.get("padding", [0, 0, 0, 0]))
+        if (pt, pl) != (pb, pr):
+            raise ValueError("nn.avg_pool2d on the host: asymmetric padding")
+        return F.avg_pool2d(x, tuple(a["pool_size"]), stride=tuple(a.get("strides", [1, 1])), padding=(pt, pl),
+                            count_include_pad=bool(a.get("count_include_pad", False)))
+    if op == "concatenate":
+        return torch.cat(list(args), dim=1)
     if op == "nn.global_avg_pool2d":
         return x.mean(dim=(2, 3), keepdim=True)
     if op == "nn.batch_flatten":

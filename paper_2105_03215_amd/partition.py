@@ -7,8 +7,9 @@ host part of the graph that calls them.
 
 * Operator-level graph (``Graph``): nodes named after the operators of the
   paper's high-level IR (``nn.conv2d``, ``nn.bias_add``, ``add``,
-  ``nn.relu``, ``clip``, ``nn.dense``, ``nn.max_pool2d``,
-  ``nn.global_avg_pool2d``, ``nn.batch_flatten``, ...), each with its
+  ``nn.relu``, ``clip``, ``nn.leaky_relu``, ``nn.dense``, ``nn.max_pool2d``,
+  ``nn.avg_pool2d``, ``concatenate``, ``nn.global_avg_pool2d``,
+  ``nn.batch_flatten``, ...), each with its
   attributes, inferred shape and dtype; weights are constant nodes.
 * Pattern-based grouping (Sec. 3.1.1): patterns built from ``wildcard()``,
   ``is_op(name)(*args)``, ``is_constant()``, ``.optional(fn)`` and ``|``;
@@ -100,6 +101,17 @@ def _infer(op, ins, attrs):
         sh, sw = attrs["strides"]
         pt, pl, pb, pr = _pads(attrs.get("padding", [0, 0, 0, 0]))
         return (n, c, _conv_out(h, r, sh, pt, pb), _conv_out(w, s, sw, pl, pr))
+    if op == "nn.avg_pool2d":
+        n, c, h, w = ins[0]
+        r, s = attrs["pool_size"]
+        sh, sw = attrs.get("strides", [1, 1])
+        pt, pl, pb, pr = _pads(attrs.get("padding", [0, 0, 0, 0]))
+        return (n, c, _conv_out(h, r, sh, pt, pb), _conv_out(w, s, sw, pl, pr))
+    if op == "concatenate":
+        if attrs.get("axis", 1) != 1 or any(len(x) != 4 or (x[0], x[2], x[3]) != (ins[0][0], ins[0][2], ins[0][3])
+                                            for x in ins):
+            raise ValueError("concatenate: channel-axis join of NCHW tensors of one batch and image, got %s" % (ins,))
+        return (ins[0][0], sum(x[1] for x in ins), ins[0][2], ins[0][3])
     if op == "nn.global_avg_pool2d":
         n, c = ins[0][:2]
         return (n, c, 1, 1)
@@ -226,6 +238,24 @@ class OpPattern(Pattern):
         return True
 
 
+class VariadicOpPattern(OpPattern):
+    """An operator over any number (at least one) of arguments, each bound
+    in order as a composite argument (e.g. ``concatenate``)."""
+
+    def __init__(self, op):
+        super().__init__(op, [])
+
+    def match(self, g, nid, env):
+        n = g.nodes[nid]
+        if n.op != self.op or not n.inputs:
+            return False
+        for i in n.inputs:
+            WildcardPattern().match(g, i, env)
+        env.setdefault("ops", []).append(nid)
+        env.setdefault("by_op", {}).setdefault(self.op, []).append(nid)
+        return True
+
+
 class AltPattern(Pattern):
     def __init__(self, first, second):
         self.first = first
@@ -292,6 +322,14 @@ def max_pool_pattern():
     return is_op("nn.max_pool2d")(wildcard("data"))
 
 
+def avg_pool_pattern():
+    return is_op("nn.avg_pool2d")(wildcard("data"))
+
+
+def concat_pattern():
+    return VariadicOpPattern("concatenate")
+
+
 def global_avg_pool_pattern():
     return is_op("nn.batch_flatten")(is_op("nn.global_avg_pool2d")(wildcard("data")))
 
@@ -333,6 +371,8 @@ PATTERN_TABLE = [
     (dense_pattern, _gemm_name("dense")),
     (global_avg_pool_pattern, lambda g, env: "global_avg_pool2d"),
     (max_pool_pattern, lambda g, env: "max_pool2d"),
+    (avg_pool_pattern, lambda g, env: "avg_pool2d"),
+    (concat_pattern, lambda g, env: "concatenate"),
     (add_pattern, lambda g, env: "add" + _act_suffix(g, env)),
 ]
 
@@ -341,14 +381,17 @@ class Composite:
     """A matched operator sequence: its member operators, its root (whose
     result is the composite's), and its arguments by role."""
 
-    def __init__(self, name, members, root, roles):
+    def __init__(self, name, members, root, roles, arglist=None):
         self.name = name
         self.members = sorted(members)
         self.root = root
         self.roles = roles  # data, weight, bias, residual -> node id
+        self.arglist = arglist  # variadic composites: every argument in order
 
     @property
     def args(self):
+        if self.arglist is not None:
+            return list(self.arglist)
         return [self.roles[r] for r in ("data", "weight", "bias", "residual") if r in self.roles]
 
 
@@ -379,7 +422,11 @@ def merge_composites(g, table=None):
                            for m in members)
             if not inner_ok:
                 continue
-            comp = Composite(namer(g, env), members, n.id, dict(env.get("roles", {})))
+            name = namer(g, env)
+            roles = dict(env.get("roles", {}))
+            if name == "concatenate":
+                roles["data"] = env["args"][0]
+            comp = Composite(name, members, n.id, roles, list(env["args"]) if name == "concatenate" else None)
             if comp.name.startswith(("conv2d", "dense")) and "weight" not in comp.roles:
                 continue
             comps[n.id] = comp
@@ -440,6 +487,18 @@ def _pool_supported(g, comp):
 @register_op_attr("global_avg_pool2d", TARGET)
 def _gap_supported(g, comp):
     return g.nodes[comp.roles["data"]].dtype in _DTYPES
+
+
+@register_op_attr("avg_pool2d", TARGET)
+def _avg_pool_supported(g, comp):
+    x = g.nodes[comp.roles["data"]]
+    return x.dtype == "bf16" and len(x.shape) == 4
+
+
+@register_op_attr("concatenate", TARGET)
+def _concat_supported(g, comp):
+    xs = [g.nodes[a] for a in comp.args]
+    return all(x.dtype == "bf16" and len(x.shape) == 4 and x.shape[1] % 8 == 0 for x in xs)
 
 
 @register_op_attr("add", TARGET)
@@ -683,6 +742,13 @@ def _serialize(g, name, us, used_outside):
             pool = g.nodes[comp.root]
             attrs = {"pool_size": list(pool.attrs["pool_size"]), "strides": list(pool.attrs["strides"]),
                      "padding": _pads(pool.attrs.get("padding", [0, 0, 0, 0]))}
+        elif comp.name == "avg_pool2d":
+            pool = g.nodes[comp.root]
+            attrs = {"pool_size": list(pool.attrs["pool_size"]), "strides": list(pool.attrs.get("strides", [1, 1])),
+                     "padding": _pads(pool.attrs.get("padding", [0, 0, 0, 0])),
+                     "count_include_pad": bool(pool.attrs.get("count_include_pad", False))}
+        elif comp.name == "concatenate":
+            attrs = {"axis": 1}
         oname = "n%d" % len(nodes_json)
         nodes_json.append({"name": oname, "composite": comp.name, "inputs": args, "attrs": attrs,
                            "out_dtype": dtype})
@@ -830,6 +896,14 @@ def lower_subgraph(graph, consts):
             act = None
         elif comp == "global_avg_pool2d":
             y = g.call("nn.batch_flatten", [g.call("nn.global_avg_pool2d", ins)])
+            act = None
+        elif comp == "avg_pool2d":
+            y = g.call("nn.avg_pool2d", ins, pool_size=list(attrs["pool_size"]), strides=list(attrs["strides"]),
+                       padding=_pads(attrs.get("padding", [0] * 4)),
+                       count_include_pad=bool(attrs.get("count_include_pad", False)))
+            act = None
+        elif comp == "concatenate":
+            y = g.call("concatenate", ins, axis=1)
             act = None
         elif comp.startswith("add"):
             y = g.call("add", ins)

@@ -32,6 +32,7 @@ CONFIG_IDS = {
     "bert_ffn": 4,
     "vgg19": 5,
     "darknet53": 6,
+    "inception_v3": 7,
 }
 
 _BN_EPS = 1e-5
@@ -162,17 +163,19 @@ class GraphBuilder:
 
     def conv(self, x, k, r, stride=1, pad=None, groups=1, act="relu", bias=True, residual=None,
              bn=True, gamma=1.0, w_std=None, b_std=None, name=None, alpha=0.1):
-        """Conv composite with He-normal weights and an optional folded BN."""
+        """Conv composite with He-normal weights and an optional folded BN.
+        ``r`` is the kernel size, or (rows, columns) for a rectangular one."""
         n, c, h, w = self.shapes[x]
-        pad = (r // 2) if pad is None else pad
+        r, sk = (r, r) if isinstance(r, int) else tuple(r)
+        pad = [r // 2, sk // 2, r // 2, sk // 2] if pad is None else pad
         pads = [pad] * 4 if isinstance(pad, int) else list(pad)
         strides = [stride, stride] if isinstance(stride, int) else list(stride)
         cg = c // groups
-        fan_in = cg * r * r
+        fan_in = cg * r * sk
         tid = self.next_tensor
         self.next_tensor += 2
         std = w_std if w_std is not None else math.sqrt(2.0 / fan_in)
-        wt = self.rng(tid).normal(0.0, std, size=(k, cg, r, r))
+        wt = self.rng(tid).normal(0.0, std, size=(k, cg, r, sk))
         m2_in = self.m2[x]
         if bn:
             var_pred = fan_in * std * std * m2_in
@@ -202,11 +205,13 @@ class GraphBuilder:
             self.mu[name or "n%d" % len(self.nodes)] = (1.0 - alpha) * math.sqrt(m2 / (2.0 * math.pi))
             m2 = 0.5 * (1.0 + alpha * alpha) * m2
         elif act:
+            if act in ("relu", "relu6"):
+                self.mu[name] = math.sqrt(m2 / (2.0 * math.pi))
             m2 = 0.5 * m2
         if act:
             comp += "_" + act
         p = (h + pads[0] + pads[2] - r) // strides[0] + 1
-        q = (w + pads[1] + pads[3] - r) // strides[1] + 1
+        q = (w + pads[1] + pads[3] - sk) // strides[1] + 1
         attrs = {"strides": strides, "padding": pads, "dilation": [1, 1], "groups": groups}
         if act == "leaky":
             attrs["alpha"] = alpha
@@ -214,7 +219,7 @@ class GraphBuilder:
                            "out_dtype": self.dtype})
         self.shapes[name] = [n, k, p, q]
         self.m2[name] = m2
-        macs = n * k * p * q * cg * r * r
+        macs = n * k * p * q * cg * r * sk
         self.macs += macs
         self.conv_macs += macs
         return name
@@ -245,7 +250,7 @@ class GraphBuilder:
         self.macs += m * n_out * kin
         return name
 
-    def max_pool(self, x, size=3, stride=2, pad=1, name=None):
+    def max_pool(self, x, size=3, stride=2, pad=1, name=None, gain=None):
         n, c, h, w = self.shapes[x]
         name = name or "n%d" % len(self.nodes)
         self.nodes.append({"name": name, "composite": "max_pool2d", "inputs": [x],
@@ -255,7 +260,37 @@ class GraphBuilder:
         p = (h + 2 * pad - size) // stride + 1
         q = (w + 2 * pad - size) // stride + 1
         self.shapes[name] = [n, c, p, q]
-        self.m2[name] = (_MAXPOOL_GAIN_2X2 if size == 2 else _MAXPOOL_GAIN) * self.m2[x]
+        if gain is None:
+            gain = _MAXPOOL_GAIN_2X2 if size == 2 else _MAXPOOL_GAIN
+        self.m2[name] = gain * self.m2[x]
+        return name
+
+    def avg_pool(self, x, size=3, stride=1, pad=1, name=None):
+        """Windowed average pool (padding not counted in the divisor)."""
+        n, c, h, w = self.shapes[x]
+        name = name or "n%d" % len(self.nodes)
+        self.nodes.append({"name": name, "composite": "avg_pool2d", "inputs": [x],
+                           "attrs": {"pool_size": [size, size], "strides": [stride, stride],
+                                     "padding": [pad] * 4, "count_include_pad": False},
+                           "out_dtype": self.dtype})
+        self.shapes[name] = [n, c, (h + 2 * pad - size) // stride + 1, (w + 2 * pad - size) // stride + 1]
+        mu = self.mu.get(x, 0.0)
+        # the window mean keeps the mean and averages the rest over
+        # correlated neighbours (taken to keep half of it)
+        self.m2[name] = mu * mu + 0.5 * (self.m2[x] - mu * mu)
+        self.mu[name] = mu
+        return name
+
+    def concat(self, xs, name=None):
+        """Channel concatenation of NCHW tensors of one batch and image."""
+        name = name or "n%d" % len(self.nodes)
+        self.nodes.append({"name": name, "composite": "concatenate", "inputs": list(xs), "attrs": {"axis": 1},
+                           "out_dtype": self.dtype})
+        n, _, h, w = self.shapes[xs[0]]
+        cs = [self.shapes[x][1] for x in xs]
+        self.shapes[name] = [n, sum(cs), h, w]
+        self.m2[name] = sum(c * self.m2[x] for c, x in zip(cs, xs)) / sum(cs)
+        self.mu[name] = sum(c * self.mu.get(x, 0.0) for c, x in zip(cs, xs)) / sum(cs)
         return name
 
     def global_avg_pool(self, x, name=None):
@@ -466,9 +501,98 @@ def darknet53(n=1, hw=256, input_dtype="bf16", num_classes=1000, alpha=0.1):
     return g.finish({"batch": n})
 
 
+# mean-square gain of Inception's unpadded 3x3 stride-2 max pools over
+# folded-normalized ReLU maps (measured on the float network with these
+# weights: 1.5-2.9; the ResNet stem pool's 5.1 would shrink every later layer)
+_INCEPTION_MAXPOOL_GAIN = 2.0
+
+
+def _inception_a(g, x, pool_features, p):
+    b1 = g.conv(x, 64, 1, name=p + ".b1")
+    b5 = g.conv(g.conv(x, 48, 1, name=p + ".b5a"), 64, 5, name=p + ".b5b")
+    b3 = g.conv(g.conv(g.conv(x, 64, 1, name=p + ".b3a"), 96, 3, name=p + ".b3b"), 96, 3, name=p + ".b3c")
+    bp = g.conv(g.avg_pool(x, 3, 1, 1, name=p + ".pool"), pool_features, 1, name=p + ".bp")
+    return g.concat([b1, b5, b3, bp], name=p)
+
+
+def _inception_b(g, x, p):
+    b3 = g.conv(x, 384, 3, stride=2, pad=0, name=p + ".b3")
+    bd = g.conv(g.conv(g.conv(x, 64, 1, name=p + ".bda"), 96, 3, name=p + ".bdb"), 96, 3, stride=2, pad=0,
+                name=p + ".bdc")
+    bp = g.max_pool(x, 3, 2, 0, name=p + ".pool", gain=_INCEPTION_MAXPOOL_GAIN)
+    return g.concat([b3, bd, bp], name=p)
+
+
+def _inception_c(g, x, c7, p):
+    b1 = g.conv(x, 192, 1, name=p + ".b1")
+    b7 = g.conv(x, c7, 1, name=p + ".b7a")
+    b7 = g.conv(b7, c7, (1, 7), name=p + ".b7b")
+    b7 = g.conv(b7, 192, (7, 1), name=p + ".b7c")
+    bd = g.conv(x, c7, 1, name=p + ".bda")
+    for i, (ks, k) in enumerate([((7, 1), c7), ((1, 7), c7), ((7, 1), c7), ((1, 7), 192)]):
+        bd = g.conv(bd, k, ks, name=p + ".bd%d" % i)
+    bp = g.conv(g.avg_pool(x, 3, 1, 1, name=p + ".pool"), 192, 1, name=p + ".bp")
+    return g.concat([b1, b7, bd, bp], name=p)
+
+
+def _inception_d(g, x, p):
+    b3 = g.conv(g.conv(x, 192, 1, name=p + ".b3a"), 320, 3, stride=2, pad=0, name=p + ".b3b")
+    b7 = g.conv(x, 192, 1, name=p + ".b7a")
+    b7 = g.conv(b7, 192, (1, 7), name=p + ".b7b")
+    b7 = g.conv(b7, 192, (7, 1), name=p + ".b7c")
+    b7 = g.conv(b7, 192, 3, stride=2, pad=0, name=p + ".b7d")
+    bp = g.max_pool(x, 3, 2, 0, name=p + ".pool", gain=_INCEPTION_MAXPOOL_GAIN)
+    return g.concat([b3, b7, bp], name=p)
+
+
+def _inception_e(g, x, p):
+    b1 = g.conv(x, 320, 1, name=p + ".b1")
+    b3 = g.conv(x, 384, 1, name=p + ".b3a")
+    b3a = g.conv(b3, 384, (1, 3), name=p + ".b3b1")
+    b3b = g.conv(b3, 384, (3, 1), name=p + ".b3b2")
+    bd = g.conv(g.conv(x, 448, 1, name=p + ".bda"), 384, 3, name=p + ".bdb")
+    bda = g.conv(bd, 384, (1, 3), name=p + ".bdc1")
+    bdb = g.conv(bd, 384, (3, 1), name=p + ".bdc2")
+    bp = g.conv(g.avg_pool(x, 3, 1, 1, name=p + ".pool"), 192, 1, name=p + ".bp")
+    # the branches' inner concatenations of the two split convs are part of
+    # the block's one concatenation (the same channel order)
+    return g.concat([b1, b3a, b3b, bda, bdb, bp], name=p)
+
+
+def inception_v3(n=1, hw=299, input_dtype="bf16", num_classes=1000):
+    """Inception V3-shaped network (a fully offloaded row of the paper's
+    Table 1), inference form: the stem of 3x3 convs and max pools, three
+    Inception-A blocks (35x35), the grid reduction B, four Inception-C blocks
+    with factorized 1x7 / 7x1 convs (17x17), reduction D and two Inception-E
+    blocks (8x8), global average pool and a dense classifier.  Every conv has
+    folded batch norm and ReLU; the pool branches average 3x3 windows
+    (stride 1, padding not counted).  Input 299x299."""
+    g = GraphBuilder("inception_v3", CONFIG_IDS["inception_v3"])
+    x = g.input("x", [n, 3, hw, hw], "uniform", dtype=input_dtype)
+    y = g.conv(x, 32, 3, stride=2, pad=0, name="stem1")
+    y = g.conv(y, 32, 3, pad=0, name="stem2")
+    y = g.conv(y, 64, 3, name="stem3")
+    y = g.max_pool(y, 3, 2, 0, name="stem_pool1", gain=_INCEPTION_MAXPOOL_GAIN)
+    y = g.conv(y, 80, 1, name="stem4")
+    y = g.conv(y, 192, 3, pad=0, name="stem5")
+    y = g.max_pool(y, 3, 2, 0, name="stem_pool2", gain=_INCEPTION_MAXPOOL_GAIN)
+    for i, pf in enumerate((32, 64, 64)):
+        y = _inception_a(g, y, pf, "mixed5%s" % "bcd"[i])
+    y = _inception_b(g, y, "mixed6a")
+    for i, c7 in enumerate((128, 160, 160, 192)):
+        y = _inception_c(g, y, c7, "mixed6%s" % "bcde"[i])
+    y = _inception_d(g, y, "mixed7a")
+    y = _inception_e(g, y, "mixed7b")
+    y = _inception_e(g, y, "mixed7c")
+    y = g.global_avg_pool(y, name="pool")
+    y = g.dense(y, num_classes, name="fc")
+    g.output(y)
+    return g.finish({"batch": n})
+
+
 def build(name, **kw):
     """Build a workload by name: conv_f32, resnet18_block, resnet50_v1,
-    resnet50_v1b, mobilenet_v2, bert_ffn, vgg19, darknet53."""
+    resnet50_v1b, mobilenet_v2, bert_ffn, vgg19, darknet53, inception_v3."""
     if name == "conv_f32":
         return conv_f32(**kw)
     if name == "resnet18_block":
@@ -485,4 +609,6 @@ def build(name, **kw):
         return vgg19(**kw)
     if name == "darknet53":
         return darknet53(**kw)
+    if name == "inception_v3":
+        return inception_v3(**kw)
     raise ValueError("unknown workload %r" % name)

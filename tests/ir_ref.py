@@ -44,6 +44,11 @@ def op_ref(node, args):
         return e / e.sum(axis=a.get("axis", -1), keepdims=True)
     if op == "nn.max_pool2d":
         return ops.max_pool2d(x, tuple(a["pool_size"]), tuple(a["strides"]), tuple(a.get("padding", [0, 0, 0, 0])))
+    if op == "nn.avg_pool2d":
+        return ops.avg_pool2d(x, tuple(a["pool_size"]), tuple(a.get("strides", [1, 1])),
+                              tuple(a.get("padding", [0, 0, 0, 0])), bool(a.get("count_include_pad", False)))
+    if op == "concatenate":
+        return ops.concatenate(args, axis=1)
     if op == "nn.global_avg_pool2d":
         y = ops.global_avg_pool2d(x)
         return y.reshape(y.shape[0], y.shape[1], 1, 1)

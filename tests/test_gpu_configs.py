@@ -197,6 +197,28 @@ def test_darknet53_bs32_sampled():
     assert np.all(np.isfinite(g))
 
 
+def test_inception_v3_bs1():
+    announce("inception_v3 bs1 299x299")
+    wl = workloads.build("inception_v3", n=1)
+    g = _gpu(wl)[0]
+    o = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    err = rel_err(g, o)
+    print("inception_v3 bs1 err %.3e" % err)
+    assert err <= BF16_TOL
+
+
+def test_inception_v3_bs32_sampled():
+    announce("inception_v3 bs32 299x299 sampled images 0 and 31")
+    wl = workloads.build("inception_v3", n=32)
+    g = _gpu(wl)[0]
+    rows = [0, 31]
+    o = oracle.run_graph(_sample_graph(wl, 2), wl.consts, _sample_inputs(wl, rows), mode="bf16io")[0]
+    err = rel_err(g[rows], o)
+    print("inception_v3 bs32 err %.3e" % err)
+    assert err <= BF16_TOL
+    assert np.all(np.isfinite(g))
+
+
 def test_bert_ffn_layers_teacher_forced():
     """All 24 dense composites at full size (1024 tokens), each recomputed by
     the oracle on 64 sampled token rows from the GPU's own layer input."""

@@ -330,3 +330,57 @@ def test_leaky_slopes_depthwise_add_and_f32():
     s = g.add(a, x, act="leaky", name="s")
     g.output(s)
     _check_f32(g.finish(), "fp32 leaky conv and add")
+
+
+AVGPOOL_CASES = [
+    # name, (n, c, h, w), size, stride, pad, count_include_pad
+    ("3x3_s1_p1", (2, 64, 17, 17), 3, 1, 1, False),
+    ("3x3_s1_p1_incl", (1, 40, 9, 7), 3, 1, 1, True),
+    ("3x3_s2_p0", (2, 24, 15, 16), 3, 2, 0, False),
+]
+
+
+@pytest.mark.parametrize("case", AVGPOOL_CASES, ids=[c[0] for c in AVGPOOL_CASES])
+def test_avg_pool_window(case):
+    name, shape, size, stride, pad, incl = case
+    g = GraphBuilder("op_avgpool_" + name, 2000 + AVGPOOL_CASES.index(case))
+    x = g.input("x", list(shape), "normal")
+    y = g.avg_pool(x, size, stride, pad, name="y")
+    g.nodes[-1]["attrs"]["count_include_pad"] = incl
+    g.output(y)
+    _check_bf16(g.finish(), "avg pool " + name)
+
+
+def test_concat_in_place_and_copied():
+    """A concatenation of conv, max-pool and avg-pool outputs (written in
+    place into their channel slices), a value also read elsewhere and a
+    graph input (copied in), with rectangular 1x7 / 7x1 / 1x3 kernels; the
+    concatenation feeds a conv and is a graph output."""
+    g = GraphBuilder("op_concat", 2100)
+    x = g.input("x", [2, 32, 13, 11], "uniform")
+    z = g.input("z", [2, 16, 13, 11], "normal")
+    a = g.conv(x, 24, (1, 7), name="a")
+    b = g.conv(g.conv(x, 16, (7, 1), name="b0"), 40, (1, 3), name="b")
+    m = g.max_pool(x, 3, 1, 1, name="m")
+    p = g.avg_pool(x, 3, 1, 1, name="p")
+    shared = g.conv(x, 8, 1, name="shared")
+    c = g.concat([a, b, m, z, shared, p], name="cat")
+    y = g.conv(c, 48, 3, name="y")
+    u = g.conv(shared, 8, 1, name="u")
+    g.output(y)
+    g.output(c)
+    g.output(u)
+    launches = _check_bf16(g.finish(), "concat in place and copied")
+    names = [l["name"] for l in launches]
+    # z (a graph input) and shared (read twice) are copied; the rest in place
+    assert names.count("concat_copy") == 2, names
+
+
+def test_concat_all_in_place():
+    g = GraphBuilder("op_concat_inplace", 2101)
+    x = g.input("x", [1, 64, 8, 8], "uniform")
+    c = g.concat([g.conv(x, 64, 1, name="a"), g.conv(x, 96, 3, name="b"), g.conv(x, 32, (3, 1), name="c")],
+                 name="cat")
+    g.output(g.conv(c, 16, 1, name="y"))
+    launches = _check_bf16(g.finish(), "concat all in place")
+    assert "concat_copy" not in [l["name"] for l in launches]

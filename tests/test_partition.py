@@ -220,7 +220,8 @@ def test_functions_validate_in_the_executor():
 @pytest.mark.parametrize("name,kw", [("resnet50_v1", {"n": 1, "hw": 64}), ("mobilenet_v2", {"n": 1, "hw": 64}),
                                      ("resnet18_block", {"n": 1, "c": 64, "hw": 14}),
                                      ("bert_ffn", {"batch": 1, "seq": 8, "layers": 3}),
-                                     ("vgg19", {"n": 1, "hw": 32}), ("darknet53", {"n": 1, "hw": 64})])
+                                     ("vgg19", {"n": 1, "hw": 32}), ("darknet53", {"n": 1, "hw": 64}),
+                                     ("inception_v3", {"n": 1, "hw": 75})])
 def test_workload_round_trip(name, kw):
     """The executor's workloads lowered to operators and partitioned with a
     host softmax head come back as one function with the same composites, in

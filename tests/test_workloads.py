@@ -95,9 +95,36 @@ def test_darknet53_structure_and_work():
     assert all(by[a["inputs"][1]]["composite"] == "conv2d_bias_leaky" for a in adds)
 
 
-@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block", "vgg19", "darknet53"])
+def test_inception_v3_structure_and_work():
+    wl = workloads.inception_v3(n=1)
+    comps = [n["composite"] for n in wl.graph["nodes"]]
+    assert comps.count("conv2d_bias_relu") == 94 and comps.count("concatenate") == 11
+    assert comps.count("avg_pool2d") == 9 and comps.count("max_pool2d") == 4
+    # block output channels of the published network, from the node list
+    wshape = {c["name"]: wl.consts[c["index"]].shape for c in wl.graph["constants"]}
+    ch = {"x": 3}
+    for n in wl.graph["nodes"]:
+        if n["composite"].startswith(("conv2d", "dense")):
+            ch[n["name"]] = wshape[n["inputs"][1]][0]
+        elif n["composite"] == "concatenate":
+            ch[n["name"]] = sum(ch[i] for i in n["inputs"])
+        else:
+            ch[n["name"]] = ch[n["inputs"][0]]
+    assert {k: ch[k] for k in ("mixed5b", "mixed5c", "mixed5d", "mixed6a", "mixed6e", "mixed7a", "mixed7b",
+                               "mixed7c")} == {"mixed5b": 256, "mixed5c": 288, "mixed5d": 288, "mixed6a": 768,
+                                               "mixed6e": 768, "mixed7a": 1280, "mixed7b": 2048, "mixed7c": 2048}
+    # 5.71 G multiply-adds per 299x299 image (the usual Inception V3 count)
+    assert abs(wl.macs / 1e9 - 5.713) < 0.01
+    rect = [n for n in wl.graph["nodes"] if n["composite"].startswith("conv2d")
+            and wl.consts[[c["index"] for c in wl.graph["constants"] if c["name"] == n["inputs"][1]][0]].shape[2:]
+            in ((1, 7), (7, 1), (1, 3), (3, 1))]
+    assert len(rect) == 4 * 6 + 2 + 2 * 4
+
+
+@pytest.mark.parametrize("name", ["resnet50_v1", "mobilenet_v2", "resnet18_block", "vgg19", "darknet53",
+                                  "inception_v3"])
 def test_activations_stay_order_one(name):
-    kw = {"vgg19": {"hw": 112}, "darknet53": {"hw": 128}}.get(name, {})
+    kw = {"vgg19": {"hw": 112}, "darknet53": {"hw": 128}, "inception_v3": {"hw": 139}}.get(name, {})
     wl = workloads.build(name, **kw)
     outs, vals = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io", keep=True)
     names = [n["name"] for n in wl.graph["nodes"]]
