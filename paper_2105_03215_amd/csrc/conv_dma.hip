@@ -336,8 +336,8 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
   static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
   float* stage = reinterpret_cast<float*>(gring);
   const ActClamp ac = act_clamp_of(p.act, p.alpha);
-  auto epilogue = [&](auto gelu_tag) {
-    constexpr bool G = decltype(gelu_tag)::value;
+  auto epilogue = [&](auto mode_tag) {
+    constexpr int G = decltype(mode_tag)::value;
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       if (pass > 0) lds_barrier();
@@ -380,10 +380,12 @@ __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams 
       }
     }
   };
-  if (p.act == kActGelu)
-    epilogue(std::true_type{});
+  if (act_mode(p.act) == 1)
+    epilogue(std::integral_constant<int, 1>{});
+  else if (act_mode(p.act) == 0)
+    epilogue(std::integral_constant<int, 0>{});
   else
-    epilogue(std::false_type{});
+    epilogue(std::integral_constant<int, 2>{});
 }
 
 template <int BM, int BN, int WM, int WN, int KG, int NS>

@@ -284,8 +284,8 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   static_assert(BM * kLd * 4 <= (NPB * PSTAGE + NSW * WSTAGE) * 16, "staging tile");
   float* stage = reinterpret_cast<float*>(lds);
   const ActClamp ac = act_clamp_of(p.act, p.alpha);
-  auto epilogue = [&](auto gelu_tag) {
-    constexpr bool G = decltype(gelu_tag)::value;
+  auto epilogue = [&](auto mode_tag) {
+    constexpr int G = decltype(mode_tag)::value;
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       if (pass > 0) lds_barrier();
@@ -321,10 +321,12 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
       }
     }
   };
-  if (p.act == kActGelu)
-    epilogue(std::true_type{});
+  if (act_mode(p.act) == 1)
+    epilogue(std::integral_constant<int, 1>{});
+  else if (act_mode(p.act) == 0)
+    epilogue(std::integral_constant<int, 0>{});
   else
-    epilogue(std::false_type{});
+    epilogue(std::integral_constant<int, 2>{});
 }
 
 // A weight-ring setting `stages` of the launchers: 2 or 3 are rings of

@@ -362,8 +362,8 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
   static_assert(BN % kEC == 0 && BM * kLd * 4 <= (int)sizeof(smem), "staging tile");
   float* stage = reinterpret_cast<float*>(smem);
   const ActClamp ac = act_clamp_of(p.act, p.alpha);
-  auto epilogue = [&](auto gelu_tag) {
-    constexpr bool G = decltype(gelu_tag)::value;
+  auto epilogue = [&](auto mode_tag) {
+    constexpr int G = decltype(mode_tag)::value;
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       lds_barrier();
@@ -400,10 +400,12 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
       }
     }
   };
-  if (p.act == kActGelu)
-    epilogue(std::true_type{});
+  if (act_mode(p.act) == 1)
+    epilogue(std::integral_constant<int, 1>{});
+  else if (act_mode(p.act) == 0)
+    epilogue(std::integral_constant<int, 0>{});
   else
-    epilogue(std::false_type{});
+    epilogue(std::integral_constant<int, 2>{});
 }
 
 // Split-K reduction: one thread per 4 channels of one pixel; partials summed

@@ -52,13 +52,19 @@ __device__ __forceinline__ ActClamp act_clamp_of(int act, float alpha) {
   const bool clamp0 = act == kActRelu || act == kActRelu6;
   return ActClamp{clamp0 ? 0.0f : -INFINITY, act == kActRelu6 ? 6.0f : INFINITY, act == kActLeaky ? alpha : 1.0f};
 }
-template <bool GELU>
+// MODE 0: any activation but GELU; 1: GELU; 2: none / ReLU / ReLU6 only
+// (the clamp alone, for the hot epilogues that dispatch on the activation).
+template <int MODE>
 __device__ __forceinline__ float act_apply(float v, ActClamp a) {
-  if constexpr (GELU)
+  if constexpr (MODE == 1)
     return gelu(v);
+  else if constexpr (MODE == 2)
+    return __builtin_amdgcn_fmed3f(v, a.lo, a.hi);
   else
     return __builtin_amdgcn_fmed3f(fmaxf(v, v * a.slope), a.lo, a.hi);
 }
+// The epilogue mode of an activation code.
+__host__ __device__ constexpr int act_mode(int act) { return act == kActGelu ? 1 : (act == kActLeaky ? 0 : 2); }
 __device__ __forceinline__ float apply_act(float v, int act, float alpha) {
   return act == kActGelu ? gelu(v) : act_apply<false>(v, act_clamp_of(act, alpha));
 }
