@@ -988,45 +988,15 @@ void Planner::plan_node_i8(int ni) {
     e->launches.push_back(L);
     return;
   }
-  if (n.op == OpKind::Concat) {  // copies of the inputs not written in place
-    const auto& cs = g.values[n.out].shape;
-    int off = 0;
-    for (int a : n.cat) {
-      const int ca = (int)g.values[a].shape[1];
-      if (alias_of[a] != n.out) {
-        Launch C;
-        C.op = Launch::CopyChannels;
-        C.info.kind = BYOC_K_ADD;
-        C.info.node = ni;
-        C.x = loc[a];
-        C.y = slice(n.out, off);
-        C.M = (int)(cs[0] * cs[2] * cs[3]);
-        C.C = ca;
-        C.Cp = cp[a];
-        C.Kp = cp[n.out];
-        C.info.bytes = 2 * act_bytes(a);
-        name(C, "concat_copy");
-        e->launches.push_back(C);
-      }
-      off += ca;
-    }
-    return;
-  }
-  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool || n.op == OpKind::AvgPoolWin) {
+  if (n.op == OpKind::MaxPool || n.op == OpKind::AvgPool) {
     PoolParams& p = L.pool;
     p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3], p.Cp = cp[n.data];
     p.R = n.pool[0], p.S = n.pool[1], p.sh = n.stride[0], p.sw = n.stride[1];
     p.pt = n.pad[0], p.pl = n.pad[1];
-    p.P = n.op != OpKind::AvgPool ? (int)ys[2] : 1;
-    p.Q = n.op != OpKind::AvgPool ? (int)ys[3] : 1;
-    p.ldy = alias_of[n.out] >= 0 ? cp[alias_of[n.out]] : 0;
+    p.P = n.op == OpKind::MaxPool ? (int)ys[2] : 1;
+    p.Q = n.op == OpKind::MaxPool ? (int)ys[3] : 1;
     L.info.bytes = act_bytes(n.data) + act_bytes(n.out);
-    if (n.op == OpKind::AvgPoolWin) {
-      L.op = Launch::AvgPoolWinBf16;
-      L.info.kind = BYOC_K_AVGPOOL;
-      L.count_include_pad = n.count_include_pad;
-      name(L, "avgpool_win_nhwc");
-    } else if (n.op == OpKind::MaxPool) {
+    if (n.op == OpKind::MaxPool) {
       L.op = Launch::MaxPoolI8;
       L.info.kind = BYOC_K_MAXPOOL;
       name(L, "maxpool_nhwc_i8");
