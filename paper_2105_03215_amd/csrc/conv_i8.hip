@@ -37,10 +37,10 @@ constexpr int kMaxStages = 4;
 __device__ __forceinline__ i32x4 as_i32x4(uint4 u) { return __builtin_bit_cast(i32x4, u); }
 
 template <int BM, int BN, int WM, int WN, int NS, bool ALIGNED>
-__global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
-  static_assert(WM * WN == 4, "4 waves");
+__global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
+  static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves");
   const ConvParams& p = q.g;
-  constexpr int kNT = 256;
+  constexpr int kNT = 64 * WM * WN;
   constexpr int kRowsPerPass = kNT / kCH;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 16, TN = WTN / 16;
@@ -313,6 +313,7 @@ __global__ __launch_bounds__(256) void conv_i8_kernel(QConvParams q) {
 
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
+  constexpr int kThreads = 64 * WM * WN;
   QConvParams q = q_in;
   ConvParams& p = q.g;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
@@ -322,8 +323,8 @@ hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
     constexpr int NS = decltype(i)::value;
     if constexpr (NS * (BM + BN) * 128 <= kLdsLimit) {
       if (ns != NS) return;
-      if (aligned) conv_i8_kernel<BM, BN, WM, WN, NS, true><<<blocks, 256, 0, s>>>(q);
-      else conv_i8_kernel<BM, BN, WM, WN, NS, false><<<blocks, 256, 0, s>>>(q);
+      if (aligned) conv_i8_kernel<BM, BN, WM, WN, NS, true><<<blocks, kThreads, 0, s>>>(q);
+      else conv_i8_kernel<BM, BN, WM, WN, NS, false><<<blocks, kThreads, 0, s>>>(q);
       r = hipGetLastError();
     }
   });
@@ -332,14 +333,21 @@ hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
 
 }  // namespace
 
-bool conv_i8_tile_supported(int bm, int bn, int stages) {
+bool conv_i8_tile_supported(int bm, int bn, int stages, int threads) {
   if (stages < 2 || stages > kMaxStages) return false;
+  if (threads == 512) return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128);
+  if (threads != 256) return false;
   return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
 }
 
-hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, hipStream_t s) {
-  if (!conv_i8_tile_supported(bm, bn, stages)) return hipErrorInvalidValue;
+hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s) {
+  if (!conv_i8_tile_supported(bm, bn, stages, threads)) return hipErrorInvalidValue;
   if (p.g.Cp % kCE != 0 || p.g.Kp % 8 != 0 || p.g.Kgp % kBK != 0) return hipErrorInvalidValue;
+  if (threads == 512) {
+    if (bm == 128 && bn == 128) return launch_tile<128, 128, 2, 4>(p, stages, s);
+    if (bm == 128 && bn == 64) return launch_tile<128, 64, 4, 2>(p, stages, s);
+    return launch_tile<64, 128, 2, 4>(p, stages, s);
+  }
   if (bm == 128 && bn == 128) return launch_tile<128, 128, 2, 2>(p, stages, s);
   if (bm == 128 && bn == 64) return launch_tile<128, 64, 2, 2>(p, stages, s);
   if (bm == 64 && bn == 64) return launch_tile<64, 64, 2, 2>(p, stages, s);

@@ -164,7 +164,8 @@ int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
 }
 
 void name_conv_i8(Launch& L) {
-  std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_%dx%d_s%d", L.tile.bm, L.tile.bn, L.tile.stages);
+  std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_%dx%d_s%d_w%d", L.tile.bm, L.tile.bn, L.tile.stages,
+                L.tile.threads / 64);
 }
 
 void name_conv(Launch& L) {
@@ -972,11 +973,11 @@ void Planner::plan_node_i8(int ni) {
     else if (tiles(128, 64) >= 512) t.bm = 128, t.bn = 64;
     else if (p.M <= 32) t.bm = 32, t.bn = 64;
     else t.bm = 64, t.bn = 64;
-    // BYOC_I8_TILE=<bm>x<bn>s<stages> forces a tile (any tile gives the same codes)
+    // BYOC_I8_TILE=<bm>x<bn>s<stages>[w<waves>] forces a tile (any tile gives the same codes)
     if (const char* te = std::getenv("BYOC_I8_TILE")) {
-      int bm = 0, bn = 0, ns = 0;
-      if (std::sscanf(te, "%dx%ds%d", &bm, &bn, &ns) == 3 && conv_i8_tile_supported(bm, bn, ns))
-        t.bm = bm, t.bn = bn, t.stages = ns;
+      int bm = 0, bn = 0, ns = 0, nw = 4;
+      if (std::sscanf(te, "%dx%ds%dw%d", &bm, &bn, &ns, &nw) >= 3 && conv_i8_tile_supported(bm, bn, ns, 64 * nw))
+        t.bm = bm, t.bn = bn, t.stages = ns, t.threads = 64 * nw;
     }
     p.xcd_py = choose_xcd_split(p, t);
     L.tile_default = t;
@@ -1204,7 +1205,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       q.g.y = (bf16_t*)c.ptr(L.y);
       q.qch = (const int32_t*)c.ptr(L.bias);
       q.wtap = (const int32_t*)c.ptr(L.other);
-      return launch_conv_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, c.s);
+      return launch_conv_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, c.s);
     }
     case Launch::MaxPoolI8:
     case Launch::AvgPoolI8: {
@@ -1466,16 +1467,20 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
 // codes, do not depend on the tiling)
 std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
   std::vector<ConvTile> c{L.tile_default};
-  for (auto bmn : {std::pair<int, int>{128, 128}, {128, 64}, {64, 64}, {32, 64}})
-    for (int ns : {2, 3, 4}) {
-      ConvTile t = ConvTile{};
-      t.bm = bmn.first;
-      t.bn = bmn.second;
-      t.stages = ns;
-      if (!conv_i8_tile_supported(t.bm, t.bn, t.stages)) continue;
-      if (t.bm == L.tile_default.bm && t.bn == L.tile_default.bn && t.stages == L.tile_default.stages) continue;
-      c.push_back(t);
-    }
+  for (int nt : {256, 512})
+    for (auto bmn : {std::pair<int, int>{128, 128}, {128, 64}, {64, 128}, {64, 64}, {32, 64}})
+      for (int ns : {2, 3, 4}) {
+        ConvTile t = ConvTile{};
+        t.bm = bmn.first;
+        t.bn = bmn.second;
+        t.stages = ns;
+        t.threads = nt;
+        if (!conv_i8_tile_supported(t.bm, t.bn, t.stages, t.threads)) continue;
+        if (t.bm == L.tile_default.bm && t.bn == L.tile_default.bn && t.stages == L.tile_default.stages &&
+            t.threads == L.tile_default.threads)
+          continue;
+        c.push_back(t);
+      }
   return c;
 }
 

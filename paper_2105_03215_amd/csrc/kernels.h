@@ -190,8 +190,10 @@ struct QConvParams {
   int zr;               // residual zero point
   float mr;             // residual rescaling factor
 };
-bool conv_i8_tile_supported(int bm, int bn, int stages);
-hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, hipStream_t s);
+// Tiles: 4 waves (256 threads) 128x128, 128x64, 64x64, 32x64; 8 waves (512)
+// 128x128, 128x64, 64x128; 2 to 4 ring stages.
+bool conv_i8_tile_supported(int bm, int bn, int stages, int threads);
+hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s);
 
 // Boundary Q: float NCHW (or [M, K] as N = M, C = K, H = W = 1) ->
 // NHWC int8 codes clip(rint(x * inv_scale) + zp) (float32 arithmetic);

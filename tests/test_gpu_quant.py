@@ -95,14 +95,14 @@ def test_int8_tiles_agree():
     import os
     g, consts, inputs = _conv_graph(2, 144, 12, 12, 136, 3, 1, 1, 21, "relu", True, seed=3)
     ref = OQ.run_quantized_graph(g, consts, inputs)[0]
-    for tile in ("128x128s2", "128x64s4", "64x64s3", "32x64s2"):
+    for tile in ("128x128s2w4", "128x64s4w4", "64x64s3w4", "32x64s2w4", "128x128s2w8", "128x64s3w8", "64x128s4w8"):
         os.environ["BYOC_I8_TILE"] = tile
         try:
             got, launches = _run(g, consts, inputs)
         finally:
             del os.environ["BYOC_I8_TILE"]
         name = [l["name"] for l in launches if l["kind"] == "conv_i8"][0]
-        assert name == "conv_i8_" + tile.replace("s", "_s"), name
+        assert name == "conv_i8_" + tile.replace("s", "_s").replace("w", "_w"), name
         assert np.array_equal(got[0], ref.astype(np.float64)), tile
 
 
