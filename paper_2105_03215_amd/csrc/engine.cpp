@@ -194,6 +194,8 @@ struct Planner {
   // zero-copy concatenation: value -> the concatenation it is written into
   // (-1: none) and its first channel there
   std::vector<int> alias_of, alias_off;
+  // int8 graphs: input value -> the conv node that reads it as im2col rows (-1: none)
+  std::vector<int> im2col_of;
 
   bool i8;                                  // partially quantized (int8) graph
   const byoc_const* consts = nullptr;       // host constants (int8 weights are quantized on the host)
@@ -778,10 +780,63 @@ Status Planner::plan_i8() {
     *H = s.size() == 4 ? (int)s[2] : 1;
     *W = s.size() == 4 ? (int)s[3] : 1;
   };
+  // A few-channel image read only by one conv is quantized straight into that
+  // conv's im2col rows (R*S taps of 4 channel codes per output pixel, padded
+  // to 16): the conv becomes a 1x1 product over a reduction of R*S*4 instead
+  // of R*S*16 (channels padded to 16), and out-of-image taps hold the zero
+  // point, so the folded -Z_x * sum(w) of the bias is exact for every pixel.
+  im2col_of.assign(g.values.size(), -1);
+  {
+    std::vector<int> uses(g.values.size(), 0), reader(g.values.size(), -1);
+    for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
+      const Node& n = g.nodes[ni];
+      for (int a : {n.data, n.residual, n.other})
+        if (a >= 0) ++uses[a], reader[a] = (int)ni;
+    }
+    for (const IoDesc& o : g.outputs) ++uses[o.value];
+    for (const IoDesc& in : g.inputs) {
+      const int v = in.value;
+      const auto& s = g.values[v].shape;
+      if (s.size() != 4 || s[1] > 4 || uses[v] != 1 || reader[v] < 0) continue;
+      const Node& n = g.nodes[reader[v]];
+      if (n.op != OpKind::Conv || n.depthwise || n.data != v) continue;
+      const auto& ws = g.values[n.weight].shape;
+      const auto& ys = g.values[n.out].shape;
+      const int64_t kc = rup(ws[2] * ws[3] * 4, 16);
+      // (the staging kernel holds the R input rows of an output row in 48 KB of LDS)
+      if (kc <= 512 && s[0] * ys[2] * ys[3] * kc < (int64_t(1) << 31) && ws[2] * s[3] * 4 <= 48 * 1024)
+        im2col_of[v] = reader[v];
+    }
+  }
   for (size_t i = 0; i < g.inputs.size(); ++i) {
     const IoDesc& in = g.inputs[i];
     const int v = in.value;
     const Value& val = g.values[v];
+    if (im2col_of[v] >= 0) {
+      const Node& n = g.nodes[im2col_of[v]];
+      const auto& ws = g.values[n.weight].shape;
+      const auto& ys = g.values[n.out].shape;
+      Launch L;
+      L.op = Launch::QuantizeIm2colI8;
+      L.info.kind = BYOC_K_TRANSFORM;
+      L.info.node = -1;
+      L.x = io(Ref::Input, (int)i);
+      L.src_bf16 = in.dtype == DType::BF16;
+      PoolParams& q = L.pool;
+      q.N = (int)val.shape[0], q.C = (int)val.shape[1], q.H = (int)val.shape[2], q.W = (int)val.shape[3];
+      q.R = (int)ws[2], q.S = (int)ws[3], q.sh = n.stride[0], q.sw = n.stride[1], q.pt = n.pad[0], q.pl = n.pad[1];
+      q.P = (int)ys[2], q.Q = (int)ys[3];
+      q.Cp = (int)rup(q.R * q.S * 4, 16);
+      cp[v] = q.Cp;
+      loc[v] = arena((int64_t)q.N * q.P * q.Q * q.Cp);
+      L.y = loc[v];
+      L.qscale = (float)(1.0 / val.qscale);
+      L.qzero = val.qzero;
+      L.info.bytes = ext_bytes(v, in.dtype) + (int64_t)q.N * q.P * q.Q * q.Cp;
+      name(L, "quantize_im2col_in");
+      e->launches.push_back(L);
+      continue;
+    }
     cp[v] = (int)rup(val.shape[1], 16);
     loc[v] = arena(internal_bytes(v));
     Launch L;
@@ -858,13 +913,20 @@ void Planner::plan_node_i8(int ni) {
     const int H = dense ? 1 : (int)xs[2], W = dense ? 1 : (int)xs[3];
     const int P = dense ? 1 : (int)ys[2], Q = dense ? 1 : (int)ys[3];
     const int Cp = cp[n.data], Kp = cp[n.out];
+    // input as im2col rows: a 1x1 product over the P x Q image of R*S*C codes
+    const bool im2col = !dense && im2col_of[n.data] == ni;
     QConvParams& q = L.qc;
     ConvParams& p = q.g;
-    p.N = N, p.H = H, p.W = W, p.Cp = Cp, p.P = P, p.Q = Q, p.R = R, p.S = S;
-    p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1];
+    if (im2col) {
+      p.N = N, p.H = P, p.W = Q, p.Cp = Cp, p.P = P, p.Q = Q, p.R = 1, p.S = 1;
+      p.sh = 1, p.sw = 1, p.pt = 0, p.pl = 0;
+    } else {
+      p.N = N, p.H = H, p.W = W, p.Cp = Cp, p.P = P, p.Q = Q, p.R = R, p.S = S;
+      p.sh = n.stride[0], p.sw = n.stride[1], p.pt = n.pad[0], p.pl = n.pad[1];
+    }
     p.M = N * P * Q;
     p.Kp = Kp;
-    p.Kg = R * S * Cp;
+    p.Kg = p.R * p.S * Cp;
     p.Kgp = (int)rup(p.Kg, 128);
     p.ldy = Kp;
     p.ldr = Kp;
@@ -872,7 +934,7 @@ void Planner::plan_node_i8(int ni) {
     p.splits = 1;
     p.k_tiles_per_split = p.Kgp / 128;
     const int rows = (int)rup(Kp, kRowPad);
-    const int64_t xb = (int64_t)N * H * W * Cp, wb = (int64_t)rows * p.Kgp, rb = (int64_t)p.M * Kp;
+    const int64_t xb = (int64_t)N * p.H * p.W * Cp, wb = (int64_t)rows * p.Kgp, rb = (int64_t)p.M * Kp;
     if (xb >= (int64_t(1) << 31) || wb >= (int64_t(1) << 31) || rb >= (int64_t(1) << 31))
       return fail("an operand of 2 GiB or more");
     if ((int64_t)p.M * P * Q >= (int64_t(1) << 40) || (int64_t)p.Kg * Cp >= (int64_t(1) << 40))
@@ -885,7 +947,7 @@ void Planner::plan_node_i8(int ni) {
     p.mg_pq = magic40(P * Q);
     p.mg_q = magic40(Q);
     p.mg_cp = magic40(Cp);
-    p.mg_s = magic40(S);
+    p.mg_s = magic40(p.S);
 
     // host quantization of the weights (per output channel, symmetric),
     // the bias and the rescaling factors
@@ -911,7 +973,7 @@ void Planner::plan_node_i8(int ni) {
       return ((const float*)bcst->data)[k];
     };
     const int RS = R * S;
-    const bool border = !dense && xv.qzero != 0 && (n.pad[0] | n.pad[1] | n.pad[2] | n.pad[3]) != 0;
+    const bool border = !dense && !im2col && xv.qzero != 0 && (n.pad[0] | n.pad[1] | n.pad[2] | n.pad[3]) != 0;
     std::vector<uint8_t> packed((size_t)rows * p.Kgp, 0);
     std::vector<int32_t> qch((size_t)rows * 2, 0), wtap(border ? (size_t)rows * RS : 0, 0);
     const double sx = xv.qscale, sy = yv.qscale;
@@ -927,7 +989,8 @@ void Planner::plan_node_i8(int ni) {
             double qv = std::nearbyint(wget(base + ((int64_t)c * R + r) * S + s2) / sw);
             qv = std::min(127.0, std::max(-127.0, qv));
             const int wq = (int)qv;
-            packed[(size_t)k * p.Kgp + (size_t)(r * S + s2) * Cp + c] = (uint8_t)(int8_t)wq;
+            const size_t col = im2col ? (size_t)(r * S + s2) * 4 + c : (size_t)(r * S + s2) * Cp + c;
+            packed[(size_t)k * p.Kgp + col] = (uint8_t)(int8_t)wq;
             total += wq;
             if (border) wtap[(size_t)k * RS + r * S + s2] += wq;
           }
@@ -1222,6 +1285,8 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       a.y = (int8_t*)c.ptr(L.y);
       return launch_add_i8(a, c.s);
     }
+    case Launch::QuantizeIm2colI8:
+      return launch_quantize_im2col_i8(c.ptr(L.x), L.src_bf16, (int8_t*)c.ptr(L.y), L.pool, L.qscale, L.qzero, c.s);
     case Launch::QuantizeI8:
       return launch_quantize_i8(c.ptr(L.x), L.src_bf16, (int8_t*)c.ptr(L.y), L.N, L.C, L.H, L.W, L.Cp, L.qscale,
                                 L.qzero, c.s);

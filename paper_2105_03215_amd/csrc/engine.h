@@ -25,7 +25,7 @@ struct Launch {
   enum Op {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
     AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows,
-    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels
+    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels, QuantizeIm2colI8
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;

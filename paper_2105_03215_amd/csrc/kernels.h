@@ -200,6 +200,15 @@ hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int 
 // channels past C are written as 0.
 hipError_t launch_quantize_i8(const void* x, bool src_bf16, int8_t* y, int N, int C, int H, int W, int Cp,
                               float inv_scale, int zp, hipStream_t s);
+// Boundary Q fused with the im2col of the conv that alone reads the input
+// (an image of C <= 4 channels): y[(n*P + p)*Q + q][kk] for kk = (r*S + s)*4
+// + c the code of x[n][c][p*sh - pt + r][q*sw - pl + s] (0 for c >= C), the
+// zero point where that tap is outside the image, 0 for kk from 4*R*S up to
+// the row length g.Cp (a multiple of 16).  Geometry in g (C, H, W, R, S,
+// sh, sw, pt, pl, P, Q); R * W * 4 <= 48 KB (the input rows of one output
+// row are staged in LDS).
+hipError_t launch_quantize_im2col_i8(const void* x, bool src_bf16, int8_t* y, const PoolParams& g, float inv_scale,
+                                     int zp, hipStream_t s);
 // Boundary DQ: NHWC int8 -> float NCHW (or [M, K]) scale * (q - zp).
 hipError_t launch_dequantize_i8(const int8_t* x, void* y, bool dst_bf16, int N, int C, int H, int W, int Cp,
                                 float scale, int zp, hipStream_t s);

@@ -24,12 +24,12 @@ __device__ __forceinline__ float load_f(const void* x, bool bf16, int64_t i) {
 __global__ __launch_bounds__(kThreads) void quantize_kernel(const void* x, int src_bf16, int8_t* y, int N, int C,
                                                             int H, int W, int Cp, float inv, int zp) {
   const int HW = H * W, G = Cp / 16;
-  const int64_t total = (int64_t)N * G * HW;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
-    const int hw = (int)(i % HW);
-    const int64_t ng = i / HW;
-    const int g = (int)(ng % G);
-    const int n = (int)(ng / G);
+  const int total = N * G * HW;  // < 2^31: the element count is bounded at parse
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
+    const int hw = i % HW;
+    const int ng = i / HW;
+    const int g = ng % G;
+    const int n = ng / G;
     uint32_t w4[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
@@ -46,16 +46,58 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const void* x, int s
   }
 }
 
+// One workgroup per output row (n, p): the R input rows it reads are
+// quantized once into LDS as one dword of 4 channel codes per pixel (the
+// zero point for rows outside the image; coalesced loads along w), then the
+// Q im2col rows of the output row are written from LDS as consecutive
+// dwords (fully coalesced stores).
+constexpr int kIm2colLds = 48 * 1024;  // bytes of staged input rows (R * W * 4)
+
+__global__ __launch_bounds__(kThreads) void quantize_im2col_kernel(const void* x, int src_bf16, int8_t* y,
+                                                                   PoolParams g, float inv, int zp) {
+  extern __shared__ uint32_t rows[];  // R * W dwords (dynamic: the launch sizes it)
+  const int n = blockIdx.x / g.P, pp = blockIdx.x - n * g.P;
+  const int HW = g.H * g.W;
+  const uint32_t zrow = ((uint32_t)zp & 0xFFu) * 0x01010101u;
+  for (int t = threadIdx.x; t < g.R * g.W; t += kThreads) {
+    const int r = t / g.W, iw = t - r * g.W;
+    const int ih = pp * g.sh - g.pt + r;
+    uint32_t w = zrow;
+    if ((unsigned)ih < (unsigned)g.H) {
+      w = 0u;
+      for (int c = 0; c < g.C; ++c) {
+        float v = rintf(load_f(x, src_bf16, ((int64_t)(n * g.C + c) * g.H + ih) * g.W + iw) * inv);
+        v = fminf(fmaxf(v, -512.0f), 512.0f);
+        w |= ((uint32_t)clip_i8((int)v + zp) & 0xFFu) << (8 * c);
+      }
+    }
+    rows[t] = w;
+  }
+  __syncthreads();
+  // each thread keeps one dword k of the row (its tap fixed) and walks the
+  // pixels: lanes 0..63 of a wave store 64 consecutive dwords of a row
+  const int KW = g.Cp / 4, RS = g.R * g.S;
+  uint32_t* out = reinterpret_cast<uint32_t*>(y + ((int64_t)n * g.P + pp) * g.Q * g.Cp);
+  for (int k = threadIdx.x & 63; k < KW; k += 64) {
+    const int r = k / g.S, s = k - r * g.S;
+    const uint32_t* src = rows + r * g.W;
+    for (int qq = threadIdx.x >> 6; qq < g.Q; qq += kThreads / 64) {
+      const int iw = qq * g.sw - g.pl + s;
+      out[qq * KW + k] = k >= RS ? 0u : ((unsigned)iw < (unsigned)g.W ? src[iw] : zrow);
+    }
+  }
+}
+
 // One thread per output element (n, c, h, w), w fastest.
 __global__ __launch_bounds__(kThreads) void dequantize_kernel(const int8_t* x, void* y, int dst_bf16, int N, int C,
                                                               int H, int W, int Cp, float scale, int zp) {
   const int HW = H * W;
-  const int64_t total = (int64_t)N * C * HW;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
-    const int hw = (int)(i % HW);
-    const int64_t nc = i / HW;
-    const int c = (int)(nc % C);
-    const int n = (int)(nc / C);
+  const int total = N * C * HW;  // < 2^31: the element count is bounded at parse
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
+    const int hw = i % HW;
+    const int nc = i / HW;
+    const int c = nc % C;
+    const int n = nc / C;
     const float v = scale * (float)((int)x[((int64_t)n * HW + hw) * Cp + c] - zp);
     if (dst_bf16) reinterpret_cast<bf16_t*>(y)[i] = f32_to_bf16(v);
     else reinterpret_cast<float*>(y)[i] = v;
@@ -66,15 +108,16 @@ __global__ __launch_bounds__(kThreads) void dequantize_kernel(const int8_t* x, v
 // window's taps inside the image.
 __global__ __launch_bounds__(kThreads) void maxpool_i8_kernel(PoolParams p) {
   const int G = p.Cp / 16;
-  const int64_t total = (int64_t)p.N * p.P * p.Q * G;
+  const int total = p.N * p.P * p.Q * G;  // < 2^31 / 16: bytes of the output
   const int8_t* x = reinterpret_cast<const int8_t*>(p.x);
   int8_t* y = reinterpret_cast<int8_t*>(p.y);
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
-    const int g = (int)(i % G);
-    const int64_t pix = i / G;
-    const int qq = (int)(pix % p.Q);
-    const int pp = (int)((pix / p.Q) % p.P);
-    const int n = (int)(pix / ((int64_t)p.P * p.Q));
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
+    const int g = i % G;
+    const int pix = i / G;
+    const int qq = pix % p.Q;
+    const int pq = pix / p.Q;
+    const int pp = pq % p.P;
+    const int n = pq / p.P;
     int m[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) m[j] = -128;
@@ -93,19 +136,19 @@ __global__ __launch_bounds__(kThreads) void maxpool_i8_kernel(PoolParams p) {
     uint32_t o[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int j = 0; j < 16; ++j) o[j >> 2] |= ((uint32_t)m[j] & 0xFFu) << (8 * (j & 3));
-    *(uint4*)(y + i * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+    *(uint4*)(y + (int64_t)i * 16) = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
 // One thread per (n, channel): the integer sum over the image is exact.
 __global__ __launch_bounds__(kThreads) void avgpool_i8_kernel(PoolParams p, int zx, int zy, float m) {
-  const int64_t total = (int64_t)p.N * p.Cp;
+  const int total = p.N * p.Cp;
   const int HW = p.H * p.W;
   const int8_t* x = reinterpret_cast<const int8_t*>(p.x);
   int8_t* y = reinterpret_cast<int8_t*>(p.y);
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
-    const int c = (int)(i % p.Cp);
-    const int n = (int)(i / p.Cp);
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
+    const int c = i % p.Cp;
+    const int n = i / p.Cp;
     const int8_t* src = x + (int64_t)n * HW * p.Cp + c;
     int sum = 0;
     for (int j = 0; j < HW; ++j) sum += (int)src[(int64_t)j * p.Cp] - zx;
@@ -138,6 +181,14 @@ hipError_t launch_quantize_i8(const void* x, bool src_bf16, int8_t* y, int N, in
   if (Cp % 16 != 0 || Cp < C) return hipErrorInvalidValue;
   quantize_kernel<<<grid_for((int64_t)N * (Cp / 16) * H * W), kThreads, 0, s>>>(x, src_bf16 ? 1 : 0, y, N, C, H, W,
                                                                                  Cp, inv_scale, zp);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_im2col_i8(const void* x, bool src_bf16, int8_t* y, const PoolParams& g, float inv_scale,
+                                     int zp, hipStream_t s) {
+  if (g.Cp % 16 != 0 || g.Cp < g.R * g.S * 4 || g.C > 4 || g.R * g.W * 4 > kIm2colLds) return hipErrorInvalidValue;
+  quantize_im2col_kernel<<<g.N * g.P, kThreads, g.R * g.W * 4, s>>>(
+      x, src_bf16 ? 1 : 0, y, g, inv_scale, zp);
   return hipGetLastError();
 }
 
