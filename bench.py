@@ -68,6 +68,11 @@ def _roofline(launches, per_launch_ms, step_ms, traffic=None):
     conv_flops = sum(l["flops"] for l in launches if l["kind"] == "conv_mfma")
     n_conv = sum(1 for l in launches if l["kind"] == "conv_mfma")
     achieved = conv_flops / (conv_ms * 1e-3) / 1e12
+    # per-layer floor: each conv launch at its own roofline, max(flops / MFMA
+    # peak, algorithmic bytes / HBM peak); the 1x1 layers are HBM-bound, so
+    # the whole class cannot reach the MFMA peak
+    floor_ms = sum(max(l["flops"] / (PEAK_BF16_TFLOPS * 1e12), l["bytes"] / (PEAK_HBM_GBS * 1e9)) * 1e3
+                   for l in launches if l["kind"] == "conv_mfma")
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
@@ -75,7 +80,9 @@ def _roofline(launches, per_launch_ms, step_ms, traffic=None):
                        "splitk_reduce kernels), %d launches per step" % n_conv),
             "flops_per_step": conv_flops, "kernel_ms_per_step": round(conv_ms, 4),
             "per_launch_event_ms_per_step": round(conv_ev_ms, 4),
-            "per_launch_event_frac": round(conv_flops / (conv_ev_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            "per_launch_event_frac": round(conv_flops / (conv_ev_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "layer_floor_ms_per_step": round(floor_ms, 4),
+            "frac_of_layer_floor": round(floor_ms / conv_ms, 4)}
 
 
 def _class_summary(launches, per_launch_ms):
