@@ -10,7 +10,7 @@ import torch
 from paper_2105_03215_amd import host_runtime, partition as P, runtime, workloads
 from ir_ref import run_partitioned
 from parity_util import BF16_TOL, announce, rel_err
-from test_partition import _mixed_graph
+from test_partition import _inception_like_graph, _mixed_graph
 
 pytestmark = pytest.mark.gpu
 
@@ -69,3 +69,14 @@ def test_resnet50_with_host_head():
     g.outputs = [g.call("nn.softmax", [g.outputs[0]], axis=-1)]
     part = _check(g, wl.inputs)
     assert len(part.functions) == 1 and part.steps[-1][0] == "host"
+
+
+def test_concat_graph_with_host_concatenation():
+    """Concatenations in place and copied, an average pool and leaky ReLU
+    offloaded; a concatenation the executor rejects (6 channels) runs on
+    the host between the functions' outputs."""
+    announce("partitioned inception-like graph with a host concatenation")
+    g = _inception_like_graph(odd=True)
+    x = workloads.to_bf16_values(np.random.default_rng(13).random((2, 16, 9, 9)).astype(np.float32))
+    part = _check(g, [x])
+    assert [g.nodes[r].op for k, r in part.steps if k == "host"] == ["concatenate"]

@@ -14,6 +14,7 @@ unpartitioned graph.
 import numpy as np
 import pytest
 
+from oracle.bf16 import round_bf16
 from paper_2105_03215_amd import capi, partition as P, workloads
 from ir_ref import run_ir, run_partitioned
 
@@ -240,3 +241,51 @@ def test_workload_round_trip(name, kw):
     assert st["mac_offload"] == 1.0
     _check_invariants(part)
     capi.validate(f.graph, f.consts)
+
+
+def _inception_like_graph(seed=11, odd=False):
+    """Branches joined by concatenation (one branch an average pool), leaky
+    ReLU convs, a concatenation of a 6-channel tensor (not offloadable: the
+    executor joins multiples of 8 channels) when ``odd``."""
+    rng = _rng(seed)
+    g = P.Graph()
+    x = g.input("x", [2, 16, 9, 9], dtype="bf16")
+    a = _conv(g, x, 16, 1, rng)
+    b = _conv(g, _conv(g, x, 8, 1, rng), 24, 3, rng)
+    p = g.call("nn.avg_pool2d", [x], pool_size=[3, 3], strides=[1, 1], padding=[1, 1, 1, 1],
+               count_include_pad=False)
+    p = _conv(g, p, 8, 1, rng)
+    cat = g.call("concatenate", [a, b, p], axis=1)
+    w = g.const(rng.normal(0, 0.2, size=(16, 48, 3, 3)))
+    y = g.call("nn.conv2d", [cat, w], strides=[2, 2], padding=[1, 1, 1, 1])
+    y = g.call("nn.bias_add", [y, g.const(rng.normal(0, 0.1, size=16))])
+    y = g.call("nn.leaky_relu", [y], alpha=0.2)
+    if odd:
+        s6 = _conv(g, y, 6, 1, rng)
+        y = g.call("concatenate", [y, s6], axis=1)
+    g.output(y)
+    # a bf16 function computes with bf16 weights: make the constants
+    # bf16 values so that the operator-level reference uses the same ones
+    for n in g.nodes:
+        if n.op == "const":
+            n.value = round_bf16(n.value).astype(np.float32)
+    return g
+
+
+@pytest.mark.parametrize("odd", [False, True])
+def test_concat_avgpool_leaky_partition_semantics(odd):
+    g = _inception_like_graph(odd=odd)
+    x = round_bf16(_rng(12).random((2, 16, 9, 9)))
+    ref = run_ir(g, [x])[0]
+    part = P.partition(g)
+    _check_invariants(part)
+    names = [n["composite"] for f in part.functions for n in f.graph["nodes"]]
+    assert "concatenate" in names and "avg_pool2d" in names and "conv2d_bias_leaky" in names
+    host = [g.nodes[r].op for k, r in part.steps if k == "host"]
+    assert host == (["concatenate"] if odd else [])
+    got = run_partitioned(part, [x], mode="exact")[0]
+    assert np.max(np.abs(got - ref)) <= 1e-10 * max(1.0, np.max(np.abs(ref)))
+    for f in part.functions:
+        capi.validate(f.graph, f.consts)
+    leaky = [n for f in part.functions for n in f.graph["nodes"] if n["composite"] == "conv2d_bias_leaky"]
+    assert leaky[0]["attrs"]["alpha"] == 0.2
