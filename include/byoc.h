@@ -32,13 +32,21 @@
  *   "outputs":   [{"name", "dtype", "layout"}]
  * Composite names (the pattern names of Sec. 3.1.1; a composite applies
  * op -> bias -> residual add -> activation):
- *   conv2d[_bias][_add][_relu|_relu6|_gelu]   inputs data, weight[, bias][, residual]
+ *   conv2d[_bias][_add][_relu|_relu6|_gelu|_leaky]   inputs data, weight[, bias][, residual]
  *       attrs strides [sh,sw], padding [top,left,bottom,right], dilation [1,1],
  *       groups (1, or groups == in channels == out channels: depthwise)
- *   dense[_bias][_add][_relu|_relu6|_gelu]    data [M,K], weight [N,K]
+ *   dense[_bias][_add][_relu|_relu6|_gelu|_leaky]    data [M,K], weight [N,K]
  *   max_pool2d        attrs pool_size, strides, padding (padding acts as -inf)
+ *   avg_pool2d        attrs pool_size, strides (default 1), padding,
+ *                     count_include_pad (default false: the divisor counts
+ *                     the window positions inside the image); bf16 graphs
  *   global_avg_pool2d output [N, C]
- *   add[_relu|_relu6] two tensors of one shape
+ *   concatenate       one or more NCHW inputs of one batch and image joined
+ *                     along channels (attrs axis 1), each with a multiple of
+ *                     8 channels; bf16 graphs
+ *   add[_relu|_relu6|_leaky] two tensors of one shape
+ * A leaky ReLU (suffix _leaky) takes its slope from attrs alpha in [0, 1)
+ * (default 0.1).
  * All nodes of a graph share one out_dtype, the graph's compute type:
  *   "bf16": bf16 activations, weights rounded to bf16 (nearest, ties to
  *           even), fp32 bias, fp32 accumulation, each node's output rounded
