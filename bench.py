@@ -222,16 +222,25 @@ def _quantized(args, wl, dev, stream, calib_images=2):
         root, ext = os.path.splitext(args.dump_launches)
         with open(root + "_int8" + ext, "w") as f:
             json.dump([dict(l, ms=round(t, 5)) for l, t in zip(launches, per_launch)], f, indent=1)
+    n = wl.inputs[0].shape[0]
     other_ms = sum(t for l, t in zip(launches, per_launch) if l["kind"] != "conv_i8")
     conv_ms = max(ms - other_ms, 1e-9)
     ops = sum(l["flops"] for l in launches if l["kind"] == "conv_i8")
     tops = ops / (conv_ms * 1e-3) / 1e12
-    n = wl.inputs[0].shape[0]
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", "traffic_int8.json")
+    if os.path.exists(tpath):
+        from paper_2105_03215_amd import profiling
+        with open(tpath) as f:
+            tj = json.load(f)
+        if (tj.get("workload") == "%s_bs%d_int8" % (args.variant, n)
+                and tj.get("conv_kernel_digest") == profiling.conv_kernel_digest(profiling.I8_SOURCES)):
+            traffic = tj.get("conv_bytes_per_step")
     return {"workload": "%s_bs%d_int8" % (args.variant, n), "images_per_s": round(n / (ms * 1e-3), 1),
             "ms_per_step": round(ms, 4), "dtype": "int8 codes, int32 accumulation",
             "calibration": "%d images through the executor, %.2f s" % (calib_images, calib_s),
             "roofline": {"bound": "mfma", "achieved": round(tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                         "frac": round(tops / PEAK_INT8_TOPS, 4), "traffic": None,
+                         "frac": round(tops / PEAK_INT8_TOPS, 4), "traffic": traffic,
                          "kernel": "conv/dense int8 MFMA class (conv_i8), %d launches per step"
                                    % sum(1 for l in launches if l["kind"] == "conv_i8"),
                          "ops_per_step": ops, "kernel_ms_per_step": round(conv_ms, 4)},
@@ -275,7 +284,9 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=32)
-    ap.add_argument("--variant", default="resnet50_v1")
+    ap.add_argument("--variant", default="resnet50_v1",
+                    help="network of the headline run: resnet50_v1 (the benchmark), resnet50_v1b, vgg19, "
+                         "darknet53, inception_v3, mobilenet_v2")
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
@@ -403,7 +414,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded uniform[0,1) images, random He-init weights with folded BN)",
         "config": {"workload": "%s_bs%d" % (args.variant, args.batch), "batch": args.batch,
-                   "input": [args.batch, 3, 224, 224], "gflop_per_image": round(2 * wl.macs / args.batch / 1e9, 3),
+                   "input": list(wl.inputs[0].shape), "gflop_per_image": round(2 * wl.macs / args.batch / 1e9, 3),
                    "launches_per_step": len(launches), "parallelism": "none (1 GPU)",
                    "launch_mode": mode},
         "eager_images_per_s": round(args.batch / (ms_eager * 1e-3), 1),

@@ -98,28 +98,34 @@ def _copy_kib(path, counter):
     return statistics.median([v for v in vals if v > 0.5 * big])
 
 
-def conv_kernel_digest():
+CONV_SOURCES = ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "lds_dma.h", "stem.hip", "dense_rows.hip",
+                "engine.cpp")
+I8_KERNELS = ("conv_i8_kernel",)
+I8_SOURCES = ("conv_i8.hip", "quant.hip", "lds_dma.h", "engine.cpp")
+
+
+def conv_kernel_digest(sources=CONV_SOURCES):
     """Digest of the conv kernel sources and of the planner that picks them."""
     h = hashlib.sha256()
-    for name in ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "lds_dma.h", "stem.hip", "dense_rows.hip",
-                 "engine.cpp"):
+    for name in sources:
         with open(os.path.join(ROOT, "paper_2105_03215_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic(fetch, write, copy_fetch, copy_write, copy_mib, workload, out, last_runs):
+def traffic(fetch, write, copy_fetch, copy_write, copy_mib, workload, out, last_runs, marker=RUN_MARKER,
+            kernels=CONV_KERNELS, sources=CONV_SOURCES):
     copy_bytes = copy_mib * 2 ** 20
     f_scale = copy_bytes / (_copy_kib(copy_fetch, "FETCH_SIZE") * 1024.0)
     w_scale = copy_bytes / (_copy_kib(copy_write, "WRITE_SIZE") * 1024.0)
     res = {}
     for name, path, counter, scale in (("fetch", fetch, "FETCH_SIZE", f_scale),
                                        ("write", write, "WRITE_SIZE", w_scale)):
-        disp, runs = _last_runs(_counter(path, counter), "name", last_runs)
-        conv = sum(d["value"] for d in disp if _is_conv(d["name"]))
+        disp, runs = _last_runs(_counter(path, counter), "name", last_runs, marker)
+        conv = sum(d["value"] for d in disp if _is_conv(d["name"], kernels))
         res[name] = conv * 1024.0 * scale / runs
         res[name + "_runs"] = runs
-    doc = {"workload": workload, "conv_kernel_digest": conv_kernel_digest(),
+    doc = {"workload": workload, "conv_kernel_digest": conv_kernel_digest(sources),
            "conv_bytes_per_step": round(res["fetch"] + res["write"]),
            "conv_fetch_bytes_per_step": round(res["fetch"]),
            "conv_write_bytes_per_step": round(res["write"]),
@@ -149,13 +155,16 @@ def main():
         b.add_argument("--" + k, required=True)
     b.add_argument("--copy-mib", type=int, required=True)
     b.add_argument("--last-runs", type=int, required=True)
+    b.add_argument("--int8", action="store_true",
+                   help="the int8 conv class (runs split at the boundary quantize kernel)")
     args = ap.parse_args()
     if args.cmd_name == "stats":
         print(stats(args.trace, args.cmd, args.out, args.last_runs, args.flops_per_run, marker=args.marker,
                     kernels=tuple(args.kernels.split(",")), class_name=args.class_name, unit=args.unit))
     else:
+        kw = dict(marker="::quantize", kernels=I8_KERNELS, sources=I8_SOURCES) if args.int8 else {}
         print(json.dumps(traffic(args.fetch, args.write, args.copy_fetch, args.copy_write,
-                                 args.copy_mib, args.workload, args.out, args.last_runs)))
+                                 args.copy_mib, args.workload, args.out, args.last_runs, **kw)))
 
 
 if __name__ == "__main__":
