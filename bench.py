@@ -154,7 +154,7 @@ def _partitioned(args, wl, dev, stream):
     t0 = time.perf_counter()
     part = partition.partition(g)
     part_ms = (time.perf_counter() - t0) * 1e3
-    mod = host_runtime.Module(part, "cuda:0")
+    mod = host_runtime.Module(part, "cuda:0", graph_replay=not args.eager)
     try:
         if not args.no_autotune:
             for e in mod.engines:
@@ -176,7 +176,8 @@ def _partitioned(args, wl, dev, stream):
         mod.close()
     st = part.stats()
     return {"images_per_s": round(args.batch / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
-            "launch_mode": "direct launches", "partition_ms": round(part_ms, 2),
+            "launch_mode": "direct launches" if args.eager else "HIP graph replay per function",
+            "partition_ms": round(part_ms, 2),
             "functions": st["functions"], "host_steps": sum(1 for k, _ in part.steps if k == "host"),
             "node_offload": round(st["node_offload"], 4), "mac_offload": round(st["mac_offload"], 4)}
 

@@ -90,9 +90,16 @@ def _host_op(node, args):
 
 
 class Module:
-    """Executable form of a partitioned model on one device."""
+    """Executable form of a partitioned model on one device.
 
-    def __init__(self, part, device="cuda:0"):
+    Every step result (host operator or function output) has a data entry
+    allocated once at creation, as the paper's data entries are (fixed IDs,
+    preallocated): a run writes them in place, so the tensors ``run``
+    returns are valid until the next run, and each engine sees the same
+    buffers on every run, which lets it replay its launch sequence as a HIP
+    graph (``graph_replay``)."""
+
+    def __init__(self, part, device="cuda:0", graph_replay=False):
         self.part = part
         self.device = torch.device(device)
         self.dev_index = self.device.index or 0
@@ -108,6 +115,20 @@ class Module:
                 self.const_entries[n.id] = torch.from_numpy(n.value).to(self.device, torch.float32)
         # one cached execution engine per offloaded function
         self.engines = [capi.Subgraph(f.graph, f.consts, device=self.dev_index) for f in part.functions]
+        if graph_replay:
+            for e in self.engines:
+                e.set_options(graph_replay=True)
+        # data entries of every step result
+        self.data = {}
+        for kind, ref in part.steps:
+            if kind == "host":
+                node = g.nodes[ref]
+                self.data[ref] = torch.empty(tuple(node.shape), dtype=_tdt(node.dtype), device=self.device)
+            else:
+                eng = self.engines[ref]
+                for j, oid in enumerate(part.functions[ref].outputs):
+                    d = eng.io_desc(1, j)
+                    self.data[oid] = torch.empty(d["shape"], dtype=_tdt(d["dtype"]), device=self.device)
 
     def close(self):
         for e in self.engines:
@@ -120,6 +141,7 @@ class Module:
         g = self.part.graph
         stream = stream or torch.cuda.current_stream(self.device)
         entries = dict(self.const_entries)
+        entries.update(self.data)
         for nid, t in zip(g.inputs, inputs):
             entries[nid] = t.to(self.device, _tdt(g.nodes[nid].dtype)).contiguous()
         with torch.cuda.stream(stream):
@@ -127,16 +149,9 @@ class Module:
                 if kind == "host":
                     node = g.nodes[ref]
                     args = [entries[i].float() for i in node.inputs]
-                    entries[ref] = _host_op(node, args).to(_tdt(node.dtype)).contiguous()
+                    self.data[ref].copy_(_host_op(node, args).reshape(self.data[ref].shape))
                 else:
                     fn = self.part.functions[ref]
-                    eng = self.engines[ref]
-                    ins = [entries[i] for i in fn.inputs]
-                    outs = []
-                    for j, oid in enumerate(fn.outputs):
-                        d = eng.io_desc(1, j)
-                        outs.append(torch.empty(d["shape"], dtype=_tdt(d["dtype"]), device=self.device))
-                    eng.run(ins, outs, stream)
-                    for oid, t in zip(fn.outputs, outs):
-                        entries[oid] = t
+                    self.engines[ref].run([entries[i] for i in fn.inputs], [self.data[o] for o in fn.outputs],
+                                          stream)
         return [entries[o] for o in g.outputs]

@@ -27,10 +27,10 @@ def _bf16_graph(g):
     return g
 
 
-def _check(g, inputs, max_ops=None, runs=2):
+def _check(g, inputs, max_ops=None, runs=2, graph_replay=False):
     part = P.partition(g, max_ops=max_ops)
     ref = run_partitioned(part, inputs, mode="bf16io")
-    mod = host_runtime.Module(part, DEV)
+    mod = host_runtime.Module(part, DEV, graph_replay=graph_replay)
     try:
         xs = [torch.from_numpy(np.asarray(x, np.float32)).to(DEV) for x in inputs]
         first = None
@@ -50,12 +50,15 @@ def _check(g, inputs, max_ops=None, runs=2):
     return part
 
 
-@pytest.mark.parametrize("max_ops", [None, 4])
-def test_mixed_graph_partitioned(max_ops):
-    announce("partitioned mixed graph max_ops=%s" % max_ops)
+@pytest.mark.parametrize("max_ops,replay", [(None, False), (4, False), (4, True)])
+def test_mixed_graph_partitioned(max_ops, replay):
+    """Host steps between several functions; with graph replay the
+    functions' engines replay their launch sequences on the module's fixed
+    data entries (three runs, identical results)."""
+    announce("partitioned mixed graph max_ops=%s replay=%s" % (max_ops, replay))
     g = _bf16_graph(_mixed_graph())
     x = workloads.to_bf16_values(np.random.default_rng(11).random((2, 3, 17, 15)).astype(np.float32))
-    part = _check(g, [x], max_ops=max_ops)
+    part = _check(g, [x], max_ops=max_ops, runs=3 if replay else 2, graph_replay=replay)
     assert len(part.functions) >= 2
     assert any(k == "host" for k, _ in part.steps)
 
