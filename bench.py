@@ -398,7 +398,10 @@ def main():
         parted = _partitioned(args, wl, dev, stream)
     quant = None
     if not args.no_quantized:
-        quant = _quantized(args, wl, dev, stream)
+        try:
+            quant = _quantized(args, wl, dev, stream)
+        except capi.ByocError as e:  # e.g. depthwise convs have no int8 form
+            quant = {"workload": "%s_bs%d_int8" % (args.variant, args.batch), "skipped": str(e)}
     other = None
     if not args.no_other:
         other = [_other_workload(args, "vgg19", 32, dev, stream),
