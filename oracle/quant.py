@@ -24,7 +24,8 @@ others in the design notes):
   rint(fl32(fl32(a) * fl32(m))), ties to even, saturated to +-2^20 before the
   conversion back to an integer (one rounding of the product; the factor
   must be finite, positive and below 2^20);
-* conv / dense: acc = sum over taps inside the image and input channels of
+* conv / dense (and depthwise conv, one input channel per output channel):
+  acc = sum over taps inside the image and input channels of
   (x_q - Z_x) W_q, plus b_q (exact integers; padding contributes nothing,
   which is zero padding of the float tensor), then
   v = Z_y + rescale(acc, S_x S_w[k] / S_y) [+ rescale(r_q - Z_r, S_r / S_y)],
@@ -119,10 +120,10 @@ def _requant_out(v, act, s_y, z_y):
     return np.clip(v, QMIN, QMAX)
 
 
-def conv_accumulate(xq, zx, wq, strides, padding):
+def conv_accumulate(xq, zx, wq, strides, padding, groups=1):
     """Exact integer sum of (x_q - Z_x) W_q over the taps inside the image."""
     d = np.asarray(xq, dtype=np.int64) - int(zx)
-    acc = ops.conv2d(d.astype(np.float64), np.asarray(wq, dtype=np.float64), strides, padding)
+    acc = ops.conv2d(d.astype(np.float64), np.asarray(wq, dtype=np.float64), strides, padding, groups)
     return np.rint(acc).astype(np.int64)
 
 
@@ -130,7 +131,7 @@ def qconv(xq, qx, w, b, attrs, qy, act=None, res=None, qr=None):
     """Quantized conv2d composite on NCHW codes.  qx, qy, qr are (S, Z)."""
     wq, s_w = quantize_weights(w)
     acc = conv_accumulate(xq, qx[1], wq, tuple(attrs.get("strides", (1, 1))),
-                          tuple(attrs.get("padding", (0, 0, 0, 0))))
+                          tuple(attrs.get("padding", (0, 0, 0, 0))), int(attrs.get("groups", 1)))
     return _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape=(1, -1, 1, 1))
 
 
@@ -221,8 +222,9 @@ def run_quantized_graph(graph, consts, inputs, keep=False):
             if has_add:
                 r, qr = codes[ins[i]], qps[ins[i]]
             if op == "conv2d":
-                if int(attrs.get("groups", 1)) != 1:
-                    raise ValueError("node %s: grouped conv has no int8 form" % node["name"])
+                groups = int(attrs.get("groups", 1))
+                if groups != 1 and not (groups == w.shape[0] and w.shape[1] == 1):
+                    raise ValueError("node %s: grouped conv other than depthwise has no int8 form" % node["name"])
                 y = qconv(codes[x], qps[x], w, b, attrs, qy, act, r, qr)
             else:
                 y = qdense(codes[x], qps[x], w, b, qy, act, r, qr)

@@ -248,3 +248,20 @@ def test_int8_graph_rejects_pool_rescaling():
     g["nodes"][2]["quant"] = {"scale": 0.05, "zero_point": -128}
     with pytest.raises(ValueError):
         Q.run_quantized_graph(g, consts, [np.zeros((2, 3, 9, 9), np.float32)])
+
+
+def test_quantized_depthwise_equals_rounded_float_depthwise():
+    """Depthwise (one input channel per output channel): the dyadic case
+    against the float64 grouped conv on dequantized codes."""
+    rng = np.random.default_rng(14)
+    sx, sw, sy, zx, zy = 2.0 ** -5, 2.0 ** -7, 2.0 ** -3, 23, -7
+    xq = rng.integers(-128, 128, size=(2, 6, 7, 5))
+    j = rng.integers(-127, 128, size=(6, 1, 3, 3))
+    j[:, 0, 0, 0] = 127
+    b = rng.integers(-900, 900, size=6) * (sx * sw)
+    attrs = {"strides": (2, 1), "padding": (1, 1, 1, 1), "groups": 6}
+    got = Q.qconv(xq, (sx, zx), j * sw, b, attrs, (sy, zy), "relu6")
+    t = ops.bias_add(ops.conv2d(sx * (xq - zx), j * sw, (2, 1), (1, 1, 1, 1), groups=6), b) / sy
+    lo, hi = Q.act_bounds("relu6", sy, zy)
+    want = np.clip(np.clip(zy + np.rint(t), lo, hi), -128, 127)
+    assert np.array_equal(got, want.astype(np.int64))
