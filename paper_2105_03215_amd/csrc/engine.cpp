@@ -904,6 +904,66 @@ void Planner::plan_node_i8(int ni) {
     hi = h < 127.0 ? (int)h : 127;
   }
 
+  if (n.op == OpKind::Conv && n.depthwise) {
+    // exact integer taps on the vector ALU; weights quantized per channel here
+    const auto& ws = g.values[n.weight].shape;
+    const int C = (int)ws[0], R = (int)ws[2], S = (int)ws[3];
+    QDwParams& d = L.qd;
+    d.N = (int)xs[0], d.H = (int)xs[2], d.W = (int)xs[3], d.Cp = cp[n.data], d.P = (int)ys[2], d.Q = (int)ys[3];
+    d.R = R, d.S = S, d.sh = n.stride[0], d.sw = n.stride[1], d.pt = n.pad[0], d.pl = n.pad[1];
+    if ((int64_t)R * S * 255 * 127 >= (int64_t(1) << 30)) return fail("window too large for int32 accumulation");
+    const byoc_const& wcst = consts[g.values[n.weight].index];
+    const byoc_const* bcst = n.bias >= 0 ? &consts[g.values[n.bias].index] : nullptr;
+    auto fget = [](const byoc_const& cst, int64_t i) -> double {
+      if (cst.dtype == BYOC_BF16) {
+        const uint32_t b = (uint32_t)((const uint16_t*)cst.data)[i] << 16;
+        float f;
+        std::memcpy(&f, &b, 4);
+        return f;
+      }
+      return ((const float*)cst.data)[i];
+    };
+    const int RS = R * S;
+    std::vector<uint8_t> packed((size_t)RS * d.Cp, 0);
+    std::vector<int32_t> qch((size_t)d.Cp * 2, 0);
+    const double sx = xv.qscale, sy = yv.qscale;
+    for (int k = 0; k < C; ++k) {
+      double amax = 0.0;
+      for (int t = 0; t < RS; ++t) amax = std::max(amax, std::fabs(fget(wcst, (int64_t)k * RS + t)));
+      const double sw = amax > 0.0 ? amax / 127.0 : 1.0;
+      for (int t = 0; t < RS; ++t) {
+        const double qv = std::min(127.0, std::max(-127.0, std::nearbyint(fget(wcst, (int64_t)k * RS + t) / sw)));
+        packed[(size_t)t * d.Cp + k] = (uint8_t)(int8_t)(int)qv;
+      }
+      double bq = 0.0;
+      if (bcst) bq = std::min(2147483647.0, std::max(-2147483648.0, std::nearbyint(fget(*bcst, k) / (sx * sw))));
+      if (bq <= -1073741824.0 || bq >= 1073741824.0)
+        return fail("quantized bias of channel " + std::to_string(k) + " outside +-2^30");
+      float mk = 0.f;
+      if (!rescale_factor((sx * sw) / sy, &mk))
+        return fail("rescaling factor of channel " + std::to_string(k) + " outside (0, 2^20)");
+      qch[(size_t)k * 2] = (int32_t)bq;
+      std::memcpy(&qch[(size_t)k * 2 + 1], &mk, 4);
+    }
+    L.w = host_blob(std::move(packed));
+    std::vector<uint8_t> qb(qch.size() * 4);
+    std::memcpy(qb.data(), qch.data(), qb.size());
+    L.bias = host_blob(std::move(qb));
+    d.zx = xv.qzero, d.zy = yv.qzero, d.lo = lo, d.hi = hi;
+    if (n.residual >= 0) {
+      const Value& rv = g.values[n.residual];
+      L.res = loc[n.residual];
+      d.zr = rv.qzero;
+      if (!rescale_factor(rv.qscale / sy, &d.mr)) return fail("residual rescaling factor outside (0, 2^20)");
+    }
+    L.op = Launch::DepthwiseI8;
+    L.info.kind = BYOC_K_DEPTHWISE;
+    L.info.flops = 2 * n.macs;
+    L.info.bytes = numel(xs) + numel(ws) + numel(ys) * (n.residual >= 0 ? 2 : 1);
+    name(L, "depthwise_nhwc_i8");
+    e->launches.push_back(L);
+    return;
+  }
   if (n.op == OpKind::Conv || n.op == OpKind::Dense) {
     const bool dense = n.op == OpKind::Dense;
     const auto& ws = g.values[n.weight].shape;
@@ -1284,6 +1344,15 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       a.b = (const int8_t*)c.ptr(L.other);
       a.y = (int8_t*)c.ptr(L.y);
       return launch_add_i8(a, c.s);
+    }
+    case Launch::DepthwiseI8: {
+      QDwParams d = L.qd;
+      d.x = (const int8_t*)c.ptr(L.x);
+      d.w = (const int8_t*)c.ptr(L.w);
+      d.qch = (const int32_t*)c.ptr(L.bias);
+      d.res = (const int8_t*)c.ptr(L.res);
+      d.y = (int8_t*)c.ptr(L.y);
+      return launch_depthwise_i8(d, c.s);
     }
     case Launch::QuantizeIm2colI8:
       return launch_quantize_im2col_i8(c.ptr(L.x), L.src_bf16, (int8_t*)c.ptr(L.y), L.pool, L.qscale, L.qzero, c.s);

@@ -25,7 +25,8 @@ struct Launch {
   enum Op {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
     AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows,
-    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels, QuantizeIm2colI8
+    ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels, QuantizeIm2colI8,
+    DepthwiseI8
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;
@@ -38,6 +39,7 @@ struct Launch {
   StemParams stem{};
   QConvParams qc{};  // int8 conv / dense (qc.g holds the geometry; tile in `tile`)
   QAddParams qa{};   // int8 add
+  QDwParams qd{};    // int8 depthwise conv
   float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
   int qzero = 0;                 // quantize / dequantize zero point
   int qzx = 0, qzy = 0;          // int8 average pool: zero points

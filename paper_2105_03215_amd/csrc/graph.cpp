@@ -515,7 +515,6 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
         if (a < 0 || g.values[a].has_q) continue;
         return serr(where + ": int8 operand '" + g.values[a].name + "' has no quant parameters");
       }
-      if (n.depthwise) return uerr(where + ": depthwise conv has no int8 form");
       if (n.act == Act::Gelu || n.act == Act::Leaky)
         return uerr(where + ": " + act_name(n.act) + " has no int8 form");
       if (n.op == OpKind::MaxPool) {

@@ -212,6 +212,21 @@ hipError_t launch_quantize_im2col_i8(const void* x, bool src_bf16, int8_t* y, co
 // Boundary DQ: NHWC int8 -> float NCHW (or [M, K]) scale * (q - zp).
 hipError_t launch_dequantize_i8(const int8_t* x, void* y, bool dst_bf16, int N, int C, int H, int W, int Cp,
                                 float scale, int zp, hipStream_t s);
+// Depthwise conv of codes, NHWC, one input channel per output channel:
+// v = zy + rescale(sum over taps inside the image of (x - zx) w + bias, m)
+// [+ rescale(res - zr, mr)], clamped to [lo, hi] (within [-128, 127]).
+// Weights [R*S][Cp] int8; qch [>= Cp][2]: int32 bias, float32 factor bits.
+struct QDwParams {
+  const int8_t* x;
+  const int8_t* w;
+  const int32_t* qch;
+  const int8_t* res;  // [N][P][Q][Cp] or nullptr
+  int8_t* y;
+  int N, H, W, Cp, P, Q, R, S, sh, sw, pt, pl;
+  int zx, zy, lo, hi, zr;
+  float mr;
+};
+hipError_t launch_depthwise_i8(const QDwParams& p, hipStream_t s);
 // Max pooling of codes, NHWC (padding never wins).
 hipError_t launch_maxpool_nhwc_i8(const PoolParams& p, hipStream_t s);
 // Global average pooling of codes: y[n][c] = clip(zy + rescale(sum(x - zx), m)), y [N][Cp].

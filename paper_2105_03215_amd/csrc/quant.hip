@@ -140,6 +140,54 @@ __global__ __launch_bounds__(kThreads) void maxpool_i8_kernel(PoolParams p) {
   }
 }
 
+// One thread per (n, p, q, 16-channel group): exact integer taps, 16 codes
+// per 16-byte load of activations and of weights.
+__global__ __launch_bounds__(kThreads) void depthwise_i8_kernel(QDwParams p) {
+  const int G = p.Cp / 16;
+  const int total = p.N * p.P * p.Q * G;  // < 2^31 / 16: bytes of the output
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
+    const int g = i % G;
+    const int pix = i / G;
+    const int qq = pix % p.Q;
+    const int pq = pix / p.Q;
+    const int pp = pq % p.P;
+    const int n = pq / p.P;
+    int acc[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[j] = 0;
+    for (int r = 0; r < p.R; ++r) {
+      const int ih = pp * p.sh - p.pt + r;
+      if ((unsigned)ih >= (unsigned)p.H) continue;
+      for (int s = 0; s < p.S; ++s) {
+        const int iw = qq * p.sw - p.pl + s;
+        if ((unsigned)iw >= (unsigned)p.W) continue;
+        const uint4 xv = *(const uint4*)(p.x + (((int64_t)n * p.H + ih) * p.W + iw) * p.Cp + g * 16);
+        const uint4 wv = *(const uint4*)(p.w + (int64_t)(r * p.S + s) * p.Cp + g * 16);
+        const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          acc[j] += ((int)(int8_t)(xw[j >> 2] >> (8 * (j & 3))) - p.zx) * (int)(int8_t)(ww[j >> 2] >> (8 * (j & 3)));
+      }
+    }
+    uint32_t rw[4] = {0u, 0u, 0u, 0u};
+    if (p.res) {
+      const uint4 rv = *(const uint4*)(p.res + (int64_t)pix * p.Cp + g * 16);
+      rw[0] = rv.x, rw[1] = rv.y, rw[2] = rv.z, rw[3] = rv.w;
+    }
+    const int2* qc = reinterpret_cast<const int2*>(p.qch) + g * 16;
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int2 q = qc[j];
+      int v = p.zy + rescale(acc[j] + q.x, __int_as_float(q.y));
+      if (p.res) v += rescale((int)(int8_t)(rw[j >> 2] >> (8 * (j & 3))) - p.zr, p.mr);
+      v = min(max(v, p.lo), p.hi);
+      o[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+    }
+    *(uint4*)(p.y + (int64_t)pix * p.Cp + g * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 // One thread per (n, channel): the integer sum over the image is exact.
 __global__ __launch_bounds__(kThreads) void avgpool_i8_kernel(PoolParams p, int zx, int zy, float m) {
   const int total = p.N * p.Cp;
@@ -197,6 +245,12 @@ hipError_t launch_dequantize_i8(const int8_t* x, void* y, bool dst_bf16, int N, 
   if (Cp < C) return hipErrorInvalidValue;
   dequantize_kernel<<<grid_for((int64_t)N * C * H * W), kThreads, 0, s>>>(x, y, dst_bf16 ? 1 : 0, N, C, H, W, Cp,
                                                                           scale, zp);
+  return hipGetLastError();
+}
+
+hipError_t launch_depthwise_i8(const QDwParams& p, hipStream_t s) {
+  if (p.Cp % 16 != 0) return hipErrorInvalidValue;
+  depthwise_i8_kernel<<<grid_for((int64_t)p.N * p.P * p.Q * (p.Cp / 16)), kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -188,3 +188,55 @@ def test_int8_resnet50_bs32_sampled():
     g2["inputs"] = [dict(d, shape=[2] + d["shape"][1:]) for d in g2["inputs"]]
     ref = OQ.run_quantized_graph(g2, wl.consts, [np.ascontiguousarray(a[rows]) for a in wl.inputs])[0]
     assert np.array_equal(got[0][rows], ref.astype(np.float64))
+
+
+DW_CASES = [
+    # n, c, h, w, stride, zx, act, residual
+    (2, 32, 13, 11, 1, 17, "relu6", False),
+    (1, 96, 14, 14, 2, -128, "relu6", False),
+    (2, 40, 7, 9, 1, 60, None, True),
+]
+
+
+@pytest.mark.parametrize("case", DW_CASES, ids=[str(i) for i in range(len(DW_CASES))])
+def test_int8_depthwise_bit_exact(case):
+    n, c, h, w, stride, zx, act, residual = case
+    announce("int8 depthwise %s" % (case,))
+    rng = np.random.default_rng(30 + DW_CASES.index(case))
+    wt = rng.normal(0, 0.4, size=(c, 1, 3, 3)).astype(np.float32)
+    b = rng.normal(0, 0.2, size=c).astype(np.float32)
+    p = (h + 2 - 3) // stride + 1
+    q = (w + 2 - 3) // stride + 1
+    ins_desc = [{"name": "x", "shape": [n, c, h, w], "dtype": "f32", "quant": _q(0.013, zx)}]
+    inputs = [rng.uniform(-1.0, 2.0, size=(n, c, h, w)).astype(np.float32)]
+    refs = ["x", "w", "b"]
+    if residual:
+        ins_desc.append({"name": "r", "shape": [n, c, p, q], "dtype": "f32", "quant": _q(0.02, 3)})
+        inputs.append(rng.normal(0, 1, size=(n, c, p, q)).astype(np.float32))
+        refs.append("r")
+    comp = "conv2d_bias" + ("_add" if residual else "") + ("_" + act if act else "")
+    g = {"format": "byoc-subgraph", "version": 1, "inputs": ins_desc,
+         "constants": [{"name": "w", "index": 0, "shape": [c, 1, 3, 3], "dtype": "f32"},
+                       {"name": "b", "index": 1, "shape": [c], "dtype": "f32"}],
+         "nodes": [{"name": "y", "composite": comp, "inputs": refs, "out_dtype": "int8",
+                    "attrs": {"strides": [stride, stride], "padding": [1, 1, 1, 1], "groups": c},
+                    "quant": _q(0.03, -20)}],
+         "outputs": [{"name": "y", "dtype": "f32"}]}
+    got, launches = _run(g, [wt, b], inputs)
+    assert any(l["name"] == "depthwise_nhwc_i8" for l in launches)
+    ref = OQ.run_quantized_graph(g, [wt, b], inputs)[0]
+    assert np.array_equal(got[0], ref.astype(np.float64))
+
+
+def test_int8_mobilenet_v2_small_full_compare():
+    import torch
+    announce("int8 mobilenet_v2 n=2 hw=64")
+    wl = workloads.build("mobilenet_v2", n=2, hw=64)
+    batch = [torch.from_numpy(np.ascontiguousarray(wl.inputs[0])).to(DEV).to(torch.bfloat16)]
+    qg = quantize.quantize_graph(wl.graph, quantize.calibrate(wl.graph, wl.consts, [batch]))
+    for o in qg["outputs"]:
+        o["dtype"] = "f32"
+    got, launches = _run(qg, wl.consts, wl.inputs)
+    assert sum(1 for l in launches if l["name"] == "depthwise_nhwc_i8") == 17
+    ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
+    assert np.array_equal(got[0], ref.astype(np.float64))
