@@ -64,8 +64,9 @@
  *           accumulate exactly in int32 on int8 MFMA; every rescaling is a
  *           fixed-point multiply m0 2^-t rounded once, ties away from zero;
  *           activations clamp in code space (ReLU >= Z, ReLU6 <= Z +
- *           rint(6/S)).  A max pool keeps its input's S and Z.  Not in int8
- *           graphs: depthwise convs and GELU.
+ *           rint(6/S)).  A max pool keeps its input's S and Z; depthwise
+ *           convs sum exactly on the vector ALU.  Not in int8 graphs: GELU,
+ *           leaky ReLU, windowed average pools, concatenation.
  * Internally activations of bf16 graphs are NHWC with channels padded to a
  * multiple of 8 (the layout-transform nodes of Sec. 3.2, Fig. 4b, sit at
  * the function boundary); callers always see the declared layouts.
