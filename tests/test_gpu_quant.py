@@ -240,3 +240,18 @@ def test_int8_mobilenet_v2_small_full_compare():
     assert sum(1 for l in launches if l["name"] == "depthwise_nhwc_i8") == 17
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
     assert np.array_equal(got[0], ref.astype(np.float64))
+
+
+def test_int8_vgg19_small_full_compare():
+    """VGG19 (2x2 max pools, the full-map fc6 conv, dense classifier) in int8."""
+    import torch
+    announce("int8 vgg19 n=2 hw=64")
+    wl = workloads.build("vgg19", n=2, hw=64)
+    batch = [torch.from_numpy(np.ascontiguousarray(wl.inputs[0])).to(DEV).to(torch.bfloat16)]
+    qg = quantize.quantize_graph(wl.graph, quantize.calibrate(wl.graph, wl.consts, [batch]))
+    for o in qg["outputs"]:
+        o["dtype"] = "f32"
+    got, launches = _run(qg, wl.consts, wl.inputs)
+    assert sum(1 for l in launches if l["kind"] == "conv_i8") == 19
+    ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
+    assert np.array_equal(got[0], ref.astype(np.float64))
