@@ -29,8 +29,9 @@ others in the design notes):
   (x_q - Z_x) W_q, plus b_q (exact integers; padding contributes nothing,
   which is zero padding of the float tensor), then
   v = Z_y + rescale(acc, S_x S_w[k] / S_y) [+ rescale(r_q - Z_r, S_r / S_y)],
-  the activation as a clamp in code space (ReLU: v >= Z_y; ReLU6 also
-  v <= Z_y + rint(6 / S_y)), and a final clip to [-128, 127];
+  the activation in code space (ReLU: v >= Z_y; ReLU6 also
+  v <= Z_y + rint(6 / S_y); leaky ReLU: a negative offset t = v - Z_y
+  becomes rint(fl32(t * alpha))), and a final clip to [-128, 127];
 * max pooling takes the largest code of the window (monotone, so the output
   keeps the input's S and Z; padding never wins);
 * global average pooling: v = Z_y + rescale(sum_hw (x_q - Z_x), S_x / (S_y H W));
@@ -108,12 +109,22 @@ def act_bounds(act, s_y, z_y):
         lo = int(z_y)
     if act == "relu6":
         hi = int(z_y) + int(np.rint(6.0 / float(s_y)))
-    if act not in (None, "relu", "relu6"):
+    if act not in (None, "relu", "relu6", "leaky"):
         raise ValueError("activation %r has no int8 form" % act)
     return lo, hi
 
 
-def _requant_out(v, act, s_y, z_y):
+def leaky_codes(v, z_y, alpha):
+    """Leaky ReLU on codes: the offset t = v - Z_y is kept where t >= 0 and
+    becomes rint(fl32(fl32(t) * fl32(alpha))) below (float32, ties to even)."""
+    t = np.asarray(v, dtype=np.int64) - int(z_y)
+    neg = np.rint(t.astype(np.float32) * np.float32(alpha)).astype(np.int64)
+    return int(z_y) + np.where(t < 0, neg, t)
+
+
+def _requant_out(v, act, s_y, z_y, alpha=0.1):
+    if act == "leaky":
+        v = leaky_codes(v, z_y, alpha)
     lo, hi = act_bounds(act, s_y, z_y)
     v = np.maximum(v, lo)
     v = np.minimum(v, hi)
@@ -127,23 +138,23 @@ def conv_accumulate(xq, zx, wq, strides, padding, groups=1):
     return np.rint(acc).astype(np.int64)
 
 
-def qconv(xq, qx, w, b, attrs, qy, act=None, res=None, qr=None):
+def qconv(xq, qx, w, b, attrs, qy, act=None, res=None, qr=None, alpha=0.1):
     """Quantized conv2d composite on NCHW codes.  qx, qy, qr are (S, Z)."""
     wq, s_w = quantize_weights(w)
     acc = conv_accumulate(xq, qx[1], wq, tuple(attrs.get("strides", (1, 1))),
                           tuple(attrs.get("padding", (0, 0, 0, 0))), int(attrs.get("groups", 1)))
-    return _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape=(1, -1, 1, 1))
+    return _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape=(1, -1, 1, 1), alpha=alpha)
 
 
-def qdense(xq, qx, w, b, qy, act=None, res=None, qr=None):
+def qdense(xq, qx, w, b, qy, act=None, res=None, qr=None, alpha=0.1):
     """Quantized dense composite on [M, K] codes."""
     wq, s_w = quantize_weights(w)
     d = (np.asarray(xq, dtype=np.int64) - int(qx[1])).astype(np.float64)
     acc = np.rint(ops.dense(d, wq.astype(np.float64))).astype(np.int64)
-    return _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape=(1, -1))
+    return _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape=(1, -1), alpha=alpha)
 
 
-def _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape):
+def _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape, alpha=0.1):
     s_x, _ = qx
     s_y, z_y = qy
     if b is not None:
@@ -154,7 +165,7 @@ def _qepilogue(acc, s_w, b, qx, qy, act, res, qr, axis_shape):
     v = v + int(z_y)
     if res is not None:
         v = v + rescale(np.asarray(res, dtype=np.int64) - int(qr[1]), float(qr[0]) / float(s_y))
-    return _requant_out(v, act, s_y, z_y)
+    return _requant_out(v, act, s_y, z_y, alpha)
 
 
 def qmax_pool2d(xq, attrs):
@@ -172,11 +183,11 @@ def qglobal_avg_pool2d(xq, qx, qy):
     return np.clip(int(qy[1]) + rescale(tot, float(qx[0]) / (float(qy[0]) * h * w)), QMIN, QMAX)
 
 
-def qadd(aq, qa, bq, qb, qy, act=None):
+def qadd(aq, qa, bq, qb, qy, act=None, alpha=0.1):
     """Quantized elementwise add with activation."""
     v = (int(qy[1]) + rescale(np.asarray(aq, dtype=np.int64) - int(qa[1]), float(qa[0]) / float(qy[0]))
          + rescale(np.asarray(bq, dtype=np.int64) - int(qb[1]), float(qb[0]) / float(qy[0])))
-    return _requant_out(v, act, qy[0], qy[1])
+    return _requant_out(v, act, qy[0], qy[1], alpha)
 
 
 def _qp(desc, where):
@@ -206,6 +217,7 @@ def run_quantized_graph(graph, consts, inputs, keep=False):
             raise ValueError("node %s: not an int8 node" % node["name"])
         op, has_bias, has_add, act = parse_composite(node["composite"])
         attrs = node.get("attrs", {})
+        alpha = float(attrs.get("alpha", 0.1))
         ins = node["inputs"]
         if op == "max_pool2d" and not node.get("quant"):
             qy = qps[ins[0]]  # a max pool keeps its input's scale and zero point
@@ -225,9 +237,9 @@ def run_quantized_graph(graph, consts, inputs, keep=False):
                 groups = int(attrs.get("groups", 1))
                 if groups != 1 and not (groups == w.shape[0] and w.shape[1] == 1):
                     raise ValueError("node %s: grouped conv other than depthwise has no int8 form" % node["name"])
-                y = qconv(codes[x], qps[x], w, b, attrs, qy, act, r, qr)
+                y = qconv(codes[x], qps[x], w, b, attrs, qy, act, r, qr, alpha)
             else:
-                y = qdense(codes[x], qps[x], w, b, qy, act, r, qr)
+                y = qdense(codes[x], qps[x], w, b, qy, act, r, qr, alpha)
         elif op == "max_pool2d":
             if qps[ins[0]] != qy:
                 raise ValueError("node %s: max pool keeps its input's scale and zero point" % node["name"])
@@ -235,7 +247,7 @@ def run_quantized_graph(graph, consts, inputs, keep=False):
         elif op == "global_avg_pool2d":
             y = qglobal_avg_pool2d(codes[ins[0]], qps[ins[0]], qy)
         else:
-            y = qadd(codes[ins[0]], qps[ins[0]], codes[ins[1]], qps[ins[1]], qy, act)
+            y = qadd(codes[ins[0]], qps[ins[0]], codes[ins[1]], qps[ins[1]], qy, act, alpha)
         codes[node["name"]] = y
         qps[node["name"]] = qy
     outs = [dequantize(codes[o["name"]], *qps[o["name"]]) for o in g["outputs"]]

@@ -99,6 +99,21 @@ def test_relu6_bound_in_code_space():
     assert Q.act_bounds(None, 0.05, 3) == (-128, 127)
     with pytest.raises(ValueError):
         Q.act_bounds("gelu", 0.1, 0)
+    assert Q.act_bounds("leaky", 0.05, -100) == (-128, 127)
+
+
+def test_leaky_codes_scale_negative_offsets():
+    """Leaky ReLU on codes is the float leaky ReLU of the dequantized value,
+    re-rounded: exact when alpha * offset is an integer, ties to even."""
+    v = np.arange(-128, 128)
+    z = -20
+    out = Q.leaky_codes(v, z, 0.25)
+    t = v - z
+    assert np.array_equal(out[t >= 0], v[t >= 0])
+    want = z + np.array([_round_half_even(Fraction(int(x), 4)) for x in t[t < 0]])
+    assert np.array_equal(out[t < 0], want)
+    assert Q.leaky_codes(np.array([z - 2]), z, 0.25)[0] == z - 0   # -0.5 -> 0 (even)
+    assert Q.leaky_codes(np.array([z - 6]), z, 0.25)[0] == z - 2   # -1.5 -> -2 (even)
 
 
 @pytest.mark.parametrize("shape,wshape,strides,padding", [
