@@ -61,12 +61,13 @@
  *           their declared "f32" or "bf16" dtype, S (q - Z).  Weights are
  *           quantized per output channel, symmetric (S_w = max|W|/127);
  *           biases become int32 in the accumulator's scale.  Conv and dense
- *           accumulate exactly in int32 on int8 MFMA; every rescaling is a
- *           fixed-point multiply m0 2^-t rounded once, ties away from zero;
- *           activations clamp in code space (ReLU >= Z, ReLU6 <= Z +
- *           rint(6/S)).  A max pool keeps its input's S and Z; depthwise
- *           convs sum exactly on the vector ALU.  Not in int8 graphs: GELU,
- *           leaky ReLU, windowed average pools, concatenation.
+ *           accumulate exactly in int32 on int8 MFMA; every rescaling is
+ *           rint(fl32(fl32(a) * m)) in float32, ties to even, saturated to
+ *           +-2^20; activations act in code space (ReLU >= Z, ReLU6 <= Z +
+ *           rint(6/S); leaky ReLU maps a negative offset t = q - Z to
+ *           rint(fl32(t * alpha))).  A max pool keeps its input's S and Z;
+ *           depthwise convs sum exactly on the vector ALU.  Not in int8
+ *           graphs: GELU, windowed average pools, concatenation.
  * Internally activations of bf16 graphs are NHWC with channels padded to a
  * multiple of 8 (the layout-transform nodes of Sec. 3.2, Fig. 4b, sit at
  * the function boundary); callers always see the declared layouts.

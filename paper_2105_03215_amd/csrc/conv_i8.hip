@@ -303,6 +303,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
       for (int c8 = 0; c8 < 8; ++c8) {
         int v = q.zy + rescale(a[c8], __int_as_float(qc[c8].y));
         if (p.res) v += rescale((int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3))) - q.zr, q.mr);
+        if (q.leaky) v = leaky_code(v, q.zy, q.slope);
         v = min(max(v, q.lo), q.hi);
         out[c8 >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (c8 & 3));
       }

@@ -118,6 +118,14 @@ __device__ __forceinline__ int rescale(int a, float m) {
   return (int)__builtin_amdgcn_fmed3f(__builtin_rintf((float)a * m), -1048576.0f, 1048576.0f);
 }
 
+// Leaky ReLU on an output code: the offset t = v - zy is kept when t >= 0,
+// otherwise it becomes rint(fl32(t * slope)) (ties to even; |t| < 2^24, so
+// the conversion to float32 is exact).
+__device__ __forceinline__ int leaky_code(int v, int zy, float slope) {
+  const int t = v - zy;
+  return t < 0 ? zy + (int)rintf((float)t * slope) : v;
+}
+
 __device__ __forceinline__ int clip_i8(int v) { return min(max(v, -128), 127); }
 
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }

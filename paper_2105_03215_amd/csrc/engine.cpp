@@ -950,6 +950,7 @@ void Planner::plan_node_i8(int ni) {
     std::memcpy(qb.data(), qch.data(), qb.size());
     L.bias = host_blob(std::move(qb));
     d.zx = xv.qzero, d.zy = yv.qzero, d.lo = lo, d.hi = hi;
+    d.leaky = n.act == Act::Leaky, d.slope = n.alpha;
     if (n.residual >= 0) {
       const Value& rv = g.values[n.residual];
       L.res = loc[n.residual];
@@ -1081,6 +1082,8 @@ void Planner::plan_node_i8(int ni) {
     q.zy = yv.qzero;
     q.lo = lo;
     q.hi = hi;
+    q.leaky = n.act == Act::Leaky;
+    q.slope = n.alpha;
     if (n.residual >= 0) {
       const Value& rv = g.values[n.residual];
       L.res = loc[n.residual];
@@ -1146,6 +1149,8 @@ void Planner::plan_node_i8(int ni) {
   a.zy = yv.qzero;
   a.lo = lo;
   a.hi = hi;
+  a.leaky = n.act == Act::Leaky;
+  a.slope = n.alpha;
   if (!rescale_factor(xv.qscale / yv.qscale, &a.ma) || !rescale_factor(bv.qscale / yv.qscale, &a.mb))
     return fail("rescaling factor outside (0, 2^20)");
   L.op = Launch::AddI8;

@@ -509,13 +509,13 @@ Status parse_graph(const char* text, size_t len, const byoc_const* consts, int32
     Status qs = parse_quant(d, where, &ov);
     if (!qs.ok()) return qs;
     if (out_dtype == DType::I8) {
-      // the int8 forms: every tensor quantized, no depthwise, no GELU; a max
+      // the int8 forms: every tensor quantized, no GELU; a max
       // pool keeps its input's codes (and inherits them when none are given)
       for (int a : {n.data, n.residual, n.other}) {
         if (a < 0 || g.values[a].has_q) continue;
         return serr(where + ": int8 operand '" + g.values[a].name + "' has no quant parameters");
       }
-      if (n.act == Act::Gelu || n.act == Act::Leaky)
+      if (n.act == Act::Gelu)
         return uerr(where + ": " + act_name(n.act) + " has no int8 form");
       if (n.op == OpKind::MaxPool) {
         const Value& xv = g.values[n.data];

@@ -189,6 +189,8 @@ struct QConvParams {
   int zy, lo, hi;       // output zero point; activation clamp in output codes (within [-128, 127])
   int zr;               // residual zero point
   float mr;             // residual rescaling factor
+  int leaky;            // leaky ReLU before the clamp: a negative offset from zy is scaled by slope
+  float slope;
 };
 // Tiles: 4 waves (256 threads) 128x128, 128x64, 64x64, 32x64; 8 waves (512)
 // 128x128, 128x64, 64x128; 2 to 4 ring stages.
@@ -225,6 +227,8 @@ struct QDwParams {
   int N, H, W, Cp, P, Q, R, S, sh, sw, pt, pl;
   int zx, zy, lo, hi, zr;
   float mr;
+  int leaky;  // leaky ReLU before the clamp (as in QConvParams)
+  float slope;
 };
 hipError_t launch_depthwise_i8(const QDwParams& p, hipStream_t s);
 // Max pooling of codes, NHWC (padding never wins).
@@ -232,7 +236,7 @@ hipError_t launch_maxpool_nhwc_i8(const PoolParams& p, hipStream_t s);
 // Global average pooling of codes: y[n][c] = clip(zy + rescale(sum(x - zx), m)), y [N][Cp].
 hipError_t launch_avgpool_nhwc_i8(const PoolParams& p, int zx, int zy, float m, hipStream_t s);
 // y = clamp(zy + rescale(a - za, ma) + rescale(b - zb, mb), lo, hi) over n codes
-// ([lo, hi] within [-128, 127]).
+// ([lo, hi] within [-128, 127]; leaky ReLU before the clamp when asked).
 struct QAddParams {
   const int8_t* a;
   const int8_t* b;
@@ -240,6 +244,8 @@ struct QAddParams {
   int64_t n;
   int za, zb, zy, lo, hi;
   float ma, mb;
+  int leaky;  // leaky ReLU before the clamp (as in QConvParams)
+  float slope;
 };
 hipError_t launch_add_i8(const QAddParams& p, hipStream_t s);
 

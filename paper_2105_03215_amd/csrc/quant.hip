@@ -181,6 +181,7 @@ __global__ __launch_bounds__(kThreads) void depthwise_i8_kernel(QDwParams p) {
       const int2 q = qc[j];
       int v = p.zy + rescale(acc[j] + q.x, __int_as_float(q.y));
       if (p.res) v += rescale((int)(int8_t)(rw[j >> 2] >> (8 * (j & 3))) - p.zr, p.mr);
+      if (p.leaky) v = leaky_code(v, p.zy, p.slope);
       v = min(max(v, p.lo), p.hi);
       o[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
     }
@@ -215,7 +216,9 @@ __global__ __launch_bounds__(kThreads) void add_i8_kernel(QAddParams p) {
     for (int j = 0; j < 16; ++j) {
       const int a = (int)(int8_t)(wa[j >> 2] >> (8 * (j & 3)));
       const int b = (int)(int8_t)(wb[j >> 2] >> (8 * (j & 3)));
-      const int v = min(max(p.zy + rescale(a - p.za, p.ma) + rescale(b - p.zb, p.mb), p.lo), p.hi);
+      int v = p.zy + rescale(a - p.za, p.ma) + rescale(b - p.zb, p.mb);
+      if (p.leaky) v = leaky_code(v, p.zy, p.slope);
+      v = min(max(v, p.lo), p.hi);
       o[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
     }
     *(uint4*)(p.y + i * 16) = make_uint4(o[0], o[1], o[2], o[3]);

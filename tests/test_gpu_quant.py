@@ -74,6 +74,8 @@ CONV_CASES = [
     (4, 256, 8, 8, 512, 1, 2, 0, 64, None, True),          # 1x1 stride 2 projection, residual
     (1, 64, 56, 56, 256, 1, 1, 0, -128, "relu6", False),  # many pixels: 128x128 tiles
     (2, 48, 5, 5, 40, 5, 1, 2, 90, "relu6", True),         # tiny image, every pixel on the border
+    (2, 128, 14, 13, 136, 3, 1, 1, -40, "leaky", True),    # leaky ReLU on codes, residual
+    (1, 64, 28, 28, 128, 1, 1, 0, 12, "leaky", False),     # leaky ReLU, 1x1
 ]
 
 
@@ -195,6 +197,7 @@ DW_CASES = [
     (2, 32, 13, 11, 1, 17, "relu6", False),
     (1, 96, 14, 14, 2, -128, "relu6", False),
     (2, 40, 7, 9, 1, 60, None, True),
+    (1, 48, 10, 10, 1, -5, "leaky", True),
 ]
 
 
@@ -253,5 +256,38 @@ def test_int8_vgg19_small_full_compare():
         o["dtype"] = "f32"
     got, launches = _run(qg, wl.consts, wl.inputs)
     assert sum(1 for l in launches if l["kind"] == "conv_i8") == 19
+    ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
+    assert np.array_equal(got[0], ref.astype(np.float64))
+
+
+def test_int8_leaky_slopes_conv_and_add():
+    """Leaky ReLU on codes with non-default slopes, in a conv and an add."""
+    announce("int8 leaky slopes 0.3 (conv), 0.25 (add)")
+    g, consts, inputs = _conv_graph(2, 64, 9, 9, 64, 3, 1, 1, 33, "leaky", False, seed=11)
+    g["nodes"][0]["attrs"]["alpha"] = 0.3
+    g["nodes"].append({"name": "s", "composite": "add_leaky", "inputs": ["y", "y2"], "out_dtype": "int8",
+                       "attrs": {"alpha": 0.25}, "quant": _q(0.031, 14)})
+    g["nodes"].insert(1, {"name": "y2", "composite": "conv2d_leaky", "inputs": ["y", "w"], "out_dtype": "int8",
+                          "attrs": {"strides": [1, 1], "padding": [1, 1, 1, 1], "alpha": 0.05},
+                          "quant": _q(0.027, -60)})
+    g["outputs"] = [{"name": "s", "dtype": "f32"}, {"name": "y", "dtype": "f32"}]
+    got, launches = _run(g, consts, inputs)
+    assert any(l["name"] == "add_i8" for l in launches), [l["name"] for l in launches]
+    ref = OQ.run_quantized_graph(g, consts, inputs)
+    for i in range(2):
+        assert np.array_equal(got[i], ref[i].astype(np.float64)), i
+
+
+def test_int8_darknet53_small_full_compare():
+    """DarkNet-53 (leaky ReLU after every conv, residual adds) in int8."""
+    import torch
+    announce("int8 darknet53 n=2 hw=64")
+    wl = workloads.build("darknet53", n=2, hw=64)
+    batch = [torch.from_numpy(np.ascontiguousarray(wl.inputs[0])).to(DEV).to(torch.bfloat16)]
+    qg = quantize.quantize_graph(wl.graph, quantize.calibrate(wl.graph, wl.consts, [batch]))
+    for o in qg["outputs"]:
+        o["dtype"] = "f32"
+    got, launches = _run(qg, wl.consts, wl.inputs)
+    assert sum(1 for l in launches if l["kind"] == "conv_i8") >= 52
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
     assert np.array_equal(got[0], ref.astype(np.float64))
