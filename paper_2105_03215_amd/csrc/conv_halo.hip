@@ -316,12 +316,14 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
         f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
         f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = act_apply<G>(f[e] + rv[e], ac);
+        for (int e = 0; e < 8; ++e) f[e] = epilogue_value<G>(f[e], rv[e], ac);
         *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
       }
     }
   };
-  if (act_mode(p.act) == 1)
+  if (p.res_post)
+    epilogue(std::integral_constant<int, 3>{});
+  else if (act_mode(p.act) == 1)
     epilogue(std::integral_constant<int, 1>{});
   else if (act_mode(p.act) == 0)
     epilogue(std::integral_constant<int, 0>{});

@@ -395,12 +395,14 @@ __global__ __launch_bounds__(kNT, 2) void conv_mfma_kernel(ConvParams p) {
         f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
         f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = act_apply<G>(f[e] + r[e], ac);
+        for (int e = 0; e < 8; ++e) f[e] = epilogue_value<G>(f[e], r[e], ac);
         *(uint4*)(p.y + (size_t)m * p.ldy + k) = pack8(f);
       }
     }
   };
-  if (act_mode(p.act) == 1)
+  if (p.res_post)
+    epilogue(std::integral_constant<int, 3>{});
+  else if (act_mode(p.act) == 1)
     epilogue(std::integral_constant<int, 1>{});
   else if (act_mode(p.act) == 0)
     epilogue(std::integral_constant<int, 0>{});
@@ -431,16 +433,24 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
     acc.z += bv.z;
     acc.w += bv.w;
   }
+  float r[4] = {0.f, 0.f, 0.f, 0.f};
   if (p.res) {
     const uint2 rr = *(const uint2*)(p.res + (size_t)m * p.ldr + k);
-    acc.x += __uint_as_float(rr.x << 16);
-    acc.y += __uint_as_float(rr.x & 0xFFFF0000u);
-    acc.z += __uint_as_float(rr.y << 16);
-    acc.w += __uint_as_float(rr.y & 0xFFFF0000u);
+    r[0] = __uint_as_float(rr.x << 16);
+    r[1] = __uint_as_float(rr.x & 0xFFFF0000u);
+    r[2] = __uint_as_float(rr.y << 16);
+    r[3] = __uint_as_float(rr.y & 0xFFFF0000u);
   }
-  *(uint2*)(p.y + (size_t)m * p.ldy + k) =
-      make_uint2(pack2_bf16(apply_act(acc.x, p.act, p.alpha), apply_act(acc.y, p.act, p.alpha)),
-                 pack2_bf16(apply_act(acc.z, p.act, p.alpha), apply_act(acc.w, p.act, p.alpha)));
+  float v[4] = {acc.x, acc.y, acc.z, acc.w};
+  if (p.res_post) {
+    const ActClamp ac = act_clamp_of(p.act, p.alpha);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = epilogue_value<3>(v[e], r[e], ac);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = apply_act(v[e] + r[e], p.act, p.alpha);
+  }
+  *(uint2*)(p.y + (size_t)m * p.ldy + k) = make_uint2(pack2_bf16(v[0], v[1]), pack2_bf16(v[2], v[3]));
 }
 
 template <int BM, int BN, int WM, int WN, int MF>

@@ -63,6 +63,17 @@ __device__ __forceinline__ float act_apply(float v, ActClamp a) {
   else
     return __builtin_amdgcn_fmed3f(fmaxf(v, v * a.slope), a.lo, a.hi);
 }
+// One output of a conv epilogue with residual r.  MODE 0-2 as above, the
+// residual added before the activation; MODE 3 (any activation but GELU):
+// the activation first, its output rounded to bf16, then the residual added
+// (the arithmetic of a separate add node reading the conv's output).
+template <int MODE>
+__device__ __forceinline__ float epilogue_value(float v, float r, ActClamp a) {
+  if constexpr (MODE == 3)
+    return bf16_to_f32(f32_to_bf16(act_apply<0>(v, a))) + r;
+  else
+    return act_apply<MODE>(v + r, a);
+}
 // The epilogue mode of an activation code.
 __host__ __device__ constexpr int act_mode(int act) { return act == kActGelu ? 1 : (act == kActLeaky ? 0 : 2); }
 __device__ __forceinline__ float apply_act(float v, int act, float alpha) {
@@ -98,7 +109,7 @@ __device__ __forceinline__ void materialize_args(const ConvParams& p) {
                "s"(p.sh), "s"(p.sw), "s"(p.pt), "s"(p.pl));
   asm volatile("" ::"s"(p.M), "s"(p.Kp), "s"(p.Kg), "s"(p.Kgp), "s"(p.ldy), "s"(p.ldr), "s"(p.act), "s"(p.alpha),
                "s"(p.splits), "s"(p.k_tiles_per_split), "s"(p.x_bytes), "s"(p.w_bytes), "s"(p.res_bytes),
-               "s"(p.xcd_py));
+               "s"(p.res_post), "s"(p.xcd_py));
   asm volatile("" ::"s"(p.mg_pq), "s"(p.mg_q), "s"(p.mg_cp), "s"(p.mg_s), "s"(p.mg_tile), "s"(p.mg_wp),
                "s"(p.mg_hp));
 }

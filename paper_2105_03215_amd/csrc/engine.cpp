@@ -191,6 +191,7 @@ struct Planner {
   Status err;
   // fused stems: conv node -> its max-pool node, max-pool node -> conv node
   std::vector<int> stem_pool, stem_conv;
+  std::vector<int> post_add, post_conv;  // conv -> the add folded into it, and back
   // zero-copy concatenation: value -> the concatenation it is written into
   // (-1: none) and its first channel there
   std::vector<int> alias_of, alias_off;
@@ -257,6 +258,7 @@ struct Planner {
   Status plan_i8();
   void plan_node(int ni);
   void plan_node_i8(int ni);
+  void find_post_adds();
   void find_stems();
   void find_concat_aliases();
   Ref slice(int vcat, int channel) const {  // channel slice of a concatenation's buffer
@@ -384,10 +386,47 @@ void Planner::find_concat_aliases() {
   }
 }
 
+// A bf16 add reading a conv's activated output that nothing else reads (the
+// residual of DarkNet's blocks comes after the leaky ReLU) folds into that
+// conv: the conv is planned at the add, writes the add's output and adds the
+// other operand to its bf16-rounded activation, which is the add's own
+// arithmetic.  BYOC_FUSE_POST_ADD=0 keeps the two launches.
+void Planner::find_post_adds() {
+  post_add.assign(g.nodes.size(), -1);
+  post_conv.assign(g.nodes.size(), -1);
+  const char* env = std::getenv("BYOC_FUSE_POST_ADD");
+  if (!bf16 || (env && env[0] == '0')) return;
+  std::vector<int> uses(g.values.size(), 0);
+  for (const Node& n : g.nodes) {
+    for (int a : {n.data, n.residual, n.other})
+      if (a >= 0) ++uses[a];
+    if (n.op == OpKind::Concat)
+      for (size_t k = 1; k < n.cat.size(); ++k) ++uses[n.cat[k]];
+  }
+  for (const IoDesc& o : g.outputs) ++uses[o.value];
+  for (size_t ai = 0; ai < g.nodes.size(); ++ai) {
+    const Node& a = g.nodes[ai];
+    if (a.op != OpKind::Add || a.act != Act::None) continue;
+    for (int v : {a.data, a.other}) {
+      const Value& cv = g.values[v];
+      if (cv.source != Value::Node || uses[v] != 1 || alias_of[v] >= 0 || cv.shape.size() != 4) continue;
+      const int ci = cv.index;
+      const Node& c = g.nodes[ci];
+      if (c.op != OpKind::Conv || c.depthwise || c.residual >= 0 || c.act == Act::Gelu) continue;
+      if (stem_pool[ci] >= 0 || stem_conv[ci] >= 0 || post_add[ci] >= 0) continue;
+      if (cv.shape[2] * cv.shape[3] == 1) continue;  // the dense-rows form keeps its own epilogue
+      post_add[ci] = (int)ai;
+      post_conv[ai] = ci;
+      break;
+    }
+  }
+}
+
 Status Planner::plan() {
   if (i8) return plan_i8();
   find_stems();
   find_concat_aliases();
+  find_post_adds();
   // concatenation outputs are allocated first: their producers write into them
   for (const Node& n : g.nodes)
     if (n.op == OpKind::Concat) {
@@ -456,7 +495,7 @@ Status Planner::plan() {
         placed = true;
       }
     }
-    if (stem_pool[ni] >= 0) {  // conv of a fused stem: its output is never stored
+    if (stem_pool[ni] >= 0 || post_add[ni] >= 0) {  // planned with the node that consumes it
       loc[v] = Ref();
       continue;
     }
@@ -468,6 +507,8 @@ Status Planner::plan() {
     if (!placed) loc[v] = arena(internal_bytes(v));
     if (stem_conv[ni] >= 0)
       plan_stem(stem_conv[ni], (int)ni);
+    else if (post_conv[ni] >= 0)
+      plan_node(post_conv[ni]);
     else
       plan_node((int)ni);
     if (!err.ok()) return err;
@@ -516,6 +557,12 @@ void Planner::plan_node(int ni) {
   L.act = (int)n.act;
   L.alpha = n.alpha;
   if (n.residual >= 0) L.res = loc[n.residual];
+  const int pa = post_add.empty() ? -1 : post_add[ni];  // add folded in after the activation
+  if (pa >= 0) {
+    const Node& a = g.nodes[pa];
+    L.y = loc[a.out];
+    L.res = loc[a.data == n.out ? a.other : a.data];
+  }
   const int64_t ebytes = bf16 ? 2 : 4;
 
   if (n.op == OpKind::Conv || n.op == OpKind::Dense) {
@@ -535,7 +582,7 @@ void Planner::plan_node(int ni) {
     const int bc = n.bias >= 0 ? g.values[n.bias].index : -1;
     L.info.flops = 2 * n.macs;
     L.info.bytes = act_bytes(n.data) + numel(ws) * ebytes + (bc >= 0 ? K * 4 : 0) +
-                   act_bytes(n.out) * (n.residual >= 0 ? 2 : 1);
+                   act_bytes(n.out) * (n.residual >= 0 || pa >= 0 ? 2 : 1);
     if (!bf16) {
       L.op = Launch::ConvF32;
       L.info.kind = BYOC_K_CONV_F32;
@@ -582,6 +629,7 @@ void Planner::plan_node(int ni) {
     p.ldr = Kp;
     p.act = (int)n.act;
     p.alpha = n.alpha;
+    p.res_post = pa >= 0;
     const int rows = (int)rup(Kp, kRowPad);
     const int64_t xb = (int64_t)N * H * W * Cp * 2, wb = (int64_t)rows * p.Kgp * 2;
     if (xb >= (int64_t(1) << 31) || wb >= (int64_t(1) << 31)) {

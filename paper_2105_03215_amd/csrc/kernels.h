@@ -37,6 +37,7 @@ struct ConvParams {
   int x_bytes;  // extent of x, w and res in bytes (buffer-load range; < 2^31)
   int w_bytes;
   int res_bytes;
+  int res_post;  // 1: the residual is added after the activation, to its bf16-rounded value
   // conv_dma tile placement: > 0 splits the tile grid into (8 / xcd_py) x
   // xcd_py blocks along (pixels, channels), one per XCD, so that an XCD's L2
   // holds only its share of both operands; 0 deals tiles out linearly.

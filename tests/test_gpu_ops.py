@@ -384,3 +384,38 @@ def test_concat_all_in_place():
     g.output(g.conv(c, 16, 1, name="y"))
     launches = _check_bf16(g.finish(), "concat all in place")
     assert "concat_copy" not in [l["name"] for l in launches]
+
+
+POST_ADD_PATHS = [
+    ("default", {}),
+    ("halo", {"BYOC_CONV_TILE": "h128x64s3"}),
+    ("register_staged", {"BYOC_CONV_TILE": "64x64"}),
+    ("split_k", {"BYOC_CONV_TILE": "64x64", "BYOC_CONV_SPLIT": "2"}),
+]
+
+
+@pytest.mark.parametrize("path", POST_ADD_PATHS, ids=[p[0] for p in POST_ADD_PATHS])
+def test_post_activation_add_folds_into_conv(path, monkeypatch):
+    """An add after a conv's activation (DarkNet's residual) runs inside the
+    conv's epilogue on every conv kernel, bit-identical to the two launches."""
+    name, env = path
+    g = GraphBuilder("op_post_add", 1950)
+    x = g.input("x", [2, 64, 14, 13], "normal")
+    a = g.conv(x, 32, 1, act="leaky", name="a")
+    b = g.conv(a, 64, 3, act="leaky", name="b")
+    s = g.add(x, b, name="s")          # the conv is the second operand
+    c = g.conv(s, 32, 1, act="relu", name="c")
+    d = g.conv(c, 64, 3, act="leaky", name="d")
+    t = g.add(d, s, name="t")          # the conv is the first operand
+    g.output(t)
+    wl = g.finish()
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    launches = _check_bf16(wl, "post-activation add, %s path" % name)
+    names = [l["name"] for l in launches]
+    assert not any(n.startswith("add_") for n in names), names
+    fused, _ = _run_gpu(wl)
+    monkeypatch.setenv("BYOC_FUSE_POST_ADD", "0")
+    plain, plain_launches = _run_gpu(wl)
+    assert sum(1 for l in plain_launches if l["name"].startswith("add_")) == 2
+    assert np.array_equal(fused[0], plain[0])
