@@ -419,3 +419,18 @@ def test_post_activation_add_folds_into_conv(path, monkeypatch):
     plain, plain_launches = _run_gpu(wl)
     assert sum(1 for l in plain_launches if l["name"].startswith("add_")) == 2
     assert np.array_equal(fused[0], plain[0])
+
+
+def test_post_activation_add_not_folded():
+    """The fold needs the conv's output to be read by the add alone, and the
+    add to carry no activation of its own; otherwise both launches stay."""
+    g = GraphBuilder("op_post_add_kept", 1960)
+    x = g.input("x", [1, 32, 9, 11], "normal")
+    b = g.conv(x, 32, 3, act="leaky", name="b")
+    s = g.add(x, b, name="s")            # b is also a graph output
+    c = g.conv(s, 32, 3, act="relu", name="c")
+    t = g.add(c, s, act="relu", name="t")  # the add has an activation
+    g.output(t)
+    g.output(b)
+    launches = _check_bf16(g.finish(), "post-activation adds that stay separate")
+    assert sum(1 for l in launches if l["name"].startswith("add_")) == 2

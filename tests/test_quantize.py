@@ -71,6 +71,15 @@ def test_int8_schema_accepts_inherited_pool_quant():
     capi.validate(g, consts)
 
 
+def test_int8_schema_accepts_leaky():
+    """Leaky ReLU has an int8 form (on the offset from the zero point)."""
+    g, consts = _mut(lambda g: g["nodes"][0].__setitem__("composite", g["nodes"][0]["composite"] + "_leaky")
+                     if not g["nodes"][0]["composite"].endswith(("relu", "relu6")) else
+                     g["nodes"][0].__setitem__("composite", g["nodes"][0]["composite"].rsplit("_", 1)[0] + "_leaky"))
+    assert g["nodes"][0]["composite"].endswith("_leaky")
+    capi.validate(g, consts)
+
+
 def test_quant_only_in_int8_graphs():
     g, consts = _tiny_int8_graph()
     gf = copy.deepcopy(g)
