@@ -182,7 +182,7 @@ def _partitioned(args, wl, dev, stream):
             "node_offload": round(st["node_offload"], 4), "mac_offload": round(st["mac_offload"], 4)}
 
 
-def _quantized(args, wl, dev, stream, calib_images=2):
+def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
     """The same network partially quantized (Sec. 3.2, Fig. 4a): scales and
     zero points calibrated through the executor on a few images, int8 codes
     inside the function, quantize / dequantize at its boundary.  Same
@@ -195,6 +195,7 @@ def _quantized(args, wl, dev, stream, calib_images=2):
 
     from paper_2105_03215_amd import capi, quantize, runtime
 
+    variant = variant or args.variant
     t0 = time.perf_counter()
     cal = copy.deepcopy(wl.graph)
     cal["inputs"] = [dict(d, shape=[calib_images] + d["shape"][1:]) for d in cal["inputs"]]
@@ -219,7 +220,7 @@ def _quantized(args, wl, dev, stream, calib_images=2):
         per_launch, _ = _profile(sg, ins, outs, stream, args.steps)
     finally:
         sg.close()
-    if args.dump_launches:
+    if args.dump_launches and variant == args.variant:
         root, ext = os.path.splitext(args.dump_launches)
         with open(root + "_int8" + ext, "w") as f:
             json.dump([dict(l, ms=round(t, 5)) for l, t in zip(launches, per_launch)], f, indent=1)
@@ -234,10 +235,10 @@ def _quantized(args, wl, dev, stream, calib_images=2):
         from paper_2105_03215_amd import profiling
         with open(tpath) as f:
             tj = json.load(f)
-        if (tj.get("workload") == "%s_bs%d_int8" % (args.variant, n)
+        if (tj.get("workload") == "%s_bs%d_int8" % (variant, n)
                 and tj.get("conv_kernel_digest") == profiling.conv_kernel_digest(profiling.I8_SOURCES)):
             traffic = tj.get("conv_bytes_per_step")
-    return {"workload": "%s_bs%d_int8" % (args.variant, n), "images_per_s": round(n / (ms * 1e-3), 1),
+    return {"workload": "%s_bs%d_int8" % (variant, n), "images_per_s": round(n / (ms * 1e-3), 1),
             "ms_per_step": round(ms, 4), "dtype": "int8 codes, int32 accumulation",
             "calibration": "%d images through the executor, %.2f s" % (calib_images, calib_s),
             "roofline": {"bound": "mfma", "achieved": round(tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
@@ -274,9 +275,17 @@ def _other_workload(args, name, batch, dev, stream):
     finally:
         sg.close()
     roof = _roofline(launches, per_launch, ms)
-    return {"workload": "%s_bs%d" % (name, batch), "images_per_s": round(batch / (ms * 1e-3), 1),
-            "ms_per_step": round(ms, 4), "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
-            "conv_tflops": roof["achieved"], "conv_frac": roof["frac"], "launches": len(launches)}
+    out = {"workload": "%s_bs%d" % (name, batch), "images_per_s": round(batch / (ms * 1e-3), 1),
+           "ms_per_step": round(ms, 4), "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
+           "conv_tflops": roof["achieved"], "conv_frac": roof["frac"], "launches": len(launches)}
+    if not args.no_quantized:  # the same network partially quantized, as the headline's int8 leg
+        try:
+            q = _quantized(args, wl, dev, stream, variant=name)
+            out["int8"] = {"images_per_s": q["images_per_s"], "ms_per_step": q["ms_per_step"],
+                           "conv_tops": q["roofline"]["achieved"], "conv_frac": q["roofline"]["frac"]}
+        except capi.ByocError as e:  # operators without an int8 form
+            out["int8"] = {"skipped": str(e)}
+    return out
 
 
 def main():
