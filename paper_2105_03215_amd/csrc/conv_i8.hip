@@ -302,9 +302,11 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
 #pragma unroll
       for (int c8 = 0; c8 < 8; ++c8) {
         int v = q.zy + rescale(a[c8], __int_as_float(qc[c8].y));
-        if (p.res) v += rescale((int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3))) - q.zr, q.mr);
+        const int rc = (int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3)));
+        if (p.res && !q.post) v += rescale(rc - q.zr, q.mr);
         if (q.leaky) v = leaky_code(v, q.zy, q.slope);
         v = min(max(v, q.lo), q.hi);
+        if (q.post) v = clip_i8(q.pz + rescale(v - q.zy, q.pm) + rescale(rc - q.zr, q.mr));
         out[c8 >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (c8 & 3));
       }
       *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) = make_uint2(out[0], out[1]);

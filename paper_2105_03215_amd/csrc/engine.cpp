@@ -395,7 +395,7 @@ void Planner::find_post_adds() {
   post_add.assign(g.nodes.size(), -1);
   post_conv.assign(g.nodes.size(), -1);
   const char* env = std::getenv("BYOC_FUSE_POST_ADD");
-  if (!bf16 || (env && env[0] == '0')) return;
+  if (!(bf16 || i8) || (env && env[0] == '0')) return;
   std::vector<int> uses(g.values.size(), 0);
   for (const Node& n : g.nodes) {
     for (int a : {n.data, n.residual, n.other})
@@ -409,12 +409,15 @@ void Planner::find_post_adds() {
     if (a.op != OpKind::Add || a.act != Act::None) continue;
     for (int v : {a.data, a.other}) {
       const Value& cv = g.values[v];
-      if (cv.source != Value::Node || uses[v] != 1 || alias_of[v] >= 0 || cv.shape.size() != 4) continue;
+      if (cv.source != Value::Node || uses[v] != 1 || cv.shape.size() != 4) continue;
+      if (!alias_of.empty() && alias_of[v] >= 0) continue;
       const int ci = cv.index;
       const Node& c = g.nodes[ci];
       if (c.op != OpKind::Conv || c.depthwise || c.residual >= 0 || c.act == Act::Gelu) continue;
-      if (stem_pool[ci] >= 0 || stem_conv[ci] >= 0 || post_add[ci] >= 0) continue;
-      if (cv.shape[2] * cv.shape[3] == 1) continue;  // the dense-rows form keeps its own epilogue
+      if (post_add[ci] >= 0) continue;
+      if (!stem_pool.empty() && (stem_pool[ci] >= 0 || stem_conv[ci] >= 0)) continue;
+      if (i8 && im2col_of[c.data] == ci) continue;     // the stem form of the int8 conv
+      if (!i8 && cv.shape[2] * cv.shape[3] == 1) continue;  // the dense-rows form keeps its own epilogue
       post_add[ci] = (int)ai;
       post_conv[ai] = ci;
       break;
@@ -902,11 +905,16 @@ Status Planner::plan_i8() {
     name(L, "quantize_in");
     e->launches.push_back(L);
   }
+  find_post_adds();
   for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
     const int v = g.nodes[ni].out;
     cp[v] = (int)rup(g.values[v].shape[1], 16);
+    if (post_add[ni] >= 0) {  // planned at the add folded into it
+      loc[v] = Ref();
+      continue;
+    }
     loc[v] = arena(internal_bytes(v));
-    plan_node_i8((int)ni);
+    plan_node_i8(post_conv[ni] >= 0 ? post_conv[ni] : (int)ni);
     if (!err.ok()) return err;
   }
   for (size_t j = 0; j < g.outputs.size(); ++j) {
@@ -1137,6 +1145,19 @@ void Planner::plan_node_i8(int ni) {
       L.res = loc[n.residual];
       q.zr = rv.qzero;
       if (!rescale_factor(rv.qscale / sy, &q.mr)) return fail("residual rescaling factor outside (0, 2^20)");
+    }
+    const int pa = post_add.empty() ? -1 : post_add[ni];
+    if (pa >= 0) {  // the add that follows, folded in: it writes the add's output
+      const Node& a = g.nodes[pa];
+      const Value& ov = g.values[a.data == n.out ? a.other : a.data];
+      const Value& av = g.values[a.out];
+      L.y = loc[a.out];
+      L.res = loc[a.data == n.out ? a.other : a.data];
+      q.post = 1;
+      q.pz = av.qzero;
+      q.zr = ov.qzero;
+      if (!rescale_factor(sy / av.qscale, &q.pm) || !rescale_factor(ov.qscale / av.qscale, &q.mr))
+        return fail("rescaling factor of the folded add outside (0, 2^20)");
     }
     // tile: the largest with at least two workgroups per CU
     auto tiles = [&](int bm, int bn) { return ((int64_t)p.M + bm - 1) / bm * ((Kp + bn - 1) / bn); };

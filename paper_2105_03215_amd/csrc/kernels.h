@@ -192,6 +192,11 @@ struct QConvParams {
   float mr;             // residual rescaling factor
   int leaky;            // leaky ReLU before the clamp: a negative offset from zy is scaled by slope
   float slope;
+  // A following add folded in (post = 1): after the clamp, the conv's code c
+  // becomes clip(pz + rescale(c - zy, pm) + rescale(res - zr, mr)), the add's
+  // own arithmetic; res is then the add's other operand, not a residual.
+  int post, pz;
+  float pm;
 };
 // Tiles: 4 waves (256 threads) 128x128, 128x64, 64x64, 32x64; 8 waves (512)
 // 128x128, 128x64, 64x128; 2 to 4 ring stages.

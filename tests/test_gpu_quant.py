@@ -289,5 +289,15 @@ def test_int8_darknet53_small_full_compare():
         o["dtype"] = "f32"
     got, launches = _run(qg, wl.consts, wl.inputs)
     assert sum(1 for l in launches if l["kind"] == "conv_i8") >= 52
+    # every residual add follows a conv's leaky ReLU and is folded into it
+    assert not any(l["name"] == "add_i8" for l in launches)
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
     assert np.array_equal(got[0], ref.astype(np.float64))
+    import os
+    os.environ["BYOC_FUSE_POST_ADD"] = "0"
+    try:
+        plain, plain_launches = _run(qg, wl.consts, wl.inputs)
+    finally:
+        del os.environ["BYOC_FUSE_POST_ADD"]
+    assert sum(1 for l in plain_launches if l["name"] == "add_i8") == 23
+    assert np.array_equal(plain[0], got[0])
