@@ -253,7 +253,7 @@ def test_avg_pool_closed_forms():
     # without padding, a window covering the image is the global mean
     z = _rand(2 * 3 * 4 * 4).reshape(2, 3, 4, 4)
     np.testing.assert_allclose(ops.avg_pool2d(z, (4, 4), (1, 1), (0, 0, 0, 0))[:, :, 0, 0],
-                               ops.global_avg_pool2d(z), rtol=1e-15)
+                               ops.global_avg_pool2d(z), rtol=1e-13)  # same 16 terms, summed in another order
 
 
 def test_concatenate_slices_back():
