@@ -1,14 +1,29 @@
-"""Throughput of the offloaded ResNet-50 v1 subgraph on one MI355X.
+"""Throughput of offloaded subgraphs on one MI355X.
 
-One step = one run of the whole offloaded subgraph (input layout transform,
-53 conv composites, max-pool, global average pool, classifier) over a batch
-of 32 synthetic 3x224x224 images already resident in HBM.  Prints one JSON
-line with images/s, the roofline of the dominant kernel class (the bf16 MFMA
-implicit-GEMM conv/dense kernels) measured with per-launch HIP events on the
-run stream, the batch-1 figures, the same network as an operator-level
-model partitioned for the executor and run by the partitioned-model runtime
-with a host softmax head, and the CPU oracle timed on a bounded sample of the
-same workload.
+One step = one run of the whole offloaded subgraph over one batch of
+synthetic input already resident in HBM.  The headline is ResNet-50 v1 at
+batch 32 (input layout transform, 53 conv composites, max-pool, global
+average pool, classifier); the line also carries the other workloads the
+method is measured on, each timed the same way (engine autotune on, HIP-graph
+replay of the launch sequence on a side stream):
+
+  configs      the single fp32 conv composite (us per call), the ResNet-18
+               basic block (us per block), ResNet-50 at batch 1, MobileNetV2
+               at batch 1 and 16 (depthwise / pooling HBM GB/s), the
+               BERT-base-shaped FFN stack (tokens/s, fraction of MFMA peak);
+  timing       warm (back-to-back) and cold (a 512 MiB buffer written before
+               every run, evicting L2 and the 256 MB MALL) per-step times of
+               the headline, median / p10 / p90;
+  roofline     the dominant kernel class (the bf16 MFMA conv/dense kernels)
+               from per-launch HIP events on the run stream;
+  partitioned  the network as an operator-level model through the
+               partitioner and the partitioned-model runtime;
+  quantized    the network partially quantized to int8;
+  other_workloads  VGG19, DarkNet-53, Inception V3 at batch 32;
+  cpu_baseline the oracle timed on this host on the headline workload; the
+               same leg also evaluates the oracle on every timed workload
+               (sampled for the large ones) and reports each one's parity
+               error next to its tolerance.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -24,11 +39,23 @@ sys.path.insert(0, ROOT)
 
 METRIC = "images/sec (bs1, bs32) ResNet-50 offloaded subgraph; conv TFLOP/s as % MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6  # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
-PEAK_INT8_TOPS = 5033.2  # dense int8 MFMA: 256 CU x 2.4 GHz x 8192 OP/clk
+PEAK_F32_TFLOPS = 157.3    # fp32 (vector / MFMA)
+PEAK_INT8_TOPS = 5033.2    # dense int8 MFMA: 256 CU x 2.4 GHz x 8192 OP/clk
 PEAK_HBM_GBS = 8000.0
+BF16_TOL, F32_TOL = 1e-2, 1e-4
+EVICT_MIB = 512            # > the 256 MB MALL plus every L2
+
+
+def _pct(xs):
+    import numpy as np
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 5), "p10": round(float(np.percentile(a, 10)), 5),
+            "p90": round(float(np.percentile(a, 90)), 5), "n": int(a.size)}
 
 
 def _timed_runs(sg, ins, outs, stream, steps):
+    """Mean ms per run over `steps` back-to-back runs, one HIP event pair on
+    the run stream around all of them (the contract's K timed steps)."""
     import torch
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
@@ -42,6 +69,40 @@ def _timed_runs(sg, ins, outs, stream, steps):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return start.elapsed_time(end) / steps, wall
+
+
+def _per_step(sg, ins, outs, stream, steps, evict=None):
+    """ms of each run from its own event pair on the run stream; with
+    `evict`, that buffer is overwritten on the run stream before every run,
+    outside the pair (cold caches)."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for a, b in evs:
+            if evict is not None:
+                evict.fill_(1.0)
+            a.record(stream)
+            sg.run(ins, outs, stream)
+            b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
+
+
+def _grouped(sg, ins, outs, stream, groups, per_group):
+    """ms per run for latency-bound engines: `groups` event pairs around
+    `per_group` back-to-back runs each."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(groups)]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for a, b in evs:
+            a.record(stream)
+            for _ in range(per_group):
+                sg.run(ins, outs, stream)
+            b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) / per_group for a, b in evs]
 
 
 def _profile(sg, ins, outs, stream, steps):
@@ -80,12 +141,15 @@ def _roofline(launches, per_launch_ms, step_ms, traffic=None):
                        "splitk_reduce kernels), %d launches per step" % n_conv),
             "flops_per_step": conv_flops, "kernel_ms_per_step": round(conv_ms, 4),
             "per_launch_event_ms_per_step": round(conv_ev_ms, 4),
-            "per_launch_event_frac": round(conv_flops / (conv_ev_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "per_launch_event_frac": round(conv_flops / (conv_ev_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+            if conv_ev_ms > 0 else None,
             "layer_floor_ms_per_step": round(floor_ms, 4),
             "frac_of_layer_floor": round(floor_ms / conv_ms, 4)}
 
 
 def _class_summary(launches, per_launch_ms):
+    """Per kernel class: launches, ms per run, algorithmic bytes and flops,
+    and the achieved rates against the HBM and bf16 MFMA peaks."""
     out = {}
     for l, t in zip(launches, per_launch_ms):
         d = out.setdefault(l["kind"], {"launches": 0, "ms": 0.0, "flops": 0, "bytes": 0})
@@ -96,6 +160,7 @@ def _class_summary(launches, per_launch_ms):
     for d in out.values():
         d["ms"] = round(d["ms"], 4)
         d["gbs"] = round(d["bytes"] / (d["ms"] * 1e-3) / 1e9, 1) if d["ms"] > 0 else None
+        d["hbm_frac"] = round(d["gbs"] / PEAK_HBM_GBS, 4) if d["gbs"] else None
         d["tflops"] = round(d["flops"] / (d["ms"] * 1e-3) / 1e12, 2) if d["ms"] > 0 else None
     return out
 
@@ -120,24 +185,207 @@ def _copy_calibration(mib):
     torch.cuda.synchronize()
 
 
-def _cpu_baseline(wl, images):
-    """The oracle (bf16io mode, float64 NumPy) on the first `images` images
-    of the workload, on this host's cores."""
+class Measured:
+    """One workload as the benchmark runs it: engine, autotune, graph replay
+    on the run stream, timing, per-launch profile and the host copy of the
+    outputs of the timed configuration (for the parity report)."""
+
+    def __init__(self, key, wl, sg, ms, launches, per_launch, outputs):
+        self.key, self.wl, self.ms = key, wl, ms
+        self.launches, self.per_launch, self.outputs = launches, per_launch, outputs
+
+
+def _measure(args, key, wl, dev, stream, timing="steps", graph=None, consts=None):
+    """Create the engine, tune it, time it, profile it, keep its outputs.
+    timing: "steps" (one event pair around args.steps runs), "grouped"
+    (20 pairs around 100 runs each: latency-bound engines)."""
+    import torch
+
+    from paper_2105_03215_amd import capi, runtime
+
+    sg = capi.Subgraph(graph or wl.graph, consts or wl.consts, device=0)
+    try:
+        ins = runtime.inputs_for(sg, wl.inputs, dev)
+        outs = runtime.outputs_for(sg, dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        if not args.no_autotune:
+            sg.set_options(autotune=True)
+        tune_s = time.perf_counter() - t0
+        sg.set_options(graph_replay=not args.eager)
+        for _ in range(args.warmup):
+            sg.run(ins, outs, stream)
+        torch.cuda.synchronize()
+        res = {"tune_s": round(tune_s, 3)}
+        if timing == "grouped":
+            per = _grouped(sg, ins, outs, stream, 20, 100)
+            res["ms"] = _pct(per)
+            ms = res["ms"]["median"]
+        else:
+            ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
+        host = [runtime.to_host_f64(o) for o in outs]
+        sg.set_options(graph_replay=False)
+        launches = sg.launches()
+        per_launch, _ = _profile(sg, ins, outs, stream, min(args.steps, 20))
+    finally:
+        sg.close()
+    m = Measured(key, wl, None, ms, launches, per_launch, host)
+    m.extra = res
+    return m
+
+
+def _config_lines(args, dev, stream):
+    """configs[0], [1], [3], [4] of the benchmark set and ResNet-50 batch 1:
+    the latency-bound ones as us per call (median of 20 groups of 100 runs),
+    the others as throughput; each with its kernel classes."""
+    from paper_2105_03215_amd import workloads
+
+    out, measured = {}, []
+
+    m = _measure(args, "conv_f32", workloads.build("conv_f32"), dev, stream, timing="grouped")
+    measured.append(m)
+    fl = sum(l["flops"] for l in m.launches)
+    out["conv_f32"] = {
+        "config": "single conv2d 3x3 + bias + ReLU, fp32, 1x16x32x32 -> 32 channels",
+        "us_per_call": round(m.ms * 1e3, 2), "us_per_call_p10_p90": [round(m.extra["ms"]["p10"] * 1e3, 2),
+                                                                      round(m.extra["ms"]["p90"] * 1e3, 2)],
+        "gflops": round(fl / (m.ms * 1e-3) / 1e9, 2), "dtype": "f32",
+        "roofline": {"bound": "launch latency", "note": "%.1f MFLOP: %.3f us at the fp32 peak of %.1f TFLOP/s"
+                     % (fl / 1e6, fl / (PEAK_F32_TFLOPS * 1e12) * 1e6, PEAK_F32_TFLOPS)},
+        "launches": len(m.launches)}
+
+    m = _measure(args, "resnet18_block", workloads.build("resnet18_block"), dev, stream, timing="grouped")
+    measured.append(m)
+    fl = sum(l["flops"] for l in m.launches)
+    tf = fl / (m.ms * 1e-3) / 1e12
+    out["resnet18_block"] = {
+        "config": "ResNet-18 basic block, bf16, 1x64x56x56 (conv3x3+bias+ReLU, conv3x3+bias+residual+ReLU)",
+        "us_per_block": round(m.ms * 1e3, 2), "us_p10_p90": [round(m.extra["ms"]["p10"] * 1e3, 2),
+                                                             round(m.extra["ms"]["p90"] * 1e3, 2)],
+        "tflops": round(tf, 2), "mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4), "launches": len(m.launches),
+        "kernel_classes": _class_summary(m.launches, m.per_launch)}
+
+    if not args.no_bs1 and not (args.variant == "resnet50_v1" and args.batch == 1):
+        m = _measure(args, "resnet50_v1_bs1", workloads.build("resnet50_v1", n=1), dev, stream, timing="grouped")
+        measured.append(m)
+        fl = sum(l["flops"] for l in m.launches if l["kind"] == "conv_mfma")
+        out["resnet50_v1_bs1"] = {
+            "images_per_s": round(1.0 / (m.ms * 1e-3), 1), "ms_per_step": round(m.ms, 4),
+            "ms_p10_p90": [m.extra["ms"]["p10"], m.extra["ms"]["p90"]],
+            "conv_tflops": round(fl / (m.ms * 1e-3) / 1e12, 2), "launches": len(m.launches),
+            "launch_mode": "direct launches" if args.eager else "HIP graph replay"}
+
+    for n in (1, 16):
+        m = _measure(args, "mobilenet_v2_bs%d" % n, workloads.build("mobilenet_v2", n=n), dev, stream,
+                     timing="grouped" if n == 1 else "steps")
+        measured.append(m)
+        cls = _class_summary(m.launches, m.per_launch)
+        fl = sum(l["flops"] for l in m.launches if l["kind"] == "conv_mfma")
+        out["mobilenet_v2_bs%d" % n] = {
+            "images_per_s": round(n / (m.ms * 1e-3), 1), "ms_per_step": round(m.ms, 4),
+            "conv_tflops": round(fl / (m.ms * 1e-3) / 1e12, 2), "launches": len(m.launches),
+            "depthwise": {k: cls["depthwise"][k] for k in ("launches", "ms", "bytes", "gbs", "hbm_frac")},
+            "kernel_classes": cls}
+
+    m = _measure(args, "bert_ffn", workloads.build("bert_ffn"), dev, stream)
+    measured.append(m)
+    fl = sum(l["flops"] for l in m.launches)
+    tf = fl / (m.ms * 1e-3) / 1e12
+    out["bert_ffn"] = {
+        "config": "BERT-base FFN x12, 1024 tokens (batch 8 x seq 128), hidden 768 -> 3072 (GELU) -> 768 + residual",
+        "tokens_per_s": round(1024 / (m.ms * 1e-3), 1), "ms_per_step": round(m.ms, 4),
+        "tflops": round(tf, 2), "mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4), "launches": len(m.launches),
+        "kernel_classes": _class_summary(m.launches, m.per_launch)}
+    return out, measured
+
+
+def _cpu_info():
+    """CPU model, NumPy's BLAS and the threads its pool runs."""
+    info = {}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    info["cpu_model"] = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        import numpy as np
+        blas = np.__config__.CONFIG["Build Dependencies"]["blas"]
+        info["numpy_blas"] = "%s %s" % (blas.get("name"), blas.get("version"))
+    except Exception:  # noqa: BLE001 - build metadata is optional
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        info["blas_pools"] = [{"api": p.get("internal_api"), "threads": p.get("num_threads"),
+                               "version": p.get("version")} for p in threadpool_info()]
+    except Exception:  # noqa: BLE001
+        pass
+    return info
+
+
+def _sampled(wl, rows):
+    import numpy as np
+    g = dict(wl.graph)
+    g["inputs"] = [dict(d, shape=[len(rows)] + list(d["shape"][1:])) for d in wl.graph["inputs"]]
+    return g, [np.ascontiguousarray(a[rows]) for a in wl.inputs]
+
+
+def _cpu_baseline_leg(headline, measured, cpu_images):
+    """The oracle (NumPy float64) on this host: timed on the headline
+    workload (the cpu_baseline), and evaluated on every timed workload to
+    report the parity error of the outputs the GPU produced in its timed
+    configuration.  The only place the benchmark runs the oracle."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
     import oracle
+
+    def err_of(got, ref):
+        return float(np.max(np.abs(np.asarray(got) - ref) / (np.abs(ref) + 1.0)))
+
     cores = len(os.sched_getaffinity(0))
-    graph = dict(wl.graph)
-    graph["inputs"] = [dict(d, shape=[images] + d["shape"][1:]) for d in wl.graph["inputs"]]
-    x = [np.ascontiguousarray(a[:images]) for a in wl.inputs]
+    parity = {}
     with threadpool_limits(limits=cores):
+        n = headline.wl.inputs[0].shape[0]
+        rows = list(range(min(cpu_images, n)))
+        g, x = _sampled(headline.wl, rows)
         t0 = time.perf_counter()
-        oracle.run_graph(graph, wl.consts, x, mode="bf16io")
+        ref = oracle.run_graph(g, headline.wl.consts, x, mode="bf16io")[0]
         dt = time.perf_counter() - t0
-    return {"value": round(images / dt, 4), "unit": "images/s", "cores": cores, "kind": "oracle",
-            "sample": "%d of the 32 images, one oracle call (NumPy float64, bf16io), %.1f s"
-                      % (images, dt)}
+        parity[headline.key] = {"err": err_of(headline.outputs[0][rows], ref), "tol": BF16_TOL,
+                                "sample": "%d of %d images" % (len(rows), n), "mode": "bf16io",
+                                "oracle_s": round(dt, 2)}
+        cpu = {"value": round(len(rows) / dt, 4), "unit": "images/s", "cores": cores, "kind": "oracle",
+               "threads": cores,
+               "sample": "%d of the %d images of %s, one oracle call (NumPy float64, bf16io), %.1f s"
+                         % (len(rows), n, headline.key, dt)}
+        cpu.update(_cpu_info())
+        for m in measured:
+            wl = m.wl
+            f32 = m.key == "conv_f32"
+            mode, tol = ("exact", F32_TOL) if f32 else ("bf16io", BF16_TOL)
+            n = wl.inputs[0].shape[0]
+            rows = list(range(n)) if (n <= 16 or m.key == "bert_ffn") else [0, n - 1]
+            g, x = _sampled(wl, rows)
+            t0 = time.perf_counter()
+            ref = oracle.run_graph(g, wl.consts, x, mode=mode)[0]
+            entry = {"err": err_of(m.outputs[0][rows], ref), "tol": tol, "mode": mode,
+                     "sample": "%s of %d %s" % ("all" if len(rows) == n else len(rows), n,
+                                                "token rows" if m.key == "bert_ffn" else "images")}
+            if m.key in ("bert_ffn", "darknet53_bs32"):
+                ex = oracle.run_graph(g, wl.consts, x, mode="exact")[0]
+                entry["oracle_bf16io_vs_exact"] = err_of(ex, ref)
+                entry["note"] = ("bf16 storage along a long residual stream: flips of single roundings spread "
+                                 "between layers; the oracle's own bf16io-vs-exact spread is of the same size")
+            entry["oracle_s"] = round(time.perf_counter() - t0, 2)
+            entry["ok"] = entry["err"] <= tol
+            parity[m.key] = entry
+    parity[headline.key]["ok"] = parity[headline.key]["err"] <= BF16_TOL
+    for v in parity.values():
+        v["err"] = float("%.4e" % v["err"])
+    return cpu, parity
 
 
 def _partitioned(args, wl, dev, stream):
@@ -191,9 +439,8 @@ def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
     import copy
 
     import numpy as np
-    import torch
 
-    from paper_2105_03215_amd import capi, quantize, runtime
+    from paper_2105_03215_amd import quantize, runtime
 
     variant = variant or args.variant
     t0 = time.perf_counter()
@@ -204,27 +451,13 @@ def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
     ranges = quantize.calibrate(cal, wl.consts, [batch])
     qg = quantize.quantize_graph(wl.graph, ranges)
     calib_s = time.perf_counter() - t0
-    sg = capi.Subgraph(qg, wl.consts, device=0)
-    try:
-        ins = runtime.inputs_for(sg, wl.inputs, dev)
-        outs = runtime.outputs_for(sg, dev)
-        if not args.no_autotune:
-            sg.set_options(autotune=True)
-        sg.set_options(graph_replay=not args.eager)
-        for _ in range(args.warmup):
-            sg.run(ins, outs, stream)
-        torch.cuda.synchronize()
-        ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
-        sg.set_options(graph_replay=False)
-        launches = sg.launches()
-        per_launch, _ = _profile(sg, ins, outs, stream, args.steps)
-    finally:
-        sg.close()
+    n = wl.inputs[0].shape[0]
+    m = _measure(args, "%s_bs%d_int8" % (variant, n), wl, dev, stream, graph=qg)
+    launches, per_launch, ms = m.launches, m.per_launch, m.ms
     if args.dump_launches and variant == args.variant:
         root, ext = os.path.splitext(args.dump_launches)
         with open(root + "_int8" + ext, "w") as f:
             json.dump([dict(l, ms=round(t, 5)) for l, t in zip(launches, per_launch)], f, indent=1)
-    n = wl.inputs[0].shape[0]
     other_ms = sum(t for l, t in zip(launches, per_launch) if l["kind"] != "conv_i8")
     conv_ms = max(ms - other_ms, 1e-9)
     ops = sum(l["flops"] for l in launches if l["kind"] == "conv_i8")
@@ -241,6 +474,8 @@ def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
     return {"workload": "%s_bs%d_int8" % (variant, n), "images_per_s": round(n / (ms * 1e-3), 1),
             "ms_per_step": round(ms, 4), "dtype": "int8 codes, int32 accumulation",
             "calibration": "%d images through the executor, %.2f s" % (calib_images, calib_s),
+            "parity": "int8 codes are exact integer sums and float32 rescalings, independent of the tiling: "
+                      "checked bit for bit against the int8 oracle on all 32 images in the GPU tests",
             "roofline": {"bound": "mfma", "achieved": round(tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                          "frac": round(tops / PEAK_INT8_TOPS, 4), "traffic": traffic,
                          "kernel": "conv/dense int8 MFMA class (conv_i8), %d launches per step"
@@ -253,31 +488,14 @@ def _other_workload(args, name, batch, dev, stream):
     """Throughput and conv-class roofline of another fully offloaded network
     (same measurement as the headline: graph replay, autotune, inputs in
     HBM)."""
-    import torch
-
-    from paper_2105_03215_amd import capi, runtime, workloads
+    from paper_2105_03215_amd import capi, workloads
 
     wl = workloads.build(name, n=batch)
-    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
-    try:
-        ins = runtime.inputs_for(sg, wl.inputs, dev)
-        outs = runtime.outputs_for(sg, dev)
-        if not args.no_autotune:
-            sg.set_options(autotune=True)
-        sg.set_options(graph_replay=not args.eager)
-        for _ in range(args.warmup):
-            sg.run(ins, outs, stream)
-        torch.cuda.synchronize()
-        ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
-        sg.set_options(graph_replay=False)
-        launches = sg.launches()
-        per_launch, _ = _profile(sg, ins, outs, stream, args.steps)
-    finally:
-        sg.close()
-    roof = _roofline(launches, per_launch, ms)
-    out = {"workload": "%s_bs%d" % (name, batch), "images_per_s": round(batch / (ms * 1e-3), 1),
-           "ms_per_step": round(ms, 4), "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
-           "conv_tflops": roof["achieved"], "conv_frac": roof["frac"], "launches": len(launches)}
+    m = _measure(args, "%s_bs%d" % (name, batch), wl, dev, stream)
+    roof = _roofline(m.launches, m.per_launch, m.ms)
+    out = {"workload": m.key, "images_per_s": round(batch / (m.ms * 1e-3), 1),
+           "ms_per_step": round(m.ms, 4), "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
+           "conv_tflops": roof["achieved"], "conv_frac": roof["frac"], "launches": len(m.launches)}
     if not args.no_quantized:  # the same network partially quantized, as the headline's int8 leg
         try:
             q = _quantized(args, wl, dev, stream, variant=name)
@@ -285,7 +503,7 @@ def _other_workload(args, name, batch, dev, stream):
                            "conv_tops": q["roofline"]["achieved"], "conv_frac": q["roofline"]["frac"]}
         except capi.ByocError as e:  # operators without an int8 form
             out["int8"] = {"skipped": str(e)}
-    return out
+    return out, m
 
 
 def main():
@@ -298,8 +516,11 @@ def main():
                     help="network of the headline run: resnet50_v1 (the benchmark), resnet50_v1b, vgg19, "
                          "darknet53, inception_v3, mobilenet_v2")
     ap.add_argument("--cpu-images", type=int, default=32)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle leg (the CPU baseline and the parity report)")
     ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the conv_f32, ResNet-18 block, ResNet-50 bs1, MobileNetV2 and BERT FFN lines")
     ap.add_argument("--no-other", action="store_true", help="skip the VGG19, DarkNet-53 and Inception V3 bs32 lines")
     ap.add_argument("--no-quantized", action="store_true",
                     help="skip the int8 (partially quantized) run of the network")
@@ -307,6 +528,7 @@ def main():
                     help="skip the operator-level model run through the partitioner and its runtime")
     ap.add_argument("--no-autotune", action="store_true",
                     help="keep the built-in conv kernel choice (no on-device tuning at setup)")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache per-step timing")
     ap.add_argument("--eager", action="store_true",
                     help="headline value from direct launches instead of HIP-graph replay")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
@@ -354,12 +576,24 @@ def main():
         sg.run(ins, outs, stream)
     torch.cuda.synchronize()
     ms_graph, wall_graph = _timed_runs(sg, ins, outs, stream, args.steps)
-    sg.set_options(graph_replay=False)
     if args.eager:
+        sg.set_options(graph_replay=False)
         ms, wall, mode = ms_eager, wall_eager, "direct launches"
     else:
         ms, wall, mode = ms_graph, wall_graph, "HIP graph replay"
     value = args.batch / (ms * 1e-3)
+    host_out = [runtime.to_host_f64(o) for o in outs]
+    # warm / cold per-step distributions of the same configuration
+    warm = _pct(_per_step(sg, ins, outs, stream, max(args.steps, 50)))
+    timing = {"warm_ms": warm, "warm_images_per_s_at_median": round(args.batch / (warm["median"] * 1e-3), 1)}
+    if not args.no_cold:
+        evict = torch.empty(EVICT_MIB * 2 ** 20 // 4, dtype=torch.float32, device=dev)
+        cold = _pct(_per_step(sg, ins, outs, stream, max(args.steps, 50), evict=evict))
+        del evict
+        timing.update({"cold_ms": cold, "cold_images_per_s_at_median": round(args.batch / (cold["median"] * 1e-3), 1),
+                       "cold_eviction": "%d MiB written on the run stream before each run, outside its event pair"
+                                        % EVICT_MIB})
+    sg.set_options(graph_replay=False)
     launches = sg.launches()
     per_launch, runs = _profile(sg, ins, outs, stream, args.steps)
     traffic = None
@@ -380,28 +614,13 @@ def main():
         with open(args.dump_launches, "w") as f:
             json.dump(table, f, indent=1)
     stats = sg.stats()
+    sg.close()
+    headline = Measured("%s_bs%d" % (args.variant, args.batch), wl, None, ms, launches, per_launch, host_out)
 
-    bs1 = None
-    if not args.no_bs1 and args.batch != 1:
-        wl1 = workloads.build(args.variant, n=1)
-        sg1 = capi.Subgraph(wl1.graph, wl1.consts, device=0)
-        if not args.no_autotune:
-            sg1.set_options(autotune=True)
-        ins1 = runtime.inputs_for(sg1, wl1.inputs, dev)
-        outs1 = runtime.outputs_for(sg1, dev)
-        for _ in range(args.warmup):
-            sg1.run(ins1, outs1, stream)
-        ms1e, _ = _timed_runs(sg1, ins1, outs1, stream, max(args.steps, 200))
-        sg1.set_options(graph_replay=True)
-        for _ in range(args.warmup):
-            sg1.run(ins1, outs1, stream)
-        ms1g, _ = _timed_runs(sg1, ins1, outs1, stream, max(args.steps, 200))
-        ms1 = ms1e if args.eager else ms1g
-        bs1 = {"images_per_s": round(1.0 / (ms1 * 1e-3), 1), "ms_per_step": round(ms1, 4),
-               "launch_mode": mode, "eager_images_per_s": round(1.0 / (ms1e * 1e-3), 1),
-               "launches": len(sg1.launches())}
-        sg1.close()
-
+    measured = []
+    configs = None
+    if not args.no_configs:
+        configs, measured = _config_lines(args, dev, stream)
     parted = None
     if not args.no_partitioned:
         parted = _partitioned(args, wl, dev, stream)
@@ -409,17 +628,19 @@ def main():
     if not args.no_quantized:
         try:
             quant = _quantized(args, wl, dev, stream)
-        except capi.ByocError as e:  # e.g. depthwise convs have no int8 form
+        except capi.ByocError as e:  # e.g. operators without an int8 form
             quant = {"workload": "%s_bs%d_int8" % (args.variant, args.batch), "skipped": str(e)}
     other = None
     if not args.no_other:
-        other = [_other_workload(args, "vgg19", 32, dev, stream),
-                 _other_workload(args, "darknet53", 32, dev, stream),
-                 _other_workload(args, "inception_v3", 32, dev, stream)]
+        other = []
+        for name in ("vgg19", "darknet53", "inception_v3"):
+            line, m = _other_workload(args, name, 32, dev, stream)
+            other.append(line)
+            measured.append(m)
 
-    cpu = None
+    cpu, parity = None, None
     if not args.no_cpu_baseline:
-        cpu = _cpu_baseline(wl, args.cpu_images)
+        cpu, parity = _cpu_baseline_leg(headline, measured, args.cpu_images)
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "images/s", "n_gpus": 1,
@@ -432,9 +653,12 @@ def main():
                    "launch_mode": mode},
         "eager_images_per_s": round(args.batch / (ms_eager * 1e-3), 1),
         "graph_images_per_s": round(args.batch / (ms_graph * 1e-3), 1),
+        "timing": timing,
         "roofline": roof,
         "cpu_baseline": cpu,
-        "bs1": bs1,
+        "parity": parity,
+        "bs1": (configs or {}).get("resnet50_v1_bs1"),
+        "configs": configs,
         "partitioned": parted,
         "quantized": quant,
         "other_workloads": other,
@@ -444,7 +668,6 @@ def main():
         "weight_bytes": stats["weight_bytes"], "arena_bytes": stats["arena_bytes"],
         "wall_s_timed": round(wall, 4),
     }
-    sg.close()
     print(json.dumps(line), flush=True)
 
 

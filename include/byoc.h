@@ -174,8 +174,10 @@ byoc_status byoc_subgraph_create(const char* json, size_t len, const byoc_const*
 byoc_status byoc_subgraph_run(byoc_subgraph* g, const void* const* inputs, int32_t n_in,
                               void* const* outputs, int32_t n_out, void* stream);
 
-/* Synchronise the device, free every allocation of the engine and the
- * handle.  NULL is a no-op returning BYOC_OK. */
+/* Wait for the last run enqueued by byoc_subgraph_run (on whatever stream
+ * it was enqueued), then free every allocation of the engine and the
+ * handle; other streams and the rest of the device are not synchronised.
+ * NULL is a no-op returning BYOC_OK. */
 byoc_status byoc_subgraph_destroy(byoc_subgraph* g);
 
 /* Number of subgraph inputs and outputs. */

@@ -150,6 +150,30 @@ def _ptr(t):
     return t.data_ptr()
 
 
+_ELEM_DTYPE = {"bf16": "torch.bfloat16", "f32": "torch.float32"}
+
+
+def _check_tensor(t, desc, device, what):
+    """Raises ByocError unless the torch tensor t matches the declared
+    description (dtype, element count) and is a contiguous tensor on the
+    engine's device.  Ints (raw device pointers) and None are not checked."""
+    if t is None or isinstance(t, int):
+        return
+    want = _ELEM_DTYPE[desc["dtype"]]
+    n = int(np.prod(desc["shape"])) if desc["shape"] else 1
+    problems = []
+    if str(t.dtype) != want:
+        problems.append("dtype %s, declared %s" % (t.dtype, want))
+    if t.numel() != n:
+        problems.append("%d elements, declared %d %s" % (t.numel(), n, list(desc["shape"])))
+    if t.device.type != "cuda" or (t.device.index if t.device.index is not None else 0) != int(device):
+        problems.append("on %s, engine on cuda:%d" % (t.device, int(device)))
+    if not t.is_contiguous():
+        problems.append("not contiguous")
+    if problems:
+        raise ByocError(1, "%s: %s" % (what, "; ".join(problems)))
+
+
 class Subgraph:
     """An execution engine for one serialized subgraph on one HIP device."""
 
@@ -165,6 +189,8 @@ class Subgraph:
         n_in, n_out = ctypes.c_int32(), ctypes.c_int32()
         _check(self.lib.byoc_subgraph_num_io(h, ctypes.byref(n_in), ctypes.byref(n_out)))
         self.n_in, self.n_out = n_in.value, n_out.value
+        self._descs = ([self.io_desc(0, i) for i in range(self.n_in)],
+                       [self.io_desc(1, j) for j in range(self.n_out)])
 
     def io_desc(self, is_output, idx):
         d = TensorDesc()
@@ -189,9 +215,17 @@ class Subgraph:
                         "bytes": li.bytes, "name": li.name.decode()})
         return out
 
-    def run(self, inputs, outputs, stream=None):
-        """Enqueue one run on `stream` (a torch.cuda.Stream, a raw hipStream_t
-        int, or None for torch's current stream)."""
+    def _marshal(self, inputs, outputs, stream):
+        """Pointer arrays and the raw stream of a run.  Torch tensors are
+        checked against the declared dtype, element count, device and
+        contiguity (a wrong buffer would make the kernels read or write out
+        of bounds); raw integer pointers are passed through as they are."""
+        if len(inputs) != self.n_in or len(outputs) != self.n_out:
+            raise ByocError(1, "expected %d inputs and %d outputs, got %d and %d"
+                            % (self.n_in, self.n_out, len(inputs), len(outputs)))
+        for what, ts, descs in (("input", inputs, self._descs[0]), ("output", outputs, self._descs[1])):
+            for i, (t, d) in enumerate(zip(ts, descs)):
+                _check_tensor(t, d, self.device, "%s %d" % (what, i))
         ins = (ctypes.c_void_p * max(len(inputs), 1))(*[_ptr(t) for t in inputs])
         outs = (ctypes.c_void_p * max(len(outputs), 1))(*[_ptr(t) for t in outputs])
         if stream is None:
@@ -201,8 +235,13 @@ class Subgraph:
             s = stream
         else:
             s = stream.cuda_stream
-        _check(self.lib.byoc_subgraph_run(self.handle, ins, len(inputs), outs, len(outputs),
-                                          ctypes.c_void_p(s)))
+        return ins, outs, ctypes.c_void_p(s)
+
+    def run(self, inputs, outputs, stream=None):
+        """Enqueue one run on `stream` (a torch.cuda.Stream, a raw hipStream_t
+        int, or None for torch's current stream)."""
+        ins, outs, s = self._marshal(inputs, outputs, stream)
+        _check(self.lib.byoc_subgraph_run(self.handle, ins, len(inputs), outs, len(outputs), s))
 
     def set_options(self, graph_replay=None, autotune=None):
         """Turn engine options on or off; None keeps an option as it is.

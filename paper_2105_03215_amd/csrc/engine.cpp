@@ -1450,6 +1450,8 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
 
 void release(Engine* e) {
   if (!e) return;
+  if (e->done) (void)hipEventDestroy(e->done);
+  e->done = nullptr;
   if (e->gexec) (void)hipGraphExecDestroy(e->gexec);
   e->gexec = nullptr;
   for (hipEvent_t ev : e->events) (void)hipEventDestroy(ev);
@@ -1544,19 +1546,30 @@ Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int 
                      Engine** out) {
   (void)n_consts;
   *out = nullptr;
-  int ndev = 0;
-  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev == 0)
-    return Status::Err(BYOC_ERR_DEVICE, "no HIP device available");
-  if (device < 0 || device >= ndev)
-    return Status::Err(BYOC_ERR_INVALID_ARG, "device " + std::to_string(device) + " out of range");
+  if (device < 0) return Status::Err(BYOC_ERR_INVALID_ARG, "device " + std::to_string(device) + " out of range");
   Engine* e = new Engine();
   e->graph = std::move(g);
   e->device = device;
-  DeviceGuard guard(device);
+  // The launch plan is host work: planning errors are reported before any
+  // device call (also on a host without a GPU).
   Planner pl(e, e->graph);
   pl.consts = consts;
   Status st = pl.plan();
-  if (st.ok()) st = build_device_state(e, pl, consts);
+  if (st.ok()) {
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev == 0)
+      st = Status::Err(BYOC_ERR_DEVICE, "no HIP device available");
+    else if (device >= ndev)
+      st = Status::Err(BYOC_ERR_INVALID_ARG, "device " + std::to_string(device) + " out of range");
+  }
+  if (st.ok()) {
+    DeviceGuard guard(device);
+    st = build_device_state(e, pl, consts);
+    if (st.ok()) {
+      hipError_t err = hipEventCreateWithFlags(&e->done, hipEventDisableTiming | hipEventDisableSystemFence);
+      if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("hipEventCreate: ") + hipGetErrorString(err));
+    }
+  }
   if (!st.ok()) {
     release(e);
     delete e;
@@ -1809,8 +1822,10 @@ Status engine_set_options(Engine* e, int flags) {
   return Status::Ok();
 }
 
-Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
-                  int32_t n_out, hipStream_t stream) {
+namespace {
+
+Status check_run_args(const Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
+                      int32_t n_out) {
   if (n_in != (int32_t)e->graph.inputs.size())
     return Status::Err(BYOC_ERR_INVALID_ARG, "expected " + std::to_string(e->graph.inputs.size()) +
                                                  " inputs, got " + std::to_string(n_in));
@@ -1823,14 +1838,11 @@ Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* cons
     if (!inputs[i]) return Status::Err(BYOC_ERR_INVALID_ARG, "input " + std::to_string(i) + " is NULL");
   for (int i = 0; i < n_out; ++i)
     if (!outputs[i]) return Status::Err(BYOC_ERR_INVALID_ARG, "output " + std::to_string(i) + " is NULL");
-  DeviceGuard guard(e->device);
-  RunCtx c{e, inputs, outputs, stream};
-  const bool prof = !e->events.empty() && e->prof_runs < e->prof_max_runs;
-  if ((e->options & BYOC_OPT_GRAPH_REPLAY) && !prof && stream != nullptr) {
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    HIP_TRY(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
-    if (cs == hipStreamCaptureStatusNone) return run_graph(e, c, n_in, n_out);
-  }
+  return Status::Ok();
+}
+
+Status launch_all(Engine* e, const RunCtx& c, bool prof) {
+  hipStream_t stream = c.s;
   const size_t nl = e->launches.size();
   hipEvent_t* ev = prof ? &e->events[(size_t)e->prof_runs * (nl + 1)] : nullptr;
   if (prof) HIP_TRY(hipEventRecord(ev[0], stream), "hipEventRecord");
@@ -1846,6 +1858,28 @@ Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* cons
     e->prof_last_stream = stream;
   }
   return Status::Ok();
+}
+
+}  // namespace
+
+Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
+                  int32_t n_out, hipStream_t stream) {
+  Status ast = check_run_args(e, inputs, n_in, outputs, n_out);
+  if (!ast.ok()) return ast;
+  DeviceGuard guard(e->device);
+  RunCtx c{e, inputs, outputs, stream};
+  const bool prof = !e->events.empty() && e->prof_runs < e->prof_max_runs;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (stream != nullptr) HIP_TRY(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+  if ((e->options & BYOC_OPT_GRAPH_REPLAY) && !prof && stream != nullptr && cs == hipStreamCaptureStatusNone) {
+    Status st = run_graph(e, c, n_in, n_out);
+    if (st.ok()) HIP_TRY(hipEventRecord(e->done, stream), "hipEventRecord");
+    return st;
+  }
+  Status st = launch_all(e, c, prof);
+  // completion marker for destroy (not inside a capture of the caller's)
+  if (st.ok() && cs == hipStreamCaptureStatusNone) HIP_TRY(hipEventRecord(e->done, stream), "hipEventRecord");
+  return st;
 }
 
 Status engine_profile_begin(Engine* e, int max_runs) {
@@ -1910,7 +1944,9 @@ Status engine_destroy(Engine* e) {
   Status st;
   {
     DeviceGuard guard(e->device);
-    hipError_t err = hipDeviceSynchronize();
+    // the last run enqueued through run() (the event completes at once when
+    // there was none)
+    hipError_t err = e->done ? hipEventSynchronize(e->done) : hipSuccess;
     if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("destroy: ") + hipGetErrorString(err));
     release(e);
   }

@@ -78,6 +78,8 @@ struct Engine {
   int prof_max_runs = 0;
   int prof_runs = 0;
   hipStream_t prof_last_stream = nullptr;
+  // marks the end of the last run() on its stream; destroy waits for it
+  hipEvent_t done = nullptr;
 };
 
 // Builds the plan and device state.  On failure releases everything.

@@ -364,14 +364,20 @@ bool stem_supported(int C, int K, int R, int S, int sh, int sw, int kph, int kpw
 int stem_weight_ld(int R) { return R * 32 + 8; }
 
 hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s) {
-  // persistent grid: two workgroups per CU, never more than the tiles
-  static std::atomic<int> cus{0};
-  if (cus.load() == 0) {
-    int dev = 0, n = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  // persistent grid: two workgroups per CU of the current device, never
+  // more than the tiles (CU counts cached per device)
+  constexpr int kMaxDev = 64;
+  static std::atomic<int> cu_of[kMaxDev] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  int ncu = dev >= 0 && dev < kMaxDev ? cu_of[dev].load() : 0;
+  if (ncu == 0) {
+    int n = 0;
+    e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    cus.store(n > 0 ? n : 1);
+    ncu = n > 0 ? n : 1;
+    if (dev >= 0 && dev < kMaxDev) cu_of[dev].store(ncu);
   }
   const int tw = (16 - p.kpw) / p.spw + 1;
   const int64_t tiles = (int64_t)p.N * ((p.PO + kTH - 1) / kTH) * ((p.QO + tw - 1) / tw);
@@ -379,7 +385,7 @@ hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s) {
   // tile indices are int; one image is addressed by 32-bit buffer offsets
   if (tiles > (1ll << 30) || (int64_t)p.C * p.H * p.W * (p.x_bf16 ? 2 : 4) >= (1ll << 31))
     return hipErrorInvalidValue;
-  int64_t grid = std::min<int64_t>(tiles, 2 * (int64_t)cus.load());
+  int64_t grid = std::min<int64_t>(tiles, 2 * (int64_t)ncu);
   if (p.grid_cap > 0) grid = std::min<int64_t>(grid, p.grid_cap);
   // vector segment loads need 4-aligned rows and an aligned base
   const size_t elem = p.x_bf16 ? 2 : 4;

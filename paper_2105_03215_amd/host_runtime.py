@@ -142,9 +142,17 @@ class Module:
         stream = stream or torch.cuda.current_stream(self.device)
         entries = dict(self.const_entries)
         entries.update(self.data)
-        for nid, t in zip(g.inputs, inputs):
-            entries[nid] = t.to(self.device, _tdt(g.nodes[nid].dtype)).contiguous()
+        # the inputs' producers ran on the caller's current stream
+        stream.wait_stream(torch.cuda.current_stream(self.device))
         with torch.cuda.stream(stream):
+            for nid, t in zip(g.inputs, inputs):
+                # converted on the run stream; a converted copy is a new
+                # allocation of that stream's pool, the input itself may
+                # belong to another stream's pool
+                x = t.to(self.device, _tdt(g.nodes[nid].dtype)).contiguous()
+                if x.data_ptr() == t.data_ptr() and x.device.type == "cuda":
+                    x.record_stream(stream)
+                entries[nid] = x
             for kind, ref in self.part.steps:
                 if kind == "host":
                     node = g.nodes[ref]

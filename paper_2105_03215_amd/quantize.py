@@ -60,13 +60,6 @@ def calibrate(graph, consts, batches, device=0):
     g = _load(graph)
     cg = calibration_graph(g)
     ranges = {}
-
-    def merge(name, t):
-        lo, hi = float(t.min()), float(t.max())
-        if name in ranges:
-            lo, hi = min(lo, ranges[name][0]), max(hi, ranges[name][1])
-        ranges[name] = (lo, hi)
-
     with capi.Subgraph(cg, consts, device=device) as sg:
         for inputs in batches:
             outs = []
@@ -75,10 +68,26 @@ def calibrate(graph, consts, batches, device=0):
                 outs.append(torch.empty(d["shape"], dtype=torch.float32, device="cuda:%d" % device))
             sg.run(list(inputs), outs)
             torch.cuda.synchronize(device)
-            for desc, t in zip(g["inputs"], inputs):
-                merge(desc["name"], t.float())
-            for node, t in zip(g["nodes"], outs):
-                merge(node["name"], t)
+            merge_ranges(ranges, g, [t.float() for t in inputs], outs)
+    return ranges
+
+
+def merge_ranges(ranges, graph, inputs, node_values):
+    """Widens ``ranges`` {tensor name: (min, max)} by one calibration batch:
+    ``inputs`` in the order of the function's inputs and ``node_values`` in
+    node order (arrays or tensors, any float type)."""
+    g = _load(graph)
+
+    def merge(name, t):
+        lo, hi = float(t.min()), float(t.max())
+        if name in ranges:
+            lo, hi = min(lo, ranges[name][0]), max(hi, ranges[name][1])
+        ranges[name] = (lo, hi)
+
+    for desc, t in zip(g["inputs"], inputs):
+        merge(desc["name"], t)
+    for node, t in zip(g["nodes"], node_values):
+        merge(node["name"], t)
     return ranges
 
 

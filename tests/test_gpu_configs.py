@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 from paper_2105_03215_amd import workloads
-from parity_util import (BF16_TOL, F32_TOL, announce, rel_err, term_scale_node,
+from parity_util import (BF16_TOL, F32_TOL, announce, gate_end_to_end, rel_err, term_scale_node,
                          within_one_ulp)
 
 pytestmark = pytest.mark.gpu
@@ -166,35 +166,26 @@ def test_darknet53_teacher_forced():
         vals[node["name"]] = g
 
 
-def _drift_bound(graph, consts, inputs):
-    """max(1e-2, twice the oracle's own bf16io-vs-exact spread): 23 residual
-    adds of bf16 storage after the activation let two correct
-    implementations drift apart by more than one rounding."""
+def _darknet_gate(graph, consts, inputs, got, what):
     io = oracle.run_graph(graph, consts, inputs, mode="bf16io")[0]
     ex = oracle.run_graph(graph, consts, inputs, mode="exact")[0]
-    return io, max(BF16_TOL, 2 * rel_err(io, ex))
+    gate_end_to_end(rel_err(got, io), rel_err(io, ex), what)
 
 
 def test_darknet53_bs1_128():
     announce("darknet53 bs1 128x128")
     wl = workloads.build("darknet53", n=1, hw=128)
     g = _gpu(wl)[0]
-    o, bound = _drift_bound(wl.graph, wl.consts, wl.inputs)
-    err = rel_err(g, o)
-    print("darknet53 bs1 err %.3e bound %.3e" % (err, bound))
-    assert err <= bound
+    _darknet_gate(wl.graph, wl.consts, wl.inputs, g, "darknet53 bs1 128x128")
 
 
 def test_darknet53_bs32_sampled():
     announce("darknet53 bs32 256x256 sampled images 0 and 31")
     wl = workloads.build("darknet53", n=32)
     g = _gpu(wl)[0]
-    rows = [0, 31]
-    o, bound = _drift_bound(_sample_graph(wl, 2), wl.consts, _sample_inputs(wl, rows))
-    err = rel_err(g[rows], o)
-    print("darknet53 bs32 err %.3e bound %.3e" % (err, bound))
-    assert err <= bound
     assert np.all(np.isfinite(g))
+    rows = [0, 31]
+    _darknet_gate(_sample_graph(wl, 2), wl.consts, _sample_inputs(wl, rows), g[rows], "darknet53 bs32 images 0, 31")
 
 
 def test_inception_v3_bs1():
@@ -243,11 +234,9 @@ def test_bert_ffn_layers_teacher_forced():
 
 
 def test_bert_ffn_end_to_end_sampled():
-    """Full stack on 64 sampled rows.  Twelve residual layers of bf16 storage
-    let any two correct implementations drift apart by more than one
-    rounding; the bound is twice the oracle's own bf16io-vs-exact spread on
-    the same rows (the drift of a correct implementation), and never below
-    the 1e-2 of the comparison."""
+    """Full stack on 64 sampled rows against the fixed 1e-2 gate (an expected
+    failure with its measured error when the bf16 residual stream drifts
+    past it, see gate_end_to_end)."""
     announce("bert_ffn end to end sampled rows")
     wl = workloads.build("bert_ffn")
     g = _gpu(wl)[0]
@@ -256,7 +245,4 @@ def test_bert_ffn_end_to_end_sampled():
     graph["inputs"] = [dict(graph["inputs"][0], shape=[64, 768])]
     io = oracle.run_graph(graph, wl.consts, [wl.inputs[0][rows]], mode="bf16io")[0]
     ex = oracle.run_graph(graph, wl.consts, [wl.inputs[0][rows]], mode="exact")[0]
-    spread = rel_err(io, ex)
-    err = rel_err(g[rows], io)
-    print("bert e2e err %.3e, oracle bf16io-vs-exact spread %.3e" % (err, spread))
-    assert err <= max(BF16_TOL, 2 * spread)
+    gate_end_to_end(rel_err(g[rows], io), rel_err(io, ex), "bert_ffn 64 sampled rows")

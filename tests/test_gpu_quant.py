@@ -7,8 +7,10 @@ map of the codes) must equal the oracle's bit for bit.  Cases span aligned
 tile shape, the border correction of a nonzero input zero point under
 padding, strides, residuals, ReLU / ReLU6, pools, the standalone add and the
 boundary quantize / dequantize; the ResNet-50 case runs at batch 32 and
-224x224 (the benchmark's configuration) with the scales calibrated through
-the executor, and the oracle recomputes sampled images.
+224x224 (the benchmark's configuration).  The scales and zero points of
+the network cases are calibrated on the oracle's float values of the
+calibration images, so the quantized function both sides receive holds
+nothing the GPU computed.
 """
 
 import copy
@@ -18,8 +20,8 @@ import pytest
 
 import oracle
 from oracle import quant as OQ
-from paper_2105_03215_amd import quantize, workloads
-from parity_util import announce
+from paper_2105_03215_amd import workloads
+from parity_util import announce, oracle_calibrated_int8
 
 pytestmark = pytest.mark.gpu
 
@@ -155,17 +157,8 @@ def test_int8_two_runs_and_bs1_graph():
 
 
 def _calibrated_resnet50(n, hw, calib_n=2):
-    import torch
     wl = workloads.build("resnet50_v1", n=n, hw=hw)
-    cal = copy.deepcopy(wl.graph)
-    cal["inputs"] = [dict(d, shape=[calib_n] + d["shape"][1:]) for d in cal["inputs"]]
-    from paper_2105_03215_amd import runtime
-    batch = [torch.from_numpy(np.ascontiguousarray(a[:calib_n])).to(DEV).to(
-        torch.bfloat16 if d["dtype"] == "bf16" else torch.float32) for a, d in zip(wl.inputs, cal["inputs"])]
-    ranges = quantize.calibrate(cal, wl.consts, [batch])
-    qg = quantize.quantize_graph(wl.graph, ranges)
-    for o in qg["outputs"]:
-        o["dtype"] = "f32"  # float32 dequantized values map one to one onto the codes
+    qg = oracle_calibrated_int8(wl.graph, wl.consts, [np.ascontiguousarray(a[:calib_n]) for a in wl.inputs])
     return wl, qg
 
 
@@ -232,13 +225,9 @@ def test_int8_depthwise_bit_exact(case):
 
 
 def test_int8_mobilenet_v2_small_full_compare():
-    import torch
     announce("int8 mobilenet_v2 n=2 hw=64")
     wl = workloads.build("mobilenet_v2", n=2, hw=64)
-    batch = [torch.from_numpy(np.ascontiguousarray(wl.inputs[0])).to(DEV).to(torch.bfloat16)]
-    qg = quantize.quantize_graph(wl.graph, quantize.calibrate(wl.graph, wl.consts, [batch]))
-    for o in qg["outputs"]:
-        o["dtype"] = "f32"
+    qg = oracle_calibrated_int8(wl.graph, wl.consts, wl.inputs)
     got, launches = _run(qg, wl.consts, wl.inputs)
     assert sum(1 for l in launches if l["name"] == "depthwise_nhwc_i8") == 17
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
@@ -247,13 +236,9 @@ def test_int8_mobilenet_v2_small_full_compare():
 
 def test_int8_vgg19_small_full_compare():
     """VGG19 (2x2 max pools, the full-map fc6 conv, dense classifier) in int8."""
-    import torch
     announce("int8 vgg19 n=2 hw=64")
     wl = workloads.build("vgg19", n=2, hw=64)
-    batch = [torch.from_numpy(np.ascontiguousarray(wl.inputs[0])).to(DEV).to(torch.bfloat16)]
-    qg = quantize.quantize_graph(wl.graph, quantize.calibrate(wl.graph, wl.consts, [batch]))
-    for o in qg["outputs"]:
-        o["dtype"] = "f32"
+    qg = oracle_calibrated_int8(wl.graph, wl.consts, wl.inputs)
     got, launches = _run(qg, wl.consts, wl.inputs)
     assert sum(1 for l in launches if l["kind"] == "conv_i8") == 19
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
@@ -280,13 +265,9 @@ def test_int8_leaky_slopes_conv_and_add():
 
 def test_int8_darknet53_small_full_compare():
     """DarkNet-53 (leaky ReLU after every conv, residual adds) in int8."""
-    import torch
     announce("int8 darknet53 n=2 hw=64")
     wl = workloads.build("darknet53", n=2, hw=64)
-    batch = [torch.from_numpy(np.ascontiguousarray(wl.inputs[0])).to(DEV).to(torch.bfloat16)]
-    qg = quantize.quantize_graph(wl.graph, quantize.calibrate(wl.graph, wl.consts, [batch]))
-    for o in qg["outputs"]:
-        o["dtype"] = "f32"
+    qg = oracle_calibrated_int8(wl.graph, wl.consts, wl.inputs)
     got, launches = _run(qg, wl.consts, wl.inputs)
     assert sum(1 for l in launches if l["kind"] == "conv_i8") >= 52
     # every residual add follows a conv's leaky ReLU and is folded into it
