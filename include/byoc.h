@@ -174,6 +174,31 @@ byoc_status byoc_subgraph_create(const char* json, size_t len, const byoc_const*
 byoc_status byoc_subgraph_run(byoc_subgraph* g, const void* const* inputs, int32_t n_in,
                               void* const* outputs, int32_t n_out, void* stream);
 
+/* Capacity of the static scratch that byoc_subgraph_run_static uses. */
+#define BYOC_STATIC_SCRATCH_BYTES ((int64_t)64 << 20)
+
+/* For callers that cannot allocate device memory while they run (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * byoc_subgraph_run with the engine's intermediates (activations between
+ * composites, split-K partial sums, concatenation buffers) placed in a
+ * static scratch array of BYOC_STATIC_SCRATCH_BYTES that the library holds
+ * on every GPU it runs on until the process ends, instead of the engine's
+ * own arena.  Arguments, layouts and ownership as for byoc_subgraph_run;
+ * always direct launches (no graph replay, no profiling events), and no
+ * allocation, no host-device copy and no synchronisation of any kind.  The
+ * first call on a device looks up that device's scratch address once.
+ * Engines whose intermediates need more than BYOC_STATIC_SCRATCH_BYTES
+ * (byoc_subgraph_stats' arena_bytes) are rejected with
+ * BYOC_ERR_INVALID_ARG before anything is enqueued.  Every call on one GPU,
+ * from any engine, shares that GPU's scratch, which keeps the last call's
+ * contents (nothing in it needs clearing: every intermediate is written
+ * before it is read): calls that overlap on one GPU - on two streams, or
+ * from two threads - race and must be serialised by the caller.  Outputs
+ * are bit-for-bit those of byoc_subgraph_run.  byoc_subgraph_destroy does
+ * not wait for these runs: synchronise their stream first. */
+byoc_status byoc_subgraph_run_static(byoc_subgraph* g, const void* const* inputs, int32_t n_in,
+                                     void* const* outputs, int32_t n_out, void* stream);
+
 /* Wait for the last run enqueued by byoc_subgraph_run (on whatever stream
  * it was enqueued), then free every allocation of the engine and the
  * handle; other streams and the rest of the device are not synchronised.

@@ -25,7 +25,7 @@ EXPORTS = ["byoc_subgraph_validate", "byoc_subgraph_create", "byoc_subgraph_run"
            "byoc_subgraph_destroy", "byoc_subgraph_num_io", "byoc_subgraph_io_desc",
            "byoc_subgraph_stats", "byoc_subgraph_num_launches", "byoc_subgraph_launch_info",
            "byoc_subgraph_profile_begin", "byoc_subgraph_profile_end",
-           "byoc_subgraph_set_options", "byoc_last_error"]
+           "byoc_subgraph_set_options", "byoc_subgraph_run_static", "byoc_last_error"]
 OPT_GRAPH_REPLAY = 1
 OPT_AUTOTUNE = 2
 
@@ -71,6 +71,7 @@ def load_library(path=LIB_PATH):
         "byoc_subgraph_create": [ctypes.c_char_p, sz, ctypes.POINTER(ByocConst), i32, i32,
                                  ctypes.POINTER(P)],
         "byoc_subgraph_run": [P, ctypes.POINTER(P), i32, ctypes.POINTER(P), i32, P],
+        "byoc_subgraph_run_static": [P, ctypes.POINTER(P), i32, ctypes.POINTER(P), i32, P],
         "byoc_subgraph_destroy": [P],
         "byoc_subgraph_num_io": [P, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "byoc_subgraph_io_desc": [P, i32, i32, ctypes.POINTER(TensorDesc)],
@@ -242,6 +243,12 @@ class Subgraph:
         int, or None for torch's current stream)."""
         ins, outs, s = self._marshal(inputs, outputs, stream)
         _check(self.lib.byoc_subgraph_run(self.handle, ins, len(inputs), outs, len(outputs), s))
+
+    def run_static(self, inputs, outputs, stream=None):
+        """run() with the intermediates in the library's static per-device
+        scratch (allocates nothing; direct launches)."""
+        ins, outs, s = self._marshal(inputs, outputs, stream)
+        _check(self.lib.byoc_subgraph_run_static(self.handle, ins, len(inputs), outs, len(outputs), s))
 
     def set_options(self, graph_replay=None, autotune=None):
         """Turn engine options on or off; None keeps an option as it is.

@@ -68,6 +68,14 @@ byoc_status byoc_subgraph_run(byoc_subgraph* g, const void* const* inputs, int32
   return st.ok() ? BYOC_OK : fail(st);
 }
 
+byoc_status byoc_subgraph_run_static(byoc_subgraph* g, const void* const* inputs, int32_t n_in,
+                                     void* const* outputs, int32_t n_out, void* stream) {
+  g_last_error.clear();
+  if (!g || !g->engine) return fail(BYOC_ERR_INVALID_ARG, "subgraph handle is NULL");
+  byoc::Status st = byoc::engine_run_static(g->engine, inputs, n_in, outputs, n_out, (hipStream_t)stream);
+  return st.ok() ? BYOC_OK : fail(st);
+}
+
 byoc_status byoc_subgraph_destroy(byoc_subgraph* g) {
   g_last_error.clear();
   if (!g) return BYOC_OK;

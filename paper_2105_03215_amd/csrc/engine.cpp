@@ -1,5 +1,6 @@
 // Engine creation (planning, constant packing, arena layout) and runs.
 #include "engine.h"
+#include "static_scratch.h"
 
 #include <algorithm>
 #include <climits>
@@ -1298,9 +1299,10 @@ struct RunCtx {
   const void* const* in;
   void* const* out;
   hipStream_t s;
+  char* arena = nullptr;  // base of the intermediates (nullptr: the engine's own arena)
   void* ptr(const Ref& r) const {
     switch (r.kind) {
-      case Ref::Arena: return e->arena + e->bufs[r.idx].off + r.off;
+      case Ref::Arena: return (arena ? arena : e->arena) + e->bufs[r.idx].off + r.off;
       case Ref::Input: return const_cast<void*>(in[r.idx]);
       case Ref::Output: return out[r.idx];
       case Ref::Weights: return e->weights + r.off;
@@ -1882,6 +1884,22 @@ Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* cons
   return st;
 }
 
+Status engine_run_static(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
+                         int32_t n_out, hipStream_t stream) {
+  Status st = check_run_args(e, inputs, n_in, outputs, n_out);
+  if (!st.ok()) return st;
+  if (e->arena_bytes > kStaticScratchBytes)
+    return Status::Err(BYOC_ERR_INVALID_ARG, "the engine's intermediates need " + std::to_string(e->arena_bytes) +
+                                                 " bytes, more than the static scratch of " +
+                                                 std::to_string(kStaticScratchBytes) + " bytes");
+  DeviceGuard guard(e->device);
+  void* scratch = nullptr;
+  HIP_TRY(static_scratch_ptr(e->device, &scratch), "static scratch address");
+  RunCtx c{e, inputs, outputs, stream};
+  c.arena = static_cast<char*>(scratch);
+  return launch_all(e, c, false);
+}
+
 Status engine_profile_begin(Engine* e, int max_runs) {
   if (max_runs < 1 || max_runs > 100000)
     return Status::Err(BYOC_ERR_INVALID_ARG, "max_runs must be in [1, 100000]");
@@ -1945,7 +1963,7 @@ Status engine_destroy(Engine* e) {
   {
     DeviceGuard guard(e->device);
     // the last run enqueued through run() (the event completes at once when
-    // there was none)
+    // there was none); runs of run_static are the caller's to synchronise
     hipError_t err = e->done ? hipEventSynchronize(e->done) : hipSuccess;
     if (err != hipSuccess) st = Status::Err(BYOC_ERR_DEVICE, std::string("destroy: ") + hipGetErrorString(err));
     release(e);

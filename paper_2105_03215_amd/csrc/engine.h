@@ -87,6 +87,10 @@ Status engine_create(Graph&& g, const byoc_const* consts, int32_t n_consts, int 
                      Engine** out);
 Status engine_run(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
                   int32_t n_out, hipStream_t stream);
+// run() with the intermediates in the library's static per-device scratch
+// instead of the engine's arena: direct launches, no allocation of any kind.
+Status engine_run_static(Engine* e, const void* const* inputs, int32_t n_in, void* const* outputs,
+                         int32_t n_out, hipStream_t stream);
 Status engine_destroy(Engine* e);
 Status engine_set_options(Engine* e, int flags);
 Status engine_profile_begin(Engine* e, int max_runs);
