@@ -48,7 +48,7 @@ constexpr int kMaxStages = 4;  // deepest operand ring (deeper rings measured no
 template <int BM, int BN, int WM, int WN, int KG, int NS, bool ALIGNED, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN * KG) void conv_dma_kernel(ConvParams p) {
   static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves per reduction group");
-  static_assert(KG == 1 || (KG == 2 && !SPLIT), "reduction groups");
+  static_assert(KG == 1 || ((KG == 2 || KG == 4) && !SPLIT), "reduction groups");
   constexpr int kNT = 64 * WM * WN;          // threads of one reduction group
   constexpr int kNTall = kNT * KG;           // threads per workgroup
   constexpr int kRowsPerPass = kNT / kCH;    // rows one load instruction of every wave covers
@@ -427,10 +427,11 @@ hipError_t launch_stages(const ConvParams& p, int ns, hipStream_t s) {
 }  // namespace
 
 bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
-  if (stages < 1 || stages > kMaxStages || (kgroups != 1 && kgroups != 2)) return false;
+  if (stages < 1 || stages > kMaxStages || (kgroups != 1 && kgroups != 2 && kgroups != 4)) return false;
   if ((bm + bn) * 128 * stages * kgroups + 64 * 16 > kLdsLimit) return false;  // LDS: stage rings + bias
   const int waves = threads / (64 * kgroups);  // per reduction group
   if (threads != 64 * waves * kgroups) return false;
+  if (waves == 4 && kgroups == 4) return (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
   if (waves == 4)
     return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128) ||
            (bm == 64 && bn == 64) || (bm == 32 && bn == 64) ||
@@ -444,6 +445,11 @@ bool conv_dma_tile_supported(int bm, int bn, int stages, int threads, int kgroup
 hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int threads, int kgroups,
                            hipStream_t s) {
   if (!conv_dma_tile_supported(bm, bn, stages, threads, kgroups)) return hipErrorInvalidValue;
+  if (kgroups == 4) {
+    if (bm == 64 && bn == 64) return launch_stages<64, 64, 2, 2, 4>(p, stages, s);
+    if (bm == 32 && bn == 64) return launch_stages<32, 64, 1, 4, 4>(p, stages, s);
+    return hipErrorInvalidValue;
+  }
   if (kgroups == 2) {
     if (bm == 128 && bn == 128) return launch_stages<128, 128, 2, 2, 2>(p, stages, s);
     if (bm == 128 && bn == 64) return launch_stages<128, 64, 2, 2, 2>(p, stages, s);

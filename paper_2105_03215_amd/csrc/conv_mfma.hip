@@ -418,16 +418,28 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
   if (idx >= p.M * k4) return;
   const int m = mdiv(idx, p.mg_tile);  // mg_tile divides by Kp / 4 here
   const int k = (idx - m * k4) * 4;
-  float4 acc = *(const float4*)(p.partial + (size_t)m * p.Kp + k);
-  for (int sp = 1; sp < p.splits; ++sp) {
-    const float4 t = *(const float4*)(p.partial + ((size_t)sp * p.M + m) * p.Kp + k);
-    acc.x += t.x;
-    acc.y += t.y;
-    acc.z += t.z;
-    acc.w += t.w;
+  // bias and residual first, then the partials of up to 8 splits at a time,
+  // all loads in flight before the first add; the sum runs in split order
+  const float4 bv = p.bias ? *(const float4*)(p.bias + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+  const uint2 rr = p.res ? *(const uint2*)(p.res + (size_t)m * p.ldr + k) : make_uint2(0u, 0u);
+  const size_t stride = (size_t)p.M * p.Kp;
+  const float* part = p.partial + (size_t)m * p.Kp + k;
+  float4 acc = *(const float4*)part;
+  for (int sp0 = 1; sp0 < p.splits; sp0 += 8) {
+    float4 t[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      t[j] = sp0 + j < p.splits ? *(const float4*)(part + (size_t)(sp0 + j) * stride) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (sp0 + j < p.splits) {
+        acc.x += t[j].x;
+        acc.y += t[j].y;
+        acc.z += t[j].z;
+        acc.w += t[j].w;
+      }
   }
   if (p.bias) {
-    const float4 bv = *(const float4*)(p.bias + k);
     acc.x += bv.x;
     acc.y += bv.y;
     acc.z += bv.z;
@@ -435,7 +447,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ConvParams p) {
   }
   float r[4] = {0.f, 0.f, 0.f, 0.f};
   if (p.res) {
-    const uint2 rr = *(const uint2*)(p.res + (size_t)m * p.ldr + k);
     r[0] = __uint_as_float(rr.x << 16);
     r[1] = __uint_as_float(rr.x & 0xFFFF0000u);
     r[2] = __uint_as_float(rr.y << 16);

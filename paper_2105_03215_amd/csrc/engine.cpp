@@ -48,11 +48,12 @@ bool rescale_factor(double m, float* out) {
   return true;
 }
 
-// Chooses the workgroup tile and split-K factor of an implicit GEMM.  The
+// Chooses the workgroup tile (and split-K factor) of an implicit GEMM.  The
 // kernel is latency bound per stage, so the model favours the largest tile
-// that still yields about two workgroups per CU, splitting the reduction
-// (deterministically, reduced by a second kernel) when the output has too
-// few tiles and the reduction is long enough to share.
+// that still yields about two workgroups per CU, and shares a long
+// reduction between several wave groups of one workgroup when the output
+// has too few tiles (split-K over workgroups, reduced deterministically by
+// a second kernel, only when asked for).
 void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* kps) {
   // Measured on MI355X over the ResNet-50 layers: 64x64 tiles (16x16x32
   // MFMA) win at most batch-32 shapes - larger tiles leave fewer workgroups
@@ -73,12 +74,28 @@ void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* 
   if (tiles < 64 && nk >= 8) {
     int s = (int)std::min<int64_t>(nk / 4, (128 + tiles - 1) / tiles);
     s = std::max(1, std::min(s, 16));
+    // Measured on MI355X (ResNet-18 block and ResNet-50 at batch 1): where
+    // split-K would split only two ways, four reduction groups of 4 waves
+    // sharing each tile's stages inside one workgroup (sums added in the
+    // epilogue) beat the split and its reduce launch (a 3x3 64-channel
+    // layer at 56x56: 8.4 against 12.5 us); where it splits four or more
+    // ways, its extra workgroups win.  BYOC_CONV_KG4_MAXSPLIT=<n> moves the
+    // threshold (0: always split-K).
+    int kg4_max = 2;
+    if (const char* e = std::getenv("BYOC_CONV_KG4_MAXSPLIT")) kg4_max = std::atoi(e);
+    if (s > 1 && s <= kg4_max) {
+      t->stages = 2;
+      t->threads = 1024;
+      t->kgroups = 4;
+      return;
+    }
     if (s > 1) {
       *kps = (nk + s - 1) / s;
       *splits = (nk + *kps - 1) / *kps;
+      return;
     }
   }
-  if (*splits == 1 && tiles <= 256 && nk >= 8) {
+  if (tiles <= 256 && nk >= 8) {
     t->stages = 3;
     t->threads = 512;
     t->kgroups = 2;
@@ -90,6 +107,13 @@ void choose_conv_tile(int64_t M, int Kp, int Kg, ConvTile* t, int* splits, int* 
 // (HBM->LDS pipeline) forces a compiled tile, BYOC_CONV_SPLIT=<n> a
 // split-K factor, for every conv/dense composite of the engine.
 void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
+  const char* split_env = std::getenv("BYOC_CONV_SPLIT");
+  if (split_env && !std::getenv("BYOC_CONV_TILE") && t->kgroups > 1) {
+    // a forced split-K runs on the register-staged kernel
+    t->stages = 0;
+    t->threads = 256;
+    t->kgroups = 1;
+  }
   if (const char* e = std::getenv("BYOC_CONV_TILE")) {
     int bm = 0, bn = 0, mf = 16;
     int ns = 0;
@@ -131,7 +155,7 @@ void apply_tile_override(int Kg, ConvTile* t, int* splits, int* kps) {
     *kps = (Kg + kKPad - 1) / kKPad;
     return;
   }
-  if (const char* e = std::getenv("BYOC_CONV_SPLIT")) {
+  if (const char* e = split_env) {
     const int nk = (Kg + kKPad - 1) / kKPad;
     const int sp = std::max(1, std::min(std::atoi(e), nk));
     *kps = (nk + sp - 1) / sp;

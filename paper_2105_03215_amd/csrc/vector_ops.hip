@@ -3,6 +3,8 @@
 // lane moves 16-byte vectors (8 bf16 channels of one NHWC pixel) and
 // consecutive lanes take consecutive channel groups of a pixel, so a wave
 // reads and writes contiguous runs of memory.
+#include <algorithm>
+
 #include "device_common.h"
 
 namespace byoc {
@@ -56,6 +58,77 @@ __global__ __launch_bounds__(kThreads) void depthwise_kernel(DwParams p) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = apply_act(acc[i], p.act, p.alpha);
   *(uint4*)(p.y + o) = pack8(acc);
+}
+
+// Depthwise 3x3 conv, NHWC bf16, stride ST (1 or 2), any padding: every
+// thread finishes V vertically adjacent output pixels of one column for 8
+// channels.  It loads the (V - 1) * ST + 3 input rows x 3 columns that the
+// strip covers once into registers (16-byte buffer loads; an offset outside
+// the image reads zeros, which is the zero padding), the 9 tap weights and
+// the bias once, and then forms the V outputs from registers, so each input
+// row is fetched once per strip instead of once per tap and output.  Lanes
+// take consecutive channel groups, then consecutive columns, so every load
+// instruction of a wave reads one contiguous run of NHWC memory.  Grid:
+// x over (column, channel group) in blocks of kThreads, y over (image,
+// strip).  The taps are summed in the order (row, column) like the generic
+// kernel, each output from the bias up, so both kernels give the same bits.
+template <int ST, int V, int MODE>
+__global__ __launch_bounds__(kThreads) void depthwise3x3_kernel(DwParams p, int x_bytes, int strips, uint64_t mg_g,
+                                                                  uint64_t mg_strips) {
+  constexpr int NR = (V - 1) * ST + 3;  // input rows of a strip
+  const int G = p.Cp / 8;
+  const int pos = blockIdx.x * kThreads + threadIdx.x;
+  if (pos >= G * p.Q) return;
+  const int q = mdiv(pos, mg_g);
+  const int g = pos - q * G;
+  const int n = mdiv(blockIdx.y, mg_strips);
+  const int p0 = (blockIdx.y - n * strips) * V;
+  const int ih0 = p0 * ST - p.pt, iw0 = q * ST - p.pl;
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p.x), (short)0, x_bytes, kBufferFlags);
+  // image n's rows, element offsets (32-bit: x_bytes < 2^31)
+  const int img = n * p.H * p.W * p.Cp + g * 8;
+  uint4 xv[NR][3];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int ih = ih0 + r;
+    const bool rok = (unsigned)ih < (unsigned)p.H;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      const int iw = iw0 + c;
+      const bool ok = rok && (unsigned)iw < (unsigned)p.W;
+      const uint32_t off = ok ? (uint32_t)(img + (ih * p.W + iw) * p.Cp) * 2u : kOOB;
+      xv[r][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+    }
+  }
+  uint4 wv[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) wv[t] = *(const uint4*)(p.w + t * p.Cp + g * 8);
+  const float4 b0 = *(const float4*)(p.bias + g * 8);
+  const float4 b1 = *(const float4*)(p.bias + g * 8 + 4);
+  const ActClamp ac = act_clamp_of(p.act, p.alpha);
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const int pp = p0 + v;
+    if (pp >= p.P) break;
+    float acc[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        float xf[8], wf[8];
+        unpack8(xv[v * ST + r][c], xf);
+        unpack8(wv[r * 3 + c], wf);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(xf[i], wf[i], acc[i]);
+      }
+    const int o = ((n * p.P + pp) * p.Q + q) * p.Cp + g * 8;
+    float rv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (p.res) unpack8(*(const uint4*)(p.res + o), rv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = act_apply<MODE>(acc[i] + rv[i], ac);
+    *(uint4*)(p.y + o) = pack8(acc);
+  }
 }
 
 // Max pool NHWC bf16; the max of bf16 values is exact, no rounding.
@@ -243,24 +316,25 @@ __global__ __launch_bounds__(kThreads) void add_f32_kernel(const float* a, const
 // NCHW (f32 or bf16) -> NHWC bf16 with Cp >= C channels (pad zero).  Thread
 // per (n, channel group, h, w) with w fastest: reads are contiguous along w
 // for each channel; each thread writes one 16-byte vector.
+// Grid x over the pixels of an image, y over (image, channel group): every
+// thread moves 8 channels of one pixel, 32-bit index math (a plane holds
+// fewer than 2^31 pixels; image offsets in size_t).
 template <typename SrcT>
-__global__ __launch_bounds__(kThreads) void nchw_to_nhwc_kernel(const SrcT* x, bf16_t* y, int N,
-                                                                int C, int H, int W, int Cp) {
+__global__ __launch_bounds__(kThreads) void nchw_to_nhwc_kernel(const SrcT* x, bf16_t* y, int N, int C, int HW,
+                                                                int Cp) {
+  const int hw = blockIdx.x * kThreads + threadIdx.x;
+  if (hw >= HW) return;
   const int G = Cp / 8;
-  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t HW = (int64_t)H * W;
-  if (idx >= (int64_t)N * G * HW) return;
-  const int64_t hw = idx % HW;
-  const int64_t t = idx / HW;
-  const int g = (int)(t % G);
-  const int n = (int)(t / G);
+  const int n = blockIdx.y / G;
+  const int g = blockIdx.y - n * G;
+  const SrcT* xn = x + (size_t)n * C * HW + hw;
   float v[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int c = g * 8 + i;
     float f = 0.f;
     if (c < C) {
-      const SrcT e = x[((size_t)n * C + c) * HW + hw];
+      const SrcT e = xn[(size_t)c * HW];
       if constexpr (sizeof(SrcT) == 2) f = bf16_to_f32(e);
       else f = e;
     }
@@ -270,25 +344,23 @@ __global__ __launch_bounds__(kThreads) void nchw_to_nhwc_kernel(const SrcT* x, b
 }
 
 template <typename DstT>
-__global__ __launch_bounds__(kThreads) void nhwc_to_nchw_kernel(const bf16_t* x, DstT* y, int N,
-                                                                int C, int H, int W, int Cp) {
+__global__ __launch_bounds__(kThreads) void nhwc_to_nchw_kernel(const bf16_t* x, DstT* y, int N, int C, int HW,
+                                                                int Cp) {
+  const int hw = blockIdx.x * kThreads + threadIdx.x;
+  if (hw >= HW) return;
   const int G = Cp / 8;
-  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t HW = (int64_t)H * W;
-  if (idx >= (int64_t)N * G * HW) return;
-  const int64_t hw = idx % HW;
-  const int64_t t = idx / HW;
-  const int g = (int)(t % G);
-  const int n = (int)(t / G);
+  const int n = blockIdx.y / G;
+  const int g = blockIdx.y - n * G;
   const uint4 u = *(const uint4*)(x + ((size_t)n * HW + hw) * Cp + g * 8);
   const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+  DstT* yn = y + (size_t)n * C * HW + hw;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int c = g * 8 + i;
     if (c >= C) break;
     const bf16_t h = (bf16_t)((i & 1) ? (w4[i >> 1] >> 16) : (w4[i >> 1] & 0xFFFF));
-    if constexpr (sizeof(DstT) == 2) y[((size_t)n * C + c) * HW + hw] = h;
-    else y[((size_t)n * C + c) * HW + hw] = bf16_to_f32(h);
+    if constexpr (sizeof(DstT) == 2) yn[(size_t)c * HW] = h;
+    else yn[(size_t)c * HW] = bf16_to_f32(h);
   }
 }
 
@@ -378,7 +450,37 @@ __global__ __launch_bounds__(kThreads) void pack_vector_kernel(const SrcT* src, 
 
 }  // namespace
 
+namespace {
+
+template <int ST, int V>
+hipError_t launch_dw3x3(const DwParams& p, int x_bytes, hipStream_t s) {
+  const int G = p.Cp / 8;
+  const int strips = (p.P + V - 1) / V;
+  const dim3 grid((unsigned)((G * p.Q + kThreads - 1) / kThreads), (unsigned)(p.N * strips));
+  const int mode = act_mode(p.act);
+  if (mode == 1)
+    depthwise3x3_kernel<ST, V, 1><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, magic40(G), magic40(strips));
+  else if (mode == 0)
+    depthwise3x3_kernel<ST, V, 0><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, magic40(G), magic40(strips));
+  else
+    depthwise3x3_kernel<ST, V, 2><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, magic40(G), magic40(strips));
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_depthwise(const DwParams& p, hipStream_t s) {
+  const int64_t x_bytes = (int64_t)p.N * p.H * p.W * p.Cp * 2;
+  const int64_t y_elems = (int64_t)p.N * p.P * p.Q * p.Cp;
+  // strip kernel: 3x3 taps, equal strides of 1 or 2, 32-bit offsets, and
+  // the index products of the magic divisions below 2^40
+  const bool strip = p.R == 3 && p.S == 3 && p.sh == p.sw && (p.sh == 1 || p.sh == 2) && p.Cp % 8 == 0 &&
+                     x_bytes < (int64_t(1) << 31) && y_elems < (int64_t(1) << 31) &&
+                     (int64_t)(p.Cp / 8) * p.Q < (int64_t(1) << 20) && (int64_t)p.N * p.P < (int64_t(1) << 20);
+  if (strip) {
+    if (p.sh == 1) return launch_dw3x3<1, 4>(p, (int)x_bytes, s);
+    return launch_dw3x3<2, 2>(p, (int)x_bytes, s);
+  }
   const int64_t n = (int64_t)p.N * p.P * p.Q * (p.Cp / 8);
   depthwise_kernel<<<grid_for(n), kThreads, 0, s>>>(p);
   return hipGetLastError();
@@ -433,23 +535,47 @@ hipError_t launch_add_f32(const float* a, const float* b, float* y, int64_t n, i
   return hipGetLastError();
 }
 
+// Both layout transforms launch one grid row per (image, channel group);
+// batches with more rows than a grid dimension holds go in image chunks.
+constexpr int64_t kMaxGridY = 65535;
+
 hipError_t launch_nchw_to_nhwc(const void* x, bool src_bf16, bf16_t* y, int N, int C, int H,
                                int W, int Cp, hipStream_t s) {
-  const int64_t n = (int64_t)N * (Cp / 8) * H * W;
-  if (src_bf16)
-    nchw_to_nhwc_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)x, y, N, C, H, W, Cp);
-  else
-    nchw_to_nhwc_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)x, y, N, C, H, W, Cp);
+  const int64_t HW = (int64_t)H * W, G = Cp / 8;
+  if (HW == 0 || G == 0 || N == 0) return hipSuccess;
+  if (HW >= (int64_t(1) << 31) || G > kMaxGridY) return hipErrorInvalidValue;
+  const int chunk = (int)std::min<int64_t>(N, kMaxGridY / G);
+  const size_t esz = src_bf16 ? 2 : 4;
+  for (int n0 = 0; n0 < N; n0 += chunk) {
+    const int nn = std::min(chunk, N - n0);
+    const dim3 grid(grid_for(HW), (unsigned)(nn * G));
+    const char* xs = (const char*)x + (size_t)n0 * C * HW * esz;
+    bf16_t* yd = y + (size_t)n0 * HW * Cp;
+    if (src_bf16)
+      nchw_to_nhwc_kernel<bf16_t><<<grid, kThreads, 0, s>>>((const bf16_t*)xs, yd, nn, C, (int)HW, Cp);
+    else
+      nchw_to_nhwc_kernel<float><<<grid, kThreads, 0, s>>>((const float*)xs, yd, nn, C, (int)HW, Cp);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_nhwc_to_nchw(const bf16_t* x, void* y, bool dst_bf16, int N, int C, int H,
                                int W, int Cp, hipStream_t s) {
-  const int64_t n = (int64_t)N * (Cp / 8) * H * W;
-  if (dst_bf16)
-    nhwc_to_nchw_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>(x, (bf16_t*)y, N, C, H, W, Cp);
-  else
-    nhwc_to_nchw_kernel<float><<<grid_for(n), kThreads, 0, s>>>(x, (float*)y, N, C, H, W, Cp);
+  const int64_t HW = (int64_t)H * W, G = Cp / 8;
+  if (HW == 0 || G == 0 || N == 0) return hipSuccess;
+  if (HW >= (int64_t(1) << 31) || G > kMaxGridY) return hipErrorInvalidValue;
+  const int chunk = (int)std::min<int64_t>(N, kMaxGridY / G);
+  const size_t esz = dst_bf16 ? 2 : 4;
+  for (int n0 = 0; n0 < N; n0 += chunk) {
+    const int nn = std::min(chunk, N - n0);
+    const dim3 grid(grid_for(HW), (unsigned)(nn * G));
+    const bf16_t* xs = x + (size_t)n0 * HW * Cp;
+    char* yd = (char*)y + (size_t)n0 * C * HW * esz;
+    if (dst_bf16)
+      nhwc_to_nchw_kernel<bf16_t><<<grid, kThreads, 0, s>>>(xs, (bf16_t*)yd, nn, C, (int)HW, Cp);
+    else
+      nhwc_to_nchw_kernel<float><<<grid, kThreads, 0, s>>>(xs, (float*)yd, nn, C, (int)HW, Cp);
+  }
   return hipGetLastError();
 }
 

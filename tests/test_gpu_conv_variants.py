@@ -5,7 +5,7 @@ whose results are bit-for-bit those of the built-in choice: every tile of the
 HBM->LDS pipelined kernel (32x64 ... 256x128 pixels x channels), ring depths
 1-4, 4 or 8 waves, the register-staged kernel, and any XCD placement of the
 tiles, all within the reduction-order class of the built-in choice (one
-reduction group, or two groups that split the stages).  The 3x3 halo kernel
+reduction group, or two or four groups that split the stages).  The 3x3 halo kernel
 (input window staged in LDS) sums in its own order; its weight rings are its
 variants.  Here each variant is forced through the tile override on three
 layers at their batch-32 shapes and checked:
@@ -30,16 +30,17 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 LDS_LIMIT = 160 * 1024
 
-# (bm, bn) per workgroup shape: 4 waves, 8 waves, two 4-wave reduction groups
+# (bm, bn) per workgroup shape: 4 waves, 8 waves, two or four 4-wave reduction groups
 TILES_W4 = [(128, 128), (128, 64), (64, 128), (64, 64), (32, 64), (64, 256), (256, 64)]
 TILES_W8 = [(128, 128), (128, 64), (64, 128), (128, 256), (256, 128)]
 TILES_KG2 = [(128, 128), (128, 64), (64, 128), (64, 64), (32, 64)]
+TILES_KG4 = [(64, 64), (32, 64)]
 
 
 def dma_variants(m_rows):
     """(override string, kgroups) of every pipelined-kernel variant."""
     out = []
-    for tiles, threads, kg in ((TILES_W4, 256, 1), (TILES_W8, 512, 1), (TILES_KG2, 512, 2)):
+    for tiles, threads, kg in ((TILES_W4, 256, 1), (TILES_W8, 512, 1), (TILES_KG2, 512, 2), (TILES_KG4, 1024, 4)):
         for bm, bn in tiles:
             if bm == 32 and m_rows >= 48:
                 continue

@@ -27,14 +27,26 @@ def _splitk_workload():
     return g.finish()
 
 
-@pytest.mark.parametrize("name", ["resnet18_block", "splitk"])
-def test_bitwise_deterministic(name):
+def _kgroups_workload():
+    g = GraphBuilder("kgroups_det", 2001)
+    x = g.input("x", [1, 64, 56, 56], "uniform")
+    y = g.conv(x, 64, 3, act="relu", name="y")
+    g.output(y)
+    return g.finish()
+
+
+@pytest.mark.parametrize("name", ["resnet18_block", "splitk", "kgroups4"])
+def test_bitwise_deterministic(name, monkeypatch):
     announce("determinism " + name)
-    wl = workloads.resnet18_block() if name == "resnet18_block" else _splitk_workload()
+    wl = {"resnet18_block": workloads.resnet18_block, "splitk": _splitk_workload,
+          "kgroups4": _kgroups_workload}[name]()
     sg = capi.Subgraph(wl.graph, wl.consts)
     try:
         if name == "splitk":
             assert any(l["kind"] == "reduce" for l in sg.launches())
+        if name == "kgroups4":  # few tiles: four reduction groups in one workgroup
+            assert any("_k4_" in l["name"] for l in sg.launches()), [l["name"] for l in sg.launches()]
+        if name != "resnet18_block":
             o = oracle.run_graph(wl.graph, wl.consts, wl.inputs)[0]
         ins = runtime.inputs_for(sg, wl.inputs, DEV)
         a = runtime.outputs_for(sg, DEV)
@@ -44,7 +56,7 @@ def test_bitwise_deterministic(name):
         torch.cuda.synchronize()
         for x, y in zip(a, b):
             assert torch.equal(x.view(torch.int16), y.view(torch.int16))
-        if name == "splitk":
+        if name != "resnet18_block":
             assert rel_err(runtime.to_host_f64(a[0]), o) <= BF16_TOL
     finally:
         sg.close()

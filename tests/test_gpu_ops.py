@@ -64,6 +64,33 @@ CONV_CASES = [
 ]
 
 
+def _conv_case_graph(case, seed):
+    name, shape, k, r, stride, pad, act, res = case
+    g = GraphBuilder("op_" + name, seed)
+    x = g.input("x", list(shape), "uniform")
+    rname = None
+    if res:
+        n, c, h, w = shape
+        pads = [pad] * 4 if isinstance(pad, int) else list(pad)
+        p = (h + pads[0] + pads[2] - r) // stride + 1
+        q = (w + pads[1] + pads[3] - r) // stride + 1
+        rname = g.input("res", [n, k, p, q], "normal")
+    y = g.conv(x, k, r, stride=stride, pad=pad, act=act, residual=rname, name="y")
+    g.output(y)
+    return g.finish()
+
+
+@pytest.mark.parametrize("case", [c for c in CONV_CASES if "splitk" in c[0]],
+                         ids=[c[0] for c in CONV_CASES if "splitk" in c[0]])
+def test_conv_composite_forced_splitk(case, monkeypatch):
+    """Few-tile layers are planned with four reduction groups per workgroup;
+    split-K over workgroups (partials reduced by a second kernel in a fixed
+    order) stays available and is held to the same bar."""
+    monkeypatch.setenv("BYOC_CONV_SPLIT", "4")
+    launches = _check_bf16(_conv_case_graph(case, 1000 + CONV_CASES.index(case)), "conv split-K " + case[0])
+    assert any(l["kind"] == "reduce" for l in launches), [l["name"] for l in launches]
+
+
 @pytest.mark.parametrize("case", CONV_CASES, ids=[c[0] for c in CONV_CASES])
 def test_conv_composite(case):
     name, shape, k, r, stride, pad, act, res = case
@@ -122,22 +149,35 @@ def test_conv_halo_composite(case, monkeypatch):
 
 
 DW_CASES = [
-    ("dw_s1_c96", (2, 96, 14, 14), 1, False),
-    ("dw_s2_c144", (1, 144, 28, 28), 2, False),
-    ("dw_s1_c40_res", (1, 40, 9, 7), 1, True),
+    # name, (n, c, h, w), kernel, stride, pad, act, residual
+    ("dw_s1_c96", (2, 96, 14, 14), 3, 1, 1, "relu6", False),
+    ("dw_s2_c144", (1, 144, 28, 28), 3, 2, 1, "relu6", False),
+    ("dw_s1_c40_res", (1, 40, 9, 7), 3, 1, 1, "relu6", True),
+    # strips of 4 (stride 1) or 2 (stride 2) rows with ragged last strips,
+    # several blocks along (column, channel group), odd sizes
+    ("dw_s1_c32_ragged_rows", (3, 32, 113, 57), 3, 1, 1, "relu6", False),
+    ("dw_s2_c96_odd", (2, 96, 113, 111), 3, 2, 1, "relu6", False),
+    ("dw_s1_c960_7x7", (2, 960, 7, 7), 3, 1, 1, "relu6", True),
+    ("dw_s2_asym_pad", (1, 24, 10, 9), 3, 2, (0, 0, 1, 1), None, False),
+    ("dw_s1_leaky_no_pad", (2, 16, 6, 11), 3, 1, 0, "leaky", False),
+    ("dw_s1_gelu", (1, 64, 5, 5), 3, 1, 1, "gelu", True),
+    # not 3x3: the generic kernel
+    ("dw_5x5_generic", (1, 48, 12, 12), 5, 1, 2, "relu", False),
+    ("dw_3x3_s3_generic", (1, 8, 13, 13), 3, 3, 1, "relu", False),
 ]
 
 
 @pytest.mark.parametrize("case", DW_CASES, ids=[c[0] for c in DW_CASES])
 def test_depthwise_composite(case):
-    name, shape, stride, res = case
+    name, shape, r, stride, pad, act, res = case
     g = GraphBuilder("op_" + name, 1100 + DW_CASES.index(case))
     x = g.input("x", list(shape), "uniform")
     n, c, h, w = shape
-    p = (h + 2 - 3) // stride + 1
-    q = (w + 2 - 3) // stride + 1
+    pads = [pad] * 4 if isinstance(pad, int) else list(pad)
+    p = (h + pads[0] + pads[2] - r) // stride + 1
+    q = (w + pads[1] + pads[3] - r) // stride + 1
     rname = g.input("res", [n, c, p, q], "normal") if res else None
-    y = g.conv(x, c, 3, stride=stride, pad=1, groups=c, act="relu6", residual=rname, name="y")
+    y = g.conv(x, c, r, stride=stride, pad=pad, groups=c, act=act, residual=rname, name="y")
     g.output(y)
     launches = _check_bf16(g.finish(), "depthwise " + name)
     assert any(l["kind"] == "depthwise" for l in launches)
@@ -217,6 +257,36 @@ def _check_f32(wl, case):
 
 def test_f32_single_composite_config():
     _check_f32(workloads.conv_f32(), "conv_f32 1x16x32x32 -> 32")
+
+
+F32_CONV_CASES = [
+    # name, (n, c, h, w), k, r, stride, pad, act, residual: the
+    # register-blocked kernel (3x3 and 1x1: odd channel counts, output
+    # channels not a multiple of its 4-channel block, strides, residual) and
+    # the direct kernel (other kernel sizes)
+    ("s2_res_leaky_k13", (2, 64, 41, 40), 13, 3, 2, 1, "leaky", True),
+    ("k5_asym_pad_direct", (1, 6, 23, 19), 20, 5, 1, (2, 0, 1, 3), "relu6", False),
+    ("1x1_odd_channels", (1, 301, 9, 30), 16, 1, 1, 0, None, True),
+    ("wide_rows", (1, 4, 5, 300), 8, 3, 1, 1, "relu", False),
+    ("tiny_odd", (3, 5, 4, 4), 7, 3, 1, 1, "relu", False),
+]
+
+
+@pytest.mark.parametrize("case", F32_CONV_CASES, ids=[c[0] for c in F32_CONV_CASES])
+def test_f32_conv_cases(case):
+    name, shape, k, r, stride, pad, act, res = case
+    g = GraphBuilder("op_f32_" + name, 1550 + F32_CONV_CASES.index(case), dtype="f32")
+    x = g.input("x", list(shape), "uniform")
+    rname = None
+    if res:
+        n, c, h, w = shape
+        pads = [pad] * 4 if isinstance(pad, int) else list(pad)
+        p = (h + pads[0] + pads[2] - r) // stride + 1
+        q = (w + pads[1] + pads[3] - r) // stride + 1
+        rname = g.input("res", [n, k, p, q], "normal")
+    y = g.conv(x, k, r, stride=stride, pad=pad, act=act, residual=rname, bn=False, w_std=0.2, name="y")
+    g.output(y)
+    _check_f32(g.finish(), "f32 conv " + name)
 
 
 def test_f32_other_ops():

@@ -2,8 +2,8 @@
 byoc_subgraph_run: the same engine, the same inputs, outputs bit for bit
 equal, for two calls in a row where the second runs a smaller input (an
 engine of the same network at a smaller batch) on the scratch the first one
-left behind, then the first engine again.  ResNet-50 at batch 1 carries
-split-K launches, whose fp32 partial sums live in the scratch too.  An
+left behind, then the first engine again.  ResNet-50 at batch 1 is built
+with split-K launches, whose fp32 partial sums live in the scratch too.  An
 engine whose intermediates exceed the scratch is rejected before anything is
 enqueued."""
 
@@ -40,11 +40,13 @@ def _static_vs_run(sg, wl, stream):
                            b.view(torch.int16) if b.dtype == torch.bfloat16 else b)
 
 
-def test_run_static_matches_run_two_calls_second_smaller():
-    announce("run_static: resnet50_v1 bs2 then bs1, then bs2 again")
+def test_run_static_matches_run_two_calls_second_smaller(monkeypatch):
+    announce("run_static: resnet50_v1 bs2 then bs1 (split-K), then bs2 again")
     s = torch.cuda.Stream(device=DEV)
     wl2, sg2 = _engine("resnet50_v1", 2)
+    monkeypatch.setenv("BYOC_CONV_SPLIT", "4")  # few-tile layers as split-K launches
     wl1, sg1 = _engine("resnet50_v1", 1)
+    monkeypatch.delenv("BYOC_CONV_SPLIT")
     try:
         a2 = sg2.stats()["arena_bytes"]
         a1 = sg1.stats()["arena_bytes"]
