@@ -280,3 +280,72 @@ def test_quantized_depthwise_equals_rounded_float_depthwise():
     lo, hi = Q.act_bounds("relu6", sy, zy)
     want = np.clip(np.clip(zy + np.rint(t), lo, hi), -128, 127)
     assert np.array_equal(got, want.astype(np.int64))
+
+
+def test_int8_graph_wiring_dyadic_hand_derived():
+    """A five-node int8 graph whose scales make every rescaling an exact
+    integer operation, checked code by code against the arithmetic written
+    out here with plain integers (not the oracle's helpers): a 1x1 conv with
+    two output channels of different weight scales, bias and a residual of
+    another scale; a max pool keeping its input's (S, Z); an add of the pool
+    and an input of a third scale; a global average pool; a dense layer.  A
+    residual, pool or add operand wired to the wrong tensor's scale or zero
+    point, or a pool over the wrong window count, changes the codes.
+
+    Scales: x (1/4, 0), r (1/2, -3), conv (1/4, 5), add (1/4, -10),
+    pool of the add (1/16, 0), dense (1/16, 0).  Weights [1, -2] quantize to
+    codes [127, -127] with scales [1/127, 2/127], biases [1/2, -1/2] to
+    [254, -127], so the conv terms are x_q + 2 and -2 (x_q + 1) exactly."""
+    q = lambda s, z: {"scale": s, "zero_point": z}
+    rng = np.random.default_rng(5)
+    xq = rng.integers(-8, 12, size=(1, 1, 4, 4))
+    rq = rng.integers(-6, 7, size=(1, 2, 4, 4))
+    zq = rng.integers(-3, 4, size=(1, 2, 2, 2))
+    x = (xq * 0.25).astype(np.float32)
+    r = ((rq + 3) * 0.5).astype(np.float32)
+    z = zq.astype(np.float32)
+    w = np.array([1.0, -2.0], np.float32).reshape(2, 1, 1, 1)
+    b = np.array([0.5, -0.5], np.float32)
+    wd = np.array([[1.0, 0.0], [0.0, 1.0], [1.0, -1.0]], np.float32)
+    g = {"format": "byoc-subgraph", "version": 1,
+         "inputs": [{"name": "x", "shape": [1, 1, 4, 4], "dtype": "f32", "quant": q(0.25, 0)},
+                    {"name": "r", "shape": [1, 2, 4, 4], "dtype": "f32", "quant": q(0.5, -3)},
+                    {"name": "z", "shape": [1, 2, 2, 2], "dtype": "f32", "quant": q(1.0, 0)}],
+         "constants": [{"name": "w", "index": 0, "shape": [2, 1, 1, 1], "dtype": "f32"},
+                       {"name": "b", "index": 1, "shape": [2], "dtype": "f32"},
+                       {"name": "wd", "index": 2, "shape": [3, 2], "dtype": "f32"}],
+         "nodes": [
+             {"name": "c", "composite": "conv2d_bias_add_relu", "inputs": ["x", "w", "b", "r"], "out_dtype": "int8",
+              "attrs": {"strides": [1, 1], "padding": [0, 0, 0, 0]}, "quant": q(0.25, 5)},
+             {"name": "p", "composite": "max_pool2d", "inputs": ["c"], "out_dtype": "int8",
+              "attrs": {"pool_size": [2, 2], "strides": [2, 2], "padding": [0, 0, 0, 0]}, "quant": q(0.25, 5)},
+             {"name": "s", "composite": "add_relu", "inputs": ["p", "z"], "out_dtype": "int8", "quant": q(0.25, -10)},
+             {"name": "gp", "composite": "global_avg_pool2d", "inputs": ["s"], "out_dtype": "int8",
+              "quant": q(1.0 / 16, 0)},
+             {"name": "d", "composite": "dense", "inputs": ["gp", "wd"], "out_dtype": "int8", "quant": q(1.0 / 16, 0)}],
+         "outputs": [{"name": "d", "dtype": "f32"}, {"name": "p", "dtype": "f32"}, {"name": "s", "dtype": "f32"}]}
+    got = Q.run_quantized_graph(g, [w, b, wd], [x, r, z])
+
+    clip = lambda v: max(-128, min(127, v))
+    c = np.zeros((2, 4, 4), dtype=np.int64)
+    for i in range(4):
+        for j in range(4):
+            t0 = (int(xq[0, 0, i, j]) + 2) + 2 * (int(rq[0, 0, i, j]) + 3)
+            t1 = -2 * (int(xq[0, 0, i, j]) + 1) + 2 * (int(rq[0, 1, i, j]) + 3)
+            c[0, i, j] = clip(max(5 + t0, 5))
+            c[1, i, j] = clip(max(5 + t1, 5))
+    p = np.zeros((2, 2, 2), dtype=np.int64)
+    for k in range(2):
+        for i in range(2):
+            for j in range(2):
+                p[k, i, j] = max(c[k, 2 * i + a, 2 * j + e] for a in range(2) for e in range(2))
+    s = np.zeros((2, 2, 2), dtype=np.int64)
+    for k in range(2):
+        for i in range(2):
+            for j in range(2):
+                s[k, i, j] = clip(max(-10 + (p[k, i, j] - 5) + 4 * int(zq[0, k, i, j]), -10))
+    gp = [clip(sum(int(s[k, i, j]) + 10 for i in range(2) for j in range(2))) for k in range(2)]
+    d = [clip(gp[0]), clip(gp[1]), clip(gp[0] - gp[1])]
+    assert np.array_equal(got[1][0], 0.25 * (p - 5)), (got[1][0], p)
+    assert np.array_equal(got[2][0], 0.25 * (s + 10)), (got[2][0], s)
+    assert np.array_equal(got[0][0], np.array(d, dtype=np.float64) / 16.0), (got[0][0], d)
