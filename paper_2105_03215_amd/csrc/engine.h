@@ -80,6 +80,16 @@ struct Engine {
   hipStream_t prof_last_stream = nullptr;
   // marks the end of the last run() on its stream; destroy waits for it
   hipEvent_t done = nullptr;
+  // two-stream execution: launch i runs on the caller's stream (lstream 0)
+  // or on the engine's side stream (1) and first waits for the event of
+  // launch lwait[i] (>= 0) on the other stream; lrecord[i]: an event is
+  // recorded after launch i
+  bool two_streams = false;
+  hipStream_t side = nullptr;
+  std::vector<int8_t> lstream, lrecord;
+  std::vector<int> lwait;
+  std::vector<hipEvent_t> lev;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
 };
 
 // Builds the plan and device state.  On failure releases everything.

@@ -239,3 +239,41 @@ def test_autotune_keeps_results_bitwise(name):
         assert [l["name"] for l in sg.launches()] == names0
     finally:
         sg.close()
+
+
+@pytest.mark.parametrize("name,n", [("resnet50_v1", 32), ("resnet50_v1", 1), ("inception_v3", 2),
+                                    ("darknet53", 2), ("mobilenet_v2", 4)])
+def test_two_streams_match_one_stream(name, n, monkeypatch):
+    """With two-stream execution (BYOC_STREAMS=2) launches that do not
+    depend on their predecessor run on the engine's side stream (fork and
+    join through events, also when captured as a graph).  Outputs equal those
+    of the single-stream plan bit for bit, on direct launches and on graph
+    replays, with the output buffer poisoned between runs (a missing
+    dependency shows as a difference)."""
+    announce("two streams vs one: %s n=%d" % (name, n))
+    wl = workloads.build(name, n=n)
+    monkeypatch.delenv("BYOC_STREAMS", raising=False)
+    one = capi.Subgraph(wl.graph, wl.consts)
+    monkeypatch.setenv("BYOC_STREAMS", "2")
+    two = capi.Subgraph(wl.graph, wl.consts)
+    monkeypatch.delenv("BYOC_STREAMS")
+    s = torch.cuda.Stream(device=DEV)
+    try:
+        ins = runtime.inputs_for(one, wl.inputs, DEV)
+        ref = runtime.outputs_for(one, DEV)
+        one.run(ins, ref, s)
+        s.synchronize()
+        for replay in (False, True, True, True):
+            two.set_options(graph_replay=replay)
+            out = runtime.outputs_for(two, DEV)
+            for o in out:
+                o.fill_(float("nan"))
+            torch.cuda.synchronize()
+            for _ in range(2):
+                two.run(ins, out, s)
+            s.synchronize()
+            for a, b in zip(ref, out):
+                assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (name, n, replay)
+    finally:
+        one.close()
+        two.close()
