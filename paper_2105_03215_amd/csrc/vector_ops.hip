@@ -4,6 +4,8 @@
 // consecutive lanes take consecutive channel groups of a pixel, so a wave
 // reads and writes contiguous runs of memory.
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 
 #include "device_common.h"
 
@@ -478,7 +480,17 @@ hipError_t launch_depthwise(const DwParams& p, hipStream_t s) {
                      x_bytes < (int64_t(1) << 31) && y_elems < (int64_t(1) << 31) &&
                      (int64_t)(p.Cp / 8) * p.Q < (int64_t(1) << 20) && (int64_t)p.N * p.P < (int64_t(1) << 20);
   if (strip) {
-    if (p.sh == 1) return launch_dw3x3<1, 4>(p, (int)x_bytes, s);
+    // strip height (output rows per thread): 4 (stride 1) and 2 (stride 2)
+    // by default; BYOC_DW_STRIP=<v1>,<v2> picks 2, 4 or 8 and 1, 2 or 4
+    int v1 = 4, v2 = 2;
+    if (const char* e = std::getenv("BYOC_DW_STRIP")) std::sscanf(e, "%d,%d", &v1, &v2);
+    if (p.sh == 1) {
+      if (v1 == 2) return launch_dw3x3<1, 2>(p, (int)x_bytes, s);
+      if (v1 == 8) return launch_dw3x3<1, 8>(p, (int)x_bytes, s);
+      return launch_dw3x3<1, 4>(p, (int)x_bytes, s);
+    }
+    if (v2 == 1) return launch_dw3x3<2, 1>(p, (int)x_bytes, s);
+    if (v2 == 4) return launch_dw3x3<2, 4>(p, (int)x_bytes, s);
     return launch_dw3x3<2, 2>(p, (int)x_bytes, s);
   }
   const int64_t n = (int64_t)p.N * p.P * p.Q * (p.Cp / 8);

@@ -161,3 +161,26 @@ def test_resnet50_bs32_int8_timed_plan_all_images():
     diff = np.abs(got[0] - ref.astype(np.float64))
     print("timed plan resnet50 bs32 int8: %d of %d outputs differ" % (int((diff > 0).sum()), diff.size))
     assert np.array_equal(got[0], ref.astype(np.float64))
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["vgg19", "darknet53"])
+def test_other_networks_bs32_int8_timed_plan_sampled(name):
+    """The int8 forms of VGG19 and DarkNet-53 at the benchmark's batch 32
+    and full resolution, autotuned and graph-replayed as the benchmark runs
+    them; the int8 oracle recomputes images 0 and 31 (each image's codes
+    depend only on that image), which must match bit for bit."""
+    from oracle import quant as OQ
+    from parity_util import oracle_calibrated_int8
+    wl = workloads.build(name, n=32)
+    qg = oracle_calibrated_int8(wl.graph, wl.consts, [np.ascontiguousarray(a[:2]) for a in wl.inputs])
+    announce("timed plan %s bs32 int8" % name)
+    got, names = timed_plan_outputs(workloads.Workload(qg, wl.consts, wl.inputs, wl.macs, wl.conv_macs))
+    assert any(n.startswith("conv_i8") for n in names)
+    rows = [0, 31]
+    g2 = dict(qg)
+    g2["inputs"] = [dict(d, shape=[2] + list(d["shape"][1:])) for d in qg["inputs"]]
+    ref = OQ.run_quantized_graph(g2, wl.consts, [np.ascontiguousarray(a[rows]) for a in wl.inputs])[0]
+    diff = np.abs(got[0][rows] - ref.astype(np.float64))
+    print("timed plan %s bs32 int8: %d of %d sampled outputs differ" % (name, int((diff > 0).sum()), diff.size))
+    assert np.array_equal(got[0][rows], ref.astype(np.float64))
