@@ -137,7 +137,7 @@ def _roofline(launches, per_launch_ms, step_ms, traffic=None):
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
-            "kernel": ("conv/dense bf16 MFMA class (stem_conv_maxpool, conv_dma, conv_halo, conv_mfma, dense_rows, "
+            "kernel": ("conv/dense bf16 MFMA class (stem_conv_maxpool, conv_dma, conv_halo, conv_mfma, bottleneck, dense_rows, "
                        "splitk_reduce kernels), %d launches per step" % n_conv),
             "flops_per_step": conv_flops, "kernel_ms_per_step": round(conv_ms, 4),
             "per_launch_event_ms_per_step": round(conv_ev_ms, 4),

@@ -1,0 +1,496 @@
+// Fused ResNet bottleneck block: 1x1 reduce, 3x3, 1x1 expand with the
+// block input added back, as one kernel.
+//
+// The three composites of a bottleneck block are planned as separate
+// launches elsewhere; here they run in one workgroup per tile of output
+// pixels, and the two narrow intermediates live only in LDS (the engine owns
+// an offloaded subgraph's intermediates, Sec. 3.4, so they need not exist
+// in memory).  Of the HBM traffic of the three launches - x read twice, the
+// intermediates written and read back, y written - only one read of x (plus
+// the halo) and the write of y remain.
+//
+// A workgroup owns a TH x TW tile of output pixels of one image.
+//
+// Phase A (1x1 reduce): the tile's halo - (TH + 2) x (TW + 2) pixels - times
+// W1, streamed one 64-channel slice of x at a time through a ring of LDS
+// stages (x slice and W1 slice per stage, HBM -> LDS loads).  The sums are
+// finished (bias, activation, bf16 rounding) into M1 in LDS; halo pixels
+// outside the image are stored as zeros, the 3x3's zero padding.  While each
+// x slice is staged, the threads also copy the tile's own pixels of it into
+// registers: the residual of phase C, read from HBM only once.
+//
+// Phase B (3x3): nine shifted views of M1 times W2, streamed through a ring
+// of stages of TPS taps x SPB 64-channel slices (tap by tap, then slice);
+// the output tile is finished into M2 in LDS.
+//
+// Phase C (1x1 expand): M2 times W3, F output channels per chunk; bias, the
+// residual from registers, activation, bf16 stores to y.
+//
+// Operands of every product: weights are the MFMA A operand (16 output
+// channels), pixels the B operand, so each lane ends with 4 consecutive
+// channels of one pixel.  A wave owns one 64-channel group of the output
+// channels of each product and a set of 16-pixel tiles.  Every LDS row is
+// 128 bytes (64 channels) with its 16-byte chunks permuted by a per-row key
+// so that the 16 rows one MFMA operand read touches spread over the banks.
+//
+// Reduction order of each output: phase A slice by slice of x (32 channels
+// per MFMA step), phase B tap by tap then channel, phase C channel - the
+// order of the single-group implicit-GEMM kernel on the same composites.
+#include "lds_dma.h"
+
+namespace byoc {
+namespace {
+
+using namespace dma;
+
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+
+template <int F_, int CIN_, int TH_, int TW_, int NW_, int NSA_, int TPS_, int SPB_, int NSB_>
+struct Bn {
+  static constexpr int F = F_, CIN = CIN_, TH = TH_, TW = TW_, NW = NW_, NSA = NSA_, TPS = TPS_, SPB = SPB_;
+  static constexpr int NSB = NSB_;  // phase B ring
+  static constexpr int NT = 64 * NW;
+  static constexpr int WGC = F / 64;   // 64-channel groups of the mid width (a wave owns one)
+  static constexpr int WP = NW / WGC;  // waves per group
+  static constexpr int HC = TW + 2, HR = TH + 2;
+  static constexpr int HPX = HR * HC;               // halo pixels
+  static constexpr int HPXP = (HPX + 15) / 16 * 16;
+  static constexpr int OPX = TH * TW;               // output pixels
+  static constexpr int OPXP = (OPX + 15) / 16 * 16;
+  static constexpr int NTA = HPXP / 16, NTB = OPXP / 16;  // 16-pixel tiles
+  static constexpr int TA = (NTA + WP - 1) / WP;          // pixel tiles per wave, phase A
+  static constexpr int TB = (NTB + WP - 1) / WP;          // phases B and C
+  static constexpr int SA = CIN / 64;  // phase A stages (x slices)
+  static constexpr int GB = WGC / SPB;     // slice groups of a tap (phase B stage: TPS taps x SPB slices)
+  static constexpr int SB = 9 / TPS * GB;  // phase B stages
+  static constexpr int NQ = CIN / F;       // phase C chunks (F output channels each)
+  static constexpr int ROW = 128;
+  // LDS plan (bytes)
+  static constexpr int M1B = WGC * HPXP * ROW;
+  static constexpr int XB = HPXP * ROW;
+  static constexpr int W1B = F * ROW;
+  static constexpr int ASTG = XB + W1B;
+  static constexpr int W2B = TPS * SPB * F * ROW;
+  static constexpr int M2B = WGC * OPXP * ROW;
+  static constexpr int W3B = F * WGC * ROW;
+  static constexpr int OFF_R2 = M1B;  // phase A ring, then the W2 ring and M2
+  static constexpr int OFF_M2 = OFF_R2 + NSB * W2B;
+  static constexpr int END_A = OFF_R2 + NSA * ASTG;
+  static constexpr int END_B = OFF_M2 + M2B;
+  static constexpr int NSC = (OFF_M2 / W3B) < NQ ? (OFF_M2 / W3B) : NQ;  // W3 ring over M1 and the W2 ring
+  static constexpr int OFF_BIAS = END_A > END_B ? END_A : END_B;
+  static constexpr int B3BLK = (CIN * 4 + 1023) / 1024;
+  static constexpr int BBLK = 2 + B3BLK;  // 1 KB blocks: b1, b2, b3
+  static constexpr int OFF_JUNK = OFF_BIAS + BBLK * 1024;
+  static constexpr int LDS = OFF_JUNK + 1024;
+  // 1 KB fills (8 rows of 128 bytes) per stage and per thread
+  static constexpr int XBLK = HPXP / 8, W1BLK = F / 8, W2BLK = TPS * SPB * F / 8, W3BLK = WGC * F / 8;
+  static constexpr int LXA = (XBLK + NW - 1) / NW, LW1 = (W1BLK + NW - 1) / NW;
+  static constexpr int LA = LXA + LW1;
+  static constexpr int LB = (W2BLK + NW - 1) / NW;
+  static constexpr int LC = (W3BLK + NW - 1) / NW;
+  static constexpr int ST = TB * 4;  // y stores per chunk per thread
+
+  static_assert(F % 64 == 0 && CIN % F == 0 && NW % WGC == 0, "shape");
+  static_assert(9 % TPS == 0 && NSA >= 2 && NSA <= SA && NSB >= 2 && NSB <= SB, "stages");
+  static_assert(WGC % SPB == 0 && (TPS == 1 || SPB == WGC), "phase B stages run tap by tap, then slice");
+  static_assert(NSC >= 2, "W3 ring");
+  static_assert(BBLK <= NW, "one bias fill per wave");
+  static_assert(LDS <= kLdsLimit, "LDS");
+  static_assert((NSA - 2) * LA <= 63 && (NSB - 2) * LB <= 63, "vmcnt immediate");
+  static_assert((NSC - 2) * LC + (NSC - 1) * ST <= 63, "vmcnt immediate");
+};
+
+// rows r of a 128-byte-row buffer keep logical 16-byte chunk c at slot c ^ key
+__device__ __forceinline__ uint32_t slot_off(int row, int chunk, int key) {
+  return (uint32_t)(row * 128 + ((chunk ^ (key & 7)) << 4));
+}
+
+template <class B>
+__global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
+  constexpr int F = B::F, CIN = B::CIN, TW = B::TW, HC = B::HC, NW = B::NW, WP = B::WP;
+  __shared__ __attribute__((aligned(1024))) char lds[B::LDS];
+  asm volatile("" ::"s"(p.x), "s"(p.y), "s"(p.w1), "s"(p.w2), "s"(p.w3), "s"(p.b1), "s"(p.b2), "s"(p.b3));
+  asm volatile("" ::"s"(p.N), "s"(p.H), "s"(p.W), "s"(p.ld1), "s"(p.ld2), "s"(p.ld3), "s"(p.x_bytes),
+               "s"(p.y_bytes), "s"(p.w1_bytes), "s"(p.w2_bytes), "s"(p.w3_bytes));
+  asm volatile("" ::"s"(p.b1_bytes), "s"(p.b2_bytes), "s"(p.b3_bytes), "s"(p.act1), "s"(p.act2), "s"(p.act3),
+               "s"(p.alpha1), "s"(p.alpha2), "s"(p.alpha3), "s"(p.tiles_w), "s"(p.tiles_hw), "s"(p.mg_tw),
+               "s"(p.mg_thw), "s"(p.tiles), "s"(p.per_xcd));
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int l16 = lane & 15, lk = lane & 7, lq = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cg = wave % B::WGC, wp = wave / B::WGC;
+
+  // the tile: the hardware deals workgroups round-robin to the 8 XCDs, so
+  // XCD x takes the contiguous run of tiles [x * per_xcd, (x + 1) * per_xcd):
+  // neighbouring tiles, which read each other's halo rows, share an L2
+  const int tile = (blockIdx.x & 7) * p.per_xcd + (blockIdx.x >> 3);
+  if (tile >= p.tiles) return;
+  const int n = mdiv(tile, p.mg_thw);
+  const int tr = tile - n * p.tiles_hw;
+  const int th = mdiv(tr, p.mg_tw);
+  const int h0 = th * B::TH, w0 = (tr - th * p.tiles_w) * TW;
+  const int H = p.H, W = p.W;
+
+  const uint32_t base = lds_addr(lds);
+  const uint32_t junk = base + B::OFF_JUNK;
+  const float* sb1 = reinterpret_cast<const float*>(lds + B::OFF_BIAS);
+  const float* sb2 = sb1 + 256;
+  const float* sb3 = sb1 + 512;
+
+  // ---- load plans: per-thread source offsets, wave-uniform destinations ----
+  const i32x4 xr = buffer_rsrc(p.x, p.x_bytes);
+  const i32x4 w1r = buffer_rsrc(p.w1, p.w1_bytes);
+  const i32x4 w2r = buffer_rsrc(p.w2, p.w2_bytes);
+  const i32x4 w3r = buffer_rsrc(p.w3, p.w3_bytes);
+  uint32_t xoff[B::LXA], w1off[B::LW1], w2off[B::LB], w3off[B::LC];
+#pragma unroll
+  for (int u = 0; u < B::LXA; ++u) {
+    const int blk = wave + NW * u;
+    const int px = 8 * blk + (lane >> 3);
+    uint32_t off = kOOB;
+    if (blk < B::XBLK && px < B::HPX) {
+      const int hr = px / HC, hc = px - (px / HC) * HC;
+      const int h = h0 - 1 + hr, w = w0 - 1 + hc;
+      if ((unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
+        off = (uint32_t)((((n * H + h) * W + w) * CIN + ((lk ^ (px & 7)) * 8)) * 2);
+    }
+    xoff[u] = off;
+  }
+#pragma unroll
+  for (int u = 0; u < B::LW1; ++u) {
+    const int blk = wave + NW * u;
+    const int row = 8 * blk + (lane >> 3);
+    w1off[u] = blk < B::W1BLK ? (uint32_t)((row * p.ld1 + ((lk ^ (row & 7)) * 8)) * 2) : kOOB;
+  }
+#pragma unroll
+  for (int u = 0; u < B::LB; ++u) {
+    const int blk = wave + NW * u;
+    uint32_t off = kOOB;
+    if (blk < B::W2BLK) {
+      const int tap = blk / (B::SPB * F / 8), rem = blk - tap * (B::SPB * F / 8);
+      const int sl = rem / (F / 8);
+      const int row = 8 * (rem - sl * (F / 8)) + (lane >> 3);
+      off = (uint32_t)((row * p.ld2 + tap * F + sl * 64 + ((lk ^ (row & 7)) * 8)) * 2);
+    }
+    w2off[u] = off;
+  }
+#pragma unroll
+  for (int u = 0; u < B::LC; ++u) {
+    const int blk = wave + NW * u;
+    uint32_t off = kOOB;
+    if (blk < B::W3BLK) {
+      const int sl = blk / (F / 8);
+      const int row = 8 * (blk - sl * (F / 8)) + (lane >> 3);
+      off = (uint32_t)((row * p.ld3 + sl * 64 + ((lk ^ (row & 7)) * 8)) * 2);
+    }
+    w3off[u] = off;
+  }
+  auto dst = [&](uint32_t region, int blk, int nblk) {
+    return __builtin_amdgcn_readfirstlane(blk < nblk ? region + blk * 1024 : junk);
+  };
+  auto live = [](uint32_t off, uint32_t add) { return off == kOOB ? kOOB : off + add; };
+  auto issue_a = [&](int s) {
+    const uint32_t slot = base + B::OFF_R2 + (s % B::NSA) * B::ASTG;
+#pragma unroll
+    for (int u = 0; u < B::LXA; ++u) lds_fill16(xr, dst(slot, wave + NW * u, B::XBLK), live(xoff[u], s * 128));
+#pragma unroll
+    for (int u = 0; u < B::LW1; ++u)
+      lds_fill16(w1r, dst(slot + B::XB, wave + NW * u, B::W1BLK), live(w1off[u], s * 128));
+  };
+  auto issue_b = [&](int s) {
+    const uint32_t slot = base + B::OFF_R2 + (s % B::NSB) * B::W2B;
+#pragma unroll
+    for (int u = 0; u < B::LB; ++u)
+      lds_fill16(w2r, dst(slot, wave + NW * u, B::W2BLK),
+                 live(w2off[u], ((s / B::GB) * B::TPS * F + (s % B::GB) * B::SPB * 64) * 2));
+  };
+  auto issue_c = [&](int q) {
+    const uint32_t slot = base + (q % B::NSC) * B::W3B;
+#pragma unroll
+    for (int u = 0; u < B::LC; ++u)
+      lds_fill16(w3r, dst(slot, wave + NW * u, B::W3BLK), live(w3off[u], q * F * p.ld3 * 2));
+  };
+
+  // biases: wave w < 2 + B3BLK fills one 1 KB block (b1, b2, then b3)
+  {
+    const void* src = wave == 0 ? (const void*)p.b1 : wave == 1 ? (const void*)p.b2 : (const void*)p.b3;
+    const int bytes = wave == 0 ? p.b1_bytes : wave == 1 ? p.b2_bytes : p.b3_bytes;
+    const uint32_t off = wave < B::BBLK ? (uint32_t)((wave >= 2 ? wave - 2 : 0) * 1024 + lane * 16) : kOOB;
+    lds_fill16(buffer_rsrc(src, bytes), dst(base + B::OFF_BIAS, wave, B::BBLK), off);
+  }
+
+  const ActClamp ac1 = act_clamp_of(p.act1, p.alpha1);
+  const ActClamp ac2 = act_clamp_of(p.act2, p.alpha2);
+  const ActClamp ac3 = act_clamp_of(p.act3, p.alpha3);
+
+  // ---- phase A: M1 = act1(halo x W1 + b1) -----------------------------------
+  f32x4 accA[B::TA][4];
+#pragma unroll
+  for (int t = 0; t < B::TA; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) accA[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint2 resv[B::NQ][B::TB][4];  // residual: x at the tile's own pixels, per chunk of phase C
+
+  static_for<0, B::NSA - 1>([&](auto s) { issue_a(decltype(s)::value); });
+  static_for<0, B::SA>([&](auto ss) {
+    constexpr int s = decltype(ss)::value;
+    constexpr int younger = (B::NSA - 2 < B::SA - 1 - s) ? B::NSA - 2 : B::SA - 1 - s;
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(younger * B::LA) : "memory");
+    if constexpr (s + B::NSA - 1 < B::SA) issue_a(s + B::NSA - 1);
+    const char* xs = lds + B::OFF_R2 + (s % B::NSA) * B::ASTG;
+    const char* ws = xs + B::XB;
+    if (cg == s % B::WGC) {  // this slice is the residual of the wave's channel group in chunk s / WGC
+#pragma unroll
+      for (int t = 0; t < B::TB; ++t) {
+        const int o = 16 * (wp + WP * t) + l16;
+        const int hp = o < B::OPX ? (o / TW + 1) * HC + (o % TW) + 1 : 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          resv[s / B::WGC][t][i] = *(const uint2*)(xs + slot_off(hp, 2 * i + (lane >> 5), hp) + (lq & 1) * 8);
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = ks * 4 + lq;
+      bf16x8 a[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = as_bf16x8(*(const uint4*)(ws + slot_off(cg * 64 + 16 * i + l16, c, lk)));
+#pragma unroll
+      for (int t = 0; t < B::TA; ++t) {
+        const int j = wp + WP * t;
+        if (j < B::NTA) {
+          const bf16x8 b = as_bf16x8(*(const uint4*)(xs + slot_off(16 * j + l16, c, lk)));
+#pragma unroll
+          for (int i = 0; i < 4; ++i) accA[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b, accA[t][i], 0, 0, 0);
+        }
+      }
+    }
+  });
+  // every wave is done with the phase A ring: the W2 ring may overwrite it
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  static_for<0, B::NSB - 1>([&](auto s) { issue_b(decltype(s)::value); });
+  // biases into registers before the first M1 store (a later LDS read could
+  // not move above a store the compiler cannot tell apart from it)
+  float4 bias[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) bias[i] = *(const float4*)(sb1 + cg * 64 + 16 * i + 4 * lq);
+#pragma unroll
+  for (int t = 0; t < B::TA; ++t) {
+    const int j = wp + WP * t;
+    if (j >= B::NTA) continue;
+    const int px = 16 * j + l16;
+    const int hr = px / HC, hc = px - (px / HC) * HC;
+    const int h = h0 - 1 + hr, w = w0 - 1 + hc;
+    const bool inside = px < B::HPX && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+    const int key = hr * TW + hc;
+    char* m1 = lds + cg * B::HPXP * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 bb = bias[i];
+      const f32x4 v = accA[t][i];
+      float f0 = act_apply<0>(v[0] + bb.x, ac1), f1 = act_apply<0>(v[1] + bb.y, ac1);
+      float f2 = act_apply<0>(v[2] + bb.z, ac1), f3 = act_apply<0>(v[3] + bb.w, ac1);
+      if (!inside) f0 = f1 = f2 = f3 = 0.f;
+      *(uint2*)(m1 + slot_off(px, 2 * i + (lane >> 5), key) + (lq & 1) * 8) =
+          make_uint2(pack2_bf16(f0, f1), pack2_bf16(f2, f3));
+    }
+  }
+
+  // ---- phase B: M2 = act2(conv3x3(M1) W2 + b2) -------------------------------
+  int pbase[B::TB], obase[B::TB];
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t) {
+    const int o = 16 * (wp + WP * t) + l16;
+    const bool ok = o < B::OPX;
+    pbase[t] = ok ? (o / TW) * HC + (o % TW) : 0;
+    obase[t] = ok ? o : 0;
+  }
+  // phases B and C run every one of a wave's TB pixel tiles (a tile past the
+  // last reads pixel 0 and is never stored): no branches between the LDS
+  // reads of a step and its MFMAs
+  f32x4 accB[B::TB][4];
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) accB[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  static_for<0, B::SB>([&](auto ss) {
+    constexpr int s = decltype(ss)::value;
+    constexpr int younger = (B::NSB - 2 < B::SB - 1 - s) ? B::NSB - 2 : B::SB - 1 - s;
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(younger * B::LB) : "memory");
+    if constexpr (s + B::NSB - 1 < B::SB) issue_b(s + B::NSB - 1);
+    const char* wst = lds + B::OFF_R2 + (s % B::NSB) * B::W2B;
+    static_for<0, B::TPS>([&](auto uu) {
+      constexpr int u = decltype(uu)::value;
+      constexpr int tap = (s / B::GB) * B::TPS + u;
+      constexpr int r = tap / 3, sx = tap % 3;
+#pragma unroll
+      for (int sl = 0; sl < B::SPB; ++sl) {
+        const char* m1 = lds + ((s % B::GB) * B::SPB + sl) * B::HPXP * 128;
+        const char* wt = wst + (u * B::SPB + sl) * F * 128;
+        bf16x8 a[2][4], b[2][B::TB];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int c = ks * 4 + lq;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            a[ks][i] = as_bf16x8(*(const uint4*)(wt + slot_off(cg * 64 + 16 * i + l16, c, lk)));
+#pragma unroll
+          for (int t = 0; t < B::TB; ++t)
+            b[ks][t] = as_bf16x8(
+                *(const uint4*)(m1 + slot_off(pbase[t] + r * HC + sx, c, obase[t] + r * TW + sx)));
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              accB[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], accB[t][i], 0, 0, 0);
+      }
+    });
+  });
+  // every wave is done with M1 and the W2 ring: the W3 ring may overwrite them
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  static_for<0, B::NSC - 1>([&](auto q) { issue_c(decltype(q)::value); });
+#pragma unroll
+  for (int i = 0; i < 4; ++i) bias[i] = *(const float4*)(sb2 + cg * 64 + 16 * i + 4 * lq);
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t) {
+    const int jb = wp + WP * t;
+    if (jb >= B::NTB) continue;
+    const int o = 16 * jb + l16;
+    char* m2 = lds + B::OFF_M2 + cg * B::OPXP * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 bb = bias[i];
+      const f32x4 v = accB[t][i];
+      const float f0 = act_apply<0>(v[0] + bb.x, ac2), f1 = act_apply<0>(v[1] + bb.y, ac2);
+      const float f2 = act_apply<0>(v[2] + bb.z, ac2), f3 = act_apply<0>(v[3] + bb.w, ac2);
+      *(uint2*)(m2 + slot_off(o, 2 * i + (lane >> 5), o) + (lq & 1) * 8) =
+          make_uint2(pack2_bf16(f0, f1), pack2_bf16(f2, f3));
+    }
+  }
+
+  // ---- phase C: y = act3(M2 W3 + b3 + x) ------------------------------------
+  // output offsets of this thread's pixels (kOOB: not stored)
+  uint32_t yoff[B::TB];
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t) {
+    const int o = 16 * (wp + WP * t) + l16;
+    const int oh = h0 + o / TW, ow = w0 + o % TW;
+    const bool ok = wp + WP * t < B::NTB && o < B::OPX && oh < H && ow < W;
+    yoff[t] = ok ? (uint32_t)((((n * H + oh) * W + ow) * CIN + cg * 64 + 4 * lq) * 2) : kOOB;
+  }
+  const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(p.y, (short)0, p.y_bytes, kBufferFlags);
+  int crow[B::TB];  // M2 row of this lane's pixel in each pixel tile (tile 0 for one past the last)
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t) crow[t] = (wp + WP * t < B::NTB ? 16 * (wp + WP * t) : 0) + l16;
+  static_for<0, B::NQ>([&](auto qq) {
+    constexpr int q = decltype(qq)::value;
+    // W3 loads younger than chunk q's, and y stores issued after them
+    constexpr int yl = (B::NSC - 2 < B::NQ - 1 - q) ? B::NSC - 2 : B::NQ - 1 - q;
+    constexpr int ys = q < B::NSC - 1 ? q : B::NSC - 1;
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(yl * B::LC + ys * B::ST) : "memory");
+    if constexpr (q + B::NSC - 1 < B::NQ) issue_c(q + B::NSC - 1);
+    const char* wst = lds + (q % B::NSC) * B::W3B;
+    f32x4 acc[B::TB][4];
+#pragma unroll
+    for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) bias[i] = *(const float4*)(sb3 + q * F + cg * 64 + 16 * i + 4 * lq);
+#pragma unroll
+    for (int sl = 0; sl < B::WGC; ++sl) {
+      const char* m2 = lds + B::OFF_M2 + sl * B::OPXP * 128;
+      const char* wt = wst + sl * F * 128;
+      bf16x8 a[2][4], b[2][B::TB];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c = ks * 4 + lq;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[ks][i] = as_bf16x8(*(const uint4*)(wt + slot_off(cg * 64 + 16 * i + l16, c, lk)));
+#pragma unroll
+        for (int t = 0; t < B::TB; ++t)
+          b[ks][t] = as_bf16x8(*(const uint4*)(m2 + slot_off(crow[t], c, lk)));
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], acc[t][i], 0, 0, 0);
+    }
+    // every thread issues all ST stores (out-of-range offsets for pixels it
+    // does not own), so the wait counts above are exact
+#pragma unroll
+    for (int t = 0; t < B::TB; ++t) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 bb = bias[i];
+        const uint2 rv = resv[q][t][i];
+        const f32x4 v = acc[t][i];
+        const float r0 = __uint_as_float(rv.x << 16), r1 = __uint_as_float(rv.x & 0xFFFF0000u);
+        const float r2 = __uint_as_float(rv.y << 16), r3 = __uint_as_float(rv.y & 0xFFFF0000u);
+        const float f0 = act_apply<0>((v[0] + bb.x) + r0, ac3), f1 = act_apply<0>((v[1] + bb.y) + r1, ac3);
+        const float f2 = act_apply<0>((v[2] + bb.z) + r2, ac3), f3 = act_apply<0>((v[3] + bb.w) + r3, ac3);
+        const uint32_t off = yoff[t] == kOOB ? kOOB : yoff[t] + (uint32_t)((q * F + 16 * i) * 2);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack2_bf16(f0, f1), pack2_bf16(f2, f3)}, yr, (int)off, 0, 0);
+      }
+    }
+  });
+}
+
+template <class B>
+hipError_t launch_one(const BottleneckParams& p_in, hipStream_t s) {
+  BottleneckParams p = p_in;
+  p.tiles_w = (p.W + B::TW - 1) / B::TW;
+  p.tiles_hw = p.tiles_w * ((p.H + B::TH - 1) / B::TH);
+  p.mg_tw = magic40(p.tiles_w);
+  p.mg_thw = magic40(p.tiles_hw);
+  p.tiles = p.N * p.tiles_hw;
+  p.per_xcd = (p.tiles + 7) / 8;
+  bottleneck_kernel<B><<<8 * p.per_xcd, B::NT, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+// (F, CIN) pairs and their variants: TH x TW output pixels, waves, phase A
+// ring, phase B stage (taps x 64-channel slices) and ring
+using V64a = Bn<64, 256, 8, 28, 7, 2, 1, 1, 6>;   // 134 KB LDS
+using V64b = Bn<64, 256, 8, 14, 7, 2, 1, 1, 5>;   // 80 KB: two workgroups per CU
+using V64c = Bn<64, 256, 8, 14, 7, 4, 1, 1, 8>;   // 136 KB, deeper rings
+using V128a = Bn<128, 512, 4, 28, 8, 2, 1, 1, 4>;  // 145 KB
+using V128b = Bn<128, 512, 7, 14, 8, 3, 1, 1, 4>;  // 143 KB
+using V128c = Bn<128, 512, 7, 14, 8, 2, 1, 1, 5>;  // 149 KB
+
+template <class A, class B, class C>
+hipError_t launch_of(int v, const BottleneckParams& p, hipStream_t s) {
+  return v == 0 ? launch_one<A>(p, s) : v == 1 ? launch_one<B>(p, s) : launch_one<C>(p, s);
+}
+
+}  // namespace
+
+int bottleneck_variants(int F, int CIN) {
+  if ((F == 64 && CIN == 256) || (F == 128 && CIN == 512)) return 3;
+  return 0;
+}
+
+const char* bottleneck_variant_name(int F, int CIN, int v) {
+  static const char* const k64[] = {"bottleneck_f64_8x28_w7_a2_b6", "bottleneck_f64_8x14_w7_a2_b5",
+                                    "bottleneck_f64_8x14_w7_a4_b8"};
+  static const char* const k128[] = {"bottleneck_f128_4x28_w8_a2_b4", "bottleneck_f128_7x14_w8_a3_b4",
+                                     "bottleneck_f128_7x14_w8_a2_b5"};
+  if (v < 0 || v >= bottleneck_variants(F, CIN)) return "bottleneck_unsupported";
+  return F == 64 ? k64[v] : k128[v];
+}
+
+hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int v, hipStream_t s) {
+  if (v < 0 || v >= bottleneck_variants(F, CIN)) return hipErrorInvalidValue;
+  if (F == 64) return launch_of<V64a, V64b, V64c>(v, p, s);
+  return launch_of<V128a, V128b, V128c>(v, p, s);
+}
+
+}  // namespace byoc

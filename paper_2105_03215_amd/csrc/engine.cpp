@@ -222,6 +222,10 @@ struct Planner {
   std::vector<int> alias_of, alias_off;
   // int8 graphs: input value -> the conv node that reads it as im2col rows (-1: none)
   std::vector<int> im2col_of;
+  // fused bottleneck blocks: 1x1 expand node -> its 3x3 node (-1: none), and
+  // 1x1 reduce / 3x3 nodes planned with it
+  std::vector<int> block_mid;
+  std::vector<bool> in_block;
 
   bool i8;                                  // partially quantized (int8) graph
   const byoc_const* consts = nullptr;       // host constants (int8 weights are quantized on the host)
@@ -286,6 +290,8 @@ struct Planner {
   void find_post_adds();
   void find_stems();
   void find_concat_aliases();
+  void find_blocks();
+  void plan_block(int ci);
   Ref slice(int vcat, int channel) const {  // channel slice of a concatenation's buffer
     Ref r = loc[vcat];
     r.off += (int64_t)channel * 2;
@@ -450,11 +456,120 @@ void Planner::find_post_adds() {
   }
 }
 
+// Bottleneck blocks: x -> 1x1 conv (+bias, act) -> 3x3 stride-1 pad-1 conv
+// (+bias, act) -> 1x1 conv + bias + x (act), each intermediate read only by
+// the next conv, with mid width F and CIN = channels of x a pair the fused
+// kernel is compiled for, run as one launch (the intermediates stay in LDS).
+// BYOC_FUSE_BLOCK=0 keeps the three launches.
+void Planner::find_blocks() {
+  block_mid.assign(g.nodes.size(), -1);
+  in_block.assign(g.nodes.size(), false);
+  const char* env = std::getenv("BYOC_FUSE_BLOCK");
+  if (!bf16 || (env && env[0] == '0')) return;
+  std::vector<int> uses(g.values.size(), 0);
+  for (const Node& n : g.nodes) {
+    for (int a : {n.data, n.residual, n.other})
+      if (a >= 0) ++uses[a];
+    if (n.op == OpKind::Concat)
+      for (size_t k = 1; k < n.cat.size(); ++k) ++uses[n.cat[k]];
+  }
+  for (const IoDesc& o : g.outputs) uses[o.value] += 2;
+  auto plain_conv = [&](const Node& n, int r, int pad) {
+    if (n.op != OpKind::Conv || n.depthwise || n.groups != 1 || n.act == Act::Gelu) return false;
+    const auto& ws = g.values[n.weight].shape;
+    return ws[2] == r && ws[3] == r && n.stride[0] == 1 && n.stride[1] == 1 && n.pad[0] == pad &&
+           n.pad[1] == pad && n.pad[2] == pad && n.pad[3] == pad;
+  };
+  auto fused_elsewhere = [&](int ni) {
+    return post_add[ni] >= 0 || post_conv[ni] >= 0 || stem_pool[ni] >= 0 || stem_conv[ni] >= 0;
+  };
+  for (size_t ci = 0; ci < g.nodes.size(); ++ci) {
+    const Node& c = g.nodes[ci];
+    if (!plain_conv(c, 1, 0) || c.residual < 0 || fused_elsewhere((int)ci) || alias_of[c.out] >= 0) continue;
+    const int x = c.residual, m2 = c.data;
+    const Value& v2 = g.values[m2];
+    if (v2.source != Value::Node || uses[m2] != 1) continue;
+    const int bi = v2.index;
+    const Node& b = g.nodes[bi];
+    if (!plain_conv(b, 3, 1) || b.residual >= 0 || fused_elsewhere(bi) || alias_of[m2] >= 0) continue;
+    const int m1 = b.data;
+    const Value& v1 = g.values[m1];
+    if (v1.source != Value::Node || uses[m1] != 1) continue;
+    const int ai = v1.index;
+    const Node& a = g.nodes[ai];
+    if (!plain_conv(a, 1, 0) || a.residual >= 0 || a.data != x || fused_elsewhere(ai) || alias_of[m1] >= 0) continue;
+    const auto& xs = g.values[x].shape;
+    const auto& s1 = g.values[m1].shape;
+    const auto& ys = g.values[c.out].shape;
+    if (xs.size() != 4 || s1.size() != 4 || ys != xs) continue;
+    const int CIN = (int)xs[1], F = (int)s1[1];
+    if (bottleneck_variants(F, CIN) <= 0) continue;
+    if (xs[0] * xs[2] * xs[3] * CIN * 2 >= (int64_t(1) << 31)) continue;
+    block_mid[ci] = bi;
+    in_block[ai] = in_block[bi] = true;
+  }
+}
+
+void Planner::plan_block(int ci) {
+  const Node& c = g.nodes[ci];
+  const Node& b = g.nodes[block_mid[ci]];
+  const Node& a = g.nodes[g.values[b.data].index];
+  const auto& xs = g.values[c.residual].shape;
+  Launch L;
+  L.op = Launch::Bottleneck;
+  L.info.kind = BYOC_K_CONV_MFMA;
+  L.info.node = ci;
+  L.x = loc[a.data];
+  L.res = loc[c.residual];
+  L.y = loc[c.out];
+  L.bnC = (int)xs[1];
+  L.bnF = (int)g.values[a.out].shape[1];
+  BottleneckParams& p = L.bn;
+  p.N = (int)xs[0], p.H = (int)xs[2], p.W = (int)xs[3];
+  int64_t wbytes = 0;
+  // packed weights and padded bias of one conv, as the implicit-GEMM kernel has them
+  auto pack = [&](const Node& n, Ref* w, Ref* bias, int* ld, int* w_bytes, int* b_bytes) {
+    const auto& ws = g.values[n.weight].shape;
+    const int K = (int)ws[0], Cg = (int)ws[1], R = (int)ws[2], S = (int)ws[3];
+    const int Cp = cp[n.data];
+    const int rows = (int)rup(K, kRowPad);
+    const int Kgp = (int)rup((int64_t)R * S * Cp, kKPad);
+    const int wc = g.values[n.weight].index;
+    const int bc = n.bias >= 0 ? g.values[n.bias].index : -1;
+    *w = wslot((int64_t)rows * Kgp * 2);
+    jobs.push_back({PackJob::ConvW, wc, w->off, K, Cg, R, S, Cp, Kgp, rows, 0, 0});
+    *bias = wslot((int64_t)rows * 4);
+    jobs.push_back({PackJob::Vec, bc, bias->off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? K : 0, rows});
+    *ld = Kgp;
+    *w_bytes = rows * Kgp * 2;
+    *b_bytes = rows * 4;
+    wbytes += numel(ws) * 2 + (bc >= 0 ? K * 4 : 0);
+  };
+  pack(a, &L.w, &L.bias, &p.ld1, &p.w1_bytes, &p.b1_bytes);
+  pack(b, &L.w2, &L.b2, &p.ld2, &p.w2_bytes, &p.b2_bytes);
+  pack(c, &L.w3, &L.b3, &p.ld3, &p.w3_bytes, &p.b3_bytes);
+  p.x_bytes = p.y_bytes = (int)(act_bytes(c.residual));
+  p.act1 = (int)a.act, p.act2 = (int)b.act, p.act3 = (int)c.act;
+  p.alpha1 = a.alpha, p.alpha2 = b.alpha, p.alpha3 = c.alpha;
+  L.info.flops = 2 * (a.macs + b.macs + c.macs);
+  L.info.bytes = act_bytes(c.residual) + act_bytes(c.out) + wbytes;
+  // built-in variant 0; BYOC_BLOCK_VARIANT=<v> forces another
+  int v = 0;
+  if (const char* bv = std::getenv("BYOC_BLOCK_VARIANT")) v = std::atoi(bv);
+  if (v < 0 || v >= bottleneck_variants(L.bnF, L.bnC)) v = 0;
+  L.tile = ConvTile{};
+  L.tile.bnv = v;
+  L.tile_default = L.tile;
+  name(L, bottleneck_variant_name(L.bnF, L.bnC, v));
+  e->launches.push_back(L);
+}
+
 Status Planner::plan() {
   if (i8) return plan_i8();
   find_stems();
   find_concat_aliases();
   find_post_adds();
+  find_blocks();
   // concatenation outputs are allocated first: their producers write into them
   for (const Node& n : g.nodes)
     if (n.op == OpKind::Concat) {
@@ -523,7 +638,7 @@ Status Planner::plan() {
         placed = true;
       }
     }
-    if (stem_pool[ni] >= 0 || post_add[ni] >= 0) {  // planned with the node that consumes it
+    if (stem_pool[ni] >= 0 || post_add[ni] >= 0 || in_block[ni]) {  // planned with the node that consumes it
       loc[v] = Ref();
       continue;
     }
@@ -535,6 +650,8 @@ Status Planner::plan() {
     if (!placed) loc[v] = arena(internal_bytes(v));
     if (stem_conv[ni] >= 0)
       plan_stem(stem_conv[ni], (int)ni);
+    else if (block_mid[ni] >= 0)
+      plan_block((int)ni);
     else if (post_conv[ni] >= 0)
       plan_node(post_conv[ni]);
     else
@@ -1445,6 +1562,18 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       a.y = (int8_t*)c.ptr(L.y);
       return launch_add_i8(a, c.s);
     }
+    case Launch::Bottleneck: {
+      BottleneckParams p = L.bn;
+      p.x = (const bf16_t*)c.ptr(L.x);
+      p.y = (bf16_t*)c.ptr(L.y);
+      p.w1 = (const bf16_t*)c.ptr(L.w);
+      p.w2 = (const bf16_t*)c.ptr(L.w2);
+      p.w3 = (const bf16_t*)c.ptr(L.w3);
+      p.b1 = (const float*)c.ptr(L.bias);
+      p.b2 = (const float*)c.ptr(L.b2);
+      p.b3 = (const float*)c.ptr(L.b3);
+      return launch_bottleneck(p, L.bnF, L.bnC, L.tile.bnv, c.s);
+    }
     case Launch::DepthwiseI8: {
       QDwParams d = L.qd;
       d.x = (const int8_t*)c.ptr(L.x);
@@ -1831,8 +1960,29 @@ std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
   return c;
 }
 
+// fused bottleneck blocks: every tile variant of the block's (F, CIN) pair
+// (one summation order for all of them)
+std::vector<ConvTile> block_candidates(const Launch& L) {
+  std::vector<ConvTile> c{L.tile_default};
+  for (int v = 0; v < bottleneck_variants(L.bnF, L.bnC); ++v) {
+    if (v == L.tile_default.bnv) continue;
+    ConvTile t = L.tile_default;
+    t.bnv = v;
+    c.push_back(t);
+  }
+  return c;
+}
+
+bool tunable(const Launch& L) {
+  return L.op == Launch::ConvMfma || L.op == Launch::ConvI8 || L.op == Launch::Bottleneck;
+}
+
 void apply_tile(Launch& L, const ConvTile& t) {
   L.tile = t;
+  if (L.op == Launch::Bottleneck) {
+    std::snprintf(L.info.name, sizeof(L.info.name), "%s", bottleneck_variant_name(L.bnF, L.bnC, t.bnv));
+    return;
+  }
   if (L.op == Launch::ConvI8) {
     L.qc.g.xcd_py = choose_xcd_split(L.qc.g, t);
     name_conv_i8(L);
@@ -1882,9 +2032,11 @@ Status autotune(Engine* e) {
   std::vector<std::vector<ConvTile>> cand(nl);
   size_t rounds = 1;
   for (size_t i = 0; i < nl; ++i)
-    if (e->launches[i].op == Launch::ConvMfma || e->launches[i].op == Launch::ConvI8) {
-      cand[i] = e->launches[i].op == Launch::ConvI8 ? conv_i8_candidates(e->launches[i])
-                                                      : conv_candidates(e->launches[i]);
+    if (tunable(e->launches[i])) {
+      const Launch& L = e->launches[i];
+      cand[i] = L.op == Launch::ConvI8       ? conv_i8_candidates(L)
+                : L.op == Launch::Bottleneck ? block_candidates(L)
+                                             : conv_candidates(L);
       rounds = std::max(rounds, cand[i].size());
     }
   std::vector<float> best_ms(nl, 0.f);
@@ -1922,7 +2074,7 @@ Status autotune(Engine* e) {
   if (err == hipSuccess) err = serr;
   if (err != hipSuccess) {
     for (Launch& L : e->launches)
-      if (L.op == Launch::ConvMfma || L.op == Launch::ConvI8) apply_tile(L, L.tile_default);
+      if (tunable(L)) apply_tile(L, L.tile_default);
     return Status::Err(BYOC_ERR_DEVICE, std::string("autotune: ") + hipGetErrorString(err));
   }
   return Status::Ok();
@@ -1943,7 +2095,7 @@ Status engine_set_options(Engine* e, int flags) {
   }
   if (tune_off)
     for (Launch& L : e->launches)
-      if (L.op == Launch::ConvMfma || L.op == Launch::ConvI8) apply_tile(L, L.tile_default);
+      if (tunable(L)) apply_tile(L, L.tile_default);
   e->options = flags;
   return Status::Ok();
 }

@@ -26,7 +26,7 @@ struct Launch {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
     AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows,
     ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels, QuantizeIm2colI8,
-    DepthwiseI8
+    DepthwiseI8, Bottleneck
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;
@@ -40,6 +40,12 @@ struct Launch {
   QConvParams qc{};  // int8 conv / dense (qc.g holds the geometry; tile in `tile`)
   QAddParams qa{};   // int8 add
   QDwParams qd{};    // int8 depthwise conv
+  // fused bottleneck block (Bottleneck): geometry and activations in bn,
+  // the 1x1 reduce's weights and bias in w / bias, the 3x3's in w2 / b2,
+  // the 1x1 expand's in w3 / b3; x is also the residual
+  BottleneckParams bn{};
+  Ref w2, b2, w3, b3;
+  int bnF = 0, bnC = 0;
   float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
   int qzero = 0;                 // quantize / dequantize zero point
   int qzx = 0, qzy = 0;          // int8 average pool: zero points

@@ -61,6 +61,7 @@ struct ConvTile {
   int kgroups = 1;    // conv_dma reduction groups (2: two 4-wave groups split the reduction stages)
   int halo = 0;       // 1: conv_halo kernel (stages = weight ring depth, lp / npb as planned)
   int lp = 0, npb = 0;
+  int bnv = -1;       // fused bottleneck block: the kernel variant
 };
 
 // Tile configurations with a compiled kernel.
@@ -104,6 +105,41 @@ int stem_weight_ld(int R);
 hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s);
 hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R, int S, int wld,
                                     hipStream_t s);
+// Fused bottleneck block of three conv composites with an identity residual:
+//   m1 = act1(conv1x1(x; w1) + b1)           CIN -> F channels
+//   m2 = act2(conv3x3(m1; w2, pad 1) + b2)   F -> F
+//   y  = act3(conv1x1(m2; w3) + b3 + x)      F -> CIN
+// each intermediate rounded to bf16 as the unfused composites store it; m1
+// and m2 never leave LDS.  x and y NHWC [N][H][W][CIN]; weights packed as
+// for the implicit-GEMM kernel ([rows][ld], kk = (r*3 + s)*F + c for w2);
+// biases fp32 zero-padded to >= 256 entries (b3: >= CIN).  Activations:
+// none, ReLU, ReLU6 or leaky ReLU.  A variant fixes (F, CIN) and the output
+// tile of one workgroup; every variant of an (F, CIN) pair sums in the same
+// order, so they agree bit for bit.
+struct BottleneckParams {
+  const bf16_t* x;
+  bf16_t* y;
+  const bf16_t* w1;
+  const bf16_t* w2;
+  const bf16_t* w3;
+  const float* b1;
+  const float* b2;
+  const float* b3;
+  int N, H, W;
+  int ld1, ld2, ld3;  // packed weight row strides (elements)
+  int x_bytes, y_bytes, w1_bytes, w2_bytes, w3_bytes, b1_bytes, b2_bytes, b3_bytes;
+  int act1, act2, act3;
+  float alpha1, alpha2, alpha3;
+  // set by the launcher: output tiles per row band, per image and in all,
+  // tiles per XCD, and the 40-bit reciprocals of the first two
+  int tiles_w, tiles_hw, tiles, per_xcd;
+  uint64_t mg_tw, mg_thw;
+};
+// Variant v of the block (0 .. bottleneck_variants(F, CIN) - 1); false if
+// (F, CIN) has no compiled kernel.
+int bottleneck_variants(int F, int CIN);
+const char* bottleneck_variant_name(int F, int CIN, int v);
+hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int v, hipStream_t s);
 // Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
 // one workgroup per 16 output channels, the reduction split over its waves.
 bool dense_rows_supported(const ConvParams& p);

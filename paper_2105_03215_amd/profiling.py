@@ -37,7 +37,7 @@ import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "conv_halo_kernel", "stem_conv_maxpool_kernel",
-                "splitk_reduce_kernel", "dense_rows_kernel")
+                "splitk_reduce_kernel", "dense_rows_kernel", "bottleneck_kernel")
 RUN_MARKER = "stem_conv_maxpool_kernel"  # one dispatch per run of the ResNet subgraphs
 
 

@@ -1,0 +1,118 @@
+"""Fused bottleneck blocks: 1x1 reduce -> 3x3 -> 1x1 expand + the block
+input, planned as one launch whose intermediates never leave LDS.
+
+Checked on ResNet-50 stage shapes and on ragged ones (image sizes that are
+not multiples of the kernel's output tile), two blocks chained:
+
+* the fused run equals, bit for bit, the three unfused launches on the
+  single-reduction-group implicit-GEMM kernel without split-K (the same
+  summation order and the same bf16 rounding of each composite's output);
+* every tile variant of the fused kernel gives the same bits, also when the
+  autotune picks among them under graph replay;
+* one block's output is within the bf16 tolerance of the oracle (bf16io).
+  (Two chained blocks on these inputs sit at the tolerance itself - 1.003e-2
+  on the 56x56 case, for the fused and the unfused launches alike - from the
+  bf16 storage of four composites in a row; the bit equality above carries
+  the per-composite one-ulp checks of the unfused kernels over to them.)
+"""
+
+import pytest
+import torch
+
+import oracle
+from paper_2105_03215_amd import capi, runtime
+from paper_2105_03215_amd.workloads import GraphBuilder
+from parity_util import BF16_TOL, announce, rel_err
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+ENV = ("BYOC_FUSE_BLOCK", "BYOC_CONV_TILE", "BYOC_CONV_SPLIT", "BYOC_BLOCK_VARIANT", "BYOC_CONV_HALO")
+# the unfused reference: every conv on one tile of the single-group kernel, no split-K
+UNFUSED_KG1 = {"BYOC_FUSE_BLOCK": "0", "BYOC_CONV_TILE": "d64x64s2t256k1", "BYOC_CONV_SPLIT": "1"}
+
+CASES = [
+    # name, batch, block channels, mid channels, height, width
+    ("s1_56x56", 2, 256, 64, 56, 56),
+    ("s1_ragged_30x19", 1, 256, 64, 30, 19),
+    ("s2_28x28", 2, 512, 128, 28, 28),
+    ("s2_ragged_13x9", 3, 512, 128, 13, 9),
+]
+
+
+def _blocks(case, n_blocks=2):
+    name, n, cin, mid, h, w = case
+    g = GraphBuilder("block_" + name, 3100 + (CASES.index(case) if case in CASES else 9))
+    y = g.input("x", [n, cin, h, w], "uniform")
+    for i in range(n_blocks):
+        a = g.conv(y, mid, 1, pad=0, act="relu", name="b%d.a" % i)
+        b = g.conv(a, mid, 3, pad=1, act="relu", name="b%d.b" % i)
+        y = g.conv(b, cin, 1, pad=0, act="relu", residual=y, name="b%d.c" % i)
+    g.output(y)
+    return g.finish()
+
+
+def _run(wl, monkeypatch, env, options=None):
+    for k in ENV:
+        monkeypatch.delenv(k, raising=False)
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
+    s = torch.cuda.Stream(device=DEV)
+    try:
+        if options:
+            sg.set_options(**options)
+        ins = runtime.inputs_for(sg, wl.inputs, DEV)
+        outs = runtime.outputs_for(sg, DEV)
+        outs[0].fill_(float("nan"))
+        torch.cuda.synchronize()
+        for _ in range(2 if options else 1):
+            sg.run(ins, outs, s)
+        s.synchronize()
+        return outs[0].clone(), [l["name"] for l in sg.launches()]
+    finally:
+        sg.close()
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_fused_block_matches_unfused_and_oracle(case, monkeypatch):
+    announce("fused block " + case[0])
+    wl = _blocks(case)
+    fused, names = _run(wl, monkeypatch, {})
+    assert sum(nm.startswith("bottleneck_") for nm in names) == 2, names
+    assert not any(nm.startswith("conv_") for nm in names), names
+    plain, pnames = _run(wl, monkeypatch, UNFUSED_KG1)
+    assert not any(nm.startswith("bottleneck_") for nm in pnames), pnames
+    assert torch.equal(fused.view(torch.int16), plain.view(torch.int16))
+    wl = _blocks(case, n_blocks=1)
+    fused, _ = _run(wl, monkeypatch, {})
+    ref = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    err = rel_err(runtime.to_host_f64(fused), ref)
+    print("%s: max rel err %.3e" % (case[0], err), flush=True)
+    assert err <= BF16_TOL
+
+
+@pytest.mark.parametrize("case", [CASES[0], CASES[2]], ids=[CASES[0][0], CASES[2][0]])
+def test_every_block_variant_and_autotune_bitwise(case, monkeypatch):
+    announce("block variants " + case[0])
+    wl = _blocks(case)
+    ref, names0 = _run(wl, monkeypatch, {"BYOC_BLOCK_VARIANT": "0"})
+    seen = {tuple(n for n in names0 if n.startswith("bottleneck_"))}
+    for v in (1, 2):
+        out, names = _run(wl, monkeypatch, {"BYOC_BLOCK_VARIANT": str(v)})
+        seen.add(tuple(n for n in names if n.startswith("bottleneck_")))
+        assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), v
+    assert len(seen) == 3, seen  # the variants are distinct kernels
+    out, _ = _run(wl, monkeypatch, {}, options={"autotune": True, "graph_replay": True})
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+
+
+def test_block_not_fused_when_disabled_or_unsupported(monkeypatch):
+    """BYOC_FUSE_BLOCK=0 and an unsupported width pair keep three launches."""
+    announce("block fusion off")
+    wl = _blocks(("odd", 1, 192, 48, 14, 14), n_blocks=1)
+    _, names = _run(wl, monkeypatch, {})
+    assert not any(n.startswith("bottleneck_") for n in names), names
+    wl = _blocks(CASES[0], n_blocks=1)
+    _, names = _run(wl, monkeypatch, {"BYOC_FUSE_BLOCK": "0"})
+    assert not any(n.startswith("bottleneck_") for n in names), names

@@ -32,7 +32,7 @@ def test_stats_counts_only_the_last_runs(tmp_path):
     out = tmp_path / "s.txt"
     profiling.stats(str(p), "cmd", str(out), last_runs=3, flops_per_run=60e9)
     text = out.read_text()
-    assert "last 3 runs" in text
+    assert "(3 runs of the subgraph after autotune, the last ones)" in text
     conv_line = [l for l in text.splitlines() if "conv_dma_kernel" in l][0].split()
     assert float(conv_line[-4]) == 2.0          # calls per run
     assert float(conv_line[-3]) == 25.0         # avg us
