@@ -41,9 +41,9 @@ def _static_vs_run(sg, wl, stream):
 
 
 def test_run_static_matches_run_two_calls_second_smaller(monkeypatch):
-    announce("run_static: resnet50_v1 bs2 then bs1 (split-K), then bs2 again")
+    announce("run_static: resnet50_v1 bs4 then bs1 (split-K), then bs4 again")
     s = torch.cuda.Stream(device=DEV)
-    wl2, sg2 = _engine("resnet50_v1", 2)
+    wl2, sg2 = _engine("resnet50_v1", 4)
     monkeypatch.setenv("BYOC_CONV_SPLIT", "4")  # few-tile layers as split-K launches
     wl1, sg1 = _engine("resnet50_v1", 1)
     monkeypatch.delenv("BYOC_CONV_SPLIT")
