@@ -487,6 +487,16 @@ const char* bottleneck_variant_name(int F, int CIN, int v) {
   return F == 64 ? k64[v] : k128[v];
 }
 
+int bottleneck_tiles(int F, int CIN, int v, int N, int H, int W) {
+  if (v < 0 || v >= bottleneck_variants(F, CIN)) return 0;
+  auto count = [&](auto cfg) {
+    using B = decltype(cfg);
+    return N * ((H + B::TH - 1) / B::TH) * ((W + B::TW - 1) / B::TW);
+  };
+  if (F == 64) return v == 0 ? count(V64a{}) : v == 1 ? count(V64b{}) : count(V64c{});
+  return v == 0 ? count(V128a{}) : v == 1 ? count(V128b{}) : count(V128c{});
+}
+
 hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int v, hipStream_t s) {
   if (v < 0 || v >= bottleneck_variants(F, CIN)) return hipErrorInvalidValue;
   if (F == 64) return launch_of<V64a, V64b, V64c>(v, p, s);

@@ -139,6 +139,8 @@ struct BottleneckParams {
 // (F, CIN) has no compiled kernel.
 int bottleneck_variants(int F, int CIN);
 const char* bottleneck_variant_name(int F, int CIN, int v);
+// Workgroups (output tiles) of variant v on an N x H x W block.
+int bottleneck_tiles(int F, int CIN, int v, int N, int H, int W);
 hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int v, hipStream_t s);
 // Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
 // one workgroup per 16 output channels, the reduction split over its waves.

@@ -28,6 +28,8 @@ pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
 ENV = ("BYOC_FUSE_BLOCK", "BYOC_CONV_TILE", "BYOC_CONV_SPLIT", "BYOC_BLOCK_VARIANT", "BYOC_CONV_HALO")
+# these blocks are small: fuse them whatever their tile count
+FUSED = {"BYOC_FUSE_BLOCK": "1"}
 # the unfused reference: every conv on one tile of the single-group kernel, no split-K
 UNFUSED_KG1 = {"BYOC_FUSE_BLOCK": "0", "BYOC_CONV_TILE": "d64x64s2t256k1", "BYOC_CONV_SPLIT": "1"}
 
@@ -78,14 +80,14 @@ def _run(wl, monkeypatch, env, options=None):
 def test_fused_block_matches_unfused_and_oracle(case, monkeypatch):
     announce("fused block " + case[0])
     wl = _blocks(case)
-    fused, names = _run(wl, monkeypatch, {})
+    fused, names = _run(wl, monkeypatch, FUSED)
     assert sum(nm.startswith("bottleneck_") for nm in names) == 2, names
     assert not any(nm.startswith("conv_") for nm in names), names
     plain, pnames = _run(wl, monkeypatch, UNFUSED_KG1)
     assert not any(nm.startswith("bottleneck_") for nm in pnames), pnames
     assert torch.equal(fused.view(torch.int16), plain.view(torch.int16))
     wl = _blocks(case, n_blocks=1)
-    fused, _ = _run(wl, monkeypatch, {})
+    fused, _ = _run(wl, monkeypatch, FUSED)
     ref = oracle.run_graph(wl.graph, wl.consts, wl.inputs, mode="bf16io")[0]
     err = rel_err(runtime.to_host_f64(fused), ref)
     print("%s: max rel err %.3e" % (case[0], err), flush=True)
@@ -96,23 +98,30 @@ def test_fused_block_matches_unfused_and_oracle(case, monkeypatch):
 def test_every_block_variant_and_autotune_bitwise(case, monkeypatch):
     announce("block variants " + case[0])
     wl = _blocks(case)
-    ref, names0 = _run(wl, monkeypatch, {"BYOC_BLOCK_VARIANT": "0"})
+    ref, names0 = _run(wl, monkeypatch, dict(FUSED, BYOC_BLOCK_VARIANT="0"))
     seen = {tuple(n for n in names0 if n.startswith("bottleneck_"))}
     for v in (1, 2):
-        out, names = _run(wl, monkeypatch, {"BYOC_BLOCK_VARIANT": str(v)})
+        out, names = _run(wl, monkeypatch, dict(FUSED, BYOC_BLOCK_VARIANT=str(v)))
         seen.add(tuple(n for n in names if n.startswith("bottleneck_")))
         assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), v
     assert len(seen) == 3, seen  # the variants are distinct kernels
-    out, _ = _run(wl, monkeypatch, {}, options={"autotune": True, "graph_replay": True})
+    out, _ = _run(wl, monkeypatch, FUSED, options={"autotune": True, "graph_replay": True})
     assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
 
 
-def test_block_not_fused_when_disabled_or_unsupported(monkeypatch):
-    """BYOC_FUSE_BLOCK=0 and an unsupported width pair keep three launches."""
-    announce("block fusion off")
+def test_block_fusion_rule(monkeypatch):
+    """Three launches where fusion is off (BYOC_FUSE_BLOCK=0), for a width
+    pair without a fused kernel, and by default for a block whose finest
+    tiling gives fewer than 256 workgroups; one launch by default from 256."""
+    announce("block fusion rule")
     wl = _blocks(("odd", 1, 192, 48, 14, 14), n_blocks=1)
-    _, names = _run(wl, monkeypatch, {})
+    _, names = _run(wl, monkeypatch, FUSED)
     assert not any(n.startswith("bottleneck_") for n in names), names
     wl = _blocks(CASES[0], n_blocks=1)
     _, names = _run(wl, monkeypatch, {"BYOC_FUSE_BLOCK": "0"})
     assert not any(n.startswith("bottleneck_") for n in names), names
+    _, names = _run(wl, monkeypatch, {})  # batch 2 at 56x56: 56 tiles of 8x14
+    assert not any(n.startswith("bottleneck_") for n in names), names
+    wl = _blocks(("s1_bs10", 10, 256, 64, 56, 56), n_blocks=1)  # 280 tiles of 8x14
+    _, names = _run(wl, monkeypatch, {})
+    assert sum(n.startswith("bottleneck_") for n in names) == 1, names
