@@ -36,6 +36,8 @@
 // Reduction order of each output: phase A slice by slice of x (32 channels
 // per MFMA step), phase B tap by tap then channel, phase C channel - the
 // order of the single-group implicit-GEMM kernel on the same composites.
+#include <cstdio>
+
 #include "lds_dma.h"
 
 namespace byoc {
@@ -45,9 +47,12 @@ using namespace dma;
 
 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 
-template <int F_, int CIN_, int TH_, int TW_, int NW_, int NSA_, int TPS_, int SPB_, int NSB_>
+template <int F_, int CIN_, int COUT_, int TH_, int TW_, int NW_, int NSA_, int TPS_, int SPB_, int NSB_>
 struct Bn {
-  static constexpr int F = F_, CIN = CIN_, TH = TH_, TW = TW_, NW = NW_, NSA = NSA_, TPS = TPS_, SPB = SPB_;
+  static constexpr int F = F_, CIN = CIN_, COUT = COUT_, TH = TH_, TW = TW_, NW = NW_, NSA = NSA_, TPS = TPS_;
+  static constexpr int SPB = SPB_;
+  // COUT != CIN: the residual is a 1x1 projection of x (CIN = 64: the x tile stays in LDS)
+  static constexpr bool PROJ = COUT_ != CIN_;
   static constexpr int NSB = NSB_;  // phase B ring
   static constexpr int NT = 64 * NW;
   static constexpr int WGC = F / 64;   // 64-channel groups of the mid width (a wave owns one)
@@ -63,36 +68,42 @@ struct Bn {
   static constexpr int SA = CIN / 64;  // phase A stages (x slices)
   static constexpr int GB = WGC / SPB;     // slice groups of a tap (phase B stage: TPS taps x SPB slices)
   static constexpr int SB = 9 / TPS * GB;  // phase B stages
-  static constexpr int NQ = CIN / F;       // phase C chunks (F output channels each)
+  static constexpr int NQ = COUT / F;      // phase C chunks (F output channels each)
   static constexpr int ROW = 128;
   // LDS plan (bytes)
   static constexpr int M1B = WGC * HPXP * ROW;
   static constexpr int XB = HPXP * ROW;
   static constexpr int W1B = F * ROW;
-  static constexpr int ASTG = XB + W1B;
+  static constexpr int ASTG = PROJ ? W1B : XB + W1B;  // phase A stage (the x slice of PROJ has its own region)
   static constexpr int W2B = TPS * SPB * F * ROW;
   static constexpr int M2B = WGC * OPXP * ROW;
   static constexpr int W3B = F * WGC * ROW;
+  static constexpr int WPB = PROJ ? F * ROW : 0;  // projection weights of a chunk (F rows x 64 channels)
+  static constexpr int CST = W3B + WPB;            // phase C stage
   static constexpr int OFF_R2 = M1B;  // phase A ring, then the W2 ring and M2
   static constexpr int OFF_M2 = OFF_R2 + NSB * W2B;
   static constexpr int END_A = OFF_R2 + NSA * ASTG;
   static constexpr int END_B = OFF_M2 + M2B;
-  static constexpr int NSC = (OFF_M2 / W3B) < NQ ? (OFF_M2 / W3B) : NQ;  // W3 ring over M1 and the W2 ring
+  static constexpr int NSC = (OFF_M2 / CST) < NQ ? (OFF_M2 / CST) : NQ;  // W3 ring over M1 and the W2 ring
   static constexpr int OFF_BIAS = END_A > END_B ? END_A : END_B;
-  static constexpr int B3BLK = (CIN * 4 + 1023) / 1024;
-  static constexpr int BBLK = 2 + B3BLK;  // 1 KB blocks: b1, b2, b3
+  static constexpr int B3BLK = (COUT * 4 + 1023) / 1024;
+  static constexpr int BBLK = 2 + (PROJ ? 2 : 1) * B3BLK;  // 1 KB blocks: b1, b2, b3 (, bp)
   static constexpr int OFF_JUNK = OFF_BIAS + BBLK * 1024;
-  static constexpr int LDS = OFF_JUNK + 1024;
+  static constexpr int OFF_X = OFF_JUNK + 1024;  // PROJ: the x tile
+  static constexpr int LDS = OFF_X + (PROJ ? XB : 0);
   // 1 KB fills (8 rows of 128 bytes) per stage and per thread
   static constexpr int XBLK = HPXP / 8, W1BLK = F / 8, W2BLK = TPS * SPB * F / 8, W3BLK = WGC * F / 8;
   static constexpr int LXA = (XBLK + NW - 1) / NW, LW1 = (W1BLK + NW - 1) / NW;
   static constexpr int LA = LXA + LW1;
   static constexpr int LB = (W2BLK + NW - 1) / NW;
-  static constexpr int LC = (W3BLK + NW - 1) / NW;
+  static constexpr int WPBLK = PROJ ? F / 8 : 0;
+  static constexpr int LC3 = (W3BLK + NW - 1) / NW, LCP = (WPBLK + NW - 1) / NW;
+  static constexpr int LC = LC3 + LCP;
   static constexpr int ST = TB * 4;  // y stores per chunk per thread
 
-  static_assert(F % 64 == 0 && CIN % F == 0 && NW % WGC == 0, "shape");
-  static_assert(9 % TPS == 0 && NSA >= 2 && NSA <= SA && NSB >= 2 && NSB <= SB, "stages");
+  static_assert(F % 64 == 0 && COUT % F == 0 && NW % WGC == 0, "shape");
+  static_assert(PROJ ? (CIN == 64 && F == 64) : CIN % F == 0, "shape");
+  static_assert(9 % TPS == 0 && NSA >= 2 && (NSA <= SA || SA == 1) && NSB >= 2 && NSB <= SB, "stages");
   static_assert(WGC % SPB == 0 && (TPS == 1 || SPB == WGC), "phase B stages run tap by tap, then slice");
   static_assert(NSC >= 2, "W3 ring");
   static_assert(BBLK <= NW, "one bias fill per wave");
@@ -113,6 +124,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   asm volatile("" ::"s"(p.x), "s"(p.y), "s"(p.w1), "s"(p.w2), "s"(p.w3), "s"(p.b1), "s"(p.b2), "s"(p.b3));
   asm volatile("" ::"s"(p.N), "s"(p.H), "s"(p.W), "s"(p.ld1), "s"(p.ld2), "s"(p.ld3), "s"(p.x_bytes),
                "s"(p.y_bytes), "s"(p.w1_bytes), "s"(p.w2_bytes), "s"(p.w3_bytes));
+  if constexpr (B::PROJ) asm volatile("" ::"s"(p.wp), "s"(p.bp), "s"(p.ldp), "s"(p.wp_bytes), "s"(p.bp_bytes));
   asm volatile("" ::"s"(p.b1_bytes), "s"(p.b2_bytes), "s"(p.b3_bytes), "s"(p.act1), "s"(p.act2), "s"(p.act3),
                "s"(p.alpha1), "s"(p.alpha2), "s"(p.alpha3), "s"(p.tiles_w), "s"(p.tiles_hw), "s"(p.mg_tw),
                "s"(p.mg_thw), "s"(p.tiles), "s"(p.per_xcd));
@@ -139,13 +151,15 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   const float* sb1 = reinterpret_cast<const float*>(lds + B::OFF_BIAS);
   const float* sb2 = sb1 + 256;
   const float* sb3 = sb1 + 512;
+  const float* sbp = sb3 + 256 * B::B3BLK;  // PROJ: projection bias
 
   // ---- load plans: per-thread source offsets, wave-uniform destinations ----
   const i32x4 xr = buffer_rsrc(p.x, p.x_bytes);
   const i32x4 w1r = buffer_rsrc(p.w1, p.w1_bytes);
   const i32x4 w2r = buffer_rsrc(p.w2, p.w2_bytes);
   const i32x4 w3r = buffer_rsrc(p.w3, p.w3_bytes);
-  uint32_t xoff[B::LXA], w1off[B::LW1], w2off[B::LB], w3off[B::LC];
+  const i32x4 wpr = buffer_rsrc(p.wp, B::PROJ ? p.wp_bytes : 0);
+  uint32_t xoff[B::LXA], w1off[B::LW1], w2off[B::LB], w3off[B::LC3], wpoff[B::LCP > 0 ? B::LCP : 1];
 #pragma unroll
   for (int u = 0; u < B::LXA; ++u) {
     const int blk = wave + NW * u;
@@ -178,7 +192,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     w2off[u] = off;
   }
 #pragma unroll
-  for (int u = 0; u < B::LC; ++u) {
+  for (int u = 0; u < B::LC3; ++u) {
     const int blk = wave + NW * u;
     uint32_t off = kOOB;
     if (blk < B::W3BLK) {
@@ -188,17 +202,24 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     }
     w3off[u] = off;
   }
+#pragma unroll
+  for (int u = 0; u < B::LCP; ++u) {
+    const int blk = wave + NW * u;
+    const int row = 8 * blk + (lane >> 3);
+    wpoff[u] = blk < B::WPBLK ? (uint32_t)((row * p.ldp + ((lk ^ (row & 7)) * 8)) * 2) : kOOB;
+  }
   auto dst = [&](uint32_t region, int blk, int nblk) {
     return __builtin_amdgcn_readfirstlane(blk < nblk ? region + blk * 1024 : junk);
   };
   auto live = [](uint32_t off, uint32_t add) { return off == kOOB ? kOOB : off + add; };
   auto issue_a = [&](int s) {
     const uint32_t slot = base + B::OFF_R2 + (s % B::NSA) * B::ASTG;
+    const uint32_t xdst = B::PROJ ? base + B::OFF_X : slot, wdst = B::PROJ ? slot : slot + B::XB;
 #pragma unroll
-    for (int u = 0; u < B::LXA; ++u) lds_fill16(xr, dst(slot, wave + NW * u, B::XBLK), live(xoff[u], s * 128));
+    for (int u = 0; u < B::LXA; ++u) lds_fill16(xr, dst(xdst, wave + NW * u, B::XBLK), live(xoff[u], s * 128));
 #pragma unroll
     for (int u = 0; u < B::LW1; ++u)
-      lds_fill16(w1r, dst(slot + B::XB, wave + NW * u, B::W1BLK), live(w1off[u], s * 128));
+      lds_fill16(w1r, dst(wdst, wave + NW * u, B::W1BLK), live(w1off[u], s * 128));
   };
   auto issue_b = [&](int s) {
     const uint32_t slot = base + B::OFF_R2 + (s % B::NSB) * B::W2B;
@@ -208,17 +229,22 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
                  live(w2off[u], ((s / B::GB) * B::TPS * F + (s % B::GB) * B::SPB * 64) * 2));
   };
   auto issue_c = [&](int q) {
-    const uint32_t slot = base + (q % B::NSC) * B::W3B;
+    const uint32_t slot = base + (q % B::NSC) * B::CST;
 #pragma unroll
-    for (int u = 0; u < B::LC; ++u)
+    for (int u = 0; u < B::LC3; ++u)
       lds_fill16(w3r, dst(slot, wave + NW * u, B::W3BLK), live(w3off[u], q * F * p.ld3 * 2));
+#pragma unroll
+    for (int u = 0; u < B::LCP; ++u)
+      lds_fill16(wpr, dst(slot + B::W3B, wave + NW * u, B::WPBLK), live(wpoff[u], q * F * p.ldp * 2));
   };
 
-  // biases: wave w < 2 + B3BLK fills one 1 KB block (b1, b2, then b3)
+  // biases: wave w < BBLK fills one 1 KB block (b1, b2, the blocks of b3, then those of bp)
   {
-    const void* src = wave == 0 ? (const void*)p.b1 : wave == 1 ? (const void*)p.b2 : (const void*)p.b3;
-    const int bytes = wave == 0 ? p.b1_bytes : wave == 1 ? p.b2_bytes : p.b3_bytes;
-    const uint32_t off = wave < B::BBLK ? (uint32_t)((wave >= 2 ? wave - 2 : 0) * 1024 + lane * 16) : kOOB;
+    const bool pb = wave >= 2 + B::B3BLK;
+    const void* src = wave == 0 ? (const void*)p.b1 : wave == 1 ? (const void*)p.b2 : pb ? (const void*)p.bp : (const void*)p.b3;
+    const int bytes = wave == 0 ? p.b1_bytes : wave == 1 ? p.b2_bytes : pb ? p.bp_bytes : p.b3_bytes;
+    const int blk = wave < 2 ? 0 : pb ? wave - 2 - B::B3BLK : wave - 2;
+    const uint32_t off = wave < B::BBLK ? (uint32_t)(blk * 1024 + lane * 16) : kOOB;
     lds_fill16(buffer_rsrc(src, bytes), dst(base + B::OFF_BIAS, wave, B::BBLK), off);
   }
 
@@ -232,7 +258,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   for (int t = 0; t < B::TA; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) accA[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  uint2 resv[B::NQ][B::TB][4];  // residual: x at the tile's own pixels, per chunk of phase C
+  uint2 resv[B::PROJ ? 1 : B::NQ][B::TB][4];  // residual: x at the tile's own pixels, per chunk of phase C
 
   static_for<0, B::NSA - 1>([&](auto s) { issue_a(decltype(s)::value); });
   static_for<0, B::SA>([&](auto ss) {
@@ -240,16 +266,16 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     constexpr int younger = (B::NSA - 2 < B::SA - 1 - s) ? B::NSA - 2 : B::SA - 1 - s;
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(younger * B::LA) : "memory");
     if constexpr (s + B::NSA - 1 < B::SA) issue_a(s + B::NSA - 1);
-    const char* xs = lds + B::OFF_R2 + (s % B::NSA) * B::ASTG;
-    const char* ws = xs + B::XB;
-    if (cg == s % B::WGC) {  // this slice is the residual of the wave's channel group in chunk s / WGC
+    const char* xs = B::PROJ ? lds + B::OFF_X : lds + B::OFF_R2 + (s % B::NSA) * B::ASTG;
+    const char* ws = B::PROJ ? lds + B::OFF_R2 + (s % B::NSA) * B::ASTG : xs + B::XB;
+    if (!B::PROJ && cg == s % B::WGC) {  // this slice is the residual of the wave's channel group in chunk s / WGC
 #pragma unroll
       for (int t = 0; t < B::TB; ++t) {
         const int o = 16 * (wp + WP * t) + l16;
         const int hp = o < B::OPX ? (o / TW + 1) * HC + (o % TW) + 1 : 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          resv[s / B::WGC][t][i] = *(const uint2*)(xs + slot_off(hp, 2 * i + (lane >> 5), hp) + (lq & 1) * 8);
+          resv[B::PROJ ? 0 : s / B::WGC][t][i] = *(const uint2*)(xs + slot_off(hp, 2 * i + (lane >> 5), hp) + (lq & 1) * 8);
       }
     }
 #pragma unroll
@@ -291,8 +317,9 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     for (int i = 0; i < 4; ++i) {
       const float4 bb = bias[i];
       const f32x4 v = accA[t][i];
-      float f0 = act_apply<0>(v[0] + bb.x, ac1), f1 = act_apply<0>(v[1] + bb.y, ac1);
-      float f2 = act_apply<0>(v[2] + bb.z, ac1), f3 = act_apply<0>(v[3] + bb.w, ac1);
+      // (+ 0: the unfused epilogue adds its zero residual, which turns a -0 into +0)
+      float f0 = act_apply<0>((v[0] + bb.x) + 0.f, ac1), f1 = act_apply<0>((v[1] + bb.y) + 0.f, ac1);
+      float f2 = act_apply<0>((v[2] + bb.z) + 0.f, ac1), f3 = act_apply<0>((v[3] + bb.w) + 0.f, ac1);
       if (!inside) f0 = f1 = f2 = f3 = 0.f;
       *(uint2*)(m1 + slot_off(px, 2 * i + (lane >> 5), key) + (lq & 1) * 8) =
           make_uint2(pack2_bf16(f0, f1), pack2_bf16(f2, f3));
@@ -367,8 +394,8 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     for (int i = 0; i < 4; ++i) {
       const float4 bb = bias[i];
       const f32x4 v = accB[t][i];
-      const float f0 = act_apply<0>(v[0] + bb.x, ac2), f1 = act_apply<0>(v[1] + bb.y, ac2);
-      const float f2 = act_apply<0>(v[2] + bb.z, ac2), f3 = act_apply<0>(v[3] + bb.w, ac2);
+      const float f0 = act_apply<0>((v[0] + bb.x) + 0.f, ac2), f1 = act_apply<0>((v[1] + bb.y) + 0.f, ac2);
+      const float f2 = act_apply<0>((v[2] + bb.z) + 0.f, ac2), f3 = act_apply<0>((v[3] + bb.w) + 0.f, ac2);
       *(uint2*)(m2 + slot_off(o, 2 * i + (lane >> 5), o) + (lq & 1) * 8) =
           make_uint2(pack2_bf16(f0, f1), pack2_bf16(f2, f3));
     }
@@ -382,12 +409,19 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     const int o = 16 * (wp + WP * t) + l16;
     const int oh = h0 + o / TW, ow = w0 + o % TW;
     const bool ok = wp + WP * t < B::NTB && o < B::OPX && oh < H && ow < W;
-    yoff[t] = ok ? (uint32_t)((((n * H + oh) * W + ow) * CIN + cg * 64 + 4 * lq) * 2) : kOOB;
+    yoff[t] = ok ? (uint32_t)((((n * H + oh) * W + ow) * B::COUT + cg * 64 + 4 * lq) * 2) : kOOB;
   }
   const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(p.y, (short)0, p.y_bytes, kBufferFlags);
   int crow[B::TB];  // M2 row of this lane's pixel in each pixel tile (tile 0 for one past the last)
 #pragma unroll
   for (int t = 0; t < B::TB; ++t) crow[t] = (wp + WP * t < B::NTB ? 16 * (wp + WP * t) : 0) + l16;
+  int xrow[B::TB];  // PROJ: halo row of this lane's pixel in the x tile
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t) {
+    const int o = crow[t];
+    xrow[t] = o < B::OPX ? (o / TW + 1) * HC + (o % TW) + 1 : 0;
+  }
+  float4 biasp[4];
   static_for<0, B::NQ>([&](auto qq) {
     constexpr int q = decltype(qq)::value;
     // W3 loads younger than chunk q's, and y stores issued after them
@@ -395,14 +429,40 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     constexpr int ys = q < B::NSC - 1 ? q : B::NSC - 1;
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(yl * B::LC + ys * B::ST) : "memory");
     if constexpr (q + B::NSC - 1 < B::NQ) issue_c(q + B::NSC - 1);
-    const char* wst = lds + (q % B::NSC) * B::W3B;
-    f32x4 acc[B::TB][4];
+    const char* wst = lds + (q % B::NSC) * B::CST;
+    f32x4 acc[B::TB][4], accp[B::TB][4];
 #pragma unroll
     for (int t = 0; t < B::TB; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 4; ++i) bias[i] = *(const float4*)(sb3 + q * F + cg * 64 + 16 * i + 4 * lq);
+    if constexpr (B::PROJ) {
+      // the projection of x over this chunk's channels (64 input channels)
+      const char* xs = lds + B::OFF_X;
+      const char* wpt = wst + B::W3B;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) biasp[i] = *(const float4*)(sbp + q * F + 16 * i + 4 * lq);
+      bf16x8 a[2][4], b[2][B::TB];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c = ks * 4 + lq;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[ks][i] = as_bf16x8(*(const uint4*)(wpt + slot_off(16 * i + l16, c, lk)));
+#pragma unroll
+        for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(*(const uint4*)(xs + slot_off(xrow[t], c, xrow[t])));
+      }
+#pragma unroll
+      for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) accp[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) accp[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], accp[t][i], 0, 0, 0);
+    }
 #pragma unroll
     for (int sl = 0; sl < B::WGC; ++sl) {
       const char* m2 = lds + B::OFF_M2 + sl * B::OPXP * 128;
@@ -431,7 +491,15 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float4 bb = bias[i];
-        const uint2 rv = resv[q][t][i];
+        uint2 rv;
+        if constexpr (B::PROJ) {  // the projection composite's output: bias, (no activation), bf16
+          const f32x4 u = accp[t][i];
+          const float4 c = biasp[i];
+          rv = make_uint2(pack2_bf16((u[0] + c.x) + 0.f, (u[1] + c.y) + 0.f),
+                          pack2_bf16((u[2] + c.z) + 0.f, (u[3] + c.w) + 0.f));
+        } else {
+          rv = resv[q][t][i];
+        }
         const f32x4 v = acc[t][i];
         const float r0 = __uint_as_float(rv.x << 16), r1 = __uint_as_float(rv.x & 0xFFFF0000u);
         const float r2 = __uint_as_float(rv.y << 16), r3 = __uint_as_float(rv.y & 0xFFFF0000u);
@@ -457,50 +525,58 @@ hipError_t launch_one(const BottleneckParams& p_in, hipStream_t s) {
   return hipGetLastError();
 }
 
-// (F, CIN) pairs and their variants: TH x TW output pixels, waves, phase A
-// ring, phase B stage (taps x 64-channel slices) and ring
-using V64a = Bn<64, 256, 8, 28, 7, 2, 1, 1, 6>;   // 134 KB LDS
-using V64b = Bn<64, 256, 8, 14, 7, 2, 1, 1, 5>;   // 80 KB: two workgroups per CU
-using V64c = Bn<64, 256, 8, 14, 7, 4, 1, 1, 8>;   // 136 KB, deeper rings
-using V128a = Bn<128, 512, 4, 28, 8, 2, 1, 1, 4>;  // 145 KB
-using V128b = Bn<128, 512, 7, 14, 8, 3, 1, 1, 4>;  // 143 KB
-using V128c = Bn<128, 512, 7, 14, 8, 2, 1, 1, 5>;  // 149 KB
+// Kinds (F, CIN, COUT) and their variants: TH x TW output pixels, waves,
+// phase A ring, phase B stage (taps x 64-channel slices) and ring
+using V64a = Bn<64, 256, 256, 8, 28, 7, 2, 1, 1, 6>;   // 134 KB LDS
+using V64b = Bn<64, 256, 256, 8, 14, 7, 2, 1, 1, 5>;   // 80 KB: two workgroups per CU
+using V64c = Bn<64, 256, 256, 8, 14, 7, 4, 1, 1, 8>;   // 136 KB, deeper rings
+using V128a = Bn<128, 512, 512, 4, 28, 8, 2, 1, 1, 4>;  // 145 KB
+using V128b = Bn<128, 512, 512, 7, 14, 8, 3, 1, 1, 4>;  // 143 KB
+using V128c = Bn<128, 512, 512, 7, 14, 8, 2, 1, 1, 5>;  // 149 KB
+using P64a = Bn<64, 64, 256, 8, 28, 7, 2, 1, 1, 6>;     // 157 KB
+using P64b = Bn<64, 64, 256, 8, 14, 7, 2, 1, 1, 2>;     // 75 KB: two workgroups per CU
+using P64c = Bn<64, 64, 256, 8, 14, 7, 2, 1, 1, 5>;     // 99 KB
 
-template <class A, class B, class C>
-hipError_t launch_of(int v, const BottleneckParams& p, hipStream_t s) {
-  return v == 0 ? launch_one<A>(p, s) : v == 1 ? launch_one<B>(p, s) : launch_one<C>(p, s);
+// f(Bn{}) on variant v of a kind, or `none` for an unknown one
+template <class R, class Fn>
+R with_variant(int F, int CIN, int COUT, int v, R none, Fn&& f) {
+  if (v < 0 || v > 2) return none;
+  if (F == 64 && CIN == 256 && COUT == 256) return v == 0 ? f(V64a{}) : v == 1 ? f(V64b{}) : f(V64c{});
+  if (F == 128 && CIN == 512 && COUT == 512) return v == 0 ? f(V128a{}) : v == 1 ? f(V128b{}) : f(V128c{});
+  if (F == 64 && CIN == 64 && COUT == 256) return v == 0 ? f(P64a{}) : v == 1 ? f(P64b{}) : f(P64c{});
+  return none;
+}
+
+template <class B>
+const char* variant_name() {
+  static char buf[64];
+  static const int once = std::snprintf(buf, sizeof(buf), "bottleneck_f%d_%s%dx%d_w%d_a%d_b%d", B::F,
+                                        B::PROJ ? "proj_" : "", B::TH, B::TW, B::NW, B::NSA, B::NSB);
+  (void)once;
+  return buf;
 }
 
 }  // namespace
 
-int bottleneck_variants(int F, int CIN) {
-  if ((F == 64 && CIN == 256) || (F == 128 && CIN == 512)) return 3;
-  return 0;
+int bottleneck_variants(int F, int CIN, int COUT) {
+  return with_variant(F, CIN, COUT, 0, 0, [](auto) { return 3; });
 }
 
-const char* bottleneck_variant_name(int F, int CIN, int v) {
-  static const char* const k64[] = {"bottleneck_f64_8x28_w7_a2_b6", "bottleneck_f64_8x14_w7_a2_b5",
-                                    "bottleneck_f64_8x14_w7_a4_b8"};
-  static const char* const k128[] = {"bottleneck_f128_4x28_w8_a2_b4", "bottleneck_f128_7x14_w8_a3_b4",
-                                     "bottleneck_f128_7x14_w8_a2_b5"};
-  if (v < 0 || v >= bottleneck_variants(F, CIN)) return "bottleneck_unsupported";
-  return F == 64 ? k64[v] : k128[v];
+const char* bottleneck_variant_name(int F, int CIN, int COUT, int v) {
+  return with_variant(F, CIN, COUT, v, (const char*)"bottleneck_unsupported",
+                      [](auto cfg) { return variant_name<decltype(cfg)>(); });
 }
 
-int bottleneck_tiles(int F, int CIN, int v, int N, int H, int W) {
-  if (v < 0 || v >= bottleneck_variants(F, CIN)) return 0;
-  auto count = [&](auto cfg) {
+int bottleneck_tiles(int F, int CIN, int COUT, int v, int N, int H, int W) {
+  return with_variant(F, CIN, COUT, v, 0, [&](auto cfg) {
     using B = decltype(cfg);
     return N * ((H + B::TH - 1) / B::TH) * ((W + B::TW - 1) / B::TW);
-  };
-  if (F == 64) return v == 0 ? count(V64a{}) : v == 1 ? count(V64b{}) : count(V64c{});
-  return v == 0 ? count(V128a{}) : v == 1 ? count(V128b{}) : count(V128c{});
+  });
 }
 
-hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int v, hipStream_t s) {
-  if (v < 0 || v >= bottleneck_variants(F, CIN)) return hipErrorInvalidValue;
-  if (F == 64) return launch_of<V64a, V64b, V64c>(v, p, s);
-  return launch_of<V128a, V128b, V128c>(v, p, s);
+hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int v, hipStream_t s) {
+  return with_variant(F, CIN, COUT, v, hipErrorInvalidValue,
+                      [&](auto cfg) { return launch_one<decltype(cfg)>(p, s); });
 }
 
 }  // namespace byoc

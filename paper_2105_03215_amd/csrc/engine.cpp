@@ -222,9 +222,9 @@ struct Planner {
   std::vector<int> alias_of, alias_off;
   // int8 graphs: input value -> the conv node that reads it as im2col rows (-1: none)
   std::vector<int> im2col_of;
-  // fused bottleneck blocks: 1x1 expand node -> its 3x3 node (-1: none), and
-  // 1x1 reduce / 3x3 nodes planned with it
-  std::vector<int> block_mid;
+  // fused bottleneck blocks: 1x1 expand node -> its 3x3 node (-1: none) and
+  // its projection node (-1: none), and the nodes planned with it
+  std::vector<int> block_mid, block_proj;
   std::vector<bool> in_block;
 
   bool i8;                                  // partially quantized (int8) graph
@@ -457,15 +457,18 @@ void Planner::find_post_adds() {
 }
 
 // Bottleneck blocks: x -> 1x1 conv (+bias, act) -> 3x3 stride-1 pad-1 conv
-// (+bias, act) -> 1x1 conv + bias + x (act), each intermediate read only by
-// the next conv, with mid width F and CIN = channels of x a pair the fused
-// kernel is compiled for, run as one launch (the intermediates stay in LDS)
+// (+bias, act) -> 1x1 conv + bias + r (act) with r = x or r = a 1x1 conv of x
+// without activation (the projection shortcut), each intermediate read only
+// by the next conv, of a kind (mid width, channels of x, channels of the
+// output) the fused kernel is compiled for, run as one launch (the
+// intermediates stay in LDS)
 // when its finest tiling gives at least one workgroup per CU (256): measured
 // on MI355X over ResNet-50 v1, fusing made batches 1-8 0.8-5% slower and
 // batch 16 (stage 1 only) and 32 faster.  BYOC_FUSE_BLOCK=0 keeps the three
 // launches everywhere, =1 fuses every supported block.
 void Planner::find_blocks() {
   block_mid.assign(g.nodes.size(), -1);
+  block_proj.assign(g.nodes.size(), -1);
   in_block.assign(g.nodes.size(), false);
   const char* env = std::getenv("BYOC_FUSE_BLOCK");
   if (!bf16 || (env && env[0] == '0')) return;
@@ -490,7 +493,18 @@ void Planner::find_blocks() {
   for (size_t ci = 0; ci < g.nodes.size(); ++ci) {
     const Node& c = g.nodes[ci];
     if (!plain_conv(c, 1, 0) || c.residual < 0 || fused_elsewhere((int)ci) || alias_of[c.out] >= 0) continue;
-    const int x = c.residual, m2 = c.data;
+    const int m2 = c.data;
+    // the residual: x itself, or the output of a projection conv of x read only here
+    int x = c.residual, pi = -1;
+    const Value& rv = g.values[c.residual];
+    if (rv.source == Value::Node) {
+      const Node& pn = g.nodes[rv.index];
+      if (plain_conv(pn, 1, 0) && pn.residual < 0 && pn.act == Act::None && uses[c.residual] == 1 &&
+          !fused_elsewhere(rv.index) && alias_of[c.residual] < 0) {
+        pi = rv.index;
+        x = pn.data;
+      }
+    }
     const Value& v2 = g.values[m2];
     if (v2.source != Value::Node || uses[m2] != 1) continue;
     const int bi = v2.index;
@@ -505,16 +519,20 @@ void Planner::find_blocks() {
     const auto& xs = g.values[x].shape;
     const auto& s1 = g.values[m1].shape;
     const auto& ys = g.values[c.out].shape;
-    if (xs.size() != 4 || s1.size() != 4 || ys != xs) continue;
-    const int CIN = (int)xs[1], F = (int)s1[1];
-    if (bottleneck_variants(F, CIN) <= 0) continue;
+    if (xs.size() != 4 || s1.size() != 4 || ys.size() != 4 || ys[0] != xs[0] || ys[2] != xs[2] ||
+        ys[3] != xs[3])
+      continue;
+    const int CIN = (int)xs[1], F = (int)s1[1], COUT = (int)ys[1];
+    if ((pi < 0) != (COUT == CIN) || bottleneck_variants(F, CIN, COUT) <= 0) continue;
     int most = 0;
-    for (int v = 0; v < bottleneck_variants(F, CIN); ++v)
-      most = std::max(most, bottleneck_tiles(F, CIN, v, (int)xs[0], (int)xs[2], (int)xs[3]));
+    for (int v = 0; v < bottleneck_variants(F, CIN, COUT); ++v)
+      most = std::max(most, bottleneck_tiles(F, CIN, COUT, v, (int)xs[0], (int)xs[2], (int)xs[3]));
     if (!always && most < 256) continue;
-    if (xs[0] * xs[2] * xs[3] * CIN * 2 >= (int64_t(1) << 31)) continue;
+    if (xs[0] * xs[2] * xs[3] * std::max(CIN, COUT) * 2 >= (int64_t(1) << 31)) continue;
     block_mid[ci] = bi;
+    block_proj[ci] = pi;
     in_block[ai] = in_block[bi] = true;
+    if (pi >= 0) in_block[pi] = true;
   }
 }
 
@@ -522,16 +540,18 @@ void Planner::plan_block(int ci) {
   const Node& c = g.nodes[ci];
   const Node& b = g.nodes[block_mid[ci]];
   const Node& a = g.nodes[g.values[b.data].index];
-  const auto& xs = g.values[c.residual].shape;
+  const int x = a.data;
+  const auto& xs = g.values[x].shape;
   Launch L;
   L.op = Launch::Bottleneck;
   L.info.kind = BYOC_K_CONV_MFMA;
   L.info.node = ci;
-  L.x = loc[a.data];
-  L.res = loc[c.residual];
+  L.x = loc[x];
+  L.res = loc[x];
   L.y = loc[c.out];
   L.bnC = (int)xs[1];
   L.bnF = (int)g.values[a.out].shape[1];
+  L.bnCout = (int)g.values[c.out].shape[1];
   BottleneckParams& p = L.bn;
   p.N = (int)xs[0], p.H = (int)xs[2], p.W = (int)xs[3];
   int64_t wbytes = 0;
@@ -556,19 +576,26 @@ void Planner::plan_block(int ci) {
   pack(a, &L.w, &L.bias, &p.ld1, &p.w1_bytes, &p.b1_bytes);
   pack(b, &L.w2, &L.b2, &p.ld2, &p.w2_bytes, &p.b2_bytes);
   pack(c, &L.w3, &L.b3, &p.ld3, &p.w3_bytes, &p.b3_bytes);
-  p.x_bytes = p.y_bytes = (int)(act_bytes(c.residual));
+  int64_t pmacs = 0;
+  if (block_proj[ci] >= 0) {
+    const Node& pn = g.nodes[block_proj[ci]];
+    pack(pn, &L.wp, &L.bp, &p.ldp, &p.wp_bytes, &p.bp_bytes);
+    pmacs = pn.macs;
+  }
+  p.x_bytes = (int)act_bytes(x);
+  p.y_bytes = (int)act_bytes(c.out);
   p.act1 = (int)a.act, p.act2 = (int)b.act, p.act3 = (int)c.act;
   p.alpha1 = a.alpha, p.alpha2 = b.alpha, p.alpha3 = c.alpha;
-  L.info.flops = 2 * (a.macs + b.macs + c.macs);
-  L.info.bytes = act_bytes(c.residual) + act_bytes(c.out) + wbytes;
+  L.info.flops = 2 * (a.macs + b.macs + c.macs + pmacs);
+  L.info.bytes = act_bytes(x) + act_bytes(c.out) + wbytes;
   // built-in variant 0; BYOC_BLOCK_VARIANT=<v> forces another
   int v = 0;
   if (const char* bv = std::getenv("BYOC_BLOCK_VARIANT")) v = std::atoi(bv);
-  if (v < 0 || v >= bottleneck_variants(L.bnF, L.bnC)) v = 0;
+  if (v < 0 || v >= bottleneck_variants(L.bnF, L.bnC, L.bnCout)) v = 0;
   L.tile = ConvTile{};
   L.tile.bnv = v;
   L.tile_default = L.tile;
-  name(L, bottleneck_variant_name(L.bnF, L.bnC, v));
+  name(L, bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, v));
   e->launches.push_back(L);
 }
 
@@ -1580,7 +1607,9 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.b1 = (const float*)c.ptr(L.bias);
       p.b2 = (const float*)c.ptr(L.b2);
       p.b3 = (const float*)c.ptr(L.b3);
-      return launch_bottleneck(p, L.bnF, L.bnC, L.tile.bnv, c.s);
+      p.wp = (const bf16_t*)c.ptr(L.wp);
+      p.bp = (const float*)c.ptr(L.bp);
+      return launch_bottleneck(p, L.bnF, L.bnC, L.bnCout, L.tile.bnv, c.s);
     }
     case Launch::DepthwiseI8: {
       QDwParams d = L.qd;
@@ -1972,7 +2001,7 @@ std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
 // (one summation order for all of them)
 std::vector<ConvTile> block_candidates(const Launch& L) {
   std::vector<ConvTile> c{L.tile_default};
-  for (int v = 0; v < bottleneck_variants(L.bnF, L.bnC); ++v) {
+  for (int v = 0; v < bottleneck_variants(L.bnF, L.bnC, L.bnCout); ++v) {
     if (v == L.tile_default.bnv) continue;
     ConvTile t = L.tile_default;
     t.bnv = v;
@@ -1988,7 +2017,7 @@ bool tunable(const Launch& L) {
 void apply_tile(Launch& L, const ConvTile& t) {
   L.tile = t;
   if (L.op == Launch::Bottleneck) {
-    std::snprintf(L.info.name, sizeof(L.info.name), "%s", bottleneck_variant_name(L.bnF, L.bnC, t.bnv));
+    std::snprintf(L.info.name, sizeof(L.info.name), "%s", bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, t.bnv));
     return;
   }
   if (L.op == Launch::ConvI8) {

@@ -42,10 +42,10 @@ struct Launch {
   QDwParams qd{};    // int8 depthwise conv
   // fused bottleneck block (Bottleneck): geometry and activations in bn,
   // the 1x1 reduce's weights and bias in w / bias, the 3x3's in w2 / b2,
-  // the 1x1 expand's in w3 / b3; x is also the residual
+  // the 1x1 expand's in w3 / b3, the projection's in wp / bp; res is x
   BottleneckParams bn{};
-  Ref w2, b2, w3, b3;
-  int bnF = 0, bnC = 0;
+  Ref w2, b2, w3, b3, wp, bp;
+  int bnF = 0, bnC = 0, bnCout = 0;
   float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
   int qzero = 0;                 // quantize / dequantize zero point
   int qzx = 0, qzy = 0;          // int8 average pool: zero points

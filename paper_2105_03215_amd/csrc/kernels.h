@@ -105,29 +105,32 @@ int stem_weight_ld(int R);
 hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s);
 hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R, int S, int wld,
                                     hipStream_t s);
-// Fused bottleneck block of three conv composites with an identity residual:
+// Fused bottleneck block of three conv composites and its residual:
 //   m1 = act1(conv1x1(x; w1) + b1)           CIN -> F channels
 //   m2 = act2(conv3x3(m1; w2, pad 1) + b2)   F -> F
-//   y  = act3(conv1x1(m2; w3) + b3 + x)      F -> CIN
-// each intermediate rounded to bf16 as the unfused composites store it; m1
-// and m2 never leave LDS.  x and y NHWC [N][H][W][CIN]; weights packed as
-// for the implicit-GEMM kernel ([rows][ld], kk = (r*3 + s)*F + c for w2);
-// biases fp32 zero-padded to >= 256 entries (b3: >= CIN).  Activations:
-// none, ReLU, ReLU6 or leaky ReLU.  A variant fixes (F, CIN) and the output
-// tile of one workgroup; every variant of an (F, CIN) pair sums in the same
-// order, so they agree bit for bit.
+//   r  = x (COUT == CIN), or the projection bf16(conv1x1(x; wp) + bp) (COUT != CIN)
+//   y  = act3(conv1x1(m2; w3) + b3 + r)      F -> COUT
+// each intermediate rounded to bf16 as the unfused composites store it; m1,
+// m2 and the projection never leave the workgroup.  x NHWC [N][H][W][CIN],
+// y [N][H][W][COUT]; weights packed as for the implicit-GEMM kernel
+// ([rows][ld], kk = (r*3 + s)*F + c for w2); biases fp32 zero-padded to
+// >= 256 entries (b3, bp: >= COUT).  Activations: none, ReLU, ReLU6 or
+// leaky ReLU.  A kind (F, CIN, COUT) has variants (output tile, rings);
+// all variants of a kind sum in the same order, so they agree bit for bit.
 struct BottleneckParams {
   const bf16_t* x;
   bf16_t* y;
   const bf16_t* w1;
   const bf16_t* w2;
   const bf16_t* w3;
+  const bf16_t* wp;  // projection weights (COUT != CIN), else unused
   const float* b1;
   const float* b2;
   const float* b3;
+  const float* bp;
   int N, H, W;
-  int ld1, ld2, ld3;  // packed weight row strides (elements)
-  int x_bytes, y_bytes, w1_bytes, w2_bytes, w3_bytes, b1_bytes, b2_bytes, b3_bytes;
+  int ld1, ld2, ld3, ldp;  // packed weight row strides (elements)
+  int x_bytes, y_bytes, w1_bytes, w2_bytes, w3_bytes, wp_bytes, b1_bytes, b2_bytes, b3_bytes, bp_bytes;
   int act1, act2, act3;
   float alpha1, alpha2, alpha3;
   // set by the launcher: output tiles per row band, per image and in all,
@@ -135,13 +138,12 @@ struct BottleneckParams {
   int tiles_w, tiles_hw, tiles, per_xcd;
   uint64_t mg_tw, mg_thw;
 };
-// Variant v of the block (0 .. bottleneck_variants(F, CIN) - 1); false if
-// (F, CIN) has no compiled kernel.
-int bottleneck_variants(int F, int CIN);
-const char* bottleneck_variant_name(int F, int CIN, int v);
-// Workgroups (output tiles) of variant v on an N x H x W block.
-int bottleneck_tiles(int F, int CIN, int v, int N, int H, int W);
-hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int v, hipStream_t s);
+// Variants of a kind (0: no compiled kernel), their names, and the
+// workgroups (output tiles) of variant v on an N x H x W block.
+int bottleneck_variants(int F, int CIN, int COUT);
+const char* bottleneck_variant_name(int F, int CIN, int COUT, int v);
+int bottleneck_tiles(int F, int CIN, int COUT, int v, int N, int H, int W);
+hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int v, hipStream_t s);
 // Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
 // one workgroup per 16 output channels, the reduction split over its waves.
 bool dense_rows_supported(const ConvParams& p);

@@ -1,8 +1,10 @@
 """Fused bottleneck blocks: 1x1 reduce -> 3x3 -> 1x1 expand + the block
-input, planned as one launch whose intermediates never leave LDS.
+input (or + a 1x1 projection of it), planned as one launch whose
+intermediates never leave LDS.
 
 Checked on ResNet-50 stage shapes and on ragged ones (image sizes that are
-not multiples of the kernel's output tile), two blocks chained:
+not multiples of the kernel's output tile), two blocks chained (a projection
+block is followed by an identity one):
 
 * the fused run equals, bit for bit, the three unfused launches on the
   single-reduction-group implicit-GEMM kernel without split-K (the same
@@ -34,22 +36,27 @@ FUSED = {"BYOC_FUSE_BLOCK": "1"}
 UNFUSED_KG1 = {"BYOC_FUSE_BLOCK": "0", "BYOC_CONV_TILE": "d64x64s2t256k1", "BYOC_CONV_SPLIT": "1"}
 
 CASES = [
-    # name, batch, block channels, mid channels, height, width
-    ("s1_56x56", 2, 256, 64, 56, 56),
-    ("s1_ragged_30x19", 1, 256, 64, 30, 19),
-    ("s2_28x28", 2, 512, 128, 28, 28),
-    ("s2_ragged_13x9", 3, 512, 128, 13, 9),
+    # name, batch, input channels, mid channels, output channels, height, width
+    ("s1_56x56", 2, 256, 64, 256, 56, 56),
+    ("s1_ragged_30x19", 1, 256, 64, 256, 30, 19),
+    ("s2_28x28", 2, 512, 128, 512, 28, 28),
+    ("s2_ragged_13x9", 3, 512, 128, 512, 13, 9),
+    ("proj_56x56", 2, 64, 64, 256, 56, 56),
+    ("proj_ragged_30x19", 1, 64, 64, 256, 30, 19),
 ]
 
 
 def _blocks(case, n_blocks=2):
-    name, n, cin, mid, h, w = case
+    name, n, cin, mid, cout, h, w = case
     g = GraphBuilder("block_" + name, 3100 + (CASES.index(case) if case in CASES else 9))
     y = g.input("x", [n, cin, h, w], "uniform")
     for i in range(n_blocks):
+        r = y
+        if g.shapes[y][1] != cout:  # the projection shortcut
+            r = g.conv(y, cout, 1, pad=0, act=None, name="b%d.p" % i)
         a = g.conv(y, mid, 1, pad=0, act="relu", name="b%d.a" % i)
         b = g.conv(a, mid, 3, pad=1, act="relu", name="b%d.b" % i)
-        y = g.conv(b, cin, 1, pad=0, act="relu", residual=y, name="b%d.c" % i)
+        y = g.conv(b, cout, 1, pad=0, act="relu", residual=r, name="b%d.c" % i)
     g.output(y)
     return g.finish()
 
@@ -94,7 +101,7 @@ def test_fused_block_matches_unfused_and_oracle(case, monkeypatch):
     assert err <= BF16_TOL
 
 
-@pytest.mark.parametrize("case", [CASES[0], CASES[2]], ids=[CASES[0][0], CASES[2][0]])
+@pytest.mark.parametrize("case", [CASES[0], CASES[2], CASES[4]], ids=[CASES[0][0], CASES[2][0], CASES[4][0]])
 def test_every_block_variant_and_autotune_bitwise(case, monkeypatch):
     announce("block variants " + case[0])
     wl = _blocks(case)
@@ -114,7 +121,7 @@ def test_block_fusion_rule(monkeypatch):
     pair without a fused kernel, and by default for a block whose finest
     tiling gives fewer than 256 workgroups; one launch by default from 256."""
     announce("block fusion rule")
-    wl = _blocks(("odd", 1, 192, 48, 14, 14), n_blocks=1)
+    wl = _blocks(("odd", 1, 192, 48, 192, 14, 14), n_blocks=1)
     _, names = _run(wl, monkeypatch, FUSED)
     assert not any(n.startswith("bottleneck_") for n in names), names
     wl = _blocks(CASES[0], n_blocks=1)
@@ -122,6 +129,6 @@ def test_block_fusion_rule(monkeypatch):
     assert not any(n.startswith("bottleneck_") for n in names), names
     _, names = _run(wl, monkeypatch, {})  # batch 2 at 56x56: 56 tiles of 8x14
     assert not any(n.startswith("bottleneck_") for n in names), names
-    wl = _blocks(("s1_bs10", 10, 256, 64, 56, 56), n_blocks=1)  # 280 tiles of 8x14
+    wl = _blocks(("s1_bs10", 10, 256, 64, 256, 56, 56), n_blocks=1)  # 280 tiles of 8x14
     _, names = _run(wl, monkeypatch, {})
     assert sum(n.startswith("bottleneck_") for n in names) == 1, names
