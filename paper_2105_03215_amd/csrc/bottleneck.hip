@@ -1,30 +1,39 @@
 // Fused ResNet bottleneck block: 1x1 reduce, 3x3, 1x1 expand with the
-// block input added back, as one kernel.
+// block input (or a 1x1 projection of it) added back, as one kernel.
 //
-// The three composites of a bottleneck block are planned as separate
-// launches elsewhere; here they run in one workgroup per tile of output
-// pixels, and the two narrow intermediates live only in LDS (the engine owns
-// an offloaded subgraph's intermediates, Sec. 3.4, so they need not exist
-// in memory).  Of the HBM traffic of the three launches - x read twice, the
-// intermediates written and read back, y written - only one read of x (plus
-// the halo) and the write of y remain.
+// The composites of a bottleneck block are planned as separate launches
+// elsewhere; here they run in one workgroup per tile of output pixels, and
+// the narrow intermediates and the projection live only in LDS and
+// registers (the engine owns an offloaded subgraph's intermediates, Sec.
+// 3.4, so they need not exist in memory).  Of the HBM traffic of the
+// separate launches - x read two or three times, the intermediates written
+// and read back, y written - one read of x (plus the halo) and the write of
+// y remain.
 //
-// A workgroup owns a TH x TW tile of output pixels of one image.
+// A workgroup owns a TH x TW tile of output pixels of one image.  The first
+// 1x1 and the projection may have stride S (2: a downsampling block); the
+// rest runs on the output grid.
 //
-// Phase A (1x1 reduce): the tile's halo - (TH + 2) x (TW + 2) pixels - times
-// W1, streamed one 64-channel slice of x at a time through a ring of LDS
-// stages (x slice and W1 slice per stage, HBM -> LDS loads).  The sums are
-// finished (bias, activation, bf16 rounding) into M1 in LDS; halo pixels
-// outside the image are stored as zeros, the 3x3's zero padding.  While each
-// x slice is staged, the threads also copy the tile's own pixels of it into
-// registers: the residual of phase C, read from HBM only once.
+// Phase A (1x1 reduce): the tile's halo - (TH + 2) x (TW + 2) positions of
+// the output grid, i.e. input pixels S apart - times W1, streamed one
+// 64-channel slice of x at a time through a ring of LDS stages (x slice and
+// W1 slice per stage, HBM -> LDS loads).  The sums are finished (bias,
+// activation, bf16 rounding) into M1 in LDS; positions outside the image
+// are stored as zeros, the 3x3's zero padding.  While each x slice is
+// staged, the threads copy the tile's own pixels of it into registers: the
+// residual of phase C (identity shortcut), or the MFMA operand fragments of
+// the projection (projection shortcut).
 //
 // Phase B (3x3): nine shifted views of M1 times W2, streamed through a ring
 // of stages of TPS taps x SPB 64-channel slices (tap by tap, then slice);
 // the output tile is finished into M2 in LDS.
 //
-// Phase C (1x1 expand): M2 times W3, F output channels per chunk; bias, the
-// residual from registers, activation, bf16 stores to y.
+// Phase C (1x1 expand): M2 times W3, F output channels per chunk, the
+// weights streamed one 64-channel slice (of M2, then of x for the
+// projection) per stage; with the projection shortcut the chunk's
+// projection is summed from the registers of phase A and finished (bias,
+// bf16 rounding) as the projection composite stores it; then bias, the
+// residual, activation, bf16 stores to y.
 //
 // Operands of every product: weights are the MFMA A operand (16 output
 // channels), pixels the B operand, so each lane ends with 4 consecutive
@@ -33,9 +42,9 @@
 // 128 bytes (64 channels) with its 16-byte chunks permuted by a per-row key
 // so that the 16 rows one MFMA operand read touches spread over the banks.
 //
-// Reduction order of each output: phase A slice by slice of x (32 channels
-// per MFMA step), phase B tap by tap then channel, phase C channel - the
-// order of the single-group implicit-GEMM kernel on the same composites.
+// Reduction order of each output: phase A and the projection slice by slice of x (32
+// channels per MFMA step), phase B tap by tap then channel, phase C channel -
+// the order of the single-group implicit-GEMM kernel on the same composites.
 #include <cstdio>
 
 #include "lds_dma.h"
@@ -47,69 +56,84 @@ using namespace dma;
 
 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 
-template <int F_, int CIN_, int COUT_, int TH_, int TW_, int NW_, int NSA_, int TPS_, int SPB_, int NSB_>
+constexpr int cmin(int a, int b) { return a < b ? a : b; }
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+template <int F_, int CIN_, int COUT_, int S_, int TH_, int TW_, int NW_, int NSA_, int TPS_, int SPB_, int NSB_>
 struct Bn {
-  static constexpr int F = F_, CIN = CIN_, COUT = COUT_, TH = TH_, TW = TW_, NW = NW_, NSA = NSA_, TPS = TPS_;
-  static constexpr int SPB = SPB_;
-  // COUT != CIN: the residual is a 1x1 projection of x (CIN = 64: the x tile stays in LDS)
-  static constexpr bool PROJ = COUT_ != CIN_;
-  static constexpr int NSB = NSB_;  // phase B ring
+  static constexpr int F = F_, CIN = CIN_, COUT = COUT_, S = S_, TH = TH_, TW = TW_, NW = NW_;
+  static constexpr int NSA = NSA_, TPS = TPS_, SPB = SPB_, NSB = NSB_;  // rings and stages
+  static constexpr bool PROJ = COUT != CIN || S != 1;  // projection shortcut
   static constexpr int NT = 64 * NW;
   static constexpr int WGC = F / 64;   // 64-channel groups of the mid width (a wave owns one)
   static constexpr int WP = NW / WGC;  // waves per group
   static constexpr int HC = TW + 2, HR = TH + 2;
-  static constexpr int HPX = HR * HC;               // halo pixels
+  static constexpr int HPX = HR * HC;  // halo positions
   static constexpr int HPXP = (HPX + 15) / 16 * 16;
-  static constexpr int OPX = TH * TW;               // output pixels
+  static constexpr int OPX = TH * TW;  // output pixels
   static constexpr int OPXP = (OPX + 15) / 16 * 16;
   static constexpr int NTA = HPXP / 16, NTB = OPXP / 16;  // 16-pixel tiles
   static constexpr int TA = (NTA + WP - 1) / WP;          // pixel tiles per wave, phase A
   static constexpr int TB = (NTB + WP - 1) / WP;          // phases B and C
-  static constexpr int SA = CIN / 64;  // phase A stages (x slices)
-  static constexpr int GB = WGC / SPB;     // slice groups of a tap (phase B stage: TPS taps x SPB slices)
-  static constexpr int SB = 9 / TPS * GB;  // phase B stages
-  static constexpr int NQ = COUT / F;      // phase C chunks (F output channels each)
+  static constexpr int SA = CIN / 64;                     // phase A stages (x slices)
+  static constexpr int PFA = NSA >= 2 ? NSA - 1 : 1;      // phase A stages issued ahead
+  static constexpr int NQ = COUT / F;                     // phase C chunks (F output channels each)
+  static constexpr int UQ = WGC + (PROJ ? SA : 0);        // phase C stages per chunk: W3 slices, then Wp slices
+  static constexpr int SC = NQ * UQ;                      // phase C stages
+  static constexpr int GB = WGC / SPB;                    // slice groups of a tap
+  static constexpr int SB = 9 / TPS * GB;                 // phase B stages
+  static constexpr int XF = PROJ ? 2 * SA : 1;            // projection fragments per pixel tile
   static constexpr int ROW = 128;
   // LDS plan (bytes)
   static constexpr int M1B = WGC * HPXP * ROW;
   static constexpr int XB = HPXP * ROW;
   static constexpr int W1B = F * ROW;
-  static constexpr int ASTG = PROJ ? W1B : XB + W1B;  // phase A stage (the x slice of PROJ has its own region)
+  static constexpr int ASTG = XB + W1B;
   static constexpr int W2B = TPS * SPB * F * ROW;
   static constexpr int M2B = WGC * OPXP * ROW;
-  static constexpr int W3B = F * WGC * ROW;
-  static constexpr int WPB = PROJ ? F * ROW : 0;  // projection weights of a chunk (F rows x 64 channels)
-  static constexpr int CST = W3B + WPB;            // phase C stage
-  static constexpr int OFF_R2 = M1B;  // phase A ring, then the W2 ring and M2
+  static constexpr int CB = F * ROW;  // phase C stage: F rows of a chunk x 64 input channels
+  static constexpr int OFF_R2 = M1B;  // the phase A ring, then the W2 ring and M2
   static constexpr int OFF_M2 = OFF_R2 + NSB * W2B;
   static constexpr int END_A = OFF_R2 + NSA * ASTG;
   static constexpr int END_B = OFF_M2 + M2B;
-  static constexpr int NSC = (OFF_M2 / CST) < NQ ? (OFF_M2 / CST) : NQ;  // W3 ring over M1 and the W2 ring
-  static constexpr int OFF_BIAS = END_A > END_B ? END_A : END_B;
+  static constexpr int NSC = cmin(OFF_M2 / CB, SC);  // phase C ring, over M1 and the W2 ring
+  static constexpr int OFF_BIAS = cmax(END_A, END_B);
   static constexpr int B3BLK = (COUT * 4 + 1023) / 1024;
   static constexpr int BBLK = 2 + (PROJ ? 2 : 1) * B3BLK;  // 1 KB blocks: b1, b2, b3 (, bp)
   static constexpr int OFF_JUNK = OFF_BIAS + BBLK * 1024;
-  static constexpr int OFF_X = OFF_JUNK + 1024;  // PROJ: the x tile
-  static constexpr int LDS = OFF_X + (PROJ ? XB : 0);
+  static constexpr int LDS = OFF_JUNK + 1024;
   // 1 KB fills (8 rows of 128 bytes) per stage and per thread
-  static constexpr int XBLK = HPXP / 8, W1BLK = F / 8, W2BLK = TPS * SPB * F / 8, W3BLK = WGC * F / 8;
+  static constexpr int XBLK = HPXP / 8, W1BLK = F / 8, W2BLK = TPS * SPB * F / 8, CBLK = F / 8;
   static constexpr int LXA = (XBLK + NW - 1) / NW, LW1 = (W1BLK + NW - 1) / NW;
   static constexpr int LA = LXA + LW1;
   static constexpr int LB = (W2BLK + NW - 1) / NW;
-  static constexpr int WPBLK = PROJ ? F / 8 : 0;
-  static constexpr int LC3 = (W3BLK + NW - 1) / NW, LCP = (WPBLK + NW - 1) / NW;
-  static constexpr int LC = LC3 + LCP;
+  static constexpr int LC = (CBLK + NW - 1) / NW;
   static constexpr int ST = TB * 4;  // y stores per chunk per thread
+  // Vector memory operations a thread may have outstanding after phase C
+  // stage k's loads: the loads of the stages issued ahead of it, and the
+  // y stores of the chunks finished since it was issued (stage i issues
+  // stage i + NSC - 1 after its wait, then computes, then - at a chunk's
+  // last stage - stores).
+  static constexpr int c_younger(int k) {
+    int stores = 0;
+    for (int i = cmax(0, k - NSC + 1); i < k; ++i) stores += (i % UQ == UQ - 1) ? ST : 0;
+    return cmin(NSC - 2, SC - 1 - k) * LC + stores;
+  }
+  static constexpr int c_younger_max() {
+    int m = 0;
+    for (int k = 0; k < SC; ++k) m = cmax(m, c_younger(k));
+    return m;
+  }
 
-  static_assert(F % 64 == 0 && COUT % F == 0 && NW % WGC == 0, "shape");
-  static_assert(PROJ ? (CIN == 64 && F == 64) : CIN % F == 0, "shape");
-  static_assert(9 % TPS == 0 && NSA >= 2 && (NSA <= SA || SA == 1) && NSB >= 2 && NSB <= SB, "stages");
+  static_assert(F % 64 == 0 && CIN % 64 == 0 && COUT % F == 0 && NW % WGC == 0, "shape");
+  static_assert(PROJ || CIN % F == 0, "identity shortcut: chunks of F channels");
+  static_assert(9 % TPS == 0 && ((NSA >= 2 && NSA <= SA) || (NSA == 1 && SA == 1)), "phase A stages");
+  static_assert(NSB >= 2 && NSB <= SB, "phase B stages");
   static_assert(WGC % SPB == 0 && (TPS == 1 || SPB == WGC), "phase B stages run tap by tap, then slice");
-  static_assert(NSC >= 2, "W3 ring");
+  static_assert(NSC >= 2, "phase C ring");
   static_assert(BBLK <= NW, "one bias fill per wave");
   static_assert(LDS <= kLdsLimit, "LDS");
-  static_assert((NSA - 2) * LA <= 63 && (NSB - 2) * LB <= 63, "vmcnt immediate");
-  static_assert((NSC - 2) * LC + (NSC - 1) * ST <= 63, "vmcnt immediate");
+  static_assert((PFA - 1) * LA <= 63 && (NSB - 2) * LB <= 63 && c_younger_max() <= 63, "vmcnt immediate");
 };
 
 // rows r of a 128-byte-row buffer keep logical 16-byte chunk c at slot c ^ key
@@ -117,13 +141,21 @@ __device__ __forceinline__ uint32_t slot_off(int row, int chunk, int key) {
   return (uint32_t)(row * 128 + ((chunk ^ (key & 7)) << 4));
 }
 
+// A ring stage is complete for this thread and - after the barrier - for
+// the whole workgroup, once at most `YOUNGER` of the thread's later vector
+// memory operations are outstanding.
+template <int YOUNGER>
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(YOUNGER) : "memory");
+}
+
 template <class B>
 __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   constexpr int F = B::F, CIN = B::CIN, TW = B::TW, HC = B::HC, NW = B::NW, WP = B::WP;
   __shared__ __attribute__((aligned(1024))) char lds[B::LDS];
   asm volatile("" ::"s"(p.x), "s"(p.y), "s"(p.w1), "s"(p.w2), "s"(p.w3), "s"(p.b1), "s"(p.b2), "s"(p.b3));
-  asm volatile("" ::"s"(p.N), "s"(p.H), "s"(p.W), "s"(p.ld1), "s"(p.ld2), "s"(p.ld3), "s"(p.x_bytes),
-               "s"(p.y_bytes), "s"(p.w1_bytes), "s"(p.w2_bytes), "s"(p.w3_bytes));
+  asm volatile("" ::"s"(p.N), "s"(p.H), "s"(p.W), "s"(p.P), "s"(p.Q), "s"(p.ld1), "s"(p.ld2), "s"(p.ld3),
+               "s"(p.x_bytes), "s"(p.y_bytes), "s"(p.w1_bytes), "s"(p.w2_bytes), "s"(p.w3_bytes));
   if constexpr (B::PROJ) asm volatile("" ::"s"(p.wp), "s"(p.bp), "s"(p.ldp), "s"(p.wp_bytes), "s"(p.bp_bytes));
   asm volatile("" ::"s"(p.b1_bytes), "s"(p.b2_bytes), "s"(p.b3_bytes), "s"(p.act1), "s"(p.act2), "s"(p.act3),
                "s"(p.alpha1), "s"(p.alpha2), "s"(p.alpha3), "s"(p.tiles_w), "s"(p.tiles_hw), "s"(p.mg_tw),
@@ -143,15 +175,15 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   const int n = mdiv(tile, p.mg_thw);
   const int tr = tile - n * p.tiles_hw;
   const int th = mdiv(tr, p.mg_tw);
-  const int h0 = th * B::TH, w0 = (tr - th * p.tiles_w) * TW;
-  const int H = p.H, W = p.W;
+  const int h0 = th * B::TH, w0 = (tr - th * p.tiles_w) * TW;  // on the output grid
+  const int H = p.H, W = p.W, P = p.P, Q = p.Q;
 
   const uint32_t base = lds_addr(lds);
   const uint32_t junk = base + B::OFF_JUNK;
   const float* sb1 = reinterpret_cast<const float*>(lds + B::OFF_BIAS);
   const float* sb2 = sb1 + 256;
   const float* sb3 = sb1 + 512;
-  const float* sbp = sb3 + 256 * B::B3BLK;  // PROJ: projection bias
+  const float* sbp = sb3 + 256 * B::B3BLK;  // projection bias
 
   // ---- load plans: per-thread source offsets, wave-uniform destinations ----
   const i32x4 xr = buffer_rsrc(p.x, p.x_bytes);
@@ -159,7 +191,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   const i32x4 w2r = buffer_rsrc(p.w2, p.w2_bytes);
   const i32x4 w3r = buffer_rsrc(p.w3, p.w3_bytes);
   const i32x4 wpr = buffer_rsrc(p.wp, B::PROJ ? p.wp_bytes : 0);
-  uint32_t xoff[B::LXA], w1off[B::LW1], w2off[B::LB], w3off[B::LC3], wpoff[B::LCP > 0 ? B::LCP : 1];
+  uint32_t xoff[B::LXA], w1off[B::LW1], w2off[B::LB], w3off[B::LC], wpoff[B::LC];
 #pragma unroll
   for (int u = 0; u < B::LXA; ++u) {
     const int blk = wave + NW * u;
@@ -167,46 +199,30 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     uint32_t off = kOOB;
     if (blk < B::XBLK && px < B::HPX) {
       const int hr = px / HC, hc = px - (px / HC) * HC;
-      const int h = h0 - 1 + hr, w = w0 - 1 + hc;
-      if ((unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
-        off = (uint32_t)((((n * H + h) * W + w) * CIN + ((lk ^ (px & 7)) * 8)) * 2);
+      const int mh = h0 - 1 + hr, mw = w0 - 1 + hc;  // position on the output grid
+      if ((unsigned)mh < (unsigned)P && (unsigned)mw < (unsigned)Q)
+        off = (uint32_t)((((n * H + B::S * mh) * W + B::S * mw) * CIN + ((lk ^ (px & 7)) * 8)) * 2);
     }
     xoff[u] = off;
   }
-#pragma unroll
-  for (int u = 0; u < B::LW1; ++u) {
-    const int blk = wave + NW * u;
+  // rows 8 * blk + lane / 8 of a weight block, chunk lk at slot lk ^ (row & 7)
+  auto row_off = [&](int blk, int nblk, int ld, int col) {
     const int row = 8 * blk + (lane >> 3);
-    w1off[u] = blk < B::W1BLK ? (uint32_t)((row * p.ld1 + ((lk ^ (row & 7)) * 8)) * 2) : kOOB;
-  }
+    return blk < nblk ? (uint32_t)((row * ld + col + ((lk ^ (row & 7)) * 8)) * 2) : kOOB;
+  };
+#pragma unroll
+  for (int u = 0; u < B::LW1; ++u) w1off[u] = row_off(wave + NW * u, B::W1BLK, p.ld1, 0);
 #pragma unroll
   for (int u = 0; u < B::LB; ++u) {
-    const int blk = wave + NW * u;
-    uint32_t off = kOOB;
-    if (blk < B::W2BLK) {
-      const int tap = blk / (B::SPB * F / 8), rem = blk - tap * (B::SPB * F / 8);
-      const int sl = rem / (F / 8);
-      const int row = 8 * (rem - sl * (F / 8)) + (lane >> 3);
-      off = (uint32_t)((row * p.ld2 + tap * F + sl * 64 + ((lk ^ (row & 7)) * 8)) * 2);
-    }
-    w2off[u] = off;
+    const int blk = wave + NW * u;  // [tap u][slice sl][F rows]
+    const int tap = blk / (B::SPB * F / 8), rem = blk - tap * (B::SPB * F / 8);
+    const int sl = rem / (F / 8);
+    w2off[u] = blk < B::W2BLK ? row_off(rem - sl * (F / 8), F / 8, p.ld2, tap * F + sl * 64) : kOOB;
   }
 #pragma unroll
-  for (int u = 0; u < B::LC3; ++u) {
-    const int blk = wave + NW * u;
-    uint32_t off = kOOB;
-    if (blk < B::W3BLK) {
-      const int sl = blk / (F / 8);
-      const int row = 8 * (blk - sl * (F / 8)) + (lane >> 3);
-      off = (uint32_t)((row * p.ld3 + sl * 64 + ((lk ^ (row & 7)) * 8)) * 2);
-    }
-    w3off[u] = off;
-  }
-#pragma unroll
-  for (int u = 0; u < B::LCP; ++u) {
-    const int blk = wave + NW * u;
-    const int row = 8 * blk + (lane >> 3);
-    wpoff[u] = blk < B::WPBLK ? (uint32_t)((row * p.ldp + ((lk ^ (row & 7)) * 8)) * 2) : kOOB;
+  for (int u = 0; u < B::LC; ++u) {  // F rows of a chunk, 64 channels of W3 (of Wp)
+    w3off[u] = row_off(wave + NW * u, B::CBLK, p.ld3, 0);
+    wpoff[u] = B::PROJ ? row_off(wave + NW * u, B::CBLK, p.ldp, 0) : kOOB;
   }
   auto dst = [&](uint32_t region, int blk, int nblk) {
     return __builtin_amdgcn_readfirstlane(blk < nblk ? region + blk * 1024 : junk);
@@ -214,12 +230,11 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   auto live = [](uint32_t off, uint32_t add) { return off == kOOB ? kOOB : off + add; };
   auto issue_a = [&](int s) {
     const uint32_t slot = base + B::OFF_R2 + (s % B::NSA) * B::ASTG;
-    const uint32_t xdst = B::PROJ ? base + B::OFF_X : slot, wdst = B::PROJ ? slot : slot + B::XB;
 #pragma unroll
-    for (int u = 0; u < B::LXA; ++u) lds_fill16(xr, dst(xdst, wave + NW * u, B::XBLK), live(xoff[u], s * 128));
+    for (int u = 0; u < B::LXA; ++u) lds_fill16(xr, dst(slot, wave + NW * u, B::XBLK), live(xoff[u], s * 128));
 #pragma unroll
     for (int u = 0; u < B::LW1; ++u)
-      lds_fill16(w1r, dst(wdst, wave + NW * u, B::W1BLK), live(w1off[u], s * 128));
+      lds_fill16(w1r, dst(slot + B::XB, wave + NW * u, B::W1BLK), live(w1off[u], s * 128));
   };
   auto issue_b = [&](int s) {
     const uint32_t slot = base + B::OFF_R2 + (s % B::NSB) * B::W2B;
@@ -228,20 +243,28 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
       lds_fill16(w2r, dst(slot, wave + NW * u, B::W2BLK),
                  live(w2off[u], ((s / B::GB) * B::TPS * F + (s % B::GB) * B::SPB * 64) * 2));
   };
-  auto issue_c = [&](int q) {
-    const uint32_t slot = base + (q % B::NSC) * B::CST;
+  auto issue_c = [&](int k) {  // chunk k / UQ: slice j = k % UQ of W3 (j < WGC), else of Wp
+    const uint32_t slot = base + (k % B::NSC) * B::CB;
+    const int q = k / B::UQ, j = k % B::UQ;
+    if (j < B::WGC) {
 #pragma unroll
-    for (int u = 0; u < B::LC3; ++u)
-      lds_fill16(w3r, dst(slot, wave + NW * u, B::W3BLK), live(w3off[u], q * F * p.ld3 * 2));
+      for (int u = 0; u < B::LC; ++u)
+        lds_fill16(w3r, dst(slot, wave + NW * u, B::CBLK), live(w3off[u], (q * F * p.ld3 + j * 64) * 2));
+    } else {
 #pragma unroll
-    for (int u = 0; u < B::LCP; ++u)
-      lds_fill16(wpr, dst(slot + B::W3B, wave + NW * u, B::WPBLK), live(wpoff[u], q * F * p.ldp * 2));
+      for (int u = 0; u < B::LC; ++u)
+        lds_fill16(wpr, dst(slot, wave + NW * u, B::CBLK),
+                   live(wpoff[u], (q * F * p.ldp + (j - B::WGC) * 64) * 2));
+    }
   };
 
   // biases: wave w < BBLK fills one 1 KB block (b1, b2, the blocks of b3, then those of bp)
   {
     const bool pb = wave >= 2 + B::B3BLK;
-    const void* src = wave == 0 ? (const void*)p.b1 : wave == 1 ? (const void*)p.b2 : pb ? (const void*)p.bp : (const void*)p.b3;
+    const void* src = wave == 0 ? (const void*)p.b1
+                      : wave == 1 ? (const void*)p.b2
+                      : pb        ? (const void*)p.bp
+                                  : (const void*)p.b3;
     const int bytes = wave == 0 ? p.b1_bytes : wave == 1 ? p.b2_bytes : pb ? p.bp_bytes : p.b3_bytes;
     const int blk = wave < 2 ? 0 : pb ? wave - 2 - B::B3BLK : wave - 2;
     const uint32_t off = wave < B::BBLK ? (uint32_t)(blk * 1024 + lane * 16) : kOOB;
@@ -252,31 +275,47 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   const ActClamp ac2 = act_clamp_of(p.act2, p.alpha2);
   const ActClamp ac3 = act_clamp_of(p.act3, p.alpha3);
 
+  // this lane's output pixel in each of the wave's pixel tiles (phases B and
+  // C): its halo row (0 past the tile)
+  int hrow[B::TB];
+#pragma unroll
+  for (int t = 0; t < B::TB; ++t) {
+    const int o = 16 * (wp + WP * t) + l16;
+    hrow[t] = o < B::OPX ? (o / TW + 1) * HC + (o % TW) + 1 : 0;
+  }
+
   // ---- phase A: M1 = act1(halo x W1 + b1) -----------------------------------
   f32x4 accA[B::TA][4];
 #pragma unroll
   for (int t = 0; t < B::TA; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) accA[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  uint2 resv[B::PROJ ? 1 : B::NQ][B::TB][4];  // residual: x at the tile's own pixels, per chunk of phase C
+  // identity shortcut: the residual of phase C per chunk, 4 bf16 channels of
+  // one pixel per (chunk, pixel tile, channel tile)
+  uint2 resv[B::PROJ ? 1 : B::NQ][B::TB][4];
+  uint4 xf[B::TB][B::XF];  // projection: x at the tile's pixels as MFMA B fragments, per 32-channel step
 
-  static_for<0, B::NSA - 1>([&](auto s) { issue_a(decltype(s)::value); });
+  static_for<0, B::PFA>([&](auto s) {
+    if constexpr (decltype(s)::value < B::SA) issue_a(decltype(s)::value);
+  });
   static_for<0, B::SA>([&](auto ss) {
     constexpr int s = decltype(ss)::value;
-    constexpr int younger = (B::NSA - 2 < B::SA - 1 - s) ? B::NSA - 2 : B::SA - 1 - s;
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(younger * B::LA) : "memory");
-    if constexpr (s + B::NSA - 1 < B::SA) issue_a(s + B::NSA - 1);
-    const char* xs = B::PROJ ? lds + B::OFF_X : lds + B::OFF_R2 + (s % B::NSA) * B::ASTG;
-    const char* ws = B::PROJ ? lds + B::OFF_R2 + (s % B::NSA) * B::ASTG : xs + B::XB;
-    if (!B::PROJ && cg == s % B::WGC) {  // this slice is the residual of the wave's channel group in chunk s / WGC
+    stage_barrier<cmin(B::PFA - 1, B::SA - 1 - s) * B::LA>();
+    if constexpr (B::NSA >= 2 && s + B::PFA < B::SA) issue_a(s + B::PFA);
+    const char* xs = lds + B::OFF_R2 + (s % B::NSA) * B::ASTG;
+    const char* ws = xs + B::XB;
+    if constexpr (B::PROJ) {
 #pragma unroll
-      for (int t = 0; t < B::TB; ++t) {
-        const int o = 16 * (wp + WP * t) + l16;
-        const int hp = o < B::OPX ? (o / TW + 1) * HC + (o % TW) + 1 : 0;
+      for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) xf[t][2 * s + ks] = *(const uint4*)(xs + slot_off(hrow[t], ks * 4 + lq, hrow[t]));
+    } else if (cg == s % B::WGC) {  // this slice is the residual of the wave's channel group in chunk s / WGC
+#pragma unroll
+      for (int t = 0; t < B::TB; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          resv[B::PROJ ? 0 : s / B::WGC][t][i] = *(const uint2*)(xs + slot_off(hp, 2 * i + (lane >> 5), hp) + (lq & 1) * 8);
-      }
+          resv[B::PROJ ? 0 : s / B::WGC][t][i] =
+              *(const uint2*)(xs + slot_off(hrow[t], 2 * i + (lane >> 5), hrow[t]) + (lq & 1) * 8);
     }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -295,7 +334,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
       }
     }
   });
-  // every wave is done with the phase A ring: the W2 ring may overwrite it
+  // every wave is done with the phase A ring: the next ring may overwrite it
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   static_for<0, B::NSB - 1>([&](auto s) { issue_b(decltype(s)::value); });
   // biases into registers before the first M1 store (a later LDS read could
@@ -309,8 +348,8 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     if (j >= B::NTA) continue;
     const int px = 16 * j + l16;
     const int hr = px / HC, hc = px - (px / HC) * HC;
-    const int h = h0 - 1 + hr, w = w0 - 1 + hc;
-    const bool inside = px < B::HPX && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+    const int mh = h0 - 1 + hr, mw = w0 - 1 + hc;
+    const bool inside = px < B::HPX && (unsigned)mh < (unsigned)P && (unsigned)mw < (unsigned)Q;
     const int key = hr * TW + hc;
     char* m1 = lds + cg * B::HPXP * 128;
 #pragma unroll
@@ -327,6 +366,9 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   }
 
   // ---- phase B: M2 = act2(conv3x3(M1) W2 + b2) -------------------------------
+  // Phases B and C run every one of a wave's TB pixel tiles (a tile past the
+  // last reads row 0 and is never stored): no branches between the LDS reads
+  // of a step and its MFMAs.
   int pbase[B::TB], obase[B::TB];
 #pragma unroll
   for (int t = 0; t < B::TB; ++t) {
@@ -335,9 +377,6 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     pbase[t] = ok ? (o / TW) * HC + (o % TW) : 0;
     obase[t] = ok ? o : 0;
   }
-  // phases B and C run every one of a wave's TB pixel tiles (a tile past the
-  // last reads pixel 0 and is never stored): no branches between the LDS
-  // reads of a step and its MFMAs
   f32x4 accB[B::TB][4];
 #pragma unroll
   for (int t = 0; t < B::TB; ++t)
@@ -345,8 +384,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     for (int i = 0; i < 4; ++i) accB[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   static_for<0, B::SB>([&](auto ss) {
     constexpr int s = decltype(ss)::value;
-    constexpr int younger = (B::NSB - 2 < B::SB - 1 - s) ? B::NSB - 2 : B::SB - 1 - s;
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(younger * B::LB) : "memory");
+    stage_barrier<cmin(B::NSB - 2, B::SB - 1 - s) * B::LB>();
     if constexpr (s + B::NSB - 1 < B::SB) issue_b(s + B::NSB - 1);
     const char* wst = lds + B::OFF_R2 + (s % B::NSB) * B::W2B;
     static_for<0, B::TPS>([&](auto uu) {
@@ -381,7 +419,7 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
   });
   // every wave is done with M1 and the W2 ring: the W3 ring may overwrite them
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  static_for<0, B::NSC - 1>([&](auto q) { issue_c(decltype(q)::value); });
+  static_for<0, B::NSC - 1>([&](auto k) { issue_c(decltype(k)::value); });
 #pragma unroll
   for (int i = 0; i < 4; ++i) bias[i] = *(const float4*)(sb2 + cg * 64 + 16 * i + 4 * lq);
 #pragma unroll
@@ -401,112 +439,89 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     }
   }
 
-  // ---- phase C: y = act3(M2 W3 + b3 + x) ------------------------------------
-  // output offsets of this thread's pixels (kOOB: not stored)
+  // ---- phase C: y = act3(M2 W3 + b3 + residual) -----------------------------
+  // output offsets of this thread's pixels (kOOB: not stored) and their M2 rows
   uint32_t yoff[B::TB];
+  int crow[B::TB];
 #pragma unroll
   for (int t = 0; t < B::TB; ++t) {
     const int o = 16 * (wp + WP * t) + l16;
     const int oh = h0 + o / TW, ow = w0 + o % TW;
-    const bool ok = wp + WP * t < B::NTB && o < B::OPX && oh < H && ow < W;
-    yoff[t] = ok ? (uint32_t)((((n * H + oh) * W + ow) * B::COUT + cg * 64 + 4 * lq) * 2) : kOOB;
+    const bool tile_ok = wp + WP * t < B::NTB;
+    const bool ok = tile_ok && o < B::OPX && oh < P && ow < Q;
+    yoff[t] = ok ? (uint32_t)((((n * P + oh) * Q + ow) * B::COUT + cg * 64 + 4 * lq) * 2) : kOOB;
+    crow[t] = tile_ok ? o : l16;
   }
   const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(p.y, (short)0, p.y_bytes, kBufferFlags);
-  int crow[B::TB];  // M2 row of this lane's pixel in each pixel tile (tile 0 for one past the last)
-#pragma unroll
-  for (int t = 0; t < B::TB; ++t) crow[t] = (wp + WP * t < B::NTB ? 16 * (wp + WP * t) : 0) + l16;
-  int xrow[B::TB];  // PROJ: halo row of this lane's pixel in the x tile
-#pragma unroll
-  for (int t = 0; t < B::TB; ++t) {
-    const int o = crow[t];
-    xrow[t] = o < B::OPX ? (o / TW + 1) * HC + (o % TW) + 1 : 0;
-  }
-  float4 biasp[4];
-  static_for<0, B::NQ>([&](auto qq) {
-    constexpr int q = decltype(qq)::value;
-    // W3 loads younger than chunk q's, and y stores issued after them
-    constexpr int yl = (B::NSC - 2 < B::NQ - 1 - q) ? B::NSC - 2 : B::NQ - 1 - q;
-    constexpr int ys = q < B::NSC - 1 ? q : B::NSC - 1;
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(yl * B::LC + ys * B::ST) : "memory");
-    if constexpr (q + B::NSC - 1 < B::NQ) issue_c(q + B::NSC - 1);
-    const char* wst = lds + (q % B::NSC) * B::CST;
-    f32x4 acc[B::TB][4], accp[B::TB][4];
-#pragma unroll
-    for (int t = 0; t < B::TB; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) bias[i] = *(const float4*)(sb3 + q * F + cg * 64 + 16 * i + 4 * lq);
-    if constexpr (B::PROJ) {
-      // the projection of x over this chunk's channels (64 input channels)
-      const char* xs = lds + B::OFF_X;
-      const char* wpt = wst + B::W3B;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) biasp[i] = *(const float4*)(sbp + q * F + 16 * i + 4 * lq);
-      bf16x8 a[2][4], b[2][B::TB];
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int c = ks * 4 + lq;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) a[ks][i] = as_bf16x8(*(const uint4*)(wpt + slot_off(16 * i + l16, c, lk)));
-#pragma unroll
-        for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(*(const uint4*)(xs + slot_off(xrow[t], c, xrow[t])));
-      }
+  f32x4 acc[B::TB][4], accp[B::TB][4];
+  static_for<0, B::SC>([&](auto kk) {
+    constexpr int k = decltype(kk)::value;
+    constexpr int q = k / B::UQ, j = k % B::UQ;
+    stage_barrier<B::c_younger(k)>();
+    if constexpr (k + B::NSC - 1 < B::SC) issue_c(k + B::NSC - 1);
+    const char* wt = lds + (k % B::NSC) * B::CB;
+    if constexpr (j == 0) {
 #pragma unroll
       for (int t = 0; t < B::TB; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) accp[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int t = 0; t < B::TB; ++t)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) accp[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], accp[t][i], 0, 0, 0);
+        for (int i = 0; i < 4; ++i) acc[t][i] = accp[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    bf16x8 a[2][4], b[2][B::TB];
 #pragma unroll
-    for (int sl = 0; sl < B::WGC; ++sl) {
-      const char* m2 = lds + B::OFF_M2 + sl * B::OPXP * 128;
-      const char* wt = wst + sl * F * 128;
-      bf16x8 a[2][4], b[2][B::TB];
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = ks * 4 + lq;
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int c = ks * 4 + lq;
+      for (int i = 0; i < 4; ++i) a[ks][i] = as_bf16x8(*(const uint4*)(wt + slot_off(cg * 64 + 16 * i + l16, c, lk)));
+      if constexpr (j < B::WGC) {  // W3: slice j of M2
+        const char* m2 = lds + B::OFF_M2 + j * B::OPXP * 128;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) a[ks][i] = as_bf16x8(*(const uint4*)(wt + slot_off(cg * 64 + 16 * i + l16, c, lk)));
+        for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(*(const uint4*)(m2 + slot_off(crow[t], c, lk)));
+      } else {  // Wp: slice j - WGC of x
 #pragma unroll
-        for (int t = 0; t < B::TB; ++t)
-          b[ks][t] = as_bf16x8(*(const uint4*)(m2 + slot_off(crow[t], c, lk)));
+        for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(xf[t][2 * (j - B::WGC) + ks]);
       }
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int t = 0; t < B::TB; ++t)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], acc[t][i], 0, 0, 0);
     }
-    // every thread issues all ST stores (out-of-range offsets for pixels it
-    // does not own), so the wait counts above are exact
 #pragma unroll
-    for (int t = 0; t < B::TB; ++t) {
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if constexpr (j < B::WGC)
+            acc[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], acc[t][i], 0, 0, 0);
+          else
+            accp[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], accp[t][i], 0, 0, 0);
+        }
+    if constexpr (j == B::UQ - 1) {
+      // the chunk's epilogue; every thread issues all ST stores (out-of-range
+      // offsets for pixels it does not own), so the wait counts are exact
+      float4 bp[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float4 bb = bias[i];
-        uint2 rv;
-        if constexpr (B::PROJ) {  // the projection composite's output: bias, (no activation), bf16
-          const f32x4 u = accp[t][i];
-          const float4 c = biasp[i];
-          rv = make_uint2(pack2_bf16((u[0] + c.x) + 0.f, (u[1] + c.y) + 0.f),
-                          pack2_bf16((u[2] + c.z) + 0.f, (u[3] + c.w) + 0.f));
-        } else {
-          rv = resv[q][t][i];
+        bias[i] = *(const float4*)(sb3 + q * F + cg * 64 + 16 * i + 4 * lq);
+        if constexpr (B::PROJ) bp[i] = *(const float4*)(sbp + q * F + cg * 64 + 16 * i + 4 * lq);
+      }
+#pragma unroll
+      for (int t = 0; t < B::TB; ++t) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 bb = bias[i];
+          uint2 rv;
+          if constexpr (B::PROJ) {  // the projection composite's output: bias, no activation, bf16
+            const f32x4 u = accp[t][i];
+            rv = make_uint2(pack2_bf16((u[0] + bp[i].x) + 0.f, (u[1] + bp[i].y) + 0.f),
+                            pack2_bf16((u[2] + bp[i].z) + 0.f, (u[3] + bp[i].w) + 0.f));
+          } else {
+            rv = resv[q][t][i];
+          }
+          const f32x4 v = acc[t][i];
+          const float r0 = __uint_as_float(rv.x << 16), r1 = __uint_as_float(rv.x & 0xFFFF0000u);
+          const float r2 = __uint_as_float(rv.y << 16), r3 = __uint_as_float(rv.y & 0xFFFF0000u);
+          const float f0 = act_apply<0>((v[0] + bb.x) + r0, ac3), f1 = act_apply<0>((v[1] + bb.y) + r1, ac3);
+          const float f2 = act_apply<0>((v[2] + bb.z) + r2, ac3), f3 = act_apply<0>((v[3] + bb.w) + r3, ac3);
+          const uint32_t off = yoff[t] == kOOB ? kOOB : yoff[t] + (uint32_t)((q * F + 16 * i) * 2);
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack2_bf16(f0, f1), pack2_bf16(f2, f3)}, yr, (int)off, 0, 0);
         }
-        const f32x4 v = acc[t][i];
-        const float r0 = __uint_as_float(rv.x << 16), r1 = __uint_as_float(rv.x & 0xFFFF0000u);
-        const float r2 = __uint_as_float(rv.y << 16), r3 = __uint_as_float(rv.y & 0xFFFF0000u);
-        const float f0 = act_apply<0>((v[0] + bb.x) + r0, ac3), f1 = act_apply<0>((v[1] + bb.y) + r1, ac3);
-        const float f2 = act_apply<0>((v[2] + bb.z) + r2, ac3), f3 = act_apply<0>((v[3] + bb.w) + r3, ac3);
-        const uint32_t off = yoff[t] == kOOB ? kOOB : yoff[t] + (uint32_t)((q * F + 16 * i) * 2);
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack2_bf16(f0, f1), pack2_bf16(f2, f3)}, yr, (int)off, 0, 0);
       }
     }
   });
@@ -515,8 +530,8 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
 template <class B>
 hipError_t launch_one(const BottleneckParams& p_in, hipStream_t s) {
   BottleneckParams p = p_in;
-  p.tiles_w = (p.W + B::TW - 1) / B::TW;
-  p.tiles_hw = p.tiles_w * ((p.H + B::TH - 1) / B::TH);
+  p.tiles_w = (p.Q + B::TW - 1) / B::TW;
+  p.tiles_hw = p.tiles_w * ((p.P + B::TH - 1) / B::TH);
   p.mg_tw = magic40(p.tiles_w);
   p.mg_thw = magic40(p.tiles_hw);
   p.tiles = p.N * p.tiles_hw;
@@ -525,57 +540,64 @@ hipError_t launch_one(const BottleneckParams& p_in, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Kinds (F, CIN, COUT) and their variants: TH x TW output pixels, waves,
-// phase A ring, phase B stage (taps x 64-channel slices) and ring
-using V64a = Bn<64, 256, 256, 8, 28, 7, 2, 1, 1, 6>;   // 134 KB LDS
-using V64b = Bn<64, 256, 256, 8, 14, 7, 2, 1, 1, 5>;   // 80 KB: two workgroups per CU
-using V64c = Bn<64, 256, 256, 8, 14, 7, 4, 1, 1, 8>;   // 136 KB, deeper rings
-using V128a = Bn<128, 512, 512, 4, 28, 8, 2, 1, 1, 4>;  // 145 KB
-using V128b = Bn<128, 512, 512, 7, 14, 8, 3, 1, 1, 4>;  // 143 KB
-using V128c = Bn<128, 512, 512, 7, 14, 8, 2, 1, 1, 5>;  // 149 KB
-using P64a = Bn<64, 64, 256, 8, 28, 7, 2, 1, 1, 6>;     // 157 KB
-using P64b = Bn<64, 64, 256, 8, 14, 7, 2, 1, 1, 2>;     // 75 KB: two workgroups per CU
-using P64c = Bn<64, 64, 256, 8, 14, 7, 2, 1, 1, 5>;     // 99 KB
+// Kinds (F, CIN, COUT, stride) and their variants: <F, CIN, COUT, S, TH, TW,
+// waves, phase A ring, phase B taps x slices per stage, phase B ring>
+using V64a = Bn<64, 256, 256, 1, 8, 28, 7, 2, 1, 1, 6>;    // 134 KB LDS
+using V64b = Bn<64, 256, 256, 1, 8, 14, 7, 2, 1, 1, 5>;    // 80 KB: two workgroups per CU
+using V64c = Bn<64, 256, 256, 1, 8, 14, 7, 4, 1, 1, 8>;    // 136 KB, deeper rings
+using V128a = Bn<128, 512, 512, 1, 4, 28, 8, 2, 1, 1, 4>;  // 145 KB
+using V128b = Bn<128, 512, 512, 1, 7, 14, 8, 3, 1, 1, 4>;  // 143 KB
+using V128c = Bn<128, 512, 512, 1, 7, 14, 8, 2, 1, 1, 5>;  // 149 KB
+using P64a = Bn<64, 64, 256, 1, 8, 28, 7, 1, 1, 1, 6>;     // projection, 64 input channels
+using P64b = Bn<64, 64, 256, 1, 8, 14, 7, 1, 1, 1, 2>;     //   (57 KB: two workgroups per CU)
+using P64c = Bn<64, 64, 256, 1, 8, 14, 7, 1, 1, 1, 5>;
+using D128a = Bn<128, 256, 512, 2, 7, 14, 8, 2, 1, 1, 5>;  // projection, stride 2
+using D128b = Bn<128, 256, 512, 2, 4, 28, 8, 2, 1, 1, 4>;
+using D128c = Bn<128, 256, 512, 2, 7, 14, 8, 2, 1, 1, 3>;
 
 // f(Bn{}) on variant v of a kind, or `none` for an unknown one
 template <class R, class Fn>
-R with_variant(int F, int CIN, int COUT, int v, R none, Fn&& f) {
+R with_variant(int F, int CIN, int COUT, int S, int v, R none, Fn&& f) {
   if (v < 0 || v > 2) return none;
-  if (F == 64 && CIN == 256 && COUT == 256) return v == 0 ? f(V64a{}) : v == 1 ? f(V64b{}) : f(V64c{});
-  if (F == 128 && CIN == 512 && COUT == 512) return v == 0 ? f(V128a{}) : v == 1 ? f(V128b{}) : f(V128c{});
-  if (F == 64 && CIN == 64 && COUT == 256) return v == 0 ? f(P64a{}) : v == 1 ? f(P64b{}) : f(P64c{});
+  if (S == 1 && F == 64 && CIN == 256 && COUT == 256) return v == 0 ? f(V64a{}) : v == 1 ? f(V64b{}) : f(V64c{});
+  if (S == 1 && F == 128 && CIN == 512 && COUT == 512)
+    return v == 0 ? f(V128a{}) : v == 1 ? f(V128b{}) : f(V128c{});
+  if (S == 1 && F == 64 && CIN == 64 && COUT == 256) return v == 0 ? f(P64a{}) : v == 1 ? f(P64b{}) : f(P64c{});
+  if (S == 2 && F == 128 && CIN == 256 && COUT == 512)
+    return v == 0 ? f(D128a{}) : v == 1 ? f(D128b{}) : f(D128c{});
   return none;
 }
 
 template <class B>
 const char* variant_name() {
   static char buf[64];
-  static const int once = std::snprintf(buf, sizeof(buf), "bottleneck_f%d_%s%dx%d_w%d_a%d_b%d", B::F,
-                                        B::PROJ ? "proj_" : "", B::TH, B::TW, B::NW, B::NSA, B::NSB);
+  static const int once =
+      std::snprintf(buf, sizeof(buf), "bottleneck_f%d_%s%dx%d_w%d_a%d_b%d", B::F,
+                    !B::PROJ ? "" : B::S == 1 ? "proj_" : "proj_s2_", B::TH, B::TW, B::NW, B::NSA, B::NSB);
   (void)once;
   return buf;
 }
 
 }  // namespace
 
-int bottleneck_variants(int F, int CIN, int COUT) {
-  return with_variant(F, CIN, COUT, 0, 0, [](auto) { return 3; });
+int bottleneck_variants(int F, int CIN, int COUT, int S) {
+  return with_variant(F, CIN, COUT, S, 0, 0, [](auto) { return 3; });
 }
 
-const char* bottleneck_variant_name(int F, int CIN, int COUT, int v) {
-  return with_variant(F, CIN, COUT, v, (const char*)"bottleneck_unsupported",
+const char* bottleneck_variant_name(int F, int CIN, int COUT, int S, int v) {
+  return with_variant(F, CIN, COUT, S, v, (const char*)"bottleneck_unsupported",
                       [](auto cfg) { return variant_name<decltype(cfg)>(); });
 }
 
-int bottleneck_tiles(int F, int CIN, int COUT, int v, int N, int H, int W) {
-  return with_variant(F, CIN, COUT, v, 0, [&](auto cfg) {
+int bottleneck_tiles(int F, int CIN, int COUT, int S, int v, int N, int P, int Q) {
+  return with_variant(F, CIN, COUT, S, v, 0, [&](auto cfg) {
     using B = decltype(cfg);
-    return N * ((H + B::TH - 1) / B::TH) * ((W + B::TW - 1) / B::TW);
+    return N * ((P + B::TH - 1) / B::TH) * ((Q + B::TW - 1) / B::TW);
   });
 }
 
-hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int v, hipStream_t s) {
-  return with_variant(F, CIN, COUT, v, hipErrorInvalidValue,
+hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int S, int v, hipStream_t s) {
+  return with_variant(F, CIN, COUT, S, v, hipErrorInvalidValue,
                       [&](auto cfg) { return launch_one<decltype(cfg)>(p, s); });
 }
 

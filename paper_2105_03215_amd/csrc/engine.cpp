@@ -481,10 +481,10 @@ void Planner::find_blocks() {
       for (size_t k = 1; k < n.cat.size(); ++k) ++uses[n.cat[k]];
   }
   for (const IoDesc& o : g.outputs) uses[o.value] += 2;
-  auto plain_conv = [&](const Node& n, int r, int pad) {
+  auto plain_conv = [&](const Node& n, int r, int pad, int stride) {
     if (n.op != OpKind::Conv || n.depthwise || n.groups != 1 || n.act == Act::Gelu) return false;
     const auto& ws = g.values[n.weight].shape;
-    return ws[2] == r && ws[3] == r && n.stride[0] == 1 && n.stride[1] == 1 && n.pad[0] == pad &&
+    return ws[2] == r && ws[3] == r && n.stride[0] == stride && n.stride[1] == stride && n.pad[0] == pad &&
            n.pad[1] == pad && n.pad[2] == pad && n.pad[3] == pad;
   };
   auto fused_elsewhere = [&](int ni) {
@@ -492,41 +492,45 @@ void Planner::find_blocks() {
   };
   for (size_t ci = 0; ci < g.nodes.size(); ++ci) {
     const Node& c = g.nodes[ci];
-    if (!plain_conv(c, 1, 0) || c.residual < 0 || fused_elsewhere((int)ci) || alias_of[c.out] >= 0) continue;
+    if (!plain_conv(c, 1, 0, 1) || c.residual < 0 || fused_elsewhere((int)ci) || alias_of[c.out] >= 0) continue;
     const int m2 = c.data;
-    // the residual: x itself, or the output of a projection conv of x read only here
-    int x = c.residual, pi = -1;
+    // the residual: x itself, or the output of a projection conv of x (stride
+    // 1 or 2, the stride of the block's first 1x1 then) read only here
+    int x = c.residual, pi = -1, S = 1;
     const Value& rv = g.values[c.residual];
     if (rv.source == Value::Node) {
       const Node& pn = g.nodes[rv.index];
-      if (plain_conv(pn, 1, 0) && pn.residual < 0 && pn.act == Act::None && uses[c.residual] == 1 &&
-          !fused_elsewhere(rv.index) && alias_of[c.residual] < 0) {
-        pi = rv.index;
-        x = pn.data;
-      }
+      for (int st : {1, 2})
+        if (plain_conv(pn, 1, 0, st) && pn.residual < 0 && pn.act == Act::None && uses[c.residual] == 1 &&
+            !fused_elsewhere(rv.index) && alias_of[c.residual] < 0) {
+          pi = rv.index;
+          x = pn.data;
+          S = st;
+        }
     }
     const Value& v2 = g.values[m2];
     if (v2.source != Value::Node || uses[m2] != 1) continue;
     const int bi = v2.index;
     const Node& b = g.nodes[bi];
-    if (!plain_conv(b, 3, 1) || b.residual >= 0 || fused_elsewhere(bi) || alias_of[m2] >= 0) continue;
+    if (!plain_conv(b, 3, 1, 1) || b.residual >= 0 || fused_elsewhere(bi) || alias_of[m2] >= 0) continue;
     const int m1 = b.data;
     const Value& v1 = g.values[m1];
     if (v1.source != Value::Node || uses[m1] != 1) continue;
     const int ai = v1.index;
     const Node& a = g.nodes[ai];
-    if (!plain_conv(a, 1, 0) || a.residual >= 0 || a.data != x || fused_elsewhere(ai) || alias_of[m1] >= 0) continue;
+    if (!plain_conv(a, 1, 0, S) || a.residual >= 0 || a.data != x || fused_elsewhere(ai) || alias_of[m1] >= 0)
+      continue;
     const auto& xs = g.values[x].shape;
     const auto& s1 = g.values[m1].shape;
     const auto& ys = g.values[c.out].shape;
-    if (xs.size() != 4 || s1.size() != 4 || ys.size() != 4 || ys[0] != xs[0] || ys[2] != xs[2] ||
-        ys[3] != xs[3])
+    if (xs.size() != 4 || s1.size() != 4 || ys.size() != 4 || ys[0] != xs[0] || ys[2] != s1[2] ||
+        ys[3] != s1[3])
       continue;
     const int CIN = (int)xs[1], F = (int)s1[1], COUT = (int)ys[1];
-    if ((pi < 0) != (COUT == CIN) || bottleneck_variants(F, CIN, COUT) <= 0) continue;
+    if ((pi < 0) != (COUT == CIN && S == 1) || bottleneck_variants(F, CIN, COUT, S) <= 0) continue;
     int most = 0;
-    for (int v = 0; v < bottleneck_variants(F, CIN, COUT); ++v)
-      most = std::max(most, bottleneck_tiles(F, CIN, COUT, v, (int)xs[0], (int)xs[2], (int)xs[3]));
+    for (int v = 0; v < bottleneck_variants(F, CIN, COUT, S); ++v)
+      most = std::max(most, bottleneck_tiles(F, CIN, COUT, S, v, (int)ys[0], (int)ys[2], (int)ys[3]));
     if (!always && most < 256) continue;
     if (xs[0] * xs[2] * xs[3] * std::max(CIN, COUT) * 2 >= (int64_t(1) << 31)) continue;
     block_mid[ci] = bi;
@@ -552,8 +556,10 @@ void Planner::plan_block(int ci) {
   L.bnC = (int)xs[1];
   L.bnF = (int)g.values[a.out].shape[1];
   L.bnCout = (int)g.values[c.out].shape[1];
+  L.bnS = a.stride[0];
   BottleneckParams& p = L.bn;
-  p.N = (int)xs[0], p.H = (int)xs[2], p.W = (int)xs[3];
+  const auto& ys = g.values[c.out].shape;
+  p.N = (int)xs[0], p.H = (int)xs[2], p.W = (int)xs[3], p.P = (int)ys[2], p.Q = (int)ys[3];
   int64_t wbytes = 0;
   // packed weights and padded bias of one conv, as the implicit-GEMM kernel has them
   auto pack = [&](const Node& n, Ref* w, Ref* bias, int* ld, int* w_bytes, int* b_bytes) {
@@ -591,11 +597,11 @@ void Planner::plan_block(int ci) {
   // built-in variant 0; BYOC_BLOCK_VARIANT=<v> forces another
   int v = 0;
   if (const char* bv = std::getenv("BYOC_BLOCK_VARIANT")) v = std::atoi(bv);
-  if (v < 0 || v >= bottleneck_variants(L.bnF, L.bnC, L.bnCout)) v = 0;
+  if (v < 0 || v >= bottleneck_variants(L.bnF, L.bnC, L.bnCout, L.bnS)) v = 0;
   L.tile = ConvTile{};
   L.tile.bnv = v;
   L.tile_default = L.tile;
-  name(L, bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, v));
+  name(L, bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, L.bnS, v));
   e->launches.push_back(L);
 }
 
@@ -1609,7 +1615,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.b3 = (const float*)c.ptr(L.b3);
       p.wp = (const bf16_t*)c.ptr(L.wp);
       p.bp = (const float*)c.ptr(L.bp);
-      return launch_bottleneck(p, L.bnF, L.bnC, L.bnCout, L.tile.bnv, c.s);
+      return launch_bottleneck(p, L.bnF, L.bnC, L.bnCout, L.bnS, L.tile.bnv, c.s);
     }
     case Launch::DepthwiseI8: {
       QDwParams d = L.qd;
@@ -2001,7 +2007,7 @@ std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
 // (one summation order for all of them)
 std::vector<ConvTile> block_candidates(const Launch& L) {
   std::vector<ConvTile> c{L.tile_default};
-  for (int v = 0; v < bottleneck_variants(L.bnF, L.bnC, L.bnCout); ++v) {
+  for (int v = 0; v < bottleneck_variants(L.bnF, L.bnC, L.bnCout, L.bnS); ++v) {
     if (v == L.tile_default.bnv) continue;
     ConvTile t = L.tile_default;
     t.bnv = v;
@@ -2017,7 +2023,8 @@ bool tunable(const Launch& L) {
 void apply_tile(Launch& L, const ConvTile& t) {
   L.tile = t;
   if (L.op == Launch::Bottleneck) {
-    std::snprintf(L.info.name, sizeof(L.info.name), "%s", bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, t.bnv));
+    std::snprintf(L.info.name, sizeof(L.info.name), "%s",
+                  bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, L.bnS, t.bnv));
     return;
   }
   if (L.op == Launch::ConvI8) {

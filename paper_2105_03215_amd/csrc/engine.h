@@ -45,7 +45,7 @@ struct Launch {
   // the 1x1 expand's in w3 / b3, the projection's in wp / bp; res is x
   BottleneckParams bn{};
   Ref w2, b2, w3, b3, wp, bp;
-  int bnF = 0, bnC = 0, bnCout = 0;
+  int bnF = 0, bnC = 0, bnCout = 0, bnS = 1;
   float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
   int qzero = 0;                 // quantize / dequantize zero point
   int qzx = 0, qzy = 0;          // int8 average pool: zero points

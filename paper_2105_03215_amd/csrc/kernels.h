@@ -106,13 +106,13 @@ hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s);
 hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R, int S, int wld,
                                     hipStream_t s);
 // Fused bottleneck block of three conv composites and its residual:
-//   m1 = act1(conv1x1(x; w1) + b1)           CIN -> F channels
-//   m2 = act2(conv3x3(m1; w2, pad 1) + b2)   F -> F
-//   r  = x (COUT == CIN), or the projection bf16(conv1x1(x; wp) + bp) (COUT != CIN)
-//   y  = act3(conv1x1(m2; w3) + b3 + r)      F -> COUT
+//   m1 = act1(conv1x1(x; w1, stride S) + b1)  CIN -> F channels
+//   m2 = act2(conv3x3(m1; w2, pad 1) + b2)    F -> F
+//   r  = x (COUT == CIN, S == 1), or the projection bf16(conv1x1(x; wp, stride S) + bp)
+//   y  = act3(conv1x1(m2; w3) + b3 + r)       F -> COUT
 // each intermediate rounded to bf16 as the unfused composites store it; m1,
 // m2 and the projection never leave the workgroup.  x NHWC [N][H][W][CIN],
-// y [N][H][W][COUT]; weights packed as for the implicit-GEMM kernel
+// y [N][P][Q][COUT] (P, Q: the output grid of the strided 1x1); weights packed as for the implicit-GEMM kernel
 // ([rows][ld], kk = (r*3 + s)*F + c for w2); biases fp32 zero-padded to
 // >= 256 entries (b3, bp: >= COUT).  Activations: none, ReLU, ReLU6 or
 // leaky ReLU.  A kind (F, CIN, COUT) has variants (output tile, rings);
@@ -128,7 +128,7 @@ struct BottleneckParams {
   const float* b2;
   const float* b3;
   const float* bp;
-  int N, H, W;
+  int N, H, W, P, Q;
   int ld1, ld2, ld3, ldp;  // packed weight row strides (elements)
   int x_bytes, y_bytes, w1_bytes, w2_bytes, w3_bytes, wp_bytes, b1_bytes, b2_bytes, b3_bytes, bp_bytes;
   int act1, act2, act3;
@@ -138,12 +138,12 @@ struct BottleneckParams {
   int tiles_w, tiles_hw, tiles, per_xcd;
   uint64_t mg_tw, mg_thw;
 };
-// Variants of a kind (0: no compiled kernel), their names, and the
-// workgroups (output tiles) of variant v on an N x H x W block.
-int bottleneck_variants(int F, int CIN, int COUT);
-const char* bottleneck_variant_name(int F, int CIN, int COUT, int v);
-int bottleneck_tiles(int F, int CIN, int COUT, int v, int N, int H, int W);
-hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int v, hipStream_t s);
+// Variants of a kind (F, CIN, COUT, S) (0: no compiled kernel), their
+// names, and the workgroups (output tiles) of variant v on an N x P x Q output.
+int bottleneck_variants(int F, int CIN, int COUT, int S);
+const char* bottleneck_variant_name(int F, int CIN, int COUT, int S, int v);
+int bottleneck_tiles(int F, int CIN, int COUT, int S, int v, int N, int P, int Q);
+hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int S, int v, hipStream_t s);
 // Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
 // one workgroup per 16 output channels, the reduction split over its waves.
 bool dense_rows_supported(const ConvParams& p);

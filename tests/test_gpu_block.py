@@ -4,7 +4,7 @@ intermediates never leave LDS.
 
 Checked on ResNet-50 stage shapes and on ragged ones (image sizes that are
 not multiples of the kernel's output tile), two blocks chained (a projection
-block is followed by an identity one):
+block, stride 1 or 2, is followed by an identity one):
 
 * the fused run equals, bit for bit, the three unfused launches on the
   single-reduction-group implicit-GEMM kernel without split-K (the same
@@ -36,25 +36,28 @@ FUSED = {"BYOC_FUSE_BLOCK": "1"}
 UNFUSED_KG1 = {"BYOC_FUSE_BLOCK": "0", "BYOC_CONV_TILE": "d64x64s2t256k1", "BYOC_CONV_SPLIT": "1"}
 
 CASES = [
-    # name, batch, input channels, mid channels, output channels, height, width
-    ("s1_56x56", 2, 256, 64, 256, 56, 56),
-    ("s1_ragged_30x19", 1, 256, 64, 256, 30, 19),
-    ("s2_28x28", 2, 512, 128, 512, 28, 28),
-    ("s2_ragged_13x9", 3, 512, 128, 512, 13, 9),
-    ("proj_56x56", 2, 64, 64, 256, 56, 56),
-    ("proj_ragged_30x19", 1, 64, 64, 256, 30, 19),
+    # name, batch, input channels, mid channels, output channels, height, width (of the input), stride
+    ("s1_56x56", 2, 256, 64, 256, 56, 56, 1),
+    ("s1_ragged_30x19", 1, 256, 64, 256, 30, 19, 1),
+    ("s2_28x28", 2, 512, 128, 512, 28, 28, 1),
+    ("s2_ragged_13x9", 3, 512, 128, 512, 13, 9, 1),
+    ("proj_56x56", 2, 64, 64, 256, 56, 56, 1),
+    ("proj_ragged_30x19", 1, 64, 64, 256, 30, 19, 1),
+    ("proj_s2_56x56", 2, 256, 128, 512, 56, 56, 2),
+    ("proj_s2_ragged_27x19", 1, 256, 128, 512, 27, 19, 2),
 ]
 
 
 def _blocks(case, n_blocks=2):
-    name, n, cin, mid, cout, h, w = case
+    name, n, cin, mid, cout, h, w, stride = case
     g = GraphBuilder("block_" + name, 3100 + (CASES.index(case) if case in CASES else 9))
     y = g.input("x", [n, cin, h, w], "uniform")
     for i in range(n_blocks):
         r = y
-        if g.shapes[y][1] != cout:  # the projection shortcut
-            r = g.conv(y, cout, 1, pad=0, act=None, name="b%d.p" % i)
-        a = g.conv(y, mid, 1, pad=0, act="relu", name="b%d.a" % i)
+        st = stride if i == 0 else 1
+        if g.shapes[y][1] != cout or st != 1:  # the projection shortcut
+            r = g.conv(y, cout, 1, stride=st, pad=0, act=None, name="b%d.p" % i)
+        a = g.conv(y, mid, 1, stride=st, pad=0, act="relu", name="b%d.a" % i)
         b = g.conv(a, mid, 3, pad=1, act="relu", name="b%d.b" % i)
         y = g.conv(b, cout, 1, pad=0, act="relu", residual=r, name="b%d.c" % i)
     g.output(y)
@@ -101,7 +104,10 @@ def test_fused_block_matches_unfused_and_oracle(case, monkeypatch):
     assert err <= BF16_TOL
 
 
-@pytest.mark.parametrize("case", [CASES[0], CASES[2], CASES[4]], ids=[CASES[0][0], CASES[2][0], CASES[4][0]])
+VARIANT_CASES = [CASES[0], CASES[2], CASES[4], CASES[6]]
+
+
+@pytest.mark.parametrize("case", VARIANT_CASES, ids=[c[0] for c in VARIANT_CASES])
 def test_every_block_variant_and_autotune_bitwise(case, monkeypatch):
     announce("block variants " + case[0])
     wl = _blocks(case)
@@ -121,7 +127,7 @@ def test_block_fusion_rule(monkeypatch):
     pair without a fused kernel, and by default for a block whose finest
     tiling gives fewer than 256 workgroups; one launch by default from 256."""
     announce("block fusion rule")
-    wl = _blocks(("odd", 1, 192, 48, 192, 14, 14), n_blocks=1)
+    wl = _blocks(("odd", 1, 192, 48, 192, 14, 14, 1), n_blocks=1)
     _, names = _run(wl, monkeypatch, FUSED)
     assert not any(n.startswith("bottleneck_") for n in names), names
     wl = _blocks(CASES[0], n_blocks=1)
@@ -129,6 +135,6 @@ def test_block_fusion_rule(monkeypatch):
     assert not any(n.startswith("bottleneck_") for n in names), names
     _, names = _run(wl, monkeypatch, {})  # batch 2 at 56x56: 56 tiles of 8x14
     assert not any(n.startswith("bottleneck_") for n in names), names
-    wl = _blocks(("s1_bs10", 10, 256, 64, 256, 56, 56), n_blocks=1)  # 280 tiles of 8x14
+    wl = _blocks(("s1_bs10", 10, 256, 64, 256, 56, 56, 1), n_blocks=1)  # 280 tiles of 8x14
     _, names = _run(wl, monkeypatch, {})
     assert sum(n.startswith("bottleneck_") for n in names) == 1, names
