@@ -106,8 +106,8 @@ def _copy_kib(path, counter):
     return statistics.median([v for v in vals if v > 0.5 * big])
 
 
-CONV_SOURCES = ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "lds_dma.h", "stem.hip", "dense_rows.hip",
-                "engine.cpp")
+CONV_SOURCES = ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "bottleneck.hip", "lds_dma.h", "stem.hip",
+                "dense_rows.hip", "engine.cpp")
 I8_KERNELS = ("conv_i8_kernel",)
 I8_SOURCES = ("conv_i8.hip", "quant.hip", "lds_dma.h", "engine.cpp")
 
