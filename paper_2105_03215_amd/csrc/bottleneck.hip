@@ -78,7 +78,8 @@ struct Bn {
   static constexpr int SA = CIN / 64;                     // phase A stages (x slices)
   static constexpr int PFA = NSA >= 2 ? NSA - 1 : 1;      // phase A stages issued ahead
   static constexpr int NQ = COUT / F;                     // phase C chunks (F output channels each)
-  static constexpr int UQ = WGC + (PROJ ? SA : 0);        // phase C stages per chunk: W3 slices, then Wp slices
+  static constexpr int CSL = PROJ ? 1 : WGC;              // 64-channel slices per phase C stage
+  static constexpr int UQ = (WGC + (PROJ ? SA : 0)) / CSL;  // phase C stages per chunk: W3, then Wp slices
   static constexpr int SC = NQ * UQ;                      // phase C stages
   static constexpr int GB = WGC / SPB;                    // slice groups of a tap
   static constexpr int SB = 9 / TPS * GB;                 // phase B stages
@@ -91,7 +92,7 @@ struct Bn {
   static constexpr int ASTG = XB + W1B;
   static constexpr int W2B = TPS * SPB * F * ROW;
   static constexpr int M2B = WGC * OPXP * ROW;
-  static constexpr int CB = F * ROW;  // phase C stage: F rows of a chunk x 64 input channels
+  static constexpr int CB = CSL * F * ROW;  // phase C stage: F rows of a chunk x CSL x 64 input channels
   static constexpr int OFF_R2 = M1B;  // the phase A ring, then the W2 ring and M2
   static constexpr int OFF_M2 = OFF_R2 + NSB * W2B;
   static constexpr int END_A = OFF_R2 + NSA * ASTG;
@@ -103,20 +104,24 @@ struct Bn {
   static constexpr int OFF_JUNK = OFF_BIAS + BBLK * 1024;
   static constexpr int LDS = OFF_JUNK + 1024;
   // 1 KB fills (8 rows of 128 bytes) per stage and per thread
-  static constexpr int XBLK = HPXP / 8, W1BLK = F / 8, W2BLK = TPS * SPB * F / 8, CBLK = F / 8;
+  static constexpr int XBLK = HPXP / 8, W1BLK = F / 8, W2BLK = TPS * SPB * F / 8, CBLK = CSL * F / 8;
   static constexpr int LXA = (XBLK + NW - 1) / NW, LW1 = (W1BLK + NW - 1) / NW;
   static constexpr int LA = LXA + LW1;
   static constexpr int LB = (W2BLK + NW - 1) / NW;
   static constexpr int LC = (CBLK + NW - 1) / NW;
   static constexpr int ST = TB * 4;  // y stores per chunk per thread
+  // Identity blocks finish a chunk after the next chunk's first stage
+  // (DEFER), projection blocks at the chunk's last stage; does stage i
+  // store a chunk?
+  static constexpr bool DEFER = !PROJ;
+  static constexpr bool stores_at(int i) { return DEFER ? (i % UQ == 0 && i >= UQ) : (i % UQ == UQ - 1); }
   // Vector memory operations a thread may have outstanding after phase C
   // stage k's loads: the loads of the stages issued ahead of it, and the
   // y stores of the chunks finished since it was issued (stage i issues
-  // stage i + NSC - 1 after its wait, then computes, then - at a chunk's
-  // last stage - stores).
+  // stage i + NSC - 1 after its wait, then computes, then stores).
   static constexpr int c_younger(int k) {
     int stores = 0;
-    for (int i = cmax(0, k - NSC + 1); i < k; ++i) stores += (i % UQ == UQ - 1) ? ST : 0;
+    for (int i = cmax(0, k - NSC + 1); i < k; ++i) stores += stores_at(i) ? ST : 0;
     return cmin(NSC - 2, SC - 1 - k) * LC + stores;
   }
   static constexpr int c_younger_max() {
@@ -220,9 +225,11 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     w2off[u] = blk < B::W2BLK ? row_off(rem - sl * (F / 8), F / 8, p.ld2, tap * F + sl * 64) : kOOB;
   }
 #pragma unroll
-  for (int u = 0; u < B::LC; ++u) {  // F rows of a chunk, 64 channels of W3 (of Wp)
-    w3off[u] = row_off(wave + NW * u, B::CBLK, p.ld3, 0);
-    wpoff[u] = B::PROJ ? row_off(wave + NW * u, B::CBLK, p.ldp, 0) : kOOB;
+  for (int u = 0; u < B::LC; ++u) {  // [slice sl][F rows of a chunk] of W3 (of Wp: one slice)
+    const int blk = wave + NW * u;
+    const int sl = blk / (F / 8);
+    w3off[u] = blk < B::CBLK ? row_off(blk - sl * (F / 8), F / 8, p.ld3, sl * 64) : kOOB;
+    wpoff[u] = B::PROJ ? row_off(blk, B::CBLK, p.ldp, 0) : kOOB;
   }
   auto dst = [&](uint32_t region, int blk, int nblk) {
     return __builtin_amdgcn_readfirstlane(blk < nblk ? region + blk * 1024 : junk);
@@ -243,13 +250,14 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
       lds_fill16(w2r, dst(slot, wave + NW * u, B::W2BLK),
                  live(w2off[u], ((s / B::GB) * B::TPS * F + (s % B::GB) * B::SPB * 64) * 2));
   };
-  auto issue_c = [&](int k) {  // chunk k / UQ: slice j = k % UQ of W3 (j < WGC), else of Wp
+  auto issue_c = [&](int k) {  // chunk k / UQ: stage j = k % UQ, W3 slices j * CSL .. (j < WGC / CSL), else Wp
     const uint32_t slot = base + (k % B::NSC) * B::CB;
     const int q = k / B::UQ, j = k % B::UQ;
-    if (j < B::WGC) {
+    if (j * B::CSL < B::WGC) {
 #pragma unroll
       for (int u = 0; u < B::LC; ++u)
-        lds_fill16(w3r, dst(slot, wave + NW * u, B::CBLK), live(w3off[u], (q * F * p.ld3 + j * 64) * 2));
+        lds_fill16(w3r, dst(slot, wave + NW * u, B::CBLK),
+                   live(w3off[u], (q * F * p.ld3 + j * B::CSL * 64) * 2));
     } else {
 #pragma unroll
       for (int u = 0; u < B::LC; ++u)
@@ -357,8 +365,8 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
       const float4 bb = bias[i];
       const f32x4 v = accA[t][i];
       // (+ 0: the unfused epilogue adds its zero residual, which turns a -0 into +0)
-      float f0 = act_apply<0>((v[0] + bb.x) + 0.f, ac1), f1 = act_apply<0>((v[1] + bb.y) + 0.f, ac1);
-      float f2 = act_apply<0>((v[2] + bb.z) + 0.f, ac1), f3 = act_apply<0>((v[3] + bb.w) + 0.f, ac1);
+      float f0 = act_apply<2>((v[0] + bb.x) + 0.f, ac1), f1 = act_apply<2>((v[1] + bb.y) + 0.f, ac1);
+      float f2 = act_apply<2>((v[2] + bb.z) + 0.f, ac1), f3 = act_apply<2>((v[3] + bb.w) + 0.f, ac1);
       if (!inside) f0 = f1 = f2 = f3 = 0.f;
       *(uint2*)(m1 + slot_off(px, 2 * i + (lane >> 5), key) + (lq & 1) * 8) =
           make_uint2(pack2_bf16(f0, f1), pack2_bf16(f2, f3));
@@ -432,8 +440,8 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     for (int i = 0; i < 4; ++i) {
       const float4 bb = bias[i];
       const f32x4 v = accB[t][i];
-      const float f0 = act_apply<0>((v[0] + bb.x) + 0.f, ac2), f1 = act_apply<0>((v[1] + bb.y) + 0.f, ac2);
-      const float f2 = act_apply<0>((v[2] + bb.z) + 0.f, ac2), f3 = act_apply<0>((v[3] + bb.w) + 0.f, ac2);
+      const float f0 = act_apply<2>((v[0] + bb.x) + 0.f, ac2), f1 = act_apply<2>((v[1] + bb.y) + 0.f, ac2);
+      const float f2 = act_apply<2>((v[2] + bb.z) + 0.f, ac2), f3 = act_apply<2>((v[3] + bb.w) + 0.f, ac2);
       *(uint2*)(m2 + slot_off(o, 2 * i + (lane >> 5), o) + (lq & 1) * 8) =
           make_uint2(pack2_bf16(f0, f1), pack2_bf16(f2, f3));
     }
@@ -453,10 +461,47 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
     crow[t] = tile_ok ? o : l16;
   }
   const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(p.y, (short)0, p.y_bytes, kBufferFlags);
-  f32x4 acc[B::TB][4], accp[B::TB][4];
+  // Identity blocks defer a chunk's epilogue past the next chunk's MFMAs
+  // (two accumulator sets), so its ALU work and stores overlap them.
+  f32x4 acc[B::DEFER ? 2 : 1][B::TB][4], accp[B::TB][4];
+  // the chunk's epilogue; every thread issues all ST stores (out-of-range
+  // offsets for pixels it does not own), so the wait counts are exact
+  auto finish = [&](auto qq) {
+    constexpr int q = decltype(qq)::value;
+    constexpr int set = B::DEFER ? q % 2 : 0;
+    float4 bp[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bias[i] = *(const float4*)(sb3 + q * F + cg * 64 + 16 * i + 4 * lq);
+      if constexpr (B::PROJ) bp[i] = *(const float4*)(sbp + q * F + cg * 64 + 16 * i + 4 * lq);
+    }
+#pragma unroll
+    for (int t = 0; t < B::TB; ++t) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 bb = bias[i];
+        uint2 rv;
+        if constexpr (B::PROJ) {  // the projection composite's output: bias, no activation, bf16
+          const f32x4 u = accp[t][i];
+          rv = make_uint2(pack2_bf16((u[0] + bp[i].x) + 0.f, (u[1] + bp[i].y) + 0.f),
+                          pack2_bf16((u[2] + bp[i].z) + 0.f, (u[3] + bp[i].w) + 0.f));
+        } else {
+          rv = resv[q][t][i];
+        }
+        const f32x4 v = acc[set][t][i];
+        const float r0 = __uint_as_float(rv.x << 16), r1 = __uint_as_float(rv.x & 0xFFFF0000u);
+        const float r2 = __uint_as_float(rv.y << 16), r3 = __uint_as_float(rv.y & 0xFFFF0000u);
+        const float f0 = act_apply<2>((v[0] + bb.x) + r0, ac3), f1 = act_apply<2>((v[1] + bb.y) + r1, ac3);
+        const float f2 = act_apply<2>((v[2] + bb.z) + r2, ac3), f3 = act_apply<2>((v[3] + bb.w) + r3, ac3);
+        const uint32_t off = yoff[t] == kOOB ? kOOB : yoff[t] + (uint32_t)((q * F + 16 * i) * 2);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack2_bf16(f0, f1), pack2_bf16(f2, f3)}, yr, (int)off, 0, 0);
+      }
+    }
+  };
   static_for<0, B::SC>([&](auto kk) {
     constexpr int k = decltype(kk)::value;
     constexpr int q = k / B::UQ, j = k % B::UQ;
+    constexpr int set = B::DEFER ? q % 2 : 0;
     stage_barrier<B::c_younger(k)>();
     if constexpr (k + B::NSC - 1 < B::SC) issue_c(k + B::NSC - 1);
     const char* wt = lds + (k % B::NSC) * B::CB;
@@ -464,67 +509,46 @@ __global__ __launch_bounds__(B::NT) void bottleneck_kernel(BottleneckParams p) {
 #pragma unroll
       for (int t = 0; t < B::TB; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[t][i] = accp[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    bf16x8 a[2][4], b[2][B::TB];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int c = ks * 4 + lq;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[ks][i] = as_bf16x8(*(const uint4*)(wt + slot_off(cg * 64 + 16 * i + l16, c, lk)));
-      if constexpr (j < B::WGC) {  // W3: slice j of M2
-        const char* m2 = lds + B::OFF_M2 + j * B::OPXP * 128;
-#pragma unroll
-        for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(*(const uint4*)(m2 + slot_off(crow[t], c, lk)));
-      } else {  // Wp: slice j - WGC of x
-#pragma unroll
-        for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(xf[t][2 * (j - B::WGC) + ks]);
-      }
+        for (int i = 0; i < 4; ++i) acc[set][t][i] = accp[t][i] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int sl = 0; sl < B::CSL; ++sl) {
+      constexpr bool w3 = j * B::CSL < B::WGC;  // W3: slice j * CSL + sl of M2; else Wp: slice j - WGC of x
+      bf16x8 a[2][4], b[2][B::TB];
 #pragma unroll
-      for (int t = 0; t < B::TB; ++t)
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c = ks * 4 + lq;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if constexpr (j < B::WGC)
-            acc[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], acc[t][i], 0, 0, 0);
-          else
-            accp[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], accp[t][i], 0, 0, 0);
+        for (int i = 0; i < 4; ++i)
+          a[ks][i] = as_bf16x8(*(const uint4*)(wt + sl * F * 128 + slot_off(cg * 64 + 16 * i + l16, c, lk)));
+        if constexpr (w3) {
+          const char* m2 = lds + B::OFF_M2 + (j * B::CSL + sl) * B::OPXP * 128;
+#pragma unroll
+          for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(*(const uint4*)(m2 + slot_off(crow[t], c, lk)));
+        } else {
+#pragma unroll
+          for (int t = 0; t < B::TB; ++t) b[ks][t] = as_bf16x8(xf[t][2 * (j - B::WGC) + ks]);
         }
-    if constexpr (j == B::UQ - 1) {
-      // the chunk's epilogue; every thread issues all ST stores (out-of-range
-      // offsets for pixels it does not own), so the wait counts are exact
-      float4 bp[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bias[i] = *(const float4*)(sb3 + q * F + cg * 64 + 16 * i + 4 * lq);
-        if constexpr (B::PROJ) bp[i] = *(const float4*)(sbp + q * F + cg * 64 + 16 * i + 4 * lq);
       }
 #pragma unroll
-      for (int t = 0; t < B::TB; ++t) {
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float4 bb = bias[i];
-          uint2 rv;
-          if constexpr (B::PROJ) {  // the projection composite's output: bias, no activation, bf16
-            const f32x4 u = accp[t][i];
-            rv = make_uint2(pack2_bf16((u[0] + bp[i].x) + 0.f, (u[1] + bp[i].y) + 0.f),
-                            pack2_bf16((u[2] + bp[i].z) + 0.f, (u[3] + bp[i].w) + 0.f));
-          } else {
-            rv = resv[q][t][i];
+        for (int t = 0; t < B::TB; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if constexpr (w3)
+              acc[set][t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], acc[set][t][i], 0, 0, 0);
+            else
+              accp[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][t], accp[t][i], 0, 0, 0);
           }
-          const f32x4 v = acc[t][i];
-          const float r0 = __uint_as_float(rv.x << 16), r1 = __uint_as_float(rv.x & 0xFFFF0000u);
-          const float r2 = __uint_as_float(rv.y << 16), r3 = __uint_as_float(rv.y & 0xFFFF0000u);
-          const float f0 = act_apply<0>((v[0] + bb.x) + r0, ac3), f1 = act_apply<0>((v[1] + bb.y) + r1, ac3);
-          const float f2 = act_apply<0>((v[2] + bb.z) + r2, ac3), f3 = act_apply<0>((v[3] + bb.w) + r3, ac3);
-          const uint32_t off = yoff[t] == kOOB ? kOOB : yoff[t] + (uint32_t)((q * F + 16 * i) * 2);
-          __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack2_bf16(f0, f1), pack2_bf16(f2, f3)}, yr, (int)off, 0, 0);
-        }
-      }
+    }
+    if constexpr (B::DEFER) {
+      if constexpr (j == 0 && q >= 1) finish(std::integral_constant<int, q - 1>{});
+    } else if constexpr (j == B::UQ - 1) {
+      finish(std::integral_constant<int, q>{});
     }
   });
+  if constexpr (B::DEFER) finish(std::integral_constant<int, B::NQ - 1>{});
 }
 
 template <class B>

@@ -482,7 +482,9 @@ void Planner::find_blocks() {
   }
   for (const IoDesc& o : g.outputs) uses[o.value] += 2;
   auto plain_conv = [&](const Node& n, int r, int pad, int stride) {
-    if (n.op != OpKind::Conv || n.depthwise || n.groups != 1 || n.act == Act::Gelu) return false;
+    // (the fused kernel applies none / ReLU / ReLU6 only)
+    if (n.op != OpKind::Conv || n.depthwise || n.groups != 1 || n.act == Act::Gelu || n.act == Act::Leaky)
+      return false;
     const auto& ws = g.values[n.weight].shape;
     return ws[2] == r && ws[3] == r && n.stride[0] == stride && n.stride[1] == stride && n.pad[0] == pad &&
            n.pad[1] == pad && n.pad[2] == pad && n.pad[3] == pad;

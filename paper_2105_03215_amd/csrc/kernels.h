@@ -114,8 +114,7 @@ hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst,
 // m2 and the projection never leave the workgroup.  x NHWC [N][H][W][CIN],
 // y [N][P][Q][COUT] (P, Q: the output grid of the strided 1x1); weights packed as for the implicit-GEMM kernel
 // ([rows][ld], kk = (r*3 + s)*F + c for w2); biases fp32 zero-padded to
-// >= 256 entries (b3, bp: >= COUT).  Activations: none, ReLU, ReLU6 or
-// leaky ReLU.  A kind (F, CIN, COUT) has variants (output tile, rings);
+// >= 256 entries (b3, bp: >= COUT).  Activations: none, ReLU or ReLU6.  A kind (F, CIN, COUT) has variants (output tile, rings);
 // all variants of a kind sum in the same order, so they agree bit for bit.
 struct BottleneckParams {
   const bf16_t* x;
