@@ -138,3 +138,18 @@ def test_block_fusion_rule(monkeypatch):
     wl = _blocks(("s1_bs10", 10, 256, 64, 256, 56, 56, 1), n_blocks=1)  # 280 tiles of 8x14
     _, names = _run(wl, monkeypatch, {})
     assert sum(n.startswith("bottleneck_") for n in names) == 1, names
+
+
+def test_resnet50_fused_equals_unfused_bitwise(monkeypatch):
+    """The whole ResNet-50 v1 graph with every supported block fused
+    (batch 4, fusion forced) equals the unfused plan bit for bit, both with
+    every other conv on the same single-group tile without split-K."""
+    announce("resnet50_v1 bs4: fused blocks vs unfused, bitwise")
+    from paper_2105_03215_amd import workloads
+    wl = workloads.build("resnet50_v1", n=4)
+    fused, names = _run(wl, monkeypatch, dict(UNFUSED_KG1, BYOC_FUSE_BLOCK="1"))
+    assert sum(n.startswith("bottleneck_") for n in names) == 7, names  # stages 1 and 2
+    plain, pnames = _run(wl, monkeypatch, UNFUSED_KG1)
+    assert not any(n.startswith("bottleneck_") for n in pnames)
+    assert torch.equal(fused.view(torch.int16) if fused.dtype == torch.bfloat16 else fused,
+                       plain.view(torch.int16) if plain.dtype == torch.bfloat16 else plain)
