@@ -287,11 +287,15 @@ struct Planner {
   Status plan_i8();
   void plan_node(int ni);
   void plan_node_i8(int ni);
+  bool quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im2col, bool border,
+                        std::vector<uint8_t>& packed, std::vector<int32_t>& qch, std::vector<int32_t>& wtap,
+                        std::string* err_msg);
   void find_post_adds();
   void find_stems();
   void find_concat_aliases();
   void find_blocks();
   void plan_block(int ci);
+  void plan_block_i8(int ci);
   Ref slice(int vcat, int channel) const {  // channel slice of a concatenation's buffer
     Ref r = loc[vcat];
     r.off += (int64_t)channel * 2;
@@ -471,7 +475,7 @@ void Planner::find_blocks() {
   block_proj.assign(g.nodes.size(), -1);
   in_block.assign(g.nodes.size(), false);
   const char* env = std::getenv("BYOC_FUSE_BLOCK");
-  if (!bf16 || (env && env[0] == '0')) return;
+  if (!(bf16 || i8) || (env && env[0] == '0')) return;
   const bool always = env && env[0] == '1';
   std::vector<int> uses(g.values.size(), 0);
   for (const Node& n : g.nodes) {
@@ -529,10 +533,13 @@ void Planner::find_blocks() {
         ys[3] != s1[3])
       continue;
     const int CIN = (int)xs[1], F = (int)s1[1], COUT = (int)ys[1];
-    if ((pi < 0) != (COUT == CIN && S == 1) || bottleneck_variants(F, CIN, COUT, S) <= 0) continue;
+    if ((pi < 0) != (COUT == CIN && S == 1) || bottleneck_variants(i8, F, CIN, COUT, S) <= 0) continue;
+    // codes: the fused epilogue sums the rescaled terms unclamped, exact while
+    // the residual's term stays below 2^19 (255 * its factor)
+    if (i8 && !(g.values[c.residual].qscale / g.values[c.out].qscale < 2048.0)) continue;
     int most = 0;
-    for (int v = 0; v < bottleneck_variants(F, CIN, COUT, S); ++v)
-      most = std::max(most, bottleneck_tiles(F, CIN, COUT, S, v, (int)ys[0], (int)ys[2], (int)ys[3]));
+    for (int v = 0; v < bottleneck_variants(i8, F, CIN, COUT, S); ++v)
+      most = std::max(most, bottleneck_tiles(i8, F, CIN, COUT, S, v, (int)ys[0], (int)ys[2], (int)ys[3]));
     if (!always && most < 256) continue;
     if (xs[0] * xs[2] * xs[3] * std::max(CIN, COUT) * 2 >= (int64_t(1) << 31)) continue;
     block_mid[ci] = bi;
@@ -599,11 +606,109 @@ void Planner::plan_block(int ci) {
   // built-in variant 0; BYOC_BLOCK_VARIANT=<v> forces another
   int v = 0;
   if (const char* bv = std::getenv("BYOC_BLOCK_VARIANT")) v = std::atoi(bv);
-  if (v < 0 || v >= bottleneck_variants(L.bnF, L.bnC, L.bnCout, L.bnS)) v = 0;
+  if (v < 0 || v >= bottleneck_variants(false, L.bnF, L.bnC, L.bnCout, L.bnS)) v = 0;
   L.tile = ConvTile{};
   L.tile.bnv = v;
   L.tile_default = L.tile;
-  name(L, bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, L.bnS, v));
+  name(L, bottleneck_variant_name(false, L.bnF, L.bnC, L.bnCout, L.bnS, v));
+  e->launches.push_back(L);
+}
+
+// The int8 form of a fused block: the three (four) convs quantized on the
+// host as the int8 conv kernel has them; each composite's output zero point
+// and activation clamp, and the residual's rescaling into y's scale.
+void Planner::plan_block_i8(int ci) {
+  const Node& c = g.nodes[ci];
+  const Node& b = g.nodes[block_mid[ci]];
+  const Node& a = g.nodes[g.values[b.data].index];
+  const int x = a.data;
+  const auto& xs = g.values[x].shape;
+  const std::string where = "node " + std::to_string(ci) + " (" + c.composite + ")";
+  Launch L;
+  L.op = Launch::Bottleneck;
+  L.info.kind = BYOC_K_CONV_I8;
+  L.info.node = ci;
+  L.x = loc[x];
+  L.res = loc[x];
+  L.y = loc[c.out];
+  L.bnI8 = true;
+  L.bnC = (int)xs[1];
+  L.bnF = (int)g.values[a.out].shape[1];
+  L.bnCout = (int)g.values[c.out].shape[1];
+  L.bnS = a.stride[0];
+  BottleneckParams& p = L.bn;
+  const auto& ys = g.values[c.out].shape;
+  p.N = (int)xs[0], p.H = (int)xs[2], p.W = (int)xs[3], p.P = (int)ys[2], p.Q = (int)ys[3];
+  // output zero point and activation clamp in codes (as the int8 conv has them)
+  auto clamp_of = [&](const Node& n, int slot) {
+    const Value& yv = g.values[n.out];
+    int lo = -128, hi = 127;
+    if (n.act == Act::Relu || n.act == Act::Relu6) lo = yv.qzero;
+    if (n.act == Act::Relu6) {
+      const double h = yv.qzero + std::nearbyint(6.0 / yv.qscale);
+      hi = h < 127.0 ? (int)h : 127;
+    }
+    p.qz[slot] = yv.qzero, p.qlo[slot] = lo, p.qhi[slot] = hi;
+  };
+  int64_t wbytes = 0;
+  auto pack = [&](const Node& n, Ref* w, Ref* bias, int* ld, int* w_bytes, int* b_bytes) {
+    const auto& ws = g.values[n.weight].shape;
+    const int K = (int)ws[0], R = (int)ws[2], S = (int)ws[3];
+    const int Cp = cp[n.data];
+    const int rows = (int)rup(K, kRowPad);
+    const int Kgp = (int)rup((int64_t)R * S * Cp, 128);
+    if ((int64_t)R * S * ws[1] * 255 * 127 >= (int64_t(1) << 30)) {
+      err = Status::Err(BYOC_ERR_UNSUPPORTED, where + ": reduction too long for int32 accumulation");
+      return;
+    }
+    std::vector<uint8_t> packed;
+    std::vector<int32_t> qch, wtap;
+    std::string why;
+    if (!quantize_conv_i8(n, Cp, Kgp, rows, false, false, packed, qch, wtap, &why)) {
+      err = Status::Err(BYOC_ERR_UNSUPPORTED, where + ": " + why);
+      return;
+    }
+    *w = host_blob(std::move(packed));
+    std::vector<uint8_t> qb(qch.size() * 4);
+    std::memcpy(qb.data(), qch.data(), qb.size());
+    *bias = host_blob(std::move(qb));
+    *ld = Kgp;
+    *w_bytes = rows * Kgp;
+    *b_bytes = rows * 8;
+    wbytes += numel(ws) + K * 8;
+  };
+  pack(a, &L.w, &L.bias, &p.ld1, &p.w1_bytes, &p.b1_bytes);
+  pack(b, &L.w2, &L.b2, &p.ld2, &p.w2_bytes, &p.b2_bytes);
+  pack(c, &L.w3, &L.b3, &p.ld3, &p.w3_bytes, &p.b3_bytes);
+  clamp_of(a, 0);
+  clamp_of(b, 1);
+  clamp_of(c, 2);
+  int64_t pmacs = 0;
+  if (block_proj[ci] >= 0) {
+    const Node& pn = g.nodes[block_proj[ci]];
+    pack(pn, &L.wp, &L.bp, &p.ldp, &p.wp_bytes, &p.bp_bytes);
+    clamp_of(pn, 3);
+    pmacs = pn.macs;
+  }
+  if (!err.ok()) return;
+  const Value& rv = g.values[c.residual];  // x, or the projection's output
+  p.zr = rv.qzero;
+  if (!rescale_factor(rv.qscale / g.values[c.out].qscale, &p.mr) || !(p.mr < 2048.f)) {
+    err = Status::Err(BYOC_ERR_UNSUPPORTED, where + ": residual rescaling factor outside (0, 2048)");
+    return;
+  }
+  p.x_bytes = (int)act_bytes(x);
+  p.y_bytes = (int)act_bytes(c.out);
+  L.info.flops = 2 * (a.macs + b.macs + c.macs + pmacs);
+  L.info.bytes = act_bytes(x) + act_bytes(c.out) + wbytes;
+  // built-in variant 0; BYOC_BLOCK_VARIANT=<v> forces another
+  int v = 0;
+  if (const char* bv = std::getenv("BYOC_BLOCK_VARIANT")) v = std::atoi(bv);
+  if (v < 0 || v >= bottleneck_variants(true, L.bnF, L.bnC, L.bnCout, L.bnS)) v = 0;
+  L.tile = ConvTile{};
+  L.tile.bnv = v;
+  L.tile_default = L.tile;
+  name(L, bottleneck_variant_name(true, L.bnF, L.bnC, L.bnCout, L.bnS, v));
   e->launches.push_back(L);
 }
 
@@ -1091,15 +1196,22 @@ Status Planner::plan_i8() {
     e->launches.push_back(L);
   }
   find_post_adds();
+  stem_pool.assign(g.nodes.size(), -1);  // (no fused stems or concatenation aliases on codes)
+  stem_conv.assign(g.nodes.size(), -1);
+  alias_of.assign(g.values.size(), -1);
+  find_blocks();
   for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
     const int v = g.nodes[ni].out;
     cp[v] = (int)rup(g.values[v].shape[1], 16);
-    if (post_add[ni] >= 0) {  // planned at the add folded into it
+    if (post_add[ni] >= 0 || in_block[ni]) {  // planned at the add folded into it, or with its block
       loc[v] = Ref();
       continue;
     }
     loc[v] = arena(internal_bytes(v));
-    plan_node_i8(post_conv[ni] >= 0 ? post_conv[ni] : (int)ni);
+    if (block_mid[ni] >= 0)
+      plan_block_i8((int)ni);
+    else
+      plan_node_i8(post_conv[ni] >= 0 ? post_conv[ni] : (int)ni);
     if (!err.ok()) return err;
   }
   for (size_t j = 0; j < g.outputs.size(); ++j) {
@@ -1122,6 +1234,86 @@ Status Planner::plan_i8() {
     e->launches.push_back(L);
   }
   return Status::Ok();
+}
+
+// Host quantization of a conv's (or dense's) weights - per output channel,
+// symmetric, int8 - its bias (int32, with -Z_x times the channel's weight sum
+// folded in) and the per-channel rescaling factors S_x S_w / S_y, as the int8
+// implicit-GEMM kernel reads them: packed [rows][Kgp], column (r*S + s)*Cp + c
+// (im2col rows: (r*S + s)*4 + c); qch [rows][2] = {bias, factor bits}; with
+// `border`, wtap [rows][R*S] the weight sums per tap.  False, with the reason
+// in *err_msg, on a value outside the kernel's ranges.
+bool Planner::quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im2col, bool border,
+                               std::vector<uint8_t>& packed, std::vector<int32_t>& qch, std::vector<int32_t>& wtap,
+                               std::string* err_msg) {
+  auto why = [&](const std::string& m) {
+    *err_msg = m;
+    return false;
+  };
+  const Value& xv = g.values[n.data];
+  const Value& yv = g.values[n.out];
+  const auto& ws = g.values[n.weight].shape;
+  const bool dense = n.op == OpKind::Dense;
+  const int K = (int)ws[0], Cg = (int)ws[1];
+  const int R = dense ? 1 : (int)ws[2], S = dense ? 1 : (int)ws[3];
+  const byoc_const& wcst = consts[g.values[n.weight].index];
+  const bool wbf = wcst.dtype == BYOC_BF16;
+  auto wget = [&](int64_t i) -> double {
+    if (wbf) {
+      const uint32_t b = (uint32_t)((const uint16_t*)wcst.data)[i] << 16;
+      float f;
+      std::memcpy(&f, &b, 4);
+      return f;
+    }
+    return ((const float*)wcst.data)[i];
+  };
+  const byoc_const* bcst = n.bias >= 0 ? &consts[g.values[n.bias].index] : nullptr;
+  auto bget = [&](int k) -> double {
+    if (bcst->dtype == BYOC_BF16) {
+      const uint32_t b = (uint32_t)((const uint16_t*)bcst->data)[k] << 16;
+      float f;
+      std::memcpy(&f, &b, 4);
+      return f;
+    }
+    return ((const float*)bcst->data)[k];
+  };
+  const int RS = R * S;
+  packed.assign((size_t)rows * Kgp, 0);
+  qch.assign((size_t)rows * 2, 0);
+  wtap.assign(border ? (size_t)rows * RS : 0, 0);
+  const double sx = xv.qscale, sy = yv.qscale;
+  for (int k = 0; k < K; ++k) {
+    const int64_t base = (int64_t)k * Cg * RS;
+    double amax = 0.0;
+    for (int64_t i = 0; i < (int64_t)Cg * RS; ++i) amax = std::max(amax, std::fabs(wget(base + i)));
+    const double sw = amax > 0.0 ? amax / 127.0 : 1.0;
+    int64_t total = 0;
+    for (int c = 0; c < Cg; ++c)
+      for (int r = 0; r < R; ++r)
+        for (int s2 = 0; s2 < S; ++s2) {
+          double qv = std::nearbyint(wget(base + ((int64_t)c * R + r) * S + s2) / sw);
+          qv = std::min(127.0, std::max(-127.0, qv));
+          const int wq = (int)qv;
+          const size_t col = im2col ? (size_t)(r * S + s2) * 4 + c : (size_t)(r * S + s2) * Cp + c;
+          packed[(size_t)k * Kgp + col] = (uint8_t)(int8_t)wq;
+          total += wq;
+          if (border) wtap[(size_t)k * RS + r * S + s2] += wq;
+        }
+    double bq = 0.0;
+    if (bcst) {
+      bq = std::nearbyint(bget(k) / (sx * sw));
+      bq = std::min(2147483647.0, std::max(-2147483648.0, bq));
+    }
+    const int64_t beff = (int64_t)bq - (int64_t)xv.qzero * total;
+    if (beff <= -(int64_t(1) << 30) || beff >= (int64_t(1) << 30))
+      return why("quantized bias of channel " + std::to_string(k) + " outside +-2^30");
+    float mk = 0.f;
+    if (!rescale_factor((sx * sw) / sy, &mk))
+      return why("rescaling factor of channel " + std::to_string(k) + " outside (0, 2^20)");
+    qch[(size_t)k * 2 + 0] = (int32_t)beff;
+    std::memcpy(&qch[(size_t)k * 2 + 1], &mk, 4);
+  }
+  return true;
 }
 
 void Planner::plan_node_i8(int ni) {
@@ -1253,63 +1445,12 @@ void Planner::plan_node_i8(int ni) {
 
     // host quantization of the weights (per output channel, symmetric),
     // the bias and the rescaling factors
-    const byoc_const& wcst = consts[g.values[n.weight].index];
-    const bool wbf = wcst.dtype == BYOC_BF16;
-    auto wget = [&](int64_t i) -> double {
-      if (wbf) {
-        const uint32_t b = (uint32_t)((const uint16_t*)wcst.data)[i] << 16;
-        float f;
-        std::memcpy(&f, &b, 4);
-        return f;
-      }
-      return ((const float*)wcst.data)[i];
-    };
-    const byoc_const* bcst = n.bias >= 0 ? &consts[g.values[n.bias].index] : nullptr;
-    auto bget = [&](int k) -> double {
-      if (bcst->dtype == BYOC_BF16) {
-        const uint32_t b = (uint32_t)((const uint16_t*)bcst->data)[k] << 16;
-        float f;
-        std::memcpy(&f, &b, 4);
-        return f;
-      }
-      return ((const float*)bcst->data)[k];
-    };
-    const int RS = R * S;
     const bool border = !dense && !im2col && xv.qzero != 0 && (n.pad[0] | n.pad[1] | n.pad[2] | n.pad[3]) != 0;
-    std::vector<uint8_t> packed((size_t)rows * p.Kgp, 0);
-    std::vector<int32_t> qch((size_t)rows * 2, 0), wtap(border ? (size_t)rows * RS : 0, 0);
-    const double sx = xv.qscale, sy = yv.qscale;
-    for (int k = 0; k < K; ++k) {
-      const int64_t base = (int64_t)k * Cg * RS;
-      double amax = 0.0;
-      for (int64_t i = 0; i < (int64_t)Cg * RS; ++i) amax = std::max(amax, std::fabs(wget(base + i)));
-      const double sw = amax > 0.0 ? amax / 127.0 : 1.0;
-      int64_t total = 0;
-      for (int c = 0; c < Cg; ++c)
-        for (int r = 0; r < R; ++r)
-          for (int s2 = 0; s2 < S; ++s2) {
-            double qv = std::nearbyint(wget(base + ((int64_t)c * R + r) * S + s2) / sw);
-            qv = std::min(127.0, std::max(-127.0, qv));
-            const int wq = (int)qv;
-            const size_t col = im2col ? (size_t)(r * S + s2) * 4 + c : (size_t)(r * S + s2) * Cp + c;
-            packed[(size_t)k * p.Kgp + col] = (uint8_t)(int8_t)wq;
-            total += wq;
-            if (border) wtap[(size_t)k * RS + r * S + s2] += wq;
-          }
-      double bq = 0.0;
-      if (bcst) {
-        bq = std::nearbyint(bget(k) / (sx * sw));
-        bq = std::min(2147483647.0, std::max(-2147483648.0, bq));
-      }
-      const int64_t beff = (int64_t)bq - (int64_t)xv.qzero * total;
-      if (beff <= -(int64_t(1) << 30) || beff >= (int64_t(1) << 30))
-        return fail("quantized bias of channel " + std::to_string(k) + " outside +-2^30");
-      float mk = 0.f;
-      if (!rescale_factor((sx * sw) / sy, &mk))
-        return fail("rescaling factor of channel " + std::to_string(k) + " outside (0, 2^20)");
-      qch[(size_t)k * 2 + 0] = (int32_t)beff;
-      std::memcpy(&qch[(size_t)k * 2 + 1], &mk, 4);
-    }
+    std::vector<uint8_t> packed;
+    std::vector<int32_t> qch, wtap;
+    std::string why;
+    if (!quantize_conv_i8(n, Cp, p.Kgp, rows, im2col, border, packed, qch, wtap, &why)) return fail(why);
+    const double sy = yv.qscale;
     L.w = host_blob(std::move(packed));
     std::vector<uint8_t> qb(qch.size() * 4);
     std::memcpy(qb.data(), qch.data(), qb.size());
@@ -1607,17 +1748,17 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
     }
     case Launch::Bottleneck: {
       BottleneckParams p = L.bn;
-      p.x = (const bf16_t*)c.ptr(L.x);
-      p.y = (bf16_t*)c.ptr(L.y);
-      p.w1 = (const bf16_t*)c.ptr(L.w);
-      p.w2 = (const bf16_t*)c.ptr(L.w2);
-      p.w3 = (const bf16_t*)c.ptr(L.w3);
-      p.b1 = (const float*)c.ptr(L.bias);
-      p.b2 = (const float*)c.ptr(L.b2);
-      p.b3 = (const float*)c.ptr(L.b3);
-      p.wp = (const bf16_t*)c.ptr(L.wp);
-      p.bp = (const float*)c.ptr(L.bp);
-      return launch_bottleneck(p, L.bnF, L.bnC, L.bnCout, L.bnS, L.tile.bnv, c.s);
+      p.x = c.ptr(L.x);
+      p.y = c.ptr(L.y);
+      p.w1 = c.ptr(L.w);
+      p.w2 = c.ptr(L.w2);
+      p.w3 = c.ptr(L.w3);
+      p.b1 = c.ptr(L.bias);
+      p.b2 = c.ptr(L.b2);
+      p.b3 = c.ptr(L.b3);
+      p.wp = c.ptr(L.wp);
+      p.bp = c.ptr(L.bp);
+      return launch_bottleneck(p, L.bnI8, L.bnF, L.bnC, L.bnCout, L.bnS, L.tile.bnv, c.s);
     }
     case Launch::DepthwiseI8: {
       QDwParams d = L.qd;
@@ -2009,7 +2150,7 @@ std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
 // (one summation order for all of them)
 std::vector<ConvTile> block_candidates(const Launch& L) {
   std::vector<ConvTile> c{L.tile_default};
-  for (int v = 0; v < bottleneck_variants(L.bnF, L.bnC, L.bnCout, L.bnS); ++v) {
+  for (int v = 0; v < bottleneck_variants(L.bnI8, L.bnF, L.bnC, L.bnCout, L.bnS); ++v) {
     if (v == L.tile_default.bnv) continue;
     ConvTile t = L.tile_default;
     t.bnv = v;
@@ -2026,7 +2167,7 @@ void apply_tile(Launch& L, const ConvTile& t) {
   L.tile = t;
   if (L.op == Launch::Bottleneck) {
     std::snprintf(L.info.name, sizeof(L.info.name), "%s",
-                  bottleneck_variant_name(L.bnF, L.bnC, L.bnCout, L.bnS, t.bnv));
+                  bottleneck_variant_name(L.bnI8, L.bnF, L.bnC, L.bnCout, L.bnS, t.bnv));
     return;
   }
   if (L.op == Launch::ConvI8) {

@@ -46,6 +46,7 @@ struct Launch {
   BottleneckParams bn{};
   Ref w2, b2, w3, b3, wp, bp;
   int bnF = 0, bnC = 0, bnCout = 0, bnS = 1;
+  bool bnI8 = false;  // on int8 codes (w*, b* hold the int8 conv's weights and tables)
   float qscale = 0.f;            // quantize: fl32(1 / S); dequantize: fl32(S)
   int qzero = 0;                 // quantize / dequantize zero point
   int qzx = 0, qzy = 0;          // int8 average pool: zero points

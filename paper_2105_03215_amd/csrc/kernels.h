@@ -108,41 +108,52 @@ hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst,
 // Fused bottleneck block of three conv composites and its residual:
 //   m1 = act1(conv1x1(x; w1, stride S) + b1)  CIN -> F channels
 //   m2 = act2(conv3x3(m1; w2, pad 1) + b2)    F -> F
-//   r  = x (COUT == CIN, S == 1), or the projection bf16(conv1x1(x; wp, stride S) + bp)
+//   r  = x (COUT == CIN, S == 1), or the projection conv1x1(x; wp, stride S) + bp
 //   y  = act3(conv1x1(m2; w3) + b3 + r)       F -> COUT
-// each intermediate rounded to bf16 as the unfused composites store it; m1,
-// m2 and the projection never leave the workgroup.  x NHWC [N][H][W][CIN],
-// y [N][P][Q][COUT] (P, Q: the output grid of the strided 1x1); weights packed as for the implicit-GEMM kernel
-// ([rows][ld], kk = (r*3 + s)*F + c for w2); biases fp32 zero-padded to
-// >= 256 entries (b3, bp: >= COUT).  Activations: none, ReLU or ReLU6.  A kind (F, CIN, COUT) has variants (output tile, rings);
-// all variants of a kind sum in the same order, so they agree bit for bit.
+// each intermediate rounded as the unfused composites store it; m1, m2 and
+// the projection never leave the workgroup.  x NHWC [N][H][W][CIN], y
+// [N][P][Q][COUT] (P, Q: the output grid of the strided 1x1); weights packed
+// as for the implicit-GEMM kernels ([rows][ld], kk = (r*3 + s)*F + c for w2).
+// bf16 (i8 = false): biases fp32 zero-padded to >= 256 entries (b3, bp: >=
+// COUT); activations none, ReLU or ReLU6.  int8 codes (i8 = true): weights
+// int8, b* the int8 conv's per-channel table {bias with the input zero
+// point folded in, float32 factor bits} (>= 128 entries, b3 and bp >= COUT),
+// each composite's output zero point and clamp in qz / qlo / qhi (0: m1,
+// 1: m2, 2: y, 3: the projection), y = clamp(qz[2] + rescale(sum + bias,
+// factor) + rescale(r - zr, mr)).  A kind (i8, F, CIN, COUT, S) has variants
+// (output tile, rings); all variants of a kind sum in the same order, so
+// they agree bit for bit.
 struct BottleneckParams {
-  const bf16_t* x;
-  bf16_t* y;
-  const bf16_t* w1;
-  const bf16_t* w2;
-  const bf16_t* w3;
-  const bf16_t* wp;  // projection weights (COUT != CIN), else unused
-  const float* b1;
-  const float* b2;
-  const float* b3;
-  const float* bp;
+  const void* x;
+  void* y;
+  const void* w1;
+  const void* w2;
+  const void* w3;
+  const void* wp;  // projection weights (COUT != CIN or S != 1), else unused
+  const void* b1;
+  const void* b2;
+  const void* b3;
+  const void* bp;
   int N, H, W, P, Q;
   int ld1, ld2, ld3, ldp;  // packed weight row strides (elements)
   int x_bytes, y_bytes, w1_bytes, w2_bytes, w3_bytes, wp_bytes, b1_bytes, b2_bytes, b3_bytes, bp_bytes;
   int act1, act2, act3;
   float alpha1, alpha2, alpha3;
+  int qz[4], qlo[4], qhi[4];  // int8: output zero points and clamps
+  int zr;                     // int8: the residual's zero point
+  float mr;                   //   and its rescaling factor into y's scale
   // set by the launcher: output tiles per row band, per image and in all,
   // tiles per XCD, and the 40-bit reciprocals of the first two
   int tiles_w, tiles_hw, tiles, per_xcd;
   uint64_t mg_tw, mg_thw;
 };
-// Variants of a kind (F, CIN, COUT, S) (0: no compiled kernel), their
-// names, and the workgroups (output tiles) of variant v on an N x P x Q output.
-int bottleneck_variants(int F, int CIN, int COUT, int S);
-const char* bottleneck_variant_name(int F, int CIN, int COUT, int S, int v);
-int bottleneck_tiles(int F, int CIN, int COUT, int S, int v, int N, int P, int Q);
-hipError_t launch_bottleneck(const BottleneckParams& p, int F, int CIN, int COUT, int S, int v, hipStream_t s);
+// Variants of a kind (0: no compiled kernel), their names, and the
+// workgroups (output tiles) of variant v on an N x P x Q output.
+int bottleneck_variants(bool i8, int F, int CIN, int COUT, int S);
+const char* bottleneck_variant_name(bool i8, int F, int CIN, int COUT, int S, int v);
+int bottleneck_tiles(bool i8, int F, int CIN, int COUT, int S, int v, int N, int P, int Q);
+hipError_t launch_bottleneck(const BottleneckParams& p, bool i8, int F, int CIN, int COUT, int S, int v,
+                             hipStream_t s);
 // Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
 // one workgroup per 16 output channels, the reduction split over its waves.
 bool dense_rows_supported(const ConvParams& p);

@@ -16,15 +16,23 @@ block, stride 1 or 2, is followed by an identity one):
   on the 56x56 case, for the fused and the unfused launches alike - from the
   bf16 storage of four composites in a row; the bit equality above carries
   the per-composite one-ulp checks of the unfused kernels over to them.)
+
+The int8 form of the same blocks (scales and zero points calibrated on the
+oracle's values of one image; the intermediates' zero point after the ReLU is
+-128, so the 3x3's padding is a nonzero code) must equal both the unfused
+int8 launches and the int8 oracle bit for bit, with every tile variant.
 """
 
+
+import numpy as np
 import pytest
 import torch
 
 import oracle
+from oracle import quant as OQ
 from paper_2105_03215_amd import capi, runtime
 from paper_2105_03215_amd.workloads import GraphBuilder
-from parity_util import BF16_TOL, announce, rel_err
+from parity_util import BF16_TOL, announce, oracle_calibrated_int8, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -64,12 +72,12 @@ def _blocks(case, n_blocks=2):
     return g.finish()
 
 
-def _run(wl, monkeypatch, env, options=None):
+def _run(wl, monkeypatch, env, options=None, graph=None):
     for k in ENV:
         monkeypatch.delenv(k, raising=False)
     for k, v in env.items():
         monkeypatch.setenv(k, v)
-    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
+    sg = capi.Subgraph(graph if graph is not None else wl.graph, wl.consts, device=0)
     s = torch.cuda.Stream(device=DEV)
     try:
         if options:
@@ -153,3 +161,39 @@ def test_resnet50_fused_equals_unfused_bitwise(monkeypatch):
     assert not any(n.startswith("bottleneck_") for n in pnames)
     assert torch.equal(fused.view(torch.int16) if fused.dtype == torch.bfloat16 else fused,
                        plain.view(torch.int16) if plain.dtype == torch.bfloat16 else plain)
+
+
+def _int8(wl):
+    return oracle_calibrated_int8(wl.graph, wl.consts, [np.ascontiguousarray(a[:1]) for a in wl.inputs])
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_int8_fused_block_exact(case, monkeypatch):
+    """int8: fused == unfused == the int8 oracle, bit for bit (two chained blocks)."""
+    announce("int8 fused block " + case[0])
+    wl = _blocks(case)
+    qg = _int8(wl)
+    fused, names = _run(wl, monkeypatch, FUSED, graph=qg)
+    assert sum(nm.startswith("bottleneck_i8_") for nm in names) == 2, names
+    assert not any(nm.startswith("conv_i8") for nm in names), names
+    plain, pnames = _run(wl, monkeypatch, {"BYOC_FUSE_BLOCK": "0"}, graph=qg)
+    assert not any(nm.startswith("bottleneck_") for nm in pnames), pnames
+    assert torch.equal(fused, plain)
+    ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
+    assert np.array_equal(runtime.to_host_f64(fused), ref.astype(np.float64))
+
+
+@pytest.mark.parametrize("case", VARIANT_CASES, ids=[c[0] for c in VARIANT_CASES])
+def test_int8_every_block_variant_and_autotune(case, monkeypatch):
+    announce("int8 block variants " + case[0])
+    wl = _blocks(case)
+    qg = _int8(wl)
+    ref, names0 = _run(wl, monkeypatch, dict(FUSED, BYOC_BLOCK_VARIANT="0"), graph=qg)
+    seen = {tuple(n for n in names0 if n.startswith("bottleneck_i8_"))}
+    for v in (1, 2):
+        out, names = _run(wl, monkeypatch, dict(FUSED, BYOC_BLOCK_VARIANT=str(v)), graph=qg)
+        seen.add(tuple(n for n in names if n.startswith("bottleneck_i8_")))
+        assert torch.equal(out, ref), v
+    assert len(seen) == 3, seen
+    out, _ = _run(wl, monkeypatch, FUSED, options={"autotune": True, "graph_replay": True}, graph=qg)
+    assert torch.equal(out, ref)
