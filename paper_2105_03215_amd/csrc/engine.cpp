@@ -289,7 +289,8 @@ struct Planner {
   void plan_node_i8(int ni);
   bool quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im2col, bool border,
                         std::vector<uint8_t>& packed, std::vector<int32_t>& qch, std::vector<int32_t>& wtap,
-                        std::string* err_msg);
+                        std::string* err_msg, int row_ld = 0);
+  void plan_stem_i8(int conv_ni, int pool_ni);
   void find_post_adds();
   void find_stems();
   void find_concat_aliases();
@@ -311,7 +312,8 @@ struct Planner {
 void Planner::find_stems() {
   stem_pool.assign(g.nodes.size(), -1);
   stem_conv.assign(g.nodes.size(), -1);
-  if (!bf16) return;
+  const char* env = std::getenv("BYOC_FUSE_STEM");  // =0: never fuse
+  if (!(bf16 || i8) || (env && env[0] == '0')) return;
   auto uses = [&](int v, int* user) {
     int count = 0;
     for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
@@ -339,6 +341,10 @@ void Planner::find_stems() {
     const auto& ws = g.values[c.weight].shape;
     if (!stem_supported((int)xs[1], (int)ws[0], (int)ws[2], (int)ws[3], c.stride[0], c.stride[1], pn.pool[0],
                         pn.pool[1], pn.stride[0], pn.stride[1]))
+      continue;
+    // codes: a clamp activation, and the pool keeps the conv's (scale, zero point)
+    if (i8 && (c.act == Act::Gelu || c.act == Act::Leaky || g.values[pn.out].qscale != g.values[c.out].qscale ||
+               g.values[pn.out].qzero != g.values[c.out].qzero))
       continue;
     stem_pool[ci] = pi;
     stem_conv[pi] = ci;
@@ -383,6 +389,63 @@ void Planner::plan_stem(int ci, int pi) {
   L.info.flops = 2 * c.macs;
   L.info.bytes = ext_bytes(c.data, g.inputs[in_idx].dtype) + numel(ws) * 2 + 64 * 4 + act_bytes(pn.out);
   name(L, "stem_conv_maxpool");
+  e->launches.push_back(L);
+}
+
+// The int8 stem: the input's codes formed in the kernel (the boundary
+// quantize of that input is not planned), weights quantized on the host as
+// the int8 conv has them, in the stem's cell layout.
+void Planner::plan_stem_i8(int ci, int pi) {
+  const Node& c = g.nodes[ci];
+  const Node& pn = g.nodes[pi];
+  const Value& xv = g.values[c.data];
+  const Value& yv = g.values[c.out];
+  const auto& xs = xv.shape;
+  const auto& cs = yv.shape;
+  const auto& ps = g.values[pn.out].shape;
+  const auto& ws = g.values[c.weight].shape;
+  const int in_idx = xv.index;
+  Launch L;
+  L.op = Launch::StemConvPool;
+  L.info.kind = BYOC_K_CONV_I8;
+  L.info.node = ci;
+  L.x = loc[c.data];
+  L.y = loc[pn.out];
+  StemParams& p = L.stem;
+  p.x_bf16 = g.inputs[in_idx].dtype == DType::BF16;
+  p.N = (int)xs[0], p.C = (int)xs[1], p.H = (int)xs[2], p.W = (int)xs[3];
+  p.R = (int)ws[2], p.S = (int)ws[3], p.sh = c.stride[0], p.sw = c.stride[1], p.pt = c.pad[0], p.pl = c.pad[1];
+  p.P = (int)cs[2], p.Q = (int)cs[3];
+  p.kph = pn.pool[0], p.kpw = pn.pool[1], p.sph = pn.stride[0], p.spw = pn.stride[1];
+  p.ppt = pn.pad[0], p.ppl = pn.pad[1];
+  p.PO = (int)ps[2], p.QO = (int)ps[3];
+  p.act = (int)c.act;
+  p.i8 = 1;
+  p.inv_scale = (float)(1.0 / xv.qscale);  // as the boundary quantize has it
+  p.zx = xv.qzero;
+  p.zy = yv.qzero;
+  p.lo = -128, p.hi = 127;
+  if (c.act == Act::Relu || c.act == Act::Relu6) p.lo = yv.qzero;
+  if (c.act == Act::Relu6) {
+    const double h = yv.qzero + std::nearbyint(6.0 / yv.qscale);
+    p.hi = h < 127.0 ? (int)h : 127;
+  }
+  p.wld = stem_weight_ld_i8(p.R);
+  if (const char* ev = std::getenv("BYOC_STEM_GRID")) p.grid_cap = std::max(0, std::atoi(ev));
+  std::vector<uint8_t> packed;
+  std::vector<int32_t> qch, wtap;
+  std::string why;
+  if (!quantize_conv_i8(c, 4, p.wld, 64, true, false, packed, qch, wtap, &why, 32)) {
+    err = Status::Err(BYOC_ERR_UNSUPPORTED, "node " + std::to_string(ci) + " (" + c.composite + "): " + why);
+    return;
+  }
+  L.w = host_blob(std::move(packed));
+  std::vector<uint8_t> qb(qch.size() * 4);
+  std::memcpy(qb.data(), qch.data(), qb.size());
+  L.bias = host_blob(std::move(qb));
+  L.info.flops = 2 * c.macs;
+  L.info.bytes = ext_bytes(c.data, g.inputs[in_idx].dtype) + numel(ws) + 64 * 8 + act_bytes(pn.out);
+  name(L, "stem_conv_maxpool_i8");
   e->launches.push_back(L);
 }
 
@@ -1126,6 +1189,10 @@ Status Planner::plan_i8() {
   // to 16): the conv becomes a 1x1 product over a reduction of R*S*4 instead
   // of R*S*16 (channels padded to 16), and out-of-image taps hold the zero
   // point, so the folded -Z_x * sum(w) of the bias is exact for every pixel.
+  find_stems();
+  std::vector<bool> stem_input(g.values.size(), false);  // read in place by a fused stem
+  for (size_t ni = 0; ni < g.nodes.size(); ++ni)
+    if (stem_pool[ni] >= 0) stem_input[g.nodes[ni].data] = true;
   im2col_of.assign(g.values.size(), -1);
   {
     std::vector<int> uses(g.values.size(), 0), reader(g.values.size(), -1);
@@ -1138,7 +1205,7 @@ Status Planner::plan_i8() {
     for (const IoDesc& in : g.inputs) {
       const int v = in.value;
       const auto& s = g.values[v].shape;
-      if (s.size() != 4 || s[1] > 4 || uses[v] != 1 || reader[v] < 0) continue;
+      if (s.size() != 4 || s[1] > 4 || uses[v] != 1 || reader[v] < 0 || stem_input[v]) continue;
       const Node& n = g.nodes[reader[v]];
       if (n.op != OpKind::Conv || n.depthwise || n.data != v) continue;
       const auto& ws = g.values[n.weight].shape;
@@ -1153,6 +1220,10 @@ Status Planner::plan_i8() {
     const IoDesc& in = g.inputs[i];
     const int v = in.value;
     const Value& val = g.values[v];
+    if (stem_input[v]) {
+      loc[v] = io(Ref::Input, (int)i);
+      continue;
+    }
     if (im2col_of[v] >= 0) {
       const Node& n = g.nodes[im2col_of[v]];
       const auto& ws = g.values[n.weight].shape;
@@ -1196,19 +1267,20 @@ Status Planner::plan_i8() {
     e->launches.push_back(L);
   }
   find_post_adds();
-  stem_pool.assign(g.nodes.size(), -1);  // (no fused stems or concatenation aliases on codes)
-  stem_conv.assign(g.nodes.size(), -1);
-  alias_of.assign(g.values.size(), -1);
+  alias_of.assign(g.values.size(), -1);  // (no concatenation aliases on codes)
   find_blocks();
   for (size_t ni = 0; ni < g.nodes.size(); ++ni) {
     const int v = g.nodes[ni].out;
     cp[v] = (int)rup(g.values[v].shape[1], 16);
-    if (post_add[ni] >= 0 || in_block[ni]) {  // planned at the add folded into it, or with its block
+    // planned at the add folded into it, with its block or with its stem's pool
+    if (post_add[ni] >= 0 || in_block[ni] || stem_pool[ni] >= 0) {
       loc[v] = Ref();
       continue;
     }
     loc[v] = arena(internal_bytes(v));
-    if (block_mid[ni] >= 0)
+    if (stem_conv[ni] >= 0)
+      plan_stem_i8(stem_conv[ni], (int)ni);
+    else if (block_mid[ni] >= 0)
       plan_block_i8((int)ni);
     else
       plan_node_i8(post_conv[ni] >= 0 ? post_conv[ni] : (int)ni);
@@ -1240,12 +1312,13 @@ Status Planner::plan_i8() {
 // symmetric, int8 - its bias (int32, with -Z_x times the channel's weight sum
 // folded in) and the per-channel rescaling factors S_x S_w / S_y, as the int8
 // implicit-GEMM kernel reads them: packed [rows][Kgp], column (r*S + s)*Cp + c
-// (im2col rows: (r*S + s)*4 + c); qch [rows][2] = {bias, factor bits}; with
+// (im2col rows: (r*S + s)*4 + c; row_ld > 0: r*row_ld + s*4 + c, the fused
+// stem's cells); qch [rows][2] = {bias, factor bits}; with
 // `border`, wtap [rows][R*S] the weight sums per tap.  False, with the reason
 // in *err_msg, on a value outside the kernel's ranges.
 bool Planner::quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im2col, bool border,
                                std::vector<uint8_t>& packed, std::vector<int32_t>& qch, std::vector<int32_t>& wtap,
-                               std::string* err_msg) {
+                               std::string* err_msg, int row_ld) {
   auto why = [&](const std::string& m) {
     *err_msg = m;
     return false;
@@ -1294,7 +1367,8 @@ bool Planner::quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im
           double qv = std::nearbyint(wget(base + ((int64_t)c * R + r) * S + s2) / sw);
           qv = std::min(127.0, std::max(-127.0, qv));
           const int wq = (int)qv;
-          const size_t col = im2col ? (size_t)(r * S + s2) * 4 + c : (size_t)(r * S + s2) * Cp + c;
+          const size_t col = row_ld > 0 ? (size_t)r * row_ld + s2 * 4 + c
+                             : im2col ? (size_t)(r * S + s2) * 4 + c : (size_t)(r * S + s2) * Cp + c;
           packed[(size_t)k * Kgp + col] = (uint8_t)(int8_t)wq;
           total += wq;
           if (border) wtap[(size_t)k * RS + r * S + s2] += wq;
@@ -1780,9 +1854,9 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
     case Launch::StemConvPool: {
       StemParams p = L.stem;
       p.x = c.ptr(L.x);
-      p.w = (const bf16_t*)c.ptr(L.w);
-      p.bias = (const float*)c.ptr(L.bias);
-      p.y = (bf16_t*)c.ptr(L.y);
+      p.w = c.ptr(L.w);
+      p.bias = c.ptr(L.bias);
+      p.y = c.ptr(L.y);
       return launch_stem_conv_maxpool(p, c.s);
     }
   }

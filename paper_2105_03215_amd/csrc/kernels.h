@@ -87,10 +87,15 @@ hipError_t launch_conv_halo(const ConvParams& p, int bm, int bn, int stages, int
 struct StemParams {
   const void* x;  // graph input [N][C][H][W], bf16 or f32
   int x_bf16;
-  const bf16_t* w;  // packed [64][wld], column r*32 + s*4 + c
+  const void* w;  // packed [64][wld] bf16 (int8 codes: bytes), column r*32 + s*4 + c
   int wld;
-  const float* bias;  // [64] or nullptr
-  bf16_t* y;          // [N][PO][QO][64]
+  const void* bias;  // [64] float or nullptr (int8 codes: [64][2] {folded bias, factor bits})
+  void* y;           // [N][PO][QO][64] bf16 (int8 codes)
+  // int8 codes (i8 = 1): the input's 1 / scale and zero point, the conv
+  // output's zero point and activation clamp in codes
+  int i8;
+  float inv_scale;
+  int zx, zy, lo, hi;
   int N, C, H, W;
   int R, S, sh, sw, pt, pl;      // conv
   int P, Q;                      // conv output size
@@ -102,6 +107,7 @@ struct StemParams {
 };
 bool stem_supported(int C, int K, int R, int S, int sh, int sw, int kph, int kpw, int sph, int spw);
 int stem_weight_ld(int R);
+int stem_weight_ld_i8(int R);  // bytes: kernel rows in pairs of 64, + 16
 hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s);
 hipError_t launch_pack_stem_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R, int S, int wld,
                                     hipStream_t s);

@@ -189,19 +189,48 @@ __global__ __launch_bounds__(kThreads) void depthwise_i8_kernel(QDwParams p) {
   }
 }
 
-// One thread per (n, channel): the integer sum over the image is exact.
+// Global average pool of codes.  Workgroup = one image x 32 groups of 16
+// channels; the 8 lanes of a group are consecutive, lane j sums pixels j,
+// j + 8, ... (16-byte loads, eight in flight), then the 8 partial sums meet
+// in a butterfly.  Integer sums: exact, so the order does not matter.
 __global__ __launch_bounds__(kThreads) void avgpool_i8_kernel(PoolParams p, int zx, int zy, float m) {
-  const int total = p.N * p.Cp;
+  const int G = p.Cp / 16;
+  const int n = blockIdx.x;
+  const int pl = threadIdx.x & 7;
+  const int g = blockIdx.y * (kThreads / 8) + (threadIdx.x >> 3);
   const int HW = p.H * p.W;
-  const int8_t* x = reinterpret_cast<const int8_t*>(p.x);
-  int8_t* y = reinterpret_cast<int8_t*>(p.y);
-  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
-    const int c = i % p.Cp;
-    const int n = i / p.Cp;
-    const int8_t* src = x + (int64_t)n * HW * p.Cp + c;
-    int sum = 0;
-    for (int j = 0; j < HW; ++j) sum += (int)src[(int64_t)j * p.Cp] - zx;
-    y[i] = (int8_t)clip_i8(zy + rescale(sum, m));
+  const bool ok = g < G;
+  const int8_t* x = reinterpret_cast<const int8_t*>(p.x) + (size_t)n * HW * p.Cp + (size_t)(ok ? g : 0) * 16;
+  int acc[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) acc[c] = 0;
+  for (int i0 = 0; i0 < HW; i0 += 64) {
+    uint4 u[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = i0 + pl + 8 * j;
+      u[j] = *(const uint4*)(x + (size_t)(i < HW ? i : 0) * p.Cp);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (i0 + pl + 8 * j >= HW) continue;
+      const uint32_t w[4] = {u[j].x, u[j].y, u[j].z, u[j].w};
+#pragma unroll
+      for (int c = 0; c < 16; ++c) acc[c] += (int)(int8_t)(w[c >> 2] >> (8 * (c & 3)));
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1)
+#pragma unroll
+    for (int c = 0; c < 16; ++c) acc[c] += __shfl_xor(acc[c], o);
+  if (ok && pl == 0) {
+    uint32_t o4[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const int v = clip_i8(zy + rescale(acc[c] - HW * zx, m));
+      o4[c >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (c & 3));
+    }
+    *(uint4*)(reinterpret_cast<int8_t*>(p.y) + (size_t)n * p.Cp + g * 16) = make_uint4(o4[0], o4[1], o4[2], o4[3]);
   }
 }
 
@@ -264,7 +293,8 @@ hipError_t launch_maxpool_nhwc_i8(const PoolParams& p, hipStream_t s) {
 }
 
 hipError_t launch_avgpool_nhwc_i8(const PoolParams& p, int zx, int zy, float m, hipStream_t s) {
-  avgpool_i8_kernel<<<grid_for((int64_t)p.N * p.Cp), kThreads, 0, s>>>(p, zx, zy, m);
+  if (p.Cp % 16 != 0) return hipErrorInvalidValue;
+  avgpool_i8_kernel<<<dim3(p.N, (p.Cp / 16 + kThreads / 8 - 1) / (kThreads / 8)), kThreads, 0, s>>>(p, zx, zy, m);
   return hipGetLastError();
 }
 

@@ -32,15 +32,28 @@
 //    after the max equals the max of rounded values), 8-byte NHWC stores.
 // Barriers inside the tile loop wait on LDS only, so the patch loads in
 // flight cross them.
+//
+// int8 codes (a partially quantized function, Sec. 3.2): the patch holds
+// the input's codes, clip(rint(x / S_x) + Z_x) as the boundary quantize
+// computes them (positions outside the image read 0 and so hold Z_x, the
+// padding the folded bias expects), one dword of 4 channel codes per cell;
+// v_mfma_i32_16x16x64_i8 takes two kernel rows per step (lane group g: row
+// 2m + g / 2, taps 4 (g % 2) .. + 3, four cells); the int32 sums start at
+// the folded bias.  Requantizing (clamp(Z_y + rescale(a, m), lo, hi), m > 0)
+// is monotone, so the pooling max is taken over the sums of the positions
+// inside the image and the maximum requantized once: the codes of the
+// unfused conv followed by the max pool of codes.
 #include "device_common.h"
 
 #include <atomic>
+#include <climits>
 
 namespace byoc {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) int i32x4;
 
 constexpr int kThreads = 256;
 constexpr int kTH = 8;        // pooled rows per tile (2 per wave)
@@ -53,7 +66,7 @@ constexpr int kK = 64;                                           // output chann
 constexpr int kWeightLdMax = 8 * 32 + 8;
 constexpr int kWChunks = (kK * kWeightLdMax / 8 + kThreads - 1) / kThreads;  // 16-byte weight chunks per thread
 constexpr int kWeightBytes = kWChunks * kThreads * 16;  // >= 64 rows of kWeightLdMax; every thread fills its chunks
-constexpr int kBiasBytes = kK * 4;
+constexpr int kBiasBytes = kK * 8;  // float bias, or {int32 bias, float32 factor} of codes
 constexpr int kPatchBytes = kUnits * kThreads * 32;  // every thread writes its units, the last ones past the patch
 constexpr int kLdsBytes = kWeightBytes + kBiasBytes + kPatchBytes;
 static_assert(kPatchBytes >= kPR * kPC * 8, "patch");
@@ -162,12 +175,50 @@ __device__ __forceinline__ void store_patch(const PatchRegs<XBF>& r, uint2* patc
   }
 }
 
-template <bool VEC, bool XBF>
+// int8: the loaded units quantized to codes, 4 channel codes per cell
+// (16 bytes per unit).
+template <bool XBF>
+__device__ __forceinline__ void store_patch_i8(const PatchRegs<XBF>& r, uint32_t* patch, int tid, float inv,
+                                               int zp) {
+#pragma unroll
+  for (int u = 0; u < kUnits; ++u) {
+    const int unit = tid + u * kThreads;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};  // cells (pixels) of the unit
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      float f[4];
+      if constexpr (XBF) {
+        const uint2 v = r.v[u][c];
+        f[0] = __uint_as_float(v.x << 16), f[1] = __uint_as_float(v.x & 0xFFFF0000u);
+        f[2] = __uint_as_float(v.y << 16), f[3] = __uint_as_float(v.y & 0xFFFF0000u);
+      } else {
+        const float4 v = r.v[u][c];
+        f[0] = v.x, f[1] = v.y, f[2] = v.z, f[3] = v.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t = fminf(fmaxf(rintf(f[e] * inv), -512.0f), 512.0f);
+        w[e] |= ((uint32_t)clip_i8((int)t + zp) & 0xFFu) << (8 * c);
+      }
+    }
+    *reinterpret_cast<uint4*>(patch + unit * 4) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// lane l + k of the same 16-lane row, as row_next, on int32
+template <int K>
+__device__ __forceinline__ int row_next_i(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x100 + K, 0xF, 0xF, false);
+}
+
+template <bool VEC, bool XBF, bool I8>
 __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemParams p) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsBytes];
   bf16_t* wl = reinterpret_cast<bf16_t*>(lds);                               // [64][wld]
-  float* sbias = reinterpret_cast<float*>(lds + kWeightBytes);               // [64]
+  const unsigned char* wl8 = lds;                                            // int8: [64][wld] bytes
+  float* sbias = reinterpret_cast<float*>(lds + kWeightBytes);               // [64] (int8: [64][2])
   uint2* patch = reinterpret_cast<uint2*>(lds + kWeightBytes + kBiasBytes);  // [kPR][kPC] cells
+  uint32_t* patch8 = reinterpret_cast<uint32_t*>(patch);                     // int8 cells
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
@@ -202,7 +253,9 @@ __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemPara
   const int lrow0 = wave * 2 * p.sph;
   int pbase[kRowsWave];
 #pragma unroll
-  for (int f = 0; f < kRowsWave; ++f) pbase[f] = (lrow0 + f) * p.sh * kPC + l16 * p.sw + 2 * g;
+  for (int f = 0; f < kRowsWave; ++f)
+    pbase[f] = I8 ? (lrow0 + f) * p.sh * kPC + l16 * p.sw + (g >> 1) * kPC + 4 * (g & 1)
+                  : (lrow0 + f) * p.sh * kPC + l16 * p.sw + 2 * g;
 
   // weights, bias and the first patch: every load is issued before the
   // first LDS write, and all are unconditional (buffer loads past the end
@@ -210,23 +263,25 @@ __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemPara
   // never come straight from a global load: the compiler's wait tracking
   // would then stall the loop on the patch loads in flight.
   {
-    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p.w), (short)0,
-                                                                         kK * p.wld * 2, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.w), (short)0,
+                                                                         kK * p.wld * (I8 ? 1 : 2), kBufferFlags);
     uint4 wv[kWChunks];
 #pragma unroll
     for (int i = 0; i < kWChunks; ++i)
       wv[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, (uint32_t)(tid + i * kThreads) * 16u, 0, 0));
-    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.bias), (short)0,
-                                                                         p.bias ? kBiasBytes : 0, kBufferFlags);
-    float4 b = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(br, tid < kK / 4 ? tid * 16u : kOOB, 0, 0));
+    constexpr int kBiasLoads = kK * (I8 ? 8 : 4) / 16;  // 16-byte loads of the bias (table)
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.bias), (short)0,
+                                                                         p.bias ? kBiasLoads * 16 : 0, kBufferFlags);
+    float4 b = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(br, tid < kBiasLoads ? tid * 16u : kOOB, 0, 0));
     PatchRegs<XBF> first;
     issue_patch(first, t);
     asm volatile("" : "+v"(b.x), "+v"(b.y), "+v"(b.z), "+v"(b.w));  // keeps the bias load ahead of the writes
     uint4* dst = reinterpret_cast<uint4*>(wl);
 #pragma unroll
     for (int i = 0; i < kWChunks; ++i) dst[tid + i * kThreads] = wv[i];
-    if (tid < kK / 4) reinterpret_cast<float4*>(sbias)[tid] = b;
-    store_patch<XBF>(first, patch, tid);
+    if (tid < kBiasLoads) reinterpret_cast<float4*>(sbias)[tid] = b;
+    if constexpr (I8) store_patch_i8<XBF>(first, patch8, tid, p.inv_scale, p.zx);
+    else store_patch<XBF>(first, patch, tid);
   }
   PatchRegs<XBF> pr;
   if (t + G < ntiles) issue_patch(pr, t + G);
@@ -237,6 +292,86 @@ __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemPara
     origin(t, n, ti, tj, cr0, cc0);
     const int off = col_off(cc0);
 
+    if constexpr (I8) {
+      // implicit GEMM on codes: the sums start at the folded bias
+      i32x4 acc[kRowsWave][4];
+      const int* sq = reinterpret_cast<const int*>(sbias);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int4 lo = *reinterpret_cast<const int4*>(sq + 2 * (j * 16 + 4 * g));
+        const int4 hi = *reinterpret_cast<const int4*>(sq + 2 * (j * 16 + 4 * g) + 4);
+#pragma unroll
+        for (int f = 0; f < kRowsWave; ++f) acc[f][j] = i32x4{lo.x, lo.z, hi.x, hi.z};
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        if (2 * m >= p.R) break;
+        i32x4 a[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          a[j] = *reinterpret_cast<const i32x4*>(wl8 + (j * 16 + l16) * p.wld + m * 64 + g * 16);
+#pragma unroll
+        for (int f = 0; f < kRowsWave; ++f) {
+          const uint32_t* c = patch8 + pbase[f] + off + 2 * m * kPC;  // four cells, 4-byte aligned
+          const i32x4 b = i32x4{(int)c[0], (int)c[1], (int)c[2], (int)c[3]};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[f][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[j], b, acc[f][j], 0, 0, 0);
+        }
+      }
+      lds_barrier();  // every wave is done with the patch
+      const int tn = t + G;
+      if (tn < ntiles) store_patch_i8<XBF>(pr, patch8, tid, p.inv_scale, p.zx);
+      if (tn + G < ntiles) issue_patch(pr, tn + G);
+      // conv positions outside the image never win the max
+      const bool colok = (unsigned)(cc0 + l16) < (unsigned)p.Q;
+#pragma unroll
+      for (int f = 0; f < kRowsWave; ++f) {
+        const bool ok = colok & ((unsigned)(cr0 + lrow0 + f) < (unsigned)p.P);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[f][j][e] = ok ? acc[f][j][e] : INT_MIN;
+      }
+      const bool lane_out = (l16 % p.spw == 0) & (l16 / p.spw < TW);
+      const int qo = tj * TW + l16 / p.spw;
+      const bool r1 = p.kph > 1, r2 = p.kph > 2, c1 = p.kpw > 1, c2 = p.kpw > 2;
+      int8_t* y8 = reinterpret_cast<int8_t*>(p.y);
+      auto pool = [&](auto sph_tag) {
+        constexpr int SPH = decltype(sph_tag)::value;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int po = ti * kTH + 2 * wave + q;
+          const bool st = lane_out & (po < p.PO) & (qo < p.QO);
+          int8_t* dst = y8 + (((size_t)n * p.PO + po) * p.QO + qo) * kK + 4 * g;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int4 lo = *reinterpret_cast<const int4*>(sq + 2 * (j * 16 + 4 * g));
+            const int4 hi = *reinterpret_cast<const int4*>(sq + 2 * (j * 16 + 4 * g) + 4);
+            const int fs[4] = {lo.y, lo.w, hi.y, hi.w};
+            uint32_t w = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              int v = acc[SPH * q][j][e];
+              v = max(v, r1 ? acc[SPH * q + 1][j][e] : INT_MIN);
+              v = max(v, r2 ? acc[SPH * q + 2][j][e] : INT_MIN);
+              const int h1 = row_next_i<1>(v), h2 = row_next_i<2>(v);
+              int h = max(v, c1 ? h1 : INT_MIN);
+              h = max(h, c2 ? h2 : INT_MIN);
+              const int code = min(max(p.zy + rescale(h, __int_as_float(fs[e])), p.lo), p.hi);
+              w |= ((uint32_t)code & 0xFFu) << (8 * e);
+            }
+            if (st) *reinterpret_cast<uint32_t*>(dst + j * 16) = w;
+          }
+        }
+      };
+      if (p.sph == 2) pool(std::integral_constant<int, 2>{});
+      else pool(std::integral_constant<int, 1>{});
+      if (tn >= ntiles) break;
+      lds_barrier();  // the next patch is in LDS
+      t = tn;
+      continue;
+    }
+    if constexpr (!I8) {
     // implicit GEMM.  Accumulators start at the bias of their channels, or
     // at -inf for conv positions outside the image (then they stay -inf:
     // the products added are finite), which excludes those positions from
@@ -305,7 +440,7 @@ __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemPara
       for (int q = 0; q < 2; ++q) {
         const int po = ti * kTH + 2 * wave + q;
         const bool st = lane_out & (po < p.PO) & (qo < p.QO);
-        bf16_t* dst = p.y + (((size_t)n * p.PO + po) * p.QO + qo) * kK + 4 * g;
+        bf16_t* dst = reinterpret_cast<bf16_t*>(p.y) + (((size_t)n * p.PO + po) * p.QO + qo) * kK + 4 * g;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           float m[4];
@@ -334,6 +469,7 @@ __global__ __launch_bounds__(kThreads, 2) void stem_conv_maxpool_kernel(StemPara
     if (tn >= ntiles) break;
     lds_barrier();  // the next patch is in LDS
     t = tn;
+    }
   }
 }
 
@@ -363,6 +499,8 @@ bool stem_supported(int C, int K, int R, int S, int sh, int sw, int kph, int kpw
 
 int stem_weight_ld(int R) { return R * 32 + 8; }
 
+int stem_weight_ld_i8(int R) { return (R + 1) / 2 * 64 + 16; }
+
 hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s) {
   // persistent grid: two workgroups per CU of the current device, never
   // more than the tiles (CU counts cached per device)
@@ -390,17 +528,23 @@ hipError_t launch_stem_conv_maxpool(const StemParams& p, hipStream_t s) {
   // vector segment loads need 4-aligned rows and an aligned base
   const size_t elem = p.x_bf16 ? 2 : 4;
   const bool vec = p.W % 4 == 0 && reinterpret_cast<uintptr_t>(p.x) % (4 * elem) == 0;
-  if (p.x_bf16) {
-    if (vec)
-      stem_conv_maxpool_kernel<true, true><<<(int)grid, kThreads, 0, s>>>(p);
-    else
-      stem_conv_maxpool_kernel<false, true><<<(int)grid, kThreads, 0, s>>>(p);
-  } else {
-    if (vec)
-      stem_conv_maxpool_kernel<true, false><<<(int)grid, kThreads, 0, s>>>(p);
-    else
-      stem_conv_maxpool_kernel<false, false><<<(int)grid, kThreads, 0, s>>>(p);
-  }
+  if (p.i8 && (p.wld % 16 != 0 || p.wld < (p.R + 1) / 2 * 64)) return hipErrorInvalidValue;
+  auto go = [&](auto i8_tag) {
+    constexpr bool Q = decltype(i8_tag)::value;
+    if (p.x_bf16) {
+      if (vec)
+        stem_conv_maxpool_kernel<true, true, Q><<<(int)grid, kThreads, 0, s>>>(p);
+      else
+        stem_conv_maxpool_kernel<false, true, Q><<<(int)grid, kThreads, 0, s>>>(p);
+    } else {
+      if (vec)
+        stem_conv_maxpool_kernel<true, false, Q><<<(int)grid, kThreads, 0, s>>>(p);
+      else
+        stem_conv_maxpool_kernel<false, false, Q><<<(int)grid, kThreads, 0, s>>>(p);
+    }
+  };
+  if (p.i8) go(std::true_type{});
+  else go(std::false_type{});
   return hipGetLastError();
 }
 

@@ -282,3 +282,43 @@ def test_int8_darknet53_small_full_compare():
         del os.environ["BYOC_FUSE_POST_ADD"]
     assert sum(1 for l in plain_launches if l["name"] == "add_i8") == 23
     assert np.array_equal(plain[0], got[0])
+
+
+STEM_I8_CASES = [
+    # name, (n, c, h, w), r, stride, pad, act, (pool size, stride, pad), input dtype, persistent workgroups
+    ("resnet_stem_224", (2, 3, 224, 224), 7, 2, 3, "relu", (3, 2, 1), "f32", 0),
+    ("resnet_stem_ragged", (2, 3, 45, 45), 7, 2, 3, "relu", (3, 2, 1), "f32", 0),
+    ("stem_bf16_in_c1", (1, 1, 32, 30), 7, 2, 3, "relu", (3, 2, 1), "bf16", 0),
+    ("stem_3x3_s1_pool2", (2, 4, 20, 21), 3, 1, 1, None, (2, 2, 0), "f32", 0),
+    ("stem_5x5_s2_pool3_s1", (1, 3, 24, 24), 5, 2, 2, "relu6", (3, 1, 1), "f32", 0),
+    ("resnet_stem_12_tiles_3_wgs", (3, 3, 64, 64), 7, 2, 3, "relu", (3, 2, 1), "f32", 3),
+    ("resnet_stem_ragged_2_wgs", (2, 3, 45, 45), 7, 2, 3, "relu", (3, 2, 1), "f32", 2),
+]
+
+
+@pytest.mark.parametrize("case", STEM_I8_CASES, ids=[c[0] for c in STEM_I8_CASES])
+def test_int8_fused_stem_exact(case, monkeypatch):
+    """The int8 stem (input codes formed in the kernel, conv, max pool) as
+    one launch equals the unfused quantize / conv / max-pool launches and the
+    int8 oracle bit for bit; with fewer persistent workgroups than tiles too."""
+    from paper_2105_03215_amd.workloads import GraphBuilder
+    name, shape, r, stride, pad, act, (ps, pst, ppad), dt, grid = case
+    announce("int8 stem " + name)
+    g = GraphBuilder("stem_i8_" + name, 2600 + STEM_I8_CASES.index(case))
+    x = g.input("x", list(shape), "uniform", dtype=dt)
+    y = g.conv(x, 64, r, stride=stride, pad=pad, act=act, name="conv")
+    p = g.max_pool(y, ps, pst, ppad, name="pool")
+    g.output(p)
+    wl = g.finish()
+    qg = oracle_calibrated_int8(wl.graph, wl.consts, [np.ascontiguousarray(a[:1]) for a in wl.inputs])
+    if grid:
+        monkeypatch.setenv("BYOC_STEM_GRID", str(grid))
+    fused, launches = _run(qg, wl.consts, wl.inputs)
+    names = [l["name"] for l in launches]
+    assert names == ["stem_conv_maxpool_i8", "dequantize_out"], names
+    monkeypatch.setenv("BYOC_FUSE_STEM", "0")
+    plain, pl = _run(qg, wl.consts, wl.inputs)
+    assert "stem_conv_maxpool_i8" not in [l["name"] for l in pl]
+    assert np.array_equal(fused[0], plain[0])
+    ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
+    assert np.array_equal(fused[0], ref.astype(np.float64))
