@@ -44,20 +44,40 @@
 // holds 4 consecutive output channels of one pixel; the epilogue (bias,
 // residual, activation, bf16 rounding, 16-byte stores through an LDS
 // staging tile) is the implicit-GEMM kernel's.
+//
+// int8 codes (I8): a 128-byte row holds 128 channels, the same two k-steps
+// of v_mfma_i32_16x16x64_i8 per row, exact int32 sums; the zero rows and
+// columns of the patch read as code 0, and the epilogue is the int8
+// implicit-GEMM kernel's (folded bias, border correction for the taps
+// outside the image, rescaling, residual, clamp).
 #include <algorithm>
+#include <type_traits>
 
 #include "lds_dma.h"
+#include "quant_epilogue.h"
 
 namespace byoc {
 namespace {
 
 using namespace dma;
 
-constexpr int kSlice = 64;  // channels per reduction slice (one 128-byte LDS row per pixel)
+constexpr int kSlice = 64;  // bf16 channels per reduction slice (one 128-byte LDS row per pixel)
 constexpr int kTaps = 9;
 
-template <int BM, int BN, int WM, int WN, int TPS, int NSW, int LP, int NPB>
-__global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
+__device__ __forceinline__ f32x4 mma(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+__device__ __forceinline__ i32x4 mma(uint4 a, uint4 b, i32x4 c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0,
+                                               0, 0);
+}
+
+template <int BM, int BN, int WM, int WN, int TPS, int NSW, int LP, int NPB, bool I8>
+__global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(QConvParams q) {
+  const ConvParams& p = q.g;
+  constexpr int ES = I8 ? 1 : 2;   // bytes per element
+  constexpr int CS = 128 / ES;     // channels per slice
+  using Acc = std::conditional_t<I8, i32x4, f32x4>;
   constexpr int kWaves = WM * WN;
   constexpr int kNT = 64 * kWaves;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
@@ -125,7 +145,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
       const int h = vr - n * HP - 1;
       const int w = col - 1;
       if ((unsigned)h < (unsigned)p.H && (unsigned)w < (unsigned)p.W)
-        off = (uint32_t)((((n * p.H + h) * p.W + w) * p.Cp + ch * 8) * 2);
+        off = (uint32_t)(((n * p.H + h) * p.W + w) * p.Cp * ES + ch * 16);
     }
     poff[i] = off;
   }
@@ -153,9 +173,9 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   const i32x4 wr = buffer_rsrc(p.w, p.w_bytes);
   uint32_t wvoff[BR];  // byte offset of this thread's weight rows and chunk
 #pragma unroll
-  for (int i = 0; i < BR; ++i) wvoff[i] = (uint32_t)(((n0 + (tid >> 3) + i * kRowsPerPass) * p.Kgp + cv * 8) * 2);
+  for (int i = 0; i < BR; ++i) wvoff[i] = (uint32_t)((n0 + (tid >> 3) + i * kRowsPerPass) * p.Kgp * ES + cv * 16);
 
-  const int nslices = p.Cp / kSlice;
+  const int nslices = p.Cp / CS;
   const int nst = SPS * nslices;  // weight stages
   // next weight stage to issue: its index, stage within the slice, slice and ring slot
   int wg = 0, wt = 0, wc = 0, wslot = 0;
@@ -164,7 +184,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
     const bool live = wg < nst;
 #pragma unroll
     for (int u = 0; u < TPS; ++u) {
-      const uint32_t col = (uint32_t)((wt * TPS + u) * p.Cp + wc * kSlice) * 2u;
+      const uint32_t col = (uint32_t)((wt * TPS + u) * p.Cp + wc * CS) * ES;
 #pragma unroll
       for (int i = 0; i < BR; ++i)
         lds_fill16(wr,
@@ -181,41 +201,40 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   auto issue_patch = [&](int c, int buf) {
     uint4* dst = patch + buf * PSTAGE;
     const bool live = c < nslices;
-    const uint32_t add = (uint32_t)c * (kSlice * 2);
+    const uint32_t add = (uint32_t)c * 128u;
 #pragma unroll
     for (int i = 0; i < LP; ++i)
       lds_fill16(xr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (i * kWaves + wave) * 64)),
                  live ? poff[i] + add : kOOB);
   };
 
-  f32x4 acc[TN][TM];
+  Acc acc[TN][TM];
 #pragma unroll
   for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
-  // One tap: 2 k-steps of the 16x16x32 MFMA.  Lane l reads 16 bytes (8
-  // consecutive channels) of row l % 16 at chunk (k-step, l / 16).
+  // One tap: 2 k-steps of the MFMA (64 bytes each).  Lane l reads 16 bytes
+  // of row l % 16 at chunk (k-step, l / 16).
   auto compute = [&](const uint4* sP, const uint4* sW, int toff, int tkey) {
 #pragma unroll
-    for (int ks = 0; ks < kSlice / 32; ++ks) {
+    for (int ks = 0; ks < 2; ++ks) {
       const int chunk = ks * 4 + (lane >> 4);
-      bf16x8 af[TN], bfr[TM];
+      uint4 af[TN], bfr[TM];
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
         const int row = wn * WTN + i * 16 + (lane & 15);
-        af[i] = as_bf16x8(sW[row * 8 + (chunk ^ (row & 7))]);
+        af[i] = sW[row * 8 + (chunk ^ (row & 7))];
       }
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
         const int pp = pbase[j] + toff;
-        bfr[j] = as_bf16x8(sP[pp * 8 + (chunk ^ ((cbase[j] + tkey) & 7))]);
+        bfr[j] = sP[pp * 8 + (chunk ^ ((cbase[j] + tkey) & 7))];
       }
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TM; ++j) acc[i][j] = mma(af[i], bfr[j], acc[i][j]);
     }
   };
 
@@ -226,7 +245,8 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   constexpr int TPP = kEC / 8;  // threads per pixel
   constexpr int EPV = (BM * TPP + kNT - 1) / kNT;  // pixels per thread per pass
   const int ec8 = (tid % TPP) * 8;
-  uint4 resv[NPASS][EPV];
+  using RT = std::conditional_t<I8, uint2, uint4>;  // the residual of 8 channels
+  RT resv[NPASS][EPV];
   {
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<bf16_t*>(p.res), (short)0, p.res ? p.res_bytes : 0, kBufferFlags);
@@ -234,20 +254,30 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
     for (int pass = 0; pass < NPASS; ++pass) {
       const int k = n0 + pass * kEC + ec8;
 #pragma unroll
-      for (int q = 0; q < EPV; ++q) {
-        const int px = (tid + q * kNT) / TPP;
+      for (int e = 0; e < EPV; ++e) {
+        const int px = (tid + e * kNT) / TPP;
         const int m = m0 + px;
-        const uint32_t off = (px < BM && m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) * 2u : kOOB;
-        resv[pass][q] = p.res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0))
-                              : make_uint4(0u, 0u, 0u, 0u);
+        const uint32_t off = (px < BM && m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) * ES : kOOB;
+        if constexpr (I8)
+          resv[pass][e] = p.res ? __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0))
+                                : make_uint2(0u, 0u);
+        else
+          resv[pass][e] = p.res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0))
+                                : make_uint4(0u, 0u, 0u, 0u);
       }
     }
   }
-  // the tile's bias, straight into LDS (zeros without a bias)
+  // the tile's bias (codes: {bias, factor} table), straight into LDS (zeros without a bias)
   if (tid < 64) {
-    const i32x4 br = buffer_rsrc(p.bias, p.bias ? ((p.Kp + 255) / 256) * 256 * 4 : 0);
-    const uint32_t off = lane < BN / 4 ? (uint32_t)(n0 + 4 * lane) * 4u : kOOB;
-    lds_fill16(br, __builtin_amdgcn_readfirstlane(lds_addr(sbias)), off);
+    if constexpr (I8) {
+      const i32x4 br = buffer_rsrc(q.qch, ((p.Kp + 255) / 256) * 256 * 8);
+      const uint32_t off = lane < BN / 2 ? (uint32_t)(n0 + 2 * lane) * 8u : kOOB;
+      lds_fill16(br, __builtin_amdgcn_readfirstlane(lds_addr(sbias)), off);
+    } else {
+      const i32x4 br = buffer_rsrc(p.bias, p.bias ? ((p.Kp + 255) / 256) * 256 * 4 : 0);
+      const uint32_t off = lane < BN / 4 ? (uint32_t)(n0 + 4 * lane) * 4u : kOOB;
+      lds_fill16(br, __builtin_amdgcn_readfirstlane(lds_addr(sbias)), off);
+    }
   }
   issue_patch(0, 0);
   static_for<0, NSW - 1>([&](auto) { issue_w(); });
@@ -282,6 +312,37 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
   // activation and stores 16 bytes.
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= (NPB * PSTAGE + NSW * WSTAGE) * 16, "staging tile");
+  if constexpr (I8) {
+    int* stage = reinterpret_cast<int*>(lds);
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      if (pass > 0) lds_barrier();
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int ch = wn * WTN + i * 16 + 4 * (lane >> 4) - pass * kEC;
+        if (ch < 0 || ch >= kEC) continue;
+#pragma unroll
+        for (int j = 0; j < TM; ++j) {
+          const int px = wm * WTM + j * 16 + (lane & 15);
+          *(i32x4*)(stage + px * kLd + ch) = acc[i][j];
+        }
+      }
+      lds_barrier();
+      const int k = n0 + pass * kEC + ec8;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        const int px = (tid + e * kNT) / TPP;
+        const int m = m0 + px;
+        if (px >= BM || m >= p.M || k >= p.Kp) continue;
+        const int* st = stage + px * kLd + ec8;
+        const int4 lo4 = *(const int4*)st, hi4 = *(const int4*)(st + 4);
+        int a[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
+        *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) =
+            finish8_i8(a, reinterpret_cast<const int2*>(sbias) + pass * kEC + ec8, resv[pass][e], q, m, k);
+      }
+    }
+    return;
+  } else {
   float* stage = reinterpret_cast<float*>(lds);
   const ActClamp ac = act_clamp_of(p.act, p.alpha);
   auto epilogue = [&](auto mode_tag) {
@@ -303,8 +364,8 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
       lds_barrier();
       const int k = n0 + pass * kEC + ec8;
 #pragma unroll
-      for (int q = 0; q < EPV; ++q) {
-        const int px = (tid + q * kNT) / TPP;
+      for (int e = 0; e < EPV; ++e) {
+        const int px = (tid + e * kNT) / TPP;
         const int m = m0 + px;
         if (px >= BM || m >= p.M || k >= p.Kp) continue;
         const float* st0 = stage + px * kLd + ec8;
@@ -312,7 +373,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
         const float4 hi = *(const float4*)(st0 + 4);
         float f[8], rv[8];
         const float4 b0 = sbias[(pass * kEC + ec8) / 4], b1 = sbias[(pass * kEC + ec8) / 4 + 1];
-        unpack8(resv[pass][q], rv);
+        unpack8(resv[pass][e], rv);
         f[0] = lo.x + b0.x; f[1] = lo.y + b0.y; f[2] = lo.z + b0.z; f[3] = lo.w + b0.w;
         f[4] = hi.x + b1.x; f[5] = hi.y + b1.y; f[6] = hi.z + b1.z; f[7] = hi.w + b1.w;
 #pragma unroll
@@ -329,6 +390,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_halo_kernel(ConvParams p) {
     epilogue(std::integral_constant<int, 0>{});
   else
     epilogue(std::integral_constant<int, 2>{});
+  }
 }
 
 // A weight-ring setting `stages` of the launchers: 2 or 3 are rings of
@@ -358,8 +420,8 @@ constexpr int kLPs[] = {4, 5, 6, 8};
 
 // Smallest patch capacity (loads per thread) that holds every tile's patch
 // and fits the LDS with `nsw` weight stages; 0 if none.
-int choose_lp(const ConvParams& p, int bm, int bn, int stages, int* npb) {
-  *npb = p.Cp / kSlice > 1 ? 2 : 1;
+int choose_lp(const ConvParams& p, int bm, int bn, int stages, int* npb, int cs) {
+  *npb = p.Cp / cs > 1 ? 2 : 1;
   const int need = max_patch_pixels(p, bm);
   for (int lp : kLPs)
     if (lp * kHaloWaves * 8 >= need &&
@@ -368,60 +430,73 @@ int choose_lp(const ConvParams& p, int bm, int bn, int stages, int* npb) {
   return 0;
 }
 
-bool shape_ok(const ConvParams& p) {
+bool shape_ok(const ConvParams& p, int cs) {
   return p.R == 3 && p.S == 3 && p.sh == 1 && p.sw == 1 && p.pt == 1 && p.pl == 1 && p.P == p.H &&
-         p.Q == p.W && p.Cp % kSlice == 0 && p.splits == 1 && p.Kg == 9 * p.Cp;
+         p.Q == p.W && p.Cp % cs == 0 && p.splits == 1 && p.Kg == 9 * p.Cp;
 }
 
-template <int BM, int BN, int WM, int WN, int TPS, int NSW, int LP, int NPB>
-hipError_t launch_one(const ConvParams& p_in, hipStream_t s) {
+template <int BM, int BN, int WM, int WN, int TPS, int NSW, int LP, int NPB, bool I8>
+hipError_t launch_one(const QConvParams& q_in, hipStream_t s) {
   if constexpr (halo_lds(BN, TPS, NSW, LP, NPB, WM * WN) > kLdsLimit) {
     return hipErrorInvalidValue;
   } else {
-    ConvParams p = p_in;
+    QConvParams q = q_in;
+    ConvParams& p = q.g;
     p.mg_wp = magic40(p.W + 2);
     p.mg_hp = magic40(p.H + 2);
     const int blocks = placed_blocks(p, BM, BN);
-    conv_halo_kernel<BM, BN, WM, WN, TPS, NSW, LP, NPB><<<blocks, 64 * WM * WN, 0, s>>>(p);
+    conv_halo_kernel<BM, BN, WM, WN, TPS, NSW, LP, NPB, I8><<<blocks, 64 * WM * WN, 0, s>>>(q);
     return hipGetLastError();
   }
 }
 
-template <int STAGES>
-hipError_t launch_stages(const ConvParams& p, int lp, int npb, hipStream_t s) {
+template <int STAGES, bool I8>
+hipError_t launch_stages(const QConvParams& q, int lp, int npb, hipStream_t s) {
   constexpr int T = taps_per_stage(STAGES);
   if (npb == 2) {
-    if (lp == 4) return launch_one<128, 64, 4, 2, T, STAGES, 4, 2>(p, s);
-    if (lp == 5) return launch_one<128, 64, 4, 2, T, STAGES, 5, 2>(p, s);
-    if (lp == 6) return launch_one<128, 64, 4, 2, T, STAGES, 6, 2>(p, s);
+    if (lp == 4) return launch_one<128, 64, 4, 2, T, STAGES, 4, 2, I8>(q, s);
+    if (lp == 5) return launch_one<128, 64, 4, 2, T, STAGES, 5, 2, I8>(q, s);
+    if (lp == 6) return launch_one<128, 64, 4, 2, T, STAGES, 6, 2, I8>(q, s);
     return hipErrorInvalidValue;
   }
-  if (lp == 4) return launch_one<128, 64, 4, 2, T, STAGES, 4, 1>(p, s);
-  if (lp == 5) return launch_one<128, 64, 4, 2, T, STAGES, 5, 1>(p, s);
-  if (lp == 6) return launch_one<128, 64, 4, 2, T, STAGES, 6, 1>(p, s);
-  if (lp == 8) return launch_one<128, 64, 4, 2, T, STAGES, 8, 1>(p, s);
+  if (lp == 4) return launch_one<128, 64, 4, 2, T, STAGES, 4, 1, I8>(q, s);
+  if (lp == 5) return launch_one<128, 64, 4, 2, T, STAGES, 5, 1, I8>(q, s);
+  if (lp == 6) return launch_one<128, 64, 4, 2, T, STAGES, 6, 1, I8>(q, s);
+  if (lp == 8) return launch_one<128, 64, 4, 2, T, STAGES, 8, 1, I8>(q, s);
+  return hipErrorInvalidValue;
+}
+
+template <bool I8>
+hipError_t launch_any(const QConvParams& q, int bm, int bn, int stages, int lp, int npb, hipStream_t s) {
+  if (bm != 128 || bn != 64 || !shape_ok(q.g, I8 ? 128 : kSlice)) return hipErrorInvalidValue;
+  if (stages == 2) return launch_stages<2, I8>(q, lp, npb, s);
+  if (stages == 3) return launch_stages<3, I8>(q, lp, npb, s);
+  if (stages == 4) return launch_stages<4, I8>(q, lp, npb, s);
+  if (stages == 6) return launch_stages<6, I8>(q, lp, npb, s);
+  if (stages == 8) return launch_stages<8, I8>(q, lp, npb, s);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb) {
-  if (bm != 128 || bn != 64 || !shape_ok(p)) return false;
+bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb, bool i8) {
+  const int cs = i8 ? 128 : kSlice;
+  if (bm != 128 || bn != 64 || !shape_ok(p, cs)) return false;
   if (stages != 2 && stages != 3 && stages != 4 && stages != 6 && stages != 8) return false;
   // index math: patch offsets and pixel bases stay within int32
   if ((int64_t)p.N * (p.H + 2) * (p.W + 2) >= (int64_t(1) << 30)) return false;
-  *lp = choose_lp(p, bm, bn, stages, npb);
+  *lp = choose_lp(p, bm, bn, stages, npb, cs);
   return *lp > 0;
 }
 
 hipError_t launch_conv_halo(const ConvParams& p, int bm, int bn, int stages, int lp, int npb, hipStream_t s) {
-  if (bm != 128 || bn != 64 || !shape_ok(p)) return hipErrorInvalidValue;
-  if (stages == 2) return launch_stages<2>(p, lp, npb, s);
-  if (stages == 3) return launch_stages<3>(p, lp, npb, s);
-  if (stages == 4) return launch_stages<4>(p, lp, npb, s);
-  if (stages == 6) return launch_stages<6>(p, lp, npb, s);
-  if (stages == 8) return launch_stages<8>(p, lp, npb, s);
-  return hipErrorInvalidValue;
+  QConvParams q{};
+  q.g = p;
+  return launch_any<false>(q, bm, bn, stages, lp, npb, s);
+}
+
+hipError_t launch_conv_halo_i8(const QConvParams& q, int bm, int bn, int stages, int lp, int npb, hipStream_t s) {
+  return launch_any<true>(q, bm, bn, stages, lp, npb, s);
 }
 
 }  // namespace byoc

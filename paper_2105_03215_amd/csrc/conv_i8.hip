@@ -23,6 +23,7 @@
 // the residual's own rescaling, the activation clamp in code space (which
 // also clips to int8), one 8-byte store.
 #include "lds_dma.h"
+#include "quant_epilogue.h"
 
 namespace byoc {
 namespace {
@@ -247,7 +248,6 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
   int* stage = reinterpret_cast<int*>(ring);
-  const int RS = p.R * p.S;
 #pragma unroll
   for (int pass = 0; pass < NPASS; ++pass) {
     if (pass > 0) lds_barrier();
@@ -271,45 +271,8 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
       const int* st = stage + px * kLd + ec8;
       const int4 lo4 = *(const int4*)st, hi4 = *(const int4*)(st + 4);
       int a[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
-      const int2* qc = sq + pass * kEC + ec8;
-#pragma unroll
-      for (int c8 = 0; c8 < 8; ++c8) a[c8] += qc[c8].x;
-      if (q.wtap) {
-        // window of this pixel: taps outside the image get Z_x * their weight sums back
-        const int n = mdiv(m, p.mg_pq);
-        const int pq = m - n * PQ;
-        const int pp = mdiv(pq, p.mg_q);
-        const int qq = pq - pp * p.Q;
-        const int ih0 = pp * p.sh - p.pt, iw0 = qq * p.sw - p.pl;
-        const bool inside = ih0 >= 0 && iw0 >= 0 && ih0 + p.R <= p.H && iw0 + p.S <= p.W;
-        if (!inside) {
-          int corr[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-          for (int rr = 0; rr < p.R; ++rr)
-            for (int ss = 0; ss < p.S; ++ss) {
-              const int ih = ih0 + rr, iw = iw0 + ss;
-              if ((unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W) continue;
-              const int* wt = q.wtap + (size_t)k * RS + rr * p.S + ss;
-#pragma unroll
-              for (int c8 = 0; c8 < 8; ++c8) corr[c8] += wt[c8 * RS];
-            }
-#pragma unroll
-          for (int c8 = 0; c8 < 8; ++c8) a[c8] += q.zx * corr[c8];
-        }
-      }
-      const uint2 rv = resv[pass][e];
-      const uint32_t rw[2] = {rv.x, rv.y};
-      uint32_t out[2] = {0u, 0u};
-#pragma unroll
-      for (int c8 = 0; c8 < 8; ++c8) {
-        int v = q.zy + rescale(a[c8], __int_as_float(qc[c8].y));
-        const int rc = (int)(int8_t)(rw[c8 >> 2] >> (8 * (c8 & 3)));
-        if (p.res && !q.post) v += rescale(rc - q.zr, q.mr);
-        if (q.leaky) v = leaky_code(v, q.zy, q.slope);
-        v = min(max(v, q.lo), q.hi);
-        if (q.post) v = clip_i8(q.pz + rescale(v - q.zy, q.pm) + rescale(rc - q.zr, q.mr));
-        out[c8 >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (c8 & 3));
-      }
-      *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) = make_uint2(out[0], out[1]);
+      *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) =
+          finish8_i8(a, sq + pass * kEC + ec8, resv[pass][e], q, m, k);
     }
   }
 }

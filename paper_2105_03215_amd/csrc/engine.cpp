@@ -189,8 +189,12 @@ int choose_xcd_split(const ConvParams& p, const ConvTile& t) {
 }
 
 void name_conv_i8(Launch& L) {
-  std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_%dx%d_s%d_w%d", L.tile.bm, L.tile.bn, L.tile.stages,
-                L.tile.threads / 64);
+  if (L.tile.halo)
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_halo_%dx%d_s%d_lp%d_pb%d", L.tile.bm, L.tile.bn,
+                  L.tile.stages, L.tile.lp, L.tile.npb);
+  else
+    std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_%dx%d_s%d_w%d", L.tile.bm, L.tile.bn, L.tile.stages,
+                  L.tile.threads / 64);
 }
 
 void name_conv(Launch& L) {
@@ -1574,6 +1578,25 @@ void Planner::plan_node_i8(int ni) {
       if (std::sscanf(te, "%dx%ds%dw%d", &bm, &bn, &ns, &nw) >= 3 && conv_i8_tile_supported(bm, bn, ns, 64 * nw))
         t.bm = bm, t.bn = bn, t.stages = ns, t.threads = 64 * nw;
     }
+    // 3x3 stride-1 convs with at least 256 input channels and enough 128x64
+    // tiles run on the windowed kernel (input window staged in LDS once per
+    // 128-channel slice; the same codes), the rule of the bf16 convs;
+    // BYOC_CONV_HALO=1 takes it wherever the shape allows, =0 never.
+    {
+      // BYOC_I8_TILE=h<stages> forces it with that weight ring depth.
+      const char* he = std::getenv("BYOC_CONV_HALO");
+      const char* te = std::getenv("BYOC_I8_TILE");
+      const int64_t halo_tiles = ((int64_t)(p.M + 127) / 128) * ((Kp + 63) / 64);
+      int ns = kHaloStages;
+      bool want = he ? he[0] == '1' : (Cp >= 256 && halo_tiles >= 160);
+      if (te) want = te[0] == 'h' && std::sscanf(te + 1, "%d", &ns) == 1;
+      int lp = 0, npb = 0;
+      if (!im2col && want && conv_halo_plan(p, 128, 64, ns, &lp, &npb, true)) {
+        t = ConvTile{};
+        t.bm = 128, t.bn = 64, t.stages = ns, t.threads = 512;
+        t.halo = 1, t.lp = lp, t.npb = npb;
+      }
+    }
     p.xcd_py = choose_xcd_split(p, t);
     L.tile_default = t;
     L.op = Launch::ConvI8;
@@ -1803,6 +1826,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       q.g.y = (bf16_t*)c.ptr(L.y);
       q.qch = (const int32_t*)c.ptr(L.bias);
       q.wtap = (const int32_t*)c.ptr(L.other);
+      if (L.tile.halo) return launch_conv_halo_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.lp, L.tile.npb, c.s);
       return launch_conv_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, c.s);
     }
     case Launch::MaxPoolI8:
@@ -2203,6 +2227,15 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
 // codes, do not depend on the tiling)
 std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
   std::vector<ConvTile> c{L.tile_default};
+  // the windowed 3x3 kernel, every weight ring depth (int32 sums: every
+  // variant gives the same codes)
+  for (int ns : {2, 3, 4, 6, 8}) {
+    ConvTile t = ConvTile{};
+    t.bm = 128, t.bn = 64, t.stages = ns, t.threads = 512, t.halo = 1;
+    if (!conv_halo_plan(L.qc.g, 128, 64, ns, &t.lp, &t.npb, true)) continue;
+    if (L.tile_default.halo && ns == L.tile_default.stages) continue;
+    c.push_back(t);
+  }
   for (int nt : {256, 512})
     for (auto bmn : {std::pair<int, int>{128, 128}, {128, 64}, {64, 128}, {64, 64}, {32, 64}})
       for (int ns : {2, 3, 4}) {

@@ -80,7 +80,7 @@ hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int 
 // thread, lp) and the number of patch buffers (npb) for a tiling; the
 // launcher takes them as planned.  `stages` is the weight ring: 2 or 3
 // stages of three taps (one kernel row), or 4, 6 or 8 stages of one tap.
-bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb);
+bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb, bool i8 = false);
 hipError_t launch_conv_halo(const ConvParams& p, int bm, int bn, int stages, int lp, int npb, hipStream_t s);
 // Fused stem: conv (C <= 4 NCHW input channels, 64 output channels) + bias
 // + activation followed by max pooling; output NHWC bf16 with 64 channels.
@@ -258,6 +258,9 @@ struct QConvParams {
 // 128x128, 128x64, 64x128; 2 to 4 ring stages.
 bool conv_i8_tile_supported(int bm, int bn, int stages, int threads);
 hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s);
+// The windowed 3x3 kernel on codes (conv_halo_plan(..., i8 = true) sizes it):
+// 128 channels per slice; the same codes as launch_conv_i8.
+hipError_t launch_conv_halo_i8(const QConvParams& q, int bm, int bn, int stages, int lp, int npb, hipStream_t s);
 
 // Boundary Q: float NCHW (or [M, K] as N = M, C = K, H = W = 1) ->
 // NHWC int8 codes clip(rint(x * inv_scale) + zp) (float32 arithmetic);

@@ -322,3 +322,30 @@ def test_int8_fused_stem_exact(case, monkeypatch):
     assert np.array_equal(fused[0], plain[0])
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
     assert np.array_equal(fused[0], ref.astype(np.float64))
+
+
+HALO_I8_CASES = [
+    # n, c, h, w, k, r, stride, pad, zx, act, residual: 3x3 stride 1, channels a multiple of 128
+    (2, 256, 14, 14, 256, 3, 1, 1, -128, "relu", False),   # ResNet stage-3 shape, border correction
+    (2, 128, 14, 13, 192, 3, 1, 1, 37, "relu", True),      # one slice, residual, ragged width
+    (3, 256, 7, 7, 136, 3, 1, 1, 5, "leaky", True),        # tiny images, ragged output channels
+    (1, 384, 9, 11, 64, 3, 1, 1, 0, None, False),          # three slices (two patch buffers), Z_x = 0
+]
+
+
+@pytest.mark.parametrize("case", HALO_I8_CASES, ids=[str(i) for i in range(len(HALO_I8_CASES))])
+def test_int8_halo_conv_exact(case, monkeypatch):
+    """The windowed 3x3 kernel on codes (input window staged once per
+    128-channel slice) equals the int8 oracle bit for bit, at every weight
+    ring depth, with the zero rows / columns of its patch corrected at the
+    border like the implicit-GEMM kernel's."""
+    n, c, h, w, k, r, stride, pad, zx, act, residual = case
+    announce("int8 halo conv %s" % (case,))
+    g, consts, inputs = _conv_graph(n, c, h, w, k, r, stride, pad, zx, act, residual, seed=40 + len(str(case)))
+    ref = OQ.run_quantized_graph(g, consts, inputs)[0]
+    for ns in (2, 3, 4, 6, 8):
+        monkeypatch.setenv("BYOC_I8_TILE", "h%d" % ns)
+        got, launches = _run(g, consts, inputs)
+        name = [l["name"] for l in launches if l["kind"] == "conv_i8"][0]
+        assert name.startswith("conv_i8_halo_128x64_s%d_" % ns), name
+        assert np.array_equal(got[0], ref.astype(np.float64)), ns
