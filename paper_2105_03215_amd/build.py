@@ -15,7 +15,7 @@ OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbyoc.so")
 ROOT = os.path.dirname(PKG)
 
-SOURCES = ["json.cpp", "graph.cpp", "capi.cpp", "engine.cpp", "conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "bottleneck.hip", "stem.hip", "dense_rows.hip", "conv_f32.hip",
+SOURCES = ["json.cpp", "graph.cpp", "capi.cpp", "engine.cpp", "conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "bottleneck.hip", "ir_block.hip", "stem.hip", "dense_rows.hip", "conv_f32.hip",
            "vector_ops.hip", "conv_i8.hip", "quant.hip", "static_scratch.hip"]
 
 # -packed-fp32-ops: keep the compiler from emitting packed fp32 ALU ops.

@@ -32,7 +32,7 @@ constexpr int kKPad = 64;     // packed reduction length is padded to this (the 
 constexpr int kHaloStages = 3;  // halo kernel weight ring: 3 stages of one kernel row (built-in choice)
 
 struct PackJob {
-  enum Kind { ConvW, DwW, Vec, Copy, StemW, Host } kind;  // Host: copy blob n, built on the host
+  enum Kind { ConvW, DwW, DwW32, Vec, Copy, StemW, Host } kind;  // Host: copy blob n, built on the host
   int cidx = -1;       // constant index
   int64_t dst = 0;     // byte offset in the weights region
   int K = 0, Cg = 0, R = 0, S = 0, Cp = 0, Kgp = 0, rows = 0;
@@ -230,6 +230,10 @@ struct Planner {
   // its projection node (-1: none), and the nodes planned with it
   std::vector<int> block_mid, block_proj;
   std::vector<bool> in_block;
+  // fused inverted-residual blocks: 1x1 project node -> its depthwise node
+  // (-1: none) and its expand node (-1: none), and the nodes planned with it
+  std::vector<int> ir_dw, ir_exp;
+  std::vector<bool> in_ir;
 
   bool i8;                                  // partially quantized (int8) graph
   const byoc_const* consts = nullptr;       // host constants (int8 weights are quantized on the host)
@@ -300,6 +304,8 @@ struct Planner {
   void find_concat_aliases();
   void find_blocks();
   void plan_block(int ci);
+  void find_ir_blocks();
+  void plan_ir(int ci);
   void plan_block_i8(int ci);
   Ref slice(int vcat, int channel) const {  // channel slice of a concatenation's buffer
     Ref r = loc[vcat];
@@ -681,6 +687,160 @@ void Planner::plan_block(int ci) {
   e->launches.push_back(L);
 }
 
+// MobileNetV2 inverted-residual blocks: [x -> 1x1 conv (+bias, act) ->]
+// depthwise 3x3 pad 1 stride 1 or 2 (+bias, act) -> 1x1 conv (+bias, act)
+// [+ x], each intermediate read only by the next composite, of channel
+// counts the fused kernel is compiled for, run as one launch when the tiling
+// gives at least one workgroup per CU (256).  BYOC_FUSE_IR=0 keeps the
+// separate launches everywhere, =1 fuses every supported block.
+void Planner::find_ir_blocks() {
+  ir_dw.assign(g.nodes.size(), -1);
+  ir_exp.assign(g.nodes.size(), -1);
+  in_ir.assign(g.nodes.size(), false);
+  const char* env = std::getenv("BYOC_FUSE_IR");
+  if (!bf16 || (env && env[0] == '0')) return;
+  const bool always = env && env[0] == '1';
+  std::vector<int> uses(g.values.size(), 0);
+  for (const Node& n : g.nodes) {
+    for (int a : {n.data, n.residual, n.other})
+      if (a >= 0) ++uses[a];
+    if (n.op == OpKind::Concat)
+      for (size_t k = 1; k < n.cat.size(); ++k) ++uses[n.cat[k]];
+  }
+  for (const IoDesc& o : g.outputs) uses[o.value] += 2;
+  auto clamp_act = [](const Node& n) { return n.act != Act::Gelu && n.act != Act::Leaky; };
+  auto conv1x1 = [&](const Node& n) {
+    if (n.op != OpKind::Conv || n.depthwise || n.groups != 1 || !clamp_act(n)) return false;
+    const auto& ws = g.values[n.weight].shape;
+    return ws[2] == 1 && ws[3] == 1 && n.stride[0] == 1 && n.stride[1] == 1 && n.pad[0] == 0 && n.pad[1] == 0 &&
+           n.pad[2] == 0 && n.pad[3] == 0;
+  };
+  auto elsewhere = [&](int ni) {
+    return post_add[ni] >= 0 || post_conv[ni] >= 0 || stem_pool[ni] >= 0 || stem_conv[ni] >= 0 || in_block[ni] ||
+           block_mid[ni] >= 0 || alias_of[g.nodes[ni].out] >= 0;
+  };
+  for (size_t ci = 0; ci < g.nodes.size(); ++ci) {
+    const Node& c = g.nodes[ci];
+    if (!conv1x1(c) || elsewhere((int)ci)) continue;
+    const Value& vd = g.values[c.data];
+    if (vd.source != Value::Node || uses[c.data] != 1) continue;
+    const int di = vd.index;
+    const Node& d = g.nodes[di];
+    if (d.op != OpKind::Conv || !d.depthwise || !clamp_act(d) || d.residual >= 0 || elsewhere(di)) continue;
+    const auto& dws = g.values[d.weight].shape;
+    const int S = d.stride[0];
+    if (dws[2] != 3 || dws[3] != 3 || d.stride[1] != S || (S != 1 && S != 2) || d.pad[0] != 1 || d.pad[1] != 1 ||
+        d.pad[2] != 1 || d.pad[3] != 1)
+      continue;
+    // the expand conv, when the depthwise input is a 1x1 conv read only here
+    int ai = -1, x = d.data;
+    const Value& ve = g.values[d.data];
+    if (ve.source == Value::Node && uses[d.data] == 1) {
+      const int e = ve.index;
+      const Node& a = g.nodes[e];
+      if (conv1x1(a) && a.residual < 0 && !elsewhere(e)) {
+        ai = e;
+        x = a.data;
+      }
+    }
+    const auto& xs = g.values[x].shape;
+    const auto& es = g.values[d.data].shape;
+    const auto& ys = g.values[c.out].shape;
+    if (xs.size() != 4 || es.size() != 4 || ys.size() != 4) continue;
+    const int CIN = (int)xs[1], F = (int)es[1], COUT = (int)ys[1];
+    if (ai < 0 && F != CIN) continue;
+    if (ai >= 0 && F == CIN) continue;  // (the kind is told apart by F != CIN)
+    if (c.residual >= 0 && (c.residual != x || S != 1 || CIN != COUT)) continue;
+    const int nv = ir_block_variants(CIN, F, COUT, S);
+    if (nv <= 0) continue;
+    int most = 0;
+    for (int v = 0; v < nv; ++v) most = std::max(most, ir_block_tiles(CIN, F, COUT, S, v, (int)ys[0], (int)ys[2], (int)ys[3]));
+    if (!always && most < 256) continue;
+    if (xs[0] * xs[2] * xs[3] * std::max(std::max(CIN, F), COUT) * 2 >= (int64_t(1) << 31)) continue;
+    ir_dw[ci] = di;
+    ir_exp[ci] = ai;
+    in_ir[di] = true;
+    if (ai >= 0) in_ir[ai] = true;
+  }
+}
+
+void Planner::plan_ir(int ci) {
+  const Node& c = g.nodes[ci];
+  const Node& d = g.nodes[ir_dw[ci]];
+  const int ai = ir_exp[ci];
+  const int x = ai >= 0 ? g.nodes[ai].data : d.data;
+  const auto& xs = g.values[x].shape;
+  const auto& ys = g.values[c.out].shape;
+  Launch L;
+  L.op = Launch::IrBlock;
+  L.info.kind = BYOC_K_CONV_MFMA;
+  L.info.node = ci;
+  L.x = loc[x];
+  L.res = loc[x];
+  L.y = loc[c.out];
+  IrParams& p = L.ir;
+  p.N = (int)xs[0], p.H = (int)xs[2], p.W = (int)xs[3], p.P = (int)ys[2], p.Q = (int)ys[3], p.S = d.stride[0];
+  p.CIN = cp[x], p.F = cp[d.data], p.COUT = cp[c.out];
+  int64_t wbytes = 0;
+  // a 1x1 conv's packed weights and padded bias, as the implicit-GEMM kernel has them
+  auto pack = [&](const Node& n, Ref* w, Ref* bias, int* ld, int* w_bytes, int* b_bytes) {
+    const auto& ws = g.values[n.weight].shape;
+    const int K = (int)ws[0], Cg = (int)ws[1];
+    const int Cp = cp[n.data];
+    const int rows = (int)rup(K, kRowPad);
+    const int Kgp = (int)rup(Cp, kKPad);
+    const int wc = g.values[n.weight].index;
+    const int bc = n.bias >= 0 ? g.values[n.bias].index : -1;
+    *w = wslot((int64_t)rows * Kgp * 2);
+    jobs.push_back({PackJob::ConvW, wc, w->off, K, Cg, 1, 1, Cp, Kgp, rows, 0, 0});
+    *bias = wslot((int64_t)rows * 4);
+    jobs.push_back({PackJob::Vec, bc, bias->off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? K : 0, rows});
+    *ld = Kgp;
+    *w_bytes = rows * Kgp * 2;
+    *b_bytes = rows * 4;
+    wbytes += numel(ws) * 2 + (bc >= 0 ? K * 4 : 0);
+  };
+  if (ai >= 0) {
+    const Node& a = g.nodes[ai];
+    pack(a, &L.w, &L.bias, &p.ldE, &p.we_bytes, &p.be_bytes);
+    p.act_e = (int)a.act, p.alpha_e = a.alpha;
+  }
+  {  // the depthwise weights [9][F] (float32 values of the bf16 taps) and bias
+    const int Cp = cp[d.data];
+    const int K = (int)g.values[d.weight].shape[0];
+    const int wc = g.values[d.weight].index;
+    const int bc = d.bias >= 0 ? g.values[d.bias].index : -1;
+    L.w2 = wslot((int64_t)9 * Cp * 4);
+    jobs.push_back({PackJob::DwW32, wc, L.w2.off, K, 1, 3, 3, Cp, 0, 0, 0, 0});
+    L.b2 = wslot(Cp * 4);
+    jobs.push_back({PackJob::Vec, bc, L.b2.off, 0, 0, 0, 0, 0, 0, 0, bc >= 0 ? K : 0, Cp});
+    p.wd_bytes = 9 * Cp * 4;
+    p.bd_bytes = Cp * 4;
+    p.act_d = (int)d.act, p.alpha_d = d.alpha;
+    wbytes += numel(g.values[d.weight].shape) * 2 + (bc >= 0 ? K * 4 : 0);
+  }
+  pack(c, &L.w3, &L.b3, &p.ldP, &p.wp_bytes, &p.bp_bytes);
+  p.act_p = (int)c.act, p.alpha_p = c.alpha;
+  p.res = c.residual >= 0;
+  p.x_bytes = (int)act_bytes(x);
+  p.y_bytes = (int)act_bytes(c.out);
+  L.info.flops = 2 * ((ai >= 0 ? g.nodes[ai].macs : 0) + d.macs + c.macs);
+  L.info.bytes = act_bytes(x) + act_bytes(c.out) + wbytes;
+  // built-in variant: the first with at least 256 tiles (else the finest);
+  // BYOC_IR_VARIANT=<v> forces one
+  const int nv = ir_block_variants(p.CIN, p.F, p.COUT, p.S);
+  int v = nv - 1;
+  for (int k = nv - 1; k >= 0; --k)
+    if (ir_block_tiles(p.CIN, p.F, p.COUT, p.S, k, p.N, p.P, p.Q) >= 256) v = k;
+  if (const char* ev = std::getenv("BYOC_IR_VARIANT")) v = std::atoi(ev);
+  if (v < 0 || v >= nv) v = 0;
+  L.tile = ConvTile{};
+  L.tile.bnv = v;
+  L.tile_default = L.tile;
+  name(L, ir_block_name(p.CIN, p.F, p.COUT, p.S, v));
+  e->launches.push_back(L);
+}
+
 // The int8 form of a fused block: the three (four) convs quantized on the
 // host as the int8 conv kernel has them; each composite's output zero point
 // and activation clamp, and the residual's rescaling into y's scale.
@@ -785,6 +945,7 @@ Status Planner::plan() {
   find_concat_aliases();
   find_post_adds();
   find_blocks();
+  find_ir_blocks();
   // concatenation outputs are allocated first: their producers write into them
   for (const Node& n : g.nodes)
     if (n.op == OpKind::Concat) {
@@ -853,7 +1014,7 @@ Status Planner::plan() {
         placed = true;
       }
     }
-    if (stem_pool[ni] >= 0 || post_add[ni] >= 0 || in_block[ni]) {  // planned with the node that consumes it
+    if (stem_pool[ni] >= 0 || post_add[ni] >= 0 || in_block[ni] || in_ir[ni]) {  // planned with the node that consumes it
       loc[v] = Ref();
       continue;
     }
@@ -867,6 +1028,8 @@ Status Planner::plan() {
       plan_stem(stem_conv[ni], (int)ni);
     else if (block_mid[ni] >= 0)
       plan_block((int)ni);
+    else if (ir_dw[ni] >= 0)
+      plan_ir((int)ni);
     else if (post_conv[ni] >= 0)
       plan_node(post_conv[ni]);
     else
@@ -1858,6 +2021,18 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       p.bp = c.ptr(L.bp);
       return launch_bottleneck(p, L.bnI8, L.bnF, L.bnC, L.bnCout, L.bnS, L.tile.bnv, c.s);
     }
+    case Launch::IrBlock: {
+      IrParams p = L.ir;
+      p.x = c.ptr(L.x);
+      p.y = c.ptr(L.y);
+      p.we = c.ptr(L.w);
+      p.be = c.ptr(L.bias);
+      p.wd = c.ptr(L.w2);
+      p.bd = c.ptr(L.b2);
+      p.wp = c.ptr(L.w3);
+      p.bp = c.ptr(L.b3);
+      return launch_ir_block(p, L.tile.bnv, c.s);
+    }
     case Launch::DepthwiseI8: {
       QDwParams d = L.qd;
       d.x = (const int8_t*)c.ptr(L.x);
@@ -1967,6 +2142,9 @@ Status build_device_state(Engine* e, Planner& pl, const byoc_const* consts) {
           break;
         case PackJob::DwW:
           err = launch_pack_dw_weights(src, sb, (bf16_t*)dst, j.K, j.R, j.S, j.Cp, nullptr);
+          break;
+        case PackJob::DwW32:
+          err = launch_pack_dw_weights_f32(src, sb, (float*)dst, j.K, j.R, j.S, j.Cp, nullptr);
           break;
         case PackJob::Vec:
           err = launch_pack_vector_f32(src, sb, (float*)dst, j.n, j.n_out, nullptr);
@@ -2266,8 +2444,22 @@ std::vector<ConvTile> block_candidates(const Launch& L) {
   return c;
 }
 
+// fused inverted-residual blocks: every variant of the kind (one summation
+// order for all of them)
+std::vector<ConvTile> ir_candidates(const Launch& L) {
+  std::vector<ConvTile> c{L.tile_default};
+  const IrParams& p = L.ir;
+  for (int v = 0; v < ir_block_variants(p.CIN, p.F, p.COUT, p.S); ++v) {
+    if (v == L.tile_default.bnv) continue;
+    ConvTile t = L.tile_default;
+    t.bnv = v;
+    c.push_back(t);
+  }
+  return c;
+}
+
 bool tunable(const Launch& L) {
-  return L.op == Launch::ConvMfma || L.op == Launch::ConvI8 || L.op == Launch::Bottleneck;
+  return L.op == Launch::ConvMfma || L.op == Launch::ConvI8 || L.op == Launch::Bottleneck || L.op == Launch::IrBlock;
 }
 
 void apply_tile(Launch& L, const ConvTile& t) {
@@ -2275,6 +2467,10 @@ void apply_tile(Launch& L, const ConvTile& t) {
   if (L.op == Launch::Bottleneck) {
     std::snprintf(L.info.name, sizeof(L.info.name), "%s",
                   bottleneck_variant_name(L.bnI8, L.bnF, L.bnC, L.bnCout, L.bnS, t.bnv));
+    return;
+  }
+  if (L.op == Launch::IrBlock) {
+    std::snprintf(L.info.name, sizeof(L.info.name), "%s", ir_block_name(L.ir.CIN, L.ir.F, L.ir.COUT, L.ir.S, t.bnv));
     return;
   }
   if (L.op == Launch::ConvI8) {
@@ -2330,6 +2526,7 @@ Status autotune(Engine* e) {
       const Launch& L = e->launches[i];
       cand[i] = L.op == Launch::ConvI8       ? conv_i8_candidates(L)
                 : L.op == Launch::Bottleneck ? block_candidates(L)
+                : L.op == Launch::IrBlock    ? ir_candidates(L)
                                              : conv_candidates(L);
       rounds = std::max(rounds, cand[i].size());
     }

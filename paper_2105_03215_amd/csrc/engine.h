@@ -26,7 +26,7 @@ struct Launch {
     ConvMfma, SplitReduce, ConvF32, Depthwise, MaxPoolBf16, AvgPoolBf16, MaxPoolF32, AvgPoolF32,
     AddBf16, AddF32, NchwToNhwc, NhwcToNchw, RowsToPadded, PaddedToRows, Cast, StemConvPool, DenseRows,
     ConvI8, MaxPoolI8, AvgPoolI8, AddI8, QuantizeI8, DequantizeI8, AvgPoolWinBf16, CopyChannels, QuantizeIm2colI8,
-    DepthwiseI8, Bottleneck
+    DepthwiseI8, Bottleneck, IrBlock
   } op;
   byoc_launch_info info{};
   Ref x, w, bias, res, y, partial, other;
@@ -44,6 +44,10 @@ struct Launch {
   // the 1x1 reduce's weights and bias in w / bias, the 3x3's in w2 / b2,
   // the 1x1 expand's in w3 / b3, the projection's in wp / bp; res is x
   BottleneckParams bn{};
+  // fused inverted-residual block (IrBlock): geometry in ir, the expand's
+  // weights and bias in w / bias, the depthwise's in w2 / b2, the project's
+  // in w3 / b3
+  IrParams ir{};
   Ref w2, b2, w3, b3, wp, bp;
   int bnF = 0, bnC = 0, bnCout = 0, bnS = 1;
   bool bnI8 = false;  // on int8 codes (w*, b* hold the int8 conv's weights and tables)

@@ -160,6 +160,44 @@ const char* bottleneck_variant_name(bool i8, int F, int CIN, int COUT, int S, in
 int bottleneck_tiles(bool i8, int F, int CIN, int COUT, int S, int v, int N, int P, int Q);
 hipError_t launch_bottleneck(const BottleneckParams& p, bool i8, int F, int CIN, int COUT, int S, int v,
                              hipStream_t s);
+// Fused MobileNetV2 inverted-residual block (bf16):
+//   e = act_e(conv1x1(x; we) + be)            CIN -> F (absent: e = x, F == CIN)
+//   d = act_d(depthwise3x3(e; wd, stride S, pad 1) + bd)
+//   y = act_p(conv1x1(d; wp) + bp [+ x])      F -> COUT (the block input added when S == 1, CIN == COUT)
+// each intermediate rounded to bf16 as the unfused composites store it; e and
+// d never leave the workgroup.  x NHWC [N][H][W][CIN], y [N][P][Q][COUT];
+// we / wp packed as for the implicit-GEMM kernel (row strides ldE / ldP
+// elements), wd the depthwise taps [9][F] as float32 values of the bf16
+// weights the depthwise kernel uses, biases fp32 zero-padded (be,
+// bd >= F entries, bp >= COUT).  Channel counts are multiples of 8, CIN <= 64.
+struct IrParams {
+  const void* x;
+  void* y;
+  const void* we;
+  const void* be;
+  const void* wd;
+  const void* bd;
+  const void* wp;
+  const void* bp;
+  int N, H, W, P, Q, S;
+  int CIN, F, COUT;
+  int ldE, ldP;
+  int x_bytes, y_bytes, we_bytes, be_bytes, wd_bytes, bd_bytes, wp_bytes, bp_bytes;
+  int act_e, act_d, act_p;
+  float alpha_e, alpha_d, alpha_p;
+  int res;
+  // set by the launcher: tiles per row band, per image and in all, tiles per
+  // XCD, and the 40-bit reciprocals of the first two
+  int tiles_w, tiles_hw, tiles, per_xcd;
+  uint64_t mg_tw, mg_thw;
+};
+// Variants of a kind (0: no compiled kernel), their names, and the
+// workgroups (output tiles) of variant v on an N x P x Q output; all
+// variants of a kind give the same bits.
+int ir_block_variants(int cin, int f, int cout, int s);
+const char* ir_block_name(int cin, int f, int cout, int s, int v);
+int ir_block_tiles(int cin, int f, int cout, int s, int v, int N, int P, int Q);
+hipError_t launch_ir_block(const IrParams& p, int v, hipStream_t s);
 // Plain matrix product of at most 64 rows (R = S = H = W = 1, no split):
 // one workgroup per 16 output channels, the reduction split over its waves.
 bool dense_rows_supported(const ConvParams& p);
@@ -322,6 +360,9 @@ hipError_t launch_pack_conv_weights(const void* src, bool src_bf16, bf16_t* dst,
 // Depthwise weights [C][1][R][S] -> [R*S][Cp] bf16.
 hipError_t launch_pack_dw_weights(const void* src, bool src_bf16, bf16_t* dst, int C, int R,
                                   int S, int Cp, hipStream_t s);
+// the same as float32 values of the bf16 weights
+hipError_t launch_pack_dw_weights_f32(const void* src, bool src_bf16, float* dst, int C, int R, int S, int Cp,
+                                      hipStream_t s);
 // Vector [K] (f32 or bf16) -> fp32 [n_out], zero-padded.
 hipError_t launch_pack_vector_f32(const void* src, bool src_bf16, float* dst, int K, int n_out,
                                   hipStream_t s);

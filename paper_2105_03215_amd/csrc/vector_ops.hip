@@ -442,6 +442,18 @@ __global__ __launch_bounds__(kThreads) void pack_dw_weights_kernel(const SrcT* s
   dst[idx] = c < C ? f32_to_bf16(load_f(src, (size_t)c * R * S + rs)) : (bf16_t)0;
 }
 
+// The same taps as float32 values of the bf16 weights (the fused
+// inverted-residual kernel reads them unpacked).
+template <typename SrcT>
+__global__ __launch_bounds__(kThreads) void pack_dw_weights_f32_kernel(const SrcT* src, float* dst, int C, int R,
+                                                                       int S, int Cp) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)R * S * Cp) return;
+  const int c = (int)(idx % Cp);
+  const int rs = (int)(idx / Cp);
+  dst[idx] = c < C ? bf16_to_f32(f32_to_bf16(load_f(src, (size_t)c * R * S + rs))) : 0.f;
+}
+
 template <typename SrcT>
 __global__ __launch_bounds__(kThreads) void pack_vector_kernel(const SrcT* src, float* dst, int K,
                                                                int n_out) {
@@ -644,6 +656,16 @@ hipError_t launch_pack_dw_weights(const void* src, bool src_bf16, bf16_t* dst, i
     pack_dw_weights_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)src, dst, C, R, S, Cp);
   else
     pack_dw_weights_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)src, dst, C, R, S, Cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_dw_weights_f32(const void* src, bool src_bf16, float* dst, int C, int R, int S, int Cp,
+                                      hipStream_t s) {
+  const int64_t n = (int64_t)R * S * Cp;
+  if (src_bf16)
+    pack_dw_weights_f32_kernel<bf16_t><<<grid_for(n), kThreads, 0, s>>>((const bf16_t*)src, dst, C, R, S, Cp);
+  else
+    pack_dw_weights_f32_kernel<float><<<grid_for(n), kThreads, 0, s>>>((const float*)src, dst, C, R, S, Cp);
   return hipGetLastError();
 }
 
