@@ -137,7 +137,7 @@ def _roofline(launches, per_launch_ms, step_ms, traffic=None):
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
-            "kernel": ("conv/dense bf16 MFMA class (stem_conv_maxpool, conv_dma, conv_halo, conv_mfma, bottleneck, dense_rows, "
+            "kernel": ("conv/dense bf16 MFMA class (stem_conv_maxpool, conv_dma, conv_halo, conv_mfma, bottleneck, ir_block, dense_rows, "
                        "splitk_reduce kernels), %d launches per step" % n_conv),
             "flops_per_step": conv_flops, "kernel_ms_per_step": round(conv_ms, 4),
             "per_launch_event_ms_per_step": round(conv_ev_ms, 4),
@@ -499,7 +499,8 @@ def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
                       "checked bit for bit against the int8 oracle on all 32 images in the GPU tests",
             "roofline": {"bound": "mfma", "achieved": round(tops, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                          "frac": round(tops / PEAK_INT8_TOPS, 4), "traffic": traffic,
-                         "kernel": "conv/dense int8 MFMA class (conv_i8), %d launches per step"
+                         "kernel": "conv/dense int8 MFMA class (the int8 stem, fused bottleneck blocks, conv_i8, "
+                                   "the windowed 3x3 kernel), %d launches per step"
                                    % sum(1 for l in launches if l["kind"] == "conv_i8"),
                          "ops_per_step": ops, "kernel_ms_per_step": round(conv_ms, 4)},
             "kernel_classes": _class_summary(launches, per_launch), "launches": len(launches)}

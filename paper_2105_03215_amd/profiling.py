@@ -11,9 +11,9 @@ traffic  HBM bytes of the conv kernels per run from two counter runs
          known size (``bench.py --copy-calibration MIB`` under the same
          counter), over the last N runs -> JSON read by bench.py.
 
-A run of the ResNet subgraph starts with its fused stem kernel (of its int8
-form: the boundary quantize kernel), the marker used to split the dispatch
-stream into runs.
+A run of the ResNet subgraph starts with its fused stem kernel, the marker
+used to split the dispatch stream into runs; the int8 form's runs are cut at
+its boundary dequantize kernel (each cut holds one whole run).
 
 classes  per kernel class of one workload: pure kernel time (kernel trace),
          HBM bytes read / written (FETCH_SIZE / WRITE_SIZE runs, scaled by a
@@ -37,16 +37,33 @@ import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CONV_KERNELS = ("conv_mfma_kernel", "conv_dma_kernel", "conv_halo_kernel", "stem_conv_maxpool_kernel",
-                "splitk_reduce_kernel", "dense_rows_kernel", "bottleneck_kernel")
+                "splitk_reduce_kernel", "dense_rows_kernel", "bottleneck_kernel", "ir_block_kernel")
 RUN_MARKER = "stem_conv_maxpool_kernel"  # one dispatch per run of the ResNet subgraphs
+# kernels compiled for bf16 and for int8 codes: the int8 form has `true` as
+# its last template argument
+DUAL_KERNELS = ("bottleneck_kernel", "conv_halo_kernel", "stem_conv_maxpool_kernel")
 
 
 def _short(name):
     return name.replace("byoc::(anonymous namespace)::", "").replace("void ", "")
 
 
+def _is_int8(name):
+    if "conv_i8_kernel" in name:
+        return True
+    if not any(k in name for k in DUAL_KERNELS):
+        return False
+    head = name.rsplit("(", 1)[0].rstrip("> ")
+    return head.rsplit(",", 1)[-1].strip() == "true"
+
+
 def _is_conv(name, kernels=CONV_KERNELS):
-    return any(k in name for k in kernels)
+    """Is the kernel in the class of `kernels`?  A kernel of DUAL_KERNELS
+    belongs to the int8 class (the one listing conv_i8_kernel) in its int8
+    form and to the other class in its bf16 form."""
+    if not any(k in name for k in kernels):
+        return False
+    return _is_int8(name) == ("conv_i8_kernel" in kernels)
 
 
 def _last_runs(rows, name_key, last_runs, marker=RUN_MARKER, skip_last=0):
@@ -106,10 +123,12 @@ def _copy_kib(path, counter):
     return statistics.median([v for v in vals if v > 0.5 * big])
 
 
-CONV_SOURCES = ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "bottleneck.hip", "lds_dma.h", "stem.hip",
-                "dense_rows.hip", "engine.cpp")
-I8_KERNELS = ("conv_i8_kernel",)
-I8_SOURCES = ("conv_i8.hip", "quant.hip", "lds_dma.h", "engine.cpp")
+CONV_SOURCES = ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "bottleneck.hip", "ir_block.hip", "lds_dma.h",
+                "stem.hip", "dense_rows.hip", "engine.cpp")
+I8_KERNELS = ("conv_i8_kernel", "bottleneck_kernel", "conv_halo_kernel", "stem_conv_maxpool_kernel")
+I8_SOURCES = ("conv_i8.hip", "conv_halo.hip", "bottleneck.hip", "stem.hip", "quant.hip", "quant_epilogue.h", "lds_dma.h",
+              "engine.cpp")
+I8_MARKER = "dequantize_kernel"  # the int8 graphs' last dispatch: runs are cut there
 
 
 def conv_kernel_digest(sources=CONV_SOURCES):
@@ -298,7 +317,7 @@ def main():
                     kernels=tuple(args.kernels.split(",")), class_name=args.class_name, unit=args.unit,
                     skip_last=args.skip_last))
     else:
-        kw = dict(marker="::quantize", kernels=I8_KERNELS, sources=I8_SOURCES) if args.int8 else {}
+        kw = dict(marker=I8_MARKER, kernels=I8_KERNELS, sources=I8_SOURCES) if args.int8 else {}
         print(json.dumps(traffic(args.fetch, args.write, args.copy_fetch, args.copy_write,
                                  args.copy_mib, args.workload, args.out, args.last_runs, **kw)))
 
