@@ -156,7 +156,11 @@ def test_resnet50_bs32_int8_timed_plan_all_images():
     qg = oracle_calibrated_int8(wl.graph, wl.consts, [np.ascontiguousarray(a[:2]) for a in wl.inputs])
     announce("timed plan resnet50_v1 bs32 int8")
     got, names = timed_plan_outputs(workloads.Workload(qg, wl.consts, wl.inputs, wl.macs, wl.conv_macs))
-    assert sum(1 for n in names if n.startswith("conv_i8")) == 54
+    # the fused int8 stem, the seven stage-1/2 blocks fused (three convs each,
+    # four with the projection), the other 30 convs and the classifier
+    assert names.count("stem_conv_maxpool_i8") == 1, names
+    assert sum(1 for n in names if n.startswith("bottleneck_i8_")) == 7, names
+    assert sum(1 for n in names if n.startswith("conv_i8")) == 30, names
     ref = OQ.run_quantized_graph(qg, wl.consts, wl.inputs)[0]
     diff = np.abs(got[0] - ref.astype(np.float64))
     print("timed plan resnet50 bs32 int8: %d of %d outputs differ" % (int((diff > 0).sum()), diff.size))
