@@ -13,7 +13,7 @@ traffic  HBM bytes of the conv kernels per run from two counter runs
 
 A run of the ResNet subgraph starts with its fused stem kernel, the marker
 used to split the dispatch stream into runs; the int8 form's runs are cut at
-its boundary dequantize kernel (each cut holds one whole run).
+its int8 stem.
 
 classes  per kernel class of one workload: pure kernel time (kernel trace),
          HBM bytes read / written (FETCH_SIZE / WRITE_SIZE runs, scaled by a
@@ -69,9 +69,10 @@ def _is_conv(name, kernels=CONV_KERNELS):
 def _last_runs(rows, name_key, last_runs, marker=RUN_MARKER, skip_last=0):
     """The rows of the last `last_runs` runs before the final `skip_last`
     runs (a run starts at its marker kernel)."""
-    starts = [i for i, r in enumerate(rows) if marker in r[name_key]]
+    hit = marker if callable(marker) else (lambda n: marker in n)
+    starts = [i for i, r in enumerate(rows) if hit(r[name_key])]
     if len(starts) < last_runs + skip_last:
-        raise RuntimeError("only %d runs (marker %s) in the trace" % (len(starts), marker))
+        raise RuntimeError("only %d runs (marker %s) in the trace" % (len(starts), getattr(marker, "__name__", marker)))
     end = starts[len(starts) - skip_last] if skip_last else len(rows)
     return rows[starts[len(starts) - skip_last - last_runs]:end], last_runs
 
@@ -128,7 +129,10 @@ CONV_SOURCES = ("conv_mfma.hip", "conv_dma.hip", "conv_halo.hip", "bottleneck.hi
 I8_KERNELS = ("conv_i8_kernel", "bottleneck_kernel", "conv_halo_kernel", "stem_conv_maxpool_kernel")
 I8_SOURCES = ("conv_i8.hip", "conv_halo.hip", "bottleneck.hip", "stem.hip", "quant.hip", "quant_epilogue.h", "lds_dma.h",
               "engine.cpp")
-I8_MARKER = "dequantize_kernel"  # the int8 graphs' last dispatch: runs are cut there
+
+
+def I8_MARKER(name):  # a run of an int8 ResNet starts at its int8 stem
+    return "stem_conv_maxpool_kernel" in name and _is_int8(name)
 
 
 def conv_kernel_digest(sources=CONV_SOURCES):
@@ -274,6 +278,7 @@ def main():
     a.add_argument("--class-name", default="conv/dense MFMA class")
     a.add_argument("--unit", default="FLOP", help="FLOP, or OP for integer work")
     a.add_argument("--skip-last", type=int, default=0, help="runs at the end of the trace to leave out")
+    a.add_argument("--int8", action="store_true", help="the int8 MFMA class, runs cut at the int8 stem")
     b = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy-fetch", "copy-write", "workload", "out"):
         b.add_argument("--" + k, required=True)
@@ -313,9 +318,9 @@ def main():
                          indent=1))
         return
     if args.cmd_name == "stats":
-        print(stats(args.trace, args.cmd, args.out, args.last_runs, args.flops_per_run, marker=args.marker,
-                    kernels=tuple(args.kernels.split(",")), class_name=args.class_name, unit=args.unit,
-                    skip_last=args.skip_last))
+        marker, kernels = (I8_MARKER, I8_KERNELS) if args.int8 else (args.marker, tuple(args.kernels.split(",")))
+        print(stats(args.trace, args.cmd, args.out, args.last_runs, args.flops_per_run, marker=marker,
+                    kernels=kernels, class_name=args.class_name, unit=args.unit, skip_last=args.skip_last))
     else:
         kw = dict(marker=I8_MARKER, kernels=I8_KERNELS, sources=I8_SOURCES) if args.int8 else {}
         print(json.dumps(traffic(args.fetch, args.write, args.copy_fetch, args.copy_write,
