@@ -17,6 +17,13 @@
 // a pixel whose window crosses the border the epilogue adds back Z_x times
 // the weight sums of its taps outside the image (wtap[k][r*S + s]).
 //
+// Reduction groups (KG > 1): KG groups of WM x WN waves each run their own
+// ring over every KG-th stage of the reduction (group g: stages g, g + KG,
+// ...), which multiplies the loads in flight of a workgroup on layers with
+// few tiles and long reductions; the groups' int32 sums are added in the
+// epilogue (exact in any order, so every tile and group count gives the
+// same codes).
+//
 // Epilogue: each thread finishes 8 consecutive channels of one pixel from
 // int32 sums staged in LDS: bias, border correction, float32 rescaling
 // (one rounding per term, the per-channel bias and factor read from LDS),
@@ -37,11 +44,13 @@ constexpr int kMaxStages = 4;
 
 __device__ __forceinline__ i32x4 as_i32x4(uint4 u) { return __builtin_bit_cast(i32x4, u); }
 
-template <int BM, int BN, int WM, int WN, int NS, bool ALIGNED>
-__global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
-  static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves");
+template <int BM, int BN, int WM, int WN, int KG, int NS, bool ALIGNED>
+__global__ __launch_bounds__(64 * WM * WN * KG) void conv_i8_kernel(QConvParams q) {
+  static_assert(WM * WN == 4 || WM * WN == 8, "4 or 8 waves per reduction group");
+  static_assert(KG == 1 || KG == 2 || KG == 4, "reduction groups");
   const ConvParams& p = q.g;
-  constexpr int kNT = 64 * WM * WN;
+  constexpr int kNT = 64 * WM * WN;  // threads of one reduction group
+  constexpr int kNTall = kNT * KG;   // threads of the workgroup
   constexpr int kRowsPerPass = kNT / kCH;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 16, TN = WTN / 16;
@@ -51,15 +60,18 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
   constexpr int STAGE = (BM + BN) * kCH;  // uint4 per stage buffer
   static_assert(NS >= 2 && NS <= kMaxStages, "stages");
 
-  __shared__ uint4 ring[NS * STAGE];
+  __shared__ uint4 ring[KG * NS * STAGE];
   __shared__ int2 sq[128];  // the tile's {bias, factor} (one wave's 16-byte fill: 128 channels)
   materialize_args(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  auto buf = [&](auto tag) -> uint4* { return ring + decltype(tag)::value * STAGE; };
+  const int kg = __builtin_amdgcn_readfirstlane(tid / kNT);                  // reduction group
+  const int tg = tid - kg * kNT;                                               // thread within the group
+  const int wave = __builtin_amdgcn_readfirstlane((tid >> 6) % (WM * WN));  // wave within the group
+  uint4* const gring = ring + kg * NS * STAGE;
+  auto buf = [&](auto tag) -> uint4* { return gring + decltype(tag)::value * STAGE; };
   const int wm = wave / WN, wn = wave % WN;
-  const int r0 = tid / kCH;
+  const int r0 = tg / kCH;
   const int cv = (lane & 7) ^ ((lane >> 3) & 7);
 
   int tm, tn;
@@ -107,8 +119,10 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
 #pragma unroll
   for (int i = 0; i < BR; ++i) wvoff[i] = (uint32_t)((n0 + r0 + i * kRowsPerPass) * p.Kgp + cv * kCE);
 
-  int r = 0, s = 0, c = ALIGNED ? 0 : cv * kCE, kk = ALIGNED ? 0 : cv * kCE, wcol = 0;
-  if (!ALIGNED) {
+  // reduction position of this group's first stage
+  int r, s, c, kk, wcol = kg * kBK;
+  {
+    kk = kg * kBK + (ALIGNED ? 0 : cv * kCE);
     const int rs = mdiv(kk, p.mg_cp);
     c = kk - rs * p.Cp;
     r = mdiv(rs, p.mg_s);
@@ -118,7 +132,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
   // Loads of the next stage into buffer SET; past the end of the reduction
   // the offsets are out of range (zero fills), which keeps the count of
   // loads in flight fixed.
-  int kleft = nkt;
+  int kleft = (nkt - kg + KG - 1) / KG;  // stages of this group
   auto issue = [&](auto set_tag) {
     uint4* dst = buf(set_tag);
     const bool live = kleft-- > 0;
@@ -142,23 +156,26 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
     for (int i = 0; i < BR; ++i)
       lds_fill16(wr, __builtin_amdgcn_readfirstlane(lds_addr(dst + (BM + i * kRowsPerPass + wave * 8) * kCH)),
                  live ? wvoff[i] + (uint32_t)wcol : kOOB);
-    wcol += kBK;
-    c += kBK;
-    if (ALIGNED) {
-      if (c == p.Cp) {
-        c = 0;
-        if (++s == p.S) {
-          s = 0;
-          ++r;
+#pragma unroll
+    for (int a = 0; a < KG; ++a) {  // to this group's next stage
+      wcol += kBK;
+      c += kBK;
+      if (ALIGNED) {
+        if (c == p.Cp) {
+          c = 0;
+          if (++s == p.S) {
+            s = 0;
+            ++r;
+          }
         }
-      }
-    } else {
-      kk += kBK;
-      while (c >= p.Cp) {
-        c -= p.Cp;
-        if (++s == p.S) {
-          s = 0;
-          ++r;
+      } else {
+        kk += kBK;
+        while (c >= p.Cp) {
+          c -= p.Cp;
+          if (++s == p.S) {
+            s = 0;
+            ++r;
+          }
         }
       }
     }
@@ -202,7 +219,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
   constexpr int kEC = 32;
   constexpr int NPASS = BN / kEC;
   constexpr int TPP = kEC / 8;
-  constexpr int EPV = (BM * TPP + kNT - 1) / kNT;
+  constexpr int EPV = (BM * TPP + kNTall - 1) / kNTall;
   const int ec8 = (tid % TPP) * 8;
   uint2 resv[NPASS][EPV];
   {
@@ -213,7 +230,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
       const int k = n0 + pass * kEC + ec8;
 #pragma unroll
       for (int e = 0; e < EPV; ++e) {
-        const int px = (tid + e * kNT) / TPP;
+        const int px = (tid + e * kNTall) / TPP;
         const int m = m0 + px;
         const uint32_t off = (px < BM && m < p.M && k < p.Kp) ? (uint32_t)(m * p.ldr + k) : kOOB;
         resv[pass][e] = p.res ? __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0))
@@ -225,7 +242,7 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
   // per-channel bias and factor of the tile, straight into LDS; issued
   // before the operand ring, so every later wait of this wave covers it
   static_assert(BN <= 128, "channel table");
-  if (wave == 0) {
+  if (tid < 64) {
     const i32x4 qr = buffer_rsrc(q.qch, ((p.Kp + 255) / 256) * 256 * 8);
     lds_fill16(qr, __builtin_amdgcn_readfirstlane(lds_addr(sq)), 2 * lane < BN ? (uint32_t)(n0 + 2 * lane) * 8u : kOOB);
   }
@@ -237,17 +254,20 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
     compute(i);
   };
   static_for<0, NS - 1>([&](auto i) { issue(i); });
+  const int nsteps = (nkt + KG - 1) / KG;  // stages per group (the last ones may read zeros)
   int t = 0;
-  for (; t + NS <= nkt; t += NS) static_for<0, NS>(round_step);
-  const int rem = nkt - t;
+  for (; t + NS <= nsteps; t += NS) static_for<0, NS>(round_step);
+  const int rem = nsteps - t;
   static_for<0, NS - 1>([&](auto i) {
     if (rem > decltype(i)::value) round_step(i);
   });
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
+  // each group parks its sums in its own ring; the finishing threads add
+  // the groups' sums
   constexpr int kLd = kEC + 4;
   static_assert(BM * kLd * 4 <= STAGE * 16, "staging tile");
-  int* stage = reinterpret_cast<int*>(ring);
+  int* stage = reinterpret_cast<int*>(gring);
 #pragma unroll
   for (int pass = 0; pass < NPASS; ++pass) {
     if (pass > 0) lds_barrier();
@@ -265,21 +285,28 @@ __global__ __launch_bounds__(64 * WM * WN) void conv_i8_kernel(QConvParams q) {
     const int k = n0 + pass * kEC + ec8;
 #pragma unroll
     for (int e = 0; e < EPV; ++e) {
-      const int px = (tid + e * kNT) / TPP;
+      const int px = (tid + e * kNTall) / TPP;
       const int m = m0 + px;
       if (px >= BM || m >= p.M || k >= p.Kp) continue;
-      const int* st = stage + px * kLd + ec8;
+      const int* st = reinterpret_cast<const int*>(ring) + px * kLd + ec8;
       const int4 lo4 = *(const int4*)st, hi4 = *(const int4*)(st + 4);
       int a[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
+#pragma unroll
+      for (int g = 1; g < KG; ++g) {
+        const int* sg = reinterpret_cast<const int*>(ring + g * NS * STAGE) + px * kLd + ec8;
+        const int4 l2 = *(const int4*)sg, h2 = *(const int4*)(sg + 4);
+        a[0] += l2.x; a[1] += l2.y; a[2] += l2.z; a[3] += l2.w;
+        a[4] += h2.x; a[5] += h2.y; a[6] += h2.z; a[7] += h2.w;
+      }
       *(uint2*)(reinterpret_cast<int8_t*>(p.y) + (size_t)m * p.ldy + k) =
           finish8_i8(a, sq + pass * kEC + ec8, resv[pass][e], q, m, k);
     }
   }
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int KG = 1>
 hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
-  constexpr int kThreads = 64 * WM * WN;
+  constexpr int kThreads = 64 * WM * WN * KG;
   QConvParams q = q_in;
   ConvParams& p = q.g;
   const bool aligned = (p.Cp % kBK) == 0 && p.R * p.S <= 32;
@@ -287,10 +314,10 @@ hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
   hipError_t r = hipErrorInvalidValue;
   static_for<2, kMaxStages + 1>([&](auto i) {
     constexpr int NS = decltype(i)::value;
-    if constexpr (NS * (BM + BN) * 128 <= kLdsLimit) {
+    if constexpr (KG * NS * (BM + BN) * 128 + 1024 <= kLdsLimit) {
       if (ns != NS) return;
-      if (aligned) conv_i8_kernel<BM, BN, WM, WN, NS, true><<<blocks, kThreads, 0, s>>>(q);
-      else conv_i8_kernel<BM, BN, WM, WN, NS, false><<<blocks, kThreads, 0, s>>>(q);
+      if (aligned) conv_i8_kernel<BM, BN, WM, WN, KG, NS, true><<<blocks, kThreads, 0, s>>>(q);
+      else conv_i8_kernel<BM, BN, WM, WN, KG, NS, false><<<blocks, kThreads, 0, s>>>(q);
       r = hipGetLastError();
     }
   });
@@ -299,16 +326,31 @@ hipError_t launch_tile(const QConvParams& q_in, int ns, hipStream_t s) {
 
 }  // namespace
 
-bool conv_i8_tile_supported(int bm, int bn, int stages, int threads) {
+bool conv_i8_tile_supported(int bm, int bn, int stages, int threads, int kgroups) {
   if (stages < 2 || stages > kMaxStages) return false;
+  if (kgroups == 2 || kgroups == 4) {  // 4-wave groups
+    if (threads != 256 * kgroups || kgroups * stages * (bm + bn) * 128 + 1024 > kLdsLimit) return false;
+    return (bm == 64 && bn == 64) || (bm == 32 && bn == 64) || (kgroups == 2 && bm == 128 && bn == 64);
+  }
+  if (kgroups != 1) return false;
   if (threads == 512) return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 128);
   if (threads != 256) return false;
   return (bm == 128 && bn == 128) || (bm == 128 && bn == 64) || (bm == 64 && bn == 64) || (bm == 32 && bn == 64);
 }
 
-hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s) {
-  if (!conv_i8_tile_supported(bm, bn, stages, threads)) return hipErrorInvalidValue;
+hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, int kgroups,
+                          hipStream_t s) {
+  if (!conv_i8_tile_supported(bm, bn, stages, threads, kgroups)) return hipErrorInvalidValue;
   if (p.g.Cp % kCE != 0 || p.g.Kp % 8 != 0 || p.g.Kgp % kBK != 0) return hipErrorInvalidValue;
+  if (kgroups == 4) {
+    if (bm == 64) return launch_tile<64, 64, 2, 2, 4>(p, stages, s);
+    return launch_tile<32, 64, 1, 4, 4>(p, stages, s);
+  }
+  if (kgroups == 2) {
+    if (bm == 128) return launch_tile<128, 64, 2, 2, 2>(p, stages, s);
+    if (bm == 64) return launch_tile<64, 64, 2, 2, 2>(p, stages, s);
+    return launch_tile<32, 64, 1, 4, 2>(p, stages, s);
+  }
   if (threads == 512) {
     if (bm == 128 && bn == 128) return launch_tile<128, 128, 2, 4>(p, stages, s);
     if (bm == 128 && bn == 64) return launch_tile<128, 64, 4, 2>(p, stages, s);

@@ -193,8 +193,8 @@ void name_conv_i8(Launch& L) {
     std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_halo_%dx%d_s%d_lp%d_pb%d", L.tile.bm, L.tile.bn,
                   L.tile.stages, L.tile.lp, L.tile.npb);
   else
-    std::snprintf(L.info.name, sizeof(L.info.name), "conv_i8_%dx%d_s%d_w%d", L.tile.bm, L.tile.bn, L.tile.stages,
-                  L.tile.threads / 64);
+    std::snprintf(L.info.name, sizeof(L.info.name), L.tile.kgroups > 1 ? "conv_i8_%dx%d_s%d_w%d_k%d" : "conv_i8_%dx%d_s%d_w%d",
+                  L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads / 64, L.tile.kgroups);
 }
 
 void name_conv(Launch& L) {
@@ -1735,11 +1735,13 @@ void Planner::plan_node_i8(int ni) {
     else if (tiles(128, 64) >= 512) t.bm = 128, t.bn = 64;
     else if (p.M <= 32) t.bm = 32, t.bn = 64;
     else t.bm = 64, t.bn = 64;
-    // BYOC_I8_TILE=<bm>x<bn>s<stages>[w<waves>] forces a tile (any tile gives the same codes)
+    // BYOC_I8_TILE=<bm>x<bn>s<stages>[w<waves>[k<groups>]] forces a tile (any
+    // tile gives the same codes)
     if (const char* te = std::getenv("BYOC_I8_TILE")) {
-      int bm = 0, bn = 0, ns = 0, nw = 4;
-      if (std::sscanf(te, "%dx%ds%dw%d", &bm, &bn, &ns, &nw) >= 3 && conv_i8_tile_supported(bm, bn, ns, 64 * nw))
-        t.bm = bm, t.bn = bn, t.stages = ns, t.threads = 64 * nw;
+      int bm = 0, bn = 0, ns = 0, nw = 4, kgr = 1;
+      if (std::sscanf(te, "%dx%ds%dw%dk%d", &bm, &bn, &ns, &nw, &kgr) >= 3 &&
+          conv_i8_tile_supported(bm, bn, ns, 64 * nw, kgr))
+        t.bm = bm, t.bn = bn, t.stages = ns, t.threads = 64 * nw, t.kgroups = kgr;
     }
     // 3x3 stride-1 convs with at least 256 input channels and enough 128x64
     // tiles run on the windowed kernel (input window staged in LDS once per
@@ -1990,7 +1992,7 @@ hipError_t exec(const Launch& L, const RunCtx& c) {
       q.qch = (const int32_t*)c.ptr(L.bias);
       q.wtap = (const int32_t*)c.ptr(L.other);
       if (L.tile.halo) return launch_conv_halo_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.lp, L.tile.npb, c.s);
-      return launch_conv_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, c.s);
+      return launch_conv_i8(q, L.tile.bm, L.tile.bn, L.tile.stages, L.tile.threads, L.tile.kgroups, c.s);
     }
     case Launch::MaxPoolI8:
     case Launch::AvgPoolI8: {
@@ -2414,20 +2416,24 @@ std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
     if (L.tile_default.halo && ns == L.tile_default.stages) continue;
     c.push_back(t);
   }
-  for (int nt : {256, 512})
-    for (auto bmn : {std::pair<int, int>{128, 128}, {128, 64}, {64, 128}, {64, 64}, {32, 64}})
-      for (int ns : {2, 3, 4}) {
-        ConvTile t = ConvTile{};
-        t.bm = bmn.first;
-        t.bn = bmn.second;
-        t.stages = ns;
-        t.threads = nt;
-        if (!conv_i8_tile_supported(t.bm, t.bn, t.stages, t.threads)) continue;
-        if (t.bm == L.tile_default.bm && t.bn == L.tile_default.bn && t.stages == L.tile_default.stages &&
-            t.threads == L.tile_default.threads)
-          continue;
-        c.push_back(t);
-      }
+  // single-group tiles of 4 or 8 waves, and 2 or 4 reduction groups of 4
+  // waves (long reductions over few tiles)
+  for (int nt : {256, 512, 1024})
+    for (int kgr : {1, 2, 4})
+      for (auto bmn : {std::pair<int, int>{128, 128}, {128, 64}, {64, 128}, {64, 64}, {32, 64}})
+        for (int ns : {2, 3, 4}) {
+          ConvTile t = ConvTile{};
+          t.bm = bmn.first;
+          t.bn = bmn.second;
+          t.stages = ns;
+          t.threads = nt;
+          t.kgroups = kgr;
+          if (!conv_i8_tile_supported(t.bm, t.bn, t.stages, t.threads, t.kgroups)) continue;
+          if (t.bm == L.tile_default.bm && t.bn == L.tile_default.bn && t.stages == L.tile_default.stages &&
+              t.threads == L.tile_default.threads && t.kgroups == L.tile_default.kgroups && !L.tile_default.halo)
+            continue;
+          c.push_back(t);
+        }
   return c;
 }
 

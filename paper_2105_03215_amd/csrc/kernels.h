@@ -293,9 +293,12 @@ struct QConvParams {
   float pm;
 };
 // Tiles: 4 waves (256 threads) 128x128, 128x64, 64x64, 32x64; 8 waves (512)
-// 128x128, 128x64, 64x128; 2 to 4 ring stages.
-bool conv_i8_tile_supported(int bm, int bn, int stages, int threads);
-hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, hipStream_t s);
+// 128x128, 128x64, 64x128; 2 to 4 ring stages.  kgroups 2 or 4: that many
+// 4-wave reduction groups (threads = 256 * kgroups) on 64x64 or 32x64
+// tiles, 2 groups also on 128x64, as far as their rings fit the LDS.
+bool conv_i8_tile_supported(int bm, int bn, int stages, int threads, int kgroups = 1);
+hipError_t launch_conv_i8(const QConvParams& p, int bm, int bn, int stages, int threads, int kgroups,
+                          hipStream_t s);
 // The windowed 3x3 kernel on codes (conv_halo_plan(..., i8 = true) sizes it):
 // 128 channels per slice; the same codes as launch_conv_i8.
 hipError_t launch_conv_halo_i8(const QConvParams& q, int bm, int bn, int stages, int lp, int npb, hipStream_t s);

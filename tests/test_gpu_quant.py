@@ -110,6 +110,37 @@ def test_int8_tiles_agree():
         assert np.array_equal(got[0], ref.astype(np.float64)), tile
 
 
+# 2 or 4 reduction groups (threads = 256 per group): each group sums every
+# 2nd / 4th stage, the int32 sums are added in the epilogue
+KG_TILES = ("64x64s3w8k2", "64x64s4w8k2", "32x64s4w8k2", "128x64s2w8k2", "128x64s3w8k2", "64x64s2w16k4",
+            "32x64s3w16k4")
+KG_CASES = [
+    # n, c, h, w, k, r, stride, pad, zx, act, residual: 144 channels (reduction not in whole 128-code
+    # stages, a ragged last stage per group), 256 channels 3x3 (aligned, 18 stages), a 1x1 with 7 stages
+    (2, 144, 12, 12, 136, 3, 1, 1, 21, "relu", True),
+    (2, 256, 7, 7, 200, 3, 1, 1, -7, "relu6", False),
+    (3, 896, 5, 5, 72, 1, 1, 0, 3, None, True),
+]
+
+
+@pytest.mark.parametrize("case", KG_CASES, ids=["c%d_r%d" % (c[1], c[5]) for c in KG_CASES])
+def test_int8_reduction_groups_exact(case):
+    """Every reduction-group tile gives the oracle's codes exactly."""
+    announce("int8 conv reduction groups %s" % (case,))
+    import os
+    g, consts, inputs = _conv_graph(*case, seed=60 + KG_CASES.index(case))
+    ref = OQ.run_quantized_graph(g, consts, inputs)[0]
+    for tile in KG_TILES:
+        os.environ["BYOC_I8_TILE"] = tile
+        try:
+            got, launches = _run(g, consts, inputs)
+        finally:
+            del os.environ["BYOC_I8_TILE"]
+        name = [l["name"] for l in launches if l["kind"] == "conv_i8"][0]
+        assert name == "conv_i8_" + tile.replace("s", "_s").replace("w", "_w").replace("k", "_k"), name
+        assert np.array_equal(got[0], ref.astype(np.float64)), tile
+
+
 def test_int8_dense_pool_add():
     announce("int8 dense, pools, add")
     rng = np.random.default_rng(7)
