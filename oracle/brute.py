@@ -87,7 +87,7 @@ def global_avg_pool2d(x):
 
 
 def gelu(v):
-    return v * 0.5 * (1.0 + math.erf(v / math.sqrt(2.0)))
+    return v * 0.5 * math.erfc(-v / math.sqrt(2.0))
 
 
 def avg_pool2d(x, pool_size=(3, 3), strides=(1, 1), padding=(1, 1, 1, 1), count_include_pad=False):

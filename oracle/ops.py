@@ -13,7 +13,7 @@ conv2d     y[n,k,p,q] = sum_{c<C/G, r<R, s<S} xpad[n, g*C/G + c, p*sh + r, q*sw 
 dense      y[m,n] = sum_k x[m,k] * W[n,k]
 bias_add   y[:, k, ...] += b[k]
 add        y = a + b (same shape)
-relu       max(y, 0);  relu6 = min(max(y, 0), 6);  gelu = y * (1 + erf(y / sqrt 2)) / 2
+relu       max(y, 0);  relu6 = min(max(y, 0), 6);  gelu = y * Phi(y) = y * erfc(-y / sqrt 2) / 2
 max_pool2d max over the in-bounds part of each window (padding acts as -inf)
 global_avg_pool2d   y[n,c] = mean over h, w of x[n,c,h,w]
 
@@ -22,7 +22,7 @@ dense), conv weights OIHW, dense weights [out, in].
 """
 
 import numpy as np
-from scipy.special import erf
+from scipy.special import erfc
 
 
 def _f64(a):
@@ -101,9 +101,11 @@ def relu6(y):
 
 
 def gelu(y):
-    """Exact GELU: y * Phi(y) with Phi the standard normal CDF."""
+    """Exact GELU: y * Phi(y) with Phi the standard normal CDF, Phi(y) =
+    erfc(-y / sqrt 2) / 2 (the same function as (1 + erf(y / sqrt 2)) / 2
+    without its cancellation for y << 0, where 1 + erf loses every digit)."""
     y = _f64(y)
-    return y * 0.5 * (1.0 + erf(y / np.sqrt(2.0)))
+    return y * 0.5 * erfc(-y / np.sqrt(2.0))
 
 
 def leaky_relu(y, alpha=0.1):

@@ -180,6 +180,17 @@ def test_gelu_against_math_erf_and_odd_part():
     assert ops.gelu(np.array([0.0]))[0] == 0.0
 
 
+def test_gelu_far_left_tail_against_ndtr():
+    """y * Phi(y) for y << 0, against SciPy's normal CDF routine (ndtr, not
+    the erfc the oracle calls): relative accuracy down to y = -37, where
+    Phi(y) is about 6e-300; the form (1 + erf(y / sqrt 2)) / 2 cancels to
+    nothing there (already about 20% off at y = -8)."""
+    from scipy.special import ndtr
+    y = -np.geomspace(1.0, 37.0, 500)
+    np.testing.assert_allclose(ops.gelu(y), y * ndtr(y), rtol=1e-12, atol=0)
+    assert np.all(ops.gelu(y) < 0)
+
+
 def test_gelu_against_normal_table(golden_dir):
     with open(os.path.join(golden_dir, "normal_cdf_table.json")) as f:
         t = json.load(f)
