@@ -2375,7 +2375,10 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
     for (int bm : bms)
       for (int bn : bns) {
         if (bm == 32 && p.M >= 48) continue;
-        if (bm >= 128 && p.M < 32 * bm) continue;
+        // large tiles only where they still give the CUs a useful share of
+        // tiles (wide GEMMs with few rows, such as a transformer FFN, have
+        // many column tiles)
+        if (bm >= 128 && ((int64_t)(p.M + bm - 1) / bm) * ((p.Kp + bn - 1) / bn) < 96) continue;
         if (bn >= 128 && p.Kp < bn) continue;
         for (int ns = 1; ns <= 4; ++ns) {
           const int threads = nt * kgr;

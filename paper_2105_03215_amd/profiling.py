@@ -19,6 +19,10 @@ classes  per kernel class of one workload: pure kernel time (kernel trace),
          HBM bytes read / written (FETCH_SIZE / WRITE_SIZE runs, scaled by a
          copy of known size), GB/s against 8 TB/s, and for the MFMA classes
          the MFMA busy fraction and the bf16 MFMA FLOPs issued -> JSON.
+run      runs one workload's engine alone (autotuned, HIP-graph replay) for a
+         kernel trace of it: the small configurations (single conv, ResNet-18
+         block, batch-1 networks, BERT FFN) are cut into runs by their launch
+         count (--launches-per-run) instead of a marker kernel.
 
 Usage:
   python -m paper_2105_03215_amd.profiling stats --trace X_kernel_trace.csv \
@@ -68,7 +72,13 @@ def _is_conv(name, kernels=CONV_KERNELS):
 
 def _last_runs(rows, name_key, last_runs, marker=RUN_MARKER, skip_last=0):
     """The rows of the last `last_runs` runs before the final `skip_last`
-    runs (a run starts at its marker kernel)."""
+    runs (a run starts at its marker kernel, or is `marker` dispatches long
+    when the marker is a number)."""
+    if isinstance(marker, int):
+        end = len(rows) - skip_last * marker
+        if end - last_runs * marker < 0:
+            raise RuntimeError("only %d dispatches in the trace" % len(rows))
+        return rows[end - last_runs * marker:end], last_runs
     hit = marker if callable(marker) else (lambda n: marker in n)
     starts = [i for i, r in enumerate(rows) if hit(r[name_key])]
     if len(starts) < last_runs + skip_last:
@@ -264,9 +274,45 @@ def class_counters(trace, fetch, write, mfma, copy_fetch, copy_write, copy_mib, 
     return doc
 
 
+def run_workload(name, batch, runs, warmup, autotune=True):
+    """One workload's engine alone: autotune (unless off), `warmup` runs,
+    then `runs` HIP-graph replays, nothing after them (so the trace ends
+    with them)."""
+    import torch
+
+    from . import capi, runtime, workloads
+
+    wl = workloads.build(name, **({("batch" if name == "bert_ffn" else "n"): batch} if batch else {}))
+    sg = capi.Subgraph(wl.graph, wl.consts, device=0)
+    try:
+        dev = "cuda:0"
+        s = torch.cuda.Stream(device=dev)
+        ins = runtime.inputs_for(sg, wl.inputs, dev)
+        outs = runtime.outputs_for(sg, dev)
+        torch.cuda.synchronize()
+        sg.set_options(autotune=autotune, graph_replay=True)
+        for _ in range(warmup):
+            sg.run(ins, outs, s)
+        s.synchronize()
+        for _ in range(runs):
+            sg.run(ins, outs, s)
+        s.synchronize()
+        launches = sg.launches()
+    finally:
+        sg.close()
+    return {"workload": name, "batch": batch, "runs": runs, "launches_per_run": len(launches),
+            "flops_per_run": sum(l["flops"] for l in launches), "launches": [l["name"] for l in launches]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd_name", required=True)
+    r = sub.add_parser("run", help="run one workload's engine alone (for a kernel trace)")
+    r.add_argument("--workload", required=True)
+    r.add_argument("--batch", type=int, default=0, help="batch size (networks); 0: the workload's default")
+    r.add_argument("--runs", type=int, default=50)
+    r.add_argument("--warmup", type=int, default=10)
+    r.add_argument("--no-autotune", action="store_true", help="keep the built-in (or forced) kernel choice")
     a = sub.add_parser("stats")
     a.add_argument("--trace", required=True)
     a.add_argument("--cmd", required=True)
@@ -279,6 +325,8 @@ def main():
     a.add_argument("--unit", default="FLOP", help="FLOP, or OP for integer work")
     a.add_argument("--skip-last", type=int, default=0, help="runs at the end of the trace to leave out")
     a.add_argument("--int8", action="store_true", help="the int8 MFMA class, runs cut at the int8 stem")
+    a.add_argument("--launches-per-run", type=int, default=0,
+                   help="cut runs by their dispatch count instead of the marker kernel")
     b = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy-fetch", "copy-write", "workload", "out"):
         b.add_argument("--" + k, required=True)
@@ -294,12 +342,20 @@ def main():
     c.add_argument("--copy-mib", type=int, required=True)
     c.add_argument("--last-runs", type=int, required=True)
     c.add_argument("--marker", default=RUN_MARKER)
+    c.add_argument("--launches-per-run", type=int, default=0,
+                   help="cut runs by their dispatch count instead of the marker kernel")
     c.add_argument("--trace-runs", type=int, default=20)
     c.add_argument("--trace-skip-last", type=int, default=0,
                    help="runs at the end of the trace to leave out (the bench's per-launch-event profile runs)")
     c.add_argument("--launches-json", default=None,
                    help="bench --dump-launches table: algorithmic bytes and flops per class")
     args = ap.parse_args()
+    if args.cmd_name == "run":
+        print(json.dumps(run_workload(args.workload, args.batch, args.runs, args.warmup, not args.no_autotune)),
+              flush=True)
+        return
+    if args.cmd_name in ("stats", "classes") and args.launches_per_run > 0:
+        args.marker = args.launches_per_run
     if args.cmd_name == "classes":
         alg_b = alg_f = None
         if args.launches_json:

@@ -202,6 +202,40 @@ def test_dense_composite(case):
     _check_bf16(g.finish(), "dense " + name)
 
 
+def _bf16_grid(lo_exp, hi_exp):
+    """Every bfloat16 value v with 2^lo_exp <= |v| < 2^hi_exp, both signs, and 0."""
+    mags = [(1.0 + m / 128.0) * 2.0 ** e for e in range(lo_exp, hi_exp) for m in range(128)]
+    return np.array([0.0] + mags + [-v for v in mags], dtype=np.float32)
+
+
+@pytest.mark.parametrize("rows", [32, 256], ids=["dense_rows", "implicit_gemm"])
+def test_gelu_every_bf16_value(rows):
+    """GELU of every bf16 value in +-[2^-12, 16) through a dense composite
+    with identity weights (x . I = x exactly in fp32), so the output is the
+    kernel's GELU of x rounded to bf16: within one bf16 ulp of the oracle's
+    exact-erf GELU everywhere and equal to it almost everywhere (the float32
+    evaluation may fall on the other side of a rounding boundary only where
+    the exact value lies within its error of one).  32 rows take the few-row
+    dense kernel, 256 the implicit-GEMM kernel's epilogue."""
+    announce("gelu over every bf16 value, %d rows" % rows)
+    vals = _bf16_grid(-12, 4)
+    c = 64
+    x = np.resize(vals, rows * c).reshape(rows, c).astype(np.float32)
+    graph = {"format": "byoc-subgraph", "version": 1,
+             "inputs": [{"name": "x", "shape": [rows, c], "dtype": "bf16", "layout": "ROWMAJOR"}],
+             "constants": [{"name": "w", "index": 0, "shape": [c, c], "dtype": "f32"}],
+             "nodes": [{"name": "y", "composite": "dense_gelu", "inputs": ["x", "w"], "out_dtype": "bf16"}],
+             "outputs": [{"name": "y", "dtype": "bf16", "layout": "ROWMAJOR"}]}
+    wl = workloads.Workload(graph, [np.eye(c, dtype=np.float32)], [x], rows * c * c, rows * c * c)
+    gpu, launches = _run_gpu(wl)
+    ref = oracle.run_graph(graph, wl.consts, wl.inputs, mode="bf16io")[0]
+    ok = within_one_ulp(gpu[0], ref)
+    assert ok.all(), (x[~ok][:5], gpu[0][~ok][:5], ref[~ok][:5])
+    same = np.mean(gpu[0] == ref)
+    print("gelu: %.5f of the bf16 outputs equal the oracle's (launches %s)" % (same, [l["name"] for l in launches]))
+    assert same >= 0.999
+
+
 def test_pools_and_add():
     g = GraphBuilder("op_pools", 1300)
     x = g.input("x", [2, 64, 29, 29], "normal")

@@ -43,6 +43,20 @@ def test_stats_counts_only_the_last_runs(tmp_path):
         profiling.stats(str(p), "cmd", str(out), last_runs=9)
 
 
+def test_stats_cut_by_launch_count(tmp_path):
+    """Workloads without a marker kernel: the last runs are the last
+    runs x launches-per-run dispatches (a run here is 4 dispatches)."""
+    p = tmp_path / "trace.csv"
+    _trace(p, [(0, 3), (1, 1), (2, 1)])
+    out = tmp_path / "s.txt"
+    profiling.stats(str(p), "cmd", str(out), last_runs=2, marker=4)
+    text = out.read_text()
+    assert "(2 runs of the subgraph" in text
+    assert "65.0 us per run" in text            # stem 10 + conv 50 + pool 5
+    with pytest.raises(RuntimeError):
+        profiling.stats(str(p), "cmd", str(out), last_runs=4, marker=4)
+
+
 def _counters(path, rows, counter):
     with open(path, "w", newline="") as f:
         w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
