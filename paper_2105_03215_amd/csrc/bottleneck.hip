@@ -757,6 +757,13 @@ using P64c = Bn<64, 64, 256, 1, 8, 14, 7, 1, 1, 1, 5>;
 using D128a = Bn<128, 256, 512, 2, 7, 14, 8, 2, 1, 1, 5>;  // projection, stride 2
 using D128b = Bn<128, 256, 512, 2, 4, 28, 8, 2, 1, 1, 4>;
 using D128c = Bn<128, 256, 512, 2, 7, 14, 8, 2, 1, 1, 3>;
+// small tiles for small batches (4 x 7 output pixels, 4 waves): at batch 1
+// the block's grids are a few dozen workgroups, so a workgroup's own
+// latency sets the time
+using V64d = Bn<64, 256, 256, 1, 4, 7, 4, 2, 1, 1, 4>;
+using V128d = Bn<128, 512, 512, 1, 4, 7, 4, 2, 1, 1, 4>;
+using P64d = Bn<64, 64, 256, 1, 4, 7, 4, 1, 1, 1, 4>;
+using D128d = Bn<128, 256, 512, 2, 4, 7, 4, 2, 1, 1, 4>;
 // int8 codes: the 64 mid channels of a pixel fill half a slice (one MFMA
 // step per tap), so three taps fit a phase B stage
 using Q64a = Bn<64, 256, 256, 1, 8, 28, 7, 2, 1, 1, 6, true>;
@@ -773,24 +780,25 @@ using E128b = Bn<128, 256, 512, 2, 4, 28, 8, 2, 1, 1, 4, true>;
 using E128c = Bn<128, 256, 512, 2, 7, 14, 8, 2, 1, 1, 6, true>;
 
 // f(Bn{}) on variant v of a kind, or `none` for an unknown one
+// (bf16 kinds: 4 variants, the last the small-batch tile; int8: 3)
 template <class R, class Fn>
 R with_variant(bool i8, int F, int CIN, int COUT, int S, int v, R none, Fn&& f) {
-  if (v < 0 || v > 2) return none;
+  if (v < 0 || v > (i8 ? 2 : 3)) return none;
   if (S == 1 && F == 64 && CIN == 256 && COUT == 256) {
     if (i8) return v == 0 ? f(Q64a{}) : v == 1 ? f(Q64b{}) : f(Q64c{});
-    return v == 0 ? f(V64a{}) : v == 1 ? f(V64b{}) : f(V64c{});
+    return v == 0 ? f(V64a{}) : v == 1 ? f(V64b{}) : v == 2 ? f(V64c{}) : f(V64d{});
   }
   if (S == 1 && F == 128 && CIN == 512 && COUT == 512) {
     if (i8) return v == 0 ? f(Q128a{}) : v == 1 ? f(Q128b{}) : f(Q128c{});
-    return v == 0 ? f(V128a{}) : v == 1 ? f(V128b{}) : f(V128c{});
+    return v == 0 ? f(V128a{}) : v == 1 ? f(V128b{}) : v == 2 ? f(V128c{}) : f(V128d{});
   }
   if (S == 1 && F == 64 && CIN == 64 && COUT == 256) {
     if (i8) return v == 0 ? f(R64a{}) : v == 1 ? f(R64b{}) : f(R64c{});
-    return v == 0 ? f(P64a{}) : v == 1 ? f(P64b{}) : f(P64c{});
+    return v == 0 ? f(P64a{}) : v == 1 ? f(P64b{}) : v == 2 ? f(P64c{}) : f(P64d{});
   }
   if (S == 2 && F == 128 && CIN == 256 && COUT == 512) {
     if (i8) return v == 0 ? f(E128a{}) : v == 1 ? f(E128b{}) : f(E128c{});
-    return v == 0 ? f(D128a{}) : v == 1 ? f(D128b{}) : f(D128c{});
+    return v == 0 ? f(D128a{}) : v == 1 ? f(D128b{}) : v == 2 ? f(D128c{}) : f(D128d{});
   }
   return none;
 }
@@ -808,7 +816,7 @@ const char* variant_name() {
 }  // namespace
 
 int bottleneck_variants(bool i8, int F, int CIN, int COUT, int S) {
-  return with_variant(i8, F, CIN, COUT, S, 0, 0, [](auto) { return 3; });
+  return with_variant(i8, F, CIN, COUT, S, 0, 0, [i8](auto) { return i8 ? 3 : 4; });
 }
 
 const char* bottleneck_variant_name(bool i8, int F, int CIN, int COUT, int S, int v) {

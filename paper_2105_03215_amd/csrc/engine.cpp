@@ -539,10 +539,13 @@ void Planner::find_post_adds() {
 // by the next conv, of a kind (mid width, channels of x, channels of the
 // output) the fused kernel is compiled for, run as one launch (the
 // intermediates stay in LDS)
-// when its finest tiling gives at least one workgroup per CU (256): measured
-// on MI355X over ResNet-50 v1, fusing made batches 1-8 0.8-5% slower and
-// batch 16 (stage 1 only) and 32 faster.  BYOC_FUSE_BLOCK=0 keeps the three
-// launches everywhere, =1 fuses every supported block.
+// on bf16 activations always: with the small-tile variant (4 x 7 pixels, 4
+// waves) offered to the autotune, measured on MI355X over ResNet-50 v1,
+// fusing every stage-1 and stage-2 block made batch 1 12% faster (0.370 ->
+// 0.324 ms), batches 2-8 4-13% faster and batches 16 and 32 faster than
+// unfused.  On int8 codes (no small-tile variant) when the finest tiling
+// gives at least one workgroup per CU (256).  BYOC_FUSE_BLOCK=0 keeps the
+// three launches everywhere, =1 fuses every supported block.
 void Planner::find_blocks() {
   block_mid.assign(g.nodes.size(), -1);
   block_proj.assign(g.nodes.size(), -1);
@@ -613,7 +616,7 @@ void Planner::find_blocks() {
     int most = 0;
     for (int v = 0; v < bottleneck_variants(i8, F, CIN, COUT, S); ++v)
       most = std::max(most, bottleneck_tiles(i8, F, CIN, COUT, S, v, (int)ys[0], (int)ys[2], (int)ys[3]));
-    if (!always && most < 256) continue;
+    if (!always && i8 && most < 256) continue;
     if (xs[0] * xs[2] * xs[3] * std::max(CIN, COUT) * 2 >= (int64_t(1) << 31)) continue;
     block_mid[ci] = bi;
     block_proj[ci] = pi;

@@ -115,25 +115,25 @@ def test_fused_block_matches_unfused_and_oracle(case, monkeypatch):
 VARIANT_CASES = [CASES[0], CASES[2], CASES[4], CASES[6]]
 
 
-@pytest.mark.parametrize("case", VARIANT_CASES, ids=[c[0] for c in VARIANT_CASES])
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_every_block_variant_and_autotune_bitwise(case, monkeypatch):
     announce("block variants " + case[0])
     wl = _blocks(case)
     ref, names0 = _run(wl, monkeypatch, dict(FUSED, BYOC_BLOCK_VARIANT="0"))
     seen = {tuple(n for n in names0 if n.startswith("bottleneck_"))}
-    for v in (1, 2):
+    for v in (1, 2, 3):  # 3: the small-batch tile (4 x 7 pixels, 4 waves)
         out, names = _run(wl, monkeypatch, dict(FUSED, BYOC_BLOCK_VARIANT=str(v)))
         seen.add(tuple(n for n in names if n.startswith("bottleneck_")))
         assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), v
-    assert len(seen) == 3, seen  # the variants are distinct kernels
+    assert len(seen) == 4, seen  # the variants are distinct kernels
     out, _ = _run(wl, monkeypatch, FUSED, options={"autotune": True, "graph_replay": True})
     assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
 
 
 def test_block_fusion_rule(monkeypatch):
-    """Three launches where fusion is off (BYOC_FUSE_BLOCK=0), for a width
-    pair without a fused kernel, and by default for a block whose finest
-    tiling gives fewer than 256 workgroups; one launch by default from 256."""
+    """Three launches where fusion is off (BYOC_FUSE_BLOCK=0) and for a width
+    pair without a fused kernel; one launch by default for a supported bf16
+    block at any batch (batch 1 at 28x28: 28 tiles of 4 x 7 pixels)."""
     announce("block fusion rule")
     wl = _blocks(("odd", 1, 192, 48, 192, 14, 14, 1), n_blocks=1)
     _, names = _run(wl, monkeypatch, FUSED)
@@ -141,9 +141,9 @@ def test_block_fusion_rule(monkeypatch):
     wl = _blocks(CASES[0], n_blocks=1)
     _, names = _run(wl, monkeypatch, {"BYOC_FUSE_BLOCK": "0"})
     assert not any(n.startswith("bottleneck_") for n in names), names
-    _, names = _run(wl, monkeypatch, {})  # batch 2 at 56x56: 56 tiles of 8x14
-    assert not any(n.startswith("bottleneck_") for n in names), names
-    wl = _blocks(("s1_bs10", 10, 256, 64, 256, 56, 56, 1), n_blocks=1)  # 280 tiles of 8x14
+    _, names = _run(wl, monkeypatch, {})
+    assert sum(n.startswith("bottleneck_") for n in names) == 1, names
+    wl = _blocks(("s2_bs1", 1, 512, 128, 512, 28, 28, 1), n_blocks=1)
     _, names = _run(wl, monkeypatch, {})
     assert sum(n.startswith("bottleneck_") for n in names) == 1, names
 
