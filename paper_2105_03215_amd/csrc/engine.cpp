@@ -693,16 +693,17 @@ void Planner::plan_block(int ci) {
 // MobileNetV2 inverted-residual blocks: [x -> 1x1 conv (+bias, act) ->]
 // depthwise 3x3 pad 1 stride 1 or 2 (+bias, act) -> 1x1 conv (+bias, act)
 // [+ x], each intermediate read only by the next composite, of channel
-// counts the fused kernel is compiled for, run as one launch when the tiling
-// gives at least one workgroup per CU (256).  BYOC_FUSE_IR=0 keeps the
-// separate launches everywhere, =1 fuses every supported block.
+// counts the fused kernel is compiled for, run as one launch at any batch:
+// measured on MI355X over MobileNetV2, fusing every supported block made
+// batch 1 17% faster (0.239 -> 0.199 ms), batches 2-8 8-13% faster and
+// batch 16 faster than fusing only the blocks with 256 or more tiles.
+// BYOC_FUSE_IR=0 keeps the separate launches everywhere.
 void Planner::find_ir_blocks() {
   ir_dw.assign(g.nodes.size(), -1);
   ir_exp.assign(g.nodes.size(), -1);
   in_ir.assign(g.nodes.size(), false);
   const char* env = std::getenv("BYOC_FUSE_IR");
   if (!bf16 || (env && env[0] == '0')) return;
-  const bool always = env && env[0] == '1';
   std::vector<int> uses(g.values.size(), 0);
   for (const Node& n : g.nodes) {
     for (int a : {n.data, n.residual, n.other})
@@ -756,9 +757,6 @@ void Planner::find_ir_blocks() {
     if (c.residual >= 0 && (c.residual != x || S != 1 || CIN != COUT)) continue;
     const int nv = ir_block_variants(CIN, F, COUT, S);
     if (nv <= 0) continue;
-    int most = 0;
-    for (int v = 0; v < nv; ++v) most = std::max(most, ir_block_tiles(CIN, F, COUT, S, v, (int)ys[0], (int)ys[2], (int)ys[3]));
-    if (!always && most < 256) continue;
     if (xs[0] * xs[2] * xs[3] * std::max(std::max(CIN, F), COUT) * 2 >= (int64_t(1) << 31)) continue;
     ir_dw[ci] = di;
     ir_exp[ci] = ai;

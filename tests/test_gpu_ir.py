@@ -146,16 +146,16 @@ def test_mobilenet_v2_fused_equals_unfused_bitwise(monkeypatch):
 
 
 def test_ir_fusion_rule(monkeypatch):
-    """By default a block fuses when its tiling gives at least 256
-    workgroups: MobileNetV2 at batch 16 fuses its early blocks, at batch 1
-    none; BYOC_FUSE_IR=0 never fuses."""
+    """By default every supported block fuses, at any batch: MobileNetV2 at
+    batch 16 and at batch 1 fuses its eleven blocks up to 64 -> 96
+    channels; BYOC_FUSE_IR=0 never fuses."""
     announce("inverted-residual fusion rule")
     from paper_2105_03215_amd import workloads
     wl = workloads.build("mobilenet_v2", n=16)
     _, names = _run(wl, monkeypatch, {})
-    assert sum(n.startswith("ir_block_") for n in names) >= 6, names
+    assert sum(n.startswith("ir_block_") for n in names) == 11, names
     _, names = _run(wl, monkeypatch, {"BYOC_FUSE_IR": "0"})
     assert not any(n.startswith("ir_block_") for n in names)
     wl = workloads.build("mobilenet_v2", n=1)
     _, names = _run(wl, monkeypatch, {})
-    assert not any(n.startswith("ir_block_") for n in names), names
+    assert sum(n.startswith("ir_block_") for n in names) == 11, names
