@@ -305,7 +305,10 @@ def _config_lines(args, dev, stream):
             "images_per_s": round(n / (m.ms * 1e-3), 1), "ms_per_step": round(m.ms, 4),
             "conv_tflops": round(fl / (m.ms * 1e-3) / 1e12, 2), "launches": len(m.launches),
             "launch_mode": m.extra["launch_mode"],
-            "depthwise": {k: cls["depthwise"][k] for k in ("launches", "ms", "bytes", "gbs", "hbm_frac")},
+            "depthwise": ({k: cls["depthwise"][k] for k in ("launches", "ms", "bytes", "gbs", "hbm_frac")}
+                          if "depthwise" in cls else
+                          {"launches": 0, "note": "every depthwise conv runs inside its fused inverted-residual "
+                                                  "block (ir_block kernels, in the conv/dense MFMA class)"}),
             "kernel_classes": cls}
 
     m = _measure(args, "bert_ffn", workloads.build("bert_ffn"), dev, stream)

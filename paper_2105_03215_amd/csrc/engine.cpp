@@ -694,9 +694,13 @@ void Planner::plan_block(int ci) {
 // depthwise 3x3 pad 1 stride 1 or 2 (+bias, act) -> 1x1 conv (+bias, act)
 // [+ x], each intermediate read only by the next composite, of channel
 // counts the fused kernel is compiled for, run as one launch at any batch:
-// measured on MI355X over MobileNetV2, fusing every supported block made
-// batch 1 17% faster (0.239 -> 0.199 ms), batches 2-8 8-13% faster and
-// batch 16 faster than fusing only the blocks with 256 or more tiles.
+// measured on MI355X over MobileNetV2, fusing every block with at most 64
+// input channels made batch 1 17% faster (0.239 -> 0.199 ms), batches 2-8
+// 8-13% faster and batch 16 faster than fusing only the blocks with 256 or
+// more tiles.  The wider blocks (96 and 160 input channels, expanded to
+// 576 and 960) stay separate unless BYOC_FUSE_IR=1: their workgroups walk
+// 9 or 15 slices of the expanded width one after the other (18-39 us per
+// block at batch 1 and 16 against 14-19 us for the three launches).
 // BYOC_FUSE_IR=0 keeps the separate launches everywhere.
 void Planner::find_ir_blocks() {
   ir_dw.assign(g.nodes.size(), -1);
@@ -704,6 +708,7 @@ void Planner::find_ir_blocks() {
   in_ir.assign(g.nodes.size(), false);
   const char* env = std::getenv("BYOC_FUSE_IR");
   if (!bf16 || (env && env[0] == '0')) return;
+  const bool always = env && env[0] == '1';
   std::vector<int> uses(g.values.size(), 0);
   for (const Node& n : g.nodes) {
     for (int a : {n.data, n.residual, n.other})
@@ -756,7 +761,7 @@ void Planner::find_ir_blocks() {
     if (ai >= 0 && F == CIN) continue;  // (the kind is told apart by F != CIN)
     if (c.residual >= 0 && (c.residual != x || S != 1 || CIN != COUT)) continue;
     const int nv = ir_block_variants(CIN, F, COUT, S);
-    if (nv <= 0) continue;
+    if (nv <= 0 || (!always && CIN > 64)) continue;
     if (xs[0] * xs[2] * xs[3] * std::max(std::max(CIN, F), COUT) * 2 >= (int64_t(1) << 31)) continue;
     ir_dw[ci] = di;
     ir_exp[ci] = ai;

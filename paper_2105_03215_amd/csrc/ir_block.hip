@@ -50,10 +50,12 @@ using namespace dma;
 
 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 
-template <int CT_, int S_, int TH_, int TW_, bool EXP_, int V_, int MINW_>
+template <int CT_, int S_, int TH_, int TW_, bool EXP_, int V_, int MINW_, int XS_ = 1, int FMAX_ = 512>
 struct Ir {
   static constexpr int CT = CT_, S = S_, TH = TH_, TW = TW_;  // CT: 16-channel tiles of the output
   static constexpr bool EXP = EXP_;                           // expand conv present
+  static constexpr int XS = XS_;      // 64-channel slices of the block input (the window's rows per pixel)
+  static constexpr int FMAX = FMAX_;  // the largest expanded width (bias tables)
   static constexpr int NW = 8, NT = 64 * NW;
   static constexpr int IH = (TH - 1) * S + 3, IW = (TW - 1) * S + 3;  // input window
   static constexpr int HPX = IH * IW, HPXP = (HPX + 15) / 16 * 16;
@@ -70,24 +72,29 @@ struct Ir {
   static constexpr int TC = (NPC + NW - 1) / NW;          // pairs per wave
   static constexpr int ROW = 128;
   // LDS plan (bytes)
-  static constexpr int OFF_X = 0, XB = HPXP * ROW;
+  // the window: slice j of pixel px in row j * HPXP + px
+  static constexpr int OFF_X = 0, XB = XS * HPXP * ROW;
   static constexpr int OFF_E = OFF_X + XB, EB = EXP ? HPXP * ROW : 0;
   static constexpr int OFF_D = OFF_E + EB, DB = OPXP * ROW;
-  static constexpr int OFF_WE = OFF_D + DB, WEB = EXP ? 64 * ROW : 0;
+  // expand weights of a slice of F: input slice j of row r in row j * 64 + r
+  static constexpr int OFF_WE = OFF_D + DB, WEB = EXP ? XS * 64 * ROW : 0;
   // depthwise slice: 9 taps x 64 float32 channels, tap t in rows 2t, 2t + 1 (x 2 buffers)
   static constexpr int OFF_WD = OFF_WE + WEB, WDB = 3 * 1024;
   static constexpr int OFF_WP = OFF_WD + 2 * WDB, WPB = CT * 16 * ROW;
-  static constexpr int BBLK = EXP ? 5 : 3;    // 1 KB blocks: [be (2),] bd (2), bp (1)
+  // 1 KB blocks of float32 biases: [be (FB),] bd (FB), bp (PB)
+  static constexpr int FB = FMAX * 4 / 1024, PB = (CT * 16 * 4 + 1023) / 1024;
+  static constexpr int BBLK = (EXP ? FB : 0) + FB + PB, LBB = (BBLK + NW - 1) / NW;
   static constexpr int OFF_B = OFF_WP + WPB;
   static constexpr int OFF_JUNK = OFF_B + BBLK * 1024;
   static constexpr int MINW = MINW_;  // waves per SIMD the registers are held to
   static constexpr int LDS = OFF_JUNK + 1024;
   // 1 KB fills (8 rows of 128 bytes) per thread
-  static constexpr int XBLK = HPXP / 8, LX = (XBLK + NW - 1) / NW;
-  static constexpr int LWE = EXP ? 1 : 0;  // 8 blocks: one per wave
+  static constexpr int XBLK = XS * HPXP / 8, LX = (XBLK + NW - 1) / NW;
+  static constexpr int LWE = EXP ? XS : 0;  // 8 blocks per input slice: one per wave
   static constexpr int LWD = 1;            // 3 blocks
   static constexpr int WPBLK = CT * 2, LWP = (WPBLK + NW - 1) / NW;
-  static_assert(CT * 16 <= 256 && LDS <= kLdsLimit && TH % V == 0 && (V == 1 || S == 1), "shape");
+  static_assert(CT * 16 <= 320 && FMAX % 256 == 0 && LDS <= kLdsLimit && TH % V == 0 && (V == 1 || S == 1),
+                "shape");
   static_assert(LWE + LWD <= 63 && LWP <= 63, "vmcnt immediate");
 };
 
@@ -173,8 +180,8 @@ __global__ __launch_bounds__(B::NT, B::MINW) void ir_block_kernel(IrParams p) {
   const uint32_t base = lds_addr(lds);
   const uint32_t junk = base + B::OFF_JUNK;
   const float* sbe = reinterpret_cast<const float*>(lds + B::OFF_B);
-  const float* sbd = sbe + (B::EXP ? 512 : 0);
-  const float* sbp = sbd + 512;
+  const float* sbd = sbe + (B::EXP ? B::FMAX : 0);
+  const float* sbp = sbd + B::FMAX;
 
   // ---- load plans ----------------------------------------------------------
   const i32x4 xr = buffer_rsrc(p.x, p.x_bytes);
@@ -184,28 +191,34 @@ __global__ __launch_bounds__(B::NT, B::MINW) void ir_block_kernel(IrParams p) {
   auto dst = [&](uint32_t region, int blk, int nblk) {
     return __builtin_amdgcn_readfirstlane(blk < nblk ? region + blk * 1024 : junk);
   };
-  // the window: row px (position (px / IW, px % IW)), logical chunk lk ^ (px & 7)
+  // the window: slice j of position px (px / IW, px % IW) in row
+  // j * HPXP + px, logical chunk lk ^ (px & 7)
   uint32_t xoff[B::LX];
 #pragma unroll
   for (int u = 0; u < B::LX; ++u) {
     const int blk = wave + NW * u;
-    const int px = 8 * blk + (lane >> 3);
+    const int j = blk / (B::HPXP / 8);
+    const int px = 8 * (blk - j * (B::HPXP / 8)) + (lane >> 3);
     const int xc = lk ^ (px & 7);
+    const int ch = j * 64 + xc * 8;
     uint32_t off = kOOB;
-    if (blk < B::XBLK && px < B::HPX && xc * 8 < CIN) {
+    if (blk < B::XBLK && px < B::HPX && ch < CIN) {
       const int ih = ih0 + px / IW, iw = iw0 + px % IW;
       if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W)
-        off = (uint32_t)((((n * H + ih) * W + iw) * CIN + xc * 8) * 2);
+        off = (uint32_t)((((n * H + ih) * W + iw) * CIN + ch) * 2);
     }
     xoff[u] = off;
   }
   // weight rows 8 * blk + lane / 8, logical chunk lk ^ (row & 7)
   const int wrow = 8 * wave + (lane >> 3);
   const int wch = lk ^ (wrow & 7);
-  auto issue_we = [&](int f) {  // expand rows f*64 + wrow, input channels (one 128-byte slice)
+  auto issue_we = [&](int f) {  // expand rows f*64 + wrow, input slice j's 64 channels
     if constexpr (B::EXP) {
-      const uint32_t off = f < FS ? (uint32_t)(((f * 64 + wrow) * p.ldE + wch * 8) * 2) : kOOB;
-      lds_fill16(wer, dst(base + B::OFF_WE, wave, 8), off);
+#pragma unroll
+      for (int j = 0; j < B::XS; ++j) {
+        const uint32_t off = f < FS ? (uint32_t)(((f * 64 + wrow) * p.ldE + j * 64 + wch * 8) * 2) : kOOB;
+        lds_fill16(wer, dst(base + B::OFF_WE + j * 64 * B::ROW, wave, 8), off);
+      }
     }
   };
   auto issue_wd = [&](int f) {  // row r: tap r / 2, channels f*64 + 32 (r % 2) + 4 lk (no permutation)
@@ -229,14 +242,16 @@ __global__ __launch_bounds__(B::NT, B::MINW) void ir_block_kernel(IrParams p) {
   // ---- prologue: the window, the biases, the first slice's weights ----------
 #pragma unroll
   for (int u = 0; u < B::LX; ++u) lds_fill16(xr, dst(base + B::OFF_X, wave + NW * u, B::XBLK), xoff[u]);
-  {
-    // blocks [0-1: be,] then 2 of bd, 1 of bp (fp32, zero past their ends)
-    const int k = wave - (B::EXP ? 2 : 0);  // index past the be blocks
-    const void* src = k < 0 ? p.be : k < 2 ? p.bd : p.bp;
-    const int bytes = k < 0 ? p.be_bytes : k < 2 ? p.bd_bytes : p.bp_bytes;
-    const int sub = k < 0 ? wave : k < 2 ? k : 0;
-    const uint32_t off = wave < B::BBLK ? (uint32_t)(sub * 1024 + lane * 16) : kOOB;
-    lds_fill16(buffer_rsrc(src, bytes), dst(base + B::OFF_B, wave, B::BBLK), off);
+#pragma unroll
+  for (int u = 0; u < B::LBB; ++u) {
+    // blocks [FB of be,] then FB of bd, PB of bp (fp32, zero past their ends)
+    const int blk = wave + NW * u;
+    const int k = blk - (B::EXP ? B::FB : 0);  // index past the be blocks
+    const void* src = k < 0 ? p.be : k < B::FB ? p.bd : p.bp;
+    const int bytes = k < 0 ? p.be_bytes : k < B::FB ? p.bd_bytes : p.bp_bytes;
+    const int sub = k < 0 ? blk : k < B::FB ? k : k - B::FB;
+    const uint32_t off = blk < B::BBLK ? (uint32_t)(sub * 1024 + lane * 16) : kOOB;
+    lds_fill16(buffer_rsrc(src, bytes), dst(base + B::OFF_B, blk, B::BBLK), off);
   }
   issue_we(0);
   issue_wd(0);
@@ -263,15 +278,17 @@ __global__ __launch_bounds__(B::NT, B::MINW) void ir_block_kernel(IrParams p) {
       const char* we = lds + B::OFF_WE;
       const char* xs = lds + B::OFF_X;
       for (int ks = 0; ks < ka; ++ks) {
-        const int c = ks * 4 + lq;
+        const int sl = ks >> 1, c = (ks & 1) * 4 + lq;  // input slice, chunk in it
+        const char* wes = we + sl * 64 * B::ROW;
+        const char* xss = xs + sl * B::HPXP * B::ROW;
         uint4 a[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) a[i] = *(const uint4*)(we + slot_off(16 * i + l16, c));
+        for (int i = 0; i < 4; ++i) a[i] = *(const uint4*)(wes + slot_off(16 * i + l16, c));
 #pragma unroll
         for (int t = 0; t < B::TA; ++t) {
           const int j = wave + NW * t;
           if (j < B::NTA) {
-            const bf16x8 b = as_bf16x8(*(const uint4*)(xs + slot_off(16 * j + l16, c)));
+            const bf16x8 b = as_bf16x8(*(const uint4*)(xss + slot_off(16 * j + l16, c)));
 #pragma unroll
             for (int i = 0; i < 4; ++i)
               accA[t][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a[i]), b, accA[t][i], 0, 0, 0);
@@ -396,11 +413,11 @@ __global__ __launch_bounds__(B::NT, B::MINW) void ir_block_kernel(IrParams p) {
     const int oh = o / TW, ow = o - (o / TW) * TW;
     const int ch = 16 * ct + 4 * lq;
     const bool ok = pr < B::NPC && o < B::OPX && h0 + oh < p.P && w0 + ow < p.Q && ch < COUT;
-    const float4 bb = *(const float4*)(sbp + (ch < 256 ? ch : 0));
+    const float4 bb = *(const float4*)(sbp + (ch < B::CT * 16 ? ch : 0));
     float r[4] = {0.f, 0.f, 0.f, 0.f};
     if (p.res && ok) {  // the block input at this output pixel (stride 1: window position (oh + 1, ow + 1))
-      const int row = (oh + 1) * IW + ow + 1;
-      const uint2 rv = *(const uint2*)(xs + slot_off(row, ch >> 3) + (ch & 7) * 2);
+      const int row = (ch >> 6) * B::HPXP + (oh + 1) * IW + ow + 1;
+      const uint2 rv = *(const uint2*)(xs + slot_off(row, (ch & 63) >> 3) + (ch & 7) * 2);
       r[0] = __uint_as_float(rv.x << 16), r[1] = __uint_as_float(rv.x & 0xFFFF0000u);
       r[2] = __uint_as_float(rv.y << 16), r[3] = __uint_as_float(rv.y & 0xFFFF0000u);
     }
@@ -450,6 +467,21 @@ struct Variants<CT, 1, true> {  // stride 1
   using V2 = Ir<CT, 1, 4, 4, true, 1, 6>;
 };
 
+// Wider blocks (input 96 or 160 channels: two or three slices of the
+// window per pixel; expanded width up to 1024; output up to 320 channels).
+template <int CT, int S, int XS>
+struct VariantsX {
+  using V0 = Ir<CT, 1, 8, 8, true, 2, 2, XS, 1024>;
+  using V1 = Ir<CT, 1, 4, 8, true, 1, 2, XS, 1024>;
+  using V2 = Ir<CT, 1, 4, 4, true, 1, 4, XS, 1024>;
+};
+template <int CT, int XS>
+struct VariantsX<CT, 2, XS> {  // stride 2: the window is (2 TH + 1) x (2 TW + 1)
+  using V0 = Ir<CT, 2, 4, 8, true, 1, 2, XS, 1024>;
+  using V1 = Ir<CT, 2, 4, 4, true, 1, 4, XS, 1024>;
+  using V2 = Ir<CT, 2, 2, 8, true, 1, 4, XS, 1024>;
+};
+
 template <class K, class R, class Fn>
 R pick(int v, Fn&& fn) {
   return v == 0 ? fn(typename K::V0{}) : v == 1 ? fn(typename K::V1{}) : fn(typename K::V2{});
@@ -457,9 +489,18 @@ R pick(int v, Fn&& fn) {
 
 template <class R, class Fn>
 R with_kind(int cin, int f, int cout, int s, int v, R none, Fn&& fn) {
-  // the window is one slice of x, the expand reduction at most 64 channels
-  if (v < 0 || v > 2 || cin > 64 || cin % 8 != 0 || f % 8 != 0 || cout % 8 != 0 || f > 512) return none;
+  if (v < 0 || v > 2 || cin % 8 != 0 || f % 8 != 0 || cout % 8 != 0) return none;
   const int ct = (cout + 15) / 16;
+  if (cin > 64) {  // MobileNetV2's later blocks
+    if (f > 1024 || f == cin) return none;
+    if (cin <= 128 && s == 1 && ct == 6) return pick<VariantsX<6, 1, 2>, R>(v, fn);
+    if (cin <= 128 && s == 2 && ct == 10) return pick<VariantsX<10, 2, 2>, R>(v, fn);
+    if (cin > 128 && cin <= 192 && s == 1 && ct == 10) return pick<VariantsX<10, 1, 3>, R>(v, fn);
+    if (cin > 128 && cin <= 192 && s == 1 && ct == 20) return pick<VariantsX<20, 1, 3>, R>(v, fn);
+    return none;
+  }
+  // the window is one slice of x, the expand reduction at most 64 channels
+  if (f > 512) return none;
   if (f == cin) return ct == 1 && s == 1 ? pick<Variants<1, 1, false>, R>(v, fn) : none;
   if (s == 2) {
     if (ct == 2) return pick<Variants<2, 2, true>, R>(v, fn);
@@ -476,8 +517,9 @@ R with_kind(int cin, int f, int cout, int s, int v, R none, Fn&& fn) {
 template <class B>
 const char* kind_name() {
   static char buf[64];
-  static const int once = std::snprintf(buf, sizeof(buf), "ir_block_c%d_s%d_%dx%d_v%d_w%d%s", B::CT * 16, B::S,
-                                        B::TH, B::TW, B::V, B::MINW, B::EXP ? "" : "_noexp");
+  static const int once = std::snprintf(buf, sizeof(buf), "ir_block_c%d_s%d_%dx%d_v%d_w%d%s%s", B::CT * 16, B::S,
+                                        B::TH, B::TW, B::V, B::MINW, B::EXP ? "" : "_noexp",
+                                        B::XS == 1 ? "" : B::XS == 2 ? "_x2" : "_x3");
   (void)once;
   return buf;
 }

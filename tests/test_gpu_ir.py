@@ -38,6 +38,11 @@ CASES = [
     ("s2_32_192_64_28x28", 2, 32, 6, 64, 28, 28, 2),
     ("s1_64_384_64_14x14", 3, 64, 6, 64, 14, 14, 1),
     ("s1_64_384_96_ragged_9x11", 2, 64, 6, 96, 9, 11, 1),
+    # the later blocks: the window two or three slices deep, expanded width up to 960
+    ("s1_96_576_96_14x14", 2, 96, 6, 96, 14, 14, 1),
+    ("s2_96_576_160_ragged_13x11", 1, 96, 6, 160, 13, 11, 2),
+    ("s1_160_960_160_7x7", 3, 160, 6, 160, 7, 7, 1),
+    ("s1_160_960_320_ragged_9x6", 2, 160, 6, 320, 9, 6, 1),
 ]
 
 
@@ -59,7 +64,7 @@ def _blocks(case, n_blocks=2):
         res = y if (st == 1 and c_in == cout) else None
         y = g.conv(hh, cout, 1, pad=0, act=None, residual=res, name="b%d.project" % i)
         c_in = cout
-        if cout > 64:  # the next block's input would not fit the fused kernel's window
+        if cout > 160:  # the next block's input would not fit the fused kernel's window
             break
     g.output(y)
     return g.finish()
@@ -110,7 +115,8 @@ def test_fused_ir_block_matches_unfused_and_oracle(case, monkeypatch):
     assert err <= BF16_TOL
 
 
-VARIANT_CASES = [CASES[0], CASES[1], CASES[2], CASES[5], CASES[6], CASES[7]]
+VARIANT_CASES = [CASES[0], CASES[1], CASES[2], CASES[5], CASES[6], CASES[7], CASES[8], CASES[9], CASES[10],
+                 CASES[11]]
 
 
 @pytest.mark.parametrize("case", VARIANT_CASES, ids=[c[0] for c in VARIANT_CASES])
@@ -139,21 +145,24 @@ def test_mobilenet_v2_fused_equals_unfused_bitwise(monkeypatch):
     wl = workloads.build("mobilenet_v2", n=2, hw=160)
     fused, names = _run(wl, monkeypatch, dict(UNFUSED_KG1, BYOC_FUSE_IR="1"))
     n_ir = sum(n.startswith("ir_block_") for n in names)
-    assert n_ir >= 10, names  # expansion 1, the 24- and 32-channel stages, the 64-channel ones, 64 -> 96
+    assert n_ir == 17, names  # every block
     plain, pnames = _run(wl, monkeypatch, UNFUSED_KG1)
     assert not any(n.startswith("ir_block_") for n in pnames)
     assert torch.equal(_bits(fused), _bits(plain))
 
 
 def test_ir_fusion_rule(monkeypatch):
-    """By default every supported block fuses, at any batch: MobileNetV2 at
-    batch 16 and at batch 1 fuses its eleven blocks up to 64 -> 96
-    channels; BYOC_FUSE_IR=0 never fuses."""
+    """By default every supported block with at most 64 input channels
+    fuses, at any batch: MobileNetV2 at batch 16 and at batch 1 fuses its
+    eleven blocks up to 64 -> 96 channels; BYOC_FUSE_IR=1 fuses all 17
+    (the wider ones too), BYOC_FUSE_IR=0 none."""
     announce("inverted-residual fusion rule")
     from paper_2105_03215_amd import workloads
     wl = workloads.build("mobilenet_v2", n=16)
     _, names = _run(wl, monkeypatch, {})
     assert sum(n.startswith("ir_block_") for n in names) == 11, names
+    _, names = _run(wl, monkeypatch, {"BYOC_FUSE_IR": "1"})
+    assert sum(n.startswith("ir_block_") for n in names) == 17, names
     _, names = _run(wl, monkeypatch, {"BYOC_FUSE_IR": "0"})
     assert not any(n.startswith("ir_block_") for n in names)
     wl = workloads.build("mobilenet_v2", n=1)
