@@ -15,7 +15,7 @@
 // tap outside reads zeros).  The affine input needs sum (x_q - Z_x) w_q: the
 // host folds -Z_x * (sum of all weights of channel k) into the bias, and for
 // a pixel whose window crosses the border the epilogue adds back Z_x times
-// the weight sums of its taps outside the image (wtap[k][r*S + s]).
+// the weight sums of its taps outside the image (wtap[r*S + s][k]).
 //
 // Reduction groups (KG > 1): KG groups of WM x WN waves each run their own
 // ring over every KG-th stage of the reduction (group g: stages g, g + KG,

@@ -1487,7 +1487,9 @@ Status Planner::plan_i8() {
 // implicit-GEMM kernel reads them: packed [rows][Kgp], column (r*S + s)*Cp + c
 // (im2col rows: (r*S + s)*4 + c; row_ld > 0: r*row_ld + s*4 + c, the fused
 // stem's cells); qch [rows][2] = {bias, factor bits}; with
-// `border`, wtap [rows][R*S] the weight sums per tap.  False, with the reason
+// `border`, wtap [R*S][rows] the weight sums per tap (tap-major: the 8
+// consecutive channels an epilogue thread finishes are 32 contiguous
+// bytes of one tap).  False, with the reason
 // in *err_msg, on a value outside the kernel's ranges.
 bool Planner::quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im2col, bool border,
                                std::vector<uint8_t>& packed, std::vector<int32_t>& qch, std::vector<int32_t>& wtap,
@@ -1544,7 +1546,7 @@ bool Planner::quantize_conv_i8(const Node& n, int Cp, int Kgp, int rows, bool im
                              : im2col ? (size_t)(r * S + s2) * 4 + c : (size_t)(r * S + s2) * Cp + c;
           packed[(size_t)k * Kgp + col] = (uint8_t)(int8_t)wq;
           total += wq;
-          if (border) wtap[(size_t)k * RS + r * S + s2] += wq;
+          if (border) wtap[(size_t)(r * S + s2) * rows + k] += wq;
         }
     double bq = 0.0;
     if (bcst) {
@@ -1707,6 +1709,7 @@ void Planner::plan_node_i8(int ni) {
       std::memcpy(tb.data(), wtap.data(), tb.size());
       L.other = host_blob(std::move(tb));
     }
+    q.wtap_ld = rows;
     q.zx = xv.qzero;
     q.zy = yv.qzero;
     q.lo = lo;

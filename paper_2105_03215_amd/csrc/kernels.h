@@ -279,7 +279,8 @@ hipError_t launch_cast(const void* x, bool src_bf16, void* y, bool dst_bf16, int
 struct QConvParams {
   ConvParams g;         // geometry and operands: x, w, res, y hold int8 data; bias, partial unused
   const int32_t* qch;   // [>= Kp][2]: bias with the input zero point folded in, float32 factor bits
-  const int32_t* wtap;  // [>= Kp][R*S] weight sums per tap (border correction), or nullptr
+  const int32_t* wtap;  // [R*S][wtap_ld >= Kp] weight sums per tap (border correction), or nullptr
+  int wtap_ld;
   int zx;               // input zero point (applied at the border through wtap)
   int zy, lo, hi;       // output zero point; activation clamp in output codes (within [-128, 127])
   int zr;               // residual zero point

@@ -26,15 +26,24 @@ __device__ __forceinline__ uint2 finish8_i8(int a[8], const int2* qc, uint2 rv, 
     const int ih0 = pp * p.sh - p.pt, iw0 = qq * p.sw - p.pl;
     const bool inside = ih0 >= 0 && iw0 >= 0 && ih0 + p.R <= p.H && iw0 + p.S <= p.W;
     if (!inside) {
+      // the table is tap-major: the 8 channels of one tap are two 16-byte loads
       int corr[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-      for (int rr = 0; rr < p.R; ++rr)
-        for (int ss = 0; ss < p.S; ++ss) {
-          const int ih = ih0 + rr, iw = iw0 + ss;
-          if ((unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W) continue;
-          const int* wt = q.wtap + (size_t)k * RS + rr * p.S + ss;
+      auto add_tap = [&](int t) {
+        const int4* wt = reinterpret_cast<const int4*>(q.wtap + (size_t)t * q.wtap_ld + k);
+        const int4 lo = wt[0], hi = wt[1];
+        corr[0] += lo.x, corr[1] += lo.y, corr[2] += lo.z, corr[3] += lo.w;
+        corr[4] += hi.x, corr[5] += hi.y, corr[6] += hi.z, corr[7] += hi.w;
+      };
+      if (p.R == 3 && p.S == 3) {  // unrolled: the loads of all outside taps in flight together
 #pragma unroll
-          for (int c8 = 0; c8 < 8; ++c8) corr[c8] += wt[c8 * RS];
+        for (int t = 0; t < 9; ++t)
+          if ((unsigned)(ih0 + t / 3) >= (unsigned)p.H || (unsigned)(iw0 + t % 3) >= (unsigned)p.W) add_tap(t);
+      } else {
+        for (int t = 0; t < RS; ++t) {
+          const int rr = t / p.S, ss = t - rr * p.S;
+          if ((unsigned)(ih0 + rr) >= (unsigned)p.H || (unsigned)(iw0 + ss) >= (unsigned)p.W) add_tap(t);
         }
+      }
 #pragma unroll
       for (int c8 = 0; c8 < 8; ++c8) a[c8] += q.zx * corr[c8];
     }
