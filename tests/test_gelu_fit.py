@@ -42,8 +42,7 @@ def test_erfc_relative_error_in_float32(lo, hi):
 def test_gelu_from_the_fit_matches_the_exact_form():
     """x * Phi(x) assembled as the kernel does (Phi = erfc(a) / 2 below
     zero, 1 - erfc(a) / 2 above, a = |x| / sqrt 2 capped at 10) against
-    x * erfc(-x / sqrt 2) / 2 in float64: relative error where no step
-    is denormal, absolute below (x under about -12.5)."""
+    x * erfc(-x / sqrt 2) / 2 in float64."""
     x = np.linspace(-14.0, 14.0, 200001).astype(np.float32)
     a = np.minimum(np.abs(x) * np.float32(0.70710678118654752440), np.float32(10.0)).astype(np.float32)
     ec = gelu_erfc_fit.erfc_f32(a, _kernel_coefficients())
@@ -51,8 +50,9 @@ def test_gelu_from_the_fit_matches_the_exact_form():
     got = (x * phi).astype(np.float64)
     x64 = x.astype(np.float64)
     ref = x64 * 0.5 * erfc(-x64 / np.sqrt(2.0))
-    # float32 is denormal below 2^-126 (absolute steps of 2^-149); erfc(a) / 2
-    # reaches that range while x * Phi(x) is still a few times above it
-    normal = np.abs(ref) >= 2.0 ** -116
-    assert np.max(np.abs(got[normal] - ref[normal]) / np.abs(ref[normal])) < 2e-6
-    assert np.max(np.abs(got[~normal] - ref[~normal])) < 2.0 ** -140
+    # the float32 rounding of a = |x| / sqrt 2 alone moves erfc(a) by up to
+    # about 2 a^2 2^-24 relative (exp(-a^2) is that sensitive to a), on top of
+    # the approximation's 1e-6; float32 steps are absolute (2^-149) in the
+    # denormal range that erfc(a) / 2 enters below x of about -13
+    bound = (2e-6 + 2.5e-7 * a.astype(np.float64) ** 2) * np.abs(ref) + 2.0 ** -140
+    assert np.all(np.abs(got - ref) <= bound)
