@@ -232,12 +232,20 @@ def _measure(args, key, wl, dev, stream, timing="steps", graph=None, consts=None
             res["ms"], res["launch_mode"] = best[1], best[0]
             ms = res["ms"]["median"]
         else:
-            sg.set_options(graph_replay=not args.eager)
-            for _ in range(args.warmup):
-                sg.run(ins, outs, stream)
-            torch.cuda.synchronize()
-            ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
-            res["launch_mode"] = "direct launches" if args.eager else "HIP graph replay"
+            # throughput engines: the K steps timed in both modes, as the
+            # headline is
+            best = None
+            for label, replay in [("direct launches", False)] + ([] if args.eager else [("HIP graph replay", True)]):
+                sg.set_options(graph_replay=replay)
+                for _ in range(args.warmup):
+                    sg.run(ins, outs, stream)
+                torch.cuda.synchronize()
+                t_ms, _ = _timed_runs(sg, ins, outs, stream, args.steps)
+                res["ms_" + ("graph" if replay else "direct")] = round(t_ms, 4)
+                if best is None or t_ms < best[0]:
+                    best = (t_ms, label, replay)
+            sg.set_options(graph_replay=best[2])
+            ms, res["launch_mode"] = best[0], best[1]
         host = [runtime.to_host_f64(o) for o in outs]
         sg.set_options(graph_replay=False)
         launches = sg.launches()
@@ -496,7 +504,8 @@ def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
                 and tj.get("conv_kernel_digest") == profiling.conv_kernel_digest(profiling.I8_SOURCES)):
             traffic = tj.get("conv_bytes_per_step")
     return {"workload": "%s_bs%d_int8" % (variant, n), "images_per_s": round(n / (ms * 1e-3), 1),
-            "ms_per_step": round(ms, 4), "dtype": "int8 codes, int32 accumulation",
+            "ms_per_step": round(ms, 4), "launch_mode": m.extra["launch_mode"],
+            "dtype": "int8 codes, int32 accumulation",
             "calibration": "%d images through the executor, %.2f s" % (calib_images, calib_s),
             "parity": "int8 codes are exact integer sums and float32 rescalings, independent of the tiling: "
                       "checked bit for bit against the int8 oracle on all 32 images in the GPU tests",
@@ -511,20 +520,22 @@ def _quantized(args, wl, dev, stream, calib_images=2, variant=None):
 
 def _other_workload(args, name, batch, dev, stream):
     """Throughput and conv-class roofline of another fully offloaded network
-    (same measurement as the headline: graph replay, autotune, inputs in
-    HBM)."""
+    (same measurement as the headline: autotune, inputs in HBM, the faster
+    of direct launches and graph replay)."""
     from paper_2105_03215_amd import capi, workloads
 
     wl = workloads.build(name, n=batch)
     m = _measure(args, "%s_bs%d" % (name, batch), wl, dev, stream)
     roof = _roofline(m.launches, m.per_launch, m.ms)
     out = {"workload": m.key, "images_per_s": round(batch / (m.ms * 1e-3), 1),
-           "ms_per_step": round(m.ms, 4), "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
+           "ms_per_step": round(m.ms, 4), "launch_mode": m.extra["launch_mode"],
+           "gflop_per_image": round(2 * wl.macs / batch / 1e9, 3),
            "conv_tflops": roof["achieved"], "conv_frac": roof["frac"], "launches": len(m.launches)}
     if not args.no_quantized:  # the same network partially quantized, as the headline's int8 leg
         try:
             q = _quantized(args, wl, dev, stream, variant=name)
             out["int8"] = {"images_per_s": q["images_per_s"], "ms_per_step": q["ms_per_step"],
+                           "launch_mode": q["launch_mode"],
                            "conv_tops": q["roofline"]["achieved"], "conv_frac": q["roofline"]["frac"]}
         except capi.ByocError as e:  # operators without an int8 form
             out["int8"] = {"skipped": str(e)}
@@ -555,7 +566,7 @@ def main():
                     help="keep the built-in conv kernel choice (no on-device tuning at setup)")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache per-step timing")
     ap.add_argument("--eager", action="store_true",
-                    help="headline value from direct launches instead of HIP-graph replay")
+                    help="headline value from direct launches even where HIP-graph replay is faster")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device copy of MIB MiB three times (counter calibration)")
@@ -601,7 +612,9 @@ def main():
         sg.run(ins, outs, stream)
     torch.cuda.synchronize()
     ms_graph, wall_graph = _timed_runs(sg, ins, outs, stream, args.steps)
-    if args.eager:
+    # the engine's figure is the faster of its two run modes, both timed
+    # the same way above (as for the latency-bound configurations)
+    if args.eager or ms_eager < ms_graph:
         sg.set_options(graph_replay=False)
         ms, wall, mode = ms_eager, wall_eager, "direct launches"
     else:

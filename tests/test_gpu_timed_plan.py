@@ -2,10 +2,10 @@
 
 bench.py times every workload with the engine's autotune on (each conv /
 dense launch takes the fastest of its result-identical kernel variants,
-chosen by timing on the device) and HIP-graph replay on a non-default
-stream.  Here each of those configurations is built the same way, at the
-benchmark's size, replayed several times (the output buffer poisoned between
-replays), and compared:
+chosen by timing on the device) on a non-default stream, in HIP-graph replay
+and in direct launches, and reports the faster mode.  Here each of those
+configurations is built the same way, at the benchmark's size, run several
+times in both modes (the output buffer poisoned between runs), and compared:
 
 * bit for bit with the engine's built-in plan (autotune changes speed only);
 * with the oracle (bf16io mode) on every image / token row of the batch,
@@ -43,9 +43,9 @@ def _bitwise_equal(a, b):
 
 
 def timed_plan_outputs(wl, replays=3):
-    """Outputs of the benchmark's launch configuration (autotune + graph
-    replay on a side stream) after `replays` replays, checked bit for bit
-    against the built-in plan's on every replay."""
+    """Outputs of the benchmark's launch configuration (autotune, a side
+    stream) after `replays` graph replays and as many direct-launch runs,
+    checked bit for bit against the built-in plan's after every run."""
     sg = capi.Subgraph(wl.graph, wl.consts, device=0)
     s = torch.cuda.Stream(device=DEV)
     try:
@@ -55,16 +55,18 @@ def timed_plan_outputs(wl, replays=3):
         sg.run(ins, ref, s)
         s.synchronize()
         sg.set_options(autotune=True)
-        sg.set_options(graph_replay=True)
         out = runtime.outputs_for(sg, DEV)
-        for rep in range(replays):
-            for o in out:
-                o.fill_(float("nan"))
-            torch.cuda.synchronize()
-            sg.run(ins, out, s)
-            s.synchronize()
-            for a, b in zip(ref, out):
-                assert _bitwise_equal(a, b), "replay %d differs from the built-in plan" % rep
+        for replay in (True, False):
+            sg.set_options(graph_replay=replay)
+            for rep in range(replays):
+                for o in out:
+                    o.fill_(float("nan"))
+                torch.cuda.synchronize()
+                sg.run(ins, out, s)
+                s.synchronize()
+                for a, b in zip(ref, out):
+                    assert _bitwise_equal(a, b), "%s run %d differs from the built-in plan" % (
+                        "graph" if replay else "direct", rep)
         names = [l["name"] for l in sg.launches()]
         return [runtime.to_host_f64(o) for o in out], names
     finally:
