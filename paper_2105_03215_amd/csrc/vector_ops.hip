@@ -70,21 +70,29 @@ __global__ __launch_bounds__(kThreads) void depthwise_kernel(DwParams p) {
 // the bias once, and then forms the V outputs from registers, so each input
 // row is fetched once per strip instead of once per tap and output.  Lanes
 // take consecutive channel groups, then consecutive columns, so every load
-// instruction of a wave reads one contiguous run of NHWC memory.  Grid:
-// x over (column, channel group) in blocks of kThreads, y over (image,
-// strip).  The taps are summed in the order (row, column) like the generic
-// kernel, each output from the bias up, so both kernels give the same bits.
+// instruction of a wave reads one contiguous run of NHWC memory.  Blocks:
+// xb blocks of kThreads over (column, channel group) per (image, strip),
+// image-major.  The hardware deals workgroups round-robin to the 8 XCDs, so
+// XCD x takes the contiguous run of blocks [x * per_xcd, (x + 1) * per_xcd):
+// the blocks of one image, which read each other's halo rows and edge
+// columns, share one L2 and fetch each input line from HBM once.  The taps
+// are summed in the order (row, column) like the generic kernel, each output
+// from the bias up, so both kernels give the same bits.
 template <int ST, int V, int MODE>
-__global__ __launch_bounds__(kThreads) void depthwise3x3_kernel(DwParams p, int x_bytes, int strips, uint64_t mg_g,
-                                                                  uint64_t mg_strips) {
+__global__ __launch_bounds__(kThreads) void depthwise3x3_kernel(DwParams p, int x_bytes, int strips, int xb,
+                                                                  int per_xcd, int blocks, uint64_t mg_g,
+                                                                  uint64_t mg_strips, uint64_t mg_xb) {
   constexpr int NR = (V - 1) * ST + 3;  // input rows of a strip
   const int G = p.Cp / 8;
-  const int pos = blockIdx.x * kThreads + threadIdx.x;
+  const int blk = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (blk >= blocks) return;
+  const int ns = mdiv(blk, mg_xb);  // (image, strip)
+  const int pos = (blk - ns * xb) * kThreads + threadIdx.x;
   if (pos >= G * p.Q) return;
   const int q = mdiv(pos, mg_g);
   const int g = pos - q * G;
-  const int n = mdiv(blockIdx.y, mg_strips);
-  const int p0 = (blockIdx.y - n * strips) * V;
+  const int n = mdiv(ns, mg_strips);
+  const int p0 = (ns - n * strips) * V;
   const int ih0 = p0 * ST - p.pt, iw0 = q * ST - p.pl;
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p.x), (short)0, x_bytes, kBufferFlags);
@@ -470,14 +478,18 @@ template <int ST, int V>
 hipError_t launch_dw3x3(const DwParams& p, int x_bytes, hipStream_t s) {
   const int G = p.Cp / 8;
   const int strips = (p.P + V - 1) / V;
-  const dim3 grid((unsigned)((G * p.Q + kThreads - 1) / kThreads), (unsigned)(p.N * strips));
+  const int xb = (G * p.Q + kThreads - 1) / kThreads;
+  const int blocks = xb * p.N * strips;  // < 2^25 (checked by the caller)
+  const int per_xcd = (blocks + 7) / 8;
+  const unsigned grid = 8u * (unsigned)per_xcd;
   const int mode = act_mode(p.act);
+  const uint64_t mg = magic40(G), ms = magic40(strips), mx = magic40(xb);
   if (mode == 1)
-    depthwise3x3_kernel<ST, V, 1><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, magic40(G), magic40(strips));
+    depthwise3x3_kernel<ST, V, 1><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, xb, per_xcd, blocks, mg, ms, mx);
   else if (mode == 0)
-    depthwise3x3_kernel<ST, V, 0><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, magic40(G), magic40(strips));
+    depthwise3x3_kernel<ST, V, 0><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, xb, per_xcd, blocks, mg, ms, mx);
   else
-    depthwise3x3_kernel<ST, V, 2><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, magic40(G), magic40(strips));
+    depthwise3x3_kernel<ST, V, 2><<<grid, kThreads, 0, s>>>(p, x_bytes, strips, xb, per_xcd, blocks, mg, ms, mx);
   return hipGetLastError();
 }
 
@@ -486,11 +498,13 @@ hipError_t launch_dw3x3(const DwParams& p, int x_bytes, hipStream_t s) {
 hipError_t launch_depthwise(const DwParams& p, hipStream_t s) {
   const int64_t x_bytes = (int64_t)p.N * p.H * p.W * p.Cp * 2;
   const int64_t y_elems = (int64_t)p.N * p.P * p.Q * p.Cp;
-  // strip kernel: 3x3 taps, equal strides of 1 or 2, 32-bit offsets, and
-  // the index products of the magic divisions below 2^40
+  // strip kernel: 3x3 taps, equal strides of 1 or 2, 32-bit offsets, the
+  // index products of the magic divisions below 2^40 and fewer than 2^25
+  // workgroups
   const bool strip = p.R == 3 && p.S == 3 && p.sh == p.sw && (p.sh == 1 || p.sh == 2) && p.Cp % 8 == 0 &&
                      x_bytes < (int64_t(1) << 31) && y_elems < (int64_t(1) << 31) &&
-                     (int64_t)(p.Cp / 8) * p.Q < (int64_t(1) << 20) && (int64_t)p.N * p.P < (int64_t(1) << 20);
+                     (int64_t)(p.Cp / 8) * p.Q < (int64_t(1) << 20) && (int64_t)p.N * p.P < (int64_t(1) << 20) &&
+                     ((int64_t)(p.Cp / 8) * p.Q + kThreads - 1) / kThreads * p.N * p.P < (int64_t(1) << 25);
   if (strip) {
     // strip height (output rows per thread): 4 (stride 1) and 2 (stride 2)
     // by default; BYOC_DW_STRIP=<v1>,<v2> picks 2, 4 or 8 and 1, 2 or 4

@@ -183,6 +183,44 @@ def test_depthwise_composite(case):
     assert any(l["kind"] == "depthwise" for l in launches)
 
 
+def _dw_graph(case, seed):
+    name, shape, r, stride, pad, act, res = case
+    g = GraphBuilder("op_" + name, seed)
+    x = g.input("x", list(shape), "uniform")
+    n, c, h, w = shape
+    p = (h + 2 * pad - r) // stride + 1
+    q = (w + 2 * pad - r) // stride + 1
+    rname = g.input("res", [n, c, p, q], "normal") if res else None
+    g.output(g.conv(x, c, r, stride=stride, pad=pad, groups=c, act=act, residual=rname, name="y"))
+    return g.finish()
+
+
+# every 3x3 case with symmetric padding, and MobileNetV2's unfused depthwise
+# layers at batch 16 (many workgroups per XCD)
+DW_STRIP_CASES = [c for c in DW_CASES if c[2] == 3 and c[3] in (1, 2) and isinstance(c[4], int)] + [
+    ("dw_s1_c576_14x14_bs16", (16, 576, 14, 14), 3, 1, 1, "relu6", False),
+    ("dw_s2_c576_14x14_bs16", (16, 576, 14, 14), 3, 2, 1, "relu6", False),
+    ("dw_s1_c960_7x7_bs16", (16, 960, 7, 7), 3, 1, 1, "relu6", False),
+]
+
+
+@pytest.mark.parametrize("case", DW_STRIP_CASES, ids=[c[0] for c in DW_STRIP_CASES])
+def test_depthwise_strip_heights_bitwise(case, monkeypatch):
+    """Every strip height of the 3x3 strip kernel (2, 4, 8 output rows per
+    thread at stride 1; 1, 2, 4 at stride 2) gives the same bits, and the
+    default one is within one ulp of the oracle."""
+    wl = _dw_graph(case, 1150 + DW_STRIP_CASES.index(case))
+    monkeypatch.delenv("BYOC_DW_STRIP", raising=False)
+    _check_bf16(wl, "depthwise strips " + case[0])
+    ref, _ = _run_gpu(wl)
+    for strip in ("2,1", "8,4"):
+        monkeypatch.setenv("BYOC_DW_STRIP", strip)
+        got, launches = _run_gpu(wl)
+        assert any(l["kind"] == "depthwise" for l in launches)
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b), (case[0], strip)
+
+
 DENSE_CASES = [
     ("fc_m1_k2048_n1000", 1, 2048, 1000, None, False),
     ("ffn1_m33_gelu", 33, 768, 3072, "gelu", False),
