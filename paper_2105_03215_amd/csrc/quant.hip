@@ -141,11 +141,16 @@ __global__ __launch_bounds__(kThreads) void maxpool_i8_kernel(PoolParams p) {
 }
 
 // One thread per (n, p, q, 16-channel group): exact integer taps, 16 codes
-// per 16-byte load of activations and of weights.
-__global__ __launch_bounds__(kThreads) void depthwise_i8_kernel(QDwParams p) {
+// per 16-byte load of activations and of weights.  Blocks of kThreads
+// threads in XCD-contiguous order (the hardware deals workgroups
+// round-robin to the 8 XCDs; XCD x takes blocks [x * per_xcd, (x + 1) *
+// per_xcd)), so neighbouring rows, which share the taps' input rows, are
+// fetched through one L2.
+__global__ __launch_bounds__(kThreads) void depthwise_i8_kernel(QDwParams p, int per_xcd) {
   const int G = p.Cp / 16;
   const int total = p.N * p.P * p.Q * G;  // < 2^31 / 16: bytes of the output
-  for (int i = blockIdx.x * kThreads + threadIdx.x; i < total; i += gridDim.x * kThreads) {
+  const int i = ((blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3)) * kThreads + threadIdx.x;
+  if (i < total) {
     const int g = i % G;
     const int pix = i / G;
     const int qq = pix % p.Q;
@@ -282,7 +287,8 @@ hipError_t launch_dequantize_i8(const int8_t* x, void* y, bool dst_bf16, int N, 
 
 hipError_t launch_depthwise_i8(const QDwParams& p, hipStream_t s) {
   if (p.Cp % 16 != 0) return hipErrorInvalidValue;
-  depthwise_i8_kernel<<<grid_for((int64_t)p.N * p.P * p.Q * (p.Cp / 16)), kThreads, 0, s>>>(p);
+  const int per_xcd = (int)((grid_for((int64_t)p.N * p.P * p.Q * (p.Cp / 16)) + 7) / 8);
+  depthwise_i8_kernel<<<8u * (unsigned)per_xcd, kThreads, 0, s>>>(p, per_xcd);
   return hipGetLastError();
 }
 
