@@ -416,17 +416,25 @@ int max_patch_pixels(const ConvParams& p, int bm) {
 }
 
 constexpr int kHaloWaves = 8;
-constexpr int kLPs[] = {4, 5, 6, 8};
+constexpr int kLPs[] = {4, 5, 6, 8};  // 128-pixel tiles
+constexpr int kLPs64[] = {3, 4};      // 64-pixel tiles
 
 // Smallest patch capacity (loads per thread) that holds every tile's patch
 // and fits the LDS with `nsw` weight stages; 0 if none.
 int choose_lp(const ConvParams& p, int bm, int bn, int stages, int* npb, int cs) {
   *npb = p.Cp / cs > 1 ? 2 : 1;
   const int need = max_patch_pixels(p, bm);
+  auto fits = [&](int lp) {
+    return lp * kHaloWaves * 8 >= need &&
+           halo_lds(bn, taps_per_stage(stages), stages, lp, *npb, kHaloWaves) <= kLdsLimit;
+  };
+  if (bm == 64) {
+    for (int lp : kLPs64)
+      if (fits(lp)) return lp;
+    return 0;
+  }
   for (int lp : kLPs)
-    if (lp * kHaloWaves * 8 >= need &&
-        halo_lds(bn, taps_per_stage(stages), stages, lp, *npb, kHaloWaves) <= kLdsLimit)
-      return lp;
+    if (fits(lp)) return lp;
   return 0;
 }
 
@@ -451,8 +459,20 @@ hipError_t launch_one(const QConvParams& q_in, hipStream_t s) {
 }
 
 template <int STAGES, bool I8>
-hipError_t launch_stages(const QConvParams& q, int lp, int npb, hipStream_t s) {
+hipError_t launch_stages(const QConvParams& q, int bm, int lp, int npb, hipStream_t s) {
   constexpr int T = taps_per_stage(STAGES);
+  if (bm == 64) {  // 64-pixel tiles (8 waves of 16 pixels x 32 channels): rings of kernel rows only
+    if constexpr (STAGES == 2 || STAGES == 3) {
+      if (npb == 2) {
+        if (lp == 3) return launch_one<64, 64, 4, 2, T, STAGES, 3, 2, I8>(q, s);
+        if (lp == 4) return launch_one<64, 64, 4, 2, T, STAGES, 4, 2, I8>(q, s);
+      } else {
+        if (lp == 3) return launch_one<64, 64, 4, 2, T, STAGES, 3, 1, I8>(q, s);
+        if (lp == 4) return launch_one<64, 64, 4, 2, T, STAGES, 4, 1, I8>(q, s);
+      }
+    }
+    return hipErrorInvalidValue;
+  }
   if (npb == 2) {
     if (lp == 4) return launch_one<128, 64, 4, 2, T, STAGES, 4, 2, I8>(q, s);
     if (lp == 5) return launch_one<128, 64, 4, 2, T, STAGES, 5, 2, I8>(q, s);
@@ -468,12 +488,12 @@ hipError_t launch_stages(const QConvParams& q, int lp, int npb, hipStream_t s) {
 
 template <bool I8>
 hipError_t launch_any(const QConvParams& q, int bm, int bn, int stages, int lp, int npb, hipStream_t s) {
-  if (bm != 128 || bn != 64 || !shape_ok(q.g, I8 ? 128 : kSlice)) return hipErrorInvalidValue;
-  if (stages == 2) return launch_stages<2, I8>(q, lp, npb, s);
-  if (stages == 3) return launch_stages<3, I8>(q, lp, npb, s);
-  if (stages == 4) return launch_stages<4, I8>(q, lp, npb, s);
-  if (stages == 6) return launch_stages<6, I8>(q, lp, npb, s);
-  if (stages == 8) return launch_stages<8, I8>(q, lp, npb, s);
+  if ((bm != 128 && bm != 64) || bn != 64 || !shape_ok(q.g, I8 ? 128 : kSlice)) return hipErrorInvalidValue;
+  if (stages == 2) return launch_stages<2, I8>(q, bm, lp, npb, s);
+  if (stages == 3) return launch_stages<3, I8>(q, bm, lp, npb, s);
+  if (stages == 4) return launch_stages<4, I8>(q, bm, lp, npb, s);
+  if (stages == 6) return launch_stages<6, I8>(q, bm, lp, npb, s);
+  if (stages == 8) return launch_stages<8, I8>(q, bm, lp, npb, s);
   return hipErrorInvalidValue;
 }
 
@@ -481,7 +501,8 @@ hipError_t launch_any(const QConvParams& q, int bm, int bn, int stages, int lp, 
 
 bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb, bool i8) {
   const int cs = i8 ? 128 : kSlice;
-  if (bm != 128 || bn != 64 || !shape_ok(p, cs)) return false;
+  // 128 x 64 tiles at every ring depth; 64 x 64 tiles with rings of kernel rows
+  if (!(bm == 128 || (bm == 64 && (stages == 2 || stages == 3))) || bn != 64 || !shape_ok(p, cs)) return false;
   if (stages != 2 && stages != 3 && stages != 4 && stages != 6 && stages != 8) return false;
   // index math: patch offsets and pixel bases stay within int32
   if ((int64_t)p.N * (p.H + 2) * (p.W + 2) >= (int64_t(1) << 30)) return false;

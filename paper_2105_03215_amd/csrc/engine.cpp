@@ -1222,28 +1222,34 @@ void Planner::plan_node(int ni) {
       // (196 tiles) and loses where the patch is large against the work
       // (64 channels at 56x56), where the implicit-GEMM kernel's 128x128
       // tiles win (128 channels at 28x28) and where 128x64 tiles leave most
-      // CUs idle (512 channels at 7x7, 104 tiles).  BYOC_CONV_HALO=1 takes
-      // it wherever the shape allows, =0 never; a forced tile decides alone.
+      // CUs idle (512 channels at 7x7, 104 tiles).  Where 128x64 tiles are
+      // too few but 64x64 tiles are enough (512 channels at 7x7: 200 tiles)
+      // it runs on 64x64 tiles.  BYOC_CONV_HALO=1 takes it wherever the
+      // shape allows, =0 never; a forced tile decides alone.
       const bool forced = L.tile.halo == 2;
       const char* he = std::getenv("BYOC_CONV_HALO");
       const int64_t halo_tiles = ((p.M + 127) / 128) * ((Kp + 63) / 64);
+      const int64_t halo64_tiles = ((p.M + 63) / 64) * ((Kp + 63) / 64);
       const bool by_rule = Cp >= 256 && halo_tiles >= 160;
-      const bool want = forced || (!std::getenv("BYOC_CONV_TILE") && (he ? he[0] == '1' : by_rule));
+      const bool by_rule64 = Cp >= 256 && !by_rule && halo64_tiles >= 160;
+      const bool want =
+          forced || (!std::getenv("BYOC_CONV_TILE") && (he ? he[0] == '1' : by_rule || by_rule64));
       const int ns = forced ? L.tile.stages : kHaloStages;
+      const int hbm = forced ? L.tile.bm : by_rule64 ? 64 : 128;
       int lp = 0, npb = 0;
       if (forced) {  // a forced halo tile also forgoes split-K
         ConvParams q = p;
         q.splits = 1;
-        if (conv_halo_plan(q, 128, 64, ns, &lp, &npb)) {
+        if (L.tile.bn == 64 && conv_halo_plan(q, hbm, 64, ns, &lp, &npb)) {
           splits = 1;
           kps = (int)((p.Kg + kKPad - 1) / kKPad);
           p.splits = splits;
           p.k_tiles_per_split = kps;
         }
       }
-      if (want && splits == 1 && conv_halo_plan(p, 128, 64, ns, &lp, &npb)) {
+      if (want && splits == 1 && conv_halo_plan(p, hbm, 64, ns, &lp, &npb)) {
         L.tile = ConvTile{};
-        L.tile.bm = 128;
+        L.tile.bm = hbm;
         L.tile.bn = 64;
         L.tile.stages = ns;
         L.tile.threads = 512;
@@ -2367,13 +2373,15 @@ namespace {
 std::vector<ConvTile> conv_candidates(const Launch& L) {
   std::vector<ConvTile> c;
   c.push_back(L.tile_default);
-  if (L.tile_default.halo) {  // the halo kernel: other weight ring depths (same reduction order)
-    for (int ns : {2, 3, 4, 6, 8}) {
-      ConvTile t = L.tile_default;
-      if (ns == t.stages || !conv_halo_plan(L.conv, t.bm, t.bn, ns, &t.lp, &t.npb)) continue;
-      t.stages = ns;
-      c.push_back(t);
-    }
+  if (L.tile_default.halo) {  // the halo kernel: other tiles and weight ring depths (same reduction order)
+    for (int bm : {128, 64})
+      for (int ns : {2, 3, 4, 6, 8}) {
+        ConvTile t = L.tile_default;
+        if ((bm == t.bm && ns == t.stages) || !conv_halo_plan(L.conv, bm, t.bn, ns, &t.lp, &t.npb)) continue;
+        t.bm = bm;
+        t.stages = ns;
+        c.push_back(t);
+      }
     return c;
   }
   if (L.conv.splits > 1 || L.tile_default.mf != 16) return c;

@@ -80,6 +80,8 @@ hipError_t launch_conv_dma(const ConvParams& p, int bm, int bn, int stages, int 
 // thread, lp) and the number of patch buffers (npb) for a tiling; the
 // launcher takes them as planned.  `stages` is the weight ring: 2 or 3
 // stages of three taps (one kernel row), or 4, 6 or 8 stages of one tap.
+// Tiles (bm x bn): 128 x 64 at every ring depth, 64 x 64 with 2 or 3
+// stages; both sum in the same order, so they give the same bits.
 bool conv_halo_plan(const ConvParams& p, int bm, int bn, int stages, int* lp, int* npb, bool i8 = false);
 hipError_t launch_conv_halo(const ConvParams& p, int bm, int bn, int stages, int lp, int npb, hipStream_t s);
 // Fused stem: conv (C <= 4 NCHW input channels, 64 output channels) + bias

@@ -6,8 +6,8 @@ HBM->LDS pipelined kernel (32x64 ... 256x128 pixels x channels), ring depths
 1-4, 4 or 8 waves, the register-staged kernel, and any XCD placement of the
 tiles, all within the reduction-order class of the built-in choice (one
 reduction group, or two or four groups that split the stages).  The 3x3 halo kernel
-(input window staged in LDS) sums in its own order; its weight rings are its
-variants.  Here each variant is forced through the tile override on three
+(input window staged in LDS) sums in its own order; its weight rings and its
+two tiles (128 or 64 pixels x 64 channels) are its variants.  Here each variant is forced through the tile override on three
 layers at their batch-32 shapes and checked:
 
 * within one bf16 ulp of the oracle (plus 2^-16 of the summed term
@@ -130,4 +130,7 @@ def test_every_variant(case, monkeypatch):
         for ring in (2, 3, 4, 6, 8):
             check("halo ring %d" % ring, {"BYOC_CONV_TILE": "h128x64s%d" % ring}, "halo",
                   "conv_halo_128x64_s%d" % ring)
+        for ring in (2, 3):
+            check("halo 64x64 ring %d" % ring, {"BYOC_CONV_TILE": "h64x64s%d" % ring}, "halo",
+                  "conv_halo_64x64_s%d" % ring)
     print("%s: %d variants checked, classes %s" % (name, checked, sorted(firsts)), flush=True)

@@ -148,6 +148,39 @@ def test_conv_halo_composite(case, monkeypatch):
         assert any(nm.startswith("conv_halo_128x64_s%d_" % ring) for nm in names), names
 
 
+HALO64_CASES = [
+    # name, (n, c, h, w), k, act, residual, weight-ring depth of the 64-pixel tile
+    ("c512_7x7_multi_image_res", (3, 512, 7, 7), 128, "relu", True, 3),
+    ("c128_7x7_ragged_k", (5, 128, 7, 7), 136, "relu", False, 2),
+    ("c192_9x5_three_slices", (3, 192, 9, 5), 72, "relu6", False, 3),
+    ("c64_30x30_one_slice", (1, 64, 30, 30), 64, None, False, 2),
+    ("c384_8x8_gelu", (2, 384, 8, 8), 64, "gelu", False, 3),
+]
+
+
+@pytest.mark.parametrize("case", HALO64_CASES, ids=[c[0] for c in HALO64_CASES])
+def test_conv_halo_64_composite(case, monkeypatch):
+    """The windowed kernel's 64-pixel tile: within one ulp of the oracle and
+    bit for bit the 128-pixel tile (the same summation order)."""
+    name, shape, k, act, res, ring = case
+    monkeypatch.setenv("BYOC_CONV_TILE", "h64x64s%d" % ring)
+    g = GraphBuilder("op_halo64_" + name, 1350 + HALO64_CASES.index(case))
+    x = g.input("x", list(shape), "uniform")
+    n, c, h, w = shape
+    rname = g.input("res", [n, k, h, w], "normal") if res else None
+    y = g.conv(x, k, 3, stride=1, pad=1, act=act, residual=rname, name="y")
+    g.output(y)
+    wl = g.finish()
+    launches = _check_bf16(wl, "conv halo 64 " + name)
+    assert any(l["name"].startswith("conv_halo_64x64_s%d_" % ring) for l in launches), launches
+    got, _ = _run_gpu(wl)
+    monkeypatch.setenv("BYOC_CONV_TILE", "h128x64s%d" % ring)
+    ref, launches = _run_gpu(wl)
+    assert any(l["name"].startswith("conv_halo_128x64") for l in launches), launches
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+
+
 DW_CASES = [
     # name, (n, c, h, w), kernel, stride, pad, act, residual
     ("dw_s1_c96", (2, 96, 14, 14), 3, 1, 1, "relu6", False),
