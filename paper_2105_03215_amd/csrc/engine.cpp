@@ -1760,20 +1760,28 @@ void Planner::plan_node_i8(int ni) {
     }
     // 3x3 stride-1 convs with at least 256 input channels and enough 128x64
     // tiles run on the windowed kernel (input window staged in LDS once per
-    // 128-channel slice; the same codes), the rule of the bf16 convs;
-    // BYOC_CONV_HALO=1 takes it wherever the shape allows, =0 never.
+    // 128-channel slice; the same codes), the rule of the bf16 convs, on
+    // 64x64 tiles where only those fill the chip; BYOC_CONV_HALO=1 takes it
+    // wherever the shape allows, =0 never.
     {
-      // BYOC_I8_TILE=h<stages> forces it with that weight ring depth.
+      // BYOC_I8_TILE=h<stages>[b<pixels>] forces it with that weight ring
+      // depth (and tile height, 128 or 64).
       const char* he = std::getenv("BYOC_CONV_HALO");
       const char* te = std::getenv("BYOC_I8_TILE");
       const int64_t halo_tiles = ((int64_t)(p.M + 127) / 128) * ((Kp + 63) / 64);
-      int ns = kHaloStages;
-      bool want = he ? he[0] == '1' : (Cp >= 256 && halo_tiles >= 160);
-      if (te) want = te[0] == 'h' && std::sscanf(te + 1, "%d", &ns) == 1;
+      const int64_t halo64_tiles = ((int64_t)(p.M + 63) / 64) * ((Kp + 63) / 64);
+      const bool r128 = Cp >= 256 && halo_tiles >= 160;
+      const bool r64 = Cp >= 256 && !r128 && halo64_tiles >= 160;
+      int ns = kHaloStages, hbm = r64 ? 64 : 128;
+      bool want = he ? he[0] == '1' : (r128 || r64);
+      if (te) {
+        hbm = 128;
+        want = te[0] == 'h' && std::sscanf(te + 1, "%db%d", &ns, &hbm) >= 1;
+      }
       int lp = 0, npb = 0;
-      if (!im2col && want && conv_halo_plan(p, 128, 64, ns, &lp, &npb, true)) {
+      if (!im2col && want && conv_halo_plan(p, hbm, 64, ns, &lp, &npb, true)) {
         t = ConvTile{};
-        t.bm = 128, t.bn = 64, t.stages = ns, t.threads = 512;
+        t.bm = hbm, t.bn = 64, t.stages = ns, t.threads = 512;
         t.halo = 1, t.lp = lp, t.npb = npb;
       }
     }
@@ -2427,15 +2435,16 @@ std::vector<ConvTile> conv_candidates(const Launch& L) {
 // codes, do not depend on the tiling)
 std::vector<ConvTile> conv_i8_candidates(const Launch& L) {
   std::vector<ConvTile> c{L.tile_default};
-  // the windowed 3x3 kernel, every weight ring depth (int32 sums: every
-  // variant gives the same codes)
-  for (int ns : {2, 3, 4, 6, 8}) {
-    ConvTile t = ConvTile{};
-    t.bm = 128, t.bn = 64, t.stages = ns, t.threads = 512, t.halo = 1;
-    if (!conv_halo_plan(L.qc.g, 128, 64, ns, &t.lp, &t.npb, true)) continue;
-    if (L.tile_default.halo && ns == L.tile_default.stages) continue;
-    c.push_back(t);
-  }
+  // the windowed 3x3 kernel, both tiles, every weight ring depth (int32
+  // sums: every variant gives the same codes)
+  for (int bm : {128, 64})
+    for (int ns : {2, 3, 4, 6, 8}) {
+      ConvTile t = ConvTile{};
+      t.bm = bm, t.bn = 64, t.stages = ns, t.threads = 512, t.halo = 1;
+      if (!conv_halo_plan(L.qc.g, bm, 64, ns, &t.lp, &t.npb, true)) continue;
+      if (L.tile_default.halo && bm == L.tile_default.bm && ns == L.tile_default.stages) continue;
+      c.push_back(t);
+    }
   // single-group tiles of 4 or 8 waves, and 2 or 4 reduction groups of 4
   // waves (long reductions over few tiles)
   for (int nt : {256, 512, 1024})

@@ -368,8 +368,8 @@ HALO_I8_CASES = [
 def test_int8_halo_conv_exact(case, monkeypatch):
     """The windowed 3x3 kernel on codes (input window staged once per
     128-channel slice) equals the int8 oracle bit for bit, at every weight
-    ring depth, with the zero rows / columns of its patch corrected at the
-    border like the implicit-GEMM kernel's."""
+    ring depth and both tile heights, with the zero rows / columns of its
+    patch corrected at the border like the implicit-GEMM kernel's."""
     n, c, h, w, k, r, stride, pad, zx, act, residual = case
     announce("int8 halo conv %s" % (case,))
     g, consts, inputs = _conv_graph(n, c, h, w, k, r, stride, pad, zx, act, residual, seed=40 + len(str(case)))
@@ -380,3 +380,9 @@ def test_int8_halo_conv_exact(case, monkeypatch):
         name = [l["name"] for l in launches if l["kind"] == "conv_i8"][0]
         assert name.startswith("conv_i8_halo_128x64_s%d_" % ns), name
         assert np.array_equal(got[0], ref.astype(np.float64)), ns
+    for ns in (2, 3):  # the 64-pixel tile
+        monkeypatch.setenv("BYOC_I8_TILE", "h%db64" % ns)
+        got, launches = _run(g, consts, inputs)
+        name = [l["name"] for l in launches if l["kind"] == "conv_i8"][0]
+        assert name.startswith("conv_i8_halo_64x64_s%d_" % ns), name
+        assert np.array_equal(got[0], ref.astype(np.float64)), ("b64", ns)
