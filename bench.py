@@ -4,8 +4,9 @@ One step = one run of the whole offloaded subgraph over one batch of
 synthetic input already resident in HBM.  The headline is ResNet-50 v1 at
 batch 32 (input layout transform, 53 conv composites, max-pool, global
 average pool, classifier); the line also carries the other workloads the
-method is measured on, each timed the same way (engine autotune on, HIP-graph
-replay of the launch sequence on a side stream):
+method is measured on, each timed the same way (engine autotune on, the
+launch sequence on a side stream both as direct launches and as HIP-graph
+replay, the faster mode reported):
 
   configs      the single fp32 conv composite (us per call), the ResNet-18
                basic block (us per block), ResNet-50 at batch 1, MobileNetV2
@@ -119,7 +120,7 @@ def _profile(sg, ins, outs, stream, steps):
 
 def _roofline(launches, per_launch_ms, step_ms, traffic=None):
     """Roofline of the conv/dense MFMA class.  Its time per step is the
-    timed step (HIP events around the graph-replayed steps) less the other
+    timed step (HIP events around the timed steps) less the other
     kernels' per-launch event times: per-launch events add a gap of their
     own to every launch, the step time only the launches' own gaps."""
     conv_kinds = ("conv_mfma", "reduce")
@@ -186,8 +187,8 @@ def _copy_calibration(mib):
 
 
 class Measured:
-    """One workload as the benchmark runs it: engine, autotune, graph replay
-    on the run stream, timing, per-launch profile and the host copy of the
+    """One workload as the benchmark runs it: engine, autotune, the faster
+    launch mode on the run stream, timing, per-launch profile and the host copy of the
     outputs of the timed configuration (for the parity report)."""
 
     def __init__(self, key, wl, sg, ms, launches, per_launch, outputs):
